@@ -1,0 +1,209 @@
+"""CPU oracle for the sparse GNN operators of CogDL (arxiv 2103.00959, section 2.2).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are the only users.  The product library never imports,
+links or runs anything here, and this package imports nothing from it.
+
+Thin numpy/ctypes wrapper over ``oracle.c`` (plain C, fp64 arithmetic); every
+function follows the definition cited in the C source.  Inputs are numpy
+arrays; outputs are float64 arrays (values before the final rounding) plus the
+forward-error scale ``Abs`` where applicable.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32, BF16, F16 = 0, 1, 2
+ROW_SPLIT, NEIGHBOR_GROUP = 1, 2
+
+_lib = None
+
+
+def build() -> str:
+    """Compile oracle.c with gcc (no fast-math, so fp64 sums stay in order)."""
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+           "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32, i64, dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    lib.oracle_round.argtypes = [P, i64, i32, P]
+    lib.oracle_decode.argtypes = [P, i64, i32, P]
+    lib.oracle_balance_mode.argtypes = [i32, i64, P]
+    lib.oracle_neighbor_groups.argtypes = [i32, P, i32, i32, P]
+    lib.oracle_neighbor_groups.restype = i64
+    lib.oracle_spmm.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, P, P, P]
+    lib.oracle_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P]
+    lib.oracle_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, P, P, P]
+    lib.oracle_edge_softmax.argtypes = [i32, i32, i64, P, P, i32, P, P, dbl, i32, P, P]
+    lib.oracle_gat.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, dbl, P, P, i32, i32, P, P, P]
+    _lib = lib
+    return lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dt):
+    return None if a is None else np.ascontiguousarray(a, dtype=dt)
+
+
+def _x_code(x: np.ndarray, x_dtype: int | None) -> int:
+    if x_dtype is not None:
+        return x_dtype
+    if x.dtype == np.float32:
+        return F32
+    raise ValueError("16-bit inputs are passed as uint16 bit patterns with an explicit dtype code")
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise RuntimeError(f"oracle {what} failed with {rc}")
+
+
+def set_threads(n: int) -> None:
+    """Thread count for the row-parallel loops (results do not depend on it)."""
+    os.environ["OMP_NUM_THREADS"] = str(n)
+    try:
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(n))
+    except OSError:
+        pass
+
+
+def round_to(values: np.ndarray, dtype: int) -> np.ndarray:
+    """Round float64 values to fp32 / bf16 / fp16 (nearest, ties to even) directly from
+    double.  Returns float32 for F32 and uint16 bit patterns otherwise."""
+    v = _c(values, np.float64).ravel()
+    out = np.empty(v.size, dtype=np.float32 if dtype == F32 else np.uint16)
+    _check(_load().oracle_round(_p(v), v.size, dtype, _p(out)), "round")
+    return out.reshape(np.shape(values))
+
+
+def decode(bits: np.ndarray, dtype: int) -> np.ndarray:
+    """Exact float64 value of stored fp32 / bf16 / fp16 data."""
+    b = np.ascontiguousarray(bits)
+    out = np.empty(b.size, dtype=np.float64)
+    _check(_load().oracle_decode(_p(b), b.size, dtype, _p(out)), "decode")
+    return out.reshape(b.shape)
+
+
+def balance_mode(rowptr: np.ndarray, nnz: int) -> int:
+    rp = _c(rowptr, np.int32)
+    return _load().oracle_balance_mode(rp.size - 1, nnz, _p(rp))
+
+
+def neighbor_groups(rowptr: np.ndarray, group_size: int, mode: int) -> np.ndarray:
+    """(row, begin, end) slices of at most group_size edges, in row order."""
+    rp = _c(rowptr, np.int32)
+    lib = _load()
+    n = lib.oracle_neighbor_groups(rp.size - 1, _p(rp), group_size, mode, None)
+    if n < 0:
+        raise ValueError("bad neighbor-group arguments")
+    out = np.empty((n, 3), dtype=np.int32)
+    lib.oracle_neighbor_groups(rp.size - 1, _p(rp), group_size, mode, _p(out))
+    return out
+
+
+def spmm(rowptr, col, val, X, n_cols=None, x_dtype=None, rows=None):
+    """Y = A X (Eq. 1, sum of products).  Returns (Y, Abs) in float64."""
+    rp, cl, vl = _c(rowptr, np.int32), _c(col, np.int32), _c(val, np.float32)
+    X = np.ascontiguousarray(X)
+    n_rows = rp.size - 1
+    n_cols = X.shape[0] if n_cols is None else n_cols
+    F = int(np.prod(X.shape[1:])) if X.ndim > 1 else 1
+    sel = _c(rows, np.int32)
+    n_out = n_rows if sel is None else sel.size
+    Y = np.empty((n_out, F), dtype=np.float64)
+    A = np.empty((n_out, F), dtype=np.float64)
+    rc = _load().oracle_spmm(n_rows, n_cols, int(rp[-1]) if n_rows else 0, _p(rp), _p(cl), _p(vl),
+                             F, _p(X), _x_code(X, x_dtype), 0 if sel is None else sel.size,
+                             _p(sel), _p(Y), _p(A))
+    _check(rc, "spmm")
+    return Y, A
+
+
+def csr_to_csc(rowptr, col, val, n_cols):
+    """Stable transpose. Returns (colptr, row_t, val_t, perm)."""
+    rp, cl, vl = _c(rowptr, np.int32), _c(col, np.int32), _c(val, np.float32)
+    nnz = int(rp[-1]) if rp.size > 1 else 0
+    colptr = np.empty(n_cols + 1, dtype=np.int32)
+    row_t = np.empty(nnz, dtype=np.int32)
+    perm = np.empty(nnz, dtype=np.int32)
+    val_t = None if vl is None else np.empty(nnz, dtype=np.float32)
+    rc = _load().oracle_csr_to_csc(rp.size - 1, n_cols, nnz, _p(rp), _p(cl), _p(vl), _p(colptr),
+                                   _p(row_t), _p(val_t), _p(perm))
+    _check(rc, "csr_to_csc")
+    return colptr, row_t, val_t, perm
+
+
+def spmm_t(rowptr, col, val, G, n_cols, g_dtype=None, cols=None):
+    """dX = A^T G from the CSR of A.  Returns (dX, Abs) in float64."""
+    rp, cl, vl = _c(rowptr, np.int32), _c(col, np.int32), _c(val, np.float32)
+    G = np.ascontiguousarray(G)
+    F = int(np.prod(G.shape[1:])) if G.ndim > 1 else 1
+    sel = _c(cols, np.int32)
+    n_out = n_cols if sel is None else sel.size
+    dX = np.empty((n_out, F), dtype=np.float64)
+    A = np.empty((n_out, F), dtype=np.float64)
+    nnz = int(rp[-1]) if rp.size > 1 else 0
+    rc = _load().oracle_spmm_t(rp.size - 1, n_cols, nnz, _p(rp), _p(cl), _p(vl), F, _p(G),
+                               _x_code(G, g_dtype), 0 if sel is None else sel.size, _p(sel),
+                               _p(dX), _p(A))
+    _check(rc, "spmm_t")
+    return dX, A
+
+
+def edge_softmax(rowptr, col, s_dst, s_src, slope=0.2, rows=None):
+    """alpha[k, h] of SDDMM -> LeakyReLU -> per-row softmax, float64 [nnz_sel, H]."""
+    rp, cl = _c(rowptr, np.int32), _c(col, np.int32)
+    sd, ss = _c(s_dst, np.float32), _c(s_src, np.float32)
+    H = sd.shape[1]
+    sel = _c(rows, np.int32)
+    if sel is None:
+        n_e = int(rp[-1])
+    else:
+        n_e = int(np.sum(rp[sel + 1].astype(np.int64) - rp[sel]))
+    alpha = np.empty((n_e, H), dtype=np.float64)
+    rc = _load().oracle_edge_softmax(rp.size - 1, ss.shape[0], int(rp[-1]), _p(rp), _p(cl), H,
+                                     _p(sd), _p(ss), float(slope),
+                                     0 if sel is None else sel.size, _p(sel), _p(alpha))
+    _check(rc, "edge_softmax")
+    return alpha
+
+
+def gat(rowptr, col, s_dst, s_src, X, H, D, slope=0.2, alpha_in=None, x_dtype=None, rows=None):
+    """Y[i,h,:] = sum_k alpha[k,h] X[col[k],h,:].  Returns (Y, Abs) float64 [n_sel, H*D]."""
+    rp, cl = _c(rowptr, np.int32), _c(col, np.int32)
+    sd, ss = _c(s_dst, np.float32), _c(s_src, np.float32)
+    ai = _c(alpha_in, np.float32)
+    X = np.ascontiguousarray(X)
+    sel = _c(rows, np.int32)
+    n_rows = rp.size - 1
+    n_out = n_rows if sel is None else sel.size
+    Y = np.empty((n_out, H * D), dtype=np.float64)
+    A = np.empty((n_out, H * D), dtype=np.float64)
+    rc = _load().oracle_gat(n_rows, X.shape[0], int(rp[-1]), _p(rp), _p(cl), H, D, _p(sd), _p(ss),
+                            float(slope), _p(ai), _p(X), _x_code(X, x_dtype),
+                            0 if sel is None else sel.size, _p(sel), _p(Y), _p(A))
+    _check(rc, "gat")
+    return Y, A

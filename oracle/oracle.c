@@ -1,0 +1,373 @@
+/*
+ * oracle.c -- plain, slow, obviously correct CPU reference for the GNN
+ * message-passing operators of the CogDL paper (arxiv 2103.00959), section 2.2
+ * "Efficient Sparse Operators".
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
+ * loads this file; only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no code, header or constant with the HIP
+ * library: it decodes its own input formats, rounds with its own routine and
+ * implements each operator straight from its definition.
+ *
+ * Conventions (readings of the paper, each listed in the design notes):
+ *  - CSR row i is the aggregating node u of Eq. 1, column j the message
+ *    source v; edge k = (i, col[k]) carries the value val[k].
+ *  - All floating-point work is in double precision, visiting the edges of a
+ *    row in CSR order; callers round once to the output format with
+ *    oracle_round().
+ *  - Duplicate (i, j) pairs are separate terms; empty rows produce zero.
+ *
+ * Functions that take (n_sel, sel) compute only the listed rows (or columns
+ * for the transposed product) and pack results in list order; sel == NULL
+ * means every row.  All array arguments are host pointers.  Every function
+ * returns 0 on success and a negative value on a bad argument.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORACLE_F32 = 0, ORACLE_BF16 = 1, ORACLE_F16 = 2 };
+
+/* ---------------------------------------------------------------- formats */
+
+/* bfloat16: the upper 16 bits of an IEEE binary32. Exact widening. */
+static double decode_bf16(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* IEEE binary16: 1 sign, 5 exponent (bias 15), 10 fraction bits. */
+static double decode_f16(uint16_t h)
+{
+    int sign = h >> 15;
+    int ex = (h >> 10) & 31;
+    int fr = h & 1023;
+    double v;
+    if (ex == 0)
+        v = ldexp((double)fr, -24);              /* subnormal: fr * 2^-24 */
+    else if (ex == 31)
+        v = fr ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024 + fr), ex - 25); /* (1 + fr/1024) * 2^(ex-15) */
+    return sign ? -v : v;
+}
+
+static double load_elem(const void *x, int dtype, int64_t i)
+{
+    if (dtype == ORACLE_F32) return (double)((const float *)x)[i];
+    if (dtype == ORACLE_BF16) return decode_bf16(((const uint16_t *)x)[i]);
+    return decode_f16(((const uint16_t *)x)[i]);
+}
+
+/* Round v to the nearest value (ties to even) of a binary format with p
+ * significand bits, minimum normal exponent emin and maximum exponent emax,
+ * directly from double (no intermediate rounding). */
+static double round_to_format(double v, int p, int emin, int emax)
+{
+    if (isnan(v) || isinf(v) || v == 0.0) return v;
+    int e;
+    frexp(fabs(v), &e);
+    int lead = e - 1;                   /* exponent of the leading bit */
+    if (lead < emin) lead = emin;       /* subnormals share one quantum */
+    double quantum = ldexp(1.0, lead - (p - 1));
+    double r = rint(v / quantum) * quantum;   /* rint: ties to even */
+    double max_finite = ldexp(2.0 - ldexp(1.0, 1 - p), emax);
+    if (fabs(r) > max_finite) r = copysign(INFINITY, v);
+    return r;
+}
+
+static uint16_t encode_f16(double r)
+{
+    /* r is already a binary16 value (or inf/nan). */
+    uint16_t sign = signbit(r) ? 0x8000 : 0;
+    double a = fabs(r);
+    if (isnan(r)) return 0x7e00;
+    if (isinf(a)) return sign | 0x7c00;
+    if (a == 0.0) return sign;
+    int e;
+    frexp(a, &e);
+    int lead = e - 1;
+    if (lead < -14) /* subnormal: a = fr * 2^-24 */
+        return sign | (uint16_t)(a / ldexp(1.0, -24));
+    uint16_t fr = (uint16_t)(a / ldexp(1.0, lead - 10) - 1024.0);
+    return sign | (uint16_t)((lead + 15) << 10) | fr;
+}
+
+/* Round n doubles to dtype (RNE) and store the encoded values in out. */
+int oracle_round(const double *in, int64_t n, int32_t dtype, void *out)
+{
+    if (n < 0 || (n > 0 && (!in || !out))) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        if (dtype == ORACLE_F32) {
+            ((float *)out)[i] = (float)round_to_format(in[i], 24, -126, 127);
+        } else if (dtype == ORACLE_BF16) {
+            float f = (float)round_to_format(in[i], 8, -126, 127);
+            uint32_t u;
+            memcpy(&u, &f, sizeof u);
+            if (isnan(f)) u = 0x7fc00000u;
+            ((uint16_t *)out)[i] = (uint16_t)(u >> 16);
+        } else if (dtype == ORACLE_F16) {
+            ((uint16_t *)out)[i] = encode_f16(round_to_format(in[i], 11, -14, 15));
+        } else {
+            return -2;
+        }
+    }
+    return 0;
+}
+
+/* Decode n stored values of dtype to double. */
+int oracle_decode(const void *in, int64_t n, int32_t dtype, double *out)
+{
+    if (n < 0 || (n > 0 && (!in || !out))) return -1;
+    if (dtype < 0 || dtype > 2) return -2;
+    for (int64_t i = 0; i < n; ++i) out[i] = load_elem(in, dtype, i);
+    return 0;
+}
+
+/* ------------------------------------------------------ the balancer (a1) */
+
+/* Section 2.2 and its workload-balance listing: a data-aware balancer picks
+ * the row-split backend when the degrees of most (90%) of the nodes are close
+ * to the average degree, otherwise the neighbor-group backend.  "Close" is
+ * read as avg/2 <= d <= 2*avg, evaluated exactly in integers:
+ *   d >= avg/2  <=>  2*d*n_rows >= nnz,   d <= 2*avg  <=>  d*n_rows <= 2*nnz.
+ * Returns 1 (row split) or 2 (neighbor group). */
+int oracle_balance_mode(int32_t n_rows, int64_t nnz, const int32_t *rowptr)
+{
+    if (n_rows < 0 || nnz < 0 || (n_rows > 0 && !rowptr)) return -1;
+    if (n_rows == 0) return 1;
+    int64_t close = 0;
+    for (int32_t i = 0; i < n_rows; ++i) {
+        int64_t d = (int64_t)rowptr[i + 1] - rowptr[i];
+        if (2 * d * n_rows >= nnz && d * n_rows <= 2 * nnz) ++close;
+    }
+    return (10 * close >= 9 * (int64_t)n_rows) ? 1 : 2;
+}
+
+/* Neighbor groups: every row is cut into consecutive slices of at most
+ * group_size edges (an empty row is one empty slice).  With mode 1 (row
+ * split) each row is one slice.  Writes (row, begin, end) triples in row
+ * order when out != NULL; returns the number of slices. */
+int64_t oracle_neighbor_groups(int32_t n_rows, const int32_t *rowptr, int32_t group_size,
+                               int32_t mode, int32_t *out)
+{
+    if (n_rows < 0 || group_size < 1 || (n_rows > 0 && !rowptr)) return -1;
+    int64_t n = 0;
+    for (int32_t i = 0; i < n_rows; ++i) {
+        int32_t beg = rowptr[i], end = rowptr[i + 1];
+        if (mode == 1 || end - beg <= group_size) {
+            if (out) { out[3 * n] = i; out[3 * n + 1] = beg; out[3 * n + 2] = end; }
+            ++n;
+            continue;
+        }
+        for (int32_t s = beg; s < end; s += group_size) {
+            int32_t e = (end - s > group_size) ? s + group_size : end;
+            if (out) { out[3 * n] = i; out[3 * n + 1] = s; out[3 * n + 2] = e; }
+            ++n;
+        }
+    }
+    return n;
+}
+
+/* ------------------------------------------------------------- SpMM (a2) */
+
+/* Eq. 1 with reduce = sum and compute = multiply, i.e. H' = A H:
+ *   Y[i,f] = sum_{k in row i} val[k] * X[col[k], f]
+ * Abs[i,f] = sum |val[k]| * |X[col[k], f]| is the forward-error scale.
+ * val == NULL means every edge value is 1. */
+int oracle_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                const int32_t *col, const float *val, int32_t F, const void *X,
+                int32_t x_dtype, int32_t n_sel, const int32_t *sel, double *Y, double *Abs)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || F < 0) return -1;
+    int32_t n_out = sel ? n_sel : n_rows;
+    #pragma omp parallel for schedule(dynamic, 64)
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        double *y = Y + (int64_t)r * F;
+        double *a = Abs ? Abs + (int64_t)r * F : NULL;
+        for (int32_t f = 0; f < F; ++f) { y[f] = 0.0; if (a) a[f] = 0.0; }
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
+            double w = val ? (double)val[k] : 1.0;
+            int64_t base = (int64_t)col[k] * F;
+            for (int32_t f = 0; f < F; ++f) {
+                double x = load_elem(X, x_dtype, base + f);
+                y[f] += w * x;
+                if (a) a[f] += fabs(w) * fabs(x);
+            }
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------- CSR -> CSC (a3) */
+
+/* Transpose of the sparsity structure by a stable counting sort of the edge
+ * ids on their column: colptr is the exclusive prefix sum of the column
+ * counts, and inside a column the edges keep increasing CSR edge id.
+ * perm[p] = CSR edge id placed at CSC slot p, row_t[p] its row, val_t[p] a
+ * bit copy of val[perm[p]] (val / val_t may be NULL together). */
+int oracle_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                      const int32_t *col, const float *val, int32_t *colptr, int32_t *row_t,
+                      float *val_t, int32_t *perm)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0) return -1;
+    int64_t *next = (int64_t *)calloc((size_t)n_cols + 1, sizeof(int64_t));
+    if (!next) return -3;
+    for (int64_t k = 0; k < nnz; ++k) next[col[k] + 1]++;
+    for (int32_t j = 0; j < n_cols; ++j) next[j + 1] += next[j];
+    for (int32_t j = 0; j <= n_cols; ++j) colptr[j] = (int32_t)next[j];
+    for (int32_t i = 0; i < n_rows; ++i) {
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
+            int64_t p = next[col[k]]++;
+            perm[p] = k;
+            row_t[p] = i;
+            if (val && val_t) memcpy(&val_t[p], &val[k], sizeof(float));
+        }
+    }
+    free(next);
+    return 0;
+}
+
+/* ---------------------------------------------- transposed SpMM (a4) */
+
+/* Backward of H' = A H with respect to H:  dX = A^T G, i.e.
+ *   dX[j,f] = sum_{k : col[k] = j} val[k] * G[row(k), f]
+ * computed by scattering straight from the CSR (not from a CSC), adding the
+ * terms of a column in increasing edge id.  With sel != NULL only the listed
+ * columns are produced (one pass over all edges). */
+int oracle_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                  const int32_t *col, const float *val, int32_t F, const void *G,
+                  int32_t g_dtype, int32_t n_sel, const int32_t *sel, double *dX, double *Abs)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || F < 0) return -1;
+    int32_t n_out = sel ? n_sel : n_cols;
+    int32_t *slot = (int32_t *)malloc(sizeof(int32_t) * ((size_t)n_cols + 1));
+    if (!slot) return -3;
+    for (int32_t j = 0; j < n_cols; ++j) slot[j] = sel ? -1 : j;
+    if (sel)
+        for (int32_t r = 0; r < n_sel; ++r) slot[sel[r]] = r;
+    for (int64_t t = 0; t < (int64_t)n_out * F; ++t) { dX[t] = 0.0; if (Abs) Abs[t] = 0.0; }
+    for (int32_t i = 0; i < n_rows; ++i) {
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
+            int32_t r = slot[col[k]];
+            if (r < 0) continue;
+            double w = val ? (double)val[k] : 1.0;
+            for (int32_t f = 0; f < F; ++f) {
+                double g = load_elem(G, g_dtype, (int64_t)i * F + f);
+                dX[(int64_t)r * F + f] += w * g;
+                if (Abs) Abs[(int64_t)r * F + f] += fabs(w) * fabs(g);
+            }
+        }
+    }
+    free(slot);
+    return 0;
+}
+
+/* ------------------------------------ SDDMM + LeakyReLU + edge softmax */
+
+/* Additive per-head attention score of edge k = (i, j) for head h:
+ *   t = s_dst[i,h] + s_src[j,h],  e = t if t > 0 else slope * t,
+ * i.e. the SDDMM A (.) (P Q^T) with P = [s_dst, 1], Q = [1, s_src] per head,
+ * followed by LeakyReLU. */
+static double edge_score(const float *s_dst, const float *s_src, int32_t H, int32_t i,
+                         int32_t j, int32_t h, double slope)
+{
+    double t = (double)s_dst[(int64_t)i * H + h] + (double)s_src[(int64_t)j * H + h];
+    return t > 0.0 ? t : slope * t;
+}
+
+/* Edge-wise softmax over the edges of each destination row, per head:
+ *   alpha[k,h] = exp(e[k,h] - m) / sum_{k' in row} exp(e[k',h] - m)
+ * where m is the row maximum (subtracting it changes nothing mathematically
+ * and keeps exp from overflowing).  Output layout alpha[k*H + h]; with sel,
+ * the listed rows' edges are packed in list order. */
+int oracle_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                        const int32_t *col, int32_t H, const float *s_dst, const float *s_src,
+                        double slope, int32_t n_sel, const int32_t *sel, double *alpha)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || H < 1) return -1;
+    int32_t n_out = sel ? n_sel : n_rows;
+    int64_t *off = (int64_t *)malloc(sizeof(int64_t) * ((size_t)n_out + 1));
+    if (!off) return -3;
+    off[0] = 0;
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        off[r + 1] = off[r] + (rowptr[i + 1] - rowptr[i]);
+    }
+    #pragma omp parallel for schedule(dynamic, 64)
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        int32_t beg = rowptr[i], end = rowptr[i + 1];
+        for (int32_t h = 0; h < H; ++h) {
+            double m = -INFINITY;
+            for (int32_t k = beg; k < end; ++k) {
+                double e = edge_score(s_dst, s_src, H, i, col[k], h, slope);
+                if (e > m) m = e;
+            }
+            double z = 0.0;
+            for (int32_t k = beg; k < end; ++k)
+                z += exp(edge_score(s_dst, s_src, H, i, col[k], h, slope) - m);
+            for (int32_t k = beg; k < end; ++k) {
+                double e = edge_score(s_dst, s_src, H, i, col[k], h, slope);
+                alpha[(off[r] + (k - beg)) * H + h] = exp(e - m) / z;
+            }
+        }
+    }
+    free(off);
+    return 0;
+}
+
+/* ------------------------------------------------- multi-head SpMM (a7) */
+
+/* GAT aggregation with one weight per edge and head:
+ *   Y[i,h,d] = sum_{k in row i} alpha[k,h] * X[col[k], h, d]
+ * X and Y are [node][head][d] row-major.  With alpha_in == NULL the weights
+ * are the edge softmax above, kept in double; otherwise alpha_in[k*H+h] (fp32)
+ * is used exactly. */
+int oracle_gat(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+               const int32_t *col, int32_t H, int32_t D, const float *s_dst, const float *s_src,
+               double slope, const float *alpha_in, const void *X, int32_t x_dtype,
+               int32_t n_sel, const int32_t *sel, double *Y, double *Abs)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || H < 1 || D < 0) return -1;
+    int32_t n_out = sel ? n_sel : n_rows;
+    int64_t HD = (int64_t)H * D;
+    int rc = 0;
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        int32_t beg = rowptr[i], end = rowptr[i + 1];
+        int32_t deg = end - beg;
+        double *y = Y + (int64_t)r * HD;
+        double *a = Abs ? Abs + (int64_t)r * HD : NULL;
+        for (int64_t t = 0; t < HD; ++t) { y[t] = 0.0; if (a) a[t] = 0.0; }
+        if (deg == 0) continue;
+        double *w = (double *)malloc(sizeof(double) * (size_t)deg * H);
+        if (!w) { rc = -3; continue; }
+        if (alpha_in) {
+            for (int32_t k = beg; k < end; ++k)
+                for (int32_t h = 0; h < H; ++h)
+                    w[(int64_t)(k - beg) * H + h] = (double)alpha_in[(int64_t)k * H + h];
+        } else {
+            oracle_edge_softmax(n_rows, n_cols, nnz, rowptr, col, H, s_dst, s_src, slope, 1, &i, w);
+        }
+        for (int32_t k = beg; k < end; ++k) {
+            int64_t base = (int64_t)col[k] * HD;
+            for (int32_t h = 0; h < H; ++h) {
+                double wk = w[(int64_t)(k - beg) * H + h];
+                for (int32_t d = 0; d < D; ++d) {
+                    double x = load_elem(X, x_dtype, base + (int64_t)h * D + d);
+                    y[(int64_t)h * D + d] += wk * x;
+                    if (a) a[(int64_t)h * D + d] += fabs(wk) * fabs(x);
+                }
+            }
+        }
+        free(w);
+    }
+    return rc;
+}

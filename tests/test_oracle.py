@@ -1,0 +1,484 @@
+"""Pins for the CPU oracle: each checks it against something other than itself
+(hand-derived values, closed forms, invariants, dense/scipy special cases,
+brute force on tiny graphs), chosen so that a dropped term, a wrong sign, a
+wrong index or a transposed operand fails at least one of them."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+
+import oracle
+from paper_2103_00959_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _dense(g):
+    A = np.zeros((g.n_rows, g.n_cols))
+    rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+    vals = np.ones(g.col.size) if g.val is None else g.val.astype(np.float64)
+    np.add.at(A, (rows, g.col), vals)          # duplicates add up
+    return A
+
+
+def _graphs(seed=0):
+    rng = np.random.default_rng(seed)
+    yield synth.random_csr(37, 37, rng, mean_deg=3)
+    yield synth.random_csr(50, 23, rng, mean_deg=5, dup=True, unsorted=True, empty_frac=0.2)
+    yield synth.random_csr(23, 61, rng, mean_deg=8, unsorted=True)
+    yield synth.random_csr(200, 150, rng, mean_deg=12, dup=True, empty_frac=0.1)
+    yield synth.random_csr(1, 5, rng, mean_deg=4)
+
+
+# ------------------------------------------------------------ formats
+
+def test_decode_known_patterns():
+    bf = np.array([0x3F80, 0xC000, 0x0001, 0x7F7F, 0x0000, 0x8000], dtype=np.uint16)
+    exp_bf = [1.0, -2.0, 2.0 ** -133, (2 - 2 ** -7) * 2.0 ** 127, 0.0, -0.0]
+    assert oracle.decode(bf, oracle.BF16).tolist() == exp_bf
+    hf = np.array([0x3C00, 0x0001, 0x7BFF, 0xC400, 0x0400, 0x3555], dtype=np.uint16)
+    exp_hf = [1.0, 2.0 ** -24, 65504.0, -4.0, 2.0 ** -14, 1365.0 / 4096.0]
+    assert oracle.decode(hf, oracle.F16).tolist() == exp_hf
+
+
+def test_round_bf16_ties_and_no_double_rounding():
+    one = 1.0
+    cases = [
+        (one + 2 ** -8, 0x3F80),                 # tie -> even (1.0)
+        (one + 3 * 2 ** -8, 0x3F82),             # tie -> even (odd neighbour skipped)
+        (one + 2 ** -8 + 2 ** -30, 0x3F81),      # just above the tie; float-first would give 0x3F80
+        (-(one + 2 ** -7), 0xBF81),
+        (2.0 ** -133, 0x0001),                   # smallest subnormal
+        (2.0 ** -134, 0x0000),                   # tie between 0 and 2^-133 -> even
+        (3.0e38 * 10, 0x7F80),                   # overflow -> inf
+    ]
+    got = oracle.round_to(np.array([c[0] for c in cases]), oracle.BF16)
+    assert got.tolist() == [c[1] for c in cases]
+
+
+def test_round_f16_matches_numpy_half():
+    rng = np.random.default_rng(3)
+    v = np.concatenate([rng.standard_normal(5000) * 10.0 ** rng.integers(-9, 5, 5000),
+                        [65504.0, 65519.9, 65520.0, 2.0 ** -25, 3 * 2.0 ** -26, 2.0 ** -24]])
+    got = oracle.round_to(v, oracle.F16)
+    with np.errstate(over="ignore"):
+        want = v.astype(np.float16).view(np.uint16)  # numpy rounds double -> half directly
+    assert np.array_equal(got, want)
+
+
+def test_round_f32_is_cast():
+    v = np.random.default_rng(4).standard_normal(1000) * 1e3
+    assert np.array_equal(oracle.round_to(v, oracle.F32), v.astype(np.float32))
+
+
+# ------------------------------------------------------------ balancer
+
+def test_balancer_modes_golden():
+    with open(os.path.join(GOLDEN, "balancer_modes.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        d = np.array(c["degrees"], dtype=np.int64)
+        rowptr = np.concatenate([[0], np.cumsum(d)]).astype(np.int32)
+        assert oracle.balance_mode(rowptr, int(d.sum())) == c["mode"], c["name"]
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 7, 64])
+def test_neighbor_groups_tile_edges(G):
+    for g in _graphs(1):
+        for mode in (oracle.ROW_SPLIT, oracle.NEIGHBOR_GROUP):
+            groups = oracle.neighbor_groups(g.rowptr, G, mode)
+            d = np.diff(g.rowptr)
+            if mode == oracle.ROW_SPLIT:
+                assert len(groups) == g.n_rows
+            else:
+                assert len(groups) == int(np.sum(np.maximum(1, -(-d // G))))
+                assert np.all(groups[:, 2] - groups[:, 1] <= G)
+            assert np.all(np.diff(groups[:, 0]) >= 0) and np.all(np.diff(groups[:, 1]) >= 0)
+            cover = np.zeros(g.nnz, dtype=np.int64)
+            for r, b, e in groups:
+                assert g.rowptr[r] <= b <= e <= g.rowptr[r + 1]
+                cover[b:e] += 1
+            assert np.all(cover == 1)
+
+
+# ------------------------------------------------------------ SpMM
+
+def test_spmm_golden_hand_example():
+    with open(os.path.join(GOLDEN, "csr_dups_unsorted.json")) as f:
+        c = json.load(f)
+    X = np.array(c["X"], dtype=np.float32)
+    Y, A = oracle.spmm(c["rowptr"], c["col"], np.array(c["val"], np.float32), X)
+    assert Y.tolist() == c["Y"]
+
+
+def test_spmm_dense_special_case():
+    rng = np.random.default_rng(5)
+    for g in _graphs(2):
+        X = rng.standard_normal((g.n_cols, 7)).astype(np.float32)
+        Y, Abs = oracle.spmm(g.rowptr, g.col, g.val, X)
+        D = _dense(g)
+        np.testing.assert_allclose(Y, D @ X.astype(np.float64), rtol=1e-12, atol=1e-12)
+        Dabs = np.zeros_like(D)
+        rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+        np.add.at(Dabs, (rows, g.col), np.abs(g.val.astype(np.float64)))
+        np.testing.assert_allclose(Abs, Dabs @ np.abs(X.astype(np.float64)), rtol=1e-12)
+
+
+def test_spmm_scipy_cross_check():
+    rng = np.random.default_rng(6)
+    g = synth.random_csr(2000, 1500, rng, mean_deg=9, dup=True, unsorted=True)
+    X = rng.standard_normal((g.n_cols, 33)).astype(np.float32)
+    Y, _ = oracle.spmm(g.rowptr, g.col, g.val, X)
+    S = sp.csr_matrix((g.val.astype(np.float64), g.col, g.rowptr), shape=(g.n_rows, g.n_cols))
+    np.testing.assert_allclose(Y, S @ X.astype(np.float64), rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("n", [2, 3, 4])
+def test_spmm_exhaustive_patterns(n):
+    """Every directed pattern on n nodes (2^(n*n) graphs, self pairs included),
+    batched as one block-diagonal graph, against dense products per block."""
+    rng = np.random.default_rng(7 + n)
+    n_pat = 1 << (n * n)
+    bits = ((np.arange(n_pat)[:, None] >> np.arange(n * n)[None, :]) & 1).astype(bool)
+    mats = bits.reshape(n_pat, n, n)
+    W = rng.standard_normal((n_pat, n, n)) * mats
+    W = W.astype(np.float32)
+    rowptr = np.concatenate([[0], np.cumsum(mats.reshape(-1, n).sum(1))]).astype(np.int32)
+    blk, r, c = np.nonzero(mats)
+    col = (blk * n + c).astype(np.int32)
+    val = W[blk, r, c]
+    F = 3
+    X = rng.standard_normal((n_pat * n, F)).astype(np.float32)
+    Y, _ = oracle.spmm(rowptr, col, val, X)
+    want = np.einsum("bij,bjf->bif", W.astype(np.float64), X.reshape(n_pat, n, F).astype(np.float64))
+    np.testing.assert_allclose(Y.reshape(n_pat, n, F), want, rtol=1e-12, atol=1e-13)
+
+
+def _regular_graphs():
+    def from_adj(nbrs, n):
+        keys = np.unique(np.array([i * n + j for i in range(n) for j in nbrs(i)] +
+                                  [i * n + i for i in range(n)], dtype=np.int64))
+        return synth._csr_from_keys(keys, n, n)
+    yield 2, from_adj(lambda i: [(i + 1) % 11, (i - 1) % 11], 11)                   # cycle C11
+    yield 6, from_adj(lambda i: [j for j in range(7) if j != i], 7)                  # K7
+    yield 5, from_adj(lambda i: [i ^ (1 << b) for b in range(5)], 32)                # hypercube Q5
+    yield 6, from_adj(lambda i: [(i + s) % 40 for s in (1, 3, 7, -1, -3, -7)], 40)  # circulant
+
+
+def test_sym_norm_ones_invariant():
+    """D^-1/2 (A+I) D^-1/2 applied to the ones vector on a k-regular graph is 1."""
+    for k, g in _regular_graphs():
+        assert np.all(np.diff(g.rowptr) == k + 1)
+        g.val = synth.sym_norm_values(g)
+        Y, _ = oracle.spmm(g.rowptr, g.col, g.val, np.ones((g.n_cols, 2), np.float32))
+        # only the fp32 storage of 1/(k+1) is inexact
+        assert np.max(np.abs(Y - 1.0)) <= (k + 1) * 2.0 ** -24
+
+
+def test_row_norm_ones_invariant():
+    rng = np.random.default_rng(8)
+    g = synth.random_csr(300, 300, rng, mean_deg=6)
+    keep = np.diff(g.rowptr) > 0
+    g.val = synth.row_norm_values(g)
+    Y, _ = oracle.spmm(g.rowptr, g.col, g.val, np.ones((g.n_cols, 1), np.float32))
+    d = np.diff(g.rowptr)
+    assert np.all(np.abs(Y[keep, 0] - 1.0) <= d[keep] * 2.0 ** -24)
+    assert np.all(Y[~keep] == 0)
+
+
+def test_spmm_identity_bit_exact_all_dtypes():
+    rng = np.random.default_rng(9)
+    n = 97
+    rowptr = np.arange(n + 1, dtype=np.int32)
+    col = np.arange(n, dtype=np.int32)
+    val = np.ones(n, dtype=np.float32)
+    x32 = rng.standard_normal((n, 9)).astype(np.float32)
+    for dt, X in ((oracle.F32, x32), (oracle.BF16, synth.f32_to_bf16_bits(x32)),
+                  (oracle.F16, synth.f32_to_f16_bits(x32))):
+        Y, _ = oracle.spmm(rowptr, col, val, X, x_dtype=dt)
+        assert np.array_equal(oracle.round_to(Y, dt), X)
+
+
+def test_spmm_linearity():
+    rng = np.random.default_rng(10)
+    g = synth.random_csr(120, 90, rng, mean_deg=7, dup=True)
+    # small integers keep a*X + b*Z exact in fp32, so only the operator is tested
+    X = rng.integers(-8, 9, (90, 5)).astype(np.float32)
+    Z = rng.integers(-8, 9, (90, 5)).astype(np.float32)
+    a, b = np.float32(0.5), np.float32(-2.0)
+    Yx, Ax = oracle.spmm(g.rowptr, g.col, g.val, X)
+    Yz, Az = oracle.spmm(g.rowptr, g.col, g.val, Z)
+    Yc, _ = oracle.spmm(g.rowptr, g.col, g.val, a * X + b * Z)
+    scale = np.abs(a) * Ax + np.abs(b) * Az + 1e-300
+    assert np.max(np.abs(Yc - (a * Yx + b * Yz)) / scale) < 1e-13
+
+
+def test_spmm_16bit_inputs_decode_independently():
+    rng = np.random.default_rng(11)
+    g = synth.random_csr(64, 40, rng, mean_deg=5)
+    x32 = rng.standard_normal((40, 8)).astype(np.float32)
+    bf = synth.f32_to_bf16_bits(x32)
+    via_numpy = (bf.astype(np.uint32) << 16).view(np.float32)
+    Yb, _ = oracle.spmm(g.rowptr, g.col, g.val, bf, x_dtype=oracle.BF16)
+    Yf, _ = oracle.spmm(g.rowptr, g.col, g.val, via_numpy)
+    assert np.array_equal(Yb, Yf)
+    hf = synth.f32_to_f16_bits(x32)
+    Yh, _ = oracle.spmm(g.rowptr, g.col, g.val, hf, x_dtype=oracle.F16)
+    Yf, _ = oracle.spmm(g.rowptr, g.col, g.val, hf.view(np.float16).astype(np.float32))
+    assert np.array_equal(Yh, Yf)
+
+
+def test_spmm_selected_rows_match_full():
+    rng = np.random.default_rng(12)
+    g = synth.random_csr(300, 200, rng, mean_deg=6, empty_frac=0.1)
+    X = rng.standard_normal((200, 4)).astype(np.float32)
+    Y, A = oracle.spmm(g.rowptr, g.col, g.val, X)
+    sel = np.array([299, 0, 17, 17, 150], dtype=np.int32)
+    Ys, As = oracle.spmm(g.rowptr, g.col, g.val, X, rows=sel)
+    assert np.array_equal(Ys, Y[sel]) and np.array_equal(As, A[sel])
+
+
+def test_spmm_empty_graph_and_zero_width():
+    rowptr = np.zeros(6, dtype=np.int32)
+    Y, _ = oracle.spmm(rowptr, np.zeros(0, np.int32), np.zeros(0, np.float32),
+                       np.ones((4, 3), np.float32))
+    assert Y.shape == (5, 3) and np.all(Y == 0)
+
+
+# ------------------------------------------------------------ CSR -> CSC
+
+def test_csc_golden_stable_with_duplicates():
+    with open(os.path.join(GOLDEN, "csr_dups_unsorted.json")) as f:
+        c = json.load(f)
+    colptr, row_t, val_t, perm = oracle.csr_to_csc(c["rowptr"], c["col"],
+                                                   np.array(c["val"], np.float32), c["n_cols"])
+    assert colptr.tolist() == c["colptr"]
+    assert perm.tolist() == c["perm"]
+    assert row_t.tolist() == c["row_t"]
+    assert val_t.tolist() == c["val_t"]
+
+
+def test_csc_matches_scipy_and_dense():
+    rng = np.random.default_rng(13)
+    for g in _graphs(3):
+        colptr, row_t, val_t, perm = oracle.csr_to_csc(g.rowptr, g.col, g.val, g.n_cols)
+        # dense A^T
+        T = np.zeros((g.n_cols, g.n_rows))
+        cols = np.repeat(np.arange(g.n_cols), np.diff(colptr))
+        np.add.at(T, (cols, row_t), val_t.astype(np.float64))
+        np.testing.assert_array_equal(T, _dense(g).T)
+        # permutation and bit copies
+        assert np.array_equal(np.sort(perm), np.arange(g.nnz))
+        assert np.array_equal(val_t.view(np.uint32), g.val[perm].view(np.uint32))
+        rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+        assert np.array_equal(row_t, rows[perm])
+        assert np.all(np.diff(g.col[perm]) >= 0)
+        # stability: inside a column, increasing CSR edge id
+        for j in range(g.n_cols):
+            seg = perm[colptr[j]:colptr[j + 1]]
+            assert np.all(np.diff(seg) > 0)
+    g = synth.random_csr(500, 400, rng, mean_deg=7)      # canonical (sorted, unique)
+    colptr, row_t, _, _ = oracle.csr_to_csc(g.rowptr, g.col, g.val, g.n_cols)
+    S = sp.csr_matrix((g.val, g.col, g.rowptr), shape=(g.n_rows, g.n_cols)).tocsc()
+    S.sort_indices()
+    assert np.array_equal(colptr, S.indptr) and np.array_equal(row_t, S.indices)
+
+
+def test_csc_double_transpose_is_identity():
+    rng = np.random.default_rng(14)
+    g = synth.random_csr(300, 250, rng, mean_deg=6, empty_frac=0.1)
+    colptr, row_t, val_t, _ = oracle.csr_to_csc(g.rowptr, g.col, g.val, g.n_cols)
+    rp2, col2, val2, _ = oracle.csr_to_csc(colptr, row_t, val_t, g.n_rows)
+    assert np.array_equal(rp2, g.rowptr) and np.array_equal(col2, g.col)
+    assert np.array_equal(val2.view(np.uint32), g.val.view(np.uint32))
+
+
+# ------------------------------------------------------------ SpMM^T
+
+def test_spmm_t_golden_hand_example():
+    with open(os.path.join(GOLDEN, "csr_dups_unsorted.json")) as f:
+        c = json.load(f)
+    dX, _ = oracle.spmm_t(c["rowptr"], c["col"], np.array(c["val"], np.float32),
+                          np.array(c["G"], np.float32), c["n_cols"])
+    assert dX.tolist() == c["dX"]
+
+
+def test_spmm_t_dense_and_adjoint():
+    rng = np.random.default_rng(15)
+    for g in _graphs(4):
+        F = 6
+        X = rng.standard_normal((g.n_cols, F)).astype(np.float32)
+        G = rng.standard_normal((g.n_rows, F)).astype(np.float32)
+        dX, _ = oracle.spmm_t(g.rowptr, g.col, g.val, G, g.n_cols)
+        np.testing.assert_allclose(dX, _dense(g).T @ G.astype(np.float64), rtol=1e-12, atol=1e-12)
+        Y, _ = oracle.spmm(g.rowptr, g.col, g.val, X)
+        lhs = float(np.sum(Y * G.astype(np.float64)))
+        rhs = float(np.sum(X.astype(np.float64) * dX))
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs))
+
+
+def test_spmm_t_equals_spmm_on_transposed_csr_and_selection():
+    rng = np.random.default_rng(16)
+    g = synth.random_csr(400, 300, rng, mean_deg=5, dup=True, unsorted=True)
+    G = rng.standard_normal((400, 4)).astype(np.float32)
+    colptr, row_t, val_t, _ = oracle.csr_to_csc(g.rowptr, g.col, g.val, g.n_cols)
+    dX, A = oracle.spmm_t(g.rowptr, g.col, g.val, G, g.n_cols)
+    Y2, A2 = oracle.spmm(colptr, row_t, val_t, G)
+    assert np.array_equal(dX, Y2) and np.array_equal(A, A2)   # same terms, same order
+    sel = np.array([5, 299, 0, 100], dtype=np.int32)
+    dXs, _ = oracle.spmm_t(g.rowptr, g.col, g.val, G, g.n_cols, cols=sel)
+    assert np.array_equal(dXs, dX[sel])
+
+
+# ------------------------------------------------------------ edge softmax
+
+def _lrelu(t, slope=0.2):
+    return np.where(t > 0, t, slope * t)
+
+
+def test_softmax_closed_forms():
+    one_row = np.array([0, 2], dtype=np.int32)
+    col = np.array([0, 1], dtype=np.int32)
+    # e = [0.5, 1.5] (positive branch): alpha = [1/(1+e), e/(1+e)] with e = exp(1)
+    a = oracle.edge_softmax(one_row, col, np.zeros((1, 1), np.float32),
+                            np.array([[0.5], [1.5]], np.float32))
+    E = math.e
+    assert abs(a[0, 0] - 1 / (1 + E)) < 1e-15 and abs(a[1, 0] - E / (1 + E)) < 1e-15
+    # t = [-1, -2] (negative branch, slope 0.2): e = [-0.2, -0.4]
+    a = oracle.edge_softmax(one_row, col, np.zeros((1, 1), np.float32),
+                            np.array([[-1.0], [-2.0]], np.float32))
+    w = math.exp(-0.2)
+    assert abs(a[0, 0] - 1 / (1 + w)) < 1e-15
+    assert abs(a[1, 0] - w / (1 + w)) < 1e-15
+    # mixed signs, two heads, s_dst added: t = s_dst + s_src
+    rp = np.array([0, 3], dtype=np.int32)
+    c3 = np.array([0, 1, 2], dtype=np.int32)
+    sd = np.array([[0.25, -1.0]], np.float32)
+    ss = np.array([[0.75, 2.0], [-1.25, 1.0], [-0.25, 0.0]], np.float32)
+    a = oracle.edge_softmax(rp, c3, sd, ss, slope=0.2)
+    e0 = np.array([1.0, -0.2, 0.0])                 # head 0: t = [1, -1, 0]
+    e1 = np.array([1.0, 0.0, -0.2])                 # head 1: t = [1, 0, -1]
+    for h, e in ((0, e0), (1, e1)):
+        want = np.exp(e) / np.exp(e).sum()
+        np.testing.assert_allclose(a[:, h], want, rtol=1e-15)
+
+
+def test_softmax_invariants_and_brute_force():
+    rng = np.random.default_rng(17)
+    for n in (1, 2, 5, 9, 16):
+        g = synth.random_csr(n, n, rng, mean_deg=4, empty_frac=0.2)
+        H = 3
+        sd = rng.standard_normal((n, H)).astype(np.float32)
+        ss = rng.standard_normal((n, H)).astype(np.float32)
+        a = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+        assert np.all(a > 0)
+        rows = np.repeat(np.arange(n), np.diff(g.rowptr))
+        for h in range(H):
+            sums = np.bincount(rows, weights=a[:, h], minlength=n)
+            nonempty = np.diff(g.rowptr) > 0
+            np.testing.assert_allclose(sums[nonempty], 1.0, rtol=0, atol=1e-14)
+            # dense masked softmax, -inf off the pattern
+            S = np.full((n, n), -np.inf)
+            S[rows, g.col] = _lrelu(sd[rows, h].astype(np.float64) + ss[g.col, h].astype(np.float64))
+            for i in np.flatnonzero(nonempty):
+                p = np.exp(S[i] - S[i].max())
+                p /= p.sum()
+                np.testing.assert_allclose(a[g.rowptr[i]:g.rowptr[i + 1], h], p[g.col[g.rowptr[i]:g.rowptr[i + 1]]],
+                                           rtol=1e-13)
+
+
+def test_softmax_special_cases():
+    rng = np.random.default_rng(18)
+    g = synth.random_csr(200, 150, rng, mean_deg=6, empty_frac=0.1, dup=True)
+    H = 4
+    sd = rng.standard_normal((200, H)).astype(np.float32)
+    d = np.diff(g.rowptr)
+    rows = np.repeat(np.arange(200), d)
+    # s_src == 0: all scores of a row are equal -> alpha = 1/d
+    a = oracle.edge_softmax(g.rowptr, g.col, sd, np.zeros((150, H), np.float32))
+    np.testing.assert_allclose(a, np.repeat(1.0 / d[rows], H).reshape(-1, H), rtol=1e-15)
+    # degree-1 rows give exactly 1
+    ss = rng.standard_normal((150, H)).astype(np.float32) * 30
+    a = oracle.edge_softmax(g.rowptr, g.col, sd, ss)
+    one = d[rows] == 1
+    assert np.all(a[one] == 1.0)
+    # huge scores: max subtraction keeps exp finite
+    a = oracle.edge_softmax(g.rowptr, g.col, sd * 1000, ss * 100)
+    assert np.all(np.isfinite(a))
+    sums = np.bincount(rows, weights=a[:, 0], minlength=200)
+    np.testing.assert_allclose(sums[d > 0], 1.0, atol=1e-13)
+    # all-positive t: a per-row shift of s_dst shifts e and leaves alpha unchanged
+    sdp = np.abs(sd) + 40.0
+    a0 = oracle.edge_softmax(g.rowptr, g.col, sdp, ss / 30)
+    a1 = oracle.edge_softmax(g.rowptr, g.col, sdp + 5.0, ss / 30)
+    np.testing.assert_allclose(a0, a1, rtol=1e-12)
+
+
+def test_softmax_selected_rows_pack_in_order():
+    rng = np.random.default_rng(19)
+    g = synth.random_csr(100, 80, rng, mean_deg=5, empty_frac=0.1)
+    sd = rng.standard_normal((100, 2)).astype(np.float32)
+    ss = rng.standard_normal((80, 2)).astype(np.float32)
+    a = oracle.edge_softmax(g.rowptr, g.col, sd, ss)
+    sel = np.array([7, 3, 99], dtype=np.int32)
+    part = oracle.edge_softmax(g.rowptr, g.col, sd, ss, rows=sel)
+    want = np.concatenate([a[g.rowptr[i]:g.rowptr[i + 1]] for i in sel])
+    assert np.array_equal(part, want)
+
+
+# ------------------------------------------------------------ GAT aggregate
+
+def test_gat_dense_per_head_brute_force():
+    rng = np.random.default_rng(20)
+    for n, H, D in ((6, 1, 4), (11, 3, 5), (16, 2, 8)):
+        g = synth.random_csr(n, n, rng, mean_deg=4, empty_frac=0.15)
+        sd = rng.standard_normal((n, H)).astype(np.float32)
+        ss = rng.standard_normal((n, H)).astype(np.float32)
+        X = rng.standard_normal((n, H * D)).astype(np.float32)
+        Y, _ = oracle.gat(g.rowptr, g.col, sd, ss, X, H, D, slope=0.2)
+        rows = np.repeat(np.arange(n), np.diff(g.rowptr))
+        Xh = X.reshape(n, H, D).astype(np.float64)
+        for h in range(H):
+            S = np.full((n, n), -np.inf)
+            S[rows, g.col] = _lrelu(sd[rows, h].astype(np.float64) + ss[g.col, h].astype(np.float64))
+            P = np.zeros((n, n))
+            for i in range(n):
+                if np.isfinite(S[i]).any():
+                    P[i] = np.exp(S[i] - S[i].max())
+                    P[i] /= P[i].sum()
+            np.testing.assert_allclose(Y.reshape(n, H, D)[:, h, :], P @ Xh[:, h, :],
+                                       rtol=1e-12, atol=1e-13)
+
+
+def test_gat_reduces_to_spmm_and_mean():
+    rng = np.random.default_rng(21)
+    g = synth.random_csr(150, 120, rng, mean_deg=6, dup=True, empty_frac=0.1)
+    X = rng.standard_normal((120, 16)).astype(np.float32)
+    # H = 1 with alpha_in = edge values is the plain SpMM
+    Yg, Ag = oracle.gat(g.rowptr, g.col, None, None, X, 1, 16, alpha_in=g.val.reshape(-1, 1))
+    Ys, As = oracle.spmm(g.rowptr, g.col, g.val, X)
+    assert np.array_equal(Yg, Ys) and np.array_equal(Ag, As)
+    # s_src == 0: every head is the mean of the neighbour rows
+    H, D = 4, 4
+    sd = rng.standard_normal((150, H)).astype(np.float32)
+    Y, _ = oracle.gat(g.rowptr, g.col, sd, np.zeros((120, H), np.float32), X, H, D)
+    for i in range(150):
+        b, e = g.rowptr[i], g.rowptr[i + 1]
+        want = X[g.col[b:e]].astype(np.float64).mean(0) if e > b else np.zeros(16)
+        np.testing.assert_allclose(Y[i], want, rtol=1e-13, atol=1e-15)
+
+
+def test_gat_each_head_is_an_spmm_with_its_weights():
+    rng = np.random.default_rng(22)
+    g = synth.random_csr(90, 70, rng, mean_deg=5)
+    H, D = 3, 2
+    alpha = rng.random((g.nnz, H)).astype(np.float32)
+    X = rng.standard_normal((70, H * D)).astype(np.float32)
+    Y, _ = oracle.gat(g.rowptr, g.col, None, None, X, H, D, alpha_in=alpha)
+    for h in range(H):
+        Yh, _ = oracle.spmm(g.rowptr, g.col, alpha[:, h].copy(),
+                            np.ascontiguousarray(X.reshape(70, H, D)[:, h, :]))
+        assert np.array_equal(Y.reshape(90, H, D)[:, h, :], Yh)
