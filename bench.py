@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Benchmark of the GNN message-passing hot path on one MI355X.
+
+One step is one pass of the whole path over the skewed R-MAT workload
+(2,400,000 nodes, 120,000,000 distinct edges plus self-loops = 122,400,000
+nonzeros, four planted hub rows of 100k-300k edges, bf16 features with fp32
+accumulation):
+
+  a1  balancer (plan rebuild) on the CSR
+  a2  SpMM   Y  = A X           X bf16 [N, 256] -> Y bf16
+  a3  CSR -> CSC transpose (stable, with perm)
+  a1  balancer on the CSC
+  a4  SpMM^T dX = A^T G         G bf16 [N, 256] -> dX bf16
+  a5-a7 fused GAT aggregation: scores -> LeakyReLU -> edge softmax -> 4 x 64 bf16 SpMM
+
+Inputs are resident in HBM before the timed region.  The value is the
+effective HBM bandwidth of the step: algorithmic bytes (what the method must
+move, one gather of a feature row per nonzero) divided by the step time.
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "SpMM & GAT-aggregate effective HBM GB/s (% of peak) and edges/sec, 1 MI355X"
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, help="workload number (default: the skewed R-MAT)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU-baseline time budget")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--group-size", type=int, default=0)
+    ap.add_argument("--alpha-out", action="store_true", help="also write alpha in the GAT step")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------- byte models
+
+def b_spmm(n_out, n_in, E, F, sx, sy):
+    return 4 * (n_out + 1) + 8 * E + E * F * sx + n_out * F * sy
+
+
+def b_csc(N, M, E):
+    return 4 * (N + 1) + 8 * E + 4 * (M + 1) + 12 * E
+
+
+def b_gat(N, E, H, D, sx, sy, alpha_out):
+    return 4 * (N + 1) + 4 * E + 4 * N * H + 4 * E * H + E * H * D * sx + N * H * D * sy + (
+        4 * E * H if alpha_out else 0)
+
+
+def b_plan(N, n_units):
+    return 4 * (N + 1) + 16 * n_units
+
+
+# ----------------------------------------------------------- CPU baseline
+
+def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
+    """Time the oracle (fp64, all host threads) on a random row sample of the
+    SpMM and GAT steps, growing the sample until the budget is spent."""
+    import oracle
+    threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    oracle.set_threads(threads)
+    rng = np.random.default_rng(9)
+    deg = np.diff(g.rowptr.astype(np.int64))
+    rows_all = rng.permutation(g.n_rows).astype(np.int32)
+    done_rows = 0
+    t_total = 0.0
+    bytes_total = 0
+    edges_total = 0
+    chunk = 2000
+    while t_total < budget_s and done_rows < g.n_rows:
+        sel = rows_all[done_rows:done_rows + chunk]
+        done_rows += sel.size
+        e = int(deg[sel].sum())
+        t0 = time.perf_counter()
+        oracle.spmm(g.rowptr, g.col, g.val, X_bits, x_dtype=oracle.BF16, rows=sel)
+        oracle.gat(g.rowptr, g.col, sd, ss, Xg_bits, H, D, slope=0.2, x_dtype=oracle.BF16, rows=sel)
+        t_total += time.perf_counter() - t0
+        bytes_total += b_spmm(sel.size, g.n_cols, e, F, 2, 2) + b_gat(sel.size, e, H, D, 2, 2, False)
+        edges_total += 2 * e
+        chunk = min(chunk * 2, 200000)
+    return dict(value=bytes_total / t_total / 1e9, unit="GB/s", cores=threads, kind="oracle",
+                sample=(f"SpMM (F=256 bf16) + fused GAT (4x64 bf16) on {done_rows} random rows "
+                        f"({edges_total // 2} nonzeros each) of the same graph, fp64 oracle"),
+                seconds=t_total, edges_per_s=edges_total / t_total)
+
+
+# ----------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path has no "
+              f"multi-GPU mode in this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2103_00959_amd as cg
+    from paper_2103_00959_amd import synth
+
+    cfg = synth.CONFIGS[args.config]
+    if "F" not in cfg or "H" not in cfg:
+        raise SystemExit("the step needs a workload with both GCN (F) and GAT (H, D) features")
+    log(f"workload {cfg['name']}; host threads {os.cpu_count()}")
+    t0 = time.time()
+    g = synth.config_graph(args.config, verbose=True)
+    N, M, E = g.n_rows, g.n_cols, g.nnz
+    F, H, D = cfg["F"], cfg["H"], cfg["D"]
+    log(f"graph ready N={N} E={E} in {time.time() - t0:.1f}s")
+    X32 = synth.normal_f32((M, F), 2000 + args.config)
+    X_bits = synth.f32_to_bf16_bits(X32)
+    del X32
+    G_bits = synth.f32_to_bf16_bits(synth.normal_f32((N, F), 4000 + args.config))
+    Xg_bits = synth.f32_to_bf16_bits(synth.normal_f32((M, H * D), 2100 + args.config))
+    rng = np.random.default_rng(3000 + args.config)
+    sd = rng.standard_normal((N, H), dtype=np.float32)
+    ss = rng.standard_normal((M, H), dtype=np.float32)
+    log(f"features ready in {time.time() - t0:.1f}s")
+
+    dev = torch.device("cuda:0")
+
+    def up(a, dt=None):
+        t = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        return t.view(dt) if dt is not None else t
+
+    rowptr, col, val = up(g.rowptr), up(g.col), up(g.val)
+    X = up(X_bits.view(np.int16), torch.bfloat16)
+    Gt = up(G_bits.view(np.int16), torch.bfloat16)
+    Xg = up(Xg_bits.view(np.int16), torch.bfloat16).view(M, H, D)
+    s_dst, s_src = up(sd), up(ss)
+    Y = torch.empty((N, F), dtype=torch.bfloat16, device=dev)
+    dX = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+    Yg = torch.empty((N, H, D), dtype=torch.bfloat16, device=dev)
+    alpha = torch.empty((E, H), dtype=torch.float32, device=dev) if args.alpha_out else None
+    colptr = torch.empty(M + 1, dtype=torch.int32, device=dev)
+    row_t = torch.empty(E, dtype=torch.int32, device=dev)
+    val_t = torch.empty(E, dtype=torch.float32, device=dev)
+    perm = torch.empty(E, dtype=torch.int32, device=dev)
+    ws = torch.empty(cg.csr_to_csc_workspace(N, M, E), dtype=torch.uint8, device=dev)
+    L = cg.lib()
+    stream = cg._stream
+
+    def csc():
+        cg._check(L.cogdl_csr_to_csc(N, M, E, cg._ptr(rowptr), cg._ptr(col), cg._ptr(val),
+                                     cg._ptr(colptr), cg._ptr(row_t), cg._ptr(val_t), cg._ptr(perm),
+                                     cg._ptr(ws), ws.numel(), stream()), "csr_to_csc")
+
+    plan = cg.Plan(rowptr, E, max_feat=max(F, H * D), max_heads=H, group_size=args.group_size)
+    csc()
+    plan_t = cg.Plan(colptr, E, max_feat=F, group_size=args.group_size)
+    torch.cuda.synchronize()
+    info, info_t = plan.info(), plan_t.info()
+    log(f"plan: {info['mode_name']} units={info['n_units']} split_rows={info['n_split_rows']} "
+        f"partials={info['n_partials']}; plan_t: {info_t['mode_name']} units={info_t['n_units']} "
+        f"split_rows={info_t['n_split_rows']}")
+
+    OPS = ["plan", "spmm", "csr_to_csc", "plan_t", "spmm_t", "gat_aggregate"]
+
+    def step(evs=None):
+        mark = (lambda i: evs[i].record()) if evs is not None else (lambda i: None)
+        mark(0)
+        plan.rebuild(rowptr)                                                   # a1
+        mark(1)
+        cg.spmm(rowptr, col, val, X, plan=plan, out=Y)                         # a2
+        mark(2)
+        csc()                                                                  # a3
+        mark(3)
+        plan_t.rebuild(colptr)                                                 # a1 (CSC)
+        mark(4)
+        cg.spmm_t(colptr, row_t, val_t, Gt, plan_t=plan_t, out=dX)             # a4
+        mark(5)
+        cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg,  # a5-a7
+                         alpha_out=alpha)
+        mark(6)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"warmup {i + 1}/{args.warmup} done")
+
+    cg.trace_enable(4096)
+    cg.trace_reset()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    step_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(OPS) + 1)]
+                for _ in range(args.steps)]
+    ev0.record()
+    for i in range(args.steps):
+        step(step_evs[i])
+    ev1.record()
+    torch.cuda.synchronize()
+    op_ms = {op: sum(e[j].elapsed_time(e[j + 1]) for e in step_evs) / args.steps
+             for j, op in enumerate(OPS)}
+    t_wall = time.perf_counter() - t_wall
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    trace = cg.trace_read()
+    cg.trace_enable(0)
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall:.2f}s)")
+
+    # per-kernel device time from the library's own HIP events
+    per = {}
+    for name, ms in trace:
+        s = per.setdefault(name, [0.0, 0])
+        s[0] += ms
+        s[1] += 1
+    kernels = {k: dict(total_ms=v[0] / args.steps, launches=v[1] // args.steps,
+                       avg_ms=v[0] / v[1]) for k, v in per.items()}
+
+    n_split = info["n_split_rows"]
+    n_split_t = info_t["n_split_rows"]
+    B = {
+        "plan": b_plan(N, info["n_units"]),
+        "plan_t": b_plan(M, info_t["n_units"]),
+        "spmm": b_spmm(N, M, E, F, 2, 2),
+        "csr_to_csc": b_csc(N, M, E),
+        "spmm_t": b_spmm(M, N, E, F, 2, 2),
+        "gat_aggregate": b_gat(N, E, H, D, 2, 2, args.alpha_out),
+    }
+    B_step = sum(B.values())
+    value = B_step / (ms_step * 1e-3) / 1e9
+    ops = {}
+    for op in OPS:
+        ms = op_ms[op]
+        ops[op] = dict(ms=ms, algorithmic_GB=B[op] / 1e9,
+                       eff_GBps=(B[op] / (ms * 1e-3) / 1e9) if ms > 0 else None,
+                       pct_peak=(B[op] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS) if ms > 0 else None,
+                       edges_per_s=(E / (ms * 1e-3)) if ms > 0 and not op.startswith("plan") else None)
+    # dominant kernel: the largest device time per step
+    dom = max(("spmm", "spmm_t", "gat"), key=lambda k: kernels.get(k, {"total_ms": 0})["total_ms"])
+    dom_bytes = {
+        "spmm": B["spmm"] - n_split * F * 2,          # split rows' Y is written by spmm_reduce
+        "spmm_t": B["spmm_t"] - n_split_t * F * 2,
+        "gat": B["gat_aggregate"] - n_split * H * D * 2,
+    }[dom]
+    dom_ms = kernels[dom]["avg_ms"]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    roofline = dict(bound="hbm", kernel=dom, achieved=achieved, peak=HBM_PEAK_GBPS, unit="GB/s",
+                    frac=achieved / HBM_PEAK_GBPS, traffic=None,
+                    bytes_per_launch=dom_bytes, avg_ms=dom_ms)
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded R-MAT graph, normal features; no dataset)",
+        "config": {"workload": (f"{cfg['name']}: R-MAT a=0.57 b=0.19 c=0.19, N={N}, nnz={E} "
+                                f"incl. self-loops, 4 hub rows (100k-300k), GCN F={F} bf16, "
+                                f"GAT H={H} x D={D} bf16, fp32 accumulation"),
+                   "n_nodes": N, "nnz": E, "F": F, "H": H, "D": D, "feature_dtype": "bf16",
+                   "accumulate": "f32", "group_size": info["group_size"],
+                   "balancer": info["mode_name"], "alpha_out": bool(args.alpha_out)},
+        "pct_peak": value / HBM_PEAK_GBPS,
+        "edges_per_s": 3 * E / (ms_step * 1e-3),
+        "edges_per_s_note": "nonzeros aggregated per second over the three gathers (SpMM, SpMM^T, GAT)",
+        "ops": ops,
+        "kernels": kernels,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("CPU baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, args.cpu_seconds)
+        log(f"CPU baseline {out['cpu_baseline']['value']:.2f} GB/s on {out['cpu_baseline']['cores']} threads")
+    plan.close()
+    plan_t.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,245 @@
+/*
+ * cogdl.h -- C ABI of the MI355X (gfx950) library of GNN message-passing
+ * operators described in section 2.2 ("Efficient Sparse Operators") of the
+ * CogDL paper (arxiv 2103.00959).
+ *
+ * Graph and feature conventions, for every call below
+ *   - The graph is a sparse matrix A in CSR form: rowptr (int32, n_rows + 1
+ *     entries, rowptr[0] = 0, non-decreasing, rowptr[n_rows] = nnz), col
+ *     (int32, nnz entries, each in [0, n_cols)) and optional per-edge values
+ *     val (fp32, nnz entries; NULL means every value is 1).  Row i is the
+ *     aggregating node u of Eq. 1 and col[k] the neighbour v whose feature is
+ *     gathered.  Columns may be unsorted inside a row and may repeat; repeated
+ *     pairs are separate terms.
+ *   - Dense features are row-major: X is n_cols x F (one row per node), Y is
+ *     n_rows x F; multi-head features are [node][head][d] (H*D per node).
+ *     Per-edge, per-head arrays are edge-major: alpha[k * H + h].
+ *   - Feature arrays may be fp32, bf16 or fp16 (cogdl_dtype); edge values,
+ *     attention scores and alpha are always fp32; accumulation is always fp32;
+ *     narrow outputs are rounded to nearest even.
+ *
+ * Memory and ownership
+ *   - Every array argument is a DEVICE pointer owned by the caller; the
+ *     library neither frees nor retains it.  Outputs are fully overwritten,
+ *     never accumulated into.
+ *   - Only cogdl_plan_create allocates device memory and only
+ *     cogdl_plan_destroy frees it.  The operator calls never allocate.
+ *
+ * Errors
+ *   - Scalars, NULL pointers, dtype codes, alignment-independent layout rules
+ *     and plan/graph consistency are checked on the host before anything is
+ *     launched; on error the call returns the code, launches nothing and
+ *     leaves every output untouched.
+ *   - The library trusts the device contents (rowptr[n_rows] == nnz, columns
+ *     in range): it does not read device memory to check them.
+ *   - A failed launch returns COGDL_ERR_LAUNCH; a device fault surfaces at the
+ *     caller's next synchronization.  No C++ exception crosses this ABI.
+ *
+ * Concurrency and determinism
+ *   - Calls are asynchronous on the given HIP stream (0 = default stream).
+ *   - A plan holds a workspace for the partial sums of split rows, so at most
+ *     one call that uses a given plan may be in flight at a time; give every
+ *     concurrent stream its own plan.
+ *   - Results are deterministic: the same inputs give the same bits on every
+ *     run (no floating-point atomics; split rows are reduced in a fixed order).
+ */
+#ifndef COGDL_H
+#define COGDL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    COGDL_OK = 0,
+    COGDL_ERR_INVALID = 1,   /* bad scalar, NULL pointer or inconsistent sizes */
+    COGDL_ERR_DTYPE = 2,     /* unknown or unsupported dtype code */
+    COGDL_ERR_PLAN = 3,      /* plan does not match the graph or the feature width */
+    COGDL_ERR_NOMEM = 4,     /* device allocation failed (plan creation only) */
+    COGDL_ERR_LAUNCH = 5,    /* a kernel launch or HIP runtime call failed */
+    COGDL_ERR_TOO_LARGE = 6  /* a size exceeds what the int32 index format can hold */
+} cogdl_status;
+
+typedef enum { COGDL_F32 = 0, COGDL_BF16 = 1, COGDL_F16 = 2 } cogdl_dtype;
+
+/* Backend choice of the workload balancer (section 2.2, the balancer listing). */
+typedef enum {
+    COGDL_BALANCE_AUTO = 0,            /* data-aware choice, see cogdl_plan_create */
+    COGDL_BALANCE_ROW_SPLIT = 1,       /* one work unit per row, rows in order */
+    COGDL_BALANCE_NEIGHBOR_GROUP = 2   /* rows cut into neighbour groups of <= group_size edges */
+} cogdl_balance;
+
+#define COGDL_MAX_HEADS 64
+#define COGDL_DEFAULT_GROUP_SIZE 256
+
+typedef struct cogdl_plan cogdl_plan;   /* opaque; owns device work lists and workspace */
+
+typedef struct {
+    int32_t n_rows;
+    int64_t nnz;
+    int32_t group_size;
+    int32_t max_feat;
+    int32_t max_heads;
+    int32_t mode;           /* COGDL_BALANCE_ROW_SPLIT or COGDL_BALANCE_NEIGHBOR_GROUP, as chosen */
+    int32_t n_units;        /* work units in execution order */
+    int32_t n_split_rows;   /* rows cut into more than one unit */
+    int32_t n_partials;     /* partial-sum slots used by split rows */
+    int64_t device_bytes;   /* device memory owned by the plan */
+} cogdl_plan_info;
+
+/* Human-readable name of a status code (static storage). */
+const char *cogdl_status_string(cogdl_status s);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int32_t cogdl_version(void);
+
+/* ------------------------------------------------------------------------
+ * Workload balancer -- section 2.2, the "workload balance abstraction"
+ * listing: a preprocessing step, run once per graph, that inspects the degree
+ * distribution, picks the row-split or the neighbour-group backend and emits
+ * the auxiliary arrays the aggregation kernels consume.
+ *
+ * mode AUTO picks ROW_SPLIT when at least 90% of the rows have a degree d with
+ * avg/2 <= d <= 2*avg (avg = nnz / n_rows), NEIGHBOR_GROUP otherwise.  In
+ * NEIGHBOR_GROUP mode each row with more than group_size edges is cut into
+ * consecutive groups of group_size edges (the last one shorter); every such
+ * group is reduced into a partial sum that a second, fixed-order pass adds up.
+ * Units are executed longest first.  The result of every operator is the same
+ * for both modes up to fp32 summation order.
+ *
+ * rowptr      device, n_rows + 1 int32 (read on `stream` during the build).
+ * max_feat    largest feature width F (or H*D) the plan will serve, >= 1.
+ * max_heads   largest head count H the plan will serve in the attention calls
+ *             (0 if it serves only cogdl_spmm / cogdl_spmm_t), <= COGDL_MAX_HEADS.
+ * group_size  neighbour-group size in edges, >= 1 (0 = COGDL_DEFAULT_GROUP_SIZE).
+ * The build runs asynchronously on `stream`; *out is valid immediately and
+ * every later call on the same stream sees the finished plan.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowptr,
+                               int32_t max_feat, int32_t max_heads, cogdl_balance mode,
+                               int32_t group_size, hipStream_t stream, cogdl_plan **out);
+
+/* Re-run the balancer of an existing plan on a rowptr with the plan's n_rows
+ * and nnz (same mode request and group size).  Allocates nothing. */
+cogdl_status cogdl_plan_rebuild(cogdl_plan *plan, const int32_t *rowptr, hipStream_t stream);
+
+/* Free the plan (synchronizes the device first).  NULL is accepted. */
+cogdl_status cogdl_plan_destroy(cogdl_plan *plan);
+
+/* Read the plan's counters back to the host (synchronizes `stream`). */
+cogdl_status cogdl_plan_query(const cogdl_plan *plan, hipStream_t stream, cogdl_plan_info *info);
+
+/* Copy the work units, in execution order, to `units` (device, 4 int32 per
+ * unit: row, first edge, end edge, partial slot or -1).  `capacity` is the
+ * number of units the buffer holds; at most min(capacity, n_units) are
+ * written.  Test and inspection aid. */
+cogdl_status cogdl_plan_units(const cogdl_plan *plan, int32_t *units, int64_t capacity,
+                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Generalized SpMM -- section 2.2, Eq. 1 with reduce = sum and compute =
+ * multiply, i.e. H' = A H:
+ *     Y[i, f] = sum_{k = rowptr[i]}^{rowptr[i+1]-1} val[k] * X[col[k], f]
+ * X: n_cols x F of x_dtype; Y: n_rows x F of y_dtype (an empty row gives 0).
+ * plan: NULL for the plain row-split mapping, else a plan built on this
+ * rowptr (same n_rows and nnz) with max_feat >= F.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                        const int32_t *col, const float *val, int32_t F, const void *X,
+                        cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype,
+                        const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * CSR -> CSC transpose of the graph structure, the setup of the backward
+ * pass of Eq. 1 (the gradient with respect to H is A^T G).
+ *   colptr[j]  = number of edges with col < j           (n_cols + 1 int32)
+ *   perm[p]    = CSR edge id stored at CSC slot p       (nnz int32, nullable)
+ *   row_t[p]   = row of that edge                       (nnz int32)
+ *   val_t[p]   = bit copy of val[perm[p]]               (nnz fp32, nullable;
+ *                                                        must be NULL if val is)
+ * Inside a column the edges appear in increasing CSR edge id (a stable sort),
+ * so every output is unique and reproduced bit for bit.
+ * workspace: device scratch of at least the size cogdl_csr_to_csc_workspace
+ * reports for these sizes (256-byte aligned); its contents are clobbered.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_csr_to_csc_workspace(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                        size_t *bytes);
+cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                              const int32_t *col, const float *val, int32_t *colptr,
+                              int32_t *row_t, float *val_t, int32_t *perm, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Transposed SpMM for the backward pass of Eq. 1:
+ *     dX[j, f] = sum_{p = colptr[j]}^{colptr[j+1]-1} val_t[p] * G[row_t[p], f]
+ * i.e. dX = A^T G, using the CSC arrays from cogdl_csr_to_csc.  n_rows,
+ * n_cols and nnz describe A (not A^T): G is n_rows x F, dX is n_cols x F.
+ * plan_t: NULL, or a plan built on colptr (n_cols rows, nnz edges).
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *colptr,
+                          const int32_t *row_t, const float *val_t, int32_t F, const void *G,
+                          cogdl_dtype g_dtype, void *dX, cogdl_dtype dx_dtype,
+                          const cogdl_plan *plan_t, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * SDDMM + LeakyReLU + edge-wise softmax -- section 2.2: the sampled
+ * dense-dense product T = A (.) (P Q^T) and the edge-wise softmax
+ *     alpha'_uv = exp(alpha_uv) / sum_{w in N(u)} exp(alpha_uw)
+ * taken over the edges of each row u, per head.  The attention score is the
+ * additive GAT form (the SDDMM with P = [s_dst, 1], Q = [1, s_src] per head):
+ *     t = s_dst[i, h] + s_src[col[k], h],   e = t > 0 ? t : negative_slope * t
+ *     alpha[k * H + h] = exp(e - m) / sum_{k' in row i} exp(e' - m)
+ * where m is the row maximum of e for head h.
+ * s_dst: n_rows x H fp32; s_src: n_cols x H fp32; alpha: nnz x H fp32.
+ * 1 <= H <= COGDL_MAX_HEADS.  plan: NULL or a plan with max_heads >= H.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col, int32_t H,
+                                      const float *s_dst, const float *s_src,
+                                      float negative_slope, float *alpha,
+                                      const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Fused GAT aggregation: the scores, LeakyReLU and edge softmax above followed
+ * by the multi-head SpMM of section 2.2 (one weight per edge and head):
+ *     Y[i, h, d] = sum_{k in row i} alpha[k, h] * X[col[k], h, d]
+ * alpha never has to reach memory.  With alpha_in != NULL the attention steps
+ * are skipped and alpha_in (nnz x H fp32, e.g. a permuted alpha for the
+ * backward pass) is used as the weights; s_dst / s_src may then be NULL.
+ * With alpha_out != NULL the softmax weights are also written (nnz x H fp32).
+ * X: n_cols x (H*D) of x_dtype; Y: n_rows x (H*D) of y_dtype.
+ * 1 <= H <= COGDL_MAX_HEADS, D >= 1.  plan: NULL or a plan with
+ * max_feat >= H*D and max_heads >= H.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                 const int32_t *rowptr, const int32_t *col, int32_t H, int32_t D,
+                                 const float *s_dst, const float *s_src, float negative_slope,
+                                 const float *alpha_in, const void *X, cogdl_dtype x_dtype,
+                                 void *Y, cogdl_dtype y_dtype, float *alpha_out,
+                                 const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel tracing (instrumentation, not part of the paper's method).  When
+ * enabled, every kernel the library launches is bracketed by two HIP events
+ * recorded on its launch stream, so the device time of each launch can be
+ * read back.  cogdl_trace_enable(capacity) creates `capacity` event pairs
+ * (0 disables tracing and frees them); launches beyond the capacity are not
+ * recorded.  cogdl_trace_get synchronizes on the i-th stop event and returns
+ * the kernel's name (static storage) and its duration in milliseconds.  The
+ * tracer is process-wide and not thread-safe.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_trace_enable(int32_t capacity);
+cogdl_status cogdl_trace_reset(void);
+int32_t cogdl_trace_count(void);
+cogdl_status cogdl_trace_get(int32_t i, const char **name, float *ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COGDL_H */

@@ -1,1 +1,294 @@
-"""MI355X-native GNN message-passing operators (CogDL, arxiv 2103.00959, section 2.2)."""
+"""MI355X-native GNN message-passing operators of the CogDL paper (arxiv 2103.00959, section 2.2).
+
+Thin ctypes binding over ``libcogdl_mi355.so`` (see ``include/cogdl.h``):
+argument marshalling only.  Every step runs in the library's HIP kernels on
+the current torch stream; torch is used for device memory and streams.  The
+binding fails loudly when the library or a GPU is missing: there is no CPU
+fallback.
+
+    spmm(rowptr, col, val, X, plan=None, out_dtype=None)          -> Y = A X
+    csr_to_csc(rowptr, col, val, n_cols)                          -> colptr, row_t, val_t, perm
+    spmm_t(colptr, row_t, val_t, G, plan_t=None, out_dtype=None)  -> dX = A^T G
+    sddmm_edge_softmax(rowptr, col, s_dst, s_src, slope, plan)    -> alpha [nnz, H]
+    gat_aggregate(rowptr, col, s_dst, s_src, X, slope, ...)       -> Y [n, H, D] (, alpha)
+    Plan(rowptr, nnz, max_feat, max_heads, mode, group_size)      -> the workload balancer
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcogdl_mi355.so")
+
+COGDL_F32, COGDL_BF16, COGDL_F16 = 0, 1, 2
+BALANCE = {"auto": 0, "row_split": 1, "neighbor_group": 2}
+MODE_NAMES = {1: "row_split", 2: "neighbor_group"}
+MAX_HEADS = 64
+
+_lib = None
+
+
+class CogdlError(RuntimeError):
+    pass
+
+
+class _PlanInfo(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int32), ("nnz", ctypes.c_int64), ("group_size", ctypes.c_int32),
+                ("max_feat", ctypes.c_int32), ("max_heads", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("n_units", ctypes.c_int32), ("n_split_rows", ctypes.c_int32),
+                ("n_partials", ctypes.c_int32), ("device_bytes", ctypes.c_int64)]
+
+
+def lib():
+    """Load the HIP library (after torch, so both share one HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+    if not os.path.exists(LIB_PATH):
+        raise CogdlError(f"{LIB_PATH} is missing: build it with `python -m paper_2103_00959_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    L.cogdl_status_string.restype = ctypes.c_char_p
+    L.cogdl_status_string.argtypes = [ctypes.c_int]
+    L.cogdl_version.restype = i32
+    L.cogdl_plan_create.argtypes = [i32, i64, P, i32, i32, ctypes.c_int, i32, P, ctypes.POINTER(P)]
+    L.cogdl_plan_rebuild.argtypes = [P, P, P]
+    L.cogdl_plan_destroy.argtypes = [P]
+    L.cogdl_plan_query.argtypes = [P, P, ctypes.POINTER(_PlanInfo)]
+    L.cogdl_plan_units.argtypes = [P, P, i64, P]
+    L.cogdl_spmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
+    L.cogdl_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
+    L.cogdl_csr_to_csc_workspace.argtypes = [i32, i32, i64, ctypes.POINTER(sz)]
+    L.cogdl_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P, sz, P]
+    L.cogdl_sddmm_edge_softmax.argtypes = [i32, i32, i64, P, P, i32, P, P, f32, P, P, P]
+    L.cogdl_gat_aggregate.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, P, ctypes.c_int,
+                                      P, ctypes.c_int, P, P, P]
+    L.cogdl_trace_enable.argtypes = [i32]
+    L.cogdl_trace_count.restype = i32
+    L.cogdl_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
+    for name in ("cogdl_trace_enable", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
+                 "cogdl_plan_units", "cogdl_spmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
+                 "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        msg = lib().cogdl_status_string(status).decode()
+        raise CogdlError(f"{what}: {msg} (status {status})")
+
+
+def _dtype_code(t) -> int:
+    import torch
+    codes = {torch.float32: COGDL_F32, torch.bfloat16: COGDL_BF16, torch.float16: COGDL_F16}
+    if t.dtype not in codes:
+        raise CogdlError(f"unsupported feature dtype {t.dtype}")
+    return codes[t.dtype]
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    import torch
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise CogdlError(f"{name} must be a CUDA (HIP) tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise CogdlError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise CogdlError(f"{name} must be contiguous")
+    return t
+
+
+class Plan:
+    """The data-aware workload balancer (section 2.2): run once per graph."""
+
+    def __init__(self, rowptr, nnz: int, max_feat: int, max_heads: int = 0, mode: str = "auto",
+                 group_size: int = 0):
+        import torch
+        _dev(rowptr, "rowptr", torch.int32)
+        self.rowptr = rowptr
+        self.n_rows = rowptr.numel() - 1
+        self.nnz = int(nnz)
+        h = ctypes.c_void_p()
+        _check(lib().cogdl_plan_create(self.n_rows, self.nnz, _ptr(rowptr), int(max_feat),
+                                       int(max_heads), BALANCE[mode], int(group_size), _stream(),
+                                       ctypes.byref(h)), "cogdl_plan_create")
+        self._h = h
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise CogdlError("plan destroyed")
+        return self._h
+
+    def rebuild(self, rowptr=None):
+        import torch
+        if rowptr is not None:
+            _dev(rowptr, "rowptr", torch.int32)
+            self.rowptr = rowptr
+        _check(lib().cogdl_plan_rebuild(self.handle, _ptr(self.rowptr), _stream()), "cogdl_plan_rebuild")
+
+    def info(self) -> dict:
+        inf = _PlanInfo()
+        _check(lib().cogdl_plan_query(self.handle, _stream(), ctypes.byref(inf)), "cogdl_plan_query")
+        d = {f: getattr(inf, f) for f, _ in _PlanInfo._fields_}
+        d["mode_name"] = MODE_NAMES.get(d["mode"], "?")
+        return d
+
+    def units(self):
+        import torch
+        n = self.info()["n_units"]
+        out = torch.empty((max(n, 1), 4), dtype=torch.int32, device="cuda")
+        _check(lib().cogdl_plan_units(self.handle, _ptr(out), n, _stream()), "cogdl_plan_units")
+        return out[:n]
+
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            lib().cogdl_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def trace_enable(capacity: int = 4096):
+    """Record HIP events around every library kernel launch (0 disables)."""
+    _check(lib().cogdl_trace_enable(int(capacity)), "cogdl_trace_enable")
+
+
+def trace_reset():
+    _check(lib().cogdl_trace_reset(), "cogdl_trace_reset")
+
+
+def trace_read() -> list:
+    """[(kernel name, milliseconds)] of the launches recorded since the last reset."""
+    L = lib()
+    out = []
+    for i in range(L.cogdl_trace_count()):
+        name, ms = ctypes.c_char_p(), ctypes.c_float()
+        _check(L.cogdl_trace_get(i, ctypes.byref(name), ctypes.byref(ms)), "cogdl_trace_get")
+        out.append((name.value.decode(), ms.value))
+    return out
+
+
+def _plan_handle(plan):
+    return None if plan is None else plan.handle
+
+
+def spmm(rowptr, col, val, X, plan: Plan | None = None, out_dtype=None, out=None):
+    """Y[i] = sum_k val[k] * X[col[k]] over row i (Eq. 1, sum of products)."""
+    import torch
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
+    _dev(val, "val", torch.float32), _dev(X, "X")
+    n_rows = rowptr.numel() - 1
+    F = X.shape[1] if X.dim() > 1 else 1
+    if out is None:
+        out = torch.empty((n_rows, F), dtype=out_dtype or X.dtype, device=X.device)
+    _dev(out, "out")
+    _check(lib().cogdl_spmm(n_rows, X.shape[0], col.numel(), _ptr(rowptr), _ptr(col), _ptr(val), F,
+                            _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), _plan_handle(plan),
+                            _stream()), "cogdl_spmm")
+    return out
+
+
+def csr_to_csc_workspace(n_rows: int, n_cols: int, nnz: int) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().cogdl_csr_to_csc_workspace(n_rows, n_cols, nnz, ctypes.byref(b)),
+           "cogdl_csr_to_csc_workspace")
+    return b.value
+
+
+def csr_to_csc(rowptr, col, val, n_cols: int, workspace=None, with_perm: bool = True):
+    """Stable transpose: (colptr, row_t, val_t, perm); inside a column edges keep CSR order."""
+    import torch
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(val, "val", torch.float32)
+    n_rows = rowptr.numel() - 1
+    nnz = col.numel()
+    dev = rowptr.device
+    colptr = torch.empty(n_cols + 1, dtype=torch.int32, device=dev)
+    row_t = torch.empty(nnz, dtype=torch.int32, device=dev)
+    val_t = None if val is None else torch.empty(nnz, dtype=torch.float32, device=dev)
+    perm = torch.empty(nnz, dtype=torch.int32, device=dev) if with_perm else None
+    need = csr_to_csc_workspace(n_rows, n_cols, nnz)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    _check(lib().cogdl_csr_to_csc(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(val),
+                                  _ptr(colptr), _ptr(row_t), _ptr(val_t), _ptr(perm), _ptr(workspace),
+                                  workspace.numel(), _stream()), "cogdl_csr_to_csc")
+    return colptr, row_t, val_t, perm
+
+
+def spmm_t(colptr, row_t, val_t, G, plan_t: Plan | None = None, out_dtype=None, out=None):
+    """dX = A^T G from the CSC arrays of A; G is n_rows x F."""
+    import torch
+    _dev(colptr, "colptr", torch.int32), _dev(row_t, "row_t", torch.int32)
+    _dev(val_t, "val_t", torch.float32), _dev(G, "G")
+    n_cols = colptr.numel() - 1
+    F = G.shape[1] if G.dim() > 1 else 1
+    if out is None:
+        out = torch.empty((n_cols, F), dtype=out_dtype or G.dtype, device=G.device)
+    _dev(out, "out")
+    _check(lib().cogdl_spmm_t(G.shape[0], n_cols, row_t.numel(), _ptr(colptr), _ptr(row_t),
+                              _ptr(val_t), F, _ptr(G), _dtype_code(G), _ptr(out), _dtype_code(out),
+                              _plan_handle(plan_t), _stream()), "cogdl_spmm_t")
+    return out
+
+
+def sddmm_edge_softmax(rowptr, col, s_dst, s_src, negative_slope: float = 0.2,
+                       plan: Plan | None = None, out=None):
+    """alpha[k, h] = softmax over row i of LeakyReLU(s_dst[i, h] + s_src[col[k], h])."""
+    import torch
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
+    _dev(s_dst, "s_dst", torch.float32), _dev(s_src, "s_src", torch.float32)
+    H = s_dst.shape[1]
+    nnz = col.numel()
+    if out is None:
+        out = torch.empty((nnz, H), dtype=torch.float32, device=col.device)
+    _dev(out, "alpha", torch.float32)
+    _check(lib().cogdl_sddmm_edge_softmax(rowptr.numel() - 1, s_src.shape[0], nnz, _ptr(rowptr),
+                                          _ptr(col), H, _ptr(s_dst), _ptr(s_src),
+                                          float(negative_slope), _ptr(out), _plan_handle(plan),
+                                          _stream()), "cogdl_sddmm_edge_softmax")
+    return out
+
+
+def gat_aggregate(rowptr, col, s_dst, s_src, X, negative_slope: float = 0.2, alpha_in=None,
+                  return_alpha: bool = False, plan: Plan | None = None, out_dtype=None, out=None,
+                  alpha_out=None):
+    """Fused GAT aggregation.  X is [n_cols, H, D]; returns Y [n_rows, H, D] (and alpha)."""
+    import torch
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(X, "X")
+    _dev(s_dst, "s_dst", torch.float32), _dev(s_src, "s_src", torch.float32)
+    _dev(alpha_in, "alpha_in", torch.float32)
+    if X.dim() != 3:
+        raise CogdlError("X must be [n_cols, H, D]")
+    n_cols, H, D = X.shape
+    n_rows = rowptr.numel() - 1
+    nnz = col.numel()
+    if out is None:
+        out = torch.empty((n_rows, H, D), dtype=out_dtype or X.dtype, device=X.device)
+    _dev(out, "out")
+    if return_alpha and alpha_out is None:
+        alpha_out = torch.empty((nnz, H), dtype=torch.float32, device=X.device)
+    _dev(alpha_out, "alpha_out", torch.float32)
+    _check(lib().cogdl_gat_aggregate(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(s_dst),
+                                     _ptr(s_src), float(negative_slope), _ptr(alpha_in), _ptr(X),
+                                     _dtype_code(X), _ptr(out), _dtype_code(out), _ptr(alpha_out),
+                                     _plan_handle(plan), _stream()), "cogdl_gat_aggregate")
+    return (out, alpha_out) if return_alpha else out

@@ -1,0 +1,218 @@
+// Device helpers shared by the gfx950 kernels: feature formats, vector loads
+// and stores, wave64 lane exchange.  Every kernel runs with 64-lane
+// wavefronts; sub-groups of S lanes (S a power of two <= 64) are aligned
+// inside a wavefront.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cogdl.h"
+
+namespace cogdl {
+
+constexpr int kWave = 64;
+
+// ----------------------------------------------------------------- formats
+
+struct bf16_t { uint16_t bits; };
+struct f16_t { uint16_t bits; };
+
+template <typename T> struct Fmt;
+template <> struct Fmt<float> { static constexpr int bytes = 4; static constexpr cogdl_dtype code = COGDL_F32; };
+template <> struct Fmt<bf16_t> { static constexpr int bytes = 2; static constexpr cogdl_dtype code = COGDL_BF16; };
+template <> struct Fmt<f16_t> { static constexpr int bytes = 2; static constexpr cogdl_dtype code = COGDL_F16; };
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t h)
+{
+    _Float16 v;
+    uint16_t b = (uint16_t)h;
+    __builtin_memcpy(&v, &b, 2);
+    return (float)v;
+}
+
+// fp32 -> fp16 with the hardware conversion (round to nearest even).
+__device__ __forceinline__ uint32_t f32_to_f16(float f)
+{
+    _Float16 v = (_Float16)f;
+    uint16_t b;
+    __builtin_memcpy(&b, &v, 2);
+    return b;
+}
+
+// Load VEC consecutive elements (VEC * bytes is 4, 8 or 16, or VEC == 1)
+// starting at element index `idx` and widen them to fp32.
+template <typename T, int VEC>
+__device__ __forceinline__ void load_vec(const T *__restrict__ base, int64_t idx, float (&out)[VEC]);
+
+template <>
+__device__ __forceinline__ void load_vec<float, 4>(const float *__restrict__ p, int64_t i, float (&o)[4])
+{
+    float4 v = *reinterpret_cast<const float4 *>(p + i);
+    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+}
+template <>
+__device__ __forceinline__ void load_vec<float, 1>(const float *__restrict__ p, int64_t i, float (&o)[1])
+{
+    o[0] = p[i];
+}
+template <>
+__device__ __forceinline__ void load_vec<bf16_t, 8>(const bf16_t *__restrict__ p, int64_t i, float (&o)[8])
+{
+    uint4 v = *reinterpret_cast<const uint4 *>(p + i);
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x); o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z); o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+}
+template <>
+__device__ __forceinline__ void load_vec<bf16_t, 1>(const bf16_t *__restrict__ p, int64_t i, float (&o)[1])
+{
+    o[0] = __uint_as_float((uint32_t)p[i].bits << 16);
+}
+template <>
+__device__ __forceinline__ void load_vec<f16_t, 8>(const f16_t *__restrict__ p, int64_t i, float (&o)[8])
+{
+    uint4 v = *reinterpret_cast<const uint4 *>(p + i);
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        o[2 * j] = f16_bits_to_f32(w[j] & 0xffffu);
+        o[2 * j + 1] = f16_bits_to_f32(w[j] >> 16);
+    }
+}
+template <>
+__device__ __forceinline__ void load_vec<f16_t, 1>(const f16_t *__restrict__ p, int64_t i, float (&o)[1])
+{
+    o[0] = f16_bits_to_f32(p[i].bits);
+}
+
+// Store VEC fp32 values as T (rounded to nearest even for narrow T).
+template <typename T, int N>
+__device__ __forceinline__ void store_vec(T *__restrict__ base, int64_t idx, const float (&v)[N]);
+
+template <>
+__device__ __forceinline__ void store_vec<float, 4>(float *__restrict__ p, int64_t i, const float (&v)[4])
+{
+    *reinterpret_cast<float4 *>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
+}
+template <>
+__device__ __forceinline__ void store_vec<float, 8>(float *__restrict__ p, int64_t i, const float (&v)[8])
+{
+    *reinterpret_cast<float4 *>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4 *>(p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <>
+__device__ __forceinline__ void store_vec<float, 1>(float *__restrict__ p, int64_t i, const float (&v)[1])
+{
+    p[i] = v[0];
+}
+template <>
+__device__ __forceinline__ void store_vec<bf16_t, 8>(bf16_t *__restrict__ p, int64_t i, const float (&v)[8])
+{
+    uint4 w;
+    w.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
+    w.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
+    w.z = f32_to_bf16(v[4]) | (f32_to_bf16(v[5]) << 16);
+    w.w = f32_to_bf16(v[6]) | (f32_to_bf16(v[7]) << 16);
+    *reinterpret_cast<uint4 *>(p + i) = w;
+}
+template <>
+__device__ __forceinline__ void store_vec<bf16_t, 4>(bf16_t *__restrict__ p, int64_t i, const float (&v)[4])
+{
+    uint2 w;
+    w.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
+    w.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
+    *reinterpret_cast<uint2 *>(p + i) = w;
+}
+template <>
+__device__ __forceinline__ void store_vec<bf16_t, 1>(bf16_t *__restrict__ p, int64_t i, const float (&v)[1])
+{
+    p[i].bits = (uint16_t)f32_to_bf16(v[0]);
+}
+template <>
+__device__ __forceinline__ void store_vec<f16_t, 8>(f16_t *__restrict__ p, int64_t i, const float (&v)[8])
+{
+    uint4 w;
+    w.x = f32_to_f16(v[0]) | (f32_to_f16(v[1]) << 16);
+    w.y = f32_to_f16(v[2]) | (f32_to_f16(v[3]) << 16);
+    w.z = f32_to_f16(v[4]) | (f32_to_f16(v[5]) << 16);
+    w.w = f32_to_f16(v[6]) | (f32_to_f16(v[7]) << 16);
+    *reinterpret_cast<uint4 *>(p + i) = w;
+}
+template <>
+__device__ __forceinline__ void store_vec<f16_t, 4>(f16_t *__restrict__ p, int64_t i, const float (&v)[4])
+{
+    uint2 w;
+    w.x = f32_to_f16(v[0]) | (f32_to_f16(v[1]) << 16);
+    w.y = f32_to_f16(v[2]) | (f32_to_f16(v[3]) << 16);
+    *reinterpret_cast<uint2 *>(p + i) = w;
+}
+template <>
+__device__ __forceinline__ void store_vec<f16_t, 1>(f16_t *__restrict__ p, int64_t i, const float (&v)[1])
+{
+    p[i].bits = (uint16_t)f32_to_f16(v[0]);
+}
+
+// Store VEC values where the output may be wider than the input vector
+// (fp32 output of a 16-bit input uses two 16-byte stores per 8 values).
+template <typename T, int VEC>
+__device__ __forceinline__ void store_out(T *__restrict__ p, int64_t i, const float (&v)[VEC])
+{
+    store_vec<T, VEC>(p, i, v);
+}
+template <>
+__device__ __forceinline__ void store_out<float, 8>(float *__restrict__ p, int64_t i, const float (&v)[8])
+{
+    store_vec<float, 8>(p, i, v);
+}
+template <>
+__device__ __forceinline__ void store_out<bf16_t, 4>(bf16_t *__restrict__ p, int64_t i, const float (&v)[4])
+{
+    store_vec<bf16_t, 4>(p, i, v);
+}
+
+// ------------------------------------------------------------ lane exchange
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
+
+// Value of `v` held by lane `src` (0..63) of the calling wavefront.
+__device__ __forceinline__ int lane_bcast(int v, int src)
+{
+    return __builtin_amdgcn_ds_bpermute(src << 2, v);
+}
+__device__ __forceinline__ float lane_bcast(float v, int src)
+{
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
+}
+
+__device__ __forceinline__ float lane_xor(float v, int mask)
+{
+    return __int_as_float(__builtin_amdgcn_ds_bpermute((lane_id() ^ mask) << 2, __float_as_int(v)));
+}
+
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Merge two online-softmax states (m, z): the pair describing
+// z * exp(m) = sum exp(e).  An empty state is (-inf, 0).
+__device__ __forceinline__ void softmax_merge(float &m, float &z, float m2, float z2)
+{
+    float mn = fmaxf(m, m2);
+    if (mn == -INFINITY) return;
+    z = z * __expf(m - mn) + z2 * __expf(m2 - mn);
+    m = mn;
+}
+
+__device__ __forceinline__ float leaky_relu(float t, float slope) { return t > 0.f ? t : slope * t; }
+
+}  // namespace cogdl

@@ -1,0 +1,672 @@
+// Attention path of section 2.2: the SDDMM of per-head scores (additive GAT
+// form), LeakyReLU, the edge-wise softmax over the edges of each destination
+// row, and the multi-head SpMM that aggregates neighbour features with one
+// weight per edge and head.
+//
+// cogdl_sddmm_edge_softmax (alpha only): a wavefront per work unit, lanes laid
+// out as (edge slot, head) so that 64/H edges are scored per step; each lane
+// keeps an online softmax state (m, z), the states of one head are merged
+// across slots with lane exchanges (a butterfly when H is a power of two), and
+// a second sweep writes alpha = exp(e - m) / z with coalesced stores.
+//
+// cogdl_gat_aggregate (fused): the gather mapping of the SpMM (S lanes x VEC
+// features per edge row).  Every lane computes the weight of its own head for
+// each gathered edge and folds it into an online softmax: when a batch of U
+// edges raises the running maximum, the accumulators and the running sum are
+// rescaled once.  The unnormalized sum is divided by z at the end, so alpha
+// never has to reach memory.  Neighbour groups of split rows leave (acc, m, z)
+// per group; a fixed-order merge combines them (the log-sum-exp rule).
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace cogdl {
+namespace {
+
+constexpr int kBlock = 256;
+
+struct GatArgs {
+    const int4 *units;
+    const int32_t *n_units;
+    int32_t n_rows;
+    const int32_t *rowptr;
+    const int32_t *col;
+    int32_t H;
+    int32_t D;
+    int64_t W;                  // H * D
+    const float *s_dst;
+    const float *s_src;
+    float slope;
+    const float *alpha_in;      // weights given: skip the attention steps
+    const void *X;
+    void *Y;
+    float *alpha_out;
+    float *partials;
+    int64_t pstride;
+    float *gstats;              // per partial slot: m[max_heads], z[max_heads]
+    int32_t sstride;            // 2 * max_heads
+    int32_t slab;
+    int32_t log2S;
+};
+
+template <typename TX, typename TY, int VEC, int CH>
+__global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
+{
+    constexpr int U = (VEC == 1 ? 16 : 8) / CH;
+    const int log2S = a.log2S;
+    const int S = 1 << log2S;
+    const int lane = lane_id();
+    const int lig = lane & (S - 1);
+    const int gbase = lane & ~(S - 1);
+    const int64_t u = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
+    const int H = a.H;
+
+    int row, beg, end, part;
+    if (a.units) {
+        if (u >= *a.n_units) return;
+        const int4 d = a.units[u];
+        row = d.x; beg = d.y; end = d.z; part = d.w;
+    } else {
+        if (u >= a.n_rows) return;
+        row = (int)u;
+        beg = a.rowptr[row];
+        end = a.rowptr[row + 1];
+        part = -1;
+    }
+    const bool soft = a.alpha_in == nullptr;
+
+    const int64_t f0 = (int64_t)blockIdx.y * a.slab;
+    const int64_t f_end = (f0 + a.slab < a.W) ? f0 + a.slab : a.W;
+    int64_t fe[CH];
+    bool act[CH];
+    int hd[CH];
+    float sd[CH], m[CH], z[CH];
+    float acc[CH][VEC];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        fe[c] = f0 + (int64_t)(c * S + lig) * VEC;
+        act[c] = fe[c] < f_end;
+        hd[c] = act[c] ? (int)(fe[c] / a.D) : 0;
+        sd[c] = soft ? a.s_dst[(int64_t)row * H + hd[c]] : 0.f;
+        m[c] = -INFINITY;
+        z[c] = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
+    }
+
+    const TX *__restrict__ X = static_cast<const TX *>(a.X);
+    const int32_t *__restrict__ col = a.col;
+
+    int c_cur = 0;
+    if (beg + lig < end) c_cur = col[beg + lig];
+    for (int k0 = beg; k0 < end; k0 += S) {
+        const int n = (end - k0 < S) ? end - k0 : S;
+        int c_nxt = 0;
+        if (k0 + S + lig < end) c_nxt = col[k0 + S + lig];
+        for (int j = 0; j < n; j += U) {
+            int cc[U];
+            bool ok[U];
+#pragma unroll
+            for (int t = 0; t < U; ++t) {
+                ok[t] = j + t < n;
+                cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
+            }
+            float w[U][CH];
+            float xv[U][CH][VEC];
+#pragma unroll
+            for (int t = 0; t < U; ++t)
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    if (ok[t] && act[c]) {
+                        w[t][c] = soft ? a.s_src[(int64_t)cc[t] * H + hd[c]]
+                                       : a.alpha_in[(int64_t)(k0 + j + t) * H + hd[c]];
+                        load_vec<TX, VEC>(X, (int64_t)cc[t] * a.W + fe[c], xv[t][c]);
+                    } else {
+                        w[t][c] = soft ? -INFINITY : 0.f;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) xv[t][c][e] = 0.f;
+                    }
+                }
+            if (soft) {
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    float mb = m[c];
+#pragma unroll
+                    for (int t = 0; t < U; ++t) {
+                        if (w[t][c] != -INFINITY) w[t][c] = leaky_relu(sd[c] + w[t][c], a.slope);
+                        mb = fmaxf(mb, w[t][c]);
+                    }
+                    if (mb > m[c]) {
+                        const float r = __expf(m[c] - mb);
+                        z[c] *= r;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
+                        m[c] = mb;
+                    }
+                    float zb = 0.f;
+#pragma unroll
+                    for (int t = 0; t < U; ++t) {
+                        w[t][c] = (w[t][c] == -INFINITY) ? 0.f : __expf(w[t][c] - m[c]);
+                        zb += w[t][c];
+                    }
+                    z[c] += zb;
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < U; ++t)
+#pragma unroll
+                for (int c = 0; c < CH; ++c)
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xv[t][c][e], acc[c][e]);
+        }
+        c_cur = c_nxt;
+    }
+
+    if (part >= 0) {
+        // neighbour group of a split row: unnormalized partial + (m, z) per head
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            if (!act[c]) continue;
+            store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+            if (soft && fe[c] % a.D == 0) {
+                a.gstats[(int64_t)part * a.sstride + hd[c]] = m[c];
+                a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + hd[c]] = z[c];
+            }
+        }
+        return;
+    }
+
+    float rz[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        rz[c] = (soft && z[c] > 0.f) ? 1.f / z[c] : 1.f;
+        float v[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[e] = acc[c][e] * rz[c];
+        if (act[c]) store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
+    }
+
+    if (!soft || a.alpha_out == nullptr) return;
+    // alpha for this whole-row unit: lanes as (edge slot, head); the (m, z) of
+    // head h comes from the lane holding the first feature of h in this slab.
+    const int eps = S / H;
+    const int h1 = lig % H;
+    const int slot = lig / H;
+    const int64_t hf = (int64_t)h1 * a.D;
+    const bool mine_head = hf >= f0 && hf < f_end;
+    const int idx = mine_head ? (int)((hf - f0) / VEC) : 0;
+    const int src_c = idx / S, src_l = idx % S;
+    float m1 = 0.f, r1 = 0.f;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const float mm = lane_bcast(m[c], gbase + src_l);
+        const float rr = lane_bcast(rz[c], gbase + src_l);
+        if (c == src_c) { m1 = mm; r1 = rr; }
+    }
+    if (!mine_head || slot >= eps) return;
+    const float sd1 = a.s_dst[(int64_t)row * H + h1];
+    for (int k = beg + slot; k < end; k += eps) {
+        const float e = leaky_relu(sd1 + a.s_src[(int64_t)col[k] * H + h1], a.slope);
+        a.alpha_out[(int64_t)k * H + h1] = __expf(e - m1) * r1;
+    }
+}
+
+// --------------------------------------------------- softmax-only kernels
+
+struct SoftArgs {
+    const int4 *units;
+    const int32_t *n_units;
+    int32_t n_rows;
+    const int32_t *rowptr;
+    const int32_t *col;
+    int32_t H;
+    const float *s_dst;
+    const float *s_src;
+    float slope;
+    float *alpha;
+    float *gstats;
+    int32_t sstride;
+    const int4 *part_units;     // k_alpha_split: {row, beg, end, split}
+    const int32_t *n_parts;
+    const float *rstats;        // per split row: m[max_heads], z[max_heads]
+};
+
+// Merge the (m, z) states of the lanes holding the same head h = lane % H:
+// slots are lane / H, eps = 64 / H of them.  Result in every lane of head h.
+__device__ __forceinline__ void merge_slots(float &m, float &z, int H)
+{
+    const int lane = lane_id();
+    if ((H & (H - 1)) == 0) {
+        for (int off = H; off < kWave; off <<= 1) {
+            const float m2 = lane_xor(m, off);
+            const float z2 = lane_xor(z, off);
+            softmax_merge(m, z, m2, z2);
+        }
+        return;
+    }
+    const int eps = kWave / H;
+    const int h = lane % H;
+    float mm = -INFINITY, zz = 0.f;
+    for (int s = 0; s < eps; ++s) {
+        const float m2 = lane_bcast(m, s * H + h < kWave ? s * H + h : h);
+        const float z2 = lane_bcast(z, s * H + h < kWave ? s * H + h : h);
+        softmax_merge(mm, zz, m2, z2);
+    }
+    m = mm;
+    z = zz;
+}
+
+__device__ __forceinline__ float edge_e(const SoftArgs &a, float sd, int k, int h)
+{
+    return leaky_relu(sd + a.s_src[(int64_t)a.col[k] * a.H + h], a.slope);
+}
+
+// One wavefront per unit.  Whole rows: alpha written; neighbour groups: (m, z)
+// per head into gstats.
+__global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
+{
+    const int lane = lane_id();
+    const int64_t u = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    int row, beg, end, part;
+    if (a.units) {
+        if (u >= *a.n_units) return;
+        const int4 d = a.units[u];
+        row = d.x; beg = d.y; end = d.z; part = d.w;
+    } else {
+        if (u >= a.n_rows) return;
+        row = (int)u;
+        beg = a.rowptr[row];
+        end = a.rowptr[row + 1];
+        part = -1;
+    }
+    const int H = a.H;
+    const int eps = kWave / H;
+    const int h = lane % H;
+    const int slot = lane / H;
+    const bool live = slot < eps;
+    const float sd = a.s_dst[(int64_t)row * H + h];
+    float m = -INFINITY, z = 0.f;
+    constexpr int R = 4;
+    for (int k0 = beg + slot; k0 < end; k0 += R * eps) {
+        float e[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int k = k0 + r * eps;
+            e[r] = (live && k < end) ? edge_e(a, sd, k, h) : -INFINITY;
+        }
+        float mb = m;
+#pragma unroll
+        for (int r = 0; r < R; ++r) mb = fmaxf(mb, e[r]);
+        if (mb > m) {
+            z *= __expf(m - mb);
+            m = mb;
+        }
+        float zb = 0.f;
+#pragma unroll
+        for (int r = 0; r < R; ++r) zb += __expf(e[r] - m);
+        z += zb;
+    }
+    if (!live) { m = -INFINITY; z = 0.f; }
+    merge_slots(m, z, H);
+    if (part >= 0) {
+        if (slot == 0) {
+            a.gstats[(int64_t)part * a.sstride + h] = m;
+            a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + h] = z;
+        }
+        return;
+    }
+    if (!live) return;
+    const float rz = 1.f / z;
+    for (int k = beg + slot; k < end; k += eps)
+        a.alpha[(int64_t)k * H + h] = __expf(edge_e(a, sd, k, h) - m) * rz;
+}
+
+// Per split row: merge the (m, z) of its groups in slot order (64/H chains,
+// then the chains in order) into rstats.
+__device__ __forceinline__ void merge_groups(const float *gstats, int sstride, int p0, int np,
+                                             int H, float &m, float &z)
+{
+    const int lane = lane_id();
+    const int chains = kWave / H;
+    const int h = lane % H;
+    const int chain = lane / H;
+    m = -INFINITY;
+    z = 0.f;
+    if (chain < chains) {
+        for (int g = chain; g < np; g += chains) {
+            const float *st = gstats + (int64_t)(p0 + g) * sstride;
+            softmax_merge(m, z, st[h], st[(sstride >> 1) + h]);
+        }
+    }
+    float mm = -INFINITY, zz = 0.f;
+    for (int s = 0; s < chains; ++s) {
+        const int src = s * H + h;
+        const float m2 = lane_bcast(m, src < kWave ? src : h);
+        const float z2 = lane_bcast(z, src < kWave ? src : h);
+        softmax_merge(mm, zz, m2, z2);
+    }
+    m = mm;
+    z = zz;
+}
+
+__global__ __launch_bounds__(kBlock) void k_softmax_merge(const int4 *__restrict__ split_rows,
+                                                          const int32_t *__restrict__ n_split,
+                                                          const float *__restrict__ gstats,
+                                                          int sstride, int H,
+                                                          float *__restrict__ rstats)
+{
+    const int lane = lane_id();
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t ns = *n_split;
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns; s += waves) {
+        const int4 d = split_rows[s];
+        float m, z;
+        merge_groups(gstats, sstride, d.y, d.z, H, m, z);
+        if (lane < H) {
+            rstats[s * sstride + lane] = m;
+            rstats[s * sstride + (sstride >> 1) + lane] = z;
+        }
+    }
+}
+
+// alpha for the edges of split rows, one wavefront per neighbour group.
+__global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
+{
+    const int lane = lane_id();
+    const int H = a.H;
+    const int eps = kWave / H;
+    const int h = lane % H;
+    const int slot = lane / H;
+    if (slot >= eps) return;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t np = *a.n_parts;
+    for (int64_t p = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; p < np; p += waves) {
+        const int4 d = a.part_units[p];
+        const float m = a.rstats[(int64_t)d.w * a.sstride + h];
+        const float rz = 1.f / a.rstats[(int64_t)d.w * a.sstride + (a.sstride >> 1) + h];
+        const float sd = a.s_dst[(int64_t)d.x * H + h];
+        for (int k = d.y + slot; k < d.z; k += eps)
+            a.alpha[(int64_t)k * H + h] = __expf(edge_e(a, sd, k, h) - m) * rz;
+    }
+}
+
+// GAT split rows: combine the groups' unnormalized sums with the log-sum-exp
+// rule, write Y and the row's (m, z) for the alpha pass.
+template <typename TY>
+__global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ split_rows,
+                                                       const int32_t *__restrict__ n_split,
+                                                       const float *__restrict__ partials,
+                                                       int64_t pstride,
+                                                       const float *__restrict__ gstats,
+                                                       int sstride, int H, int D,
+                                                       float *__restrict__ rstats,
+                                                       TY *__restrict__ Y)
+{
+    const int lane = lane_id();
+    const int wv = threadIdx.x / kWave;
+    const int64_t W = (int64_t)H * D;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t ns = *n_split;
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + wv; s < ns; s += waves) {
+        const int4 d = split_rows[s];
+        const int64_t row = d.x;
+        const int p0 = d.y, np = d.z;
+        float m, z;
+        merge_groups(gstats, sstride, p0, np, H, m, z);
+        if (lane < H) {
+            rstats[s * sstride + lane] = m;
+            rstats[s * sstride + (sstride >> 1) + lane] = z;
+        }
+        // lane h holds the merged state of head h
+        for (int64_t f0 = 0; f0 < W; f0 += kWave) {
+            const int64_t f = f0 + lane;
+            const int h = f < W ? (int)(f / D) : 0;
+            const float M = lane_bcast(m, h);
+            const float rZ = 1.f / lane_bcast(z, h);
+            if (f >= W) continue;
+            float a0 = 0.f, a1 = 0.f;
+            int g = 0;
+            for (; g + 2 <= np; g += 2) {
+                const int64_t q0 = (int64_t)(p0 + g), q1 = q0 + 1;
+                a0 = fmaf(partials[q0 * pstride + f], __expf(gstats[q0 * sstride + h] - M), a0);
+                a1 = fmaf(partials[q1 * pstride + f], __expf(gstats[q1 * sstride + h] - M), a1);
+            }
+            if (g < np) {
+                const int64_t q0 = (int64_t)(p0 + g);
+                a0 = fmaf(partials[q0 * pstride + f], __expf(gstats[q0 * sstride + h] - M), a0);
+            }
+            const float v[1] = {(a0 + a1) * rZ};
+            store_vec<TY, 1>(Y, row * W + f, v);
+        }
+    }
+}
+
+// Plain weighted sums of split rows (alpha_in given): Y = sum of partials.
+template <typename TY>
+__global__ __launch_bounds__(kBlock) void k_sum_reduce(const int4 *__restrict__ split_rows,
+                                                       const int32_t *__restrict__ n_split,
+                                                       const float *__restrict__ partials,
+                                                       int64_t pstride, int64_t W,
+                                                       TY *__restrict__ Y)
+{
+    const int lane = lane_id();
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t ns = *n_split;
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns; s += waves) {
+        const int4 d = split_rows[s];
+        for (int64_t f = lane; f < W; f += kWave) {
+            float a0 = 0.f, a1 = 0.f;
+            const float *p = partials + (int64_t)d.y * pstride + f;
+            int g = 0;
+            for (; g + 2 <= d.z; g += 2) {
+                a0 += p[(int64_t)g * pstride];
+                a1 += p[(int64_t)(g + 1) * pstride];
+            }
+            if (g < d.z) a0 += p[(int64_t)g * pstride];
+            const float v[1] = {a0 + a1};
+            store_vec<TY, 1>(Y, (int64_t)d.x * W + f, v);
+        }
+    }
+}
+
+using GatKernel = void (*)(GatArgs);
+
+template <typename TX, typename TY>
+GatKernel pick_gat_kernel(int vec, int ch)
+{
+    constexpr int V = (int)(16 / sizeof(TX));
+    if (vec == 1) {
+        if (ch == 1) return k_gat<TX, TY, 1, 1>;
+        if (ch == 2) return k_gat<TX, TY, 1, 2>;
+        return k_gat<TX, TY, 1, 4>;
+    }
+    if (ch == 1) return k_gat<TX, TY, V, 1>;
+    if (ch == 2) return k_gat<TX, TY, V, 2>;
+    return k_gat<TX, TY, V, 4>;
+}
+
+template <typename TX>
+GatKernel pick_gat_y(int ydt, int vec, int ch)
+{
+    if (ydt == COGDL_F32) return pick_gat_kernel<TX, float>(vec, ch);
+    if (ydt == COGDL_BF16) return pick_gat_kernel<TX, bf16_t>(vec, ch);
+    return pick_gat_kernel<TX, f16_t>(vec, ch);
+}
+
+GatKernel pick_gat(int xdt, int ydt, int vec, int ch)
+{
+    if (xdt == COGDL_F32) return pick_gat_y<float>(ydt, vec, ch);
+    if (xdt == COGDL_BF16) return pick_gat_y<bf16_t>(ydt, vec, ch);
+    return pick_gat_y<f16_t>(ydt, vec, ch);
+}
+
+unsigned grid_waves(int64_t work)
+{
+    int64_t b = (work + (kBlock / kWave) - 1) / (kBlock / kWave);
+    if (b > 2048) b = 2048;
+    if (b < 1) b = 1;
+    return (unsigned)b;
+}
+
+cogdl_status check_graph(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                         const int32_t *col, int32_t H)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
+    if (H < 1 || H > COGDL_MAX_HEADS) return COGDL_ERR_INVALID;
+    if (nnz > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (n_rows > 0 && !rowptr) return COGDL_ERR_INVALID;
+    if (nnz > 0 && (!col || n_rows == 0 || n_cols == 0)) return COGDL_ERR_INVALID;
+    return COGDL_OK;
+}
+
+}  // namespace
+}  // namespace cogdl
+
+using namespace cogdl;
+
+extern "C" {
+
+cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col, int32_t H,
+                                      const float *s_dst, const float *s_src, float negative_slope,
+                                      float *alpha, const cogdl_plan *plan, hipStream_t stream)
+{
+    cogdl_status st = check_graph(n_rows, n_cols, nnz, rowptr, col, H);
+    if (st != COGDL_OK) return st;
+    if (n_rows > 0 && !s_dst) return COGDL_ERR_INVALID;
+    if (nnz > 0 && (!s_src || !alpha)) return COGDL_ERR_INVALID;
+    const Plan *P = plan_of(plan);
+    if (P && (P->n_rows != n_rows || P->nnz != nnz || P->max_heads < H)) return COGDL_ERR_PLAN;
+    if (nnz == 0) return COGDL_OK;
+
+    SoftArgs a{};
+    a.units = P ? P->units : nullptr;
+    a.n_units = P ? P->n_units_dev() : nullptr;
+    a.n_rows = n_rows;
+    a.rowptr = rowptr;
+    a.col = col;
+    a.H = H;
+    a.s_dst = s_dst;
+    a.s_src = s_src;
+    a.slope = negative_slope;
+    a.alpha = alpha;
+    a.gstats = P ? P->gstats : nullptr;
+    a.sstride = P ? 2 * P->max_heads : 0;
+    a.part_units = P ? P->part_units : nullptr;
+    a.n_parts = P ? P->n_parts_dev() : nullptr;
+    a.rstats = P ? P->rstats : nullptr;
+    const int64_t units = P ? P->cap_units : n_rows;
+    const unsigned blocks = (unsigned)((units + (kBlock / kWave) - 1) / (kBlock / kWave));
+    COGDL_LAUNCH("softmax", k_softmax, blocks, kBlock, stream, a);
+    if (P) {
+        COGDL_LAUNCH("softmax_merge", k_softmax_merge, grid_waves(P->cap_split), kBlock, stream,
+                     P->split_rows, P->n_split_dev(), P->gstats, a.sstride, H, P->rstats);
+        COGDL_LAUNCH("softmax_alpha_split", k_alpha_split, grid_waves(P->cap_partials), kBlock,
+                     stream, a);
+    }
+    return COGDL_OK;
+}
+
+cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                 const int32_t *rowptr, const int32_t *col, int32_t H, int32_t D,
+                                 const float *s_dst, const float *s_src, float negative_slope,
+                                 const float *alpha_in, const void *X, cogdl_dtype x_dtype,
+                                 void *Y, cogdl_dtype y_dtype, float *alpha_out,
+                                 const cogdl_plan *plan, hipStream_t stream)
+{
+    cogdl_status st = check_graph(n_rows, n_cols, nnz, rowptr, col, H);
+    if (st != COGDL_OK) return st;
+    if (D < 1) return COGDL_ERR_INVALID;
+    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype)) return COGDL_ERR_DTYPE;
+    const int64_t W = (int64_t)H * D;
+    if (W > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    const bool soft = alpha_in == nullptr;
+    if (soft && n_rows > 0 && !s_dst) return COGDL_ERR_INVALID;
+    if (soft && nnz > 0 && !s_src) return COGDL_ERR_INVALID;
+    if (n_rows > 0 && !Y) return COGDL_ERR_INVALID;
+    if (nnz > 0 && !X) return COGDL_ERR_INVALID;
+    const Plan *P = plan_of(plan);
+    if (P && (P->n_rows != n_rows || P->nnz != nnz || P->max_feat < W || (soft && P->max_heads < H)))
+        return COGDL_ERR_PLAN;
+    if (n_rows == 0) return COGDL_OK;
+
+    const bool aligned = ((uintptr_t)X % 16 == 0) && ((uintptr_t)Y % 16 == 0);
+    RowMap m = row_map(W, dtype_bytes(x_dtype), D, aligned);
+    if (m.S < H) {
+        m.S = next_pow2(H);
+        m.log2S = log2i(m.S);
+        m.slab = m.S * m.ch * m.vec;
+        m.n_slabs = (int)((W + m.slab - 1) / m.slab);
+    }
+    GatArgs a{};
+    a.units = P ? P->units : nullptr;
+    a.n_units = P ? P->n_units_dev() : nullptr;
+    a.n_rows = n_rows;
+    a.rowptr = rowptr;
+    a.col = col;
+    a.H = H;
+    a.D = D;
+    a.W = W;
+    a.s_dst = s_dst;
+    a.s_src = s_src;
+    a.slope = negative_slope;
+    a.alpha_in = alpha_in;
+    a.X = X;
+    a.Y = Y;
+    a.alpha_out = soft ? alpha_out : nullptr;
+    a.partials = P ? P->partials : nullptr;
+    a.pstride = P ? (P->max_feat + 7) / 8 * 8 : 0;
+    a.gstats = P ? P->gstats : nullptr;
+    a.sstride = P ? 2 * P->max_heads : 0;
+    a.slab = m.slab;
+    a.log2S = m.log2S;
+    const int64_t units = P ? P->cap_units : n_rows;
+    const int64_t upb = kBlock >> m.log2S;
+    const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
+    GatKernel k = pick_gat(x_dtype, y_dtype, m.vec, m.ch);
+    COGDL_LAUNCH("gat", k, grid, kBlock, stream, a);
+    if (!P) return COGDL_OK;
+
+    const unsigned rb = grid_waves(P->cap_split);
+    if (!soft) {
+        if (y_dtype == COGDL_F32)
+            COGDL_LAUNCH("gat_sum_reduce", k_sum_reduce<float>, rb, kBlock, stream, P->split_rows,
+                         P->n_split_dev(), P->partials, a.pstride, W, static_cast<float *>(Y));
+        else if (y_dtype == COGDL_BF16)
+            COGDL_LAUNCH("gat_sum_reduce", k_sum_reduce<bf16_t>, rb, kBlock, stream, P->split_rows,
+                         P->n_split_dev(), P->partials, a.pstride, W, static_cast<bf16_t *>(Y));
+        else
+            COGDL_LAUNCH("gat_sum_reduce", k_sum_reduce<f16_t>, rb, kBlock, stream, P->split_rows,
+                         P->n_split_dev(), P->partials, a.pstride, W, static_cast<f16_t *>(Y));
+        return COGDL_OK;
+    }
+    if (y_dtype == COGDL_F32)
+        COGDL_LAUNCH("gat_reduce", k_gat_reduce<float>, rb, kBlock, stream, P->split_rows,
+                     P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats,
+                     static_cast<float *>(Y));
+    else if (y_dtype == COGDL_BF16)
+        COGDL_LAUNCH("gat_reduce", k_gat_reduce<bf16_t>, rb, kBlock, stream, P->split_rows,
+                     P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats,
+                     static_cast<bf16_t *>(Y));
+    else
+        COGDL_LAUNCH("gat_reduce", k_gat_reduce<f16_t>, rb, kBlock, stream, P->split_rows,
+                     P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats,
+                     static_cast<f16_t *>(Y));
+    if (alpha_out) {
+        SoftArgs sa{};
+        sa.col = col;
+        sa.H = H;
+        sa.s_dst = s_dst;
+        sa.s_src = s_src;
+        sa.slope = negative_slope;
+        sa.alpha = alpha_out;
+        sa.sstride = a.sstride;
+        sa.part_units = P->part_units;
+        sa.n_parts = P->n_parts_dev();
+        sa.rstats = P->rstats;
+        COGDL_LAUNCH("gat_alpha_split", k_alpha_split, grid_waves(P->cap_partials), kBlock, stream,
+                     sa);
+    }
+    return COGDL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,151 @@
+// Host-side internals shared by the translation units of the library: the
+// plan object, the device primitives (scan, stable radix sort) and argument
+// validation helpers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "cogdl.h"
+
+namespace cogdl {
+
+// Work unit: rows [beg, end) of one row, reduced either straight into the
+// output (part < 0) or into partial-sum slot `part`.
+// Layout int4 {row, beg, end, part}.
+
+struct Plan {
+    int32_t n_rows = 0;
+    int64_t nnz = 0;
+    int32_t group_size = 0;
+    int32_t max_feat = 0;
+    int32_t max_heads = 0;
+    cogdl_balance mode_req = COGDL_BALANCE_AUTO;
+    int device = 0;
+
+    int64_t cap_units = 0;     // >= sum_i max(1, ceil(d_i / G))
+    int64_t cap_split = 0;     // >= number of rows with d_i > G
+    int64_t cap_partials = 0;  // >= sum over split rows of ceil(d_i / G)
+
+    void *base = nullptr;
+    size_t bytes = 0;
+
+    int4 *units = nullptr;        // [cap_units] execution order
+    int4 *units_tmp = nullptr;    // [cap_units] row order (build scratch)
+    int4 *split_rows = nullptr;   // [cap_split] {row, first partial slot, #slots, 0}
+    int4 *part_units = nullptr;   // [cap_partials] {row, beg, end, split index}
+    int32_t *row_units = nullptr; // [n_rows + 1] exclusive scan; [n_rows] = #units
+    int32_t *row_parts = nullptr; // [n_rows + 1]; [n_rows] = #partial slots
+    int32_t *row_split = nullptr; // [n_rows + 1]; [n_rows] = #split rows
+    int32_t *counters = nullptr;  // [4]: 0 close-degree rows, 1 chosen mode
+    uint32_t *sort_keys = nullptr;   // [3 * cap_units]: keys, then 2 ping buffers
+    uint32_t *sort_vals = nullptr;   // [3 * cap_units]: order, then 2 ping buffers
+    void *sort_ws = nullptr;
+    size_t sort_ws_bytes = 0;
+    void *scan_ws = nullptr;
+    size_t scan_ws_bytes = 0;
+    float *partials = nullptr;    // [cap_partials * max_feat]
+    float *gstats = nullptr;      // [cap_partials * max_heads * 2] per-group (m, z)
+    float *rstats = nullptr;      // [cap_split * max_heads * 2] per-split-row (m, z)
+
+    const int32_t *n_units_dev() const { return row_units + n_rows; }
+    const int32_t *n_split_dev() const { return row_split + n_rows; }
+    const int32_t *n_parts_dev() const { return row_parts + n_rows; }
+};
+
+const Plan *plan_of(const cogdl_plan *h);
+
+// Kernel tracing hooks (no-ops unless cogdl_trace_enable was called).
+int trace_begin(const char *name, hipStream_t s);
+void trace_end(int slot, hipStream_t s);
+
+// ---------------------------------------------------------- primitives
+
+// Exclusive prefix sum of n int32 values; out has n + 1 entries and out[n]
+// receives the total.  in and out may alias.  Workspace size from
+// scan_workspace_bytes(n).
+size_t scan_workspace_bytes(int64_t n);
+hipError_t exclusive_scan(const int32_t *in, int32_t *out, int64_t n, void *ws, hipStream_t s);
+
+// Stable LSD radix sort of (key, value) pairs on the low `bits` bits of the
+// keys.  vals_in == nullptr means values 0..n-1.  Results land in keys_out /
+// vals_out (keys_out may be nullptr when the sorted keys are not needed).
+// ping: 2 * n keys and 2 * n values of scratch.
+size_t radix_workspace_bytes(int64_t n);
+hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
+                            uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
+                            uint32_t *ping_vals, void *ws, hipStream_t s);
+
+// Fill n int32 with a value (a kernel, so it is safe inside graph capture).
+hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+
+// ---------------------------------------------------------- validation
+
+inline bool dtype_ok(int d) { return d == COGDL_F32 || d == COGDL_BF16 || d == COGDL_F16; }
+inline int dtype_bytes(int d) { return d == COGDL_F32 ? 4 : 2; }
+
+inline int bits_for(uint64_t max_value)
+{
+    int b = 0;
+    while (b < 32 && (max_value >> b) != 0) ++b;
+    return b;
+}
+
+inline int next_pow2(int v)
+{
+    int p = 1;
+    while (p < v) p <<= 1;
+    return p;
+}
+
+inline int log2i(int v)
+{
+    int l = 0;
+    while ((1 << l) < v) ++l;
+    return l;
+}
+
+// Launch geometry of the gather kernels for one row of `width` elements of a
+// `bytes`-wide format: VEC elements per lane, S lanes per edge row, CH chunks
+// per lane and the number of feature slabs.
+struct RowMap {
+    int vec = 1;
+    int S = 64;
+    int log2S = 6;
+    int ch = 1;
+    int slab = 0;      // elements per slab
+    int n_slabs = 1;
+};
+
+RowMap row_map(int64_t width, int elem_bytes, int unit_elems /* vec must divide it */,
+               bool aligned16);
+
+}  // namespace cogdl
+
+// Launch a kernel between the tracing events; return COGDL_ERR_LAUNCH from the
+// enclosing function if the launch fails.
+#define COGDL_LAUNCH(name, kern, grid, block, stream, ...)            \
+    do {                                                             \
+        const int _slot = ::cogdl::trace_begin(name, stream);        \
+        kern<<<(grid), (block), 0, (stream)>>>(__VA_ARGS__);         \
+        const hipError_t _e = hipGetLastError();                     \
+        ::cogdl::trace_end(_slot, stream);                           \
+        if (_e != hipSuccess) return COGDL_ERR_LAUNCH;               \
+    } while (0)
+
+// Same for functions returning hipError_t.
+#define COGDL_LAUNCH_HIP(name, kern, grid, block, stream, ...)        \
+    do {                                                             \
+        const int _slot = ::cogdl::trace_begin(name, stream);        \
+        kern<<<(grid), (block), 0, (stream)>>>(__VA_ARGS__);         \
+        const hipError_t _e = hipGetLastError();                     \
+        ::cogdl::trace_end(_slot, stream);                           \
+        if (_e != hipSuccess) return _e;                             \
+    } while (0)
+
+#define COGDL_HIP_TRY(expr)                                  \
+    do {                                                     \
+        hipError_t _e = (expr);                              \
+        if (_e != hipSuccess) return COGDL_ERR_LAUNCH;       \
+    } while (0)

@@ -1,0 +1,289 @@
+// Device-wide building blocks used by the balancer and the CSR -> CSC
+// transpose: an exclusive prefix sum and a stable least-significant-digit
+// radix sort of (key, value) pairs.  Both are deterministic (integer work,
+// fixed tile order); neither allocates.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace cogdl {
+
+namespace {
+
+constexpr int kScanBlock = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanBlock * kScanItems;   // 2048
+
+constexpr int kSortBlock = 256;                      // 4 wavefronts
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortBlock * kSortItems;   // 4096
+constexpr int kDigits = 256;                         // 8-bit digits
+
+__device__ __forceinline__ int wave_inclusive_scan(int x)
+{
+    const int lane = lane_id();
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        int y = __builtin_amdgcn_ds_bpermute((lane >= d ? lane - d : lane) << 2, x);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+// Exclusive scan of one value per thread across a 256-thread block; returns
+// the exclusive prefix and writes the block total to *total.
+__device__ __forceinline__ int block_exclusive_scan(int x, int *total)
+{
+    __shared__ int wsum[kScanBlock / kWave];
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    int inc = wave_inclusive_scan(x);
+    if (lane == kWave - 1) wsum[w] = inc;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int i = 0; i < kScanBlock / kWave; ++i) {
+        if (i < w) before += wsum[i];
+        all += wsum[i];
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - x;
+}
+
+__global__ __launch_bounds__(kScanBlock) void k_tile_reduce(const int32_t *__restrict__ in, int64_t n,
+                                                            int32_t *__restrict__ tile_sums)
+{
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i)
+        if (base + i < n) s += in[base + i];
+    int total;
+    block_exclusive_scan(s, &total);
+    if (threadIdx.x == 0) tile_sums[blockIdx.x] = total;
+}
+
+// Scan one tile; add the tile's offset (tile_offs == nullptr: single tile).
+// The block holding the last element also writes out[n] = total.
+__global__ __launch_bounds__(kScanBlock) void k_tile_scan(const int32_t *in, int32_t *out, int64_t n,
+                                                          const int32_t *__restrict__ tile_offs)
+{
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int v[kScanItems];
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        v[i] = (base + i < n) ? in[base + i] : 0;
+        s += v[i];
+    }
+    int total;
+    int run = block_exclusive_scan(s, &total);   // contains a barrier: all reads done
+    const int off = tile_offs ? tile_offs[blockIdx.x] : 0;
+    run += off;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        if (base + i < n) out[base + i] = run;
+        run += v[i];
+    }
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = off + total;
+}
+
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// Per-tile histogram of one 8-bit digit, stored digit-major so that an
+// exclusive scan of the whole table yields every (digit, tile) start slot.
+__global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__restrict__ keys, int64_t n,
+                                                           int shift, int n_tiles,
+                                                           int32_t *__restrict__ hist)
+{
+    __shared__ int32_t h[kDigits];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+#pragma unroll 4
+    for (int i = 0; i < kSortItems; ++i) {
+        int64_t e = base + (int64_t)i * kSortBlock + threadIdx.x;
+        if (e < n) atomicAdd(&h[(keys[e] >> shift) & (kDigits - 1)], 1);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = h[threadIdx.x];
+}
+
+// Stable scatter of one tile.  Wavefront w owns the contiguous quarter
+// [w * 1024, (w + 1) * 1024) of the tile and walks it 64 keys at a time; the
+// rank of a key among equal digits is the number of lower lanes with the same
+// digit (found with eight ballots) plus the running per-wave count, and the
+// waves are then stacked in order per digit.
+__global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
+    const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
+    uint32_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, int64_t n, int shift,
+    int n_tiles, const int32_t *__restrict__ offsets)
+{
+    constexpr int kWaves = kSortBlock / kWave;
+    __shared__ int32_t wcnt[kWaves][kDigits];
+    const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
+#pragma unroll
+    for (int i = 0; i < kWaves; ++i) wcnt[i][tid] = 0;
+    __syncthreads();
+
+    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)w * kWave * kSortItems;
+    const uint64_t lower = __lanemask_lt();
+    uint32_t key[kSortItems], val[kSortItems];
+    int local[kSortItems], dig[kSortItems];
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const int64_t e = base + i * kWave + lane;
+        const bool valid = e < n;
+        const uint32_t k = valid ? keys_in[e] : 0u;
+        key[i] = k;
+        val[i] = valid ? (vals_in ? vals_in[e] : (uint32_t)e) : 0u;
+        const int d = (int)((k >> shift) & (kDigits - 1));
+        uint64_t peers = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const int bit = (d >> b) & 1;
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const int rank = __popcll(peers & lower);
+        int old = 0;
+        if (valid) old = wcnt[w][d];
+        local[i] = old + rank;
+        if (valid && rank == 0) wcnt[w][d] = old + __popcll(peers);
+        dig[i] = valid ? d : -1;
+    }
+    __syncthreads();
+    {
+        int run = offsets[(int64_t)tid * n_tiles + blockIdx.x];
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i) {
+            const int c = wcnt[i][tid];
+            wcnt[i][tid] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        if (dig[i] >= 0) {
+            const int pos = wcnt[w][dig[i]] + local[i];
+            if (keys_out) keys_out[pos] = key[i];
+            vals_out[pos] = val[i];
+        }
+    }
+}
+
+int64_t scan_levels_ints(int64_t n)
+{
+    int64_t total = 0;
+    while (n > kScanTile) {
+        int64_t t = (n + kScanTile - 1) / kScanTile;
+        total += t + 1;
+        n = t;
+    }
+    return total;
+}
+
+hipError_t scan_rec(const int32_t *in, int32_t *out, int64_t n, int32_t *ws, hipStream_t s)
+{
+    if (n <= 0) {
+        COGDL_LAUNCH_HIP("fill", k_fill_i32, 1, 64, s, out, 1, 0);
+        return hipSuccess;
+    }
+    const int64_t tiles = (n + kScanTile - 1) / kScanTile;
+    if (tiles == 1) {
+        COGDL_LAUNCH_HIP("scan_tile", k_tile_scan, 1, kScanBlock, s, in, out, n, nullptr);
+        return hipSuccess;
+    }
+    int32_t *sums = ws;
+    COGDL_LAUNCH_HIP("scan_reduce", k_tile_reduce, (unsigned)tiles, kScanBlock, s, in, n, sums);
+    hipError_t e = scan_rec(sums, sums, tiles, ws + tiles + 1, s);
+    if (e != hipSuccess) return e;
+    COGDL_LAUNCH_HIP("scan_tile", k_tile_scan, (unsigned)tiles, kScanBlock, s, in, out, n, sums);
+    return hipSuccess;
+}
+
+}  // namespace
+
+size_t scan_workspace_bytes(int64_t n) { return (size_t)(scan_levels_ints(n) + 16) * 4; }
+
+hipError_t exclusive_scan(const int32_t *in, int32_t *out, int64_t n, void *ws, hipStream_t s)
+{
+    return scan_rec(in, out, n, static_cast<int32_t *>(ws), s);
+}
+
+hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    COGDL_LAUNCH_HIP("fill", k_fill_i32, (unsigned)blocks, 256, s, p, n, v);
+    return hipSuccess;
+}
+
+size_t radix_workspace_bytes(int64_t n)
+{
+    const int64_t tiles = (n + kSortTile - 1) / kSortTile;
+    const int64_t hist = (int64_t)kDigits * (tiles > 0 ? tiles : 1) + 1;
+    size_t b = (size_t)(hist + 64) * 4;
+    b = (b + 255) & ~size_t(255);
+    return b + scan_workspace_bytes(hist);
+}
+
+hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
+                            uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
+                            uint32_t *ping_vals, void *ws, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    const int64_t tiles = (n + kSortTile - 1) / kSortTile;
+    const int64_t hist_n = (int64_t)kDigits * tiles;
+    int32_t *hist = static_cast<int32_t *>(ws);
+    size_t hist_bytes = ((size_t)(hist_n + 1 + 64) * 4 + 255) & ~size_t(255);
+    void *scan_ws = static_cast<char *>(ws) + hist_bytes;
+
+    int passes = (bits + 7) / 8;
+    if (passes < 1) passes = 1;
+    const uint32_t *src_k = keys_in;
+    const uint32_t *src_v = vals_in;
+    for (int p = 0; p < passes; ++p) {
+        const bool last = (p == passes - 1);
+        uint32_t *dst_k = last ? keys_out : ping_keys + (p & 1) * n;
+        uint32_t *dst_v = last ? vals_out : ping_vals + (p & 1) * n;
+        COGDL_LAUNCH_HIP("radix_hist", k_radix_hist, (unsigned)tiles, kSortBlock, s, src_k, n, 8 * p,
+                         (int)tiles, hist);
+        hipError_t e = exclusive_scan(hist, hist, hist_n, scan_ws, s);
+        if (e != hipSuccess) return e;
+        COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter, (unsigned)tiles, kSortBlock, s, src_k,
+                         src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist);
+        src_k = dst_k;
+        src_v = dst_v;
+    }
+    return hipSuccess;
+}
+
+RowMap row_map(int64_t width, int elem_bytes, int unit_elems, bool aligned16)
+{
+    RowMap m;
+    const int v16 = 16 / elem_bytes;
+    m.vec = (aligned16 && width % v16 == 0 && unit_elems % v16 == 0) ? v16 : 1;
+    const int64_t lanes = (width + m.vec - 1) / m.vec;
+    if (lanes <= kWave) {
+        m.S = next_pow2((int)(lanes > 0 ? lanes : 1));
+        m.ch = 1;
+    } else {
+        m.S = kWave;
+        const int64_t ch = (lanes + kWave - 1) / kWave;
+        m.ch = ch <= 1 ? 1 : (ch <= 2 ? 2 : 4);
+    }
+    m.log2S = log2i(m.S);
+    m.slab = m.S * m.ch * m.vec;
+    m.n_slabs = (int)((width + m.slab - 1) / m.slab);
+    if (m.n_slabs < 1) m.n_slabs = 1;
+    return m;
+}
+
+}  // namespace cogdl

@@ -1,0 +1,308 @@
+// Generalized SpMM of section 2.2, Eq. 1 with reduce = sum and compute =
+// multiply (H' = A H), and the transposed product A^T G of its backward pass.
+//
+// Mapping on gfx950 (64-lane wavefronts):
+//   - A work unit (a whole row, or a neighbour group of a long row) belongs to
+//     a sub-group of S lanes; S lanes times VEC elements cover one feature row
+//     (S = 32 for a 512-byte row read as 16-byte vectors), CH chunks when the
+//     row is wider than 64 vectors, feature slabs beyond that.
+//   - The sub-group reads the unit's column indices and edge values S at a
+//     time with one coalesced load, prefetching the next S while it works, and
+//     hands them to every lane with ds_bpermute.
+//   - For every edge each lane gathers its VEC contiguous features of the
+//     neighbour row (one 16-byte load) and accumulates in fp32 registers; U
+//     edges are unrolled so that U row gathers are in flight per lane.
+//   - A unit that covers a whole row writes the output row once; a neighbour
+//     group writes an fp32 partial row, and a second kernel adds the partials
+//     of each split row in a fixed order (no floating-point atomics).
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace cogdl {
+namespace {
+
+constexpr int kBlock = 256;
+
+struct SpmmArgs {
+    const int4 *units;          // nullptr: one unit per row in row order
+    const int32_t *n_units;     // device count when units != nullptr
+    int32_t n_rows;
+    const int32_t *rowptr;
+    const int32_t *col;
+    const float *val;           // nullptr: all ones
+    const void *X;
+    void *Y;
+    float *partials;
+    int64_t pstride;
+    int64_t F;
+    int32_t slab;
+    int32_t log2S;
+};
+
+template <typename TX, typename TY, int VEC, int CH>
+__global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
+{
+    constexpr int U = (VEC == 1 ? 16 : 8) / CH;
+    const int log2S = a.log2S;
+    const int S = 1 << log2S;
+    const int lane = lane_id();
+    const int lig = lane & (S - 1);
+    const int gbase = lane & ~(S - 1);
+    const int64_t u = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
+
+    int row, beg, end, part;
+    if (a.units) {
+        if (u >= *a.n_units) return;
+        const int4 d = a.units[u];
+        row = d.x; beg = d.y; end = d.z; part = d.w;
+    } else {
+        if (u >= a.n_rows) return;
+        row = (int)u;
+        beg = a.rowptr[row];
+        end = a.rowptr[row + 1];
+        part = -1;
+    }
+
+    const int64_t f0 = (int64_t)blockIdx.y * a.slab;
+    const int64_t f_end = (f0 + a.slab < a.F) ? f0 + a.slab : a.F;
+    int64_t fe[CH];
+    bool act[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        fe[c] = f0 + (int64_t)(c * S + lig) * VEC;
+        act[c] = fe[c] < f_end;
+    }
+    float acc[CH][VEC];
+#pragma unroll
+    for (int c = 0; c < CH; ++c)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
+
+    const TX *__restrict__ X = static_cast<const TX *>(a.X);
+    const int32_t *__restrict__ col = a.col;
+    const float *__restrict__ val = a.val;
+
+    int c_cur = 0;
+    float v_cur = 0.f;
+    if (beg + lig < end) {
+        c_cur = col[beg + lig];
+        v_cur = val ? val[beg + lig] : 1.f;
+    }
+    for (int k0 = beg; k0 < end; k0 += S) {
+        const int n = (end - k0 < S) ? end - k0 : S;
+        const int kn = k0 + S + lig;
+        int c_nxt = 0;
+        float v_nxt = 0.f;
+        if (kn < end) {
+            c_nxt = col[kn];
+            v_nxt = val ? val[kn] : 1.f;
+        }
+        int j = 0;
+        for (; j + U <= n; j += U) {
+            int cc[U];
+            float vv[U];
+#pragma unroll
+            for (int t = 0; t < U; ++t) {
+                cc[t] = lane_bcast(c_cur, gbase + j + t);
+                vv[t] = lane_bcast(v_cur, gbase + j + t);
+            }
+            float xv[U][CH][VEC];
+#pragma unroll
+            for (int t = 0; t < U; ++t)
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    if (act[c]) {
+                        load_vec<TX, VEC>(X, (int64_t)cc[t] * a.F + fe[c], xv[t][c]);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) xv[t][c][e] = 0.f;
+                    }
+                }
+#pragma unroll
+            for (int t = 0; t < U; ++t)
+#pragma unroll
+                for (int c = 0; c < CH; ++c)
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(vv[t], xv[t][c][e], acc[c][e]);
+        }
+        for (; j < n; ++j) {
+            const int cj = lane_bcast(c_cur, gbase + j);
+            const float vj = lane_bcast(v_cur, gbase + j);
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                if (act[c]) {
+                    float x[VEC];
+                    load_vec<TX, VEC>(X, (int64_t)cj * a.F + fe[c], x);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(vj, x[e], acc[c][e]);
+                }
+            }
+        }
+        c_cur = c_nxt;
+        v_cur = v_nxt;
+    }
+
+    if (part < 0) {
+        TY *__restrict__ Y = static_cast<TY *>(a.Y);
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+            if (act[c]) store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
+    } else {
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+            if (act[c]) store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+    }
+}
+
+// Y[row, :] = sum of the row's partial rows, in slot order.  One wavefront per
+// split row (grid-stride over the device-side count); four interleaved chains
+// keep the fp32 summation short for rows with many groups.
+template <typename TY>
+__global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__ split_rows,
+                                                        const int32_t *__restrict__ n_split,
+                                                        const float *__restrict__ partials,
+                                                        int64_t pstride, int64_t F, TY *__restrict__ Y)
+{
+    const int lane = lane_id();
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t ns = *n_split;
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns; s += waves) {
+        const int4 d = split_rows[s];
+        const int64_t row = d.x, p0 = d.y;
+        const int np = d.z;
+        for (int64_t f = lane; f < F; f += kWave) {
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+            const float *p = partials + p0 * pstride + f;
+            int g = 0;
+            for (; g + 4 <= np; g += 4) {
+                a0 += p[(int64_t)g * pstride];
+                a1 += p[(int64_t)(g + 1) * pstride];
+                a2 += p[(int64_t)(g + 2) * pstride];
+                a3 += p[(int64_t)(g + 3) * pstride];
+            }
+            for (; g < np; ++g) a0 += p[(int64_t)g * pstride];
+            const float v[1] = {(a0 + a1) + (a2 + a3)};
+            store_vec<TY, 1>(Y, row * F + f, v);
+        }
+    }
+}
+
+using SpmmKernel = void (*)(SpmmArgs);
+
+template <typename TX, typename TY>
+SpmmKernel pick_kernel(int vec, int ch)
+{
+    constexpr int V = (int)(16 / sizeof(TX));
+    if (vec == 1) {
+        if (ch == 1) return k_spmm<TX, TY, 1, 1>;
+        if (ch == 2) return k_spmm<TX, TY, 1, 2>;
+        return k_spmm<TX, TY, 1, 4>;
+    }
+    if (ch == 1) return k_spmm<TX, TY, V, 1>;
+    if (ch == 2) return k_spmm<TX, TY, V, 2>;
+    return k_spmm<TX, TY, V, 4>;
+}
+
+template <typename TX>
+SpmmKernel pick_y(int ydt, int vec, int ch)
+{
+    if (ydt == COGDL_F32) return pick_kernel<TX, float>(vec, ch);
+    if (ydt == COGDL_BF16) return pick_kernel<TX, bf16_t>(vec, ch);
+    return pick_kernel<TX, f16_t>(vec, ch);
+}
+
+SpmmKernel pick(int xdt, int ydt, int vec, int ch)
+{
+    if (xdt == COGDL_F32) return pick_y<float>(ydt, vec, ch);
+    if (xdt == COGDL_BF16) return pick_y<bf16_t>(ydt, vec, ch);
+    return pick_y<f16_t>(ydt, vec, ch);
+}
+
+cogdl_status reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
+                           hipStream_t s)
+{
+    const int64_t pstride = (P.max_feat + 7) / 8 * 8;
+    int64_t blocks = (P.cap_split + (kBlock / kWave) - 1) / (kBlock / kWave);
+    if (blocks > 2048) blocks = 2048;
+    if (blocks < 1) blocks = 1;
+    const unsigned b = (unsigned)blocks;
+    if (ydt == COGDL_F32)
+        COGDL_LAUNCH(name, k_spmm_reduce<float>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+                     P.partials, pstride, F, static_cast<float *>(Y));
+    else if (ydt == COGDL_BF16)
+        COGDL_LAUNCH(name, k_spmm_reduce<bf16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+                     P.partials, pstride, F, static_cast<bf16_t *>(Y));
+    else
+        COGDL_LAUNCH(name, k_spmm_reduce<f16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+                     P.partials, pstride, F, static_cast<f16_t *>(Y));
+    return COGDL_OK;
+}
+
+// Shared body of cogdl_spmm and cogdl_spmm_t: out_rows x F output, gathering
+// rows of an in_rows x F input through (ptr, idx, w).
+cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const int32_t *ptr,
+                         const int32_t *idx, const float *w, int32_t F, const void *X, int xdt,
+                         void *Y, int ydt, const cogdl_plan *plan_h, hipStream_t s,
+                         const char *name, const char *reduce_name)
+{
+    if (out_rows < 0 || in_rows < 0 || nnz < 0 || F < 0) return COGDL_ERR_INVALID;
+    if (!dtype_ok(xdt) || !dtype_ok(ydt)) return COGDL_ERR_DTYPE;
+    if (nnz > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (out_rows > 0 && !ptr) return COGDL_ERR_INVALID;
+    if (nnz > 0 && (!idx || out_rows == 0 || in_rows == 0)) return COGDL_ERR_INVALID;
+    if (out_rows > 0 && F > 0 && !Y) return COGDL_ERR_INVALID;
+    if (nnz > 0 && F > 0 && !X) return COGDL_ERR_INVALID;
+    const Plan *P = plan_of(plan_h);
+    if (P && (P->n_rows != out_rows || P->nnz != nnz || P->max_feat < F)) return COGDL_ERR_PLAN;
+    if (out_rows == 0 || F == 0) return COGDL_OK;
+
+    const bool aligned = ((uintptr_t)X % 16 == 0) && ((uintptr_t)Y % 16 == 0);
+    const RowMap m = row_map(F, dtype_bytes(xdt), F, aligned);
+    SpmmArgs a;
+    a.units = P ? P->units : nullptr;
+    a.n_units = P ? P->n_units_dev() : nullptr;
+    a.n_rows = out_rows;
+    a.rowptr = ptr;
+    a.col = idx;
+    a.val = w;
+    a.X = X;
+    a.Y = Y;
+    a.partials = P ? P->partials : nullptr;
+    a.pstride = P ? (P->max_feat + 7) / 8 * 8 : 0;
+    a.F = F;
+    a.slab = m.slab;
+    a.log2S = m.log2S;
+    const int64_t units = P ? P->cap_units : out_rows;
+    const int64_t upb = kBlock >> m.log2S;
+    const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
+    SpmmKernel k = pick(xdt, ydt, m.vec, m.ch);
+    COGDL_LAUNCH(name, k, grid, kBlock, s, a);
+    if (P) return reduce_launch(reduce_name, *P, F, Y, ydt, s);
+    return COGDL_OK;
+}
+
+}  // namespace
+}  // namespace cogdl
+
+extern "C" {
+
+cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                        const int32_t *col, const float *val, int32_t F, const void *X,
+                        cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, const cogdl_plan *plan,
+                        hipStream_t stream)
+{
+    return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
+                              (int)y_dtype, plan, stream, "spmm", "spmm_reduce");
+}
+
+cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *colptr,
+                          const int32_t *row_t, const float *val_t, int32_t F, const void *G,
+                          cogdl_dtype g_dtype, void *dX, cogdl_dtype dx_dtype,
+                          const cogdl_plan *plan_t, hipStream_t stream)
+{
+    // A^T has n_cols rows, each gathering rows of the n_rows x F input G.
+    return cogdl::spmm_common(n_cols, n_rows, nnz, colptr, row_t, val_t, F, G, (int)g_dtype, dX,
+                              (int)dx_dtype, plan_t, stream, "spmm_t", "spmm_t_reduce");
+}
+
+}  // extern "C"

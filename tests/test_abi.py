@@ -1,0 +1,144 @@
+"""C-ABI contract tests that need no GPU: the library loads, exports every
+entry point the header declares, and rejects bad arguments on the host before
+anything is launched (only calls whose validation fails are made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2103_00959_amd as cg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cogdl.h")
+
+OK, INVALID, DTYPE, PLAN, NOMEM, LAUNCH, TOO_LARGE = range(7)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(cg.LIB_PATH):
+        from paper_2103_00959_amd import build
+        build.build(verbose=False)
+    return cg.lib()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cogdl_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(L):
+    syms = declared_symbols()
+    assert len(syms) >= 13
+    for s in syms:
+        assert hasattr(L, s), s
+
+
+def test_status_strings_and_version(L):
+    for code in range(7):
+        assert len(L.cogdl_status_string(code)) > 0
+    assert L.cogdl_status_string(99) == b"unknown status"
+    assert L.cogdl_version() >= 100
+
+
+def _p(v):
+    return ctypes.c_void_p(v)
+
+
+FAKE = _p(0x1000)   # never dereferenced: every call below fails validation first
+
+
+def test_spmm_validation(L):
+    # negative sizes
+    assert L.cogdl_spmm(-1, 1, 0, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    assert L.cogdl_spmm(1, 1, -1, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    assert L.cogdl_spmm(1, 1, 0, FAKE, FAKE, None, -4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    # dtype codes
+    assert L.cogdl_spmm(1, 1, 1, FAKE, FAKE, None, 4, FAKE, 3, FAKE, 0, None, None) == DTYPE
+    assert L.cogdl_spmm(1, 1, 1, FAKE, FAKE, None, 4, FAKE, 0, FAKE, -1, None, None) == DTYPE
+    # null pointers
+    assert L.cogdl_spmm(2, 2, 3, None, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    assert L.cogdl_spmm(2, 2, 3, FAKE, None, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    assert L.cogdl_spmm(2, 2, 3, FAKE, FAKE, None, 4, None, 0, FAKE, 0, None, None) == INVALID
+    assert L.cogdl_spmm(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, None, 0, None, None) == INVALID
+    # nnz beyond int32 indices
+    assert L.cogdl_spmm(2, 2, 1 << 31, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == TOO_LARGE
+    # edges but no columns to gather from
+    assert L.cogdl_spmm(2, 0, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    # empty work returns OK without touching the device
+    assert L.cogdl_spmm(0, 5, 0, None, None, None, 4, None, 0, None, 0, None, None) == OK
+    assert L.cogdl_spmm(3, 5, 7, FAKE, FAKE, None, 0, None, 0, None, 0, None, None) == OK
+
+
+def test_spmm_t_validation(L):
+    assert L.cogdl_spmm_t(3, -2, 0, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+    assert L.cogdl_spmm_t(3, 2, 5, FAKE, FAKE, None, 4, FAKE, 7, FAKE, 0, None, None) == DTYPE
+    assert L.cogdl_spmm_t(0, 2, 5, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
+
+
+def test_csc_validation(L):
+    b = ctypes.c_size_t()
+    assert L.cogdl_csr_to_csc_workspace(10, 10, 100, ctypes.byref(b)) == OK
+    small = b.value
+    assert L.cogdl_csr_to_csc_workspace(10, 10, 100000, ctypes.byref(b)) == OK
+    assert b.value > small
+    assert L.cogdl_csr_to_csc_workspace(10, 10, -1, ctypes.byref(b)) == INVALID
+    assert L.cogdl_csr_to_csc_workspace(10, 10, 1 << 31, ctypes.byref(b)) == TOO_LARGE
+    assert L.cogdl_csr_to_csc_workspace(10, 10, 5, None) == INVALID
+    ws = _p(0x10000)
+    # workspace too small / misaligned / missing
+    assert L.cogdl_csr_to_csc(4, 4, 8, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, ws, 16, None) == INVALID
+    assert L.cogdl_csr_to_csc(4, 4, 8, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, _p(0x10010),
+                              1 << 30, None) == INVALID
+    assert L.cogdl_csr_to_csc(4, 4, 8, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, None, 1 << 30,
+                              None) == INVALID
+    # val and val_t must be given together
+    assert L.cogdl_csr_to_csc(4, 4, 8, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws, 1 << 30,
+                              None) == INVALID
+    assert L.cogdl_csr_to_csc(4, 4, 8, FAKE, FAKE, None, None, FAKE, None, FAKE, ws, 1 << 30,
+                              None) == INVALID
+
+
+def test_attention_validation(L):
+    s = ctypes.c_float(0.2)
+    # head count bounds
+    assert L.cogdl_sddmm_edge_softmax(4, 4, 8, FAKE, FAKE, 0, FAKE, FAKE, s, FAKE, None, None) == INVALID
+    assert L.cogdl_sddmm_edge_softmax(4, 4, 8, FAKE, FAKE, 65, FAKE, FAKE, s, FAKE, None, None) == INVALID
+    assert L.cogdl_sddmm_edge_softmax(4, 4, 8, FAKE, FAKE, 2, None, FAKE, s, FAKE, None, None) == INVALID
+    assert L.cogdl_sddmm_edge_softmax(4, 4, 8, FAKE, FAKE, 2, FAKE, FAKE, s, None, None, None) == INVALID
+    assert L.cogdl_gat_aggregate(4, 4, 8, FAKE, FAKE, 2, 0, FAKE, FAKE, s, None, FAKE, 0, FAKE, 0,
+                                 None, None, None) == INVALID
+    assert L.cogdl_gat_aggregate(4, 4, 8, FAKE, FAKE, 2, 4, FAKE, FAKE, s, None, FAKE, 5, FAKE, 0,
+                                 None, None, None) == DTYPE
+    # scores needed unless alpha_in is given
+    assert L.cogdl_gat_aggregate(4, 4, 8, FAKE, FAKE, 2, 4, None, FAKE, s, None, FAKE, 0, FAKE, 0,
+                                 None, None, None) == INVALID
+    assert L.cogdl_gat_aggregate(4, 4, 8, FAKE, FAKE, 2, 4, FAKE, FAKE, s, None, None, 0, FAKE, 0,
+                                 None, None, None) == INVALID
+    assert L.cogdl_gat_aggregate(0, 4, 0, None, None, 2, 4, None, None, s, None, None, 0, None, 0,
+                                 None, None, None) == OK
+
+
+def test_plan_validation(L):
+    h = ctypes.c_void_p()
+    assert L.cogdl_plan_create(4, 8, FAKE, 16, 0, 0, 0, None, None) == INVALID
+    assert L.cogdl_plan_create(-1, 8, FAKE, 16, 0, 0, 0, None, ctypes.byref(h)) == INVALID
+    assert L.cogdl_plan_create(4, 8, FAKE, 0, 0, 0, 0, None, ctypes.byref(h)) == INVALID
+    assert L.cogdl_plan_create(4, 8, FAKE, 16, 65, 0, 0, None, ctypes.byref(h)) == INVALID
+    assert L.cogdl_plan_create(4, 8, FAKE, 16, 0, 3, 0, None, ctypes.byref(h)) == INVALID
+    assert L.cogdl_plan_create(4, 8, FAKE, 16, 0, 0, -5, None, ctypes.byref(h)) == INVALID
+    assert L.cogdl_plan_create(4, 8, None, 16, 0, 0, 0, None, ctypes.byref(h)) == INVALID
+    assert L.cogdl_plan_create(4, 1 << 31, FAKE, 16, 0, 0, 0, None, ctypes.byref(h)) == TOO_LARGE
+    assert L.cogdl_plan_destroy(None) == OK
+    assert L.cogdl_plan_rebuild(None, FAKE, None) == INVALID
+    assert L.cogdl_plan_query(None, None, None) == INVALID
+    assert L.cogdl_plan_units(None, FAKE, 4, None) == INVALID
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    x = torch.zeros(3, 4)
+    with pytest.raises(cg.CogdlError):
+        cg.spmm(torch.zeros(4, dtype=torch.int32), torch.zeros(0, dtype=torch.int32), None, x)

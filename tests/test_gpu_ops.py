@@ -1,0 +1,374 @@
+"""GPU parity: every entry point of the C ABI against the CPU oracle on seeded
+inputs that span several tiles, ragged tails, empty rows, duplicates, unsorted
+columns, hub rows and both balancer backends."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2103_00959_amd import synth
+
+from gpu_util import (TOL_ALPHA, TOL_F32, dev, features, graph_to_dev, say, scaled_error, to_f64,
+                      tol_for)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def cg():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2103_00959_amd as m
+    m.lib()
+    return m
+
+
+def _graph(kind, seed=0):
+    rng = np.random.default_rng(seed)
+    if kind == "small":
+        return synth.random_csr(300, 250, rng, mean_deg=6, empty_frac=0.1)
+    if kind == "dups":
+        return synth.random_csr(500, 170, rng, mean_deg=9, dup=True, unsorted=True, empty_frac=0.15)
+    if kind == "rect":
+        return synth.random_csr(97, 1031, rng, mean_deg=20, unsorted=True)
+    if kind == "hubs":
+        # a few rows far longer than the default neighbour group, many empty rows
+        g = synth.random_csr(3000, 2000, rng, mean_deg=3, empty_frac=0.3)
+        deg = np.diff(g.rowptr).astype(np.int64)
+        hub_rows = [5, 1234, 2999]
+        deg[hub_rows] = [1800, 2000, 700]
+        rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+        col = np.concatenate([np.sort(rng.choice(2000, d, replace=False)) for d in deg]).astype(np.int32)
+        val = rng.standard_normal(col.size).astype(np.float32)
+        return synth.Graph(rowptr, col, val, 3000, 2000)
+    if kind == "cfg1":
+        return synth.config_graph(1)
+    if kind == "empty":
+        return synth.Graph(np.zeros(11, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32), 10, 7)
+    raise KeyError(kind)
+
+
+PLANS = [None, ("auto", 0), ("row_split", 0), ("neighbor_group", 0), ("neighbor_group", 5)]
+
+
+def _make_plan(cg, rowptr_d, nnz, plan_spec, max_feat, max_heads=0):
+    if plan_spec is None:
+        return None
+    mode, G = plan_spec
+    return cg.Plan(rowptr_d, nnz, max_feat=max_feat, max_heads=max_heads, mode=mode, group_size=G)
+
+
+# ---------------------------------------------------------------- SpMM
+
+@pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1"])
+@pytest.mark.parametrize("plan_spec", PLANS)
+def test_spmm_f32(cg, kind, plan_spec):
+    g = _graph(kind)
+    say(f"spmm f32 {kind} plan={plan_spec} n={g.n_rows} nnz={g.nnz}")
+    rp, cl, vl = graph_to_dev(g)
+    for F in (1, 3, 64, 128):
+        xh, xc, xd = features((g.n_cols, F), 7 + F, "f32")
+        plan = _make_plan(cg, rp, g.nnz, plan_spec, F)
+        try:
+            Y = cg.spmm(rp, cl, vl, xd, plan=plan)
+            Yr, Ar = oracle.spmm(g.rowptr, g.col, g.val, xh, x_dtype=xc)
+            err = scaled_error(Y, Yr, Ar)
+            assert err <= TOL_F32, (kind, plan_spec, F, err)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+@pytest.mark.parametrize("F", [2, 8, 65, 256, 300, 1000, 2050])
+def test_spmm_feature_widths(cg, F):
+    g = _graph("hubs", seed=3)
+    say(f"spmm widths F={F}")
+    rp, cl, vl = graph_to_dev(g)
+    xh, xc, xd = features((g.n_cols, F), 11, "f32")
+    Yr, Ar = oracle.spmm(g.rowptr, g.col, g.val, xh, x_dtype=xc)
+    for spec in (None, ("neighbor_group", 64)):
+        plan = _make_plan(cg, rp, g.nnz, spec, F)
+        try:
+            Y = cg.spmm(rp, cl, vl, xd, plan=plan)
+            assert scaled_error(Y, Yr, Ar) <= TOL_F32, (F, spec)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+@pytest.mark.parametrize("xk,yk", [("bf16", "bf16"), ("bf16", "f32"), ("f16", "f16"), ("f16", "f32"),
+                                   ("f32", "bf16"), ("f32", "f16"), ("bf16", "f16")])
+@pytest.mark.parametrize("F", [64, 256, 7])
+def test_spmm_mixed_precision(cg, xk, yk, F):
+    import torch
+    g = _graph("hubs", seed=4)
+    say(f"spmm {xk}->{yk} F={F}")
+    rp, cl, vl = graph_to_dev(g)
+    xh, xc, xd = features((g.n_cols, F), 21, xk)
+    out_dtype = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[yk]
+    Yr, Ar = oracle.spmm(g.rowptr, g.col, g.val, xh, x_dtype=xc)
+    for spec in (None, ("auto", 0), ("neighbor_group", 32)):
+        plan = _make_plan(cg, rp, g.nnz, spec, F)
+        try:
+            Y = cg.spmm(rp, cl, vl, xd, plan=plan, out_dtype=out_dtype)
+            assert Y.dtype == out_dtype
+            err = scaled_error(Y, Yr, Ar)
+            assert err <= tol_for(xk, yk), (xk, yk, F, spec, err)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+def test_spmm_identity_bit_exact(cg):
+    import torch
+    n = 1000
+    rp = dev(np.arange(n + 1, dtype=np.int32))
+    cl = dev(np.arange(n, dtype=np.int32))
+    vl = dev(np.ones(n, np.float32))
+    for kind in ("f32", "bf16", "f16"):
+        xh, xc, xd = features((n, 40), 5, kind)
+        Y = cg.spmm(rp, cl, vl, xd)
+        assert torch.equal(Y.view(torch.int16) if kind != "f32" else Y, xd.view(torch.int16) if kind != "f32" else xd)
+
+
+def test_spmm_no_values_and_empty(cg):
+    g = _graph("dups", seed=8)
+    rp, cl, _ = graph_to_dev(g)
+    xh, xc, xd = features((g.n_cols, 16), 9, "f32")
+    Y = cg.spmm(rp, cl, None, xd)
+    Yr, Ar = oracle.spmm(g.rowptr, g.col, None, xh)
+    assert scaled_error(Y, Yr, Ar) <= TOL_F32
+    e = _graph("empty")
+    rp, cl, vl = graph_to_dev(e)
+    xh, xc, xd = features((7, 5), 1, "f32")
+    for spec in (None, ("auto", 0)):
+        plan = _make_plan(cg, rp, 0, spec, 5)
+        Y = cg.spmm(rp, cl, vl, xd, plan=plan)
+        assert Y.shape == (10, 5) and float(Y.abs().max()) == 0.0
+        if plan is not None:
+            plan.close()
+
+
+def test_spmm_deterministic(cg):
+    import torch
+    g = _graph("hubs", seed=12)
+    rp, cl, vl = graph_to_dev(g)
+    _, _, xd = features((g.n_cols, 128), 2, "f32")
+    plan = cg.Plan(rp, g.nnz, 128, mode="neighbor_group", group_size=16)
+    try:
+        a = cg.spmm(rp, cl, vl, xd, plan=plan)
+        b = cg.spmm(rp, cl, vl, xd, plan=plan)
+        assert torch.equal(a, b)
+    finally:
+        plan.close()
+
+
+# ---------------------------------------------------------------- plan
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1", "empty"])
+@pytest.mark.parametrize("G", [1, 3, 16, 256])
+def test_plan_matches_balancer_definition(cg, kind, G):
+    g = _graph(kind)
+    rp = dev(g.rowptr)
+    want_mode = oracle.balance_mode(g.rowptr, g.nnz)
+    for mode_name, mode in (("auto", want_mode), ("row_split", 1), ("neighbor_group", 2)):
+        plan = cg.Plan(rp, g.nnz, 8, mode=mode_name, group_size=G)
+        try:
+            info = plan.info()
+            assert info["mode"] == mode, (kind, mode_name)
+            units = plan.units().cpu().numpy()
+            groups = oracle.neighbor_groups(g.rowptr, G, mode)
+            assert info["n_units"] == len(groups)
+            # same set of (row, begin, end) slices; partial slots only on split rows
+            got = sorted(map(tuple, units[:, :3].tolist()))
+            assert got == sorted(map(tuple, groups.tolist()))
+            split = units[:, 3] >= 0
+            sizes = units[:, 2] - units[:, 1]
+            d = np.diff(g.rowptr)
+            assert np.all((d[units[:, 0]] > G)[split]) and np.all(~(d[units[:, 0]] > G)[~split] | (mode == 1))
+            if split.any():
+                assert np.array_equal(np.sort(units[split, 3]), np.arange(split.sum()))
+            assert info["n_partials"] == split.sum()
+            if mode == 2:
+                assert np.all(np.diff(sizes) <= 0)       # longest first
+            else:
+                assert np.array_equal(units[:, 0], np.arange(g.n_rows))
+        finally:
+            plan.close()
+
+
+def test_plan_rebuild_no_alloc_path(cg):
+    g = _graph("hubs")
+    rp = dev(g.rowptr)
+    plan = cg.Plan(rp, g.nnz, 64, group_size=32)
+    try:
+        u0 = plan.units().clone()
+        plan.rebuild(rp)
+        import torch
+        assert torch.equal(u0, plan.units())
+    finally:
+        plan.close()
+
+
+# ---------------------------------------------------------------- CSR -> CSC, SpMM^T
+
+@pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1", "empty"])
+def test_csr_to_csc_bit_exact(cg, kind):
+    g = _graph(kind)
+    say(f"csc {kind}")
+    rp, cl, vl = graph_to_dev(g)
+    colptr, row_t, val_t, perm = cg.csr_to_csc(rp, cl, vl, g.n_cols)
+    c_ref, r_ref, v_ref, p_ref = oracle.csr_to_csc(g.rowptr, g.col, g.val, g.n_cols)
+    assert np.array_equal(colptr.cpu().numpy(), c_ref)
+    assert np.array_equal(row_t.cpu().numpy(), r_ref)
+    assert np.array_equal(perm.cpu().numpy(), p_ref)
+    assert np.array_equal(val_t.cpu().numpy().view(np.uint32), v_ref.view(np.uint32))
+
+
+def test_csr_to_csc_many_columns(cg):
+    # column ids needing three radix passes (> 2^16 columns)
+    rng = np.random.default_rng(31)
+    g = synth.random_csr(5000, 300000, rng, mean_deg=30, dup=True, unsorted=True)
+    rp, cl, vl = graph_to_dev(g)
+    colptr, row_t, val_t, perm = cg.csr_to_csc(rp, cl, vl, g.n_cols)
+    c_ref, r_ref, v_ref, p_ref = oracle.csr_to_csc(g.rowptr, g.col, g.val, g.n_cols)
+    assert np.array_equal(colptr.cpu().numpy(), c_ref)
+    assert np.array_equal(perm.cpu().numpy(), p_ref)
+    assert np.array_equal(row_t.cpu().numpy(), r_ref)
+
+
+@pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1"])
+@pytest.mark.parametrize("gk", ["f32", "bf16"])
+def test_spmm_t(cg, kind, gk):
+    g = _graph(kind)
+    say(f"spmm_t {kind} {gk}")
+    rp, cl, vl = graph_to_dev(g)
+    colptr, row_t, val_t, _ = cg.csr_to_csc(rp, cl, vl, g.n_cols)
+    F = 64
+    gh, gc, gd = features((g.n_rows, F), 17, gk)
+    dXr, Ar = oracle.spmm_t(g.rowptr, g.col, g.val, gh, g.n_cols, g_dtype=gc)
+    for spec in (None, ("auto", 0), ("neighbor_group", 8)):
+        plan = _make_plan(cg, colptr, g.nnz, spec, F)
+        try:
+            dX = cg.spmm_t(colptr, row_t, val_t, gd, plan_t=plan)
+            assert dX.shape == (g.n_cols, F)
+            assert scaled_error(dX, dXr, Ar) <= tol_for(gk), (kind, spec)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+# ---------------------------------------------------------------- attention
+
+def _scores(n_rows, n_cols, H, seed, scale=1.0):
+    rng = np.random.default_rng(seed)
+    sd = (rng.standard_normal((n_rows, H)) * scale).astype(np.float32)
+    ss = (rng.standard_normal((n_cols, H)) * scale).astype(np.float32)
+    return sd, ss
+
+
+def _alpha_close(a_gpu, a_ref):
+    a = to_f64(a_gpu).reshape(a_ref.shape)
+    if a_ref.size == 0:
+        return 0.0
+    return float(np.max(np.abs(a - a_ref) / a_ref))
+
+
+@pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1"])
+@pytest.mark.parametrize("H", [1, 3, 4, 8, 64])
+def test_sddmm_edge_softmax(cg, kind, H):
+    g = _graph(kind)
+    say(f"softmax {kind} H={H}")
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 40 + H)
+    a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+    for spec in (None, ("auto", 0), ("neighbor_group", 7)):
+        plan = _make_plan(cg, rp, g.nnz, spec, 1, max_heads=H)
+        try:
+            a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
+            err = _alpha_close(a, a_ref)
+            assert err <= TOL_ALPHA, (kind, H, spec, err)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+def test_softmax_degree_one_rows_exact_and_wide_scores(cg):
+    import torch
+    g = _graph("hubs", seed=5)
+    rp, cl, _ = graph_to_dev(g)
+    H = 4
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 77, scale=8.0)
+    a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2)
+    d = np.diff(g.rowptr)
+    rows = np.repeat(np.arange(g.n_rows), d)
+    a_h = a.cpu().numpy()
+    assert np.all(a_h[d[rows] == 1] == 1.0)
+    sums = np.zeros((g.n_rows, H))
+    np.add.at(sums, rows, a_h.astype(np.float64))
+    assert np.max(np.abs(sums[d > 0] - 1.0)) <= 1e-5
+    a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+    # with wide score ranges the tiny weights carry the exp argument's rounding
+    rel = np.abs(a_h - a_ref) / a_ref
+    assert np.max(rel[a_ref > 1e-6]) <= TOL_ALPHA
+
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
+@pytest.mark.parametrize("H,D,xk,yk", [(8, 16, "f32", "f32"), (4, 64, "bf16", "bf16"), (3, 5, "f32", "f32"),
+                                       (1, 1, "f32", "f32"), (2, 40, "f16", "f32"), (4, 64, "f32", "bf16"),
+                                       (16, 80, "f32", "f32")])
+def test_gat_aggregate(cg, kind, H, D, xk, yk):
+    import torch
+    g = _graph(kind)
+    say(f"gat {kind} H={H} D={D} {xk}->{yk}")
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 50 + H)
+    xh, xc, xd = features((g.n_cols, H, D), 60 + D, xk)
+    out_dtype = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[yk]
+    Yr, Ar = oracle.gat(g.rowptr, g.col, sd, ss, xh.reshape(g.n_cols, H * D), H, D, slope=0.2, x_dtype=xc)
+    a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+    for spec in (None, ("auto", 0), ("neighbor_group", 6)):
+        plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+        try:
+            Y, a = cg.gat_aggregate(rp, cl, dev(sd), dev(ss), xd, 0.2, plan=plan, out_dtype=out_dtype,
+                                    return_alpha=True)
+            err = scaled_error(Y.reshape(g.n_rows, H * D), Yr, Ar)
+            assert err <= tol_for(xk, yk), (kind, H, D, spec, err)
+            assert _alpha_close(a, a_ref) <= TOL_ALPHA, (kind, H, D, spec)
+            Y2 = cg.gat_aggregate(rp, cl, dev(sd), dev(ss), xd, 0.2, plan=plan, out_dtype=out_dtype)
+            assert torch.equal(Y2, Y)                        # alpha_out does not change Y
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+@pytest.mark.parametrize("spec", [None, ("neighbor_group", 9)])
+def test_gat_alpha_in_equals_weighted_spmm(cg, spec):
+    g = _graph("hubs", seed=6)
+    rp, cl, vl = graph_to_dev(g)
+    H, D = 4, 16
+    rng = np.random.default_rng(3)
+    alpha = rng.random((g.nnz, H)).astype(np.float32)
+    xh, xc, xd = features((g.n_cols, H, D), 70, "f32")
+    plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+    try:
+        Y = cg.gat_aggregate(rp, cl, None, None, xd, alpha_in=dev(alpha), plan=plan)
+        Yr, Ar = oracle.gat(g.rowptr, g.col, None, None, xh.reshape(g.n_cols, H * D), H, D, alpha_in=alpha)
+        assert scaled_error(Y.reshape(g.n_rows, H * D), Yr, Ar) <= TOL_F32
+    finally:
+        if plan is not None:
+            plan.close()
+
+
+def test_plan_errors_on_mismatch(cg):
+    g = _graph("small")
+    rp, cl, vl = graph_to_dev(g)
+    _, _, xd = features((g.n_cols, 64), 1, "f32")
+    plan = cg.Plan(rp, g.nnz, max_feat=32)
+    try:
+        with pytest.raises(cg.CogdlError, match="plan"):
+            cg.spmm(rp, cl, vl, xd, plan=plan)          # F = 64 > max_feat
+        sd, ss = _scores(g.n_rows, g.n_cols, 2, 1)
+        with pytest.raises(cg.CogdlError, match="plan"):
+            cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), plan=plan)   # no heads reserved
+    finally:
+        plan.close()
