@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--group-size", type=int, default=0)
     ap.add_argument("--alpha-out", action="store_true", help="also write alpha in the GAT step")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before the steps, copy a buffer of this many MiB (counter calibration)")
     return ap.parse_args()
 
 
@@ -188,6 +190,17 @@ def main():
         cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg,  # a5-a7
                          alpha_out=alpha)
         mark(6)
+
+    if args.calib_copy_mib > 0:
+        # a plain device-to-device copy of known size, for scaling the HBM counters
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calib_copy_mib} MiB done")
+        del src, dst
 
     for i in range(args.warmup):
         step()

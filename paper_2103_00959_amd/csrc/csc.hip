@@ -2,10 +2,11 @@
 // pass of Eq. 1 (the gradient with respect to the node features is A^T G).
 //
 // A stable LSD radix sort of the edge ids keyed by column (8-bit digits, as
-// many passes as the column count needs) gives perm directly; colptr is read
-// off the sorted keys, and row_t / val_t are gathered through perm.  Every
-// step is integer work in a fixed order, so the result is bit-for-bit unique:
-// inside a column the edges keep increasing CSR edge id.
+// many passes as the column count needs) gives perm directly, with each
+// edge's row and value bits carried along as payloads (so nothing is gathered
+// at random afterwards); colptr is read off the sorted keys.  Every step is
+// integer work in a fixed order, so the result is bit-for-bit unique: inside
+// a column the edges keep increasing CSR edge id.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -41,22 +42,8 @@ __global__ __launch_bounds__(kBlock) void k_colptr(const uint32_t *__restrict__ 
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_gather_csc(const uint32_t *__restrict__ perm, int64_t nnz,
-                                                       const uint32_t *__restrict__ row_of,
-                                                       const float *__restrict__ val,
-                                                       int32_t *__restrict__ row_t,
-                                                       float *__restrict__ val_t)
-{
-    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kBlock) {
-        const uint32_t k = perm[p];
-        row_t[p] = (int32_t)row_of[k];
-        if (val_t) val_t[p] = val[k];
-    }
-}
-
 struct CscLayout {
-    size_t row_of, ping_k, ping_v, skeys, vtmp, radix, total;
+    size_t row_of, ping_k, ping_v, ping_r, ping_w, skeys, vtmp, radix, total;
 };
 
 size_t al(size_t b) { return (b + 255) & ~size_t(255); }
@@ -68,6 +55,8 @@ CscLayout csc_layout(int64_t nnz)
     L.row_of = off; off += al(4 * (size_t)nnz);
     L.ping_k = off; off += al(8 * (size_t)nnz);
     L.ping_v = off; off += al(8 * (size_t)nnz);
+    L.ping_r = off; off += al(8 * (size_t)nnz);
+    L.ping_w = off; off += al(8 * (size_t)nnz);
     L.skeys = off;  off += al(4 * (size_t)nnz);
     L.vtmp = off;   off += al(4 * (size_t)nnz);
     L.radix = off;  off += al(radix_workspace_bytes(nnz));
@@ -127,12 +116,18 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
     COGDL_LAUNCH("csc_expand_rows", k_expand_rows, grid_for(n_rows, kBlock / kWave), kBlock, stream,
                  rowptr, n_rows, row_of);
     const int bits = bits_for((uint64_t)(n_cols - 1));
+    RadixPayload rows{row_of, reinterpret_cast<uint32_t *>(row_t),
+                      reinterpret_cast<uint32_t *>(ws + L.ping_r)};
+    RadixPayload vals;
+    if (val) {
+        vals.in = reinterpret_cast<const uint32_t *>(val);
+        vals.out = reinterpret_cast<uint32_t *>(val_t);
+        vals.ping = reinterpret_cast<uint32_t *>(ws + L.ping_w);
+    }
     COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), nullptr, skeys, order,
-                                   nnz, bits, ping_k, ping_v, ws + L.radix, stream));
+                                   nnz, bits, ping_k, ping_v, ws + L.radix, stream, rows, vals));
     COGDL_LAUNCH("csc_colptr", k_colptr, grid_for(nnz, kBlock), kBlock, stream, skeys, nnz, n_cols,
                  colptr);
-    COGDL_LAUNCH("csc_gather", k_gather_csc, grid_for(nnz, kBlock), kBlock, stream, order, nnz,
-                 row_of, val, row_t, val_t);
     return COGDL_OK;
 }
 

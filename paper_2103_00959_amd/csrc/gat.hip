@@ -390,8 +390,11 @@ __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
 }
 
 // GAT split rows: combine the groups' unnormalized sums with the log-sum-exp
-// rule, write Y and the row's (m, z) for the alpha pass.
-template <typename TY>
+// rule, write Y and the row's (m, z) for the alpha pass.  One workgroup per
+// split row; every wavefront merges the (m, z) states (cheap, identical), then
+// wavefront w adds the groups g = w, w + 4, ... scaled by exp(m_g - m), and the
+// four sums are combined in wavefront order through LDS.
+template <typename TY, int VEC>
 __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ split_rows,
                                                        const int32_t *__restrict__ n_split,
                                                        const float *__restrict__ partials,
@@ -401,69 +404,70 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
                                                        float *__restrict__ rstats,
                                                        TY *__restrict__ Y)
 {
+    constexpr int kW = kBlock / kWave;
+    __shared__ float red[kW][kWave * VEC];
     const int lane = lane_id();
-    const int wv = threadIdx.x / kWave;
+    const int w = threadIdx.x / kWave;
     const int64_t W = (int64_t)H * D;
-    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
     const int32_t ns = *n_split;
-    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + wv; s < ns; s += waves) {
+    for (int64_t s = blockIdx.x; s < ns; s += gridDim.x) {
         const int4 d = split_rows[s];
         const int64_t row = d.x;
         const int p0 = d.y, np = d.z;
         float m, z;
-        merge_groups(gstats, sstride, p0, np, H, m, z);
-        if (lane < H) {
+        merge_groups(gstats, sstride, p0, np, H, m, z);   // lane h holds head h
+        if (w == 0 && lane < H) {
             rstats[s * sstride + lane] = m;
             rstats[s * sstride + (sstride >> 1) + lane] = z;
         }
-        // lane h holds the merged state of head h
-        for (int64_t f0 = 0; f0 < W; f0 += kWave) {
-            const int64_t f = f0 + lane;
-            const int h = f < W ? (int)(f / D) : 0;
+        for (int64_t fb = 0; fb < W; fb += kWave * VEC) {
+            const int64_t f = fb + (int64_t)lane * VEC;
+            const bool act = f < W;
+            const int h = act ? (int)(f / D) : 0;
             const float M = lane_bcast(m, h);
             const float rZ = 1.f / lane_bcast(z, h);
-            if (f >= W) continue;
-            float a0 = 0.f, a1 = 0.f;
-            int g = 0;
-            for (; g + 2 <= np; g += 2) {
-                const int64_t q0 = (int64_t)(p0 + g), q1 = q0 + 1;
-                a0 = fmaf(partials[q0 * pstride + f], __expf(gstats[q0 * sstride + h] - M), a0);
-                a1 = fmaf(partials[q1 * pstride + f], __expf(gstats[q1 * sstride + h] - M), a1);
+            float a0[VEC], a1[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) a0[e] = a1[e] = 0.f;
+            if (act) {
+                int g = w;
+                for (; g + kW < np; g += 2 * kW) {
+                    const int64_t q0 = p0 + g, q1 = q0 + kW;
+                    const float s0 = __expf(gstats[q0 * sstride + h] - M);
+                    const float s1 = __expf(gstats[q1 * sstride + h] - M);
+                    float x0[VEC], x1[VEC];
+                    load_vec<float, VEC>(partials, q0 * pstride + f, x0);
+                    load_vec<float, VEC>(partials, q1 * pstride + f, x1);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        a0[e] = fmaf(x0[e], s0, a0[e]);
+                        a1[e] = fmaf(x1[e], s1, a1[e]);
+                    }
+                }
+                if (g < np) {
+                    const int64_t q0 = p0 + g;
+                    const float s0 = __expf(gstats[q0 * sstride + h] - M);
+                    float x0[VEC];
+                    load_vec<float, VEC>(partials, q0 * pstride + f, x0);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) a0[e] = fmaf(x0[e], s0, a0[e]);
+                }
             }
-            if (g < np) {
-                const int64_t q0 = (int64_t)(p0 + g);
-                a0 = fmaf(partials[q0 * pstride + f], __expf(gstats[q0 * sstride + h] - M), a0);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) red[w][lane * VEC + e] = a0[e] + a1[e];
+            __syncthreads();
+            if (w == 0 && act) {
+                float v[VEC];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    float t = red[0][lane * VEC + e];
+#pragma unroll
+                    for (int i = 1; i < kW; ++i) t += red[i][lane * VEC + e];
+                    v[e] = t * rZ;
+                }
+                store_out<TY, VEC>(Y, row * W + f, v);
             }
-            const float v[1] = {(a0 + a1) * rZ};
-            store_vec<TY, 1>(Y, row * W + f, v);
-        }
-    }
-}
-
-// Plain weighted sums of split rows (alpha_in given): Y = sum of partials.
-template <typename TY>
-__global__ __launch_bounds__(kBlock) void k_sum_reduce(const int4 *__restrict__ split_rows,
-                                                       const int32_t *__restrict__ n_split,
-                                                       const float *__restrict__ partials,
-                                                       int64_t pstride, int64_t W,
-                                                       TY *__restrict__ Y)
-{
-    const int lane = lane_id();
-    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
-    const int32_t ns = *n_split;
-    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns; s += waves) {
-        const int4 d = split_rows[s];
-        for (int64_t f = lane; f < W; f += kWave) {
-            float a0 = 0.f, a1 = 0.f;
-            const float *p = partials + (int64_t)d.y * pstride + f;
-            int g = 0;
-            for (; g + 2 <= d.z; g += 2) {
-                a0 += p[(int64_t)g * pstride];
-                a1 += p[(int64_t)(g + 1) * pstride];
-            }
-            if (g < d.z) a0 += p[(int64_t)g * pstride];
-            const float v[1] = {a0 + a1};
-            store_vec<TY, 1>(Y, (int64_t)d.x * W + f, v);
+            __syncthreads();
         }
     }
 }
@@ -626,31 +630,22 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     COGDL_LAUNCH("gat", k, grid, kBlock, stream, a);
     if (!P) return COGDL_OK;
 
-    const unsigned rb = grid_waves(P->cap_split);
-    if (!soft) {
-        if (y_dtype == COGDL_F32)
-            COGDL_LAUNCH("gat_sum_reduce", k_sum_reduce<float>, rb, kBlock, stream, P->split_rows,
-                         P->n_split_dev(), P->partials, a.pstride, W, static_cast<float *>(Y));
-        else if (y_dtype == COGDL_BF16)
-            COGDL_LAUNCH("gat_sum_reduce", k_sum_reduce<bf16_t>, rb, kBlock, stream, P->split_rows,
-                         P->n_split_dev(), P->partials, a.pstride, W, static_cast<bf16_t *>(Y));
-        else
-            COGDL_LAUNCH("gat_sum_reduce", k_sum_reduce<f16_t>, rb, kBlock, stream, P->split_rows,
-                         P->n_split_dev(), P->partials, a.pstride, W, static_cast<f16_t *>(Y));
-        return COGDL_OK;
+    if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, stream);
+    const int64_t rblocks = P->cap_split < 4096 ? P->cap_split : 4096;
+    const unsigned rb = (unsigned)(rblocks < 1 ? 1 : rblocks);
+    const bool v4 = D % 4 == 0 && (uintptr_t)Y % (4 * dtype_bytes(y_dtype)) == 0;
+#define COGDL_GAT_REDUCE(TY, V)                                                                  \
+    COGDL_LAUNCH("gat_reduce", (k_gat_reduce<TY, V>), rb, kBlock, stream, P->split_rows,         \
+                 P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats, \
+                 static_cast<TY *>(Y))
+    if (y_dtype == COGDL_F32) {
+        if (v4) COGDL_GAT_REDUCE(float, 4); else COGDL_GAT_REDUCE(float, 1);
+    } else if (y_dtype == COGDL_BF16) {
+        if (v4) COGDL_GAT_REDUCE(bf16_t, 4); else COGDL_GAT_REDUCE(bf16_t, 1);
+    } else {
+        if (v4) COGDL_GAT_REDUCE(f16_t, 4); else COGDL_GAT_REDUCE(f16_t, 1);
     }
-    if (y_dtype == COGDL_F32)
-        COGDL_LAUNCH("gat_reduce", k_gat_reduce<float>, rb, kBlock, stream, P->split_rows,
-                     P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats,
-                     static_cast<float *>(Y));
-    else if (y_dtype == COGDL_BF16)
-        COGDL_LAUNCH("gat_reduce", k_gat_reduce<bf16_t>, rb, kBlock, stream, P->split_rows,
-                     P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats,
-                     static_cast<bf16_t *>(Y));
-    else
-        COGDL_LAUNCH("gat_reduce", k_gat_reduce<f16_t>, rb, kBlock, stream, P->split_rows,
-                     P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats,
-                     static_cast<f16_t *>(Y));
+#undef COGDL_GAT_REDUCE
     if (alpha_out) {
         SoftArgs sa{};
         sa.col = col;

@@ -56,6 +56,10 @@ struct Plan {
 
 const Plan *plan_of(const cogdl_plan *h);
 
+// Y[row] = sum of the partial rows of every split row of the plan (F columns).
+cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
+                               hipStream_t s);
+
 // Kernel tracing hooks (no-ops unless cogdl_trace_enable was called).
 int trace_begin(const char *name, hipStream_t s);
 void trace_end(int slot, hipStream_t s);
@@ -68,14 +72,24 @@ void trace_end(int slot, hipStream_t s);
 size_t scan_workspace_bytes(int64_t n);
 hipError_t exclusive_scan(const int32_t *in, int32_t *out, int64_t n, void *ws, hipStream_t s);
 
+// An extra 32-bit array carried through a radix sort: read from `in`,
+// written in sorted order to `out`; `ping` is 2 * n elements of scratch.
+struct RadixPayload {
+    const uint32_t *in = nullptr;
+    uint32_t *out = nullptr;
+    uint32_t *ping = nullptr;
+};
+
 // Stable LSD radix sort of (key, value) pairs on the low `bits` bits of the
 // keys.  vals_in == nullptr means values 0..n-1.  Results land in keys_out /
-// vals_out (keys_out may be nullptr when the sorted keys are not needed).
-// ping: 2 * n keys and 2 * n values of scratch.
+// vals_out (keys_out may be nullptr when the sorted keys are not needed); up
+// to two payload arrays move with the keys.  ping: 2 * n keys and 2 * n
+// values of scratch.
 size_t radix_workspace_bytes(int64_t n);
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
                             uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
-                            uint32_t *ping_vals, void *ws, hipStream_t s);
+                            uint32_t *ping_vals, void *ws, hipStream_t s,
+                            RadixPayload pay0 = RadixPayload(), RadixPayload pay1 = RadixPayload());
 
 // Fill n int32 with a value (a kernel, so it is safe inside graph capture).
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);

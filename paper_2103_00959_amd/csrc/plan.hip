@@ -22,17 +22,26 @@ struct cogdl_plan {
 namespace cogdl {
 namespace {
 
-__global__ void k_plan_close(const int32_t *__restrict__ rowptr, int32_t n_rows, int64_t nnz,
-                             int32_t *__restrict__ counters)
+// Rows whose degree is close to the average; one atomic per workgroup (a
+// grid-stride loop over a bounded grid keeps same-address atomics few).
+__global__ __launch_bounds__(256) void k_plan_close(const int32_t *__restrict__ rowptr, int32_t n_rows,
+                                                    int64_t nnz, int32_t *__restrict__ counters)
 {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    __shared__ int wsum[4];
     int close = 0;
-    if (i < n_rows) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_rows;
+         i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t d = (int64_t)rowptr[i + 1] - rowptr[i];
-        close = (2 * d * n_rows >= nnz && d * n_rows <= 2 * nnz) ? 1 : 0;
+        close += (2 * d * n_rows >= nnz && d * n_rows <= 2 * nnz) ? 1 : 0;
     }
-    const uint64_t b = __ballot(close);
-    if (lane_id() == 0 && b) atomicAdd(&counters[0], (int)__popcll(b));
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) close += __shfl_xor(close, off);
+    if (lane_id() == 0) wsum[threadIdx.x / kWave] = close;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int t = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+        if (t) atomicAdd(&counters[0], t);
+    }
 }
 
 __device__ __forceinline__ int plan_mode(const int32_t *counters, int32_t n_rows, int req)
@@ -125,7 +134,8 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, hipStream_t s)
         return COGDL_OK;
     }
     const unsigned blocks = (unsigned)((n + 255) / 256);
-    COGDL_LAUNCH("plan_close", k_plan_close, blocks, 256, s, rowptr, n, P.nnz, P.counters);
+    COGDL_LAUNCH("plan_close", k_plan_close, blocks < 512 ? blocks : 512, 256, s, rowptr, n, P.nnz,
+                 P.counters);
     COGDL_LAUNCH("plan_counts", k_plan_counts, blocks, 256, s, rowptr, n, P.group_size,
                  (int)P.mode_req, P.counters, P.row_units, P.row_parts, P.row_split);
     COGDL_HIP_TRY(exclusive_scan(P.row_units, P.row_units, n, P.scan_ws, s));

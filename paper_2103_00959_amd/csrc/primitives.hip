@@ -117,11 +117,13 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__res
 // [w * 1024, (w + 1) * 1024) of the tile and walks it 64 keys at a time; the
 // rank of a key among equal digits is the number of lower lanes with the same
 // digit (found with eight ballots) plus the running per-wave count, and the
-// waves are then stacked in order per digit.
+// waves are then stacked in order per digit.  NP extra 32-bit payloads travel
+// with each key.
+template <int NP>
 __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint32_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, int64_t n, int shift,
-    int n_tiles, const int32_t *__restrict__ offsets)
+    int n_tiles, const int32_t *__restrict__ offsets, RadixPayload p0, RadixPayload p1)
 {
     constexpr int kWaves = kSortBlock / kWave;
     __shared__ int32_t wcnt[kWaves][kDigits];
@@ -132,8 +134,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 
     const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)w * kWave * kSortItems;
     const uint64_t lower = __lanemask_lt();
-    uint32_t key[kSortItems], val[kSortItems];
-    int local[kSortItems], dig[kSortItems];
+    uint32_t key[kSortItems], val[kSortItems], pa[NP > 0 ? kSortItems : 1], pb[NP > 1 ? kSortItems : 1];
+    int local[kSortItems];
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const int64_t e = base + i * kWave + lane;
@@ -141,6 +143,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         const uint32_t k = valid ? keys_in[e] : 0u;
         key[i] = k;
         val[i] = valid ? (vals_in ? vals_in[e] : (uint32_t)e) : 0u;
+        if constexpr (NP > 0) pa[i] = valid ? p0.in[e] : 0u;
+        if constexpr (NP > 1) pb[i] = valid ? p1.in[e] : 0u;
         const int d = (int)((k >> shift) & (kDigits - 1));
         uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -152,9 +156,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         const int rank = __popcll(peers & lower);
         int old = 0;
         if (valid) old = wcnt[w][d];
-        local[i] = old + rank;
+        local[i] = valid ? old + rank : -1;
         if (valid && rank == 0) wcnt[w][d] = old + __popcll(peers);
-        dig[i] = valid ? d : -1;
     }
     __syncthreads();
     {
@@ -169,10 +172,13 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
-        if (dig[i] >= 0) {
-            const int pos = wcnt[w][dig[i]] + local[i];
+        if (local[i] >= 0) {
+            const int d = (int)((key[i] >> shift) & (kDigits - 1));
+            const int pos = wcnt[w][d] + local[i];
             if (keys_out) keys_out[pos] = key[i];
             vals_out[pos] = val[i];
+            if constexpr (NP > 0) p0.out[pos] = pa[i];
+            if constexpr (NP > 1) p1.out[pos] = pb[i];
         }
     }
 }
@@ -236,9 +242,11 @@ size_t radix_workspace_bytes(int64_t n)
 
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
                             uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
-                            uint32_t *ping_vals, void *ws, hipStream_t s)
+                            uint32_t *ping_vals, void *ws, hipStream_t s, RadixPayload pay0,
+                            RadixPayload pay1)
 {
     if (n <= 0) return hipSuccess;
+    const int np = pay0.in ? (pay1.in ? 2 : 1) : 0;
     const int64_t tiles = (n + kSortTile - 1) / kSortTile;
     const int64_t hist_n = (int64_t)kDigits * tiles;
     int32_t *hist = static_cast<int32_t *>(ws);
@@ -249,18 +257,30 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
     if (passes < 1) passes = 1;
     const uint32_t *src_k = keys_in;
     const uint32_t *src_v = vals_in;
+    RadixPayload a = pay0, b = pay1;
     for (int p = 0; p < passes; ++p) {
         const bool last = (p == passes - 1);
         uint32_t *dst_k = last ? keys_out : ping_keys + (p & 1) * n;
         uint32_t *dst_v = last ? vals_out : ping_vals + (p & 1) * n;
+        RadixPayload pa{a.in, last ? pay0.out : (pay0.ping ? pay0.ping + (p & 1) * n : nullptr), nullptr};
+        RadixPayload pb{b.in, last ? pay1.out : (pay1.ping ? pay1.ping + (p & 1) * n : nullptr), nullptr};
         COGDL_LAUNCH_HIP("radix_hist", k_radix_hist, (unsigned)tiles, kSortBlock, s, src_k, n, 8 * p,
                          (int)tiles, hist);
         hipError_t e = exclusive_scan(hist, hist, hist_n, scan_ws, s);
         if (e != hipSuccess) return e;
-        COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter, (unsigned)tiles, kSortBlock, s, src_k,
-                         src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist);
+        if (np == 0)
+            COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<0>, (unsigned)tiles, kSortBlock, s,
+                             src_k, src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist, pa, pb);
+        else if (np == 1)
+            COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<1>, (unsigned)tiles, kSortBlock, s,
+                             src_k, src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist, pa, pb);
+        else
+            COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<2>, (unsigned)tiles, kSortBlock, s,
+                             src_k, src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist, pa, pb);
         src_k = dst_k;
         src_v = dst_v;
+        a.in = pa.out;
+        b.in = pb.out;
     }
     return hipSuccess;
 }

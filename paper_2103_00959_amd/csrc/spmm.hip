@@ -154,35 +154,63 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
     }
 }
 
-// Y[row, :] = sum of the row's partial rows, in slot order.  One wavefront per
-// split row (grid-stride over the device-side count); four interleaved chains
-// keep the fp32 summation short for rows with many groups.
-template <typename TY>
+// Y[row, :] = sum of the row's partial rows.  One workgroup per split row
+// (grid-stride over the device-side count, uniform per workgroup): wavefront
+// w adds the slots g = w, w + 4, ... in increasing order on two interleaved
+// chains, VEC features per lane, and the four wavefront sums are added in
+// wavefront order through LDS, so the result does not depend on timing.
+template <typename TY, int VEC>
 __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__ split_rows,
                                                         const int32_t *__restrict__ n_split,
                                                         const float *__restrict__ partials,
                                                         int64_t pstride, int64_t F, TY *__restrict__ Y)
 {
+    constexpr int kW = kBlock / kWave;
+    __shared__ float red[kW][kWave * VEC];
     const int lane = lane_id();
-    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int w = threadIdx.x / kWave;
     const int32_t ns = *n_split;
-    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns; s += waves) {
+    for (int64_t s = blockIdx.x; s < ns; s += gridDim.x) {
         const int4 d = split_rows[s];
         const int64_t row = d.x, p0 = d.y;
         const int np = d.z;
-        for (int64_t f = lane; f < F; f += kWave) {
-            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-            const float *p = partials + p0 * pstride + f;
-            int g = 0;
-            for (; g + 4 <= np; g += 4) {
-                a0 += p[(int64_t)g * pstride];
-                a1 += p[(int64_t)(g + 1) * pstride];
-                a2 += p[(int64_t)(g + 2) * pstride];
-                a3 += p[(int64_t)(g + 3) * pstride];
+        for (int64_t fb = 0; fb < F; fb += kWave * VEC) {
+            const int64_t f = fb + (int64_t)lane * VEC;
+            const bool act = f < F;
+            float a0[VEC], a1[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) a0[e] = a1[e] = 0.f;
+            if (act) {
+                const float *p = partials + p0 * pstride + f;
+                int g = w;
+                for (; g + kW < np; g += 2 * kW) {
+                    float x0[VEC], x1[VEC];
+                    load_vec<float, VEC>(p, (int64_t)g * pstride, x0);
+                    load_vec<float, VEC>(p, (int64_t)(g + kW) * pstride, x1);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) { a0[e] += x0[e]; a1[e] += x1[e]; }
+                }
+                if (g < np) {
+                    float x0[VEC];
+                    load_vec<float, VEC>(p, (int64_t)g * pstride, x0);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) a0[e] += x0[e];
+                }
             }
-            for (; g < np; ++g) a0 += p[(int64_t)g * pstride];
-            const float v[1] = {(a0 + a1) + (a2 + a3)};
-            store_vec<TY, 1>(Y, row * F + f, v);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) red[w][lane * VEC + e] = a0[e] + a1[e];
+            __syncthreads();
+            if (w == 0 && act) {
+                float v[VEC];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    v[e] = red[0][lane * VEC + e];
+#pragma unroll
+                    for (int i = 1; i < kW; ++i) v[e] += red[i][lane * VEC + e];
+                }
+                store_out<TY, VEC>(Y, row * F + f, v);
+            }
+            __syncthreads();
         }
     }
 }
@@ -218,25 +246,41 @@ SpmmKernel pick(int xdt, int ydt, int vec, int ch)
     return pick_y<f16_t>(ydt, vec, ch);
 }
 
-cogdl_status reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                           hipStream_t s)
+template <int VEC>
+cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
+                             hipStream_t s)
 {
     const int64_t pstride = (P.max_feat + 7) / 8 * 8;
-    int64_t blocks = (P.cap_split + (kBlock / kWave) - 1) / (kBlock / kWave);
-    if (blocks > 2048) blocks = 2048;
+    int64_t blocks = P.cap_split;
+    if (blocks > 4096) blocks = 4096;
     if (blocks < 1) blocks = 1;
     const unsigned b = (unsigned)blocks;
     if (ydt == COGDL_F32)
-        COGDL_LAUNCH(name, k_spmm_reduce<float>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+        COGDL_LAUNCH(name, (k_spmm_reduce<float, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
                      P.partials, pstride, F, static_cast<float *>(Y));
     else if (ydt == COGDL_BF16)
-        COGDL_LAUNCH(name, k_spmm_reduce<bf16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+        COGDL_LAUNCH(name, (k_spmm_reduce<bf16_t, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
                      P.partials, pstride, F, static_cast<bf16_t *>(Y));
     else
-        COGDL_LAUNCH(name, k_spmm_reduce<f16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+        COGDL_LAUNCH(name, (k_spmm_reduce<f16_t, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
                      P.partials, pstride, F, static_cast<f16_t *>(Y));
     return COGDL_OK;
 }
+
+}  // namespace
+
+// Four features per lane when the rows allow 16-byte partial loads and
+// aligned output stores, one otherwise.
+cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
+                               hipStream_t s)
+{
+    const int ybytes = dtype_bytes(ydt);
+    if (F % 4 == 0 && (uintptr_t)Y % (4 * ybytes) == 0)
+        return reduce_launch_v<4>(name, P, F, Y, ydt, s);
+    return reduce_launch_v<1>(name, P, F, Y, ydt, s);
+}
+
+namespace {
 
 // Shared body of cogdl_spmm and cogdl_spmm_t: out_rows x F output, gathering
 // rows of an in_rows x F input through (ptr, idx, w).
@@ -277,7 +321,7 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
     SpmmKernel k = pick(xdt, ydt, m.vec, m.ch);
     COGDL_LAUNCH(name, k, grid, kBlock, s, a);
-    if (P) return reduce_launch(reduce_name, *P, F, Y, ydt, s);
+    if (P) return sum_reduce_launch(reduce_name, *P, F, Y, ydt, s);
     return COGDL_OK;
 }
 

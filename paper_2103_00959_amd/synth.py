@@ -39,6 +39,7 @@ from __future__ import annotations
 
 import dataclasses
 import os
+import sys
 import time
 
 import numpy as np
@@ -328,7 +329,7 @@ def config_graph(k: int, cache: bool = True, verbose: bool = False) -> Graph:
     g = _build_graph(k)
     if verbose:
         print(f"[synth] built {cfg['name']}: n={g.n_rows} nnz={g.nnz} in {time.time() - t0:.1f}s",
-              flush=True)
+              flush=True, file=sys.stderr)
     if cache:
         os.makedirs(d, exist_ok=True)
         for f in names:

@@ -51,9 +51,27 @@ def to_f64(t):
     return t.detach().to(torch.float64).cpu().numpy()
 
 
+# significand bits and minimum normal exponent of the output formats
+_FORMATS = {"float32": (24, -126), "bfloat16": (8, -126), "float16": (11, -14)}
+
+
+def half_quantum(y_ref, torch_dtype):
+    """Half the spacing of the output format at |y_ref|: the rounding of the
+    stored result itself, which dominates near the subnormal range of fp16."""
+    p, emin = _FORMATS[str(torch_dtype).replace("torch.", "")]
+    e = np.floor(np.log2(np.maximum(np.abs(y_ref), 2.0 ** (emin - p))))
+    e = np.maximum(e, emin)
+    return 0.5 * np.exp2(e - (p - 1))
+
+
 def scaled_error(y_gpu, y_ref, abs_ref):
+    """max |Y_gpu - Y_ref| / Abs, after allowing the output format's own rounding
+    (half a unit in the last place of the stored value)."""
     y = to_f64(y_gpu).reshape(y_ref.shape)
-    err = np.abs(y - y_ref) / np.maximum(abs_ref, 1e-30)
+    diff = np.abs(y - y_ref)
+    if y_gpu.dtype != __import__("torch").float32:
+        diff = np.maximum(diff - half_quantum(y_ref, y_gpu.dtype), 0.0)
+    err = diff / np.maximum(abs_ref, 1e-30)
     return float(err.max()) if err.size else 0.0
 
 
