@@ -171,16 +171,86 @@ __device__ __forceinline__ void store_out(T *__restrict__ p, int64_t i, const fl
 {
     store_vec<T, VEC>(p, i, v);
 }
-template <>
-__device__ __forceinline__ void store_out<float, 8>(float *__restrict__ p, int64_t i, const float (&v)[8])
-{
-    store_vec<float, 8>(p, i, v);
-}
-template <>
-__device__ __forceinline__ void store_out<bf16_t, 4>(bf16_t *__restrict__ p, int64_t i, const float (&v)[4])
-{
-    store_vec<bf16_t, 4>(p, i, v);
-}
+
+// ------------------------------------------------------------ row gathers
+
+// Raw buffer descriptor word 3 for gfx9-family (CDNA) buffers: 32-bit data,
+// no swizzle, raw (stride 0) addressing.
+constexpr int kBufferWord3 = 0x00020000;
+// Largest buffer the 32-bit offsets of the buffer gathers address.
+constexpr uint64_t kBufferMaxBytes = 0xffffff00ull;
+
+template <typename T, int VEC> struct VecBytes { static constexpr int value = (int)sizeof(T) * VEC; };
+
+// Gathers VEC consecutive feature elements of one row of X.
+//   BUF = true : raw buffer loads with 32-bit byte offsets (X smaller than
+//                4 GiB); a masked lane passes an offset past the end of the
+//                buffer and reads zeros without touching memory, so no branch.
+//   BUF = false: 64-bit addresses; a masked lane reads element 0 and discards.
+template <typename TX, int VEC, bool BUF>
+struct RowGather {
+    __amdgpu_buffer_rsrc_t rsrc;
+    const TX *base;
+    uint32_t oob;
+
+    __device__ __forceinline__ RowGather(const void *x, uint64_t bytes)
+    {
+        base = static_cast<const TX *>(x);
+        oob = (uint32_t)(bytes > 0xffffffffull ? 0xffffffffull : bytes);
+        if constexpr (BUF)
+            rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(x), (short)0, (int)oob,
+                                                     kBufferWord3);
+    }
+
+    // Elements [idx, idx + VEC) widened to fp32; zeros when !ok.
+    __device__ __forceinline__ void load(int64_t idx, bool ok, float (&o)[VEC]) const
+    {
+        if constexpr (BUF) {
+            const uint32_t off = ok ? (uint32_t)idx * (uint32_t)sizeof(TX) : oob;
+            if constexpr (VecBytes<TX, VEC>::value == 16) {
+                const auto w = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)off, 0, 0);
+                unpack16(w[0], w[1], w[2], w[3], o);
+            } else if constexpr (sizeof(TX) == 4) {
+                o[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)off, 0, 0));
+            } else {
+                const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(rsrc, (int)off, 0, 0);
+                o[0] = widen1(h);
+            }
+        } else {
+            const int64_t i = ok ? idx : 0;
+            load_vec<TX, VEC>(base, i, o);
+            if (!ok) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) o[e] = 0.f;
+            }
+        }
+    }
+
+  private:
+    __device__ __forceinline__ static float widen1(uint32_t h)
+    {
+        if constexpr (Fmt<TX>::code == COGDL_BF16) return __uint_as_float(h << 16);
+        else return f16_bits_to_f32(h & 0xffffu);
+    }
+    __device__ __forceinline__ static void unpack16(uint32_t a, uint32_t b, uint32_t c, uint32_t d,
+                                                    float (&o)[VEC])
+    {
+        const uint32_t w[4] = {a, b, c, d};
+        if constexpr (sizeof(TX) == 4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) o[j] = __uint_as_float(w[j]);
+        } else if constexpr (Fmt<TX>::code == COGDL_BF16) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) { o[2 * j] = bf16_lo(w[j]); o[2 * j + 1] = bf16_hi(w[j]); }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                o[2 * j] = f16_bits_to_f32(w[j] & 0xffffu);
+                o[2 * j + 1] = f16_bits_to_f32(w[j] >> 16);
+            }
+        }
+    }
+};
 
 // ------------------------------------------------------------ lane exchange
 

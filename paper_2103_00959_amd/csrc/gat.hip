@@ -38,6 +38,7 @@ struct GatArgs {
     float slope;
     const float *alpha_in;      // weights given: skip the attention steps
     const void *X;
+    uint64_t x_bytes;           // size of X, bounds the buffer gathers
     void *Y;
     float *alpha_out;
     float *partials;
@@ -48,7 +49,7 @@ struct GatArgs {
     int32_t log2S;
 };
 
-template <typename TX, typename TY, int VEC, int CH>
+template <typename TX, typename TY, int VEC, int CH, bool BUF>
 __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
 {
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
@@ -93,72 +94,80 @@ __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
         for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
     }
 
-    const TX *__restrict__ X = static_cast<const TX *>(a.X);
+    const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const int32_t *__restrict__ col = a.col;
+    const float *__restrict__ wsrc = soft ? a.s_src : a.alpha_in;
 
-    int c_cur = 0;
-    if (beg + lig < end) c_cur = col[beg + lig];
-    for (int k0 = beg; k0 < end; k0 += S) {
-        const int n = (end - k0 < S) ? end - k0 : S;
-        int c_nxt = 0;
-        if (k0 + S + lig < end) c_nxt = col[k0 + S + lig];
-        for (int j = 0; j < n; j += U) {
-            int cc[U];
-            bool ok[U];
+    if (end > beg) {
+        // Branch-free batches: index loads are clamped to the unit's last edge,
+        // masked gathers read zeros, masked weights are -inf (softmax) or 0.
+        const int last = end - 1;
+        int k = beg + lig < last ? beg + lig : last;
+        int c_cur = col[k];
+        for (int k0 = beg; k0 < end; k0 += S) {
+            const int n = (end - k0 < S) ? end - k0 : S;
+            k = k0 + S + lig < last ? k0 + S + lig : last;
+            const int c_nxt = col[k];
+            for (int j = 0; j < n; j += U) {
+                int cc[U];
+                bool ok[U];
 #pragma unroll
-            for (int t = 0; t < U; ++t) {
-                ok[t] = j + t < n;
-                cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
-            }
-            float w[U][CH];
-            float xv[U][CH][VEC];
-#pragma unroll
-            for (int t = 0; t < U; ++t)
-#pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    if (ok[t] && act[c]) {
-                        w[t][c] = soft ? a.s_src[(int64_t)cc[t] * H + hd[c]]
-                                       : a.alpha_in[(int64_t)(k0 + j + t) * H + hd[c]];
-                        load_vec<TX, VEC>(X, (int64_t)cc[t] * a.W + fe[c], xv[t][c]);
-                    } else {
-                        w[t][c] = soft ? -INFINITY : 0.f;
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) xv[t][c][e] = 0.f;
-                    }
+                for (int t = 0; t < U; ++t) {
+                    ok[t] = j + t < n;
+                    cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
                 }
-            if (soft) {
+                float w[U][CH];
+                float xv[U][CH][VEC];
 #pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    float mb = m[c];
+                for (int t = 0; t < U; ++t)
 #pragma unroll
-                    for (int t = 0; t < U; ++t) {
-                        if (w[t][c] != -INFINITY) w[t][c] = leaky_relu(sd[c] + w[t][c], a.slope);
-                        mb = fmaxf(mb, w[t][c]);
+                    for (int c = 0; c < CH; ++c) {
+                        const bool on = ok[t] && act[c];
+                        const int64_t wi = soft ? (int64_t)cc[t] * H + hd[c]
+                                                : (int64_t)(k0 + j + t) * H + hd[c];
+                        w[t][c] = wsrc[on ? wi : 0];
+                        X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
                     }
-                    if (mb > m[c]) {
-                        const float r = __expf(m[c] - mb);
-                        z[c] *= r;
+                if (soft) {
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
-                        m[c] = mb;
-                    }
-                    float zb = 0.f;
+                    for (int c = 0; c < CH; ++c) {
+                        float mb = m[c];
 #pragma unroll
-                    for (int t = 0; t < U; ++t) {
-                        w[t][c] = (w[t][c] == -INFINITY) ? 0.f : __expf(w[t][c] - m[c]);
-                        zb += w[t][c];
+                        for (int t = 0; t < U; ++t) {
+                            w[t][c] = (ok[t] && act[c]) ? leaky_relu(sd[c] + w[t][c], a.slope) : -INFINITY;
+                            mb = fmaxf(mb, w[t][c]);
+                        }
+                        if (mb > m[c]) {
+                            const float r = __expf(m[c] - mb);
+                            z[c] *= r;
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
+                            m[c] = mb;
+                        }
+                        float zb = 0.f;
+#pragma unroll
+                        for (int t = 0; t < U; ++t) {
+                            w[t][c] = (w[t][c] == -INFINITY) ? 0.f : __expf(w[t][c] - m[c]);
+                            zb += w[t][c];
+                        }
+                        z[c] += zb;
                     }
-                    z[c] += zb;
+                } else {
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+#pragma unroll
+                        for (int c = 0; c < CH; ++c)
+                            if (!(ok[t] && act[c])) w[t][c] = 0.f;
                 }
+#pragma unroll
+                for (int t = 0; t < U; ++t)
+#pragma unroll
+                    for (int c = 0; c < CH; ++c)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xv[t][c][e], acc[c][e]);
             }
-#pragma unroll
-            for (int t = 0; t < U; ++t)
-#pragma unroll
-                for (int c = 0; c < CH; ++c)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xv[t][c][e], acc[c][e]);
+            c_cur = c_nxt;
         }
-        c_cur = c_nxt;
     }
 
     if (part >= 0) {
@@ -474,33 +483,39 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
 
 using GatKernel = void (*)(GatArgs);
 
-template <typename TX, typename TY>
+template <typename TX, typename TY, bool BUF>
 GatKernel pick_gat_kernel(int vec, int ch)
 {
     constexpr int V = (int)(16 / sizeof(TX));
     if (vec == 1) {
-        if (ch == 1) return k_gat<TX, TY, 1, 1>;
-        if (ch == 2) return k_gat<TX, TY, 1, 2>;
-        return k_gat<TX, TY, 1, 4>;
+        if (ch == 1) return k_gat<TX, TY, 1, 1, BUF>;
+        if (ch == 2) return k_gat<TX, TY, 1, 2, BUF>;
+        return k_gat<TX, TY, 1, 4, BUF>;
     }
-    if (ch == 1) return k_gat<TX, TY, V, 1>;
-    if (ch == 2) return k_gat<TX, TY, V, 2>;
-    return k_gat<TX, TY, V, 4>;
+    if (ch == 1) return k_gat<TX, TY, V, 1, BUF>;
+    if (ch == 2) return k_gat<TX, TY, V, 2, BUF>;
+    return k_gat<TX, TY, V, 4, BUF>;
 }
 
-template <typename TX>
+template <typename TX, bool BUF>
 GatKernel pick_gat_y(int ydt, int vec, int ch)
 {
-    if (ydt == COGDL_F32) return pick_gat_kernel<TX, float>(vec, ch);
-    if (ydt == COGDL_BF16) return pick_gat_kernel<TX, bf16_t>(vec, ch);
-    return pick_gat_kernel<TX, f16_t>(vec, ch);
+    if (ydt == COGDL_F32) return pick_gat_kernel<TX, float, BUF>(vec, ch);
+    if (ydt == COGDL_BF16) return pick_gat_kernel<TX, bf16_t, BUF>(vec, ch);
+    return pick_gat_kernel<TX, f16_t, BUF>(vec, ch);
 }
 
-GatKernel pick_gat(int xdt, int ydt, int vec, int ch)
+template <bool BUF>
+GatKernel pick_gat_x(int xdt, int ydt, int vec, int ch)
 {
-    if (xdt == COGDL_F32) return pick_gat_y<float>(ydt, vec, ch);
-    if (xdt == COGDL_BF16) return pick_gat_y<bf16_t>(ydt, vec, ch);
-    return pick_gat_y<f16_t>(ydt, vec, ch);
+    if (xdt == COGDL_F32) return pick_gat_y<float, BUF>(ydt, vec, ch);
+    if (xdt == COGDL_BF16) return pick_gat_y<bf16_t, BUF>(ydt, vec, ch);
+    return pick_gat_y<f16_t, BUF>(ydt, vec, ch);
+}
+
+GatKernel pick_gat(int xdt, int ydt, int vec, int ch, bool buf)
+{
+    return buf ? pick_gat_x<true>(xdt, ydt, vec, ch) : pick_gat_x<false>(xdt, ydt, vec, ch);
 }
 
 unsigned grid_waves(int64_t work)
@@ -615,6 +630,7 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     a.slope = negative_slope;
     a.alpha_in = alpha_in;
     a.X = X;
+    a.x_bytes = (uint64_t)n_cols * (uint64_t)W * (uint64_t)dtype_bytes(x_dtype);
     a.Y = Y;
     a.alpha_out = soft ? alpha_out : nullptr;
     a.partials = P ? P->partials : nullptr;
@@ -626,7 +642,7 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     const int64_t units = P ? P->cap_units : n_rows;
     const int64_t upb = kBlock >> m.log2S;
     const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
-    GatKernel k = pick_gat(x_dtype, y_dtype, m.vec, m.ch);
+    GatKernel k = pick_gat(x_dtype, y_dtype, m.vec, m.ch, a.x_bytes <= kBufferMaxBytes);
     COGDL_LAUNCH("gat", k, grid, kBlock, stream, a);
     if (!P) return COGDL_OK;
 

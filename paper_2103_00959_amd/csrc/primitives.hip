@@ -116,9 +116,10 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__res
 // Stable scatter of one tile.  Wavefront w owns the contiguous quarter
 // [w * 1024, (w + 1) * 1024) of the tile and walks it 64 keys at a time; the
 // rank of a key among equal digits is the number of lower lanes with the same
-// digit (found with eight ballots) plus the running per-wave count, and the
-// waves are then stacked in order per digit.  NP extra 32-bit payloads travel
-// with each key.
+// digit (found with eight ballots) plus the running per-wave count.  Each
+// array is then staged in LDS in tile-sorted order and written out by
+// consecutive threads, so equal digits leave as contiguous runs instead of
+// scattered 4-byte stores.  NP extra 32-bit payloads travel with each key.
 template <int NP>
 __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
@@ -126,15 +127,21 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     int n_tiles, const int32_t *__restrict__ offsets, RadixPayload p0, RadixPayload p1)
 {
     constexpr int kWaves = kSortBlock / kWave;
-    __shared__ int32_t wcnt[kWaves][kDigits];
+    __shared__ int32_t wcnt[kWaves][kDigits];   // per-wave counts, then tile-local run starts
+    __shared__ int32_t dstart[kDigits];         // tile-local start of each digit
+    __shared__ int32_t gstart[kDigits];         // global start of this tile's run of each digit
+    __shared__ uint32_t stage[kSortTile];
+    __shared__ uint8_t qdig[kSortTile];
     const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) wcnt[i][tid] = 0;
     __syncthreads();
 
-    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)w * kWave * kSortItems;
+    const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
+    const int count = (int)((n - tile0) < kSortTile ? (n - tile0) : kSortTile);
+    const int64_t base = tile0 + (int64_t)w * kWave * kSortItems;
     const uint64_t lower = __lanemask_lt();
-    uint32_t key[kSortItems], val[kSortItems], pa[NP > 0 ? kSortItems : 1], pb[NP > 1 ? kSortItems : 1];
+    uint32_t key[kSortItems];
     int local[kSortItems];
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
@@ -142,9 +149,6 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         const bool valid = e < n;
         const uint32_t k = valid ? keys_in[e] : 0u;
         key[i] = k;
-        val[i] = valid ? (vals_in ? vals_in[e] : (uint32_t)e) : 0u;
-        if constexpr (NP > 0) pa[i] = valid ? p0.in[e] : 0u;
-        if constexpr (NP > 1) pb[i] = valid ? p1.in[e] : 0u;
         const int d = (int)((k >> shift) & (kDigits - 1));
         uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -161,7 +165,15 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     }
     __syncthreads();
     {
-        int run = offsets[(int64_t)tid * n_tiles + blockIdx.x];
+        // tile-local start of digit `tid`, and of each wave's share of it
+        int tot = 0;
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i) tot += wcnt[i][tid];
+        int all;
+        const int start = block_exclusive_scan(tot, &all);
+        dstart[tid] = start;
+        gstart[tid] = offsets[(int64_t)tid * n_tiles + blockIdx.x];
+        int run = start;
 #pragma unroll
         for (int i = 0; i < kWaves; ++i) {
             const int c = wcnt[i][tid];
@@ -170,15 +182,39 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         }
     }
     __syncthreads();
+    // tile-sorted position of each of this thread's keys
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         if (local[i] >= 0) {
             const int d = (int)((key[i] >> shift) & (kDigits - 1));
-            const int pos = wcnt[w][d] + local[i];
-            if (keys_out) keys_out[pos] = key[i];
-            vals_out[pos] = val[i];
-            if constexpr (NP > 0) p0.out[pos] = pa[i];
-            if constexpr (NP > 1) p1.out[pos] = pb[i];
+            local[i] += wcnt[w][d];
+            stage[local[i]] = key[i];
+            qdig[local[i]] = (uint8_t)d;
+        }
+    }
+    __syncthreads();
+    if (keys_out)
+        for (int q = tid; q < count; q += kSortBlock) {
+            const int d = qdig[q];
+            keys_out[gstart[d] + (q - dstart[d])] = stage[q];
+        }
+    // values and payloads, one array at a time through the same staging buffer
+#pragma unroll
+    for (int arr = 0; arr <= NP; ++arr) {
+        const uint32_t *src = arr == 0 ? vals_in : (arr == 1 ? p0.in : p1.in);
+        uint32_t *dst = arr == 0 ? vals_out : (arr == 1 ? p0.out : p1.out);
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kSortItems; ++i) {
+            if (local[i] >= 0) {
+                const int64_t e = base + i * kWave + lane;
+                stage[local[i]] = src ? src[e] : (uint32_t)e;
+            }
+        }
+        __syncthreads();
+        for (int q = tid; q < count; q += kSortBlock) {
+            const int d = qdig[q];
+            dst[gstart[d] + (q - dstart[d])] = stage[q];
         }
     }
 }

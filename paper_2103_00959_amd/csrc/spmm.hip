@@ -35,11 +35,12 @@ struct SpmmArgs {
     float *partials;
     int64_t pstride;
     int64_t F;
+    uint64_t x_bytes;           // size of X, bounds the buffer gathers
     int32_t slab;
     int32_t log2S;
 };
 
-template <typename TX, typename TY, int VEC, int CH>
+template <typename TX, typename TY, int VEC, int CH, bool BUF>
 __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
 {
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
@@ -78,68 +79,49 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
 
-    const TX *__restrict__ X = static_cast<const TX *>(a.X);
+    const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ val = a.val;
 
-    int c_cur = 0;
-    float v_cur = 0.f;
-    if (beg + lig < end) {
-        c_cur = col[beg + lig];
-        v_cur = val ? val[beg + lig] : 1.f;
-    }
-    for (int k0 = beg; k0 < end; k0 += S) {
-        const int n = (end - k0 < S) ? end - k0 : S;
-        const int kn = k0 + S + lig;
-        int c_nxt = 0;
-        float v_nxt = 0.f;
-        if (kn < end) {
-            c_nxt = col[kn];
-            v_nxt = val ? val[kn] : 1.f;
-        }
-        int j = 0;
-        for (; j + U <= n; j += U) {
-            int cc[U];
-            float vv[U];
+    if (end > beg) {
+        // Index loads are clamped to the unit's last edge instead of masked, so
+        // they need no branch; lanes past the end are never read back.
+        const int last = end - 1;
+        int k = beg + lig < last ? beg + lig : last;
+        int c_cur = col[k];
+        float v_cur = val ? val[k] : 1.f;
+        for (int k0 = beg; k0 < end; k0 += S) {
+            const int n = (end - k0 < S) ? end - k0 : S;
+            k = k0 + S + lig < last ? k0 + S + lig : last;
+            const int c_nxt = col[k];
+            const float v_nxt = val ? val[k] : 1.f;
+            for (int j = 0; j < n; j += U) {
+                int cc[U];
+                float vv[U];
+                bool ok[U];
 #pragma unroll
-            for (int t = 0; t < U; ++t) {
-                cc[t] = lane_bcast(c_cur, gbase + j + t);
-                vv[t] = lane_bcast(v_cur, gbase + j + t);
-            }
-            float xv[U][CH][VEC];
-#pragma unroll
-            for (int t = 0; t < U; ++t)
-#pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    if (act[c]) {
-                        load_vec<TX, VEC>(X, (int64_t)cc[t] * a.F + fe[c], xv[t][c]);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) xv[t][c][e] = 0.f;
-                    }
+                for (int t = 0; t < U; ++t) {
+                    ok[t] = j + t < n;
+                    const int src = gbase + (ok[t] ? j + t : j);
+                    cc[t] = lane_bcast(c_cur, src);
+                    vv[t] = lane_bcast(v_cur, src);
                 }
+                float xv[U][CH][VEC];
 #pragma unroll
-            for (int t = 0; t < U; ++t)
+                for (int t = 0; t < U; ++t)
 #pragma unroll
-                for (int c = 0; c < CH; ++c)
+                    for (int c = 0; c < CH; ++c)
+                        X.load((int64_t)cc[t] * a.F + fe[c], ok[t] && act[c], xv[t][c]);
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(vv[t], xv[t][c][e], acc[c][e]);
-        }
-        for (; j < n; ++j) {
-            const int cj = lane_bcast(c_cur, gbase + j);
-            const float vj = lane_bcast(v_cur, gbase + j);
+                for (int t = 0; t < U; ++t)
 #pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                if (act[c]) {
-                    float x[VEC];
-                    load_vec<TX, VEC>(X, (int64_t)cj * a.F + fe[c], x);
+                    for (int c = 0; c < CH; ++c)
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(vj, x[e], acc[c][e]);
-                }
+                        for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(vv[t], xv[t][c][e], acc[c][e]);
             }
+            c_cur = c_nxt;
+            v_cur = v_nxt;
         }
-        c_cur = c_nxt;
-        v_cur = v_nxt;
     }
 
     if (part < 0) {
@@ -217,33 +199,39 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
 
 using SpmmKernel = void (*)(SpmmArgs);
 
-template <typename TX, typename TY>
+template <typename TX, typename TY, bool BUF>
 SpmmKernel pick_kernel(int vec, int ch)
 {
     constexpr int V = (int)(16 / sizeof(TX));
     if (vec == 1) {
-        if (ch == 1) return k_spmm<TX, TY, 1, 1>;
-        if (ch == 2) return k_spmm<TX, TY, 1, 2>;
-        return k_spmm<TX, TY, 1, 4>;
+        if (ch == 1) return k_spmm<TX, TY, 1, 1, BUF>;
+        if (ch == 2) return k_spmm<TX, TY, 1, 2, BUF>;
+        return k_spmm<TX, TY, 1, 4, BUF>;
     }
-    if (ch == 1) return k_spmm<TX, TY, V, 1>;
-    if (ch == 2) return k_spmm<TX, TY, V, 2>;
-    return k_spmm<TX, TY, V, 4>;
+    if (ch == 1) return k_spmm<TX, TY, V, 1, BUF>;
+    if (ch == 2) return k_spmm<TX, TY, V, 2, BUF>;
+    return k_spmm<TX, TY, V, 4, BUF>;
 }
 
-template <typename TX>
+template <typename TX, bool BUF>
 SpmmKernel pick_y(int ydt, int vec, int ch)
 {
-    if (ydt == COGDL_F32) return pick_kernel<TX, float>(vec, ch);
-    if (ydt == COGDL_BF16) return pick_kernel<TX, bf16_t>(vec, ch);
-    return pick_kernel<TX, f16_t>(vec, ch);
+    if (ydt == COGDL_F32) return pick_kernel<TX, float, BUF>(vec, ch);
+    if (ydt == COGDL_BF16) return pick_kernel<TX, bf16_t, BUF>(vec, ch);
+    return pick_kernel<TX, f16_t, BUF>(vec, ch);
 }
 
-SpmmKernel pick(int xdt, int ydt, int vec, int ch)
+template <bool BUF>
+SpmmKernel pick_x(int xdt, int ydt, int vec, int ch)
 {
-    if (xdt == COGDL_F32) return pick_y<float>(ydt, vec, ch);
-    if (xdt == COGDL_BF16) return pick_y<bf16_t>(ydt, vec, ch);
-    return pick_y<f16_t>(ydt, vec, ch);
+    if (xdt == COGDL_F32) return pick_y<float, BUF>(ydt, vec, ch);
+    if (xdt == COGDL_BF16) return pick_y<bf16_t, BUF>(ydt, vec, ch);
+    return pick_y<f16_t, BUF>(ydt, vec, ch);
+}
+
+SpmmKernel pick(int xdt, int ydt, int vec, int ch, bool buf)
+{
+    return buf ? pick_x<true>(xdt, ydt, vec, ch) : pick_x<false>(xdt, ydt, vec, ch);
 }
 
 template <int VEC>
@@ -314,12 +302,13 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     a.partials = P ? P->partials : nullptr;
     a.pstride = P ? (P->max_feat + 7) / 8 * 8 : 0;
     a.F = F;
+    a.x_bytes = (uint64_t)in_rows * (uint64_t)F * (uint64_t)dtype_bytes(xdt);
     a.slab = m.slab;
     a.log2S = m.log2S;
     const int64_t units = P ? P->cap_units : out_rows;
     const int64_t upb = kBlock >> m.log2S;
     const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
-    SpmmKernel k = pick(xdt, ydt, m.vec, m.ch);
+    SpmmKernel k = pick(xdt, ydt, m.vec, m.ch, a.x_bytes <= kBufferMaxBytes);
     COGDL_LAUNCH(name, k, grid, kBlock, s, a);
     if (P) return sum_reduce_launch(reduce_name, *P, F, Y, ydt, s);
     return COGDL_OK;
