@@ -212,6 +212,19 @@ def power_law_exponent(mean: float, lo: float, hi: float) -> float:
     return 0.5 * (a + b)
 
 
+def _weighted_draw(rng, cdf: np.ndarray, size: int, table: np.ndarray) -> np.ndarray:
+    """Indices i with probability proportional to the weights behind ``cdf``
+    (inverse CDF; ``table`` maps 2^k equal buckets of [0, 1) to their first
+    candidate index, so a short linear probe finishes the search)."""
+    u = rng.random(size)
+    idx = table[(u * table.size).astype(np.int64)]
+    todo = np.flatnonzero(cdf[idx] <= u)
+    while todo.size:
+        idx[todo] += 1
+        todo = todo[cdf[idx[todo]] <= u[todo]]
+    return idx
+
+
 def chung_lu(n: int, nnz: int, dmin: int, dmax: int, seed: int) -> Graph:
     rng = np.random.default_rng(seed)
     mean = nnz / n
@@ -229,16 +242,23 @@ def chung_lu(n: int, nnz: int, dmin: int, dmax: int, seed: int) -> Graph:
         diff = nnz - int(deg.sum())
     cdf = np.cumsum(w)
     cdf /= cdf[-1]
-    rows_all = np.repeat(np.arange(n, dtype=np.int64), deg)
+    cdf[-1] = 1.0 + 1e-12                       # every u < 1 stops at the last index
+    table = np.searchsorted(cdf, np.arange(1 << 20) / float(1 << 20), side="right")
+    # first round: deg[i] draws for every row; later rounds draw each row's
+    # shortfall and merge only the new distinct keys into the sorted key set
+    need_rows = np.repeat(np.arange(n, dtype=np.int64), deg)
     keys = np.empty(0, dtype=np.int64)
-    need_rows = rows_all
     while need_rows.size:
-        cols = np.searchsorted(cdf, rng.random(need_rows.size), side="right").astype(np.int64)
-        cols = np.minimum(cols, n - 1)
+        cols = _weighted_draw(rng, cdf, need_rows.size, table)
         ok = cols != need_rows
-        keys = np.unique(np.concatenate([keys, need_rows[ok] * n + cols[ok]]))
-        have = np.bincount(keys // n, minlength=n)
-        short = deg - have
+        new = np.unique(need_rows[ok] * n + cols[ok])
+        if keys.size:
+            pos = np.searchsorted(keys, new)
+            fresh = (pos >= keys.size) | (keys[np.minimum(pos, keys.size - 1)] != new)
+            keys = np.insert(keys, pos[fresh], new[fresh])
+        else:
+            keys = new
+        short = deg - np.bincount(keys // n, minlength=n)
         need_rows = np.repeat(np.arange(n, dtype=np.int64), np.maximum(short, 0))
     return _csr_from_keys(keys, n, n)
 
