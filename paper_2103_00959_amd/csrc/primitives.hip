@@ -116,10 +116,11 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__res
 // Stable scatter of one tile.  Wavefront w owns the contiguous quarter
 // [w * 1024, (w + 1) * 1024) of the tile and walks it 64 keys at a time; the
 // rank of a key among equal digits is the number of lower lanes with the same
-// digit (found with eight ballots) plus the running per-wave count.  Each
-// array is then staged in LDS in tile-sorted order and written out by
-// consecutive threads, so equal digits leave as contiguous runs instead of
-// scattered 4-byte stores.  NP extra 32-bit payloads travel with each key.
+// digit (found with eight ballots) plus the running per-wave count.  All
+// arrays of the tile are loaded up front (one memory round trip), then staged
+// in LDS in tile-sorted order two at a time and written out by consecutive
+// threads, so equal digits leave as contiguous runs instead of scattered
+// 4-byte stores.  NP extra 32-bit payloads travel with each key.
 template <int NP>
 __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
@@ -130,26 +131,33 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     __shared__ int32_t wcnt[kWaves][kDigits];   // per-wave counts, then tile-local run starts
     __shared__ int32_t dstart[kDigits];         // tile-local start of each digit
     __shared__ int32_t gstart[kDigits];         // global start of this tile's run of each digit
-    __shared__ uint32_t stage[kSortTile];
+    __shared__ uint32_t stage[2][kSortTile];
     __shared__ uint8_t qdig[kSortTile];
     const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) wcnt[i][tid] = 0;
-    __syncthreads();
 
     const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
     const int count = (int)((n - tile0) < kSortTile ? (n - tile0) : kSortTile);
     const int64_t base = tile0 + (int64_t)w * kWave * kSortItems;
-    const uint64_t lower = __lanemask_lt();
-    uint32_t key[kSortItems];
-    int local[kSortItems];
+    uint32_t key[kSortItems], val[kSortItems], pa[NP > 0 ? kSortItems : 1], pb[NP > 1 ? kSortItems : 1];
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const int64_t e = base + i * kWave + lane;
-        const bool valid = e < n;
-        const uint32_t k = valid ? keys_in[e] : 0u;
-        key[i] = k;
-        const int d = (int)((k >> shift) & (kDigits - 1));
+        const int64_t ec = e < n ? e : n - 1;     // clamped: loads need no branch
+        key[i] = keys_in[ec];
+        val[i] = vals_in ? vals_in[ec] : (uint32_t)e;
+        if constexpr (NP > 0) pa[i] = p0.in[ec];
+        if constexpr (NP > 1) pb[i] = p1.in[ec];
+    }
+    __syncthreads();
+
+    const uint64_t lower = __lanemask_lt();
+    int local[kSortItems];
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const bool valid = base + i * kWave + lane < n;
+        const int d = (int)((key[i] >> shift) & (kDigits - 1));
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
@@ -182,39 +190,38 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         }
     }
     __syncthreads();
-    // tile-sorted position of each of this thread's keys
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         if (local[i] >= 0) {
             const int d = (int)((key[i] >> shift) & (kDigits - 1));
             local[i] += wcnt[w][d];
-            stage[local[i]] = key[i];
+            stage[0][local[i]] = key[i];
+            stage[1][local[i]] = val[i];
             qdig[local[i]] = (uint8_t)d;
         }
     }
     __syncthreads();
-    if (keys_out)
-        for (int q = tid; q < count; q += kSortBlock) {
-            const int d = qdig[q];
-            keys_out[gstart[d] + (q - dstart[d])] = stage[q];
-        }
-    // values and payloads, one array at a time through the same staging buffer
-#pragma unroll
-    for (int arr = 0; arr <= NP; ++arr) {
-        const uint32_t *src = arr == 0 ? vals_in : (arr == 1 ? p0.in : p1.in);
-        uint32_t *dst = arr == 0 ? vals_out : (arr == 1 ? p0.out : p1.out);
+    for (int q = tid; q < count; q += kSortBlock) {
+        const int d = qdig[q];
+        const int pos = gstart[d] + (q - dstart[d]);
+        if (keys_out) keys_out[pos] = stage[0][q];
+        vals_out[pos] = stage[1][q];
+    }
+    if constexpr (NP > 0) {
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < kSortItems; ++i) {
             if (local[i] >= 0) {
-                const int64_t e = base + i * kWave + lane;
-                stage[local[i]] = src ? src[e] : (uint32_t)e;
+                stage[0][local[i]] = pa[i];
+                if constexpr (NP > 1) stage[1][local[i]] = pb[i];
             }
         }
         __syncthreads();
         for (int q = tid; q < count; q += kSortBlock) {
             const int d = qdig[q];
-            dst[gstart[d] + (q - dstart[d])] = stage[q];
+            const int pos = gstart[d] + (q - dstart[d]);
+            p0.out[pos] = stage[0][q];
+            if constexpr (NP > 1) p1.out[pos] = stage[1][q];
         }
     }
 }
