@@ -197,9 +197,21 @@ def main():
     plan_t = cg.Plan(colptr, E, max_feat=F, group_size=args.group_size)
     torch.cuda.synchronize()
     info, info_t = plan.info(), plan_t.info()
-    log(f"plan: {info['mode_name']} units={info['n_units']} split_rows={info['n_split_rows']} "
-        f"partials={info['n_partials']}; plan_t: {info_t['mode_name']} units={info_t['n_units']} "
-        f"split_rows={info_t['n_split_rows']}")
+    log(f"plan: {info['mode_name']} units={info['n_units']} long={info['n_long_units']} "
+        f"split_rows={info['n_split_rows']} partials={info['n_partials']}; plan_t: "
+        f"{info_t['mode_name']} units={info_t['n_units']} split_rows={info_t['n_split_rows']}")
+    # Edges and directly written rows of the long-unit and tiny-unit kernels
+    # (split rows are written by the reduce kernel): the algorithmic bytes of
+    # an op are split exactly between its kernels.
+    def unit_split(p, inf):
+        un = p.units().cpu().numpy().astype(np.int64)
+        nb = inf["n_long_units"]
+        size = un[:, 2] - un[:, 1]
+        direct = un[:, 3] < 0
+        return dict(E_long=int(size[:nb].sum()), R_long=int(direct[:nb].sum()),
+                    E_tiny=int(size[nb:].sum()), R_tiny=int(direct[nb:].sum()),
+                    R_split=inf["n_split_rows"])
+    us, us_t = unit_split(plan, info), unit_split(plan_t, info_t)
 
     OPS = ["plan", "spmm", "csr_to_csc", "plan_t", "spmm_t", "gat_aggregate"]
 
@@ -265,8 +277,6 @@ def main():
     kernels = {k: dict(total_ms=v[0] / args.steps, launches=v[1] // args.steps,
                        avg_ms=v[0] / v[1]) for k, v in per.items()}
 
-    n_split = info["n_split_rows"]
-    n_split_t = info_t["n_split_rows"]
     B = {
         "plan": b_plan(N, info["n_units"]),
         "plan_t": b_plan(M, info_t["n_units"]),
@@ -284,13 +294,18 @@ def main():
                        eff_GBps=(B[op] / (ms * 1e-3) / 1e9) if ms > 0 else None,
                        pct_peak=(B[op] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS) if ms > 0 else None,
                        edges_per_s=(E / (ms * 1e-3)) if ms > 0 and not op.startswith("plan") else None)
-    # dominant kernel: the largest device time per step
-    dom = max(("spmm", "spmm_t", "gat"), key=lambda k: kernels.get(k, {"total_ms": 0})["total_ms"])
-    dom_bytes = {
-        "spmm": B["spmm"] - n_split * F * 2,          # split rows' Y is written by spmm_reduce
-        "spmm_t": B["spmm_t"] - n_split_t * F * 2,
-        "gat": B["gat_aggregate"] - n_split * H * D * 2,
-    }[dom]
+    # dominant kernel: the largest device time per step; its algorithmic bytes
+    # are its own edges and output rows (per nonzero: index, value, one feature
+    # row; per row: row pointer and the output row)
+    e_sp, r_sp = 8 + F * 2, 4 + F * 2
+    e_gat, r_gat = 4 + 4 * H + H * D * 2, 4 + 4 * H + H * D * 2
+    kbytes = {
+        "spmm": us["E_long"] * e_sp + us["R_long"] * r_sp,
+        "spmm_t": us_t["E_long"] * e_sp + us_t["R_long"] * r_sp,
+        "gat": us["E_long"] * e_gat + us["R_long"] * r_gat,
+    }
+    dom = max(kbytes, key=lambda k: kernels.get(k, {"total_ms": 0})["total_ms"])
+    dom_bytes = kbytes[dom]
     dom_ms = kernels[dom]["avg_ms"]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     tr = recorded_traffic(cfg["name"], dom)

@@ -75,7 +75,6 @@ typedef enum {
 } cogdl_balance;
 
 #define COGDL_MAX_HEADS 64
-#define COGDL_DEFAULT_GROUP_SIZE 256
 
 typedef struct cogdl_plan cogdl_plan;   /* opaque; owns device work lists and workspace */
 
@@ -87,6 +86,7 @@ typedef struct {
     int32_t max_heads;
     int32_t mode;           /* COGDL_BALANCE_ROW_SPLIT or COGDL_BALANCE_NEIGHBOR_GROUP, as chosen */
     int32_t n_units;        /* work units in execution order */
+    int32_t n_long_units;   /* leading units with more than 8 edges; the rest run a narrow path */
     int32_t n_split_rows;   /* rows cut into more than one unit */
     int32_t n_partials;     /* partial-sum slots used by split rows */
     int64_t device_bytes;   /* device memory owned by the plan */
@@ -116,7 +116,9 @@ int32_t cogdl_version(void);
  * max_feat    largest feature width F (or H*D) the plan will serve, >= 1.
  * max_heads   largest head count H the plan will serve in the attention calls
  *             (0 if it serves only cogdl_spmm / cogdl_spmm_t), <= COGDL_MAX_HEADS.
- * group_size  neighbour-group size in edges, >= 1 (0 = COGDL_DEFAULT_GROUP_SIZE).
+ * group_size  neighbour-group size in edges, >= 1; 0 picks it from the graph size:
+ *             the power of two at or below nnz / 16384, clamped to [256, 4096]
+ *             (large groups mean fewer partial sums, small ones better balance).
  * The build runs asynchronously on `stream`; *out is valid immediately and
  * every later call on the same stream sees the finished plan.
  * ---------------------------------------------------------------------- */

@@ -36,7 +36,8 @@ class CogdlError(RuntimeError):
 class _PlanInfo(ctypes.Structure):
     _fields_ = [("n_rows", ctypes.c_int32), ("nnz", ctypes.c_int64), ("group_size", ctypes.c_int32),
                 ("max_feat", ctypes.c_int32), ("max_heads", ctypes.c_int32), ("mode", ctypes.c_int32),
-                ("n_units", ctypes.c_int32), ("n_split_rows", ctypes.c_int32),
+                ("n_units", ctypes.c_int32), ("n_long_units", ctypes.c_int32),
+                ("n_split_rows", ctypes.c_int32),
                 ("n_partials", ctypes.c_int32), ("device_bytes", ctypes.c_int64)]
 
 

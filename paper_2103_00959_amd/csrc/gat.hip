@@ -26,7 +26,8 @@ constexpr int kBlock = 256;
 
 struct GatArgs {
     const int4 *units;
-    const int32_t *n_units;
+    const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
+    const int32_t *u_hi;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -49,6 +50,16 @@ struct GatArgs {
     int32_t log2S;
 };
 
+// Descriptor {row, first edge, end edge, partial slot} of unit u (an empty
+// unit past the end, so prefetching one unit ahead needs no branch around it).
+__device__ __forceinline__ int4 fetch_unit(const GatArgs &a, int64_t u, int64_t hi)
+{
+    if (u >= hi) return make_int4(0, 0, 0, -1);
+    if (a.units) return a.units[u];
+    const int r = (int)u;
+    return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
+}
+
 template <typename TX, typename TY, int VEC, int CH, bool BUF>
 __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
 {
@@ -58,56 +69,59 @@ __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
     const int lane = lane_id();
     const int lig = lane & (S - 1);
     const int gbase = lane & ~(S - 1);
-    const int64_t u = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
     const int H = a.H;
-
-    int row, beg, end, part;
-    if (a.units) {
-        if (u >= *a.n_units) return;
-        const int4 d = a.units[u];
-        row = d.x; beg = d.y; end = d.z; part = d.w;
-    } else {
-        if (u >= a.n_rows) return;
-        row = (int)u;
-        beg = a.rowptr[row];
-        end = a.rowptr[row + 1];
-        part = -1;
-    }
     const bool soft = a.alpha_in == nullptr;
+    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
+    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
+    const int64_t lo = a.units ? *a.u_lo : 0;
+    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
 
     const int64_t f0 = (int64_t)blockIdx.y * a.slab;
     const int64_t f_end = (f0 + a.slab < a.W) ? f0 + a.slab : a.W;
     int64_t fe[CH];
     bool act[CH];
     int hd[CH];
-    float sd[CH], m[CH], z[CH];
-    float acc[CH][VEC];
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         fe[c] = f0 + (int64_t)(c * S + lig) * VEC;
         act[c] = fe[c] < f_end;
         hd[c] = act[c] ? (int)(fe[c] / a.D) : 0;
-        sd[c] = soft ? a.s_dst[(int64_t)row * H + hd[c]] : 0.f;
-        m[c] = -INFINITY;
-        z[c] = 0.f;
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
     }
-
     const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ wsrc = soft ? a.s_src : a.alpha_in;
+    // (edge slot, head) lane layout of the alpha sweep: eps edges per step
+    const int eps = S / H;
+    const int q_slot = lig / H, q_head = lig % H;
 
-    if (end > beg) {
-        // Branch-free batches: index loads are clamped to the unit's last edge,
-        // masked gathers read zeros, masked weights are -inf (softmax) or 0.
+    // Resident grid, software-pipelined over units as in the SpMM kernel.
+    int64_t u = lo + sub;
+    if (u >= hi) return;
+    int4 d = fetch_unit(a, u, hi);
+    int c_cur = 0;
+    if (d.z > d.y) c_cur = col[d.y + lig < d.z - 1 ? d.y + lig : d.z - 1];
+    for (;;) {
+        const int64_t un = u + stride;
+        const int4 dn = fetch_unit(a, un, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        float sd[CH], m[CH], z[CH];
+        float acc[CH][VEC];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            sd[c] = soft ? a.s_dst[(int64_t)row * H + hd[c]] : 0.f;
+            m[c] = -INFINITY;
+            z[c] = 0.f;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
+        }
+
+        // Branch-free batches: index loads are clamped to the unit's last
+        // edge, masked gathers read zeros, masked weights are -inf (softmax)
+        // or 0.
         const int last = end - 1;
-        int k = beg + lig < last ? beg + lig : last;
-        int c_cur = col[k];
         for (int k0 = beg; k0 < end; k0 += S) {
             const int n = (end - k0 < S) ? end - k0 : S;
-            k = k0 + S + lig < last ? k0 + S + lig : last;
-            const int c_nxt = col[k];
+            const int c_nxt = col[k0 + S + lig < last ? k0 + S + lig : last];
             for (int j = 0; j < n; j += U) {
                 int cc[U];
                 bool ok[U];
@@ -168,54 +182,59 @@ __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
             }
             c_cur = c_nxt;
         }
-    }
+        const int c_first_next = (dn.z > dn.y) ? col[dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1] : 0;
 
-    if (part >= 0) {
-        // neighbour group of a split row: unnormalized partial + (m, z) per head
+        if (part >= 0) {
+            // neighbour group of a split row: unnormalized partial + (m, z) per head
 #pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            if (!act[c]) continue;
-            store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
-            if (soft && fe[c] % a.D == 0) {
-                a.gstats[(int64_t)part * a.sstride + hd[c]] = m[c];
-                a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + hd[c]] = z[c];
+            for (int c = 0; c < CH; ++c) {
+                if (!act[c]) continue;
+                store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+                if (soft && fe[c] % a.D == 0) {
+                    a.gstats[(int64_t)part * a.sstride + hd[c]] = m[c];
+                    a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + hd[c]] = z[c];
+                }
+            }
+        } else {
+            float rz[CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                rz[c] = (soft && z[c] > 0.f) ? 1.f / z[c] : 1.f;
+                float v[VEC];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) v[e] = acc[c][e] * rz[c];
+                if (act[c]) store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
+            }
+            if (soft && a.alpha_out != nullptr) {
+                // alpha of this whole-row unit: lanes as (edge slot, head); the
+                // (m, z) of head h comes from the lane holding the first feature
+                // of h in this slab.
+                const int h1 = q_head;
+                const int slot = q_slot;
+                const int64_t hf = (int64_t)h1 * a.D;
+                const bool mine_head = hf >= f0 && hf < f_end;
+                const int idx = mine_head ? (int)((hf - f0) / VEC) : 0;
+                const int src_c = idx / S, src_l = idx % S;
+                float m1 = 0.f, r1 = 0.f;
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const float mm = lane_bcast(m[c], gbase + src_l);
+                    const float rr = lane_bcast(rz[c], gbase + src_l);
+                    if (c == src_c) { m1 = mm; r1 = rr; }
+                }
+                if (mine_head && slot < eps) {
+                    const float sd1 = a.s_dst[(int64_t)row * H + h1];
+                    for (int k = beg + slot; k < end; k += eps) {
+                        const float e = leaky_relu(sd1 + a.s_src[(int64_t)col[k] * H + h1], a.slope);
+                        a.alpha_out[(int64_t)k * H + h1] = __expf(e - m1) * r1;
+                    }
+                }
             }
         }
-        return;
-    }
-
-    float rz[CH];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        rz[c] = (soft && z[c] > 0.f) ? 1.f / z[c] : 1.f;
-        float v[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) v[e] = acc[c][e] * rz[c];
-        if (act[c]) store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
-    }
-
-    if (!soft || a.alpha_out == nullptr) return;
-    // alpha for this whole-row unit: lanes as (edge slot, head); the (m, z) of
-    // head h comes from the lane holding the first feature of h in this slab.
-    const int eps = S / H;
-    const int h1 = lig % H;
-    const int slot = lig / H;
-    const int64_t hf = (int64_t)h1 * a.D;
-    const bool mine_head = hf >= f0 && hf < f_end;
-    const int idx = mine_head ? (int)((hf - f0) / VEC) : 0;
-    const int src_c = idx / S, src_l = idx % S;
-    float m1 = 0.f, r1 = 0.f;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        const float mm = lane_bcast(m[c], gbase + src_l);
-        const float rr = lane_bcast(rz[c], gbase + src_l);
-        if (c == src_c) { m1 = mm; r1 = rr; }
-    }
-    if (!mine_head || slot >= eps) return;
-    const float sd1 = a.s_dst[(int64_t)row * H + h1];
-    for (int k = beg + slot; k < end; k += eps) {
-        const float e = leaky_relu(sd1 + a.s_src[(int64_t)col[k] * H + h1], a.slope);
-        a.alpha_out[(int64_t)k * H + h1] = __expf(e - m1) * r1;
+        if (un >= hi) break;
+        u = un;
+        d = dn;
+        c_cur = c_first_next;
     }
 }
 
@@ -618,7 +637,8 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     }
     GatArgs a{};
     a.units = P ? P->units : nullptr;
-    a.n_units = P ? P->n_units_dev() : nullptr;
+    a.u_lo = P ? P->zero_dev() : nullptr;
+    a.u_hi = P ? P->n_units_dev() : nullptr;
     a.n_rows = n_rows;
     a.rowptr = rowptr;
     a.col = col;
@@ -639,11 +659,33 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     a.sstride = P ? 2 * P->max_heads : 0;
     a.slab = m.slab;
     a.log2S = m.log2S;
+    const bool buf = a.x_bytes <= kBufferMaxBytes;
     const int64_t units = P ? P->cap_units : n_rows;
-    const int64_t upb = kBlock >> m.log2S;
-    const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
-    GatKernel k = pick_gat(x_dtype, y_dtype, m.vec, m.ch, a.x_bytes <= kBufferMaxBytes);
-    COGDL_LAUNCH("gat", k, grid, kBlock, stream, a);
+    // tiny units (the sorted tail): S/4 lanes and four chunks per lane
+    const bool tiny = P && m.ch == 1 && m.S >= 8 && m.S / 4 >= H;
+    if (tiny) a.u_hi = P->n_big_dev();
+    {
+        const int64_t upb = kBlock >> m.log2S;
+        GatKernel k = pick_gat(x_dtype, y_dtype, m.vec, m.ch, buf);
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH("gat", k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock,
+                     stream, a);
+    }
+    if (tiny) {
+        GatArgs b = a;
+        b.u_lo = P->n_big_dev();
+        b.u_hi = P->n_units_dev();
+        b.log2S = m.log2S - 2;
+        const int64_t upb = kBlock >> b.log2S;
+        GatKernel k = pick_gat(x_dtype, y_dtype, m.vec, 4, buf);
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH("gat_tiny", k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
+                     kBlock, stream, b);
+    }
     if (!P) return COGDL_OK;
 
     if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, stream);

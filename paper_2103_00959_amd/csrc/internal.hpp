@@ -38,8 +38,9 @@ struct Plan {
     int32_t *row_units = nullptr; // [n_rows + 1] exclusive scan; [n_rows] = #units
     int32_t *row_parts = nullptr; // [n_rows + 1]; [n_rows] = #partial slots
     int32_t *row_split = nullptr; // [n_rows + 1]; [n_rows] = #split rows
-    int32_t *counters = nullptr;  // [4]: 0 close-degree rows, 1 chosen mode
-    uint32_t *sort_keys = nullptr;   // [3 * cap_units]: keys, then 2 ping buffers
+    int32_t *counters = nullptr;  // [4]: 0 close-degree rows, 1 chosen mode,
+                                  //      2 units longer than kTinyUnit, 3 zero
+    uint32_t *sort_keys = nullptr;   // [4 * cap_units]: keys, 2 ping buffers, sorted keys
     uint32_t *sort_vals = nullptr;   // [3 * cap_units]: order, then 2 ping buffers
     void *sort_ws = nullptr;
     size_t sort_ws_bytes = 0;
@@ -50,11 +51,20 @@ struct Plan {
     float *rstats = nullptr;      // [cap_split * max_heads * 2] per-split-row (m, z)
 
     const int32_t *n_units_dev() const { return row_units + n_rows; }
+    const int32_t *n_big_dev() const { return counters + 2; }
+    const int32_t *zero_dev() const { return counters + 3; }
     const int32_t *n_split_dev() const { return row_split + n_rows; }
     const int32_t *n_parts_dev() const { return row_parts + n_rows; }
 };
 
+// Units of at most this many edges run in the narrow-sub-group path.
+constexpr int kTinyUnit = 8;
+
 const Plan *plan_of(const cogdl_plan *h);
+
+// Workgroups of `block` threads of `kernel` that fit on the device at once
+// (all compute units), cached per kernel.
+int resident_blocks(const void *kernel, int block);
 
 // Y[row] = sum of the partial rows of every split row of the plan (F columns).
 cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,

@@ -99,6 +99,24 @@ __global__ void k_plan_emit(const int32_t *__restrict__ rowptr, int32_t n_rows, 
     }
 }
 
+// Units are sorted by key G - size (ascending): the tiny units (size <= T)
+// form the tail.  counters[2] = number of units longer than T (all of them
+// in row-split mode, whose keys are all 0), counters[3] = 0.
+__global__ void k_plan_split(const uint32_t *__restrict__ sorted_keys,
+                             const int32_t *__restrict__ n_units, int32_t G, int32_t T,
+                             int32_t *__restrict__ counters)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    const uint32_t bound = G > T ? (uint32_t)(G - T) : 0u;
+    int32_t lo = 0, hi = *n_units;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (sorted_keys[mid] < bound) lo = mid + 1; else hi = mid;
+    }
+    counters[2] = (G > T) ? lo : *n_units;
+    counters[3] = 0;
+}
+
 __global__ void k_plan_gather(const int4 *__restrict__ units_tmp, const uint32_t *__restrict__ order,
                               const int32_t *__restrict__ n_units, int64_t cap,
                               int4 *__restrict__ units)
@@ -128,6 +146,7 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, hipStream_t s)
     const uint32_t pad = (uint32_t)P.group_size + 1u;
     COGDL_HIP_TRY(fill_i32(reinterpret_cast<int32_t *>(P.sort_keys), P.cap_units, (int32_t)pad, s));
     if (n == 0) {
+        COGDL_HIP_TRY(fill_i32(P.counters, 4, 0, s));
         COGDL_HIP_TRY(fill_i32(P.row_units, 1, 0, s));
         COGDL_HIP_TRY(fill_i32(P.row_parts, 1, 0, s));
         COGDL_HIP_TRY(fill_i32(P.row_split, 1, 0, s));
@@ -147,9 +166,12 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, hipStream_t s)
     uint32_t *order = P.sort_vals;                    // [cap]: final order
     uint32_t *ping_k = P.sort_keys + P.cap_units;     // [2 * cap] ping buffers
     uint32_t *ping_v = P.sort_vals + P.cap_units;
+    uint32_t *sorted = P.sort_keys + 3 * P.cap_units; // [cap] keys in execution order
     const int bits = bits_for(pad);
-    COGDL_HIP_TRY(radix_sort_pairs(P.sort_keys, nullptr, nullptr, order, P.cap_units, bits, ping_k,
+    COGDL_HIP_TRY(radix_sort_pairs(P.sort_keys, nullptr, sorted, order, P.cap_units, bits, ping_k,
                                    ping_v, P.sort_ws, s));
+    COGDL_LAUNCH("plan_split", k_plan_split, 1, 64, s, sorted, P.n_units_dev(), P.group_size,
+                 kTinyUnit, P.counters);
     const int64_t gb = (P.cap_units + 255) / 256;
     COGDL_LAUNCH("plan_gather", k_plan_gather, (unsigned)(gb < 8192 ? gb : 8192), 256, s,
                  P.units_tmp, order, P.n_units_dev(), P.cap_units, P.units);
@@ -191,7 +213,11 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
         return COGDL_ERR_INVALID;
     if (nnz > INT32_MAX || n_rows == INT32_MAX) return COGDL_ERR_TOO_LARGE;
     if (n_rows == 0 && nnz != 0) return COGDL_ERR_INVALID;
-    const int32_t G = group_size == 0 ? COGDL_DEFAULT_GROUP_SIZE : group_size;
+    int32_t G = group_size;
+    if (G == 0) {
+        G = 256;
+        while (G < 4096 && (int64_t)G * 2 * 16384 <= nnz) G *= 2;
+    }
 
     cogdl_plan *h = new (std::nothrow) cogdl_plan;
     if (!h) return COGDL_ERR_NOMEM;
@@ -218,7 +244,7 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
     const size_t o_row_parts = take(4 * ((size_t)n_rows + 1));
     const size_t o_row_split = take(4 * ((size_t)n_rows + 1));
     const size_t o_counters = take(4 * 4);
-    const size_t o_keys = take(4 * 3 * (size_t)P.cap_units);
+    const size_t o_keys = take(4 * 4 * (size_t)P.cap_units);
     const size_t o_vals = take(4 * 3 * (size_t)P.cap_units);
     P.sort_ws_bytes = cogdl::radix_workspace_bytes(P.cap_units);
     const size_t o_sort_ws = take(P.sort_ws_bytes);
@@ -281,11 +307,12 @@ cogdl_status cogdl_plan_query(const cogdl_plan *plan, hipStream_t stream, cogdl_
 {
     if (!plan || !info) return COGDL_ERR_INVALID;
     const Plan &P = plan->p;
-    int32_t v[4] = {0, 0, 0, 0};
+    int32_t v[5] = {0, 0, 0, 0, 0};
     COGDL_HIP_TRY(hipMemcpyAsync(&v[0], P.n_units_dev(), 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[1], P.n_split_dev(), 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[2], P.n_parts_dev(), 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[3], P.counters + 1, 4, hipMemcpyDeviceToHost, stream));
+    COGDL_HIP_TRY(hipMemcpyAsync(&v[4], P.counters + 2, 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipStreamSynchronize(stream));
     info->n_rows = P.n_rows;
     info->nnz = P.nnz;
@@ -293,6 +320,7 @@ cogdl_status cogdl_plan_query(const cogdl_plan *plan, hipStream_t stream, cogdl_
     info->max_feat = P.max_feat;
     info->max_heads = P.max_heads;
     info->n_units = v[0];
+    info->n_long_units = v[4];
     info->n_split_rows = v[1];
     info->n_partials = v[2];
     info->mode = P.n_rows == 0 ? (P.mode_req == COGDL_BALANCE_AUTO ? COGDL_BALANCE_ROW_SPLIT

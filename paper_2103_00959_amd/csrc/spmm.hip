@@ -25,7 +25,8 @@ constexpr int kBlock = 256;
 
 struct SpmmArgs {
     const int4 *units;          // nullptr: one unit per row in row order
-    const int32_t *n_units;     // device count when units != nullptr
+    const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
+    const int32_t *u_hi;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -40,6 +41,16 @@ struct SpmmArgs {
     int32_t log2S;
 };
 
+// Descriptor {row, first edge, end edge, partial slot} of unit u (an empty
+// unit past the end, so prefetching one unit ahead needs no branch around it).
+__device__ __forceinline__ int4 fetch_unit(const SpmmArgs &a, int64_t u, int64_t hi)
+{
+    if (u >= hi) return make_int4(0, 0, 0, -1);
+    if (a.units) return a.units[u];
+    const int r = (int)u;
+    return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
+}
+
 template <typename TX, typename TY, int VEC, int CH, bool BUF>
 __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
 {
@@ -49,20 +60,10 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
     const int lane = lane_id();
     const int lig = lane & (S - 1);
     const int gbase = lane & ~(S - 1);
-    const int64_t u = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
-
-    int row, beg, end, part;
-    if (a.units) {
-        if (u >= *a.n_units) return;
-        const int4 d = a.units[u];
-        row = d.x; beg = d.y; end = d.z; part = d.w;
-    } else {
-        if (u >= a.n_rows) return;
-        row = (int)u;
-        beg = a.rowptr[row];
-        end = a.rowptr[row + 1];
-        part = -1;
-    }
+    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
+    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
+    const int64_t lo = a.units ? *a.u_lo : 0;
+    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
 
     const int64_t f0 = (int64_t)blockIdx.y * a.slab;
     const int64_t f_end = (f0 + a.slab < a.F) ? f0 + a.slab : a.F;
@@ -73,26 +74,41 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
         fe[c] = f0 + (int64_t)(c * S + lig) * VEC;
         act[c] = fe[c] < f_end;
     }
-    float acc[CH][VEC];
-#pragma unroll
-    for (int c = 0; c < CH; ++c)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
-
     const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ val = a.val;
 
-    if (end > beg) {
-        // Index loads are clamped to the unit's last edge instead of masked, so
-        // they need no branch; lanes past the end are never read back.
+    // Resident grid: sub-group i runs units lo + i, lo + i + stride, ...; the
+    // units are sorted by length, so neighbouring sub-groups get equal work.
+    // The loop is software-pipelined: the next unit's descriptor is fetched
+    // when a unit starts and its first index chunk before the current output
+    // is stored, so short units do not pay three dependent memory trips each.
+    int64_t u = lo + sub;
+    if (u >= hi) return;
+    int4 d = fetch_unit(a, u, hi);
+    int c_cur = 0;
+    float v_cur = 0.f;
+    if (d.z > d.y) {
+        // index loads are clamped to the unit's last edge instead of masked:
+        // no branch, and lanes past the end are never read back
+        const int k = d.y + lig < d.z - 1 ? d.y + lig : d.z - 1;
+        c_cur = col[k];
+        v_cur = val ? val[k] : 1.f;
+    }
+    for (;;) {
+        const int64_t un = u + stride;
+        const int4 dn = fetch_unit(a, un, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        float acc[CH][VEC];
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
+
         const int last = end - 1;
-        int k = beg + lig < last ? beg + lig : last;
-        int c_cur = col[k];
-        float v_cur = val ? val[k] : 1.f;
         for (int k0 = beg; k0 < end; k0 += S) {
             const int n = (end - k0 < S) ? end - k0 : S;
-            k = k0 + S + lig < last ? k0 + S + lig : last;
+            const int k = k0 + S + lig < last ? k0 + S + lig : last;
             const int c_nxt = col[k];
             const float v_nxt = val ? val[k] : 1.f;
             for (int j = 0; j < n; j += U) {
@@ -122,17 +138,26 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
             c_cur = c_nxt;
             v_cur = v_nxt;
         }
-    }
 
-    if (part < 0) {
-        TY *__restrict__ Y = static_cast<TY *>(a.Y);
+        // first index chunk of the next unit, issued before this unit's stores
+        if (dn.z > dn.y) {
+            const int k = dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1;
+            c_cur = col[k];
+            v_cur = val ? val[k] : 1.f;
+        }
+        if (part < 0) {
+            TY *__restrict__ Y = static_cast<TY *>(a.Y);
 #pragma unroll
-        for (int c = 0; c < CH; ++c)
-            if (act[c]) store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
-    } else {
+            for (int c = 0; c < CH; ++c)
+                if (act[c]) store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
+        } else {
 #pragma unroll
-        for (int c = 0; c < CH; ++c)
-            if (act[c]) store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+            for (int c = 0; c < CH; ++c)
+                if (act[c]) store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+        }
+        if (un >= hi) break;
+        u = un;
+        d = dn;
     }
 }
 
@@ -275,7 +300,7 @@ namespace {
 cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const int32_t *ptr,
                          const int32_t *idx, const float *w, int32_t F, const void *X, int xdt,
                          void *Y, int ydt, const cogdl_plan *plan_h, hipStream_t s,
-                         const char *name, const char *reduce_name)
+                         const char *name, const char *tiny_name, const char *reduce_name)
 {
     if (out_rows < 0 || in_rows < 0 || nnz < 0 || F < 0) return COGDL_ERR_INVALID;
     if (!dtype_ok(xdt) || !dtype_ok(ydt)) return COGDL_ERR_DTYPE;
@@ -292,7 +317,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     const RowMap m = row_map(F, dtype_bytes(xdt), F, aligned);
     SpmmArgs a;
     a.units = P ? P->units : nullptr;
-    a.n_units = P ? P->n_units_dev() : nullptr;
+    a.u_lo = P ? P->zero_dev() : nullptr;
+    a.u_hi = P ? P->n_units_dev() : nullptr;
     a.n_rows = out_rows;
     a.rowptr = ptr;
     a.col = idx;
@@ -305,11 +331,34 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     a.x_bytes = (uint64_t)in_rows * (uint64_t)F * (uint64_t)dtype_bytes(xdt);
     a.slab = m.slab;
     a.log2S = m.log2S;
+    const bool buf = a.x_bytes <= kBufferMaxBytes;
     const int64_t units = P ? P->cap_units : out_rows;
-    const int64_t upb = kBlock >> m.log2S;
-    const dim3 grid((unsigned)((units + upb - 1) / upb), (unsigned)m.n_slabs);
-    SpmmKernel k = pick(xdt, ydt, m.vec, m.ch, a.x_bytes <= kBufferMaxBytes);
-    COGDL_LAUNCH(name, k, grid, kBlock, s, a);
+    // Units of at most kTinyUnit edges (the sorted tail) run with S/4 lanes and
+    // four chunks per lane: four times as many rows in flight per wavefront.
+    const bool tiny = P && m.ch == 1 && m.S >= 8;
+    if (tiny) a.u_hi = P->n_big_dev();
+    {
+        const int64_t upb = kBlock >> m.log2S;
+        SpmmKernel k = pick(xdt, ydt, m.vec, m.ch, buf);
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH(name, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock, s,
+                     a);
+    }
+    if (tiny) {
+        SpmmArgs b = a;
+        b.u_lo = P->n_big_dev();
+        b.u_hi = P->n_units_dev();
+        b.log2S = m.log2S - 2;
+        const int64_t upb = kBlock >> b.log2S;
+        SpmmKernel k = pick(xdt, ydt, m.vec, 4, buf);
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH(tiny_name, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
+                     kBlock, s, b);
+    }
     if (P) return sum_reduce_launch(reduce_name, *P, F, Y, ydt, s);
     return COGDL_OK;
 }
@@ -325,7 +374,7 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         hipStream_t stream)
 {
     return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
-                              (int)y_dtype, plan, stream, "spmm", "spmm_reduce");
+                              (int)y_dtype, plan, stream, "spmm", "spmm_tiny", "spmm_reduce");
 }
 
 cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *colptr,
@@ -335,7 +384,7 @@ cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int
 {
     // A^T has n_cols rows, each gathering rows of the n_rows x F input G.
     return cogdl::spmm_common(n_cols, n_rows, nnz, colptr, row_t, val_t, F, G, (int)g_dtype, dX,
-                              (int)dx_dtype, plan_t, stream, "spmm_t", "spmm_t_reduce");
+                              (int)dx_dtype, plan_t, stream, "spmm_t", "spmm_t_tiny", "spmm_t_reduce");
 }
 
 }  // extern "C"

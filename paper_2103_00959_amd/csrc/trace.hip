@@ -5,6 +5,7 @@
 // The tracer is process-wide and not thread-safe.
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "common.hpp"
@@ -48,6 +49,27 @@ int trace_begin(const char *name, hipStream_t s)
 void trace_end(int slot, hipStream_t s)
 {
     if (slot >= 0) (void)hipEventRecord(g_trace.stop[slot], s);
+}
+
+int resident_blocks(const void *kernel, int block)
+{
+    struct Entry { const void *kernel; int device, block, blocks; };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) { (void)hipGetLastError(); return 2048; }
+    std::lock_guard<std::mutex> lock(mu);
+    for (const Entry &e : cache)
+        if (e.kernel == kernel && e.device == dev && e.block == block) return e.blocks;
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, 0) != hipSuccess ||
+        cus < 1 || per_cu < 1) {
+        (void)hipGetLastError();
+        return 2048;
+    }
+    cache.push_back(Entry{kernel, dev, block, cus * per_cu});
+    return cus * per_cu;
 }
 
 }  // namespace cogdl
