@@ -482,3 +482,67 @@ def test_gat_each_head_is_an_spmm_with_its_weights():
         Yh, _ = oracle.spmm(g.rowptr, g.col, alpha[:, h].copy(),
                             np.ascontiguousarray(X.reshape(70, H, D)[:, h, :]))
         assert np.array_equal(Y.reshape(90, H, D)[:, h, :], Yh)
+
+
+# ------------------------------------------------------------ GSpMM mean / max
+
+def test_gspmm_sum_is_spmm_and_mean_is_degree_normalized():
+    rng = np.random.default_rng(30)
+    for g in _graphs(5):
+        X = rng.standard_normal((g.n_cols, 5)).astype(np.float32)
+        Ys, As, _ = oracle.gspmm(g.rowptr, g.col, g.val, X, reduce="sum")
+        Y0, A0 = oracle.spmm(g.rowptr, g.col, g.val, X)
+        assert np.array_equal(Ys, Y0) and np.array_equal(As, A0)
+        Ym, Am, arg = oracle.gspmm(g.rowptr, g.col, g.val, X, reduce="mean")
+        assert arg is None
+        d = np.diff(g.rowptr).astype(np.float64)
+        want = (_dense(g) @ X.astype(np.float64)) / np.maximum(d, 1.0)[:, None]
+        np.testing.assert_allclose(Ym, want, rtol=1e-12, atol=1e-14)
+        # no edge values: the neighbour mean
+        Yn, _, _ = oracle.gspmm(g.rowptr, g.col, None, X, reduce="mean")
+        for i in range(g.n_rows):
+            b, e = g.rowptr[i], g.rowptr[i + 1]
+            w = X[g.col[b:e]].astype(np.float64).mean(0) if e > b else np.zeros(5)
+            np.testing.assert_allclose(Yn[i], w, rtol=1e-13, atol=1e-15)
+
+
+def test_gspmm_max_dense_masked_max():
+    """max_j fl32(W_ij * X_jf) over the pattern, with numpy's float32 product and
+    first-index argmax on graphs with sorted, distinct columns."""
+    rng = np.random.default_rng(31)
+    for n_rows, n_cols in ((40, 30), (7, 50), (60, 60)):
+        g = synth.random_csr(n_rows, n_cols, rng, mean_deg=5, empty_frac=0.15)
+        X = rng.standard_normal((n_cols, 6)).astype(np.float32)
+        Y, A, arg = oracle.gspmm(g.rowptr, g.col, g.val, X, reduce="max")
+        assert np.all(A == 0)
+        Wd = np.zeros((n_rows, n_cols), np.float32)
+        mask = np.zeros((n_rows, n_cols), bool)
+        rows = np.repeat(np.arange(n_rows), np.diff(g.rowptr))
+        Wd[rows, g.col] = g.val
+        mask[rows, g.col] = True
+        P = Wd[:, :, None] * X[None, :, :]                      # float32 products
+        P = np.where(mask[:, :, None], P, -np.inf)
+        jmax = np.argmax(P, axis=1)                             # first max in column order
+        empty = ~mask.any(1)
+        want = np.where(empty[:, None], 0.0, P.max(1).astype(np.float64))
+        assert np.array_equal(Y, want)
+        # the first maximal column of a sorted row is its first maximal edge
+        want_arg = np.where(empty[:, None], -1,
+                            g.rowptr[:-1, None] + np.array([[np.searchsorted(g.col[g.rowptr[i]:g.rowptr[i + 1]], jmax[i, f])
+                                                             for f in range(6)] for i in range(n_rows)]))
+        assert np.array_equal(arg, want_arg)
+
+
+def test_gspmm_max_ties_take_the_first_edge():
+    # row 0: the same column three times with equal weights -> the first edge
+    rowptr = np.array([0, 3, 5], np.int32)
+    col = np.array([1, 1, 1, 0, 1], np.int32)
+    val = np.array([2.0, 2.0, 2.0, -1.0, -1.0], np.float32)
+    X = np.array([[1.0, -3.0], [0.5, -0.25]], np.float32)
+    Y, _, arg = oracle.gspmm(rowptr, col, val, X, reduce="max")
+    assert Y.tolist() == [[1.0, -0.5], [-0.5, 3.0]]
+    assert arg.tolist() == [[0, 0], [4, 3]]
+    # no edge values: the plain neighbour max
+    Y, _, arg = oracle.gspmm(rowptr, col, None, X, reduce="max")
+    assert Y.tolist() == [[0.5, -0.25], [1.0, -0.25]]
+    assert arg.tolist() == [[0, 0], [3, 4]]
