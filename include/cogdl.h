@@ -67,6 +67,9 @@ typedef enum {
 
 typedef enum { COGDL_F32 = 0, COGDL_BF16 = 1, COGDL_F16 = 2 } cogdl_dtype;
 
+/* Reduce operation phi of Eq. 1 (section 2.2). */
+typedef enum { COGDL_REDUCE_SUM = 0, COGDL_REDUCE_MEAN = 1, COGDL_REDUCE_MAX = 2 } cogdl_reduce;
+
 /* Backend choice of the workload balancer (section 2.2, the balancer listing). */
 typedef enum {
     COGDL_BALANCE_AUTO = 0,            /* data-aware choice, see cogdl_plan_create */
@@ -155,6 +158,23 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         const int32_t *col, const float *val, int32_t F, const void *X,
                         cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype,
                         const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * GSpMM with a choice of reduce -- section 2.2, Eq. 1 (the user picks the
+ * reduce and compute operations; compute here is the multiplication by the
+ * edge value, or a copy of the neighbour feature when val is NULL):
+ *   SUM : Y[i, f] = sum_k val[k] * X[col[k], f]           (= cogdl_spmm)
+ *   MEAN: Y[i, f] = (1 / d_i) * sum_k val[k] * X[col[k], f], d_i = edges of row i
+ *   MAX : Y[i, f] = max_k val[k] * X[col[k], f] (products rounded to fp32), and
+ *         arg[i, f] = the first edge id k, in CSR order, attaining the max
+ * An empty row gives 0 (and arg -1).  arg: device int32 n_rows x F, written
+ * for MAX only, may be NULL.  MAX supports y_dtype equal to x_dtype or fp32
+ * (COGDL_ERR_DTYPE otherwise).  Other arguments as for cogdl_spmm.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                         const int32_t *col, const float *val, int32_t F, const void *X,
+                         cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, cogdl_reduce reduce,
+                         int32_t *arg, const cogdl_plan *plan, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * CSR -> CSC transpose of the graph structure, the setup of the backward

@@ -60,6 +60,8 @@ def lib():
     L.cogdl_plan_query.argtypes = [P, P, ctypes.POINTER(_PlanInfo)]
     L.cogdl_plan_units.argtypes = [P, P, i64, P]
     L.cogdl_spmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
+    L.cogdl_gspmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int,
+                              ctypes.c_int, P, P, P]
     L.cogdl_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_csr_to_csc_workspace.argtypes = [i32, i32, i64, ctypes.POINTER(sz)]
     L.cogdl_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P, sz, P]
@@ -70,7 +72,7 @@ def lib():
     L.cogdl_trace_count.restype = i32
     L.cogdl_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
     for name in ("cogdl_trace_enable", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
-                 "cogdl_plan_units", "cogdl_spmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
+                 "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -206,6 +208,36 @@ def spmm(rowptr, col, val, X, plan: Plan | None = None, out_dtype=None, out=None
                             _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), _plan_handle(plan),
                             _stream()), "cogdl_spmm")
     return out
+
+
+REDUCE = {"sum": 0, "mean": 1, "max": 2}
+
+
+def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, out_dtype=None,
+          out=None, return_arg: bool = False, arg=None):
+    """Eq. 1 with reduce = sum, mean or max over row i of val[k] * X[col[k]].
+
+    For max, ``return_arg`` also returns the int32 edge id of the first edge
+    attaining each output (-1 on empty rows); max keeps X's dtype or fp32."""
+    import torch
+    if reduce not in REDUCE:
+        raise ValueError(f"reduce must be one of {sorted(REDUCE)}")
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
+    _dev(val, "val", torch.float32), _dev(X, "X")
+    n_rows = rowptr.numel() - 1
+    F = X.shape[1] if X.dim() > 1 else 1
+    if out is None:
+        out = torch.empty((n_rows, F), dtype=out_dtype or X.dtype, device=X.device)
+    _dev(out, "out")
+    if return_arg and reduce != "max":
+        raise ValueError("return_arg needs reduce='max'")
+    if return_arg and arg is None:
+        arg = torch.empty((n_rows, F), dtype=torch.int32, device=X.device)
+    _dev(arg, "arg", torch.int32)
+    _check(lib().cogdl_gspmm(n_rows, X.shape[0], col.numel(), _ptr(rowptr), _ptr(col), _ptr(val), F,
+                             _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), REDUCE[reduce],
+                             _ptr(arg), _plan_handle(plan), _stream()), "cogdl_gspmm")
+    return (out, arg) if return_arg else out
 
 
 def csr_to_csc_workspace(n_rows: int, n_cols: int, nnz: int) -> int:

@@ -688,7 +688,7 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     }
     if (!P) return COGDL_OK;
 
-    if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, stream);
+    if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, false, stream);
     const int64_t rblocks = P->cap_split < 4096 ? P->cap_split : 4096;
     const unsigned rb = (unsigned)(rblocks < 1 ? 1 : rblocks);
     const bool v4 = D % 4 == 0 && (uintptr_t)Y % (4 * dtype_bytes(y_dtype)) == 0;

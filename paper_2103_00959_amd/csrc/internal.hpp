@@ -33,7 +33,7 @@ struct Plan {
 
     int4 *units = nullptr;        // [cap_units] execution order
     int4 *units_tmp = nullptr;    // [cap_units] row order (build scratch)
-    int4 *split_rows = nullptr;   // [cap_split] {row, first partial slot, #slots, 0}
+    int4 *split_rows = nullptr;   // [cap_split] {row, first partial slot, #slots, degree}
     int4 *part_units = nullptr;   // [cap_partials] {row, beg, end, split index}
     int32_t *row_units = nullptr; // [n_rows + 1] exclusive scan; [n_rows] = #units
     int32_t *row_parts = nullptr; // [n_rows + 1]; [n_rows] = #partial slots
@@ -47,6 +47,7 @@ struct Plan {
     void *scan_ws = nullptr;
     size_t scan_ws_bytes = 0;
     float *partials = nullptr;    // [cap_partials * max_feat]
+    int32_t *parg = nullptr;      // [cap_partials * max_feat] edge ids of partial maxima
     float *gstats = nullptr;      // [cap_partials * max_heads * 2] per-group (m, z)
     float *rstats = nullptr;      // [cap_split * max_heads * 2] per-split-row (m, z)
 
@@ -66,9 +67,10 @@ const Plan *plan_of(const cogdl_plan *h);
 // (all compute units), cached per kernel.
 int resident_blocks(const void *kernel, int block);
 
-// Y[row] = sum of the partial rows of every split row of the plan (F columns).
+// Y[row] = sum of the partial rows of every split row of the plan (F columns),
+// divided by the row's degree when `mean`.
 cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                               hipStream_t s);
+                               bool mean, hipStream_t s);
 
 // Kernel tracing hooks (no-ops unless cogdl_trace_enable was called).
 int trace_begin(const char *name, hipStream_t s);

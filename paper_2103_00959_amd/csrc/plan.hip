@@ -89,7 +89,7 @@ __global__ void k_plan_emit(const int32_t *__restrict__ rowptr, int32_t n_rows, 
     }
     const int p0 = row_parts[i];
     const int s = row_split[i];
-    split_rows[s] = make_int4(i, p0, nu, 0);
+    split_rows[s] = make_int4(i, p0, nu, end - beg);
     for (int g = 0; g < nu; ++g) {
         const int b = beg + g * G;
         const int e = (end - b > G) ? b + G : end;
@@ -251,6 +251,7 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
     P.scan_ws_bytes = cogdl::scan_workspace_bytes(n_rows);
     const size_t o_scan_ws = take(P.scan_ws_bytes);
     const size_t o_partials = take(sizeof(float) * (size_t)P.cap_partials * pstride);
+    const size_t o_parg = take(sizeof(int32_t) * (size_t)P.cap_partials * pstride);
     const size_t o_gstats = take(sizeof(float) * 2 * (size_t)P.cap_partials * max_heads);
     const size_t o_rstats = take(sizeof(float) * 2 * (size_t)P.cap_split * max_heads);
     P.bytes = off;
@@ -273,6 +274,7 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
     P.sort_ws = b + o_sort_ws;
     P.scan_ws = b + o_scan_ws;
     P.partials = reinterpret_cast<float *>(b + o_partials);
+    P.parg = reinterpret_cast<int32_t *>(b + o_parg);
     P.gstats = reinterpret_cast<float *>(b + o_gstats);
     P.rstats = reinterpret_cast<float *>(b + o_rstats);
 

@@ -1,5 +1,6 @@
-// Generalized SpMM of section 2.2, Eq. 1 with reduce = sum and compute =
-// multiply (H' = A H), and the transposed product A^T G of its backward pass.
+// Generalized SpMM of section 2.2, Eq. 1 (H' = A H with reduce = sum, mean or
+// max and compute = multiply by the edge value), and the transposed product
+// A^T G of its backward pass.
 //
 // Mapping on gfx950 (64-lane wavefronts):
 //   - A work unit (a whole row, or a neighbour group of a long row) belongs to
@@ -13,8 +14,9 @@
 //     neighbour row (one 16-byte load) and accumulates in fp32 registers; U
 //     edges are unrolled so that U row gathers are in flight per lane.
 //   - A unit that covers a whole row writes the output row once; a neighbour
-//     group writes an fp32 partial row, and a second kernel adds the partials
-//     of each split row in a fixed order (no floating-point atomics).
+//     group writes an fp32 partial row (for max also the edge id of each
+//     partial maximum), and a second kernel combines the partials of each
+//     split row in a fixed order (no floating-point atomics).
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -33,12 +35,15 @@ struct SpmmArgs {
     const float *val;           // nullptr: all ones
     const void *X;
     void *Y;
+    int32_t *arg;               // max: edge id of each output maximum (nullable)
     float *partials;
+    int32_t *parg;              // max: edge id of each partial maximum
     int64_t pstride;
     int64_t F;
     uint64_t x_bytes;           // size of X, bounds the buffer gathers
     int32_t slab;
     int32_t log2S;
+    int32_t mean;               // sum / mean: divide whole rows by their degree
 };
 
 // Descriptor {row, first edge, end edge, partial slot} of unit u (an empty
@@ -51,10 +56,31 @@ __device__ __forceinline__ int4 fetch_unit(const SpmmArgs &a, int64_t u, int64_t
     return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
 }
 
-template <typename TX, typename TY, int VEC, int CH, bool BUF>
+// Stores N edge ids (16-byte stores when N is a multiple of four; the offsets
+// and the base are then 16-byte aligned).
+template <int N>
+__device__ __forceinline__ void store_ids(int32_t *__restrict__ p, int64_t i, const int32_t (&v)[N])
+{
+    if constexpr (N % 4 == 0) {
+#pragma unroll
+        for (int e = 0; e < N; e += 4)
+            *reinterpret_cast<int4 *>(p + i + e) = make_int4(v[e], v[e + 1], v[e + 2], v[e + 3]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) p[i + e] = v[e];
+    }
+}
+
+// MAXR = false: sum of products (mean scales whole rows by 1 / degree);
+// MAXR = true: maximum of the products, edges taken in CSR order, the first
+// edge kept unconditionally and a later one only if strictly greater, so the
+// recorded edge is the first that attains the maximum.
+template <typename TX, typename TY, int VEC, int CH, bool BUF, bool MAXR>
 __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
 {
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
+    constexpr int AC = MAXR ? CH : 1;
+    constexpr int AV = MAXR ? VEC : 1;
     const int log2S = a.log2S;
     const int S = 1 << log2S;
     const int lane = lane_id();
@@ -100,10 +126,15 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
         const int4 dn = fetch_unit(a, un, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
         float acc[CH][VEC];
+        int32_t am[AC][AV];
 #pragma unroll
         for (int c = 0; c < CH; ++c)
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
+#pragma unroll
+        for (int c = 0; c < AC; ++c)
+#pragma unroll
+            for (int e = 0; e < AV; ++e) am[c][e] = -1;
 
         const int last = end - 1;
         for (int k0 = beg; k0 < end; k0 += S) {
@@ -128,12 +159,27 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
 #pragma unroll
                     for (int c = 0; c < CH; ++c)
                         X.load((int64_t)cc[t] * a.F + fe[c], ok[t] && act[c], xv[t][c]);
+                if constexpr (MAXR) {
 #pragma unroll
-                for (int t = 0; t < U; ++t)
+                    for (int t = 0; t < U; ++t)
 #pragma unroll
-                    for (int c = 0; c < CH; ++c)
+                        for (int c = 0; c < CH; ++c)
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(vv[t], xv[t][c][e], acc[c][e]);
+                            for (int e = 0; e < VEC; ++e) {
+                                const float p = vv[t] * xv[t][c][e];
+                                const bool take = ok[t] && (am[c][e] < 0 || p > acc[c][e]);
+                                acc[c][e] = take ? p : acc[c][e];
+                                am[c][e] = take ? k0 + j + t : am[c][e];
+                            }
+                } else {
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+#pragma unroll
+                        for (int c = 0; c < CH; ++c)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e)
+                                acc[c][e] = fmaf(vv[t], xv[t][c][e], acc[c][e]);
+                }
             }
             c_cur = c_nxt;
             v_cur = v_nxt;
@@ -147,13 +193,29 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
         }
         if (part < 0) {
             TY *__restrict__ Y = static_cast<TY *>(a.Y);
+            if (!MAXR && a.mean && end > beg) {
+                const float r = 1.f / (float)(end - beg);
 #pragma unroll
-            for (int c = 0; c < CH; ++c)
-                if (act[c]) store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
+                for (int c = 0; c < CH; ++c)
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
+            }
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                if (!act[c]) continue;
+                store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
+                if constexpr (MAXR) {
+                    if (a.arg) store_ids<VEC>(a.arg, (int64_t)row * a.F + fe[c], am[c]);
+                }
+            }
         } else {
 #pragma unroll
-            for (int c = 0; c < CH; ++c)
-                if (act[c]) store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+            for (int c = 0; c < CH; ++c) {
+                if (!act[c]) continue;
+                store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+                if constexpr (MAXR)
+                    store_ids<VEC>(a.parg, (int64_t)part * a.pstride + fe[c], am[c]);
+            }
         }
         if (un >= hi) break;
         u = un;
@@ -161,16 +223,18 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
     }
 }
 
-// Y[row, :] = sum of the row's partial rows.  One workgroup per split row
-// (grid-stride over the device-side count, uniform per workgroup): wavefront
-// w adds the slots g = w, w + 4, ... in increasing order on two interleaved
-// chains, VEC features per lane, and the four wavefront sums are added in
-// wavefront order through LDS, so the result does not depend on timing.
+// Y[row, :] = sum of the row's partial rows (times 1 / degree for mean).  One
+// workgroup per split row (grid-stride over the device-side count, uniform
+// per workgroup): wavefront w adds the slots g = w, w + 4, ... in increasing
+// order on two interleaved chains, VEC features per lane, and the four
+// wavefront sums are added in wavefront order through LDS, so the result does
+// not depend on timing.
 template <typename TY, int VEC>
 __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__ split_rows,
                                                         const int32_t *__restrict__ n_split,
                                                         const float *__restrict__ partials,
-                                                        int64_t pstride, int64_t F, TY *__restrict__ Y)
+                                                        int64_t pstride, int64_t F, int mean,
+                                                        TY *__restrict__ Y)
 {
     constexpr int kW = kBlock / kWave;
     __shared__ float red[kW][kWave * VEC];
@@ -181,6 +245,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
         const int4 d = split_rows[s];
         const int64_t row = d.x, p0 = d.y;
         const int np = d.z;
+        const float scale = (mean && d.w > 0) ? 1.f / (float)d.w : 1.f;
         for (int64_t fb = 0; fb < F; fb += kWave * VEC) {
             const int64_t f = fb + (int64_t)lane * VEC;
             const bool act = f < F;
@@ -214,6 +279,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
                     v[e] = red[0][lane * VEC + e];
 #pragma unroll
                     for (int i = 1; i < kW; ++i) v[e] += red[i][lane * VEC + e];
+                    if (mean) v[e] *= scale;
                 }
                 store_out<TY, VEC>(Y, row * F + f, v);
             }
@@ -222,61 +288,124 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
     }
 }
 
+// Max over a split row's partial maxima, slots in edge order: the first slot
+// is kept and a later one only if strictly greater, which keeps the first
+// edge attaining the row maximum.  One wavefront per split row, one feature
+// per lane (split rows are few; the slots of a row are contiguous, so each
+// wavefront reads whole 256-byte lines).
+template <typename TY>
+__global__ __launch_bounds__(kBlock) void k_spmm_reduce_max(const int4 *__restrict__ split_rows,
+                                                            const int32_t *__restrict__ n_split,
+                                                            const float *__restrict__ partials,
+                                                            const int32_t *__restrict__ parg,
+                                                            int64_t pstride, int64_t F,
+                                                            TY *__restrict__ Y,
+                                                            int32_t *__restrict__ arg)
+{
+    const int lane = lane_id();
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t ns = *n_split;
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns;
+         s += waves) {
+        const int4 d = split_rows[s];
+        for (int64_t f = lane; f < F; f += kWave) {
+            float best = 0.f;
+            int32_t bk = -1;
+            for (int g = 0; g < d.z; ++g) {
+                const int64_t q = (int64_t)(d.y + g) * pstride + f;
+                const float v = partials[q];
+                if (bk < 0 || v > best) { best = v; bk = parg[q]; }
+            }
+            const float out[1] = {best};
+            store_out<TY, 1>(Y, (int64_t)d.x * F + f, out);
+            if (arg) arg[(int64_t)d.x * F + f] = bk;
+        }
+    }
+}
+
 using SpmmKernel = void (*)(SpmmArgs);
 
-template <typename TX, typename TY, bool BUF>
+template <typename TX, typename TY, bool BUF, bool MAXR>
 SpmmKernel pick_kernel(int vec, int ch)
 {
     constexpr int V = (int)(16 / sizeof(TX));
     if (vec == 1) {
-        if (ch == 1) return k_spmm<TX, TY, 1, 1, BUF>;
-        if (ch == 2) return k_spmm<TX, TY, 1, 2, BUF>;
-        return k_spmm<TX, TY, 1, 4, BUF>;
+        if (ch == 1) return k_spmm<TX, TY, 1, 1, BUF, MAXR>;
+        if (ch == 2) return k_spmm<TX, TY, 1, 2, BUF, MAXR>;
+        return k_spmm<TX, TY, 1, 4, BUF, MAXR>;
     }
-    if (ch == 1) return k_spmm<TX, TY, V, 1, BUF>;
-    if (ch == 2) return k_spmm<TX, TY, V, 2, BUF>;
-    return k_spmm<TX, TY, V, 4, BUF>;
+    if (ch == 1) return k_spmm<TX, TY, V, 1, BUF, MAXR>;
+    if (ch == 2) return k_spmm<TX, TY, V, 2, BUF, MAXR>;
+    return k_spmm<TX, TY, V, 4, BUF, MAXR>;
 }
 
+// Max outputs keep the input format or widen it to fp32 (each output is one
+// fp32 product rounded once); the caller rejects other pairs.
 template <typename TX, bool BUF>
-SpmmKernel pick_y(int ydt, int vec, int ch)
+SpmmKernel pick_y(int ydt, int vec, int ch, bool maxr)
 {
-    if (ydt == COGDL_F32) return pick_kernel<TX, float, BUF>(vec, ch);
-    if (ydt == COGDL_BF16) return pick_kernel<TX, bf16_t, BUF>(vec, ch);
-    return pick_kernel<TX, f16_t, BUF>(vec, ch);
+    if (maxr) {
+        if (ydt == COGDL_F32) return pick_kernel<TX, float, BUF, true>(vec, ch);
+        return pick_kernel<TX, TX, BUF, true>(vec, ch);
+    }
+    if (ydt == COGDL_F32) return pick_kernel<TX, float, BUF, false>(vec, ch);
+    if (ydt == COGDL_BF16) return pick_kernel<TX, bf16_t, BUF, false>(vec, ch);
+    return pick_kernel<TX, f16_t, BUF, false>(vec, ch);
 }
 
 template <bool BUF>
-SpmmKernel pick_x(int xdt, int ydt, int vec, int ch)
+SpmmKernel pick_x(int xdt, int ydt, int vec, int ch, bool maxr)
 {
-    if (xdt == COGDL_F32) return pick_y<float, BUF>(ydt, vec, ch);
-    if (xdt == COGDL_BF16) return pick_y<bf16_t, BUF>(ydt, vec, ch);
-    return pick_y<f16_t, BUF>(ydt, vec, ch);
+    if (xdt == COGDL_F32) return pick_y<float, BUF>(ydt, vec, ch, maxr);
+    if (xdt == COGDL_BF16) return pick_y<bf16_t, BUF>(ydt, vec, ch, maxr);
+    return pick_y<f16_t, BUF>(ydt, vec, ch, maxr);
 }
 
-SpmmKernel pick(int xdt, int ydt, int vec, int ch, bool buf)
+SpmmKernel pick(int xdt, int ydt, int vec, int ch, bool buf, bool maxr)
 {
-    return buf ? pick_x<true>(xdt, ydt, vec, ch) : pick_x<false>(xdt, ydt, vec, ch);
+    return buf ? pick_x<true>(xdt, ydt, vec, ch, maxr) : pick_x<false>(xdt, ydt, vec, ch, maxr);
 }
 
 template <int VEC>
 cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                             hipStream_t s)
+                             bool mean, hipStream_t s)
 {
     const int64_t pstride = (P.max_feat + 7) / 8 * 8;
     int64_t blocks = P.cap_split;
     if (blocks > 4096) blocks = 4096;
     if (blocks < 1) blocks = 1;
     const unsigned b = (unsigned)blocks;
+    const int mn = mean ? 1 : 0;
     if (ydt == COGDL_F32)
         COGDL_LAUNCH(name, (k_spmm_reduce<float, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, pstride, F, static_cast<float *>(Y));
+                     P.partials, pstride, F, mn, static_cast<float *>(Y));
     else if (ydt == COGDL_BF16)
         COGDL_LAUNCH(name, (k_spmm_reduce<bf16_t, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, pstride, F, static_cast<bf16_t *>(Y));
+                     P.partials, pstride, F, mn, static_cast<bf16_t *>(Y));
     else
         COGDL_LAUNCH(name, (k_spmm_reduce<f16_t, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, pstride, F, static_cast<f16_t *>(Y));
+                     P.partials, pstride, F, mn, static_cast<f16_t *>(Y));
+    return COGDL_OK;
+}
+
+cogdl_status max_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
+                               int32_t *arg, hipStream_t s)
+{
+    const int64_t pstride = (P.max_feat + 7) / 8 * 8;
+    constexpr int wpb = kBlock / kWave;
+    int64_t blocks = (P.cap_split + wpb - 1) / wpb;
+    if (blocks > 2048) blocks = 2048;
+    if (blocks < 1) blocks = 1;
+    const unsigned b = (unsigned)blocks;
+    if (ydt == COGDL_F32)
+        COGDL_LAUNCH(name, k_spmm_reduce_max<float>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+                     P.partials, P.parg, pstride, F, static_cast<float *>(Y), arg);
+    else if (ydt == COGDL_BF16)
+        COGDL_LAUNCH(name, k_spmm_reduce_max<bf16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+                     P.partials, P.parg, pstride, F, static_cast<bf16_t *>(Y), arg);
+    else
+        COGDL_LAUNCH(name, k_spmm_reduce_max<f16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
+                     P.partials, P.parg, pstride, F, static_cast<f16_t *>(Y), arg);
     return COGDL_OK;
 }
 
@@ -285,25 +414,33 @@ cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y
 // Four features per lane when the rows allow 16-byte partial loads and
 // aligned output stores, one otherwise.
 cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                               hipStream_t s)
+                               bool mean, hipStream_t s)
 {
     const int ybytes = dtype_bytes(ydt);
     if (F % 4 == 0 && (uintptr_t)Y % (4 * ybytes) == 0)
-        return reduce_launch_v<4>(name, P, F, Y, ydt, s);
-    return reduce_launch_v<1>(name, P, F, Y, ydt, s);
+        return reduce_launch_v<4>(name, P, F, Y, ydt, mean, s);
+    return reduce_launch_v<1>(name, P, F, Y, ydt, mean, s);
 }
 
 namespace {
 
-// Shared body of cogdl_spmm and cogdl_spmm_t: out_rows x F output, gathering
-// rows of an in_rows x F input through (ptr, idx, w).
+struct LaunchNames {
+    const char *main, *tiny, *reduce;
+};
+
+// Shared body of the SpMM entry points: out_rows x F output, gathering rows of
+// an in_rows x F input through (ptr, idx, w), combined by `reduce`.
 cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const int32_t *ptr,
                          const int32_t *idx, const float *w, int32_t F, const void *X, int xdt,
-                         void *Y, int ydt, const cogdl_plan *plan_h, hipStream_t s,
-                         const char *name, const char *tiny_name, const char *reduce_name)
+                         void *Y, int ydt, int reduce, int32_t *arg, const cogdl_plan *plan_h,
+                         hipStream_t s, LaunchNames names)
 {
     if (out_rows < 0 || in_rows < 0 || nnz < 0 || F < 0) return COGDL_ERR_INVALID;
+    if (reduce != COGDL_REDUCE_SUM && reduce != COGDL_REDUCE_MEAN && reduce != COGDL_REDUCE_MAX)
+        return COGDL_ERR_INVALID;
     if (!dtype_ok(xdt) || !dtype_ok(ydt)) return COGDL_ERR_DTYPE;
+    const bool maxr = reduce == COGDL_REDUCE_MAX;
+    if (maxr && ydt != COGDL_F32 && ydt != xdt) return COGDL_ERR_DTYPE;
     if (nnz > INT32_MAX) return COGDL_ERR_TOO_LARGE;
     if (out_rows > 0 && !ptr) return COGDL_ERR_INVALID;
     if (nnz > 0 && (!idx || out_rows == 0 || in_rows == 0)) return COGDL_ERR_INVALID;
@@ -313,7 +450,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     if (P && (P->n_rows != out_rows || P->nnz != nnz || P->max_feat < F)) return COGDL_ERR_PLAN;
     if (out_rows == 0 || F == 0) return COGDL_OK;
 
-    const bool aligned = ((uintptr_t)X % 16 == 0) && ((uintptr_t)Y % 16 == 0);
+    const bool aligned = ((uintptr_t)X % 16 == 0) && ((uintptr_t)Y % 16 == 0) &&
+                         (!maxr || !arg || (uintptr_t)arg % 16 == 0);
     const RowMap m = row_map(F, dtype_bytes(xdt), F, aligned);
     SpmmArgs a;
     a.units = P ? P->units : nullptr;
@@ -325,12 +463,15 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     a.val = w;
     a.X = X;
     a.Y = Y;
+    a.arg = maxr ? arg : nullptr;
     a.partials = P ? P->partials : nullptr;
+    a.parg = P ? P->parg : nullptr;
     a.pstride = P ? (P->max_feat + 7) / 8 * 8 : 0;
     a.F = F;
     a.x_bytes = (uint64_t)in_rows * (uint64_t)F * (uint64_t)dtype_bytes(xdt);
     a.slab = m.slab;
     a.log2S = m.log2S;
+    a.mean = reduce == COGDL_REDUCE_MEAN ? 1 : 0;
     const bool buf = a.x_bytes <= kBufferMaxBytes;
     const int64_t units = P ? P->cap_units : out_rows;
     // Units of at most kTinyUnit edges (the sorted tail) run with S/4 lanes and
@@ -339,12 +480,12 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     if (tiny) a.u_hi = P->n_big_dev();
     {
         const int64_t upb = kBlock >> m.log2S;
-        SpmmKernel k = pick(xdt, ydt, m.vec, m.ch, buf);
+        SpmmKernel k = pick(xdt, ydt, m.vec, m.ch, buf, maxr);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(name, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock, s,
-                     a);
+        COGDL_LAUNCH(names.main, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
+                     kBlock, s, a);
     }
     if (tiny) {
         SpmmArgs b = a;
@@ -352,15 +493,16 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
         b.u_hi = P->n_units_dev();
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
-        SpmmKernel k = pick(xdt, ydt, m.vec, 4, buf);
+        SpmmKernel k = pick(xdt, ydt, m.vec, 4, buf, maxr);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(tiny_name, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
+        COGDL_LAUNCH(names.tiny, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
                      kBlock, s, b);
     }
-    if (P) return sum_reduce_launch(reduce_name, *P, F, Y, ydt, s);
-    return COGDL_OK;
+    if (!P) return COGDL_OK;
+    if (maxr) return max_reduce_launch(names.reduce, *P, F, Y, ydt, a.arg, s);
+    return sum_reduce_launch(names.reduce, *P, F, Y, ydt, a.mean != 0, s);
 }
 
 }  // namespace
@@ -374,7 +516,18 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         hipStream_t stream)
 {
     return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
-                              (int)y_dtype, plan, stream, "spmm", "spmm_tiny", "spmm_reduce");
+                              (int)y_dtype, COGDL_REDUCE_SUM, nullptr, plan, stream,
+                              {"spmm", "spmm_tiny", "spmm_reduce"});
+}
+
+cogdl_status cogdl_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                         const int32_t *col, const float *val, int32_t F, const void *X,
+                         cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, cogdl_reduce reduce,
+                         int32_t *arg, const cogdl_plan *plan, hipStream_t stream)
+{
+    return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
+                              (int)y_dtype, (int)reduce, arg, plan, stream,
+                              {"gspmm", "gspmm_tiny", "gspmm_reduce"});
 }
 
 cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *colptr,
@@ -384,7 +537,8 @@ cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int
 {
     // A^T has n_cols rows, each gathering rows of the n_rows x F input G.
     return cogdl::spmm_common(n_cols, n_rows, nnz, colptr, row_t, val_t, F, G, (int)g_dtype, dX,
-                              (int)dx_dtype, plan_t, stream, "spmm_t", "spmm_t_tiny", "spmm_t_reduce");
+                              (int)dx_dtype, COGDL_REDUCE_SUM, nullptr, plan_t, stream,
+                              {"spmm_t", "spmm_t_tiny", "spmm_t_reduce"});
 }
 
 }  // extern "C"

@@ -72,6 +72,23 @@ def test_spmm_validation(L):
     assert L.cogdl_spmm(3, 5, 7, FAKE, FAKE, None, 0, None, 0, None, 0, None, None) == OK
 
 
+def test_gspmm_validation(L):
+    G = L.cogdl_gspmm
+    # reduce codes outside sum / mean / max
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 3, None, None, None) == INVALID
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, -1, None, None, None) == INVALID
+    # max keeps the input format or widens to fp32: bf16 -> fp16 is refused
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 1, FAKE, 2, 2, None, None, None) == DTYPE
+    # fp32 -> bf16 is refused for max, but not for sum / mean (those fail later, on nulls)
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 1, 2, None, None, None) == DTYPE
+    assert G(2, 2, 3, FAKE, None, None, 4, FAKE, 0, FAKE, 1, 1, None, None, None) == INVALID
+    # the checks shared with cogdl_spmm
+    assert G(-1, 1, 0, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 1, None, None, None) == INVALID
+    assert G(2, 2, 1 << 31, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 2, None, None, None) == TOO_LARGE
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, None, 0, FAKE, 0, 2, None, None, None) == INVALID
+    assert G(0, 5, 0, None, None, None, 4, None, 0, None, 0, 2, None, None, None) == OK
+
+
 def test_spmm_t_validation(L):
     assert L.cogdl_spmm_t(3, -2, 0, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == INVALID
     assert L.cogdl_spmm_t(3, 2, 5, FAKE, FAKE, None, 4, FAKE, 7, FAKE, 0, None, None) == DTYPE

@@ -162,6 +162,102 @@ def test_spmm_deterministic(cg):
         plan.close()
 
 
+# ---------------------------------------------------------------- GSpMM mean / max
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1", "empty"])
+@pytest.mark.parametrize("plan_spec", PLANS)
+def test_gspmm_mean(cg, kind, plan_spec):
+    import torch
+    g = _graph(kind)
+    say(f"gspmm mean {kind} plan={plan_spec} n={g.n_rows} nnz={g.nnz}")
+    rp, cl, vl = graph_to_dev(g)
+    for F, xk in ((3, "f32"), (64, "f32"), (128, "bf16")):
+        xh, xc, xd = features((g.n_cols, F), 31 + F, xk)
+        plan = _make_plan(cg, rp, g.nnz, plan_spec, F)
+        try:
+            Y = cg.gspmm(rp, cl, vl, xd, "mean", plan=plan, out_dtype=torch.float32)
+            Yr, Ar, _ = oracle.gspmm(g.rowptr, g.col, g.val, xh, "mean", n_cols=g.n_cols, x_dtype=xc)
+            err = scaled_error(Y, Yr, Ar)
+            assert err <= TOL_F32, (kind, plan_spec, F, err)
+            if g.n_rows:
+                empty = np.flatnonzero(np.diff(g.rowptr) == 0)
+                assert float(Y[dev(empty).long()].abs().max() if empty.size else 0.0) == 0.0
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+def _check_max(cg, g, rp, cl, vl, val_h, F, xk, yk, plan, seed):
+    """Max values equal the oracle's maximum product rounded once to the output
+    format, and the edge ids equal the oracle's (first edge attaining it)."""
+    import torch
+    xh, xc, xd = features((g.n_cols, F), seed, xk)
+    out_dtype = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[yk]
+    Y, arg = cg.gspmm(rp, cl, vl, xd, "max", plan=plan, out_dtype=out_dtype, return_arg=True)
+    Yr, _, ar = oracle.gspmm(g.rowptr, g.col, val_h, xh, "max", n_cols=g.n_cols, x_dtype=xc)
+    code = {"f32": oracle.F32, "bf16": oracle.BF16, "f16": oracle.F16}[yk]
+    want = oracle.decode(oracle.round_to(Yr, code), code)
+    got = to_f64(Y).reshape(Yr.shape)
+    assert np.array_equal(got, want.reshape(Yr.shape)), (xk, yk, F)
+    assert np.array_equal(arg.cpu().numpy().reshape(ar.shape), ar), (xk, yk, F)
+    # the value-only call (no edge ids) gives the same outputs
+    Y2 = cg.gspmm(rp, cl, vl, xd, "max", plan=plan, out_dtype=out_dtype)
+    assert torch.equal(Y2.view(torch.int16) if yk != "f32" else Y2,
+                       Y.view(torch.int16) if yk != "f32" else Y)
+
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1", "empty"])
+@pytest.mark.parametrize("plan_spec", PLANS)
+def test_gspmm_max_bit_exact(cg, kind, plan_spec):
+    g = _graph(kind)
+    say(f"gspmm max {kind} plan={plan_spec} n={g.n_rows} nnz={g.nnz}")
+    rp, cl, vl = graph_to_dev(g)
+    for F, xk, yk in ((1, "f32", "f32"), (64, "f32", "f32"), (128, "bf16", "bf16"), (24, "f16", "f32")):
+        plan = _make_plan(cg, rp, g.nnz, plan_spec, F)
+        try:
+            _check_max(cg, g, rp, cl, vl, g.val, F, xk, yk, plan, 41 + F)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+@pytest.mark.parametrize("F", [7, 256, 1000])
+def test_gspmm_max_ties_first_edge(cg, F):
+    """Without edge values, duplicate columns and small-integer features tie
+    often: the recorded edge must be the first in CSR order, in whole rows and
+    across the neighbour groups of split rows."""
+    import torch
+    g = _graph("dups", seed=21)
+    deg = np.diff(g.rowptr)
+    rp, cl = dev(g.rowptr), dev(g.col)
+    xi = np.random.default_rng(5).integers(-2, 3, size=(g.n_cols, F)).astype(np.float32)
+    Yr, _, ar = oracle.gspmm(g.rowptr, g.col, None, xi, "max")
+    assert (deg > 1).any()
+    for spec in (None, ("neighbor_group", 3), ("neighbor_group", 4)):
+        plan = _make_plan(cg, rp, g.nnz, spec, F)
+        try:
+            Y, arg = cg.gspmm(rp, cl, None, dev(xi), "max", plan=plan, return_arg=True)
+            assert np.array_equal(to_f64(Y), Yr), spec
+            assert np.array_equal(arg.cpu().numpy(), ar), spec
+            assert int(torch.sum(arg < 0)) == int(np.sum(deg == 0)) * F
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+def test_gspmm_sum_matches_spmm_bit_exact(cg):
+    import torch
+    g = _graph("hubs", seed=13)
+    rp, cl, vl = graph_to_dev(g)
+    _, _, xd = features((g.n_cols, 64), 3, "f32")
+    plan = cg.Plan(rp, g.nnz, 64)
+    try:
+        assert torch.equal(cg.gspmm(rp, cl, vl, xd, "sum", plan=plan), cg.spmm(rp, cl, vl, xd, plan=plan))
+        assert torch.equal(cg.gspmm(rp, cl, vl, xd, "sum"), cg.spmm(rp, cl, vl, xd))
+    finally:
+        plan.close()
+
+
 # ---------------------------------------------------------------- plan
 
 @pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1", "empty"])
