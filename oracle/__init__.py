@@ -52,7 +52,7 @@ def _load():
     lib.oracle_neighbor_groups.argtypes = [i32, P, i32, i32, P]
     lib.oracle_neighbor_groups.restype = i64
     lib.oracle_spmm.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, P, P, P]
-    lib.oracle_gspmm.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, i32, P, P, P, P]
+    lib.oracle_gspmm.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, i32, i32, P, P, P, P]
     lib.oracle_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P]
     lib.oracle_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, P, P, P]
     lib.oracle_edge_softmax.argtypes = [i32, i32, i64, P, P, i32, P, P, dbl, i32, P, P]
@@ -144,11 +144,13 @@ def spmm(rowptr, col, val, X, n_cols=None, x_dtype=None, rows=None):
 
 
 REDUCE = {"sum": 0, "mean": 1, "max": 2}
+COMPUTE = {"mul": 0, "add": 1, "sub": 2, "copy": 3}
 
 
-def gspmm(rowptr, col, val, X, reduce="sum", n_cols=None, x_dtype=None, rows=None):
-    """Eq. 1 with a sum / mean / max reduce.  Returns (Y, Abs, arg); arg is the
-    first edge attaining the max (-1 for empty rows), None for sum / mean."""
+def gspmm(rowptr, col, val, X, reduce="sum", n_cols=None, x_dtype=None, rows=None, compute="mul"):
+    """Eq. 1 with a sum / mean / max reduce and a mul / add / sub / copy message.
+    Returns (Y, Abs, arg); arg is the first edge attaining the max (-1 for empty
+    rows), None for sum / mean."""
     rp, cl, vl = _c(rowptr, np.int32), _c(col, np.int32), _c(val, np.float32)
     X = np.ascontiguousarray(X)
     n_rows = rp.size - 1
@@ -160,7 +162,7 @@ def gspmm(rowptr, col, val, X, reduce="sum", n_cols=None, x_dtype=None, rows=Non
     A = np.empty((n_out, F), dtype=np.float64)
     arg = np.empty((n_out, F), dtype=np.int32) if reduce == "max" else None
     rc = _load().oracle_gspmm(n_rows, n_cols, int(rp[-1]) if n_rows else 0, _p(rp), _p(cl), _p(vl),
-                              F, _p(X), _x_code(X, x_dtype), REDUCE[reduce],
+                              F, _p(X), _x_code(X, x_dtype), REDUCE[reduce], COMPUTE[compute],
                               0 if sel is None else sel.size, _p(sel), _p(Y), _p(A), _p(arg))
     _check(rc, "gspmm")
     return Y, A, arg

@@ -204,58 +204,71 @@ int oracle_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowp
     return 0;
 }
 
-/* ------------------------------------------------ GSpMM reduce variants */
+/* ------------------------------------------------ GSpMM reduce / compute */
 
-/* Eq. 1 with compute = multiply by the edge value (copy of X when val is
- * NULL) and reduce = sum (0), mean (1) or max (2):
- *   sum : Y[i,f] = sum_k w_k x_kf
- *   mean: Y[i,f] = (1/d_i) sum_k w_k x_kf          (d_i = number of edges of row i)
- *   max : Y[i,f] = max_k fl32(w_k * x_kf),  arg[i,f] = the first k (CSR order)
- *         attaining it
- * An empty row gives 0 (and arg -1).  The max compares the products as the
- * fp32 values a GPU multiply produces (the product of two floats rounded once
- * to float), so the chosen edge is decided in the kernel's precision; its
- * value is then exact.  Abs is the error scale of sum / mean (0 for max). */
+/* The message of edge k for feature f under the compute operator psi of
+ * Eq. 1, with w = val[k] (1 when val is NULL): multiply (0) w * x, add (1)
+ * x + w, subtract (2) x - w, copy (3) x.  Evaluated in double. */
+static double gspmm_message(int32_t compute, double w, double x)
+{
+    switch (compute) {
+    case 0: return w * x;
+    case 1: return x + w;
+    case 2: return x - w;
+    default: return x;
+    }
+}
+
+/* Eq. 1 with compute psi (above) and reduce phi = sum (0), mean (1) or
+ * max (2) over the edges of row i:
+ *   sum : Y[i,f] = sum_k m_kf                    Abs[i,f] = sum_k |m_kf|
+ *   mean: Y[i,f] = (1/d_i) sum_k m_kf            Abs scaled the same way
+ *         (d_i = number of edges of row i, duplicates included)
+ *   max : Y[i,f] = max_k fl32(m_kf), arg[i,f] = the first k (CSR order)
+ *         attaining it; Abs = 0
+ * An empty row gives 0 (and arg -1).  The max compares the messages as the
+ * fp32 values a GPU multiply / add produces (the exact result rounded once to
+ * float), so the chosen edge is decided in the kernel's precision; its value
+ * is then exact.  With compute = multiply, sum is oracle_spmm. */
 int oracle_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
                  const int32_t *col, const float *val, int32_t F, const void *X, int32_t x_dtype,
-                 int32_t reduce, int32_t n_sel, const int32_t *sel, double *Y, double *Abs,
-                 int32_t *arg)
+                 int32_t reduce, int32_t compute, int32_t n_sel, const int32_t *sel, double *Y,
+                 double *Abs, int32_t *arg)
 {
-    if (n_rows < 0 || n_cols < 0 || nnz < 0 || F < 0 || reduce < 0 || reduce > 2) return -1;
-    if (reduce != 2)
-        {
-            int rc = oracle_spmm(n_rows, n_cols, nnz, rowptr, col, val, F, X, x_dtype, n_sel, sel,
-                                 Y, Abs);
-            if (rc != 0 || reduce == 0) return rc;
-            int32_t n_out = sel ? n_sel : n_rows;
-            for (int32_t r = 0; r < n_out; ++r) {
-                int32_t i = sel ? sel[r] : r;
-                int32_t d = rowptr[i + 1] - rowptr[i];
-                for (int32_t f = 0; f < F; ++f) {
-                    int64_t t = (int64_t)r * F + f;
-                    Y[t] = d > 0 ? Y[t] / d : 0.0;
-                    if (Abs) Abs[t] = d > 0 ? Abs[t] / d : 0.0;
-                }
-            }
-            return 0;
-        }
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || F < 0 || reduce < 0 || reduce > 2 ||
+        compute < 0 || compute > 3)
+        return -1;
     int32_t n_out = sel ? n_sel : n_rows;
     #pragma omp parallel for schedule(dynamic, 64)
     for (int32_t r = 0; r < n_out; ++r) {
         int32_t i = sel ? sel[r] : r;
+        int32_t d = rowptr[i + 1] - rowptr[i];
         for (int32_t f = 0; f < F; ++f) {
             int64_t t = (int64_t)r * F + f;
+            double sum = 0.0, abs_sum = 0.0;
             float best = 0.0f;
             int32_t best_k = -1;
             for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
-                float w = val ? val[k] : 1.0f;
-                float x = (float)load_elem(X, x_dtype, (int64_t)col[k] * F + f);
-                float p = (float)((double)w * (double)x);   /* exact product, rounded once */
-                if (best_k < 0 || p > best) { best = p; best_k = k; }
+                double w = val ? (double)val[k] : 1.0;
+                double x = load_elem(X, x_dtype, (int64_t)col[k] * F + f);
+                double m = gspmm_message(compute, w, x);
+                if (reduce == 2) {
+                    float p = (float)m;
+                    if (best_k < 0 || p > best) { best = p; best_k = k; }
+                } else {
+                    sum += m;
+                    abs_sum += fabs(m);
+                }
             }
-            Y[t] = best_k < 0 ? 0.0 : (double)best;
-            if (Abs) Abs[t] = 0.0;
-            if (arg) arg[t] = best_k;
+            if (reduce == 2) {
+                Y[t] = best_k < 0 ? 0.0 : (double)best;
+                if (Abs) Abs[t] = 0.0;
+                if (arg) arg[t] = best_k;
+            } else {
+                if (reduce == 1 && d > 0) { sum /= d; abs_sum /= d; }
+                Y[t] = sum;
+                if (Abs) Abs[t] = abs_sum;
+            }
         }
     }
     return 0;

@@ -546,3 +546,91 @@ def test_gspmm_max_ties_take_the_first_edge():
     Y, _, arg = oracle.gspmm(rowptr, col, None, X, reduce="max")
     assert Y.tolist() == [[0.5, -0.25], [1.0, -0.25]]
     assert arg.tolist() == [[0, 0], [3, 4]]
+
+
+# ------------------------------------------------------------ GSpMM compute operators
+
+def _pattern_and_rowsum(g):
+    """Dense pattern counts P (duplicates add up) and the row sums of the edge values."""
+    P = np.zeros((g.n_rows, g.n_cols))
+    rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+    np.add.at(P, (rows, g.col), 1.0)
+    wsum = np.zeros(g.n_rows)
+    np.add.at(wsum, rows, g.val.astype(np.float64))
+    return P, wsum
+
+
+def test_gspmm_add_sub_sum_and_mean_closed_forms():
+    """sum_k (x_kf + w_k) = (P X)_if + sum_k w_k, and the same with -w for sub;
+    mean divides both by the degree; Abs is the sum of |message|."""
+    rng = np.random.default_rng(32)
+    for g in _graphs(6):
+        X = rng.standard_normal((g.n_cols, 4)).astype(np.float32)
+        P, wsum = _pattern_and_rowsum(g)
+        PX = P @ X.astype(np.float64)
+        d = np.diff(g.rowptr).astype(np.float64)
+        for op, sign in (("add", 1.0), ("sub", -1.0)):
+            Y, A, _ = oracle.gspmm(g.rowptr, g.col, g.val, X, "sum", compute=op)
+            np.testing.assert_allclose(Y, PX + sign * wsum[:, None], rtol=1e-12, atol=1e-12)
+            Ym, Am, _ = oracle.gspmm(g.rowptr, g.col, g.val, X, "mean", compute=op)
+            np.testing.assert_allclose(Ym, (PX + sign * wsum[:, None]) / np.maximum(d, 1)[:, None],
+                                       rtol=1e-12, atol=1e-12)
+            # error scale by brute force over the edges of each row
+            for i in range(g.n_rows):
+                b, e = g.rowptr[i], g.rowptr[i + 1]
+                m = X[g.col[b:e]].astype(np.float64) + sign * g.val[b:e, None].astype(np.float64)
+                np.testing.assert_allclose(A[i], np.abs(m).sum(0), rtol=1e-13, atol=0)
+                np.testing.assert_allclose(Am[i], np.abs(m).sum(0) / max(e - b, 1), rtol=1e-13, atol=0)
+
+
+def test_gspmm_copy_ignores_values():
+    rng = np.random.default_rng(33)
+    for g in _graphs(7):
+        X = rng.standard_normal((g.n_cols, 3)).astype(np.float32)
+        P, _ = _pattern_and_rowsum(g)
+        Y, _, _ = oracle.gspmm(g.rowptr, g.col, g.val, X, "sum", compute="copy")
+        np.testing.assert_allclose(Y, P @ X.astype(np.float64), rtol=1e-12, atol=1e-12)
+        for red in ("sum", "mean", "max"):
+            a = oracle.gspmm(g.rowptr, g.col, g.val, X, red, compute="copy")
+            b = oracle.gspmm(g.rowptr, g.col, None, X, red, compute="mul")
+            assert np.array_equal(a[0], b[0])
+            assert (a[2] is None and b[2] is None) or np.array_equal(a[2], b[2])
+
+
+def test_gspmm_max_add_dense_masked_max():
+    """max_j fl32(X_jf + W_ij) over the pattern with numpy's float32 sum."""
+    rng = np.random.default_rng(34)
+    for n_rows, n_cols in ((30, 40), (64, 20)):
+        g = synth.random_csr(n_rows, n_cols, rng, mean_deg=6, empty_frac=0.2)
+        X = rng.standard_normal((n_cols, 5)).astype(np.float32)
+        rows = np.repeat(np.arange(n_rows), np.diff(g.rowptr))
+        mask = np.zeros((n_rows, n_cols), bool)
+        mask[rows, g.col] = True
+        empty = ~mask.any(1)
+        for op, sign in (("add", 1), ("sub", -1)):
+            Wd = np.zeros((n_rows, n_cols), np.float32)
+            Wd[rows, g.col] = g.val
+            M = X[None, :, :] + np.float32(sign) * Wd[:, :, None]       # float32 sums
+            M = np.where(mask[:, :, None], M, -np.inf)
+            Y, _, arg = oracle.gspmm(g.rowptr, g.col, g.val, X, "max", compute=op)
+            assert np.array_equal(Y, np.where(empty[:, None], 0.0, M.max(1).astype(np.float64)))
+            jmax = np.argmax(M, axis=1)
+            got_cols = np.where(arg >= 0, g.col[np.maximum(arg, 0)], -1)
+            assert np.array_equal(got_cols, np.where(empty[:, None], -1, jmax))
+
+
+def test_gspmm_compute_hand_example():
+    # row 0: edges (col 1, w 2), (col 0, w -1); row 1 empty; X = [[1, -3], [0.5, -0.25]]
+    rowptr = np.array([0, 2, 2], np.int32)
+    col = np.array([1, 0], np.int32)
+    val = np.array([2.0, -1.0], np.float32)
+    X = np.array([[1.0, -3.0], [0.5, -0.25]], np.float32)
+    Y, A, _ = oracle.gspmm(rowptr, col, val, X, "sum", compute="add")
+    assert Y.tolist() == [[2.5 + 0.0, 1.75 - 4.0], [0.0, 0.0]]
+    assert A.tolist() == [[2.5, 1.75 + 4.0], [0.0, 0.0]]
+    Y, _, arg = oracle.gspmm(rowptr, col, val, X, "max", compute="sub")
+    # messages: edge 0 -> (0.5-2, -0.25-2) = (-1.5, -2.25); edge 1 -> (1+1, -3+1) = (2, -2)
+    assert Y.tolist() == [[2.0, -2.0], [0.0, 0.0]]
+    assert arg.tolist() == [[1, 1], [-1, -1]]
+    Y, _, _ = oracle.gspmm(rowptr, col, val, X, "mean", compute="sub")
+    assert Y.tolist() == [[(-1.5 + 2.0) / 2, (-2.25 - 2.0) / 2], [0.0, 0.0]]
