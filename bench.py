@@ -315,8 +315,9 @@ def main():
                     traffic_detail=tr)
 
     # Entry points outside the fused forward step, timed on the same inputs:
-    # the standalone SDDMM + edge softmax (alpha written) and the fused
-    # aggregation with alpha written for the backward pass.
+    # the standalone SDDMM + edge softmax (alpha written), the fused
+    # aggregation with alpha written for the backward pass, and the GSpMM
+    # mean and max reduces (max with the int32 edge id of every output).
     alpha_buf = torch.empty((E, H), dtype=torch.float32, device=dev)
 
     def time_op(fn, reps=5):
@@ -334,6 +335,13 @@ def main():
                                                     out=alpha_buf))
     ms_gat_a = time_op(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
                                                 out=Yg, alpha_out=alpha_buf))
+    ms_mean = time_op(lambda: cg.gspmm(rowptr, col, val, X, "mean", plan=plan, out=Y))
+    arg_buf = torch.empty((N, F), dtype=torch.int32, device=dev)
+    ms_max = time_op(lambda: cg.gspmm(rowptr, col, val, X, "max", plan=plan, out=Y,
+                                      return_arg=True, arg=arg_buf))
+    del arg_buf
+    b_mean = b_spmm(N, M, E, F, 2, 2)
+    b_max = b_mean + 4 * N * F
     b_soft = 4 * (N + 1) + 4 * E + 4 * N * H + 4 * E * H + 4 * E * H
     b_gat_a = b_gat(N, E, H, D, 2, 2, True)
     extra_ops = {
@@ -343,8 +351,15 @@ def main():
         "gat_aggregate_with_alpha": dict(ms=ms_gat_a, algorithmic_GB=b_gat_a / 1e9,
                                          eff_GBps=b_gat_a / (ms_gat_a * 1e-3) / 1e9,
                                          edges_per_s=E / (ms_gat_a * 1e-3)),
+        "gspmm_mean": dict(ms=ms_mean, algorithmic_GB=b_mean / 1e9,
+                           eff_GBps=b_mean / (ms_mean * 1e-3) / 1e9,
+                           edges_per_s=E / (ms_mean * 1e-3)),
+        "gspmm_max_with_arg": dict(ms=ms_max, algorithmic_GB=b_max / 1e9,
+                                   eff_GBps=b_max / (ms_max * 1e-3) / 1e9,
+                                   edges_per_s=E / (ms_max * 1e-3)),
     }
-    log(f"extra: sddmm_edge_softmax {ms_soft:.3f} ms, gat_aggregate+alpha {ms_gat_a:.3f} ms")
+    log(f"extra: sddmm_edge_softmax {ms_soft:.3f} ms, gat_aggregate+alpha {ms_gat_a:.3f} ms, "
+        f"gspmm mean {ms_mean:.3f} ms, max+arg {ms_max:.3f} ms")
 
     out = {
         "metric": METRIC, "value": value, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,

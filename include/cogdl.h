@@ -70,6 +70,15 @@ typedef enum { COGDL_F32 = 0, COGDL_BF16 = 1, COGDL_F16 = 2 } cogdl_dtype;
 /* Reduce operation phi of Eq. 1 (section 2.2). */
 typedef enum { COGDL_REDUCE_SUM = 0, COGDL_REDUCE_MEAN = 1, COGDL_REDUCE_MAX = 2 } cogdl_reduce;
 
+/* Compute (message) operation psi of Eq. 1: the message of edge k to feature f,
+ * with w = val[k] (1 when val is NULL) and x = X[col[k], f]. */
+typedef enum {
+    COGDL_COMPUTE_MUL = 0,   /* w * x */
+    COGDL_COMPUTE_ADD = 1,   /* x + w */
+    COGDL_COMPUTE_SUB = 2,   /* x - w */
+    COGDL_COMPUTE_COPY = 3   /* x (val ignored) */
+} cogdl_compute;
+
 /* Backend choice of the workload balancer (section 2.2, the balancer listing). */
 typedef enum {
     COGDL_BALANCE_AUTO = 0,            /* data-aware choice, see cogdl_plan_create */
@@ -160,21 +169,24 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         const cogdl_plan *plan, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * GSpMM with a choice of reduce -- section 2.2, Eq. 1 (the user picks the
- * reduce and compute operations; compute here is the multiplication by the
- * edge value, or a copy of the neighbour feature when val is NULL):
- *   SUM : Y[i, f] = sum_k val[k] * X[col[k], f]           (= cogdl_spmm)
- *   MEAN: Y[i, f] = (1 / d_i) * sum_k val[k] * X[col[k], f], d_i = edges of row i
- *   MAX : Y[i, f] = max_k val[k] * X[col[k], f] (products rounded to fp32), and
+ * GSpMM with a choice of reduce and compute -- section 2.2, Eq. 1 (the user
+ * picks the reduce phi and the message psi).  With m_kf the message of edge
+ * k (cogdl_compute) and d_i the number of edges of row i:
+ *   SUM : Y[i, f] = sum_k m_kf        (MUL: = cogdl_spmm)
+ *   MEAN: Y[i, f] = (1 / d_i) * sum_k m_kf
+ *   MAX : Y[i, f] = max_k m_kf (messages rounded once to fp32), and
  *         arg[i, f] = the first edge id k, in CSR order, attaining the max
- * An empty row gives 0 (and arg -1).  arg: device int32 n_rows x F, written
- * for MAX only, may be NULL.  MAX supports y_dtype equal to x_dtype or fp32
- * (COGDL_ERR_DTYPE otherwise).  Other arguments as for cogdl_spmm.
+ * An empty row gives 0 (and arg -1).  Messages and sums are computed in
+ * fp32.  arg: device int32 n_rows x F, written for MAX only, may be NULL.
+ * MAX supports y_dtype equal to x_dtype or fp32 (COGDL_ERR_DTYPE otherwise);
+ * an unknown reduce or compute code is COGDL_ERR_INVALID.  Other arguments
+ * and errors as for cogdl_spmm.
  * ---------------------------------------------------------------------- */
 cogdl_status cogdl_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
                          const int32_t *col, const float *val, int32_t F, const void *X,
                          cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, cogdl_reduce reduce,
-                         int32_t *arg, const cogdl_plan *plan, hipStream_t stream);
+                         cogdl_compute compute, int32_t *arg, const cogdl_plan *plan,
+                         hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * CSR -> CSC transpose of the graph structure, the setup of the backward

@@ -61,7 +61,7 @@ def lib():
     L.cogdl_plan_units.argtypes = [P, P, i64, P]
     L.cogdl_spmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_gspmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int,
-                              ctypes.c_int, P, P, P]
+                              ctypes.c_int, ctypes.c_int, P, P, P]
     L.cogdl_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_csr_to_csc_workspace.argtypes = [i32, i32, i64, ctypes.POINTER(sz)]
     L.cogdl_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P, sz, P]
@@ -211,17 +211,22 @@ def spmm(rowptr, col, val, X, plan: Plan | None = None, out_dtype=None, out=None
 
 
 REDUCE = {"sum": 0, "mean": 1, "max": 2}
+COMPUTE = {"mul": 0, "add": 1, "sub": 2, "copy": 3}
 
 
 def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, out_dtype=None,
-          out=None, return_arg: bool = False, arg=None):
-    """Eq. 1 with reduce = sum, mean or max over row i of val[k] * X[col[k]].
+          out=None, return_arg: bool = False, arg=None, compute: str = "mul"):
+    """Eq. 1 with reduce = sum, mean or max over the edges k of row i of the
+    message val[k] * x (compute "mul"), x + val[k] ("add"), x - val[k] ("sub")
+    or x ("copy"), x = X[col[k]].
 
     For max, ``return_arg`` also returns the int32 edge id of the first edge
     attaining each output (-1 on empty rows); max keeps X's dtype or fp32."""
     import torch
     if reduce not in REDUCE:
         raise ValueError(f"reduce must be one of {sorted(REDUCE)}")
+    if compute not in COMPUTE:
+        raise ValueError(f"compute must be one of {sorted(COMPUTE)}")
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
     _dev(val, "val", torch.float32), _dev(X, "X")
     n_rows = rowptr.numel() - 1
@@ -236,7 +241,8 @@ def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, ou
     _dev(arg, "arg", torch.int32)
     _check(lib().cogdl_gspmm(n_rows, X.shape[0], col.numel(), _ptr(rowptr), _ptr(col), _ptr(val), F,
                              _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), REDUCE[reduce],
-                             _ptr(arg), _plan_handle(plan), _stream()), "cogdl_gspmm")
+                             COMPUTE[compute], _ptr(arg), _plan_handle(plan), _stream()),
+           "cogdl_gspmm")
     return (out, arg) if return_arg else out
 
 

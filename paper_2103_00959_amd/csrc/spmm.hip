@@ -1,6 +1,7 @@
-// Generalized SpMM of section 2.2, Eq. 1 (H' = A H with reduce = sum, mean or
-// max and compute = multiply by the edge value), and the transposed product
-// A^T G of its backward pass.
+// Generalized SpMM of section 2.2, Eq. 1: H' = A H (reduce = sum, compute =
+// multiply by the edge value), its reduce (mean, max) and compute (add,
+// subtract, copy) variants, and the transposed product A^T G of its backward
+// pass.  The gather kernel itself is in spmm_kernel.hpp.
 //
 // Mapping on gfx950 (64-lane wavefronts):
 //   - A work unit (a whole row, or a neighbour group of a long row) belongs to
@@ -17,211 +18,12 @@
 //     group writes an fp32 partial row (for max also the edge id of each
 //     partial maximum), and a second kernel combines the partials of each
 //     split row in a fixed order (no floating-point atomics).
-#include "common.hpp"
-#include "internal.hpp"
+#include "spmm_kernel.hpp"
 
 namespace cogdl {
 namespace {
 
-constexpr int kBlock = 256;
-
-struct SpmmArgs {
-    const int4 *units;          // nullptr: one unit per row in row order
-    const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
-    const int32_t *u_hi;
-    int32_t n_rows;
-    const int32_t *rowptr;
-    const int32_t *col;
-    const float *val;           // nullptr: all ones
-    const void *X;
-    void *Y;
-    int32_t *arg;               // max: edge id of each output maximum (nullable)
-    float *partials;
-    int32_t *parg;              // max: edge id of each partial maximum
-    int64_t pstride;
-    int64_t F;
-    uint64_t x_bytes;           // size of X, bounds the buffer gathers
-    int32_t slab;
-    int32_t log2S;
-    int32_t mean;               // sum / mean: divide whole rows by their degree
-};
-
-// Descriptor {row, first edge, end edge, partial slot} of unit u (an empty
-// unit past the end, so prefetching one unit ahead needs no branch around it).
-__device__ __forceinline__ int4 fetch_unit(const SpmmArgs &a, int64_t u, int64_t hi)
-{
-    if (u >= hi) return make_int4(0, 0, 0, -1);
-    if (a.units) return a.units[u];
-    const int r = (int)u;
-    return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
-}
-
-// Stores N edge ids (16-byte stores when N is a multiple of four; the offsets
-// and the base are then 16-byte aligned).
-template <int N>
-__device__ __forceinline__ void store_ids(int32_t *__restrict__ p, int64_t i, const int32_t (&v)[N])
-{
-    if constexpr (N % 4 == 0) {
-#pragma unroll
-        for (int e = 0; e < N; e += 4)
-            *reinterpret_cast<int4 *>(p + i + e) = make_int4(v[e], v[e + 1], v[e + 2], v[e + 3]);
-    } else {
-#pragma unroll
-        for (int e = 0; e < N; ++e) p[i + e] = v[e];
-    }
-}
-
-// MAXR = false: sum of products (mean scales whole rows by 1 / degree);
-// MAXR = true: maximum of the products, edges taken in CSR order, the first
-// edge kept unconditionally and a later one only if strictly greater, so the
-// recorded edge is the first that attains the maximum.
-template <typename TX, typename TY, int VEC, int CH, bool BUF, bool MAXR>
-__global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a)
-{
-    constexpr int U = (VEC == 1 ? 16 : 8) / CH;
-    constexpr int AC = MAXR ? CH : 1;
-    constexpr int AV = MAXR ? VEC : 1;
-    const int log2S = a.log2S;
-    const int S = 1 << log2S;
-    const int lane = lane_id();
-    const int lig = lane & (S - 1);
-    const int gbase = lane & ~(S - 1);
-    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
-    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
-    const int64_t lo = a.units ? *a.u_lo : 0;
-    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
-
-    const int64_t f0 = (int64_t)blockIdx.y * a.slab;
-    const int64_t f_end = (f0 + a.slab < a.F) ? f0 + a.slab : a.F;
-    int64_t fe[CH];
-    bool act[CH];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        fe[c] = f0 + (int64_t)(c * S + lig) * VEC;
-        act[c] = fe[c] < f_end;
-    }
-    const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
-    const int32_t *__restrict__ col = a.col;
-    const float *__restrict__ val = a.val;
-
-    // Resident grid: sub-group i runs units lo + i, lo + i + stride, ...; the
-    // units are sorted by length, so neighbouring sub-groups get equal work.
-    // The loop is software-pipelined: the next unit's descriptor is fetched
-    // when a unit starts and its first index chunk before the current output
-    // is stored, so short units do not pay three dependent memory trips each.
-    int64_t u = lo + sub;
-    if (u >= hi) return;
-    int4 d = fetch_unit(a, u, hi);
-    int c_cur = 0;
-    float v_cur = 0.f;
-    if (d.z > d.y) {
-        // index loads are clamped to the unit's last edge instead of masked:
-        // no branch, and lanes past the end are never read back
-        const int k = d.y + lig < d.z - 1 ? d.y + lig : d.z - 1;
-        c_cur = col[k];
-        v_cur = val ? val[k] : 1.f;
-    }
-    for (;;) {
-        const int64_t un = u + stride;
-        const int4 dn = fetch_unit(a, un, hi);
-        const int row = d.x, beg = d.y, end = d.z, part = d.w;
-        float acc[CH][VEC];
-        int32_t am[AC][AV];
-#pragma unroll
-        for (int c = 0; c < CH; ++c)
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
-#pragma unroll
-        for (int c = 0; c < AC; ++c)
-#pragma unroll
-            for (int e = 0; e < AV; ++e) am[c][e] = -1;
-
-        const int last = end - 1;
-        for (int k0 = beg; k0 < end; k0 += S) {
-            const int n = (end - k0 < S) ? end - k0 : S;
-            const int k = k0 + S + lig < last ? k0 + S + lig : last;
-            const int c_nxt = col[k];
-            const float v_nxt = val ? val[k] : 1.f;
-            for (int j = 0; j < n; j += U) {
-                int cc[U];
-                float vv[U];
-                bool ok[U];
-#pragma unroll
-                for (int t = 0; t < U; ++t) {
-                    ok[t] = j + t < n;
-                    const int src = gbase + (ok[t] ? j + t : j);
-                    cc[t] = lane_bcast(c_cur, src);
-                    vv[t] = lane_bcast(v_cur, src);
-                }
-                float xv[U][CH][VEC];
-#pragma unroll
-                for (int t = 0; t < U; ++t)
-#pragma unroll
-                    for (int c = 0; c < CH; ++c)
-                        X.load((int64_t)cc[t] * a.F + fe[c], ok[t] && act[c], xv[t][c]);
-                if constexpr (MAXR) {
-#pragma unroll
-                    for (int t = 0; t < U; ++t)
-#pragma unroll
-                        for (int c = 0; c < CH; ++c)
-#pragma unroll
-                            for (int e = 0; e < VEC; ++e) {
-                                const float p = vv[t] * xv[t][c][e];
-                                const bool take = ok[t] && (am[c][e] < 0 || p > acc[c][e]);
-                                acc[c][e] = take ? p : acc[c][e];
-                                am[c][e] = take ? k0 + j + t : am[c][e];
-                            }
-                } else {
-#pragma unroll
-                    for (int t = 0; t < U; ++t)
-#pragma unroll
-                        for (int c = 0; c < CH; ++c)
-#pragma unroll
-                            for (int e = 0; e < VEC; ++e)
-                                acc[c][e] = fmaf(vv[t], xv[t][c][e], acc[c][e]);
-                }
-            }
-            c_cur = c_nxt;
-            v_cur = v_nxt;
-        }
-
-        // first index chunk of the next unit, issued before this unit's stores
-        if (dn.z > dn.y) {
-            const int k = dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1;
-            c_cur = col[k];
-            v_cur = val ? val[k] : 1.f;
-        }
-        if (part < 0) {
-            TY *__restrict__ Y = static_cast<TY *>(a.Y);
-            if (!MAXR && a.mean && end > beg) {
-                const float r = 1.f / (float)(end - beg);
-#pragma unroll
-                for (int c = 0; c < CH; ++c)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
-            }
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                if (!act[c]) continue;
-                store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
-                if constexpr (MAXR) {
-                    if (a.arg) store_ids<VEC>(a.arg, (int64_t)row * a.F + fe[c], am[c]);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                if (!act[c]) continue;
-                store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
-                if constexpr (MAXR)
-                    store_ids<VEC>(a.parg, (int64_t)part * a.pstride + fe[c], am[c]);
-            }
-        }
-        if (un >= hi) break;
-        u = un;
-        d = dn;
-    }
-}
+constexpr int kBlock = kSpmmBlock;
 
 // Y[row, :] = sum of the row's partial rows (times 1 / degree for mean).  One
 // workgroup per split row (grid-stride over the device-side count, uniform
@@ -323,49 +125,6 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce_max(const int4 *__restri
     }
 }
 
-using SpmmKernel = void (*)(SpmmArgs);
-
-template <typename TX, typename TY, bool BUF, bool MAXR>
-SpmmKernel pick_kernel(int vec, int ch)
-{
-    constexpr int V = (int)(16 / sizeof(TX));
-    if (vec == 1) {
-        if (ch == 1) return k_spmm<TX, TY, 1, 1, BUF, MAXR>;
-        if (ch == 2) return k_spmm<TX, TY, 1, 2, BUF, MAXR>;
-        return k_spmm<TX, TY, 1, 4, BUF, MAXR>;
-    }
-    if (ch == 1) return k_spmm<TX, TY, V, 1, BUF, MAXR>;
-    if (ch == 2) return k_spmm<TX, TY, V, 2, BUF, MAXR>;
-    return k_spmm<TX, TY, V, 4, BUF, MAXR>;
-}
-
-// Max outputs keep the input format or widen it to fp32 (each output is one
-// fp32 product rounded once); the caller rejects other pairs.
-template <typename TX, bool BUF>
-SpmmKernel pick_y(int ydt, int vec, int ch, bool maxr)
-{
-    if (maxr) {
-        if (ydt == COGDL_F32) return pick_kernel<TX, float, BUF, true>(vec, ch);
-        return pick_kernel<TX, TX, BUF, true>(vec, ch);
-    }
-    if (ydt == COGDL_F32) return pick_kernel<TX, float, BUF, false>(vec, ch);
-    if (ydt == COGDL_BF16) return pick_kernel<TX, bf16_t, BUF, false>(vec, ch);
-    return pick_kernel<TX, f16_t, BUF, false>(vec, ch);
-}
-
-template <bool BUF>
-SpmmKernel pick_x(int xdt, int ydt, int vec, int ch, bool maxr)
-{
-    if (xdt == COGDL_F32) return pick_y<float, BUF>(ydt, vec, ch, maxr);
-    if (xdt == COGDL_BF16) return pick_y<bf16_t, BUF>(ydt, vec, ch, maxr);
-    return pick_y<f16_t, BUF>(ydt, vec, ch, maxr);
-}
-
-SpmmKernel pick(int xdt, int ydt, int vec, int ch, bool buf, bool maxr)
-{
-    return buf ? pick_x<true>(xdt, ydt, vec, ch, maxr) : pick_x<false>(xdt, ydt, vec, ch, maxr);
-}
-
 template <int VEC>
 cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
                              bool mean, hipStream_t s)
@@ -432,12 +191,13 @@ struct LaunchNames {
 // an in_rows x F input through (ptr, idx, w), combined by `reduce`.
 cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const int32_t *ptr,
                          const int32_t *idx, const float *w, int32_t F, const void *X, int xdt,
-                         void *Y, int ydt, int reduce, int32_t *arg, const cogdl_plan *plan_h,
-                         hipStream_t s, LaunchNames names)
+                         void *Y, int ydt, int reduce, int compute, int32_t *arg,
+                         const cogdl_plan *plan_h, hipStream_t s, LaunchNames names)
 {
     if (out_rows < 0 || in_rows < 0 || nnz < 0 || F < 0) return COGDL_ERR_INVALID;
     if (reduce != COGDL_REDUCE_SUM && reduce != COGDL_REDUCE_MEAN && reduce != COGDL_REDUCE_MAX)
         return COGDL_ERR_INVALID;
+    if (compute < COGDL_COMPUTE_MUL || compute > COGDL_COMPUTE_COPY) return COGDL_ERR_INVALID;
     if (!dtype_ok(xdt) || !dtype_ok(ydt)) return COGDL_ERR_DTYPE;
     const bool maxr = reduce == COGDL_REDUCE_MAX;
     if (maxr && ydt != COGDL_F32 && ydt != xdt) return COGDL_ERR_DTYPE;
@@ -460,7 +220,7 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     a.n_rows = out_rows;
     a.rowptr = ptr;
     a.col = idx;
-    a.val = w;
+    a.val = compute == COGDL_COMPUTE_COPY ? nullptr : w;
     a.X = X;
     a.Y = Y;
     a.arg = maxr ? arg : nullptr;
@@ -472,7 +232,13 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     a.slab = m.slab;
     a.log2S = m.log2S;
     a.mean = reduce == COGDL_REDUCE_MEAN ? 1 : 0;
+    a.bsign = compute == COGDL_COMPUTE_SUB ? -1.f : 1.f;
+    const bool addop = compute == COGDL_COMPUTE_ADD || compute == COGDL_COMPUTE_SUB;
     const bool buf = a.x_bytes <= kBufferMaxBytes;
+    auto pick = [&](int ch) {
+        return (maxr || addop) ? gspmm_pick(maxr, addop, xdt, ydt, m.vec, ch, buf)
+                               : spmm_pick<false, false>(xdt, ydt, m.vec, ch, buf);
+    };
     const int64_t units = P ? P->cap_units : out_rows;
     // Units of at most kTinyUnit edges (the sorted tail) run with S/4 lanes and
     // four chunks per lane: four times as many rows in flight per wavefront.
@@ -480,7 +246,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     if (tiny) a.u_hi = P->n_big_dev();
     {
         const int64_t upb = kBlock >> m.log2S;
-        SpmmKernel k = pick(xdt, ydt, m.vec, m.ch, buf, maxr);
+        SpmmKernel k = pick(m.ch);
+        if (!k) return COGDL_ERR_DTYPE;
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
@@ -493,7 +260,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
         b.u_hi = P->n_units_dev();
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
-        SpmmKernel k = pick(xdt, ydt, m.vec, 4, buf, maxr);
+        SpmmKernel k = pick(4);
+        if (!k) return COGDL_ERR_DTYPE;
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
@@ -516,17 +284,18 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         hipStream_t stream)
 {
     return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
-                              (int)y_dtype, COGDL_REDUCE_SUM, nullptr, plan, stream,
-                              {"spmm", "spmm_tiny", "spmm_reduce"});
+                              (int)y_dtype, COGDL_REDUCE_SUM, COGDL_COMPUTE_MUL, nullptr, plan,
+                              stream, {"spmm", "spmm_tiny", "spmm_reduce"});
 }
 
 cogdl_status cogdl_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
                          const int32_t *col, const float *val, int32_t F, const void *X,
                          cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, cogdl_reduce reduce,
-                         int32_t *arg, const cogdl_plan *plan, hipStream_t stream)
+                         cogdl_compute compute, int32_t *arg, const cogdl_plan *plan,
+                         hipStream_t stream)
 {
     return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
-                              (int)y_dtype, (int)reduce, arg, plan, stream,
+                              (int)y_dtype, (int)reduce, (int)compute, arg, plan, stream,
                               {"gspmm", "gspmm_tiny", "gspmm_reduce"});
 }
 
@@ -537,8 +306,8 @@ cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int
 {
     // A^T has n_cols rows, each gathering rows of the n_rows x F input G.
     return cogdl::spmm_common(n_cols, n_rows, nnz, colptr, row_t, val_t, F, G, (int)g_dtype, dX,
-                              (int)dx_dtype, COGDL_REDUCE_SUM, nullptr, plan_t, stream,
-                              {"spmm_t", "spmm_t_tiny", "spmm_t_reduce"});
+                              (int)dx_dtype, COGDL_REDUCE_SUM, COGDL_COMPUTE_MUL, nullptr, plan_t,
+                              stream, {"spmm_t", "spmm_t_tiny", "spmm_t_reduce"});
 }
 
 }  // extern "C"

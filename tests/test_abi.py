@@ -73,20 +73,24 @@ def test_spmm_validation(L):
 
 
 def test_gspmm_validation(L):
-    G = L.cogdl_gspmm
-    # reduce codes outside sum / mean / max
-    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 3, None, None, None) == INVALID
-    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, -1, None, None, None) == INVALID
+    def G(*a):
+        # (n_rows, n_cols, nnz, rowptr, col, val, F, X, x_dt, Y, y_dt, reduce, compute)
+        return L.cogdl_gspmm(*a, None, None, None)
+    # reduce codes outside sum / mean / max, compute codes outside mul / add / sub / copy
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 3, 0) == INVALID
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, -1, 0) == INVALID
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 0, 4) == INVALID
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 2, -1) == INVALID
     # max keeps the input format or widens to fp32: bf16 -> fp16 is refused
-    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 1, FAKE, 2, 2, None, None, None) == DTYPE
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 1, FAKE, 2, 2, 0) == DTYPE
     # fp32 -> bf16 is refused for max, but not for sum / mean (those fail later, on nulls)
-    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 1, 2, None, None, None) == DTYPE
-    assert G(2, 2, 3, FAKE, None, None, 4, FAKE, 0, FAKE, 1, 1, None, None, None) == INVALID
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 1, 2, 1) == DTYPE
+    assert G(2, 2, 3, FAKE, None, None, 4, FAKE, 0, FAKE, 1, 1, 2) == INVALID
     # the checks shared with cogdl_spmm
-    assert G(-1, 1, 0, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 1, None, None, None) == INVALID
-    assert G(2, 2, 1 << 31, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 2, None, None, None) == TOO_LARGE
-    assert G(2, 2, 3, FAKE, FAKE, None, 4, None, 0, FAKE, 0, 2, None, None, None) == INVALID
-    assert G(0, 5, 0, None, None, None, 4, None, 0, None, 0, 2, None, None, None) == OK
+    assert G(-1, 1, 0, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 1, 0) == INVALID
+    assert G(2, 2, 1 << 31, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 2, 3) == TOO_LARGE
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, None, 0, FAKE, 0, 2, 0) == INVALID
+    assert G(0, 5, 0, None, None, None, 4, None, 0, None, 0, 2, 1) == OK
 
 
 def test_spmm_t_validation(L):

@@ -245,6 +245,37 @@ def test_gspmm_max_ties_first_edge(cg, F):
                 plan.close()
 
 
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
+@pytest.mark.parametrize("plan_spec", [None, ("auto", 0), ("neighbor_group", 5)])
+@pytest.mark.parametrize("compute", ["add", "sub", "copy"])
+def test_gspmm_compute_ops(cg, kind, plan_spec, compute):
+    """Messages x + w, x - w and x under every reduce: sum / mean to the fp32
+    tolerance (error scale: sum of |message|), max bit for bit with edge ids."""
+    import torch
+    g = _graph(kind)
+    say(f"gspmm {compute} {kind} plan={plan_spec}")
+    rp, cl, vl = graph_to_dev(g)
+    for F, xk in ((5, "f32"), (64, "f32"), (128, "bf16")):
+        xh, xc, xd = features((g.n_cols, F), 51 + F, xk)
+        plan = _make_plan(cg, rp, g.nnz, plan_spec, F)
+        try:
+            for red in ("sum", "mean"):
+                Y = cg.gspmm(rp, cl, vl, xd, red, plan=plan, out_dtype=torch.float32, compute=compute)
+                Yr, Ar, _ = oracle.gspmm(g.rowptr, g.col, g.val, xh, red, n_cols=g.n_cols, x_dtype=xc,
+                                         compute=compute)
+                err = scaled_error(Y, Yr, Ar)
+                assert err <= TOL_F32, (kind, plan_spec, compute, red, F, err)
+            Y, arg = cg.gspmm(rp, cl, vl, xd, "max", plan=plan, out_dtype=torch.float32,
+                              return_arg=True, compute=compute)
+            Yr, _, ar = oracle.gspmm(g.rowptr, g.col, g.val, xh, "max", n_cols=g.n_cols, x_dtype=xc,
+                                     compute=compute)
+            assert np.array_equal(to_f64(Y), Yr), (kind, plan_spec, compute, F)
+            assert np.array_equal(arg.cpu().numpy(), ar), (kind, plan_spec, compute, F)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
 def test_gspmm_sum_matches_spmm_bit_exact(cg):
     import torch
     g = _graph("hubs", seed=13)
