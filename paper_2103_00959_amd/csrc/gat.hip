@@ -3,11 +3,13 @@
 // row, and the multi-head SpMM that aggregates neighbour features with one
 // weight per edge and head.
 //
-// cogdl_sddmm_edge_softmax (alpha only): a wavefront per work unit, lanes laid
-// out as (edge slot, head) so that 64/H edges are scored per step; each lane
-// keeps an online softmax state (m, z), the states of one head are merged
-// across slots with lane exchanges (a butterfly when H is a power of two), and
-// a second sweep writes alpha = exp(e - m) / z with coalesced stores.
+// cogdl_sddmm_edge_softmax (alpha only): a sub-group of lanes per work unit
+// (a wavefront for long units, 4H lanes for the tiny tail), laid out as (edge
+// slot, head) so that S/H edges are scored per step with several steps in
+// flight; each lane keeps an online softmax state (m, z), the states of one
+// head are merged across slots with lane exchanges (a butterfly when H is a
+// power of two), and alpha = exp(e - m) / z is written with coalesced stores,
+// from registers when the unit fitted in one pass.
 //
 // cogdl_gat_aggregate (fused): the gather mapping of the SpMM (S lanes x VEC
 // features per edge row).  Every lane computes the weight of its own head for
@@ -58,6 +60,35 @@ __device__ __forceinline__ int4 fetch_unit(const GatArgs &a, int64_t u, int64_t 
     if (a.units) return a.units[u];
     const int r = (int)u;
     return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
+}
+
+// alpha[k, h] = exp(e_kh - m) * rz for the edges k = beg + slot + j * slots
+// of one head h, R gathers in flight per lane: the column indices of R edges
+// are loaded together (clamped to the last edge), then their R source scores,
+// then the R results are stored.
+template <int R>
+__device__ __forceinline__ void alpha_sweep(const int32_t *__restrict__ col,
+                                            const float *__restrict__ s_src,
+                                            float *__restrict__ alpha, int H, int h, float sd,
+                                            float slope, float m, float rz, int beg, int end,
+                                            int slot, int slots)
+{
+    for (int k0 = beg + slot; k0 < end; k0 += R * slots) {
+        int cc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int k = k0 + r * slots;
+            cc[r] = col[k < end ? k : end - 1];
+        }
+        float sv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) sv[r] = s_src[(int64_t)cc[r] * H + h];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int k = k0 + r * slots;
+            if (k < end) alpha[(int64_t)k * H + h] = __expf(leaky_relu(sd + sv[r], slope) - m) * rz;
+        }
+    }
 }
 
 template <typename TX, typename TY, int VEC, int CH, bool BUF>
@@ -222,13 +253,9 @@ __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
                     const float rr = lane_bcast(rz[c], gbase + src_l);
                     if (c == src_c) { m1 = mm; r1 = rr; }
                 }
-                if (mine_head && slot < eps) {
-                    const float sd1 = a.s_dst[(int64_t)row * H + h1];
-                    for (int k = beg + slot; k < end; k += eps) {
-                        const float e = leaky_relu(sd1 + a.s_src[(int64_t)col[k] * H + h1], a.slope);
-                        a.alpha_out[(int64_t)k * H + h1] = __expf(e - m1) * r1;
-                    }
-                }
+                if (mine_head && slot < eps)
+                    alpha_sweep<4>(col, a.s_src, a.alpha_out, H, h1, a.s_dst[(int64_t)row * H + h1],
+                                   a.slope, m1, r1, beg, end, slot, eps);
             }
         }
         if (un >= hi) break;
@@ -242,7 +269,8 @@ __global__ __launch_bounds__(kBlock) void k_gat(GatArgs a)
 
 struct SoftArgs {
     const int4 *units;
-    const int32_t *n_units;
+    const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
+    const int32_t *u_hi;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -253,99 +281,153 @@ struct SoftArgs {
     float *alpha;
     float *gstats;
     int32_t sstride;
+    int32_t log2S;              // k_softmax: lanes per unit
+    int32_t parked;             // k_alpha_split: alpha holds the raw scores of split rows
     const int4 *part_units;     // k_alpha_split: {row, beg, end, split}
     const int32_t *n_parts;
     const float *rstats;        // per split row: m[max_heads], z[max_heads]
 };
 
-// Merge the (m, z) states of the lanes holding the same head h = lane % H:
-// slots are lane / H, eps = 64 / H of them.  Result in every lane of head h.
-__device__ __forceinline__ void merge_slots(float &m, float &z, int H)
+// Merge the (m, z) states of the lanes of one S-lane sub-group (base gbase)
+// that hold the same head h = lane % H: slots are (lane - gbase) / H, S / H of
+// them.  Result in every lane of head h.
+__device__ __forceinline__ void merge_slots(float &m, float &z, int H, int S, int gbase)
 {
-    const int lane = lane_id();
     if ((H & (H - 1)) == 0) {
-        for (int off = H; off < kWave; off <<= 1) {
+        for (int off = H; off < S; off <<= 1) {
             const float m2 = lane_xor(m, off);
             const float z2 = lane_xor(z, off);
             softmax_merge(m, z, m2, z2);
         }
         return;
     }
-    const int eps = kWave / H;
-    const int h = lane % H;
+    const int slots = S / H;
+    const int h = (lane_id() - gbase) % H;
     float mm = -INFINITY, zz = 0.f;
-    for (int s = 0; s < eps; ++s) {
-        const float m2 = lane_bcast(m, s * H + h < kWave ? s * H + h : h);
-        const float z2 = lane_bcast(z, s * H + h < kWave ? s * H + h : h);
+    for (int s = 0; s < slots; ++s) {
+        const float m2 = lane_bcast(m, gbase + s * H + h);
+        const float z2 = lane_bcast(z, gbase + s * H + h);
         softmax_merge(mm, zz, m2, z2);
     }
     m = mm;
     z = zz;
 }
 
-__device__ __forceinline__ float edge_e(const SoftArgs &a, float sd, int k, int h)
+__device__ __forceinline__ int4 fetch_soft_unit(const SoftArgs &a, int64_t u, int64_t hi)
 {
-    return leaky_relu(sd + a.s_src[(int64_t)a.col[k] * a.H + h], a.slope);
+    if (u >= hi) return make_int4(0, 0, 0, -1);
+    if (a.units) return a.units[u];
+    const int r = (int)u;
+    return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
 }
 
-// One wavefront per unit.  Whole rows: alpha written; neighbour groups: (m, z)
-// per head into gstats.
+// S lanes per work unit laid out as (edge slot, head), slots = S / H edges per
+// step and R steps in flight per lane; resident grid, each sub-group striding
+// over the units with the next descriptor prefetched.  Whole rows: alpha
+// written (from the scores kept in registers when the row fits in one pass of
+// R steps, else by a second, batched sweep); neighbour groups: (m, z) per head
+// into gstats.
+template <int R>
 __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
 {
+    const int log2S = a.log2S;
+    const int S = 1 << log2S;
     const int lane = lane_id();
-    const int64_t u = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
-    int row, beg, end, part;
-    if (a.units) {
-        if (u >= *a.n_units) return;
-        const int4 d = a.units[u];
-        row = d.x; beg = d.y; end = d.z; part = d.w;
-    } else {
-        if (u >= a.n_rows) return;
-        row = (int)u;
-        beg = a.rowptr[row];
-        end = a.rowptr[row + 1];
-        part = -1;
-    }
+    const int lig = lane & (S - 1);
+    const int gbase = lane & ~(S - 1);
     const int H = a.H;
-    const int eps = kWave / H;
-    const int h = lane % H;
-    const int slot = lane / H;
-    const bool live = slot < eps;
-    const float sd = a.s_dst[(int64_t)row * H + h];
-    float m = -INFINITY, z = 0.f;
-    constexpr int R = 4;
-    for (int k0 = beg + slot; k0 < end; k0 += R * eps) {
-        float e[R];
+    const int slots = S / H;
+    const int h = lig % H;
+    const int slot = lig / H;
+    const bool live = slot < slots;
+    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
+    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
+    const int64_t lo = a.units ? *a.u_lo : 0;
+    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const int32_t *__restrict__ col = a.col;
+
+    int64_t u = lo + sub;
+    if (u >= hi) return;
+    int4 d = fetch_soft_unit(a, u, hi);
+    for (;;) {
+        const int64_t un = u + stride;
+        const int4 dn = fetch_soft_unit(a, un, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        const float sd = a.s_dst[(int64_t)row * H + h];
+        // A unit longer than one pass parks its raw scores in alpha and the
+        // second sweep reads them back (each lane only its own elements):
+        // a contiguous re-read instead of a second random gather of s_src.
+        const bool park = end - beg > R * slots || part >= 0;
+        float m = -INFINITY, z = 0.f;
+        float ev[R];
+        for (int k0 = beg + slot; k0 < end + slot; k0 += R * slots) {
+            int cc[R];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int k = k0 + r * eps;
-            e[r] = (live && k < end) ? edge_e(a, sd, k, h) : -INFINITY;
+            for (int r = 0; r < R; ++r) {
+                const int k = k0 + r * slots;
+                cc[r] = col[k < end ? k : end - 1];
+            }
+            float mb = m;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const float sv = a.s_src[(int64_t)cc[r] * H + h];
+                ev[r] = (live && k0 + r * slots < end) ? leaky_relu(sd + sv, a.slope) : -INFINITY;
+                mb = fmaxf(mb, ev[r]);
+            }
+            if (park && live) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = k0 + r * slots;
+                    if (k < end) a.alpha[(int64_t)k * H + h] = ev[r];
+                }
+            }
+            if (mb > m) {
+                z *= __expf(m - mb);
+                m = mb;
+            }
+            // masked steps (score -inf) add nothing, also while m is still -inf
+            float zb = 0.f;
+#pragma unroll
+            for (int r = 0; r < R; ++r) zb += ev[r] == -INFINITY ? 0.f : __expf(ev[r] - m);
+            z += zb;
         }
-        float mb = m;
+        if (!live) { m = -INFINITY; z = 0.f; }
+        merge_slots(m, z, H, S, gbase);
+        if (part >= 0) {
+            if (slot == 0) {
+                a.gstats[(int64_t)part * a.sstride + h] = m;
+                a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + h] = z;
+            }
+        } else if (live && end > beg) {
+            const float rz = 1.f / z;
+            if (!park) {
+                // one pass: this lane's scores are still in ev
 #pragma unroll
-        for (int r = 0; r < R; ++r) mb = fmaxf(mb, e[r]);
-        if (mb > m) {
-            z *= __expf(m - mb);
-            m = mb;
+                for (int r = 0; r < R; ++r) {
+                    const int k = beg + slot + r * slots;
+                    if (k < end) a.alpha[(int64_t)k * H + h] = __expf(ev[r] - m) * rz;
+                }
+            } else {
+                // the parked scores, same lane-to-element map as when they were written
+                for (int k0 = beg + slot; k0 < end; k0 += R * slots) {
+                    float e[R];
+#pragma unroll
+                    for (int r = 0; r < R; ++r) {
+                        const int k = k0 + r * slots;
+                        e[r] = k < end ? a.alpha[(int64_t)k * H + h] : 0.f;
+                    }
+#pragma unroll
+                    for (int r = 0; r < R; ++r) {
+                        const int k = k0 + r * slots;
+                        if (k < end) a.alpha[(int64_t)k * H + h] = __expf(e[r] - m) * rz;
+                    }
+                }
+            }
         }
-        float zb = 0.f;
-#pragma unroll
-        for (int r = 0; r < R; ++r) zb += __expf(e[r] - m);
-        z += zb;
+        if (un >= hi) break;
+        u = un;
+        d = dn;
     }
-    if (!live) { m = -INFINITY; z = 0.f; }
-    merge_slots(m, z, H);
-    if (part >= 0) {
-        if (slot == 0) {
-            a.gstats[(int64_t)part * a.sstride + h] = m;
-            a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + h] = z;
-        }
-        return;
-    }
-    if (!live) return;
-    const float rz = 1.f / z;
-    for (int k = beg + slot; k < end; k += eps)
-        a.alpha[(int64_t)k * H + h] = __expf(edge_e(a, sd, k, h) - m) * rz;
 }
 
 // Per split row: merge the (m, z) of its groups in slot order (64/H chains,
@@ -396,7 +478,8 @@ __global__ __launch_bounds__(kBlock) void k_softmax_merge(const int4 *__restrict
     }
 }
 
-// alpha for the edges of split rows, one wavefront per neighbour group.
+// alpha for the edges of split rows, one wavefront per neighbour group: from
+// the raw scores k_softmax parked in alpha, or by gathering the scores again.
 __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
 {
     const int lane = lane_id();
@@ -411,9 +494,25 @@ __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
         const int4 d = a.part_units[p];
         const float m = a.rstats[(int64_t)d.w * a.sstride + h];
         const float rz = 1.f / a.rstats[(int64_t)d.w * a.sstride + (a.sstride >> 1) + h];
-        const float sd = a.s_dst[(int64_t)d.x * H + h];
-        for (int k = d.y + slot; k < d.z; k += eps)
-            a.alpha[(int64_t)k * H + h] = __expf(edge_e(a, sd, k, h) - m) * rz;
+        if (a.parked) {
+            constexpr int R = 8;
+            for (int k0 = d.y + slot; k0 < d.z; k0 += R * eps) {
+                float e[R];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = k0 + r * eps;
+                    e[r] = k < d.z ? a.alpha[(int64_t)k * H + h] : 0.f;
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = k0 + r * eps;
+                    if (k < d.z) a.alpha[(int64_t)k * H + h] = __expf(e[r] - m) * rz;
+                }
+            }
+        } else {
+            const float sd = a.s_dst[(int64_t)d.x * H + h];
+            alpha_sweep<8>(a.col, a.s_src, a.alpha, H, h, sd, a.slope, m, rz, d.y, d.z, slot, eps);
+        }
     }
 }
 
@@ -578,7 +677,8 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
 
     SoftArgs a{};
     a.units = P ? P->units : nullptr;
-    a.n_units = P ? P->n_units_dev() : nullptr;
+    a.u_lo = P ? P->zero_dev() : nullptr;
+    a.u_hi = P ? P->n_big_dev() : nullptr;
     a.n_rows = n_rows;
     a.rowptr = rowptr;
     a.col = col;
@@ -592,10 +692,30 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
     a.part_units = P ? P->part_units : nullptr;
     a.n_parts = P ? P->n_parts_dev() : nullptr;
     a.rstats = P ? P->rstats : nullptr;
+    // Units with more than kTinyUnit edges: a wavefront each, 8 steps of 64 / H
+    // edges in flight.  The sorted tail of tiny units: 4H lanes each (at most
+    // 64), two steps, so that one pass covers a unit of kTinyUnit edges.
     const int64_t units = P ? P->cap_units : n_rows;
-    const unsigned blocks = (unsigned)((units + (kBlock / kWave) - 1) / (kBlock / kWave));
-    COGDL_LAUNCH("softmax", k_softmax, blocks, kBlock, stream, a);
+    auto launch = [&](const char *name, void (*k)(SoftArgs), const SoftArgs &args) {
+        const int64_t upb = kBlock >> args.log2S;
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH(name, k, (unsigned)(blocks > 0 ? blocks : 1), kBlock, stream, args);
+        return COGDL_OK;
+    };
+    a.log2S = 6;
+    a.parked = 1;
+    if (!P) a.u_hi = nullptr;
+    st = launch("softmax", k_softmax<8>, a);
+    if (st != COGDL_OK) return st;
     if (P) {
+        SoftArgs b = a;
+        b.u_lo = P->n_big_dev();
+        b.u_hi = P->n_units_dev();
+        b.log2S = log2i(next_pow2(4 * H) < kWave ? next_pow2(4 * H) : kWave);
+        st = launch("softmax_tiny", k_softmax<2>, b);
+        if (st != COGDL_OK) return st;
         COGDL_LAUNCH("softmax_merge", k_softmax_merge, grid_waves(P->cap_split), kBlock, stream,
                      P->split_rows, P->n_split_dev(), P->gstats, a.sstride, H, P->rstats);
         COGDL_LAUNCH("softmax_alpha_split", k_alpha_split, grid_waves(P->cap_partials), kBlock,

@@ -408,7 +408,7 @@ def test_sddmm_edge_softmax(cg, kind, H):
     rp, cl, _ = graph_to_dev(g)
     sd, ss = _scores(g.n_rows, g.n_cols, H, 40 + H)
     a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
-    for spec in (None, ("auto", 0), ("neighbor_group", 7)):
+    for spec in (None, ("auto", 0), ("row_split", 0), ("neighbor_group", 7), ("neighbor_group", 3)):
         plan = _make_plan(cg, rp, g.nnz, spec, 1, max_heads=H)
         try:
             a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
