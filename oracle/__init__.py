@@ -57,6 +57,9 @@ def _load():
     lib.oracle_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, i32, i32, P, P, P]
     lib.oracle_edge_softmax.argtypes = [i32, i32, i64, P, P, i32, P, P, dbl, i32, P, P]
     lib.oracle_gat.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, dbl, P, P, i32, i32, P, P, P]
+    lib.oracle_gat_backward.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, dbl, P, P, i32, P, i32,
+                                        i32, P, P, P, P, P, P, P, i32, P, P, P, P, P]
+    lib.oracle_sddmm_dot.argtypes = [i32, i32, i64, P, P, i32, i32, P, i32, P, i32, i32, P, P, P]
     _lib = lib
     return lib
 
@@ -233,3 +236,56 @@ def gat(rowptr, col, s_dst, s_src, X, H, D, slope=0.2, alpha_in=None, x_dtype=No
                             0 if sel is None else sel.size, _p(sel), _p(Y), _p(A))
     _check(rc, "gat")
     return Y, A
+
+
+def _edges_of_rows(rp, sel):
+    if sel is None:
+        return int(rp[-1])
+    return int(np.sum(rp[sel + 1].astype(np.int64) - rp[sel]))
+
+
+def gat_backward(rowptr, col, s_dst, s_src, alpha, X, dY, H, D, slope=0.2, x_dtype=None,
+                 dy_dtype=None, rows=None, cols=None, n_cols=None):
+    """Gradients of the GAT layer (see oracle.c).  Returns a dict of float64 arrays:
+    dalpha, dscore ([edges of the selected rows, H]), ds_dst ([rows, H]), ds_src
+    ([cols, H]), dX ([cols, H*D]), each with its error scale under the key + "_abs"."""
+    rp, cl = _c(rowptr, np.int32), _c(col, np.int32)
+    sd, ss, al = _c(s_dst, np.float32), _c(s_src, np.float32), _c(alpha, np.float32)
+    X, dY = np.ascontiguousarray(X), np.ascontiguousarray(dY)
+    n_rows = rp.size - 1
+    n_cols = X.shape[0] if n_cols is None else n_cols
+    sel, csel = _c(rows, np.int32), _c(cols, np.int32)
+    n_e = _edges_of_rows(rp, sel)
+    n_r = n_rows if sel is None else sel.size
+    n_c = n_cols if csel is None else csel.size
+    out = {k: np.empty(shape, np.float64) for k, shape in (
+        ("dalpha", (n_e, H)), ("dalpha_abs", (n_e, H)), ("dscore", (n_e, H)), ("dscore_abs", (n_e, H)),
+        ("ds_dst", (n_r, H)), ("ds_dst_abs", (n_r, H)), ("ds_src", (n_c, H)), ("ds_src_abs", (n_c, H)),
+        ("dX", (n_c, H * D)), ("dX_abs", (n_c, H * D)))}
+    rc = _load().oracle_gat_backward(
+        n_rows, n_cols, int(rp[-1]), _p(rp), _p(cl), H, D, _p(sd), _p(ss), float(slope), _p(al),
+        _p(X), _x_code(X, x_dtype), _p(dY), _x_code(dY, dy_dtype),
+        0 if sel is None else sel.size, _p(sel), _p(out["dalpha"]), _p(out["dalpha_abs"]),
+        _p(out["dscore"]), _p(out["dscore_abs"]), _p(out["ds_dst"]), _p(out["ds_dst_abs"]),
+        0 if csel is None else csel.size, _p(csel), _p(out["ds_src"]), _p(out["ds_src_abs"]),
+        _p(out["dX"]), _p(out["dX_abs"]))
+    _check(rc, "gat_backward")
+    return out
+
+
+def sddmm_dot(rowptr, col, P, Q, H, D, p_dtype=None, q_dtype=None, rows=None, n_cols=None):
+    """out[k,h] = <P[i,h,:], Q[col[k],h,:]> (section 2.2 SDDMM per head).  Returns
+    (out, Abs) float64 [edges of the selected rows, H]."""
+    rp, cl = _c(rowptr, np.int32), _c(col, np.int32)
+    P, Q = np.ascontiguousarray(P), np.ascontiguousarray(Q)
+    n_rows = rp.size - 1
+    n_cols = Q.shape[0] if n_cols is None else n_cols
+    sel = _c(rows, np.int32)
+    n_e = _edges_of_rows(rp, sel)
+    out = np.empty((n_e, H), np.float64)
+    ab = np.empty((n_e, H), np.float64)
+    rc = _load().oracle_sddmm_dot(n_rows, n_cols, int(rp[-1]), _p(rp), _p(cl), H, D, _p(P),
+                                  _x_code(P, p_dtype), _p(Q), _x_code(Q, q_dtype),
+                                  0 if sel is None else sel.size, _p(sel), _p(out), _p(ab))
+    _check(rc, "sddmm_dot")
+    return out, ab

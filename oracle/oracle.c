@@ -441,3 +441,216 @@ int oracle_gat(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowpt
     }
     return rc;
 }
+
+/* ---------------------------------------------------- GAT backward (next) */
+
+/* Gradients of the GAT layer of section 2.2 for a loss L with dY = dL/dY,
+ * derived by the chain rule through the forward operators (score SDDMM,
+ * LeakyReLU, edge softmax per row, weighted multi-head SpMM).  For edge
+ * k = (i, j) and head h, with alpha the forward weights (given, used exactly):
+ *   dalpha[k,h] = sum_d dY[i,h,d] * X[j,h,d]
+ *                 (the dot-product SDDMM A (.) (dY_h X_h^T) of section 2.2,
+ *                  which carries the gradient to the attention matrix)
+ *   c[i,h]      = sum_{k in row i} alpha[k,h] * dalpha[k,h]
+ *   dscore[k,h] = f_kh * alpha[k,h] * (dalpha[k,h] - c[i,h])
+ *                 (softmax backward times the LeakyReLU slope: f = 1 when the
+ *                  pre-activation t = s_dst[i,h] + s_src[j,h] is > 0, else slope)
+ *   ds_dst[i,h] = sum_{k in row i} dscore[k,h]
+ *   ds_src[j,h] = sum_{k: col[k] = j} dscore[k,h]
+ *   dX[j,h,d]   = sum_{k: col[k] = j} alpha[k,h] * dY[i,h,d]
+ * Each value comes with its error scale (_abs): the same expression with
+ * every term replaced by its absolute value and every difference by a sum.
+ * Row outputs (dalpha, dscore: packed edges of the selected rows in list and
+ * CSR order; ds_dst) are for rows sel[0..n_sel) (all when sel is NULL);
+ * column outputs (ds_src, dX) for columns csel[0..n_csel) (all when NULL).
+ * Any output may be NULL.  Sums run over edges in CSR order. */
+static void gat_bwd_row(int32_t i, const int32_t *rowptr, const int32_t *col, int32_t H,
+                        int32_t D, const float *s_dst, const float *s_src, double slope,
+                        const float *alpha, const void *X, int32_t x_dtype, const void *dY,
+                        int32_t dy_dtype, double *da, double *da_abs, double *dt, double *dt_abs)
+{
+    int32_t beg = rowptr[i], end = rowptr[i + 1];
+    int64_t HD = (int64_t)H * D;
+    for (int32_t h = 0; h < H; ++h) {
+        double c = 0.0, c_abs = 0.0;
+        for (int32_t k = beg; k < end; ++k) {
+            double s = 0.0, s_abs = 0.0;
+            for (int32_t d = 0; d < D; ++d) {
+                double g = load_elem(dY, dy_dtype, (int64_t)i * HD + (int64_t)h * D + d);
+                double x = load_elem(X, x_dtype, (int64_t)col[k] * HD + (int64_t)h * D + d);
+                s += g * x;
+                s_abs += fabs(g) * fabs(x);
+            }
+            int64_t e = (int64_t)(k - beg) * H + h;
+            da[e] = s;
+            da_abs[e] = s_abs;
+            double a = (double)alpha[(int64_t)k * H + h];
+            c += a * s;
+            c_abs += fabs(a) * s_abs;
+        }
+        for (int32_t k = beg; k < end; ++k) {
+            int64_t e = (int64_t)(k - beg) * H + h;
+            double t = (double)s_dst[(int64_t)i * H + h] + (double)s_src[(int64_t)col[k] * H + h];
+            double f = t > 0.0 ? 1.0 : slope;
+            double a = (double)alpha[(int64_t)k * H + h];
+            dt[e] = f * a * (da[e] - c);
+            dt_abs[e] = fabs(f) * fabs(a) * (da_abs[e] + c_abs);
+        }
+    }
+}
+
+int oracle_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                        const int32_t *col, int32_t H, int32_t D, const float *s_dst,
+                        const float *s_src, double slope, const float *alpha, const void *X,
+                        int32_t x_dtype, const void *dY, int32_t dy_dtype, int32_t n_sel,
+                        const int32_t *sel, double *dalpha, double *dalpha_abs, double *dscore,
+                        double *dscore_abs, double *ds_dst, double *ds_dst_abs, int32_t n_csel,
+                        const int32_t *csel, double *ds_src, double *ds_src_abs, double *dX,
+                        double *dX_abs)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || H < 1 || D < 0) return -1;
+    int64_t HD = (int64_t)H * D;
+    int rc = 0;
+
+    /* row outputs */
+    int32_t n_out = sel ? n_sel : n_rows;
+    int64_t *off = (int64_t *)malloc(sizeof(int64_t) * ((size_t)n_out + 1));
+    if (!off) return -3;
+    off[0] = 0;
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        off[r + 1] = off[r] + (rowptr[i + 1] - rowptr[i]);
+    }
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        int32_t deg = rowptr[i + 1] - rowptr[i];
+        size_t n = (size_t)deg * H + 1;
+        double *da = (double *)malloc(sizeof(double) * n), *dab = (double *)malloc(sizeof(double) * n);
+        double *dt = (double *)malloc(sizeof(double) * n), *dtb = (double *)malloc(sizeof(double) * n);
+        if (!da || !dab || !dt || !dtb) {
+            rc = -3;
+        } else {
+            gat_bwd_row(i, rowptr, col, H, D, s_dst, s_src, slope, alpha, X, x_dtype, dY, dy_dtype,
+                        da, dab, dt, dtb);
+            for (int32_t h = 0; h < H; ++h) {
+                double s = 0.0, sb = 0.0;
+                for (int32_t e = 0; e < deg; ++e) {
+                    int64_t q = (off[r] + e) * H + h, p = (int64_t)e * H + h;
+                    if (dalpha) dalpha[q] = da[p];
+                    if (dalpha_abs) dalpha_abs[q] = dab[p];
+                    if (dscore) dscore[q] = dt[p];
+                    if (dscore_abs) dscore_abs[q] = dtb[p];
+                    s += dt[p];
+                    sb += dtb[p];
+                }
+                if (ds_dst) ds_dst[(int64_t)r * H + h] = s;
+                if (ds_dst_abs) ds_dst_abs[(int64_t)r * H + h] = sb;
+            }
+        }
+        free(da); free(dab); free(dt); free(dtb);
+    }
+    free(off);
+    if (rc != 0 || (!ds_src && !ds_src_abs && !dX && !dX_abs)) return rc;
+
+    /* column outputs: the edges into the selected columns, from the rows holding them */
+    int32_t n_cout = csel ? n_csel : n_cols;
+    int32_t *slot = (int32_t *)malloc(sizeof(int32_t) * ((size_t)n_cols + 1));
+    char *need = (char *)calloc((size_t)n_rows + 1, 1);
+    int64_t *roff = (int64_t *)malloc(sizeof(int64_t) * ((size_t)n_rows + 1));
+    if (!slot || !need || !roff) { free(slot); free(need); free(roff); return -3; }
+    for (int32_t j = 0; j < n_cols; ++j) slot[j] = csel ? -1 : j;
+    if (csel)
+        for (int32_t c = 0; c < n_csel; ++c) slot[csel[c]] = c;
+    for (int32_t i = 0; i < n_rows; ++i)
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1] && !need[i]; ++k)
+            if (slot[col[k]] >= 0) need[i] = 1;
+    roff[0] = 0;
+    for (int32_t i = 0; i < n_rows; ++i)
+        roff[i + 1] = roff[i] + (need[i] ? (int64_t)(rowptr[i + 1] - rowptr[i]) * H : 0);
+    double *dt = (double *)malloc(sizeof(double) * ((size_t)roff[n_rows] + 1));
+    double *dtb = (double *)malloc(sizeof(double) * ((size_t)roff[n_rows] + 1));
+    if (!dt || !dtb) { free(slot); free(need); free(roff); free(dt); free(dtb); return -3; }
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int32_t i = 0; i < n_rows; ++i) {
+        if (!need[i]) continue;
+        size_t n = (size_t)(rowptr[i + 1] - rowptr[i]) * H + 1;
+        double *da = (double *)malloc(sizeof(double) * n), *dab = (double *)malloc(sizeof(double) * n);
+        if (!da || !dab) { rc = -3; free(da); free(dab); continue; }
+        gat_bwd_row(i, rowptr, col, H, D, s_dst, s_src, slope, alpha, X, x_dtype, dY, dy_dtype,
+                    da, dab, dt + roff[i], dtb + roff[i]);
+        free(da); free(dab);
+    }
+    if (rc == 0) {
+        for (int32_t c = 0; c < n_cout; ++c) {
+            for (int32_t h = 0; h < H; ++h) {
+                if (ds_src) ds_src[(int64_t)c * H + h] = 0.0;
+                if (ds_src_abs) ds_src_abs[(int64_t)c * H + h] = 0.0;
+            }
+            for (int64_t t = 0; t < HD; ++t) {
+                if (dX) dX[(int64_t)c * HD + t] = 0.0;
+                if (dX_abs) dX_abs[(int64_t)c * HD + t] = 0.0;
+            }
+        }
+        for (int32_t i = 0; i < n_rows; ++i) {
+            if (!need[i]) continue;
+            for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
+                int32_t c = slot[col[k]];
+                if (c < 0) continue;
+                for (int32_t h = 0; h < H; ++h) {
+                    int64_t p = roff[i] + (int64_t)(k - rowptr[i]) * H + h;
+                    if (ds_src) ds_src[(int64_t)c * H + h] += dt[p];
+                    if (ds_src_abs) ds_src_abs[(int64_t)c * H + h] += dtb[p];
+                    double a = (double)alpha[(int64_t)k * H + h];
+                    for (int32_t d = 0; d < D; ++d) {
+                        double g = load_elem(dY, dy_dtype, (int64_t)i * HD + (int64_t)h * D + d);
+                        if (dX) dX[(int64_t)c * HD + (int64_t)h * D + d] += a * g;
+                        if (dX_abs) dX_abs[(int64_t)c * HD + (int64_t)h * D + d] += fabs(a) * fabs(g);
+                    }
+                }
+            }
+        }
+    }
+    free(slot); free(need); free(roff); free(dt); free(dtb);
+    return rc;
+}
+
+/* The dot-product SDDMM of section 2.2, T = A (.) (P Q^T), per head:
+ *   out[k,h] = sum_d P[i,h,d] * Q[col[k],h,d]   for edge k = (i, col[k])
+ * (structure only: the edge values of A are not applied), with its error
+ * scale; rows sel[0..n_sel) (all when NULL), edges packed as above. */
+int oracle_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                     const int32_t *col, int32_t H, int32_t D, const void *P, int32_t p_dtype,
+                     const void *Q, int32_t q_dtype, int32_t n_sel, const int32_t *sel, double *out,
+                     double *out_abs)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || H < 1 || D < 0) return -1;
+    int64_t HD = (int64_t)H * D;
+    int32_t n_out = sel ? n_sel : n_rows;
+    int64_t *off = (int64_t *)malloc(sizeof(int64_t) * ((size_t)n_out + 1));
+    if (!off) return -3;
+    off[0] = 0;
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        off[r + 1] = off[r] + (rowptr[i + 1] - rowptr[i]);
+    }
+    #pragma omp parallel for schedule(dynamic, 64)
+    for (int32_t r = 0; r < n_out; ++r) {
+        int32_t i = sel ? sel[r] : r;
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k)
+            for (int32_t h = 0; h < H; ++h) {
+                double s = 0.0, sb = 0.0;
+                for (int32_t d = 0; d < D; ++d) {
+                    double p = load_elem(P, p_dtype, (int64_t)i * HD + (int64_t)h * D + d);
+                    double q = load_elem(Q, q_dtype, (int64_t)col[k] * HD + (int64_t)h * D + d);
+                    s += p * q;
+                    sb += fabs(p) * fabs(q);
+                }
+                int64_t e = (off[r] + (k - rowptr[i])) * H + h;
+                out[e] = s;
+                if (out_abs) out_abs[e] = sb;
+            }
+    }
+    free(off);
+    return 0;
+}

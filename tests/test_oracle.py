@@ -634,3 +634,155 @@ def test_gspmm_compute_hand_example():
     assert arg.tolist() == [[1, 1], [-1, -1]]
     Y, _, _ = oracle.gspmm(rowptr, col, val, X, "mean", compute="sub")
     assert Y.tolist() == [[(-1.5 + 2.0) / 2, (-2.25 - 2.0) / 2], [0.0, 0.0]]
+
+
+# ------------------------------------------------------------ GAT backward
+
+def _dense_heads(g, H, D, Xf, dYf):
+    return Xf.reshape(g.n_cols, H, D).astype(np.float64), dYf.reshape(g.n_rows, H, D).astype(np.float64)
+
+
+def test_sddmm_dot_dense():
+    """out[k,h] = (P_h Q_h^T)[i, col[k]] for every edge, duplicates included."""
+    rng = np.random.default_rng(40)
+    for g in _graphs(8):
+        H, D = 3, 5
+        P = rng.standard_normal((g.n_rows, H * D)).astype(np.float32)
+        Q = rng.standard_normal((g.n_cols, H * D)).astype(np.float32)
+        out, ab = oracle.sddmm_dot(g.rowptr, g.col, P, Q, H, D)
+        rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+        for h in range(H):
+            M = P.reshape(-1, H, D)[:, h, :].astype(np.float64) @ Q.reshape(-1, H, D)[:, h, :].astype(np.float64).T
+            Ma = np.abs(P.reshape(-1, H, D)[:, h, :].astype(np.float64)) @ np.abs(Q.reshape(-1, H, D)[:, h, :].astype(np.float64)).T
+            np.testing.assert_allclose(out[:, h], M[rows, g.col], rtol=1e-13, atol=1e-13)
+            np.testing.assert_allclose(ab[:, h], Ma[rows, g.col], rtol=1e-13, atol=1e-13)
+        # selected rows pack their edges in list order
+        sel = np.array([g.n_rows - 1, 0], np.int32)
+        o2, _ = oracle.sddmm_dot(g.rowptr, g.col, P, Q, H, D, rows=sel)
+        idx = np.concatenate([np.arange(g.rowptr[r], g.rowptr[r + 1]) for r in sel])
+        assert np.array_equal(o2, out[idx])
+
+
+def test_gat_backward_hand_example():
+    # one row, two edges, H = D = 1; alpha is an input of the backward, chosen by hand
+    rowptr = np.array([0, 2], np.int32)
+    col = np.array([0, 1], np.int32)
+    X = np.array([[2.0], [3.0]], np.float32)
+    dY = np.array([[1.0]], np.float32)
+    s_dst = np.array([[0.0]], np.float32)
+    s_src = np.array([[1.0], [-1.0]], np.float32)
+    alpha = np.array([[0.75], [0.25]], np.float32)
+    r = oracle.gat_backward(rowptr, col, s_dst, s_src, alpha, X, dY, 1, 1, slope=0.2)
+    assert r["dalpha"].ravel().tolist() == [2.0, 3.0]
+    # c = 0.75*2 + 0.25*3 = 2.25; t = (1, -1) -> f = (1, 0.2)
+    assert r["dscore"].ravel().tolist() == [0.75 * (2 - 2.25), 0.2 * 0.25 * (3 - 2.25)]
+    assert r["ds_dst"].ravel().tolist() == [0.75 * (2 - 2.25) + 0.2 * 0.25 * (3 - 2.25)]
+    assert r["ds_src"].ravel().tolist() == [0.75 * (2 - 2.25), 0.2 * 0.25 * (3 - 2.25)]
+    assert r["dX"].ravel().tolist() == [0.75, 0.25]
+
+
+def _softmax_forward_dense(g, sd, ss, X, H, D, slope):
+    """Dense fp64 GAT forward on a graph without duplicate edges."""
+    mask = np.zeros((g.n_rows, g.n_cols), bool)
+    rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+    mask[rows, g.col] = True
+    Y = np.zeros((g.n_rows, H, D))
+    A = np.zeros((H, g.n_rows, g.n_cols))
+    for h in range(H):
+        t = sd[:, h, None] + ss[None, :, h]
+        e = np.where(t > 0, t, slope * t)
+        e = np.where(mask, e, -np.inf)
+        m = e.max(1, keepdims=True)
+        m[~np.isfinite(m)] = 0.0
+        p = np.where(mask, np.exp(e - m), 0.0)
+        z = p.sum(1, keepdims=True)
+        a = np.divide(p, z, out=np.zeros_like(p), where=z > 0)
+        A[h] = a
+        Y[:, h, :] = a @ X[:, h, :]
+    return Y, A
+
+
+def test_gat_backward_matches_finite_differences():
+    """ds_dst and ds_src against central differences of a dense fp64 forward,
+    dX against the transposed dense attention, dalpha against the dense SDDMM."""
+    rng = np.random.default_rng(41)
+    H, D, slope = 2, 3, 0.2
+    for n in (6, 11, 16):
+        g = synth.random_csr(n, n, rng, mean_deg=3, empty_frac=0.1)
+        while True:
+            sd = rng.standard_normal((n, H)).astype(np.float32)
+            ss = rng.standard_normal((n, H)).astype(np.float32)
+            t = sd.astype(np.float64)[np.repeat(np.arange(n), np.diff(g.rowptr))] + ss.astype(np.float64)[g.col]
+            if np.abs(t).min() > 1e-2:      # keep clear of the LeakyReLU kink
+                break
+        X = rng.standard_normal((n, H * D)).astype(np.float32)
+        dY = rng.standard_normal((n, H * D)).astype(np.float32)
+        Xd, dYd = _dense_heads(g, H, D, X, dY)
+        _, A = _softmax_forward_dense(g, sd.astype(np.float64), ss.astype(np.float64), Xd, H, D, slope)
+        rows = np.repeat(np.arange(n), np.diff(g.rowptr))
+        alpha = np.stack([A[h][rows, g.col] for h in range(H)], 1).astype(np.float32)
+        r = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, X, dY, H, D, slope=slope)
+
+        def loss(sd64, ss64):
+            Y, _ = _softmax_forward_dense(g, sd64, ss64, Xd, H, D, slope)
+            return float(np.sum(Y * dYd))
+
+        eps = 1e-6
+        base_d, base_s = sd.astype(np.float64), ss.astype(np.float64)
+        fd_dst = np.zeros((n, H))
+        fd_src = np.zeros((n, H))
+        for i in range(n):
+            for h in range(H):
+                p, m = base_d.copy(), base_d.copy()
+                p[i, h] += eps
+                m[i, h] -= eps
+                fd_dst[i, h] = (loss(p, base_s) - loss(m, base_s)) / (2 * eps)
+                p, m = base_s.copy(), base_s.copy()
+                p[i, h] += eps
+                m[i, h] -= eps
+                fd_src[i, h] = (loss(base_d, p) - loss(base_d, m)) / (2 * eps)
+        # alpha is rounded to fp32 for the backward: agreement to ~1e-6 of the scale
+        scale = np.abs(fd_dst).max() + np.abs(fd_src).max() + 1.0
+        assert np.abs(r["ds_dst"] - fd_dst).max() <= 2e-6 * scale
+        assert np.abs(r["ds_src"] - fd_src).max() <= 2e-6 * scale
+        for h in range(H):
+            dXh = A[h].astype(np.float32).astype(np.float64).T @ dYd[:, h, :]
+            np.testing.assert_allclose(r["dX"].reshape(n, H, D)[:, h, :], dXh, rtol=1e-12, atol=1e-12)
+            M = dYd[:, h, :] @ Xd[:, h, :].T
+            np.testing.assert_allclose(r["dalpha"][:, h], M[rows, g.col], rtol=1e-12, atol=1e-12)
+
+
+def test_gat_backward_invariants():
+    rng = np.random.default_rng(42)
+    H, D = 3, 4
+    for g in _graphs(9):
+        sd = rng.standard_normal((g.n_rows, H)).astype(np.float32)
+        ss = rng.standard_normal((g.n_cols, H)).astype(np.float32)
+        alpha = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=1.0).astype(np.float32)
+        X = rng.standard_normal((g.n_cols, H * D)).astype(np.float32)
+        dY = rng.standard_normal((g.n_rows, H * D)).astype(np.float32)
+        # slope 1: the softmax backward sums to zero over each row (sum alpha = 1)
+        r = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, X, dY, H, D, slope=1.0)
+        assert np.all(np.abs(r["ds_dst"]) <= 1e-6 * r["ds_dst_abs"] + 1e-300)
+        # degree-1 rows: alpha = 1 exactly, so their score gradients are exactly 0
+        d = np.diff(g.rowptr)
+        one = np.flatnonzero(np.repeat(d, d) == 1)
+        assert np.all(r["dscore"][one] == 0.0)
+        # adjoint identity for dX with the forward aggregation at fixed weights
+        Z = rng.standard_normal((g.n_cols, H * D)).astype(np.float32)
+        Yz, _ = oracle.gat(g.rowptr, g.col, None, None, Z, H, D, alpha_in=alpha)
+        lhs = float(np.sum(r["dX"] * Z.astype(np.float64)))
+        rhs = float(np.sum(Yz * dY.astype(np.float64)))
+        assert abs(lhs - rhs) <= 1e-11 * (np.abs(r["dX"]).sum() * np.abs(Z).max() + 1.0)
+        # dalpha is the dot-product SDDMM of dY and X
+        dot, _ = oracle.sddmm_dot(g.rowptr, g.col, dY, X, H, D)
+        assert np.array_equal(dot, r["dalpha"])
+        # row and column selections give the same values
+        sel = np.array([g.n_rows - 1, 0], np.int32)
+        csel = np.array([g.n_cols - 1, 0], np.int32)
+        r2 = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, X, dY, H, D, slope=1.0, rows=sel, cols=csel)
+        assert np.array_equal(r2["ds_dst"], r["ds_dst"][sel])
+        assert np.array_equal(r2["ds_src"], r["ds_src"][csel])
+        assert np.array_equal(r2["dX"], r["dX"][csel])
+        idx = np.concatenate([np.arange(g.rowptr[x], g.rowptr[x + 1]) for x in sel])
+        assert np.array_equal(r2["dscore"], r["dscore"][idx])
