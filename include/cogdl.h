@@ -258,6 +258,50 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                  const cogdl_plan *plan, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Dot-product SDDMM -- section 2.2, T = A (.) (P Q^T), per head: for every
+ * edge k = (i, col[k]) and head h
+ *     out[k * H + h] = sum_d P[i, h, d] * Q[col[k], h, d]
+ * P: n_rows x H x D of p_dtype; Q: n_cols x H x D of q_dtype; out: nnz x H
+ * fp32 (the structure of A only: edge values are not applied).  fp32
+ * accumulation.  plan: NULL or a plan on this rowptr (any max_feat).
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                             const int32_t *col, int32_t H, int32_t D, const void *P,
+                             cogdl_dtype p_dtype, const void *Q, cogdl_dtype q_dtype, float *out,
+                             const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Backward of the attention layer of cogdl_gat_aggregate (section 2.2: the
+ * SDDMM carries the loss gradient to the attention matrix; the rest is the
+ * chain rule through the edge softmax, LeakyReLU and the multi-head SpMM).
+ * Given dY = dL/dY (n_rows x H x D) and the forward weights alpha (nnz x H,
+ * as written by cogdl_gat_aggregate's alpha_out), for edge k = (i, j):
+ *   dalpha[k,h] = sum_d dY[i,h,d] * X[j,h,d]
+ *   c[i,h]      = sum_{k in row i} alpha[k,h] * dalpha[k,h]
+ *   dscore[k,h] = f * alpha[k,h] * (dalpha[k,h] - c[i,h]),  f = 1 when
+ *                 s_dst[i,h] + s_src[j,h] > 0, else negative_slope
+ *                 (dL/d of the pre-activation score)
+ *   ds_dst[i,h] = sum_{k in row i} dscore[k,h]     (n_rows x H)
+ *   ds_src[j,h] = sum_{k: col[k] = j} dscore[k,h]  (n_cols x H)
+ *   dX[j,h,:]   = sum_{k: col[k] = j} alpha[k,h] * dY[i,h,:]   (n_cols x H x D)
+ * colptr, row_t, perm: the CSC of the same graph from cogdl_csr_to_csc.
+ * plan: NULL or a plan on rowptr with max_heads >= H; plan_t: NULL or a plan
+ * on colptr with max_feat >= H*D and max_heads >= H.  dalpha and dscore are
+ * nnz x H fp32 outputs (dscore also serves as scratch during the call).
+ * fp32 accumulation; every output is overwritten.  Both plans' workspaces are
+ * used: one call per plan pair in flight.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                const int32_t *rowptr, const int32_t *col, const int32_t *colptr,
+                                const int32_t *row_t, const int32_t *perm, int32_t H, int32_t D,
+                                const float *s_dst, const float *s_src, float negative_slope,
+                                const float *alpha, const void *X, cogdl_dtype x_dtype,
+                                const void *dY, cogdl_dtype dy_dtype, void *dX,
+                                cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
+                                float *ds_src, const cogdl_plan *plan, const cogdl_plan *plan_t,
+                                hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Kernel tracing (instrumentation, not part of the paper's method).  When
  * enabled, every kernel the library launches is bracketed by two HIP events
  * recorded on its launch stream, so the device time of each launch can be

@@ -7,10 +7,13 @@ binding fails loudly when the library or a GPU is missing: there is no CPU
 fallback.
 
     spmm(rowptr, col, val, X, plan=None, out_dtype=None)          -> Y = A X
+    gspmm(rowptr, col, val, X, reduce, compute=..., ...)          -> Eq. 1 with sum/mean/max, mul/add/sub/copy
     csr_to_csc(rowptr, col, val, n_cols)                          -> colptr, row_t, val_t, perm
     spmm_t(colptr, row_t, val_t, G, plan_t=None, out_dtype=None)  -> dX = A^T G
     sddmm_edge_softmax(rowptr, col, s_dst, s_src, slope, plan)    -> alpha [nnz, H]
     gat_aggregate(rowptr, col, s_dst, s_src, X, slope, ...)       -> Y [n, H, D] (, alpha)
+    sddmm_dot(rowptr, col, P, Q)                                  -> <P[i,h], Q[j,h]> per edge
+    gat_backward(rowptr, col, colptr, row_t, perm, ..., dY)       -> dX, dalpha, dscore, ds_dst, ds_src
     Plan(rowptr, nnz, max_feat, max_heads, mode, group_size)      -> the workload balancer
 """
 from __future__ import annotations
@@ -68,12 +71,18 @@ def lib():
     L.cogdl_sddmm_edge_softmax.argtypes = [i32, i32, i64, P, P, i32, P, P, f32, P, P, P]
     L.cogdl_gat_aggregate.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, P, ctypes.c_int,
                                       P, ctypes.c_int, P, P, P]
+    L.cogdl_sddmm_dot.argtypes = [i32, i32, i64, P, P, i32, i32, P, ctypes.c_int, P, ctypes.c_int,
+                                  P, P, P]
+    L.cogdl_gat_backward.argtypes = [i32, i32, i64, P, P, P, P, P, i32, i32, P, P, f32, P, P,
+                                     ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P,
+                                     P, P]
     L.cogdl_trace_enable.argtypes = [i32]
     L.cogdl_trace_count.restype = i32
     L.cogdl_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
     for name in ("cogdl_trace_enable", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
-                 "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate"):
+                 "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate",
+                 "cogdl_sddmm_dot", "cogdl_gat_backward"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -331,3 +340,59 @@ def gat_aggregate(rowptr, col, s_dst, s_src, X, negative_slope: float = 0.2, alp
                                      _dtype_code(X), _ptr(out), _dtype_code(out), _ptr(alpha_out),
                                      _plan_handle(plan), _stream()), "cogdl_gat_aggregate")
     return (out, alpha_out) if return_alpha else out
+
+
+def sddmm_dot(rowptr, col, P, Q, plan: Plan | None = None, out=None):
+    """out[k, h] = <P[i, h, :], Q[col[k], h, :]> for every edge k = (i, col[k]):
+    the SDDMM of section 2.2 per head.  P is [n_rows, H, D], Q [n_cols, H, D]."""
+    import torch
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(P, "P"), _dev(Q, "Q")
+    if P.dim() != 3 or Q.dim() != 3 or P.shape[1:] != Q.shape[1:]:
+        raise CogdlError("P and Q must be [n, H, D] with the same H and D")
+    _, H, D = P.shape
+    n_rows = rowptr.numel() - 1
+    nnz = col.numel()
+    if out is None:
+        out = torch.empty((nnz, H), dtype=torch.float32, device=P.device)
+    _dev(out, "out", torch.float32)
+    _check(lib().cogdl_sddmm_dot(n_rows, Q.shape[0], nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(P),
+                                 _dtype_code(P), _ptr(Q), _dtype_code(Q), _ptr(out), _plan_handle(plan),
+                                 _stream()), "cogdl_sddmm_dot")
+    return out
+
+
+def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
+                 negative_slope: float = 0.2, plan: Plan | None = None, plan_t: Plan | None = None,
+                 dx_dtype=None, out=None):
+    """Gradients of gat_aggregate for dY = dL/dY.  X is [n_cols, H, D], dY [n_rows, H, D],
+    alpha [nnz, H] the forward weights; (colptr, row_t, perm) the CSC from csr_to_csc.
+    Returns dict(dX, dalpha, dscore, ds_dst, ds_src); ``out`` may supply these tensors."""
+    import torch
+    for t, name, dt in ((rowptr, "rowptr", torch.int32), (col, "col", torch.int32),
+                        (colptr, "colptr", torch.int32), (row_t, "row_t", torch.int32),
+                        (perm, "perm", torch.int32), (s_dst, "s_dst", torch.float32),
+                        (s_src, "s_src", torch.float32), (alpha, "alpha", torch.float32)):
+        _dev(t, name, dt)
+    _dev(X, "X"), _dev(dY, "dY")
+    if X.dim() != 3 or dY.dim() != 3 or X.shape[1:] != dY.shape[1:]:
+        raise CogdlError("X and dY must be [n, H, D] with the same H and D")
+    n_cols, H, D = X.shape
+    n_rows = rowptr.numel() - 1
+    nnz = col.numel()
+    dev = X.device
+    o = dict(out or {})
+    o.setdefault("dX", torch.empty((n_cols, H, D), dtype=dx_dtype or X.dtype, device=dev))
+    o.setdefault("dalpha", torch.empty((nnz, H), dtype=torch.float32, device=dev))
+    o.setdefault("dscore", torch.empty((nnz, H), dtype=torch.float32, device=dev))
+    o.setdefault("ds_dst", torch.empty((n_rows, H), dtype=torch.float32, device=dev))
+    o.setdefault("ds_src", torch.empty((n_cols, H), dtype=torch.float32, device=dev))
+    _dev(o["dX"], "dX")
+    for k in ("dalpha", "dscore", "ds_dst", "ds_src"):
+        _dev(o[k], k, torch.float32)
+    _check(lib().cogdl_gat_backward(
+        n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(colptr), _ptr(row_t), _ptr(perm), H, D,
+        _ptr(s_dst), _ptr(s_src), float(negative_slope), _ptr(alpha), _ptr(X), _dtype_code(X),
+        _ptr(dY), _dtype_code(dY), _ptr(o["dX"]), _dtype_code(o["dX"]), _ptr(o["dalpha"]),
+        _ptr(o["dscore"]), _ptr(o["ds_dst"]), _ptr(o["ds_src"]), _plan_handle(plan),
+        _plan_handle(plan_t), _stream()), "cogdl_gat_backward")
+    return o

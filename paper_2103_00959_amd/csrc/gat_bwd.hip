@@ -1,0 +1,612 @@
+// Backward pass of the attention path of section 2.2, and the dot-product
+// SDDMM that carries the gradient to the attention matrix.
+//
+// For the loss gradient dY of Y[i,h,:] = sum_k alpha[k,h] X[col[k],h,:]:
+//   dalpha[k,h] = <dY[i,h,:], X[j,h,:]>          SDDMM  A (.) (dY_h X_h^T)
+//   c[i,h]      = sum_{k in row i} alpha[k,h] dalpha[k,h]
+//   dscore[k,h] = f * alpha[k,h] * (dalpha[k,h] - c[i,h]),  f = 1 if the
+//                 pre-activation s_dst[i,h] + s_src[j,h] > 0 else the slope
+//   ds_dst[i,h] = sum_{k in row i} dscore[k,h]
+//   ds_src[j,h] = sum_{k: col[k] = j} dscore[k,h]
+//   dX[j,h,:]   = sum_{k: col[k] = j} alpha[k,h] dY[i,h,:]
+//
+// Pass 1 runs on the CSR units.  With the SpMM lane map (S lanes x VEC
+// features of a row, the L = D / VEC lanes of a head side by side) each lane
+// multiplies its dY elements into every gathered neighbour row and a
+// butterfly over the head's lanes completes the dot product, so the gathered
+// rows are read once, as in the forward aggregation.  The lanes fold the row
+// sum c as they go and park dalpha and the pre-activation of every edge in
+// the two outputs (each value by a fixed lane); once c is complete, the same
+// lanes read their own parked values back and write dscore and ds_dst.  A
+// neighbour group of a split row leaves its share of c in the plan, and two
+// small kernels finish those rows once every group is done.
+//
+// Pass 2 is the aggregation kernel run on the CSC (rows = source nodes) with
+// the forward weights reached through perm, summing dscore per head along the
+// way: dX and ds_src in one sweep over dY.
+#include "gat_kernel.hpp"
+
+namespace cogdl {
+namespace {
+
+constexpr int kBlock = kGatBlock;
+
+struct BwdArgs {
+    const int4 *units;          // nullptr: one unit per row in row order
+    const int32_t *u_lo;
+    const int32_t *u_hi;
+    int32_t n_rows;
+    const int32_t *rowptr;
+    const int32_t *col;
+    int32_t H;
+    int32_t D;
+    int64_t W;                  // H * D
+    const float *s_dst;
+    const float *s_src;
+    float slope;
+    const float *alpha;         // forward weights [nnz][H]; nullptr: the SDDMM alone
+    const void *X;              // gathered operand, n_cols x W
+    uint64_t x_bytes;
+    const void *P;              // row operand (dY), n_rows x W
+    float *dalpha;              // [nnz][H]
+    float *dscore;              // [nnz][H]; holds the pre-activations until the end
+    float *ds_dst;              // [n_rows][H]
+    float *gstats;              // split rows: per partial slot c[max_heads], sum[max_heads]
+    int32_t sstride;            // 2 * max_heads
+    const int4 *part_units;     // {row, beg, end, split index} per partial slot
+    const int32_t *n_parts;
+    const int4 *split_rows;     // {row, first slot, #slots, degree}
+    const int32_t *n_split;
+    int32_t log2S;
+    int32_t log2L;              // lanes per head (fast kernel)
+};
+
+__device__ __forceinline__ int4 fetch_bwd_unit(const BwdArgs &a, int64_t u, int64_t hi)
+{
+    if (u >= hi) return make_int4(0, 0, 0, -1);
+    if (a.units) return a.units[u];
+    const int r = (int)u;
+    return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
+}
+
+__device__ __forceinline__ float score_grad(float t, float slope, float al, float da, float c)
+{
+    return (t > 0.f ? 1.f : slope) * al * (da - c);
+}
+
+// Pass 1, feature-parallel: one S-lane sub-group per unit, lane = VEC
+// consecutive features, head h on lanes [h L, (h + 1) L).  Requires one
+// chunk per lane (H * D <= S * VEC) and L a power of two.  Every edge k of a
+// unit is parked by lane q = (k - beg) mod M of its head, M = min(L, U).
+template <typename TX, int VEC, bool BUF, bool DOT>
+__global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
+{
+    constexpr int U = VEC == 1 ? 16 : 8;
+    const int log2S = a.log2S;
+    const int S = 1 << log2S;
+    const int lane = lane_id();
+    const int lig = lane & (S - 1);
+    const int gbase = lane & ~(S - 1);
+    const int L = 1 << a.log2L;
+    const int q = lig & (L - 1);
+    const int h = lig >> a.log2L;
+    const int M = L < U ? L : U;
+    const int64_t fe = (int64_t)lig * VEC;
+    const bool act = fe < a.W;
+    const bool writer = act && q < M;
+    const int H = a.H;
+    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
+    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
+    const int64_t lo = a.units ? *a.u_lo : 0;
+    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
+    const TX *__restrict__ P = static_cast<const TX *>(a.P);
+    const int32_t *__restrict__ col = a.col;
+
+    int64_t u = lo + sub;
+    if (u >= hi) return;
+    int4 d = fetch_bwd_unit(a, u, hi);
+    int c_cur = 0;
+    if (d.z > d.y) c_cur = col[d.y + lig < d.z - 1 ? d.y + lig : d.z - 1];
+    for (;;) {
+        const int64_t un = u + stride;
+        const int4 dn = fetch_bwd_unit(a, un, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        float p[VEC];
+        if (act) {
+            load_vec<TX, VEC>(P, (int64_t)row * a.W + fe, p);
+        } else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) p[e] = 0.f;
+        }
+        const float sd = (!DOT && act) ? a.s_dst[(int64_t)row * H + h] : 0.f;
+        float c = 0.f;
+
+        const int last = end - 1;
+        for (int k0 = beg; k0 < end; k0 += S) {
+            const int n = (end - k0 < S) ? end - k0 : S;
+            const int c_nxt = col[k0 + S + lig < last ? k0 + S + lig : last];
+            for (int j = 0; j < n; j += U) {
+                int cc[U];
+                bool ok[U];
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    ok[t] = j + t < n;
+                    cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
+                }
+                float xv[U][VEC];
+                float al[U], ss[U];
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    const bool on = ok[t] && act;
+                    X.load((int64_t)cc[t] * a.W + fe, on, xv[t]);
+                    if constexpr (!DOT) {
+                        al[t] = a.alpha[on ? (int64_t)(k0 + j + t) * H + h : 0];
+                        ss[t] = a.s_src[on ? (int64_t)cc[t] * H + h : 0];
+                    }
+                }
+                float pd[U];
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    float s = 0.f;
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) s = fmaf(p[e], xv[t][e], s);
+                    pd[t] = s;
+                }
+                // complete the dot products over the head's lanes (every lane of
+                // the head ends with the same bits: each level adds the same pair)
+                for (int off = 1; off < L; off <<= 1) {
+#pragma unroll
+                    for (int t = 0; t < U; ++t) pd[t] += lane_xor(pd[t], off);
+                }
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    const int64_t k = k0 + j + t;
+                    if constexpr (!DOT) c += (ok[t] && act) ? al[t] * pd[t] : 0.f;
+                    if (ok[t] && writer && (t & (M - 1)) == q) {
+                        a.dalpha[k * H + h] = pd[t];
+                        if constexpr (!DOT) a.dscore[k * H + h] = sd + ss[t];
+                    }
+                }
+            }
+            c_cur = c_nxt;
+        }
+        const int c_first_next =
+            (dn.z > dn.y) ? col[dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1] : 0;
+
+        if constexpr (!DOT) {
+            if (part >= 0) {
+                if (act && q == 0) a.gstats[(int64_t)part * a.sstride + h] = c;
+            } else {
+                // this lane's parked edges: offsets q, q + M, ... of the row
+                constexpr int R = 4;
+                float sdt = 0.f;
+                if (writer) {
+                    for (int o0 = q; o0 < end - beg; o0 += R * M) {
+                        float da[R], tv[R], av[R];
+#pragma unroll
+                        for (int r = 0; r < R; ++r) {
+                            const int o = o0 + r * M;
+                            const int64_t k = (int64_t)beg + (o < end - beg ? o : o0);
+                            da[r] = a.dalpha[k * H + h];
+                            tv[r] = a.dscore[k * H + h];
+                            av[r] = a.alpha[k * H + h];
+                        }
+#pragma unroll
+                        for (int r = 0; r < R; ++r) {
+                            const int o = o0 + r * M;
+                            if (o < end - beg) {
+                                const float g = score_grad(tv[r], a.slope, av[r], da[r], c);
+                                a.dscore[((int64_t)beg + o) * H + h] = g;
+                                sdt += g;
+                            }
+                        }
+                    }
+                }
+                for (int off = 1; off < L; off <<= 1) sdt += lane_xor(sdt, off);
+                if (act && q == 0) a.ds_dst[(int64_t)row * H + h] = sdt;
+            }
+        }
+        if (un >= hi) break;
+        u = un;
+        d = dn;
+        c_cur = c_first_next;
+    }
+}
+
+// Sum over the slots of one head in a wavefront laid out as (slot, head):
+// lanes s * H + h, s < 64 / H.  The same fixed order in every lane of h.
+__device__ __forceinline__ float slot_sum(float v, int H)
+{
+    if ((H & (H - 1)) == 0) {
+        for (int off = H; off < kWave; off <<= 1) v += lane_xor(v, off);
+        return v;
+    }
+    const int slots = kWave / H;
+    const int h = lane_id() % H;
+    float s = 0.f;
+    for (int i = 0; i < slots; ++i) s += lane_bcast(v, i * H + h);
+    return s;
+}
+
+// Pass 1 for any shape: a wavefront per unit, lanes as (edge slot, head),
+// each lane forming whole dot products element by element.  Every edge is
+// parked by the lane of its slot.
+template <typename TX, typename TP, bool DOT>
+__global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
+{
+    const int lane = lane_id();
+    const int H = a.H;
+    const int eps = kWave / H;
+    const int h = lane % H;
+    const int slot = lane / H;
+    const bool live = slot < eps;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int64_t lo = a.units ? *a.u_lo : 0;
+    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const TX *__restrict__ X = static_cast<const TX *>(a.X);
+    const TP *__restrict__ P = static_cast<const TP *>(a.P);
+    for (int64_t u = lo + (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; u < hi;
+         u += waves) {
+        const int4 d = fetch_bwd_unit(a, u, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        const float sd = DOT ? 0.f : a.s_dst[(int64_t)row * H + h];
+        float c = 0.f;
+        if (live) {
+            for (int k = beg + slot; k < end; k += eps) {
+                const int j = a.col[k];
+                float s = 0.f;
+                for (int e = 0; e < a.D; ++e) {
+                    float pv[1], xv[1];
+                    load_vec<TP, 1>(P, (int64_t)row * a.W + (int64_t)h * a.D + e, pv);
+                    load_vec<TX, 1>(X, (int64_t)j * a.W + (int64_t)h * a.D + e, xv);
+                    s = fmaf(pv[0], xv[0], s);
+                }
+                a.dalpha[(int64_t)k * H + h] = s;
+                if constexpr (!DOT) {
+                    c += a.alpha[(int64_t)k * H + h] * s;
+                    a.dscore[(int64_t)k * H + h] = sd + a.s_src[(int64_t)j * H + h];
+                }
+            }
+        }
+        if constexpr (DOT) continue;
+        c = slot_sum(live ? c : 0.f, H);
+        if (part >= 0) {
+            if (slot == 0) a.gstats[(int64_t)part * a.sstride + h] = c;
+            continue;
+        }
+        float sdt = 0.f;
+        if (live) {
+            for (int k = beg + slot; k < end; k += eps) {
+                const int64_t i = (int64_t)k * H + h;
+                const float g = score_grad(a.dscore[i], a.slope, a.alpha[i], a.dalpha[i], c);
+                a.dscore[i] = g;
+                sdt += g;
+            }
+        }
+        sdt = slot_sum(live ? sdt : 0.f, H);
+        if (slot == 0) a.ds_dst[(int64_t)row * H + h] = sdt;
+    }
+}
+
+// Split rows, after pass 1: every neighbour group adds up the shares of c of
+// all groups of its row (slot order), turns its parked edges into dscore and
+// leaves its share of ds_dst.  One wavefront per group, lanes (slot, head).
+__global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
+{
+    const int lane = lane_id();
+    const int H = a.H;
+    const int eps = kWave / H;
+    const int h = lane % H;
+    const int slot = lane / H;
+    const bool live = slot < eps;
+    const int half = a.sstride >> 1;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t np = *a.n_parts;
+    for (int64_t p = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; p < np;
+         p += waves) {
+        const int4 d = a.part_units[p];
+        const int4 sr = a.split_rows[d.w];
+        float c = 0.f;
+        for (int g = 0; g < sr.z; ++g) c += a.gstats[(int64_t)(sr.y + g) * a.sstride + h];
+        constexpr int R = 8;
+        float sdt = 0.f;
+        if (live) {
+            for (int k0 = d.y + slot; k0 < d.z; k0 += R * eps) {
+                float da[R], tv[R], av[R];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = k0 + r * eps;
+                    const int64_t i = (int64_t)(k < d.z ? k : k0) * H + h;
+                    da[r] = a.dalpha[i];
+                    tv[r] = a.dscore[i];
+                    av[r] = a.alpha[i];
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = k0 + r * eps;
+                    if (k < d.z) {
+                        const float g = score_grad(tv[r], a.slope, av[r], da[r], c);
+                        a.dscore[(int64_t)k * H + h] = g;
+                        sdt += g;
+                    }
+                }
+            }
+        }
+        sdt = slot_sum(live ? sdt : 0.f, H);
+        if (slot == 0) a.gstats[p * a.sstride + half + h] = sdt;
+    }
+}
+
+// ds[row, h] = sum of the groups' shares (slot order), one wavefront per split
+// row; the shares sit at offset `base` of each partial slot's stats.
+__global__ __launch_bounds__(kBlock) void k_split_head_sums(const int4 *__restrict__ split_rows,
+                                                            const int32_t *__restrict__ n_split,
+                                                            const float *__restrict__ gstats,
+                                                            int sstride, int base, int H,
+                                                            float *__restrict__ out)
+{
+    const int lane = lane_id();
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int32_t ns = *n_split;
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns;
+         s += waves) {
+        const int4 d = split_rows[s];
+        if (lane < H) {
+            float v = 0.f;
+            for (int g = 0; g < d.z; ++g) v += gstats[(int64_t)(d.y + g) * sstride + base + lane];
+            out[(int64_t)d.x * H + lane] = v;
+        }
+    }
+}
+
+using BwdKernel = void (*)(BwdArgs);
+
+template <bool DOT>
+BwdKernel pick_rows(int dt, bool buf, int vec)
+{
+    if (dt == COGDL_F32) {
+        if (vec == 4) return buf ? k_bwd_rows<float, 4, true, DOT> : k_bwd_rows<float, 4, false, DOT>;
+        return buf ? k_bwd_rows<float, 1, true, DOT> : k_bwd_rows<float, 1, false, DOT>;
+    }
+    if (dt == COGDL_BF16) {
+        if (vec == 8) return buf ? k_bwd_rows<bf16_t, 8, true, DOT> : k_bwd_rows<bf16_t, 8, false, DOT>;
+        return buf ? k_bwd_rows<bf16_t, 1, true, DOT> : k_bwd_rows<bf16_t, 1, false, DOT>;
+    }
+    if (vec == 8) return buf ? k_bwd_rows<f16_t, 8, true, DOT> : k_bwd_rows<f16_t, 8, false, DOT>;
+    return buf ? k_bwd_rows<f16_t, 1, true, DOT> : k_bwd_rows<f16_t, 1, false, DOT>;
+}
+
+template <typename TX, bool DOT>
+BwdKernel pick_any_p(int pdt)
+{
+    if (pdt == COGDL_F32) return k_bwd_rows_any<TX, float, DOT>;
+    if (pdt == COGDL_BF16) return k_bwd_rows_any<TX, bf16_t, DOT>;
+    return k_bwd_rows_any<TX, f16_t, DOT>;
+}
+
+template <bool DOT>
+BwdKernel pick_any(int xdt, int pdt)
+{
+    if (xdt == COGDL_F32) return pick_any_p<float, DOT>(pdt);
+    if (xdt == COGDL_BF16) return pick_any_p<bf16_t, DOT>(pdt);
+    return pick_any_p<f16_t, DOT>(pdt);
+}
+
+unsigned wave_grid(int64_t work)
+{
+    int64_t b = (work + (kBlock / kWave) - 1) / (kBlock / kWave);
+    if (b > 2048) b = 2048;
+    if (b < 1) b = 1;
+    return (unsigned)b;
+}
+
+// Pass 1 over the units of `plan` (or the rows in order): the fast kernel
+// when the shape allows it, else the general one.
+template <bool DOT>
+cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *name,
+                       hipStream_t stream)
+{
+    const int64_t units = P ? P->cap_units : a.n_rows;
+    const int xb = dtype_bytes(xdt);
+    const bool aligned = ((uintptr_t)a.X % 16 == 0) && ((uintptr_t)a.P % 16 == 0);
+    const RowMap m = row_map(a.W, xb, a.D, aligned);
+    const int L = a.D / m.vec;
+    const bool fast = xdt == pdt && m.ch == 1 && m.n_slabs == 1 && (L & (L - 1)) == 0;
+    if (fast) {
+        a.log2S = m.log2S;
+        a.log2L = log2i(L);
+        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec);
+        const int64_t upb = kBlock >> m.log2S;
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH(name, k, (unsigned)(blocks > 0 ? blocks : 1), kBlock, stream, a);
+    } else {
+        BwdKernel k = pick_any<DOT>(xdt, pdt);
+        int64_t blocks = (units + (kBlock / kWave) - 1) / (kBlock / kWave);
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH(name, k, (unsigned)(blocks > 0 ? blocks : 1), kBlock, stream, a);
+    }
+    return COGDL_OK;
+}
+
+cogdl_status check_heads(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                         const int32_t *col, int32_t H, int32_t D)
+{
+    if (n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
+    if (H < 1 || H > COGDL_MAX_HEADS || D < 1) return COGDL_ERR_INVALID;
+    if (nnz > INT32_MAX || (int64_t)H * D > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (n_rows > 0 && !rowptr) return COGDL_ERR_INVALID;
+    if (nnz > 0 && (!col || n_rows == 0 || n_cols == 0)) return COGDL_ERR_INVALID;
+    return COGDL_OK;
+}
+
+}  // namespace
+}  // namespace cogdl
+
+using namespace cogdl;
+
+extern "C" {
+
+cogdl_status cogdl_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                             const int32_t *col, int32_t H, int32_t D, const void *P,
+                             cogdl_dtype p_dtype, const void *Q, cogdl_dtype q_dtype, float *out,
+                             const cogdl_plan *plan, hipStream_t stream)
+{
+    cogdl_status st = check_heads(n_rows, n_cols, nnz, rowptr, col, H, D);
+    if (st != COGDL_OK) return st;
+    if (!dtype_ok(p_dtype) || !dtype_ok(q_dtype)) return COGDL_ERR_DTYPE;
+    if (nnz > 0 && (!P || !Q || !out)) return COGDL_ERR_INVALID;
+    const Plan *Pl = plan_of(plan);
+    if (Pl && (Pl->n_rows != n_rows || Pl->nnz != nnz)) return COGDL_ERR_PLAN;
+    if (nnz == 0) return COGDL_OK;
+    BwdArgs a{};
+    a.units = Pl ? Pl->units : nullptr;
+    a.u_lo = Pl ? Pl->zero_dev() : nullptr;
+    a.u_hi = Pl ? Pl->n_units_dev() : nullptr;
+    a.n_rows = n_rows;
+    a.rowptr = rowptr;
+    a.col = col;
+    a.H = H;
+    a.D = D;
+    a.W = (int64_t)H * D;
+    a.X = Q;
+    a.x_bytes = (uint64_t)n_cols * (uint64_t)a.W * (uint64_t)dtype_bytes(q_dtype);
+    a.P = P;
+    a.dalpha = out;
+    return rows_pass<true>(a, Pl, (int)q_dtype, (int)p_dtype, "sddmm_dot", stream);
+}
+
+cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                const int32_t *rowptr, const int32_t *col, const int32_t *colptr,
+                                const int32_t *row_t, const int32_t *perm, int32_t H, int32_t D,
+                                const float *s_dst, const float *s_src, float negative_slope,
+                                const float *alpha, const void *X, cogdl_dtype x_dtype,
+                                const void *dY, cogdl_dtype dy_dtype, void *dX,
+                                cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
+                                float *ds_src, const cogdl_plan *plan, const cogdl_plan *plan_t,
+                                hipStream_t stream)
+{
+    cogdl_status st = check_heads(n_rows, n_cols, nnz, rowptr, col, H, D);
+    if (st != COGDL_OK) return st;
+    if (!dtype_ok(x_dtype) || !dtype_ok(dy_dtype) || !dtype_ok(dx_dtype)) return COGDL_ERR_DTYPE;
+    if (n_cols > 0 && (!colptr || !dX || !ds_src)) return COGDL_ERR_INVALID;
+    if (n_rows > 0 && (!ds_dst || !s_dst || !dY)) return COGDL_ERR_INVALID;
+    if (nnz > 0 && (!row_t || !perm || !s_src || !alpha || !X || !dalpha || !dscore))
+        return COGDL_ERR_INVALID;
+    const int64_t W = (int64_t)H * D;
+    const Plan *Pr = plan_of(plan);
+    const Plan *Pc = plan_of(plan_t);
+    if (Pr && (Pr->n_rows != n_rows || Pr->nnz != nnz || Pr->max_heads < H)) return COGDL_ERR_PLAN;
+    if (Pc && (Pc->n_rows != n_cols || Pc->nnz != nnz || Pc->max_feat < W || Pc->max_heads < H))
+        return COGDL_ERR_PLAN;
+
+    // pass 1 on the CSR: dalpha, dscore, ds_dst
+    if (n_rows > 0) {
+        BwdArgs a{};
+        a.units = Pr ? Pr->units : nullptr;
+        a.u_lo = Pr ? Pr->zero_dev() : nullptr;
+        a.u_hi = Pr ? Pr->n_units_dev() : nullptr;
+        a.n_rows = n_rows;
+        a.rowptr = rowptr;
+        a.col = col;
+        a.H = H;
+        a.D = D;
+        a.W = W;
+        a.s_dst = s_dst;
+        a.s_src = s_src;
+        a.slope = negative_slope;
+        a.alpha = alpha;
+        a.X = X;
+        a.x_bytes = (uint64_t)n_cols * (uint64_t)W * (uint64_t)dtype_bytes(x_dtype);
+        a.P = dY;
+        a.dalpha = dalpha;
+        a.dscore = dscore;
+        a.ds_dst = ds_dst;
+        a.gstats = Pr ? Pr->gstats : nullptr;
+        a.sstride = Pr ? 2 * Pr->max_heads : 0;
+        a.part_units = Pr ? Pr->part_units : nullptr;
+        a.n_parts = Pr ? Pr->n_parts_dev() : nullptr;
+        a.split_rows = Pr ? Pr->split_rows : nullptr;
+        a.n_split = Pr ? Pr->n_split_dev() : nullptr;
+        st = rows_pass<false>(a, Pr, (int)x_dtype, (int)dy_dtype, "gat_bwd_rows", stream);
+        if (st != COGDL_OK) return st;
+        if (Pr) {
+            COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges, wave_grid(Pr->cap_partials),
+                         kBlock, stream, a);
+            COGDL_LAUNCH("gat_bwd_split_dst", k_split_head_sums, wave_grid(Pr->cap_split), kBlock,
+                         stream, Pr->split_rows, Pr->n_split_dev(), Pr->gstats, a.sstride,
+                         Pr->max_heads, H, ds_dst);
+        }
+    }
+    if (n_cols == 0) return COGDL_OK;
+
+    // pass 2 on the CSC: dX and ds_src
+    const bool aligned = ((uintptr_t)dY % 16 == 0) && ((uintptr_t)dX % 16 == 0);
+    RowMap m = row_map(W, dtype_bytes(dy_dtype), D, aligned);
+    if (m.S < H) {
+        m.S = next_pow2(H);
+        m.log2S = log2i(m.S);
+        m.slab = m.S * m.ch * m.vec;
+        m.n_slabs = (int)((W + m.slab - 1) / m.slab);
+    }
+    GatArgs g{};
+    g.units = Pc ? Pc->units : nullptr;
+    g.u_lo = Pc ? Pc->zero_dev() : nullptr;
+    g.u_hi = Pc ? Pc->n_units_dev() : nullptr;
+    g.n_rows = n_cols;
+    g.rowptr = colptr;
+    g.col = row_t;
+    g.H = H;
+    g.D = D;
+    g.W = W;
+    g.alpha_in = alpha;
+    g.X = dY;
+    g.x_bytes = (uint64_t)n_rows * (uint64_t)W * (uint64_t)dtype_bytes(dy_dtype);
+    g.Y = dX;
+    g.partials = Pc ? Pc->partials : nullptr;
+    g.pstride = Pc ? (Pc->max_feat + 7) / 8 * 8 : 0;
+    g.gstats = Pc ? Pc->gstats : nullptr;
+    g.sstride = Pc ? 2 * Pc->max_heads : 0;
+    g.perm = perm;
+    g.dscore = dscore;
+    g.ds_out = ds_src;
+    g.slab = m.slab;
+    g.log2S = m.log2S;
+    const bool buf = g.x_bytes <= kBufferMaxBytes;
+    const int64_t units = Pc ? Pc->cap_units : n_cols;
+    const bool tiny = Pc && m.ch == 1 && m.S >= 8 && m.S / 4 >= H;
+    if (tiny) g.u_hi = Pc->n_big_dev();
+    {
+        const int64_t upb = kBlock >> m.log2S;
+        GatKernel k = gat_pick<true>((int)dy_dtype, (int)dx_dtype, m.vec, m.ch, buf);
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH("gat_bwd_cols", k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
+                     kBlock, stream, g);
+    }
+    if (tiny) {
+        GatArgs b = g;
+        b.u_lo = Pc->n_big_dev();
+        b.u_hi = Pc->n_units_dev();
+        b.log2S = m.log2S - 2;
+        const int64_t upb = kBlock >> b.log2S;
+        GatKernel k = gat_pick<true>((int)dy_dtype, (int)dx_dtype, m.vec, 4, buf);
+        int64_t blocks = (units + upb - 1) / upb;
+        const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
+        if (blocks > res) blocks = res;
+        COGDL_LAUNCH("gat_bwd_cols_tiny", k,
+                     dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock, stream, b);
+    }
+    if (!Pc) return COGDL_OK;
+    st = sum_reduce_launch("gat_bwd_dx_reduce", *Pc, W, dX, (int)dx_dtype, false, stream);
+    if (st != COGDL_OK) return st;
+    COGDL_LAUNCH("gat_bwd_split_src", k_split_head_sums, wave_grid(Pc->cap_split), kBlock, stream,
+                 Pc->split_rows, Pc->n_split_dev(), Pc->gstats, g.sstride, 0, H, ds_src);
+    return COGDL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,324 @@
+// The gather kernel of the attention path (section 2.2: SDDMM of the scores,
+// LeakyReLU, edge softmax and multi-head SpMM, fused), shared by gat.hip (the
+// forward variants) and gat_bwd.hip (the backward variant on the CSC).  See
+// gat.hip for the mapping onto gfx950.
+#pragma once
+
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace cogdl {
+
+constexpr int kGatBlock = 256;
+
+struct GatArgs {
+    const int4 *units;
+    const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
+    const int32_t *u_hi;
+    int32_t n_rows;
+    const int32_t *rowptr;
+    const int32_t *col;
+    int32_t H;
+    int32_t D;
+    int64_t W;                  // H * D
+    const float *s_dst;
+    const float *s_src;
+    float slope;
+    const float *alpha_in;      // weights given: skip the attention steps
+    const void *X;
+    uint64_t x_bytes;           // size of X, bounds the buffer gathers
+    void *Y;
+    float *alpha_out;
+    float *partials;
+    int64_t pstride;
+    float *gstats;              // per partial slot: m[max_heads], z[max_heads]
+    const int32_t *perm;        // BWD: weight of edge k is alpha_in[perm[k]] (CSC of the graph)
+    const float *dscore;        // BWD: per-edge, per-head values summed per row (through perm)
+    float *ds_out;              // BWD: those sums, n_rows x H (split rows: gstats)
+    int32_t sstride;            // 2 * max_heads
+    int32_t slab;
+    int32_t log2S;
+};
+
+// Descriptor {row, first edge, end edge, partial slot} of unit u (an empty
+// unit past the end, so prefetching one unit ahead needs no branch around it).
+__device__ __forceinline__ int4 fetch_gat_unit(const GatArgs &a, int64_t u, int64_t hi)
+{
+    if (u >= hi) return make_int4(0, 0, 0, -1);
+    if (a.units) return a.units[u];
+    const int r = (int)u;
+    return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
+}
+
+// alpha[k, h] = exp(e_kh - m) * rz for the edges k = beg + slot + j * slots
+// of one head h, R gathers in flight per lane: the column indices of R edges
+// are loaded together (clamped to the last edge), then their R source scores,
+// then the R results are stored.
+template <int R>
+__device__ __forceinline__ void alpha_sweep(const int32_t *__restrict__ col,
+                                            const float *__restrict__ s_src,
+                                            float *__restrict__ alpha, int H, int h, float sd,
+                                            float slope, float m, float rz, int beg, int end,
+                                            int slot, int slots)
+{
+    for (int k0 = beg + slot; k0 < end; k0 += R * slots) {
+        int cc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int k = k0 + r * slots;
+            cc[r] = col[k < end ? k : end - 1];
+        }
+        float sv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) sv[r] = s_src[(int64_t)cc[r] * H + h];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int k = k0 + r * slots;
+            if (k < end) alpha[(int64_t)k * H + h] = __expf(leaky_relu(sd + sv[r], slope) - m) * rz;
+        }
+    }
+}
+
+// BWD = true: the backward pass of the aggregation, run on the CSC of the
+// graph (rows of this launch = source nodes): the weights are the forward
+// alpha through perm, and each row also sums dscore (through perm) per head.
+template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD>
+__global__ __launch_bounds__(kGatBlock) void k_gat(GatArgs a)
+{
+    constexpr int U = (VEC == 1 ? 16 : 8) / CH;
+    const int log2S = a.log2S;
+    const int S = 1 << log2S;
+    const int lane = lane_id();
+    const int lig = lane & (S - 1);
+    const int gbase = lane & ~(S - 1);
+    const int H = a.H;
+    const bool soft = a.alpha_in == nullptr;
+    const int64_t sub = (int64_t)blockIdx.x * (kGatBlock >> log2S) + (threadIdx.x >> log2S);
+    const int64_t stride = (int64_t)gridDim.x * (kGatBlock >> log2S);
+    const int64_t lo = a.units ? *a.u_lo : 0;
+    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+
+    const int64_t f0 = (int64_t)blockIdx.y * a.slab;
+    const int64_t f_end = (f0 + a.slab < a.W) ? f0 + a.slab : a.W;
+    int64_t fe[CH];
+    bool act[CH];
+    int hd[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        fe[c] = f0 + (int64_t)(c * S + lig) * VEC;
+        act[c] = fe[c] < f_end;
+        hd[c] = act[c] ? (int)(fe[c] / a.D) : 0;
+    }
+    const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
+    const int32_t *__restrict__ col = a.col;
+    const float *__restrict__ wsrc = soft ? a.s_src : a.alpha_in;
+    // (edge slot, head) lane layout of the alpha sweep: eps edges per step
+    const int eps = S / H;
+    const int q_slot = lig / H, q_head = lig % H;
+
+    // Resident grid, software-pipelined over units as in the SpMM kernel.
+    int64_t u = lo + sub;
+    if (u >= hi) return;
+    int4 d = fetch_gat_unit(a, u, hi);
+    int c_cur = 0, p_cur = 0;
+    if (d.z > d.y) {
+        const int k = d.y + lig < d.z - 1 ? d.y + lig : d.z - 1;
+        c_cur = col[k];
+        if constexpr (BWD) p_cur = a.perm[k];
+    }
+    for (;;) {
+        const int64_t un = u + stride;
+        const int4 dn = fetch_gat_unit(a, un, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        float sd[CH], m[CH], z[CH], dsum[CH];
+        float acc[CH][VEC];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            dsum[c] = 0.f;
+            sd[c] = soft ? a.s_dst[(int64_t)row * H + hd[c]] : 0.f;
+            m[c] = -INFINITY;
+            z[c] = 0.f;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
+        }
+
+        // Branch-free batches: index loads are clamped to the unit's last
+        // edge, masked gathers read zeros, masked weights are -inf (softmax)
+        // or 0.
+        const int last = end - 1;
+        for (int k0 = beg; k0 < end; k0 += S) {
+            const int n = (end - k0 < S) ? end - k0 : S;
+            const int kn = k0 + S + lig < last ? k0 + S + lig : last;
+            const int c_nxt = col[kn];
+            const int p_nxt = BWD ? a.perm[kn] : 0;
+            for (int j = 0; j < n; j += U) {
+                int cc[U], pk[U];
+                bool ok[U];
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    ok[t] = j + t < n;
+                    cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
+                    if constexpr (BWD) pk[t] = lane_bcast(p_cur, gbase + (ok[t] ? j + t : j));
+                }
+                float w[U][CH];
+                float xv[U][CH][VEC];
+#pragma unroll
+                for (int t = 0; t < U; ++t)
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) {
+                        const bool on = ok[t] && act[c];
+                        const int64_t wi = BWD ? (int64_t)pk[t] * H + hd[c]
+                                         : soft ? (int64_t)cc[t] * H + hd[c]
+                                                : (int64_t)(k0 + j + t) * H + hd[c];
+                        w[t][c] = wsrc[on ? wi : 0];
+                        if constexpr (BWD) {
+                            const float g = a.dscore[on ? wi : 0];
+                            dsum[c] += on ? g : 0.f;
+                        }
+                        X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
+                    }
+                if (soft) {
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) {
+                        float mb = m[c];
+#pragma unroll
+                        for (int t = 0; t < U; ++t) {
+                            w[t][c] = (ok[t] && act[c]) ? leaky_relu(sd[c] + w[t][c], a.slope) : -INFINITY;
+                            mb = fmaxf(mb, w[t][c]);
+                        }
+                        if (mb > m[c]) {
+                            const float r = __expf(m[c] - mb);
+                            z[c] *= r;
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
+                            m[c] = mb;
+                        }
+                        float zb = 0.f;
+#pragma unroll
+                        for (int t = 0; t < U; ++t) {
+                            w[t][c] = (w[t][c] == -INFINITY) ? 0.f : __expf(w[t][c] - m[c]);
+                            zb += w[t][c];
+                        }
+                        z[c] += zb;
+                    }
+                } else {
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+#pragma unroll
+                        for (int c = 0; c < CH; ++c)
+                            if (!(ok[t] && act[c])) w[t][c] = 0.f;
+                }
+#pragma unroll
+                for (int t = 0; t < U; ++t)
+#pragma unroll
+                    for (int c = 0; c < CH; ++c)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xv[t][c][e], acc[c][e]);
+            }
+            c_cur = c_nxt;
+            if constexpr (BWD) p_cur = p_nxt;
+        }
+        int c_first_next = 0, p_first_next = 0;
+        if (dn.z > dn.y) {
+            const int k = dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1;
+            c_first_next = col[k];
+            if constexpr (BWD) p_first_next = a.perm[k];
+        }
+        if constexpr (BWD) {
+            // the per-head sum, written once by the lane holding the head's first feature
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                if (!act[c] || fe[c] % a.D != 0) continue;
+                if (part >= 0) a.gstats[(int64_t)part * a.sstride + hd[c]] = dsum[c];
+                else a.ds_out[(int64_t)row * H + hd[c]] = dsum[c];
+            }
+        }
+
+        if (part >= 0) {
+            // neighbour group of a split row: unnormalized partial + (m, z) per head
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                if (!act[c]) continue;
+                store_vec<float, VEC>(a.partials, (int64_t)part * a.pstride + fe[c], acc[c]);
+                if (soft && fe[c] % a.D == 0) {
+                    a.gstats[(int64_t)part * a.sstride + hd[c]] = m[c];
+                    a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + hd[c]] = z[c];
+                }
+            }
+        } else {
+            float rz[CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                rz[c] = (soft && z[c] > 0.f) ? 1.f / z[c] : 1.f;
+                float v[VEC];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) v[e] = acc[c][e] * rz[c];
+                if (act[c]) store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
+            }
+            if (soft && a.alpha_out != nullptr) {
+                // alpha of this whole-row unit: lanes as (edge slot, head); the
+                // (m, z) of head h comes from the lane holding the first feature
+                // of h in this slab.
+                const int h1 = q_head;
+                const int slot = q_slot;
+                const int64_t hf = (int64_t)h1 * a.D;
+                const bool mine_head = hf >= f0 && hf < f_end;
+                const int idx = mine_head ? (int)((hf - f0) / VEC) : 0;
+                const int src_c = idx / S, src_l = idx % S;
+                float m1 = 0.f, r1 = 0.f;
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const float mm = lane_bcast(m[c], gbase + src_l);
+                    const float rr = lane_bcast(rz[c], gbase + src_l);
+                    if (c == src_c) { m1 = mm; r1 = rr; }
+                }
+                if (mine_head && slot < eps)
+                    alpha_sweep<4>(col, a.s_src, a.alpha_out, H, h1, a.s_dst[(int64_t)row * H + h1],
+                                   a.slope, m1, r1, beg, end, slot, eps);
+            }
+        }
+        if (un >= hi) break;
+        u = un;
+        d = dn;
+        c_cur = c_first_next;
+        p_cur = p_first_next;
+    }
+}
+
+using GatKernel = void (*)(GatArgs);
+
+template <typename TX, typename TY, bool BUF, bool BWD>
+GatKernel gat_pick_vec(int vec, int ch)
+{
+    constexpr int V = (int)(16 / sizeof(TX));
+    if (vec == 1) {
+        if (ch == 1) return k_gat<TX, TY, 1, 1, BUF, BWD>;
+        if (ch == 2) return k_gat<TX, TY, 1, 2, BUF, BWD>;
+        return k_gat<TX, TY, 1, 4, BUF, BWD>;
+    }
+    if (ch == 1) return k_gat<TX, TY, V, 1, BUF, BWD>;
+    if (ch == 2) return k_gat<TX, TY, V, 2, BUF, BWD>;
+    return k_gat<TX, TY, V, 4, BUF, BWD>;
+}
+
+template <typename TX, bool BUF, bool BWD>
+GatKernel gat_pick_y(int ydt, int vec, int ch)
+{
+    if (ydt == COGDL_F32) return gat_pick_vec<TX, float, BUF, BWD>(vec, ch);
+    if (ydt == COGDL_BF16) return gat_pick_vec<TX, bf16_t, BUF, BWD>(vec, ch);
+    return gat_pick_vec<TX, f16_t, BUF, BWD>(vec, ch);
+}
+
+template <bool BWD>
+GatKernel gat_pick(int xdt, int ydt, int vec, int ch, bool buf)
+{
+    if (buf) {
+        if (xdt == COGDL_F32) return gat_pick_y<float, true, BWD>(ydt, vec, ch);
+        if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, true, BWD>(ydt, vec, ch);
+        return gat_pick_y<f16_t, true, BWD>(ydt, vec, ch);
+    }
+    if (xdt == COGDL_F32) return gat_pick_y<float, false, BWD>(ydt, vec, ch);
+    if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, false, BWD>(ydt, vec, ch);
+    return gat_pick_y<f16_t, false, BWD>(ydt, vec, ch);
+}
+}  // namespace cogdl

@@ -163,3 +163,35 @@ def test_binding_refuses_host_tensors():
     x = torch.zeros(3, 4)
     with pytest.raises(cg.CogdlError):
         cg.spmm(torch.zeros(4, dtype=torch.int32), torch.zeros(0, dtype=torch.int32), None, x)
+
+
+def test_sddmm_dot_validation(L):
+    S = L.cogdl_sddmm_dot
+    # heads and width
+    assert S(2, 2, 3, FAKE, FAKE, 0, 4, FAKE, 0, FAKE, 0, FAKE, None, None) == INVALID
+    assert S(2, 2, 3, FAKE, FAKE, 65, 4, FAKE, 0, FAKE, 0, FAKE, None, None) == INVALID
+    assert S(2, 2, 3, FAKE, FAKE, 2, 0, FAKE, 0, FAKE, 0, FAKE, None, None) == INVALID
+    assert S(2, 2, 3, FAKE, FAKE, 2, 4, FAKE, 5, FAKE, 0, FAKE, None, None) == DTYPE
+    assert S(2, 2, 3, FAKE, FAKE, 2, 4, None, 0, FAKE, 0, FAKE, None, None) == INVALID
+    assert S(2, 2, 3, FAKE, FAKE, 2, 4, FAKE, 0, FAKE, 0, None, None, None) == INVALID
+    assert S(2, 2, 1 << 31, FAKE, FAKE, 2, 4, FAKE, 0, FAKE, 0, FAKE, None, None) == TOO_LARGE
+    assert S(0, 3, 0, None, None, 2, 4, None, 0, None, 0, None, None, None) == OK
+
+
+def test_gat_backward_validation(L):
+    def B(n_rows, n_cols, nnz, H=2, D=4, xdt=0, ydt=0, dxdt=0, colptr=FAKE, perm=FAKE, alpha=FAKE,
+          dscore=FAKE, ds_src=FAKE):
+        return L.cogdl_gat_backward(n_rows, n_cols, nnz, FAKE, FAKE, colptr, FAKE, perm, H, D, FAKE,
+                                    FAKE, ctypes.c_float(0.2), alpha, FAKE, xdt, FAKE, ydt, FAKE, dxdt,
+                                    FAKE, dscore, FAKE, ds_src, None, None, None)
+    assert B(2, 2, 3, H=0) == INVALID
+    assert B(2, 2, 3, D=0) == INVALID
+    assert B(2, 2, 3, xdt=4) == DTYPE
+    assert B(2, 2, 3, dxdt=-1) == DTYPE
+    assert B(2, 2, 3, colptr=None) == INVALID
+    assert B(2, 2, 3, perm=None) == INVALID
+    assert B(2, 2, 3, alpha=None) == INVALID
+    assert B(2, 2, 3, dscore=None) == INVALID
+    assert B(2, 2, 3, ds_src=None) == INVALID
+    assert B(2, 2, 1 << 31) == TOO_LARGE
+    assert B(-1, 2, 0) == INVALID

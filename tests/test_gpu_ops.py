@@ -499,3 +499,105 @@ def test_plan_errors_on_mismatch(cg):
             cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), plan=plan)   # no heads reserved
     finally:
         plan.close()
+
+
+# ---------------------------------------------------------------- SDDMM and GAT backward
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
+@pytest.mark.parametrize("H,D,pk,qk", [(1, 1, "f32", "f32"), (4, 64, "bf16", "bf16"), (8, 16, "f32", "f32"),
+                                       (3, 5, "f32", "f32"), (2, 40, "f32", "f32"), (4, 64, "f32", "f32"),
+                                       (2, 32, "f16", "f16"), (16, 80, "f32", "f32"), (4, 16, "bf16", "f32")])
+def test_sddmm_dot(cg, kind, H, D, pk, qk):
+    g = _graph(kind)
+    say(f"sddmm_dot {kind} H={H} D={D} {pk}.{qk}")
+    rp, cl, _ = graph_to_dev(g)
+    ph, pc, pd = features((g.n_rows, H, D), 81 + D, pk)
+    qh, qc, qd = features((g.n_cols, H, D), 91 + D, qk)
+    ref, ab = oracle.sddmm_dot(g.rowptr, g.col, ph.reshape(g.n_rows, H * D), qh.reshape(g.n_cols, H * D),
+                               H, D, p_dtype=pc, q_dtype=qc)
+    for spec in (None, ("auto", 0), ("neighbor_group", 5)):
+        plan = _make_plan(cg, rp, g.nnz, spec, 1)
+        try:
+            out = cg.sddmm_dot(rp, cl, pd, qd, plan=plan)
+            assert scaled_error(out, ref, ab) <= TOL_F32, (kind, H, D, spec)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+def _bwd_inputs(g, H, D, xk, seed, softmax_alpha=True):
+    sd, ss = _scores(g.n_rows, g.n_cols, H, seed)
+    if softmax_alpha:
+        alpha = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2).astype(np.float32)
+    else:
+        alpha = np.random.default_rng(seed).random((g.nnz, H)).astype(np.float32)
+    xh, xc, xd = features((g.n_cols, H, D), seed + 1, xk)
+    gh, gc, gd = features((g.n_rows, H, D), seed + 2, xk)
+    return sd, ss, alpha, (xh, xc, xd), (gh, gc, gd)
+
+
+def _check_bwd(out, ref, what):
+    for k in ("dalpha", "dscore", "ds_dst", "ds_src"):
+        err = scaled_error(out[k], ref[k], ref[k + "_abs"])
+        assert err <= TOL_F32, (what, k, err)
+    err = scaled_error(out["dX"].reshape(ref["dX"].shape), ref["dX"], ref["dX_abs"])
+    assert err <= tol_for("f32" if out["dX"].dtype == __import__("torch").float32 else "bf16"), (what, "dX", err)
+
+
+PLAN_PAIRS = [(None, None), (("auto", 0), ("auto", 0)), (("row_split", 0), ("row_split", 0)),
+              (("neighbor_group", 5), ("neighbor_group", 3)), (("neighbor_group", 64), ("neighbor_group", 9))]
+
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
+@pytest.mark.parametrize("H,D,xk,dxk", [(4, 64, "bf16", "bf16"), (8, 16, "f32", "f32"), (3, 5, "f32", "f32"),
+                                        (1, 1, "f32", "f32"), (2, 40, "f16", "f32"), (4, 64, "bf16", "f32"),
+                                        (16, 80, "f32", "f32")])
+def test_gat_backward(cg, kind, H, D, xk, dxk):
+    import torch
+    g = _graph(kind)
+    say(f"gat_backward {kind} H={H} D={D} {xk}->{dxk}")
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss, alpha, (xh, xc, xd), (gh, gc, gd) = _bwd_inputs(g, H, D, xk, 100 + H * D)
+    colptr, row_t, _, perm = oracle.csr_to_csc(g.rowptr, g.col, None, g.n_cols)
+    ref = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, xh.reshape(g.n_cols, H * D),
+                              gh.reshape(g.n_rows, H * D), H, D, slope=0.2, x_dtype=xc, dy_dtype=gc)
+    dx_dtype = {"f32": torch.float32, "bf16": torch.bfloat16}[dxk]
+    cp_d, rt_d, pm_d = dev(colptr), dev(row_t), dev(perm)
+    for spec, spec_t in PLAN_PAIRS:
+        plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+        plan_t = _make_plan(cg, cp_d, g.nnz, spec_t, H * D, max_heads=H)
+        try:
+            out = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
+                                  plan=plan, plan_t=plan_t, dx_dtype=dx_dtype)
+            _check_bwd(out, ref, (kind, H, D, spec, spec_t))
+        finally:
+            for p in (plan, plan_t):
+                if p is not None:
+                    p.close()
+
+
+def test_gat_backward_unnormalized_weights_and_repeat(cg):
+    """Any fp32 weights (not only softmax outputs), two calls in a row on the
+    same plans give the same bits (the plan workspaces are reused)."""
+    import torch
+    g = _graph("hubs", seed=14)
+    H, D = 4, 64
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss, alpha, (xh, xc, xd), (gh, gc, gd) = _bwd_inputs(g, H, D, "bf16", 7, softmax_alpha=False)
+    colptr, row_t, _, perm = oracle.csr_to_csc(g.rowptr, g.col, None, g.n_cols)
+    cp_d, rt_d, pm_d = dev(colptr), dev(row_t), dev(perm)
+    ref = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, xh.reshape(g.n_cols, H * D),
+                              gh.reshape(g.n_rows, H * D), H, D, slope=0.2, x_dtype=xc, dy_dtype=gc)
+    plan = cg.Plan(rp, g.nnz, H * D, max_heads=H, mode="neighbor_group", group_size=32)
+    plan_t = cg.Plan(cp_d, g.nnz, H * D, max_heads=H, mode="neighbor_group", group_size=16)
+    try:
+        a = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
+                            plan=plan, plan_t=plan_t, dx_dtype=torch.float32)
+        _check_bwd(a, ref, "unnormalized")
+        b = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
+                            plan=plan, plan_t=plan_t, dx_dtype=torch.float32)
+        for k in a:
+            assert torch.equal(a[k], b[k]), k
+    finally:
+        plan.close()
+        plan_t.close()
