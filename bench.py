@@ -72,34 +72,54 @@ def b_plan(N, n_units):
 
 # ----------------------------------------------------------- HBM counters
 
-def kernel_source_sha() -> str:
-    import glob
+# The step's candidate roofline kernels: the sources that define each one, its
+# instantiation on the benchmark workload (bf16 in and out, 16-byte vectors,
+# one chunk, buffer gathers), and which of that kernel's dispatches in one step
+# is the op (the SpMM and the transposed SpMM share an instantiation).
+ROOFLINE_KERNELS = {
+    "spmm": dict(files=["common.hpp", "internal.hpp", "spmm_kernel.hpp", "spmm.hip"],
+                 name="void k_spmm<bf16_t, bf16_t, 8, 1, true, false, false>", per_step=2, index=0),
+    "spmm_t": dict(files=["common.hpp", "internal.hpp", "spmm_kernel.hpp", "spmm.hip"],
+                   name="void k_spmm<bf16_t, bf16_t, 8, 1, true, false, false>", per_step=2, index=1),
+    "gat": dict(files=["common.hpp", "internal.hpp", "gat_kernel.hpp", "gat.hip"],
+                name="void k_gat<bf16_t, bf16_t, 8, 1, true, false>", per_step=1, index=0),
+}
+
+
+def kernel_source_sha(kernel: str) -> str:
     import hashlib
     here = os.path.dirname(os.path.abspath(__file__))
-    files = sorted(glob.glob(os.path.join(here, "paper_2103_00959_amd", "csrc", "*")))
-    return hashlib.sha256(b"".join(open(f, "rb").read() for f in files)).hexdigest()[:16]
+    csrc = os.path.join(here, "paper_2103_00959_amd", "csrc")
+    files = ROOFLINE_KERNELS[kernel]["files"]
+    return hashlib.sha256(b"".join(open(os.path.join(csrc, f), "rb").read() for f in files)).hexdigest()[:16]
 
 
-def recorded_traffic(workload: str, trace_name: str):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE summary (already scaled by the copy calibration),
-    or None when the kernels changed since the counters were taken."""
-    here = os.path.dirname(os.path.abspath(__file__))
-    path = os.path.join(here, "profiles", f"{workload}_hbm_traffic.json")
+def recorded_traffic(workload: str, kernel: str, profiles_dir: str | None = None):
+    """HBM bytes of one launch of the step's kernel `kernel` from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled by the copy calibration;
+    the dispatch of the timed step of a --warmup 1 run), or None when that
+    kernel's sources changed since the counters were taken."""
+    if profiles_dir is None:
+        profiles_dir = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles")
+    path = os.path.join(profiles_dir, f"{workload}_hbm_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("source_sha16") != kernel_source_sha():
+    shas = rec.get("source_sha16")
+    if not isinstance(shas, dict) or shas.get(kernel) != kernel_source_sha(kernel):
         return None
-    prefix = {"gat": "void k_gat<", "spmm": "void k_spmm<", "spmm_t": "void k_spmm<"}[trace_name]
-    for k, v in rec["kernels"].items():
-        if k.startswith(prefix):
-            return dict(bytes=v["fetch_bytes"] + v["write_bytes"], fetch_bytes=v["fetch_bytes"],
-                        write_bytes=v["write_bytes"], kernel=k, source=os.path.basename(path))
-    return None
+    spec = ROOFLINE_KERNELS[kernel]
+    disp = rec["kernels"].get(spec["name"])
+    if not disp:
+        return None
+    i = spec["per_step"] * rec.get("warmup", 1) + spec["index"]
+    if i >= len(disp):
+        return None
+    d = disp[i]
+    return dict(bytes=d["fetch_bytes"] + d["write_bytes"], fetch_bytes=d["fetch_bytes"],
+                write_bytes=d["write_bytes"], kernel=spec["name"], dispatch=i, dur_ms=d["dur_ms"],
+                source=os.path.basename(path))
 
-
-# ----------------------------------------------------------- CPU baseline
 
 def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
     """Time the oracle (fp64, all host threads) on a random row sample of the
@@ -194,7 +214,7 @@ def main():
 
     plan = cg.Plan(rowptr, E, max_feat=max(F, H * D), max_heads=H, group_size=args.group_size)
     csc()
-    plan_t = cg.Plan(colptr, E, max_feat=F, group_size=args.group_size)
+    plan_t = cg.Plan(colptr, E, max_feat=F, max_heads=H, group_size=args.group_size)
     torch.cuda.synchronize()
     info, info_t = plan.info(), plan_t.info()
     log(f"plan: {info['mode_name']} units={info['n_units']} long={info['n_long_units']} "
@@ -335,6 +355,42 @@ def main():
                                                     out=alpha_buf))
     ms_gat_a = time_op(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
                                                 out=Yg, alpha_out=alpha_buf))
+    def time_op_kernels(fn, reps=5):
+        """Average time of fn and of each library kernel it launches."""
+        ms = time_op(fn, reps)
+        cg.trace_enable(4096)
+        cg.trace_reset()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        per_k = {}
+        for name, kms in cg.trace_read():
+            per_k[name] = per_k.get(name, 0.0) + kms / reps
+        cg.trace_enable(0)
+        return ms, per_k
+
+    # GAT backward (dY random bf16, the forward's alpha), CSR pass + CSC pass
+    dYg = up(synth.f32_to_bf16_bits(synth.normal_f32((N, H * D), 4100 + args.config)).view(np.int16),
+             torch.bfloat16).view(N, H, D)
+    cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg, alpha_out=alpha_buf)
+    bwd_out = {"dX": torch.empty((M, H, D), dtype=torch.bfloat16, device=dev),
+               "dalpha": torch.empty((E, H), dtype=torch.float32, device=dev),
+               "dscore": torch.empty((E, H), dtype=torch.float32, device=dev),
+               "ds_dst": torch.empty((N, H), dtype=torch.float32, device=dev),
+               "ds_src": torch.empty((M, H), dtype=torch.float32, device=dev)}
+    ms_bwd, k_bwd = time_op_kernels(lambda: cg.gat_backward(
+        rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha_buf, Xg, dYg, 0.2, plan=plan,
+        plan_t=plan_t, out=bwd_out))
+    dot_out = torch.empty((E, H), dtype=torch.float32, device=dev)
+    ms_dot, k_dot = time_op_kernels(lambda: cg.sddmm_dot(rowptr, col, dYg, Xg, plan=plan, out=dot_out))
+    b_dot = 4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * E * H
+    del bwd_out, dYg, dot_out
+    b_bwd_rows = (4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * N * H + 4 * E * H
+                  + 4 * E * H + 4 * E * H + 4 * E * H + 4 * N * H)
+    b_bwd_cols = (4 * (M + 1) + 4 * E + 4 * E + E * H * D * 2 + 4 * E * H + 4 * E * H
+                  + M * H * D * 2 + 4 * M * H)
+    b_bwd = b_bwd_rows + b_bwd_cols
+
     ms_mean = time_op(lambda: cg.gspmm(rowptr, col, val, X, "mean", plan=plan, out=Y))
     arg_buf = torch.empty((N, F), dtype=torch.int32, device=dev)
     ms_max = time_op(lambda: cg.gspmm(rowptr, col, val, X, "max", plan=plan, out=Y,
@@ -351,6 +407,17 @@ def main():
         "gat_aggregate_with_alpha": dict(ms=ms_gat_a, algorithmic_GB=b_gat_a / 1e9,
                                          eff_GBps=b_gat_a / (ms_gat_a * 1e-3) / 1e9,
                                          edges_per_s=E / (ms_gat_a * 1e-3)),
+        "gat_backward": dict(ms=ms_bwd, algorithmic_GB=b_bwd / 1e9,
+                             eff_GBps=b_bwd / (ms_bwd * 1e-3) / 1e9,
+                             edges_per_s=E / (ms_bwd * 1e-3),
+                             kernels_ms=k_bwd,
+                             rows_pass_GBps=b_bwd_rows / (k_bwd.get("gat_bwd_rows", 0) * 1e-3) / 1e9
+                             if k_bwd.get("gat_bwd_rows") else None,
+                             cols_pass_GBps=b_bwd_cols / ((k_bwd.get("gat_bwd_cols", 0)
+                                                           + k_bwd.get("gat_bwd_cols_tiny", 0)) * 1e-3) / 1e9
+                             if k_bwd.get("gat_bwd_cols") else None),
+        "sddmm_dot": dict(ms=ms_dot, algorithmic_GB=b_dot / 1e9,
+                          eff_GBps=b_dot / (ms_dot * 1e-3) / 1e9, edges_per_s=E / (ms_dot * 1e-3)),
         "gspmm_mean": dict(ms=ms_mean, algorithmic_GB=b_mean / 1e9,
                            eff_GBps=b_mean / (ms_mean * 1e-3) / 1e9,
                            edges_per_s=E / (ms_mean * 1e-3)),
@@ -359,7 +426,9 @@ def main():
                                    edges_per_s=E / (ms_max * 1e-3)),
     }
     log(f"extra: sddmm_edge_softmax {ms_soft:.3f} ms, gat_aggregate+alpha {ms_gat_a:.3f} ms, "
-        f"gspmm mean {ms_mean:.3f} ms, max+arg {ms_max:.3f} ms")
+        f"gspmm mean {ms_mean:.3f} ms, max+arg {ms_max:.3f} ms, sddmm_dot {ms_dot:.3f} ms, "
+        f"gat backward {ms_bwd:.3f} ms "
+        f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd.items())})")
 
     out = {
         "metric": METRIC, "value": value, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
