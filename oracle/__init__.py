@@ -60,6 +60,9 @@ def _load():
     lib.oracle_gat_backward.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, dbl, P, P, i32, P, i32,
                                         i32, P, P, P, P, P, P, P, i32, P, P, P, P, P]
     lib.oracle_sddmm_dot.argtypes = [i32, i32, i64, P, P, i32, i32, P, i32, P, i32, i32, P, P, P]
+    lib.oracle_epilogue.argtypes = [i64, i32, P, i32, P]
+    lib.oracle_linear.argtypes = [i64, i32, i32, P, i32, P, i32, P, i32, P, P]
+    lib.oracle_head_scores.argtypes = [i64, i32, i32, P, i32, P, P, P, P, P, P]
     _lib = lib
     return lib
 
@@ -289,3 +292,113 @@ def sddmm_dot(rowptr, col, P, Q, H, D, p_dtype=None, q_dtype=None, rows=None, n_
                                   0 if sel is None else sel.size, _p(sel), _p(out), _p(ab))
     _check(rc, "sddmm_dot")
     return out, ab
+
+
+ACT = {"none": 0, "relu": 1, "elu": 2}
+
+
+def epilogue(Y, bias=None, act="none"):
+    """act(Y + bias) in place on a float64 [n, F] array (returns it)."""
+    Y = np.ascontiguousarray(Y, dtype=np.float64)
+    b = _c(bias, np.float32)
+    n, F = Y.shape
+    _check(_load().oracle_epilogue(n, F, _p(b), ACT[act], _p(Y)), "epilogue")
+    return Y
+
+
+def linear(X, W, bias=None, act="none", x_dtype=None, w_dtype=None):
+    """Y = act(X W^T + bias) in float64 with its error scale.  X [n, k], W [m, k]
+    (fp32 arrays, or uint16 bit patterns with explicit dtype codes)."""
+    X, W = np.ascontiguousarray(X), np.ascontiguousarray(W)
+    b = _c(bias, np.float32)
+    n, k = X.shape
+    m = W.shape[0]
+    Y = np.empty((n, m), np.float64)
+    A = np.empty((n, m), np.float64)
+    _check(_load().oracle_linear(n, k, m, _p(X), _x_code(X, x_dtype), _p(W), _x_code(W, w_dtype),
+                                 _p(b), ACT[act], _p(Y), _p(A)), "linear")
+    return Y, A
+
+
+def head_scores(Z, a_src, a_dst, H, D, z_dtype=None):
+    """(s_src, s_dst, src_abs, dst_abs) float64 [n, H] for Z [n, H*D]."""
+    Z = np.ascontiguousarray(Z)
+    a_s, a_d = _c(a_src, np.float32), _c(a_dst, np.float32)
+    n = Z.shape[0]
+    out = [np.empty((n, H), np.float64) for _ in range(4)]
+    _check(_load().oracle_head_scores(n, H, D, _p(Z), _x_code(Z, z_dtype), _p(a_s), _p(a_d),
+                                      *[_p(o) for o in out]), "head_scores")
+    return tuple(out)
+
+
+def _row_max_over_edges(rowptr, col, per_row, per_col):
+    """M[i, h] = max over the edges k of row i of per_row[i, h] + per_col[col[k], h] (0 when empty)."""
+    rp = np.asarray(rowptr, np.int64)
+    deg = np.diff(rp)
+    rows = np.repeat(np.arange(rp.size - 1), deg)
+    v = per_row[rows] + per_col[np.asarray(col)]
+    M = np.zeros_like(per_row)
+    nz = deg > 0
+    if v.size:
+        M[nz] = np.maximum.reduceat(v, rp[:-1][nz], axis=0)
+    return M
+
+
+def gcn_forward(rowptr, col, val, X, params, x_dtype=BF16, act_dtype=BF16, rows=None):
+    """2-layer GCN inference with the activations stored in act_dtype between the
+    steps, as the GPU pipeline stores them: Z1 = X W1^T, H1 = relu(A Z1 + b1),
+    Z2 = H1 W2^T, Y = A Z2 + b2 (everything else in float64).
+    Returns (Y, E): the output before its own rounding and an error scale E that
+    bounds how far a one-unit difference in the rounding of any stored
+    intermediate can move Y: each stage's scale is the stage applied to the
+    absolute values of its inputs' scales (the activations are 1-Lipschitz).
+    `rows` restricts the rows of the last aggregation."""
+    W1, b1, W2, b2 = params["W1"], params["b1"], params["W2"], params["b2"]
+    wd = params.get("w_dtype", BF16)
+    aval = None if val is None else np.abs(np.asarray(val, np.float32))
+    Z1, EZ1 = linear(X, W1, x_dtype=x_dtype, w_dtype=wd)
+    H1, _ = spmm(rowptr, col, val, round_to(Z1, act_dtype), x_dtype=act_dtype)
+    H1 = epilogue(H1, b1, "relu")
+    EH1, _ = spmm(rowptr, col, aval, EZ1.astype(np.float32))
+    EH1 += np.abs(np.asarray(b1, np.float64))[None, :]
+    Z2, _ = linear(round_to(H1, act_dtype), W2, x_dtype=act_dtype, w_dtype=wd)
+    EZ2, _ = linear(EH1.astype(np.float32), np.abs(decode(W2, wd)).astype(np.float32))
+    Y, _ = spmm(rowptr, col, val, round_to(Z2, act_dtype), x_dtype=act_dtype, rows=rows)
+    Y = epilogue(Y, b2, "none")
+    EY, _ = spmm(rowptr, col, aval, EZ2.astype(np.float32), rows=rows)
+    return Y, EY + np.abs(np.asarray(b2, np.float64))[None, :]
+
+
+def _gat_layer(rowptr, col, Zs, EZ, a_src, a_dst, H, D, slope, bias, act, act_dtype, rows=None):
+    """One GAT layer on stored features Zs [n, H*D] (act_dtype bits) with scale EZ:
+    scores from the stored features, rounded to fp32 as they are stored; output and scale."""
+    ss, sd, s_abs, d_abs = head_scores(Zs, a_src, a_dst, H, D, z_dtype=act_dtype)
+    ss32, sd32 = ss.astype(np.float32), sd.astype(np.float32)
+    Y, A = gat(rowptr, col, sd32, ss32, Zs, H, D, slope=slope, x_dtype=act_dtype, rows=rows)
+    Y = epilogue(Y, bias, act)
+    EY, _ = gat(rowptr, col, sd32, ss32, EZ.astype(np.float32), H, D, slope=slope, rows=rows)
+    # a change of the scores by at most delta_e moves each weight by at most
+    # 2 delta_e alpha; delta_e <= (scale of s_dst + scale of s_src) per edge
+    M = _row_max_over_edges(rowptr, col, d_abs, s_abs)
+    if rows is not None:
+        M = M[np.asarray(rows)]
+    EY += 2.0 * np.repeat(M, D, axis=1) * A
+    if bias is not None:
+        EY += np.abs(np.asarray(bias, np.float64))[None, :]
+    return Y, EY
+
+
+def gat_forward(rowptr, col, X, params, slope=0.2, x_dtype=BF16, act_dtype=BF16, rows=None):
+    """2-layer GAT inference (layer 1: H heads of D concatenated, ELU; layer 2: one
+    head of C outputs), activations stored in act_dtype, scores in fp32, the rest in
+    float64.  Returns (Y, E) as gcn_forward."""
+    H, D = np.asarray(params["a_src1"]).shape
+    C = params["W2"].shape[0]
+    wd = params.get("w_dtype", BF16)
+    Z1, EZ1 = linear(X, params["W1"], x_dtype=x_dtype, w_dtype=wd)
+    H1, EH1 = _gat_layer(rowptr, col, round_to(Z1, act_dtype), EZ1, params["a_src1"], params["a_dst1"],
+                         H, D, slope, params["b1"], "elu", act_dtype)
+    Z2, _ = linear(round_to(H1, act_dtype), params["W2"], x_dtype=act_dtype, w_dtype=wd)
+    EZ2, _ = linear(EH1.astype(np.float32), np.abs(decode(params["W2"], wd)).astype(np.float32))
+    return _gat_layer(rowptr, col, round_to(Z2, act_dtype), EZ2, params["a_src2"], params["a_dst2"],
+                      1, C, slope, params["b2"], "none", act_dtype, rows=rows)

@@ -654,3 +654,78 @@ int oracle_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t 
     free(off);
     return 0;
 }
+
+/* ------------------------------------------------ dense layers (next row 3) */
+
+/* The activations of the layer epilogues: 0 identity, 1 ReLU max(v, 0),
+ * 2 ELU (v > 0 ? v : exp(v) - 1). */
+static double act_apply(int32_t act, double v)
+{
+    if (act == 1) return v > 0.0 ? v : 0.0;
+    if (act == 2) return v > 0.0 ? v : expm1(v);
+    return v;
+}
+
+/* In-place act(v + bias[f]) over an n x F array (bias may be NULL). */
+int oracle_epilogue(int64_t n, int32_t F, const float *bias, int32_t act, double *v)
+{
+    if (n < 0 || F < 0 || act < 0 || act > 2) return -1;
+    for (int64_t i = 0; i < n; ++i)
+        for (int32_t f = 0; f < F; ++f) {
+            double x = v[i * F + f] + (bias ? (double)bias[f] : 0.0);
+            v[i * F + f] = act_apply(act, x);
+        }
+    return 0;
+}
+
+/* Dense layer: Y[i,c] = act(sum_j X[i,j] W[c,j] + bias[c]) with X n x k and W
+ * m x k (the layer's out x in weights), in double; Abs[i,c] = sum_j |X||W| +
+ * |bias[c]| (the activations are 1-Lipschitz, so it bounds the error of the
+ * activated value too). */
+int oracle_linear(int64_t n, int32_t k, int32_t m, const void *X, int32_t x_dtype, const void *W,
+                  int32_t w_dtype, const float *bias, int32_t act, double *Y, double *Abs)
+{
+    if (n < 0 || k < 0 || m < 0 || act < 0 || act > 2) return -1;
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        for (int32_t c = 0; c < m; ++c) {
+            double s = 0.0, sa = 0.0;
+            for (int32_t j = 0; j < k; ++j) {
+                double x = load_elem(X, x_dtype, i * k + j);
+                double w = load_elem(W, w_dtype, (int64_t)c * k + j);
+                s += x * w;
+                sa += fabs(x) * fabs(w);
+            }
+            double b = bias ? (double)bias[c] : 0.0;
+            Y[i * m + c] = act_apply(act, s + b);
+            if (Abs) Abs[i * m + c] = sa + fabs(b);
+        }
+    return 0;
+}
+
+/* Per-head attention scores: s_src[i,h] = sum_d Z[i,h,d] a_src[h,d], s_dst
+ * likewise with a_dst, in double, with their error scales (sums of |terms|). */
+int oracle_head_scores(int64_t n, int32_t H, int32_t D, const void *Z, int32_t z_dtype,
+                       const float *a_src, const float *a_dst, double *s_src, double *s_dst,
+                       double *src_abs, double *dst_abs)
+{
+    if (n < 0 || H < 1 || D < 1) return -1;
+    int64_t HD = (int64_t)H * D;
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        for (int32_t h = 0; h < H; ++h) {
+            double ps = 0.0, pd = 0.0, as = 0.0, ad = 0.0;
+            for (int32_t d = 0; d < D; ++d) {
+                double z = load_elem(Z, z_dtype, i * HD + (int64_t)h * D + d);
+                ps += z * (double)a_src[(int64_t)h * D + d];
+                pd += z * (double)a_dst[(int64_t)h * D + d];
+                as += fabs(z) * fabs((double)a_src[(int64_t)h * D + d]);
+                ad += fabs(z) * fabs((double)a_dst[(int64_t)h * D + d]);
+            }
+            s_src[i * H + h] = ps;
+            s_dst[i * H + h] = pd;
+            if (src_abs) src_abs[i * H + h] = as;
+            if (dst_abs) dst_abs[i * H + h] = ad;
+        }
+    return 0;
+}

@@ -786,3 +786,112 @@ def test_gat_backward_invariants():
         assert np.array_equal(r2["dX"], r["dX"][csel])
         idx = np.concatenate([np.arange(g.rowptr[x], g.rowptr[x + 1]) for x in sel])
         assert np.array_equal(r2["dscore"], r["dscore"][idx])
+
+
+# ------------------------------------------------------------ dense layers and 2-layer models
+
+def _bf16(x):
+    return synth.f32_to_bf16_bits(np.asarray(x, np.float32))
+
+
+def _dec(bits):
+    return oracle.decode(bits, oracle.BF16)
+
+
+def test_linear_against_numpy():
+    rng = np.random.default_rng(50)
+    for n, k, m in ((7, 5, 3), (33, 602, 41), (1, 16, 128)):
+        X, W = _bf16(rng.standard_normal((n, k))), _bf16(rng.standard_normal((m, k)))
+        b = rng.standard_normal(m).astype(np.float32)
+        for act in ("none", "relu", "elu"):
+            Y, A = oracle.linear(X, W, b, act, x_dtype=oracle.BF16, w_dtype=oracle.BF16)
+            pre = _dec(X) @ _dec(W).T + b.astype(np.float64)
+            want = {"none": pre, "relu": np.maximum(pre, 0.0), "elu": np.where(pre > 0, pre, np.expm1(pre))}[act]
+            np.testing.assert_allclose(Y, want, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(A, np.abs(_dec(X)) @ np.abs(_dec(W)).T + np.abs(b), rtol=1e-12)
+
+
+def test_epilogue_closed_forms():
+    v = np.array([[-1.0, 0.0, 2.0]])
+    assert oracle.epilogue(v.copy(), None, "relu").tolist() == [[0.0, 0.0, 2.0]]
+    e = oracle.epilogue(v.copy(), None, "elu")
+    assert e[0, 0] == np.expm1(-1.0) and e[0, 1] == 0.0 and e[0, 2] == 2.0
+    b = np.array([1.0, -1.0, 0.5], np.float32)
+    assert oracle.epilogue(v.copy(), b, "none").tolist() == [[0.0, -1.0, 2.5]]
+
+
+def test_head_scores_against_numpy():
+    rng = np.random.default_rng(51)
+    n, H, D = 40, 3, 7
+    Z = _bf16(rng.standard_normal((n, H * D)))
+    a_s, a_d = rng.standard_normal((H, D)).astype(np.float32), rng.standard_normal((H, D)).astype(np.float32)
+    ss, sd, sa, da = oracle.head_scores(Z, a_s, a_d, H, D, z_dtype=oracle.BF16)
+    Zd = _dec(Z).reshape(n, H, D)
+    np.testing.assert_allclose(ss, np.einsum("nhd,hd->nh", Zd, a_s.astype(np.float64)), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(sd, np.einsum("nhd,hd->nh", Zd, a_d.astype(np.float64)), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(sa, np.einsum("nhd,hd->nh", np.abs(Zd), np.abs(a_s)), rtol=1e-12)
+    np.testing.assert_allclose(da, np.einsum("nhd,hd->nh", np.abs(Zd), np.abs(a_d)), rtol=1e-12)
+
+
+def _mlp_params(rng, k, hid, out):
+    return dict(W1=_bf16(rng.standard_normal((hid, k)) * 0.3), b1=rng.standard_normal(hid).astype(np.float32),
+                W2=_bf16(rng.standard_normal((out, hid)) * 0.3), b2=rng.standard_normal(out).astype(np.float32))
+
+
+def test_gcn_forward_identity_graph_is_an_mlp():
+    """With A = I the model is relu(X W1^T + b1) W2^T + b2, activations stored in bf16."""
+    rng = np.random.default_rng(52)
+    n, k, hid, out = 30, 12, 16, 5
+    rowptr = np.arange(n + 1, dtype=np.int32)
+    col = np.arange(n, dtype=np.int32)
+    X = _bf16(rng.standard_normal((n, k)))
+    p = _mlp_params(rng, k, hid, out)
+    Y, E = oracle.gcn_forward(rowptr, col, None, X, p)
+    Z1 = _dec(oracle.round_to(_dec(X) @ _dec(p["W1"]).T, oracle.BF16))
+    H1 = _dec(oracle.round_to(np.maximum(Z1 + p["b1"], 0.0), oracle.BF16))
+    Z2 = _dec(oracle.round_to(H1 @ _dec(p["W2"]).T, oracle.BF16))
+    np.testing.assert_allclose(Y, Z2 + p["b2"], rtol=1e-12, atol=1e-12)
+    assert np.all(np.abs(Y) <= E * (1 + 2 ** -6))
+    # selected output rows
+    sel = np.array([n - 1, 3], np.int32)
+    Ys, Es = oracle.gcn_forward(rowptr, col, None, X, p, rows=sel)
+    assert np.array_equal(Ys, Y[sel]) and np.array_equal(Es, E[sel])
+
+
+def test_gcn_forward_dense_graph():
+    """On a small irregular graph: the dense A applied between the stored layers."""
+    rng = np.random.default_rng(53)
+    g = synth.random_csr(25, 25, rng, mean_deg=4, empty_frac=0.1)
+    X = _bf16(rng.standard_normal((25, 10)))
+    p = _mlp_params(rng, 10, 8, 3)
+    Y, E = oracle.gcn_forward(g.rowptr, g.col, g.val, X, p)
+    A = _dense(g)
+    Z1 = _dec(oracle.round_to(_dec(X) @ _dec(p["W1"]).T, oracle.BF16))
+    H1 = _dec(oracle.round_to(np.maximum(A @ Z1 + p["b1"], 0.0), oracle.BF16))
+    Z2 = _dec(oracle.round_to(H1 @ _dec(p["W2"]).T, oracle.BF16))
+    np.testing.assert_allclose(Y, A @ Z2 + p["b2"], rtol=1e-11, atol=1e-11)
+
+
+def test_gat_forward_zero_attention_is_a_mean():
+    """With zero attention vectors every score is 0: each layer averages its
+    neighbours' stored features (then bias, ELU on the first layer)."""
+    rng = np.random.default_rng(54)
+    g = synth.random_csr(25, 25, rng, mean_deg=4, empty_frac=0.1)
+    n, k, H, D, C = 25, 10, 2, 4, 3
+    X = _bf16(rng.standard_normal((n, k)))
+    p = dict(W1=_bf16(rng.standard_normal((H * D, k)) * 0.3), a_src1=np.zeros((H, D), np.float32),
+             a_dst1=np.zeros((H, D), np.float32), b1=rng.standard_normal(H * D).astype(np.float32),
+             W2=_bf16(rng.standard_normal((C, H * D)) * 0.3), a_src2=np.zeros((1, C), np.float32),
+             a_dst2=np.zeros((1, C), np.float32), b2=rng.standard_normal(C).astype(np.float32))
+    Y, E = oracle.gat_forward(g.rowptr, g.col, X, p)
+    counts = np.zeros((n, n))
+    rows = np.repeat(np.arange(n), np.diff(g.rowptr))
+    np.add.at(counts, (rows, g.col), 1.0)
+    deg = counts.sum(1, keepdims=True)
+    M = np.divide(counts, deg, out=np.zeros_like(counts), where=deg > 0)
+    Z1 = _dec(oracle.round_to(_dec(X) @ _dec(p["W1"]).T, oracle.BF16))
+    pre = M @ Z1 + p["b1"]
+    H1 = _dec(oracle.round_to(np.where(pre > 0, pre, np.expm1(pre)), oracle.BF16))
+    Z2 = _dec(oracle.round_to(H1 @ _dec(p["W2"]).T, oracle.BF16))
+    np.testing.assert_allclose(Y, M @ Z2 + p["b2"], rtol=1e-11, atol=1e-11)
+    assert np.all(np.abs(Y) <= E * (1 + 2 ** -6))
