@@ -79,6 +79,10 @@ typedef enum {
     COGDL_COMPUTE_COPY = 3   /* x (val ignored) */
 } cogdl_compute;
 
+/* Activation applied by the epilogues of the layer entry points (after the
+ * bias): identity, max(v, 0), or ELU v > 0 ? v : exp(v) - 1. */
+typedef enum { COGDL_ACT_NONE = 0, COGDL_ACT_RELU = 1, COGDL_ACT_ELU = 2 } cogdl_act;
+
 /* Backend choice of the workload balancer (section 2.2, the balancer listing). */
 typedef enum {
     COGDL_BALANCE_AUTO = 0,            /* data-aware choice, see cogdl_plan_create */
@@ -179,14 +183,16 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
  * An empty row gives 0 (and arg -1).  Messages and sums are computed in
  * fp32.  arg: device int32 n_rows x F, written for MAX only, may be NULL.
  * MAX supports y_dtype equal to x_dtype or fp32 (COGDL_ERR_DTYPE otherwise);
- * an unknown reduce or compute code is COGDL_ERR_INVALID.  Other arguments
- * and errors as for cogdl_spmm.
+ * an unknown reduce, compute or act code is COGDL_ERR_INVALID.  Epilogue
+ * (the aggregation half of a GCN layer): Y[i, f] = act(Y[i, f] + bias[f]),
+ * bias fp32 F entries or NULL, applied to every row (an empty row gives
+ * act(bias)).  Other arguments and errors as for cogdl_spmm.
  * ---------------------------------------------------------------------- */
 cogdl_status cogdl_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
                          const int32_t *col, const float *val, int32_t F, const void *X,
                          cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, cogdl_reduce reduce,
-                         cogdl_compute compute, int32_t *arg, const cogdl_plan *plan,
-                         hipStream_t stream);
+                         cogdl_compute compute, const float *bias, cogdl_act act, int32_t *arg,
+                         const cogdl_plan *plan, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * CSR -> CSC transpose of the graph structure, the setup of the backward
@@ -256,6 +262,38 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                  const float *alpha_in, const void *X, cogdl_dtype x_dtype,
                                  void *Y, cogdl_dtype y_dtype, float *alpha_out,
                                  const cogdl_plan *plan, hipStream_t stream);
+
+/* The same with an epilogue (the aggregation half of a GAT layer):
+ * Y[i, h, d] = act(aggregate + bias[h * D + d]), bias fp32 H*D entries or
+ * NULL, every row included; act outside cogdl_act is COGDL_ERR_INVALID. */
+cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                     const int32_t *rowptr, const int32_t *col, int32_t H,
+                                     int32_t D, const float *s_dst, const float *s_src,
+                                     float negative_slope, const float *alpha_in, const void *X,
+                                     cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype,
+                                     float *alpha_out, const float *bias, cogdl_act act,
+                                     const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Dense layer of the GCN and GAT models that the sparse operators of section
+ * 2.2 serve (the feature transform of every layer; the paper's end-to-end
+ * inference workload is a 2-layer GCN or GAT):
+ *     Y[i, c] = act(sum_j X[i, j] * W[c, j] + bias[c])
+ * X: n x k, W: m x k (the out x in weights of the layer), both bf16 or both
+ * fp16 (dtype; other codes COGDL_ERR_DTYPE); bias: fp32, m entries, or NULL;
+ * Y: n x m of y_dtype.  fp32 accumulation on the matrix cores.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_linear(int64_t n, int32_t k, int32_t m, const void *X, const void *W,
+                          cogdl_dtype dtype, const float *bias, cogdl_act act, void *Y,
+                          cogdl_dtype y_dtype, hipStream_t stream);
+
+/* Per-head attention scores of a GAT layer (section 2.2, the SDDMM inputs):
+ *     s_src[i, h] = sum_d Z[i, h, d] * a_src[h, d],  s_dst likewise with a_dst
+ * Z: n x H x D of z_dtype; a_src, a_dst: fp32 H x D; s_src, s_dst: fp32 n x H
+ * (either may be NULL, with its vector).  fp32 accumulation. */
+cogdl_status cogdl_head_scores(int64_t n, int32_t H, int32_t D, const void *Z,
+                               cogdl_dtype z_dtype, const float *a_src, const float *a_dst,
+                               float *s_src, float *s_dst, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Dot-product SDDMM -- section 2.2, T = A (.) (P Q^T), per head: for every

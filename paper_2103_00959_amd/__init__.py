@@ -64,7 +64,11 @@ def lib():
     L.cogdl_plan_units.argtypes = [P, P, i64, P]
     L.cogdl_spmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_gspmm.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int,
-                              ctypes.c_int, ctypes.c_int, P, P, P]
+                              ctypes.c_int, ctypes.c_int, P, ctypes.c_int, P, P, P]
+    L.cogdl_gat_aggregate_act.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, P,
+                                          ctypes.c_int, P, ctypes.c_int, P, P, ctypes.c_int, P, P]
+    L.cogdl_linear.argtypes = [i64, i32, i32, P, P, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P]
+    L.cogdl_head_scores.argtypes = [i64, i32, i32, P, ctypes.c_int, P, P, P, P, P]
     L.cogdl_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_csr_to_csc_workspace.argtypes = [i32, i32, i64, ctypes.POINTER(sz)]
     L.cogdl_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P, sz, P]
@@ -82,7 +86,8 @@ def lib():
     for name in ("cogdl_trace_enable", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate",
-                 "cogdl_sddmm_dot", "cogdl_gat_backward"):
+                 "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act", "cogdl_linear",
+                 "cogdl_head_scores"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -221,13 +226,15 @@ def spmm(rowptr, col, val, X, plan: Plan | None = None, out_dtype=None, out=None
 
 REDUCE = {"sum": 0, "mean": 1, "max": 2}
 COMPUTE = {"mul": 0, "add": 1, "sub": 2, "copy": 3}
+ACT = {"none": 0, "relu": 1, "elu": 2}
 
 
 def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, out_dtype=None,
-          out=None, return_arg: bool = False, arg=None, compute: str = "mul"):
+          out=None, return_arg: bool = False, arg=None, compute: str = "mul", bias=None,
+          act: str = "none"):
     """Eq. 1 with reduce = sum, mean or max over the edges k of row i of the
     message val[k] * x (compute "mul"), x + val[k] ("add"), x - val[k] ("sub")
-    or x ("copy"), x = X[col[k]].
+    or x ("copy"), x = X[col[k]]; then act(. + bias) (bias fp32 [F] or None).
 
     For max, ``return_arg`` also returns the int32 edge id of the first edge
     attaining each output (-1 on empty rows); max keeps X's dtype or fp32."""
@@ -236,6 +243,9 @@ def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, ou
         raise ValueError(f"reduce must be one of {sorted(REDUCE)}")
     if compute not in COMPUTE:
         raise ValueError(f"compute must be one of {sorted(COMPUTE)}")
+    if act not in ACT:
+        raise ValueError(f"act must be one of {sorted(ACT)}")
+    _dev(bias, "bias", torch.float32)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
     _dev(val, "val", torch.float32), _dev(X, "X")
     n_rows = rowptr.numel() - 1
@@ -250,8 +260,8 @@ def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, ou
     _dev(arg, "arg", torch.int32)
     _check(lib().cogdl_gspmm(n_rows, X.shape[0], col.numel(), _ptr(rowptr), _ptr(col), _ptr(val), F,
                              _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), REDUCE[reduce],
-                             COMPUTE[compute], _ptr(arg), _plan_handle(plan), _stream()),
-           "cogdl_gspmm")
+                             COMPUTE[compute], _ptr(bias), ACT[act], _ptr(arg), _plan_handle(plan),
+                             _stream()), "cogdl_gspmm")
     return (out, arg) if return_arg else out
 
 
@@ -318,9 +328,13 @@ def sddmm_edge_softmax(rowptr, col, s_dst, s_src, negative_slope: float = 0.2,
 
 def gat_aggregate(rowptr, col, s_dst, s_src, X, negative_slope: float = 0.2, alpha_in=None,
                   return_alpha: bool = False, plan: Plan | None = None, out_dtype=None, out=None,
-                  alpha_out=None):
-    """Fused GAT aggregation.  X is [n_cols, H, D]; returns Y [n_rows, H, D] (and alpha)."""
+                  alpha_out=None, bias=None, act: str = "none"):
+    """Fused GAT aggregation.  X is [n_cols, H, D]; returns Y [n_rows, H, D] (and alpha).
+    With bias (fp32 [H*D]) or act, Y = act(aggregate + bias) (cogdl_gat_aggregate_act)."""
     import torch
+    if act not in ACT:
+        raise ValueError(f"act must be one of {sorted(ACT)}")
+    _dev(bias, "bias", torch.float32)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(X, "X")
     _dev(s_dst, "s_dst", torch.float32), _dev(s_src, "s_src", torch.float32)
     _dev(alpha_in, "alpha_in", torch.float32)
@@ -335,10 +349,18 @@ def gat_aggregate(rowptr, col, s_dst, s_src, X, negative_slope: float = 0.2, alp
     if return_alpha and alpha_out is None:
         alpha_out = torch.empty((nnz, H), dtype=torch.float32, device=X.device)
     _dev(alpha_out, "alpha_out", torch.float32)
-    _check(lib().cogdl_gat_aggregate(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(s_dst),
-                                     _ptr(s_src), float(negative_slope), _ptr(alpha_in), _ptr(X),
-                                     _dtype_code(X), _ptr(out), _dtype_code(out), _ptr(alpha_out),
-                                     _plan_handle(plan), _stream()), "cogdl_gat_aggregate")
+    if bias is None and act == "none":
+        _check(lib().cogdl_gat_aggregate(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D,
+                                         _ptr(s_dst), _ptr(s_src), float(negative_slope),
+                                         _ptr(alpha_in), _ptr(X), _dtype_code(X), _ptr(out),
+                                         _dtype_code(out), _ptr(alpha_out), _plan_handle(plan),
+                                         _stream()), "cogdl_gat_aggregate")
+    else:
+        _check(lib().cogdl_gat_aggregate_act(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D,
+                                             _ptr(s_dst), _ptr(s_src), float(negative_slope),
+                                             _ptr(alpha_in), _ptr(X), _dtype_code(X), _ptr(out),
+                                             _dtype_code(out), _ptr(alpha_out), _ptr(bias), ACT[act],
+                                             _plan_handle(plan), _stream()), "cogdl_gat_aggregate_act")
     return (out, alpha_out) if return_alpha else out
 
 
@@ -396,3 +418,62 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
         _ptr(o["dscore"]), _ptr(o["ds_dst"]), _ptr(o["ds_src"]), _plan_handle(plan),
         _plan_handle(plan_t), _stream()), "cogdl_gat_backward")
     return o
+
+
+def linear(X, W, bias=None, act: str = "none", out_dtype=None, out=None):
+    """Y = act(X W^T + bias) on the matrix cores.  X [n, k] and W [m, k] (a layer's out x in
+    weights) both bf16 or both fp16; bias fp32 [m] or None."""
+    import torch
+    _dev(X, "X"), _dev(W, "W"), _dev(bias, "bias", torch.float32)
+    if act not in ACT:
+        raise ValueError(f"act must be one of {sorted(ACT)}")
+    if X.dim() != 2 or W.dim() != 2 or X.shape[1] != W.shape[1] or X.dtype != W.dtype:
+        raise CogdlError("X must be [n, k] and W [m, k] of the same dtype")
+    n, k = X.shape
+    m = W.shape[0]
+    if out is None:
+        out = torch.empty((n, m), dtype=out_dtype or X.dtype, device=X.device)
+    _dev(out, "out")
+    _check(lib().cogdl_linear(n, k, m, _ptr(X), _ptr(W), _dtype_code(X), _ptr(bias), ACT[act],
+                              _ptr(out), _dtype_code(out), _stream()), "cogdl_linear")
+    return out
+
+
+def head_scores(Z, a_src, a_dst):
+    """s_src[i, h] = <Z[i, h, :], a_src[h]>, s_dst likewise; Z [n, H, D], a_* fp32 [H, D]."""
+    import torch
+    _dev(Z, "Z"), _dev(a_src, "a_src", torch.float32), _dev(a_dst, "a_dst", torch.float32)
+    n, H, D = Z.shape
+    s_src = torch.empty((n, H), dtype=torch.float32, device=Z.device)
+    s_dst = torch.empty((n, H), dtype=torch.float32, device=Z.device)
+    _check(lib().cogdl_head_scores(n, H, D, _ptr(Z), _dtype_code(Z), _ptr(a_src), _ptr(a_dst),
+                                   _ptr(s_src), _ptr(s_dst), _stream()), "cogdl_head_scores")
+    return s_src, s_dst
+
+
+def gcn_forward(rowptr, col, val, X, params, plan: Plan | None = None):
+    """2-layer GCN inference: H1 = relu(A (X W1^T) + b1), Y = A (H1 W2^T) + b2, every step a
+    library kernel (dense layers on the matrix cores, aggregations with the bias and
+    activation in their epilogue).  params: dict of W1 [hid, in], b1 [hid], W2 [out, hid],
+    b2 [out]; activations stay in X's dtype."""
+    Z1 = linear(X, params["W1"])
+    H1 = gspmm(rowptr, col, val, Z1, "sum", plan=plan, bias=params["b1"], act="relu")
+    Z2 = linear(H1, params["W2"])
+    return gspmm(rowptr, col, val, Z2, "sum", plan=plan, bias=params["b2"], act="none")
+
+
+def gat_forward(rowptr, col, X, params, negative_slope: float = 0.2, plan: Plan | None = None):
+    """2-layer GAT inference: layer 1 with H heads of D (concatenated, ELU), layer 2 with one
+    head of C outputs.  params: W1 [H*D, in], a_src1 / a_dst1 [H, D], b1 [H*D], W2 [C, H*D],
+    a_src2 / a_dst2 [1, C], b2 [C]."""
+    H, D = params["a_src1"].shape
+    C = params["W2"].shape[0]
+    n = X.shape[0]
+    Z1 = linear(X, params["W1"]).view(n, H, D)
+    s_src, s_dst = head_scores(Z1, params["a_src1"], params["a_dst1"])
+    H1 = gat_aggregate(rowptr, col, s_dst, s_src, Z1, negative_slope, plan=plan, bias=params["b1"],
+                       act="elu")
+    Z2 = linear(H1.view(n, H * D), params["W2"]).view(n, 1, C)
+    s_src2, s_dst2 = head_scores(Z2, params["a_src2"], params["a_dst2"])
+    return gat_aggregate(rowptr, col, s_dst2, s_src2, Z2, negative_slope, plan=plan,
+                         bias=params["b2"]).view(n, C)

@@ -226,6 +226,21 @@ struct RowGather {
         }
     }
 
+    // The 16 raw bytes of elements [idx, idx + VEC) of a 16-byte vector
+    // (packed pairs for 16-bit formats); zeros when !ok.
+    __device__ __forceinline__ uint4 load_raw16(int64_t idx, bool ok) const
+    {
+        static_assert(VecBytes<TX, VEC>::value == 16, "16-byte vectors only");
+        if constexpr (BUF) {
+            const uint32_t off = ok ? (uint32_t)idx * (uint32_t)sizeof(TX) : oob;
+            const auto w = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)off, 0, 0);
+            return make_uint4(w[0], w[1], w[2], w[3]);
+        } else {
+            const uint4 v = *reinterpret_cast<const uint4 *>(base + (ok ? idx : 0));
+            return ok ? v : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+
   private:
     __device__ __forceinline__ static float widen1(uint32_t h)
     {
@@ -251,6 +266,22 @@ struct RowGather {
         }
     }
 };
+
+// c + a.lo * b.lo + a.hi * b.hi for two packed 16-bit pairs (the gfx950 dot2
+// instructions, fp32 accumulation).
+template <typename T>
+__device__ __forceinline__ float dot2_acc(uint32_t a, uint32_t b, float c)
+{
+    if constexpr (Fmt<T>::code == COGDL_BF16) {
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                               __builtin_bit_cast(bf16x2_t, b), c, false);
+    } else {
+        typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+        return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, a), __builtin_bit_cast(f16x2_t, b),
+                                      c, false);
+    }
+}
 
 // ------------------------------------------------------------ lane exchange
 
@@ -284,5 +315,29 @@ __device__ __forceinline__ void softmax_merge(float &m, float &z, float m2, floa
 }
 
 __device__ __forceinline__ float leaky_relu(float t, float slope) { return t > 0.f ? t : slope * t; }
+
+// The epilogue activations of the layer entry points (cogdl_act codes).
+__device__ __forceinline__ float apply_act(float v, int act)
+{
+    if (act == COGDL_ACT_RELU) return v > 0.f ? v : 0.f;
+    if (act == COGDL_ACT_ELU) return v > 0.f ? v : expm1f(v);
+    return v;
+}
+
+// v[e] = act(v[e] + bias[f + e]) over VEC features starting at f; nothing to
+// do for a plain aggregation (no bias, no activation).
+template <int VEC>
+__device__ __forceinline__ void epilogue(float (&v)[VEC], const float *__restrict__ bias, int act,
+                                         int64_t f)
+{
+    if (bias) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[e] += bias[f + e];
+    }
+    if (act != COGDL_ACT_NONE) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[e] = apply_act(v[e], act);
+    }
+}
 
 }  // namespace cogdl

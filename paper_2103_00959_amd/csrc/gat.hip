@@ -289,6 +289,7 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
                                                        const float *__restrict__ gstats,
                                                        int sstride, int H, int D,
                                                        float *__restrict__ rstats,
+                                                       const float *__restrict__ bias, int act_code,
                                                        TY *__restrict__ Y)
 {
     constexpr int kW = kBlock / kWave;
@@ -352,6 +353,7 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
                     for (int i = 1; i < kW; ++i) t += red[i][lane * VEC + e];
                     v[e] = t * rZ;
                 }
+                epilogue<VEC>(v, bias, act_code, f);
                 store_out<TY, VEC>(Y, row * W + f, v);
             }
             __syncthreads();
@@ -454,6 +456,20 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                  void *Y, cogdl_dtype y_dtype, float *alpha_out,
                                  const cogdl_plan *plan, hipStream_t stream)
 {
+    return cogdl_gat_aggregate_act(n_rows, n_cols, nnz, rowptr, col, H, D, s_dst, s_src,
+                                   negative_slope, alpha_in, X, x_dtype, Y, y_dtype, alpha_out,
+                                   nullptr, COGDL_ACT_NONE, plan, stream);
+}
+
+cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                     const int32_t *rowptr, const int32_t *col, int32_t H,
+                                     int32_t D, const float *s_dst, const float *s_src,
+                                     float negative_slope, const float *alpha_in, const void *X,
+                                     cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype,
+                                     float *alpha_out, const float *bias, cogdl_act act,
+                                     const cogdl_plan *plan, hipStream_t stream)
+{
+    if (act < COGDL_ACT_NONE || act > COGDL_ACT_ELU) return COGDL_ERR_INVALID;
     cogdl_status st = check_graph(n_rows, n_cols, nnz, rowptr, col, H);
     if (st != COGDL_OK) return st;
     if (D < 1) return COGDL_ERR_INVALID;
@@ -496,6 +512,8 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     a.x_bytes = (uint64_t)n_cols * (uint64_t)W * (uint64_t)dtype_bytes(x_dtype);
     a.Y = Y;
     a.alpha_out = soft ? alpha_out : nullptr;
+    a.bias = bias;
+    a.act = act;
     a.partials = P ? P->partials : nullptr;
     a.pstride = P ? (P->max_feat + 7) / 8 * 8 : 0;
     a.gstats = P ? P->gstats : nullptr;
@@ -531,14 +549,14 @@ cogdl_status cogdl_gat_aggregate(int32_t n_rows, int32_t n_cols, int64_t nnz,
     }
     if (!P) return COGDL_OK;
 
-    if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, false, stream);
+    if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, false, bias, act, stream);
     const int64_t rblocks = P->cap_split < 4096 ? P->cap_split : 4096;
     const unsigned rb = (unsigned)(rblocks < 1 ? 1 : rblocks);
     const bool v4 = D % 4 == 0 && (uintptr_t)Y % (4 * dtype_bytes(y_dtype)) == 0;
 #define COGDL_GAT_REDUCE(TY, V)                                                                  \
     COGDL_LAUNCH("gat_reduce", (k_gat_reduce<TY, V>), rb, kBlock, stream, P->split_rows,         \
                  P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats, \
-                 static_cast<TY *>(Y))
+                 bias, act, static_cast<TY *>(Y))
     if (y_dtype == COGDL_F32) {
         if (v4) COGDL_GAT_REDUCE(float, 4); else COGDL_GAT_REDUCE(float, 1);
     } else if (y_dtype == COGDL_BF16) {

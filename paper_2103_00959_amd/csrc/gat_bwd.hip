@@ -82,6 +82,9 @@ template <typename TX, int VEC, bool BUF, bool DOT>
 __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 {
     constexpr int U = VEC == 1 ? 16 : 8;
+    // 16-bit features stay packed: four dot2 instructions per 16-byte vector
+    // instead of widening both operands to fp32 (half the registers).
+    constexpr bool PACKED = sizeof(TX) == 2 && VEC == 8;
     const int log2S = a.log2S;
     const int S = 1 << log2S;
     const int lane = lane_id();
@@ -112,8 +115,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
         const int64_t un = u + stride;
         const int4 dn = fetch_bwd_unit(a, un, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
-        float p[VEC];
-        if (act) {
+        float p[PACKED ? 1 : VEC];
+        uint4 pw = make_uint4(0u, 0u, 0u, 0u);
+        if constexpr (PACKED) {
+            if (act) pw = *reinterpret_cast<const uint4 *>(P + (int64_t)row * a.W + fe);
+        } else if (act) {
             load_vec<TX, VEC>(P, (int64_t)row * a.W + fe, p);
         } else {
 #pragma unroll
@@ -134,12 +140,14 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                     ok[t] = j + t < n;
                     cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
                 }
-                float xv[U][VEC];
+                float xv[PACKED ? 1 : U][VEC];
+                uint4 xw[PACKED ? U : 1];
                 float al[U], ss[U];
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
                     const bool on = ok[t] && act;
-                    X.load((int64_t)cc[t] * a.W + fe, on, xv[t]);
+                    if constexpr (PACKED) xw[t] = X.load_raw16((int64_t)cc[t] * a.W + fe, on);
+                    else X.load((int64_t)cc[t] * a.W + fe, on, xv[t]);
                     if constexpr (!DOT) {
                         al[t] = a.alpha[on ? (int64_t)(k0 + j + t) * H + h : 0];
                         ss[t] = a.s_src[on ? (int64_t)cc[t] * H + h : 0];
@@ -149,8 +157,15 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
                     float s = 0.f;
+                    if constexpr (PACKED) {
+                        s = dot2_acc<TX>(xw[t].x, pw.x, s);
+                        s = dot2_acc<TX>(xw[t].y, pw.y, s);
+                        s = dot2_acc<TX>(xw[t].z, pw.z, s);
+                        s = dot2_acc<TX>(xw[t].w, pw.w, s);
+                    } else {
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) s = fmaf(p[e], xv[t][e], s);
+                        for (int e = 0; e < VEC; ++e) s = fmaf(p[e], xv[t][e], s);
+                    }
                     pd[t] = s;
                 }
                 // complete the dot products over the head's lanes (every lane of
@@ -602,7 +617,8 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
                      dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock, stream, b);
     }
     if (!Pc) return COGDL_OK;
-    st = sum_reduce_launch("gat_bwd_dx_reduce", *Pc, W, dX, (int)dx_dtype, false, stream);
+    st = sum_reduce_launch("gat_bwd_dx_reduce", *Pc, W, dX, (int)dx_dtype, false, nullptr,
+                           COGDL_ACT_NONE, stream);
     if (st != COGDL_OK) return st;
     COGDL_LAUNCH("gat_bwd_split_src", k_split_head_sums, wave_grid(Pc->cap_split), kBlock, stream,
                  Pc->split_rows, Pc->n_split_dev(), Pc->gstats, g.sstride, 0, H, ds_src);

@@ -35,6 +35,8 @@ struct GatArgs {
     const int32_t *perm;        // BWD: weight of edge k is alpha_in[perm[k]] (CSC of the graph)
     const float *dscore;        // BWD: per-edge, per-head values summed per row (through perm)
     float *ds_out;              // BWD: those sums, n_rows x H (split rows: gstats)
+    const float *bias;          // epilogue: Y = act(aggregate + bias), bias nullable
+    int32_t act;
     int32_t sstride;            // 2 * max_heads
     int32_t slab;
     int32_t log2S;
@@ -253,7 +255,10 @@ __global__ __launch_bounds__(kGatBlock) void k_gat(GatArgs a)
                 float v[VEC];
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) v[e] = acc[c][e] * rz[c];
-                if (act[c]) store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
+                if (act[c]) {
+                    epilogue<VEC>(v, a.bias, a.act, fe[c]);
+                    store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
+                }
             }
             if (soft && a.alpha_out != nullptr) {
                 // alpha of this whole-row unit: lanes as (edge slot, head); the

@@ -68,9 +68,9 @@ const Plan *plan_of(const cogdl_plan *h);
 int resident_blocks(const void *kernel, int block);
 
 // Y[row] = sum of the partial rows of every split row of the plan (F columns),
-// divided by the row's degree when `mean`.
+// divided by the row's degree when `mean`, then act(. + bias) when given.
 cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                               bool mean, hipStream_t s);
+                               bool mean, const float *bias, int act, hipStream_t s);
 
 // Kernel tracing hooks (no-ops unless cogdl_trace_enable was called).
 int trace_begin(const char *name, hipStream_t s);

@@ -36,6 +36,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
                                                         const int32_t *__restrict__ n_split,
                                                         const float *__restrict__ partials,
                                                         int64_t pstride, int64_t F, int mean,
+                                                        const float *__restrict__ bias, int act_code,
                                                         TY *__restrict__ Y)
 {
     constexpr int kW = kBlock / kWave;
@@ -83,6 +84,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
                     for (int i = 1; i < kW; ++i) v[e] += red[i][lane * VEC + e];
                     if (mean) v[e] *= scale;
                 }
+                epilogue<VEC>(v, bias, act_code, f);
                 store_out<TY, VEC>(Y, row * F + f, v);
             }
             __syncthreads();
@@ -101,6 +103,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce_max(const int4 *__restri
                                                             const float *__restrict__ partials,
                                                             const int32_t *__restrict__ parg,
                                                             int64_t pstride, int64_t F,
+                                                            const float *__restrict__ bias, int act_code,
                                                             TY *__restrict__ Y,
                                                             int32_t *__restrict__ arg)
 {
@@ -118,7 +121,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce_max(const int4 *__restri
                 const float v = partials[q];
                 if (bk < 0 || v > best) { best = v; bk = parg[q]; }
             }
-            const float out[1] = {best};
+            float out[1] = {best};
+            epilogue<1>(out, bias, act_code, f);
             store_out<TY, 1>(Y, (int64_t)d.x * F + f, out);
             if (arg) arg[(int64_t)d.x * F + f] = bk;
         }
@@ -127,7 +131,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce_max(const int4 *__restri
 
 template <int VEC>
 cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                             bool mean, hipStream_t s)
+                             bool mean, const float *bias, int act, hipStream_t s)
 {
     const int64_t pstride = (P.max_feat + 7) / 8 * 8;
     int64_t blocks = P.cap_split;
@@ -137,18 +141,18 @@ cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y
     const int mn = mean ? 1 : 0;
     if (ydt == COGDL_F32)
         COGDL_LAUNCH(name, (k_spmm_reduce<float, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, pstride, F, mn, static_cast<float *>(Y));
+                     P.partials, pstride, F, mn, bias, act, static_cast<float *>(Y));
     else if (ydt == COGDL_BF16)
         COGDL_LAUNCH(name, (k_spmm_reduce<bf16_t, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, pstride, F, mn, static_cast<bf16_t *>(Y));
+                     P.partials, pstride, F, mn, bias, act, static_cast<bf16_t *>(Y));
     else
         COGDL_LAUNCH(name, (k_spmm_reduce<f16_t, VEC>), b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, pstride, F, mn, static_cast<f16_t *>(Y));
+                     P.partials, pstride, F, mn, bias, act, static_cast<f16_t *>(Y));
     return COGDL_OK;
 }
 
 cogdl_status max_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                               int32_t *arg, hipStream_t s)
+                               const float *bias, int act, int32_t *arg, hipStream_t s)
 {
     const int64_t pstride = (P.max_feat + 7) / 8 * 8;
     constexpr int wpb = kBlock / kWave;
@@ -158,13 +162,13 @@ cogdl_status max_reduce_launch(const char *name, const Plan &P, int64_t F, void 
     const unsigned b = (unsigned)blocks;
     if (ydt == COGDL_F32)
         COGDL_LAUNCH(name, k_spmm_reduce_max<float>, b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, P.parg, pstride, F, static_cast<float *>(Y), arg);
+                     P.partials, P.parg, pstride, F, bias, act, static_cast<float *>(Y), arg);
     else if (ydt == COGDL_BF16)
         COGDL_LAUNCH(name, k_spmm_reduce_max<bf16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, P.parg, pstride, F, static_cast<bf16_t *>(Y), arg);
+                     P.partials, P.parg, pstride, F, bias, act, static_cast<bf16_t *>(Y), arg);
     else
         COGDL_LAUNCH(name, k_spmm_reduce_max<f16_t>, b, kBlock, s, P.split_rows, P.n_split_dev(),
-                     P.partials, P.parg, pstride, F, static_cast<f16_t *>(Y), arg);
+                     P.partials, P.parg, pstride, F, bias, act, static_cast<f16_t *>(Y), arg);
     return COGDL_OK;
 }
 
@@ -173,12 +177,12 @@ cogdl_status max_reduce_launch(const char *name, const Plan &P, int64_t F, void 
 // Four features per lane when the rows allow 16-byte partial loads and
 // aligned output stores, one otherwise.
 cogdl_status sum_reduce_launch(const char *name, const Plan &P, int64_t F, void *Y, int ydt,
-                               bool mean, hipStream_t s)
+                               bool mean, const float *bias, int act, hipStream_t s)
 {
     const int ybytes = dtype_bytes(ydt);
     if (F % 4 == 0 && (uintptr_t)Y % (4 * ybytes) == 0)
-        return reduce_launch_v<4>(name, P, F, Y, ydt, mean, s);
-    return reduce_launch_v<1>(name, P, F, Y, ydt, mean, s);
+        return reduce_launch_v<4>(name, P, F, Y, ydt, mean, bias, act, s);
+    return reduce_launch_v<1>(name, P, F, Y, ydt, mean, bias, act, s);
 }
 
 namespace {
@@ -191,13 +195,14 @@ struct LaunchNames {
 // an in_rows x F input through (ptr, idx, w), combined by `reduce`.
 cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const int32_t *ptr,
                          const int32_t *idx, const float *w, int32_t F, const void *X, int xdt,
-                         void *Y, int ydt, int reduce, int compute, int32_t *arg,
-                         const cogdl_plan *plan_h, hipStream_t s, LaunchNames names)
+                         void *Y, int ydt, int reduce, int compute, const float *bias, int act,
+                         int32_t *arg, const cogdl_plan *plan_h, hipStream_t s, LaunchNames names)
 {
     if (out_rows < 0 || in_rows < 0 || nnz < 0 || F < 0) return COGDL_ERR_INVALID;
     if (reduce != COGDL_REDUCE_SUM && reduce != COGDL_REDUCE_MEAN && reduce != COGDL_REDUCE_MAX)
         return COGDL_ERR_INVALID;
     if (compute < COGDL_COMPUTE_MUL || compute > COGDL_COMPUTE_COPY) return COGDL_ERR_INVALID;
+    if (act < COGDL_ACT_NONE || act > COGDL_ACT_ELU) return COGDL_ERR_INVALID;
     if (!dtype_ok(xdt) || !dtype_ok(ydt)) return COGDL_ERR_DTYPE;
     const bool maxr = reduce == COGDL_REDUCE_MAX;
     if (maxr && ydt != COGDL_F32 && ydt != xdt) return COGDL_ERR_DTYPE;
@@ -233,6 +238,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     a.log2S = m.log2S;
     a.mean = reduce == COGDL_REDUCE_MEAN ? 1 : 0;
     a.bsign = compute == COGDL_COMPUTE_SUB ? -1.f : 1.f;
+    a.bias = bias;
+    a.act = act;
     const bool addop = compute == COGDL_COMPUTE_ADD || compute == COGDL_COMPUTE_SUB;
     const bool buf = a.x_bytes <= kBufferMaxBytes;
     auto pick = [&](int ch) {
@@ -269,8 +276,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
                      kBlock, s, b);
     }
     if (!P) return COGDL_OK;
-    if (maxr) return max_reduce_launch(names.reduce, *P, F, Y, ydt, a.arg, s);
-    return sum_reduce_launch(names.reduce, *P, F, Y, ydt, a.mean != 0, s);
+    if (maxr) return max_reduce_launch(names.reduce, *P, F, Y, ydt, bias, act, a.arg, s);
+    return sum_reduce_launch(names.reduce, *P, F, Y, ydt, a.mean != 0, bias, act, s);
 }
 
 }  // namespace
@@ -284,19 +291,20 @@ cogdl_status cogdl_spmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         hipStream_t stream)
 {
     return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
-                              (int)y_dtype, COGDL_REDUCE_SUM, COGDL_COMPUTE_MUL, nullptr, plan,
-                              stream, {"spmm", "spmm_tiny", "spmm_reduce"});
+                              (int)y_dtype, COGDL_REDUCE_SUM, COGDL_COMPUTE_MUL, nullptr,
+                              COGDL_ACT_NONE, nullptr, plan, stream,
+                              {"spmm", "spmm_tiny", "spmm_reduce"});
 }
 
 cogdl_status cogdl_gspmm(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
                          const int32_t *col, const float *val, int32_t F, const void *X,
                          cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype, cogdl_reduce reduce,
-                         cogdl_compute compute, int32_t *arg, const cogdl_plan *plan,
-                         hipStream_t stream)
+                         cogdl_compute compute, const float *bias, cogdl_act act, int32_t *arg,
+                         const cogdl_plan *plan, hipStream_t stream)
 {
     return cogdl::spmm_common(n_rows, n_cols, nnz, rowptr, col, val, F, X, (int)x_dtype, Y,
-                              (int)y_dtype, (int)reduce, (int)compute, arg, plan, stream,
-                              {"gspmm", "gspmm_tiny", "gspmm_reduce"});
+                              (int)y_dtype, (int)reduce, (int)compute, bias, (int)act, arg, plan,
+                              stream, {"gspmm", "gspmm_tiny", "gspmm_reduce"});
 }
 
 cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *colptr,
@@ -306,8 +314,9 @@ cogdl_status cogdl_spmm_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int
 {
     // A^T has n_cols rows, each gathering rows of the n_rows x F input G.
     return cogdl::spmm_common(n_cols, n_rows, nnz, colptr, row_t, val_t, F, G, (int)g_dtype, dX,
-                              (int)dx_dtype, COGDL_REDUCE_SUM, COGDL_COMPUTE_MUL, nullptr, plan_t,
-                              stream, {"spmm_t", "spmm_t_tiny", "spmm_t_reduce"});
+                              (int)dx_dtype, COGDL_REDUCE_SUM, COGDL_COMPUTE_MUL, nullptr,
+                              COGDL_ACT_NONE, nullptr, plan_t, stream,
+                              {"spmm_t", "spmm_t_tiny", "spmm_t_reduce"});
 }
 
 }  // extern "C"

@@ -31,6 +31,8 @@ struct SpmmArgs {
     int32_t log2S;
     int32_t mean;               // sum / mean: divide whole rows by their degree
     float bsign;                // ADDOP: message x + bsign * val (+1 add, -1 subtract)
+    const float *bias;          // epilogue: Y = act(reduced + bias), bias nullable
+    int32_t act;
 };
 
 // Descriptor {row, first edge, end edge, partial slot} of unit u (an empty
@@ -197,6 +199,7 @@ __global__ __launch_bounds__(kSpmmBlock) void k_spmm(SpmmArgs a)
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 if (!act[c]) continue;
+                epilogue<VEC>(acc[c], a.bias, a.act, fe[c]);
                 store_out<TY, VEC>(Y, (int64_t)row * a.F + fe[c], acc[c]);
                 if constexpr (MAXR) {
                     if (a.arg) store_ids<VEC>(a.arg, (int64_t)row * a.F + fe[c], am[c]);

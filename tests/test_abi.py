@@ -73,9 +73,11 @@ def test_spmm_validation(L):
 
 
 def test_gspmm_validation(L):
-    def G(*a):
+    def G(*a, act=0):
         # (n_rows, n_cols, nnz, rowptr, col, val, F, X, x_dt, Y, y_dt, reduce, compute)
-        return L.cogdl_gspmm(*a, None, None, None)
+        return L.cogdl_gspmm(*a, None, act, None, None, None)
+    # activation codes outside none / relu / elu
+    assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 0, 0, act=3) == INVALID
     # reduce codes outside sum / mean / max, compute codes outside mul / add / sub / copy
     assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, 3, 0) == INVALID
     assert G(2, 2, 3, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, -1, 0) == INVALID
@@ -195,3 +197,24 @@ def test_gat_backward_validation(L):
     assert B(2, 2, 3, ds_src=None) == INVALID
     assert B(2, 2, 1 << 31) == TOO_LARGE
     assert B(-1, 2, 0) == INVALID
+
+
+def test_linear_and_head_scores_validation(L):
+    lin = L.cogdl_linear
+    # n, k, m, X, W, dtype, bias, act, Y, y_dtype, stream
+    assert lin(-1, 4, 4, FAKE, FAKE, 1, None, 0, FAKE, 1, None) == INVALID
+    assert lin(8, 4, 4, FAKE, FAKE, 0, None, 0, FAKE, 1, None) == DTYPE     # fp32 operands
+    assert lin(8, 4, 4, FAKE, FAKE, 1, None, 0, FAKE, 7, None) == DTYPE
+    assert lin(8, 4, 4, FAKE, FAKE, 1, None, 5, FAKE, 1, None) == INVALID
+    assert lin(8, 4, 4, None, FAKE, 1, None, 0, FAKE, 1, None) == INVALID
+    assert lin(8, 4, 4, FAKE, None, 1, None, 0, FAKE, 1, None) == INVALID
+    assert lin(8, 4, 4, FAKE, FAKE, 1, None, 0, None, 1, None) == INVALID
+    assert lin(0, 4, 4, None, FAKE, 1, None, 0, None, 1, None) == OK
+    hs = L.cogdl_head_scores
+    # n, H, D, Z, z_dtype, a_src, a_dst, s_src, s_dst, stream
+    assert hs(4, 0, 8, FAKE, 1, FAKE, FAKE, FAKE, FAKE, None) == INVALID
+    assert hs(4, 2, 0, FAKE, 1, FAKE, FAKE, FAKE, FAKE, None) == INVALID
+    assert hs(4, 2, 8, FAKE, 9, FAKE, FAKE, FAKE, FAKE, None) == DTYPE
+    assert hs(4, 2, 8, FAKE, 1, None, FAKE, FAKE, FAKE, None) == INVALID
+    assert hs(4, 2, 8, None, 1, FAKE, FAKE, FAKE, FAKE, None) == INVALID
+    assert hs(4, 2, 8, FAKE, 1, None, None, None, None, None) == OK

@@ -192,3 +192,50 @@ def test_skewed_mixed_precision_sampled(cg):
         del c_ref_cols
     finally:
         plan_t.close()
+
+
+@pytest.mark.timeout(900)
+def test_gat_backward_skewed_sampled(cg):
+    """2.4M nodes, 122.4M nonzeros with hubs, H = 4 x D = 64 bf16: the GAT
+    backward in the benchmark's launch configuration, compared on sampled rows
+    (attention and score gradients, ds_dst) and sampled columns (ds_src, dX),
+    the largest in-degree columns included."""
+    import torch
+    g = synth.config_graph(5, verbose=True)
+    N, E = g.n_rows, g.nnz
+    H, D = 4, 64
+    say(f"GAT backward skewed n={N} nnz={E}")
+    rp, cl = dev(g.rowptr), dev(g.col)
+    rng = np.random.default_rng(3105)
+    sd = rng.standard_normal((N, H), dtype=np.float32)
+    ss = rng.standard_normal((N, H), dtype=np.float32)
+    alpha = rng.random((E, H), dtype=np.float32)
+    xh, xc, xd = features((N, H, D), 2205, "bf16")
+    gh, gc, gd = features((N, H, D), 4105, "bf16")
+    colptr, row_t, _, perm = cg.csr_to_csc(rp, cl, None, N)
+    plan = cg.Plan(rp, E, max_feat=H * D, max_heads=H)
+    plan_t = cg.Plan(colptr, E, max_feat=H * D, max_heads=H)
+    try:
+        out = cg.gat_backward(rp, cl, colptr, row_t, perm, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
+                              plan=plan, plan_t=plan_t)
+        torch.cuda.synchronize()
+    finally:
+        plan.close()
+        plan_t.close()
+    rows = _sample_rows(g)
+    cdeg = np.diff(colptr.cpu().numpy())
+    cols = np.unique(np.concatenate([np.argsort(-cdeg, kind="stable")[:12],
+                                     np.random.default_rng(8).choice(N, 1500, replace=False)])).astype(np.int32)
+    ref = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, xh.reshape(N, H * D), gh.reshape(N, H * D),
+                              H, D, slope=0.2, x_dtype=xc, dy_dtype=gc, rows=rows, cols=cols)
+    e_idx = torch.from_numpy(_edges_of(g, rows)).long().cuda()
+    r_idx = torch.from_numpy(rows).long().cuda()
+    c_idx = torch.from_numpy(cols).long().cuda()
+    for k, got in (("dalpha", out["dalpha"][e_idx]), ("dscore", out["dscore"][e_idx]),
+                   ("ds_dst", out["ds_dst"][r_idx]), ("ds_src", out["ds_src"][c_idx])):
+        err = scaled_error(got, ref[k], ref[k + "_abs"])
+        say(f"GAT backward {k} sampled error {err:.3g}")
+        assert err <= TOL_F32, k
+    err = scaled_error(out["dX"].reshape(N, H * D)[c_idx], ref["dX"], ref["dX_abs"])
+    say(f"GAT backward dX sampled error {err:.3g}")
+    assert err <= TOL_16
