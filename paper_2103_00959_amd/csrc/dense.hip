@@ -7,10 +7,11 @@
 // v_mfma_f32_32x32x16_{bf16,f16} (A = 32 rows x 16 k of X, B = 16 k x 32
 // columns of W^T), fp32 accumulators in registers, and the bias and the
 // activation are applied before the single store.  Operand fragments are read
-// straight from memory (8 consecutive 16-bit values per lane, one 16-byte load
-// when the width k is a multiple of 8): the layers are tall and skinny (k, m at
-// most a few hundred, n in the millions), so X is streamed once per column
-// block and W stays in the caches.
+// straight from memory (8 consecutive 16-bit values per lane, one 16-byte load,
+// unaligned when the width k is even but not a multiple of 8, element loads
+// for the partial last k-step): the layers are tall and skinny (k, m at most a
+// few hundred, n in the millions), so X is streamed once per column block and
+// W stays in the caches.
 //
 // cogdl_head_scores: a wavefront per node, lanes over the features of one
 // head, a butterfly for each head's two dot products.
@@ -40,25 +41,33 @@ __device__ __forceinline__ f32x16 mfma_32x32x16(uint4 a, uint4 b, f32x16 c)
                                                       __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Elements [i, i + 8) of a row of width k (zero past the end of the row or
-// when !ok).  VEC16: k is a multiple of 8 and the rows are 16-byte aligned.
-template <typename T, bool VEC16>
-__device__ __forceinline__ uint4 load8(const T *__restrict__ p, int64_t row_base, int kk, int k,
-                                       bool ok)
+typedef uint4 uint4_a4 __attribute__((aligned(4)));
+
+// Elements [i, i + 8) of a row, all inside the row, as one 16-byte load (zeros
+// when !ok).  ALIGN16: the address is 16-byte aligned; else only 4-byte
+// aligned (gfx950 serves unaligned vector loads).
+template <typename T, bool ALIGN16>
+__device__ __forceinline__ uint4 load8_full(const T *__restrict__ p, int64_t i, bool ok)
 {
-    if constexpr (VEC16) {
-        if (!ok || kk >= k) return make_uint4(0u, 0u, 0u, 0u);
-        return *reinterpret_cast<const uint4 *>(p + row_base + kk);
-    } else {
-        uint32_t w[4];
+    if (!ok) return make_uint4(0u, 0u, 0u, 0u);
+    if constexpr (ALIGN16) return *reinterpret_cast<const uint4 *>(p + i);
+    else return *reinterpret_cast<const uint4_a4 *>(p + i);
+}
+
+// Elements [kk, kk + 8) of the row at row_base, zero past its width k or when
+// !ok (element loads: the last, partial k-step of a row).
+template <typename T>
+__device__ __forceinline__ uint4 load8_tail(const T *__restrict__ p, int64_t row_base, int kk, int k,
+                                            bool ok)
+{
+    uint32_t w[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint32_t lo = (ok && kk + 2 * j < k) ? p[row_base + kk + 2 * j].bits : 0u;
-            const uint32_t hi = (ok && kk + 2 * j + 1 < k) ? p[row_base + kk + 2 * j + 1].bits : 0u;
-            w[j] = lo | (hi << 16);
-        }
-        return make_uint4(w[0], w[1], w[2], w[3]);
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = (ok && kk + 2 * j < k) ? p[row_base + kk + 2 * j].bits : 0u;
+        const uint32_t hi = (ok && kk + 2 * j + 1 < k) ? p[row_base + kk + 2 * j + 1].bits : 0u;
+        w[j] = lo | (hi << 16);
     }
+    return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 struct LinearArgs {
@@ -72,7 +81,10 @@ struct LinearArgs {
     void *Y;            // n x m
 };
 
-template <typename T, typename TY, int NT, bool VEC16>
+// MODE 0: rows 16-byte aligned (k % 8 == 0); 1: rows 4-byte aligned (k even);
+// 2: element loads only.  Full 16-k steps use one 16-byte load per operand
+// fragment in modes 0 and 1; the partial last step (and mode 2) load elements.
+template <typename T, typename TY, int NT, int MODE>
 __global__ __launch_bounds__(kBlock) void k_linear(LinearArgs a)
 {
     const int lane = lane_id();
@@ -90,13 +102,24 @@ __global__ __launch_bounds__(kBlock) void k_linear(LinearArgs a)
     for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
-    for (int k0 = 0; k0 < a.k; k0 += 16) {
+    const int k_full = MODE == 2 ? 0 : a.k / 16 * 16;
+    for (int k0 = 0; k0 < k_full; k0 += 16) {
         const int kk = k0 + kq;
-        const uint4 af = load8<T, VEC16>(X, xr * a.k, kk, a.k, x_ok);
+        const uint4 af = load8_full<T, MODE == 0>(X, xr * a.k + kk, x_ok);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const int c = c0 + 32 * t + i;
-            const uint4 bf = load8<T, VEC16>(W, (int64_t)c * a.k, kk, a.k, c < a.m);
+            const uint4 bf = load8_full<T, MODE == 0>(W, (int64_t)c * a.k + kk, c < a.m);
+            acc[t] = mfma_32x32x16<T>(af, bf, acc[t]);
+        }
+    }
+    for (int k0 = k_full; k0 < a.k; k0 += 16) {
+        const int kk = k0 + kq;
+        const uint4 af = load8_tail<T>(X, xr * a.k, kk, a.k, x_ok);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int c = c0 + 32 * t + i;
+            const uint4 bf = load8_tail<T>(W, (int64_t)c * a.k, kk, a.k, c < a.m);
             acc[t] = mfma_32x32x16<T>(af, bf, acc[t]);
         }
     }
@@ -156,17 +179,19 @@ __global__ __launch_bounds__(kBlock) void k_head_scores(int64_t n, int H, int D,
 using LinearKernel = void (*)(LinearArgs);
 
 template <typename T, typename TY>
-LinearKernel pick_linear_v(bool vec16)
+LinearKernel pick_linear_v(int mode)
 {
-    return vec16 ? k_linear<T, TY, 4, true> : k_linear<T, TY, 4, false>;
+    if (mode == 0) return k_linear<T, TY, 4, 0>;
+    if (mode == 1) return k_linear<T, TY, 4, 1>;
+    return k_linear<T, TY, 4, 2>;
 }
 
 template <typename T>
-LinearKernel pick_linear_y(int ydt, bool vec16)
+LinearKernel pick_linear_y(int ydt, int mode)
 {
-    if (ydt == COGDL_F32) return pick_linear_v<T, float>(vec16);
-    if (ydt == COGDL_BF16) return pick_linear_v<T, bf16_t>(vec16);
-    return pick_linear_v<T, f16_t>(vec16);
+    if (ydt == COGDL_F32) return pick_linear_v<T, float>(mode);
+    if (ydt == COGDL_BF16) return pick_linear_v<T, bf16_t>(mode);
+    return pick_linear_v<T, f16_t>(mode);
 }
 
 }  // namespace
@@ -191,9 +216,10 @@ cogdl_status cogdl_linear(int64_t n, int32_t k, int32_t m, const void *X, const 
     const int64_t row_blocks = (n + kRowsPerBlock - 1) / kRowsPerBlock;
     if (row_blocks > INT32_MAX) return COGDL_ERR_TOO_LARGE;
     LinearArgs a{n, k, m, X, W, bias, (int32_t)act, Y};
-    const bool vec16 = k % 8 == 0 && (uintptr_t)X % 16 == 0 && (uintptr_t)W % 16 == 0;
-    LinearKernel kern = dtype == COGDL_BF16 ? pick_linear_y<bf16_t>((int)y_dtype, vec16)
-                                            : pick_linear_y<f16_t>((int)y_dtype, vec16);
+    const int mode = (k % 8 == 0 && (uintptr_t)X % 16 == 0 && (uintptr_t)W % 16 == 0) ? 0
+                     : (k % 2 == 0 && (uintptr_t)X % 4 == 0 && (uintptr_t)W % 4 == 0) ? 1 : 2;
+    LinearKernel kern = dtype == COGDL_BF16 ? pick_linear_y<bf16_t>((int)y_dtype, mode)
+                                            : pick_linear_y<f16_t>((int)y_dtype, mode);
     const dim3 grid((unsigned)row_blocks, (unsigned)((m + 127) / 128));
     COGDL_LAUNCH("linear", kern, grid, kBlock, stream, a);
     return COGDL_OK;

@@ -389,3 +389,31 @@ def random_csr(n_rows: int, n_cols: int, rng: np.random.Generator, mean_deg: flo
     col = np.concatenate(cols).astype(np.int32) if cols else np.zeros(0, np.int32)
     val = rng.standard_normal(col.size).astype(np.float32) if values else None
     return Graph(rowptr.astype(np.int32), col, val, n_rows, n_cols)
+
+
+# ------------------------------------------------ 2-layer inference workload
+
+# The end-to-end inference workload (2-layer GCN and GAT, hidden size 128, the
+# GAT with 4 heads) on the Reddit-shaped dense-degree graph of workload 3,
+# with Reddit's feature and class counts (602 inputs, 41 classes).
+INFERENCE = dict(graph=3, F_in=602, hidden=128, classes=41, heads=4, head_dim=32, slope=0.2)
+
+
+def model_params(kind: str, F_in: int, hidden: int, classes: int, heads: int = 1, seed: int = 7000):
+    """Seeded fp32 parameters of a 2-layer model (Glorot-like scales; biases small):
+    GCN: W1 [hidden, F_in], b1, W2 [classes, hidden], b2.
+    GAT: W1 [hidden, F_in] (hidden = heads * head dim), a_src1 / a_dst1 [heads, hidden/heads],
+    b1 [hidden], W2 [classes, hidden], a_src2 / a_dst2 [1, classes], b2 [classes]."""
+    rng = np.random.default_rng(seed)
+    f32 = np.float32
+    p = dict(W1=(rng.standard_normal((hidden, F_in)) / np.sqrt(F_in)).astype(f32),
+             b1=(0.1 * rng.standard_normal(hidden)).astype(f32),
+             W2=(rng.standard_normal((classes, hidden)) / np.sqrt(hidden)).astype(f32),
+             b2=(0.1 * rng.standard_normal(classes)).astype(f32))
+    if kind == "gat":
+        D = hidden // heads
+        p["a_src1"] = (rng.standard_normal((heads, D)) / np.sqrt(D)).astype(f32)
+        p["a_dst1"] = (rng.standard_normal((heads, D)) / np.sqrt(D)).astype(f32)
+        p["a_src2"] = (rng.standard_normal((1, classes)) / np.sqrt(classes)).astype(f32)
+        p["a_dst2"] = (rng.standard_normal((1, classes)) / np.sqrt(classes)).astype(f32)
+    return p

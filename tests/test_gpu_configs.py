@@ -239,3 +239,38 @@ def test_gat_backward_skewed_sampled(cg):
     err = scaled_error(out["dX"].reshape(N, H * D)[c_idx], ref["dX"], ref["dX_abs"])
     say(f"GAT backward dX sampled error {err:.3g}")
     assert err <= TOL_16
+
+
+@pytest.mark.timeout(900)
+def test_inference_reddit_shaped_sampled(cg):
+    """2-layer GCN and GAT inference (hidden 128, 4 heads, 602 inputs, 41 classes) on
+    the Reddit-shaped graph (232,965 nodes, 114.6M nonzeros), bf16 activations:
+    sampled output rows against the oracle models, within the model bound."""
+    import torch
+    spec = synth.INFERENCE
+    g = synth.config_graph(spec["graph"], verbose=True)
+    N = g.n_rows
+    k, hid, C, Hh = spec["F_in"], spec["hidden"], spec["classes"], spec["heads"]
+    rp, cl, vl = dev(g.rowptr), dev(g.col), dev(g.val)
+    xb = synth.f32_to_bf16_bits(synth.normal_f32((N, k), 7003))
+    xd = dev(xb.view(np.int16)).view(torch.bfloat16)
+    rows = _sample_rows(g, n_random=800)
+    idx = torch.from_numpy(rows).long().cuda()
+    plan = cg.Plan(rp, g.nnz, max_feat=hid, max_heads=Hh)
+    try:
+        for kind in ("gcn", "gat"):
+            p = synth.model_params(kind, k, hid, C, Hh, seed=7100 if kind == "gcn" else 7200)
+            host = {n: (synth.f32_to_bf16_bits(v) if n.startswith("W") else v) for n, v in p.items()}
+            devp = {n: (dev(synth.f32_to_bf16_bits(v).view(np.int16)).view(torch.bfloat16)
+                        if n.startswith("W") else dev(v)) for n, v in p.items()}
+            if kind == "gcn":
+                Y = cg.gcn_forward(rp, cl, vl, xd, devp, plan=plan)
+                Yr, E = oracle.gcn_forward(g.rowptr, g.col, g.val, xb, host, rows=rows)
+            else:
+                Y = cg.gat_forward(rp, cl, xd, devp, spec["slope"], plan=plan)
+                Yr, E = oracle.gat_forward(g.rowptr, g.col, xb, host, slope=spec["slope"], rows=rows)
+            err = scaled_error(Y[idx], Yr, E)
+            say(f"{kind} inference sampled error {err:.3g}")
+            assert err <= 3 * 2.0 ** -7 + 1e-3, kind
+    finally:
+        plan.close()
