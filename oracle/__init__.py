@@ -63,6 +63,10 @@ def _load():
     lib.oracle_epilogue.argtypes = [i64, i32, P, i32, P]
     lib.oracle_linear.argtypes = [i64, i32, i32, P, i32, P, i32, P, i32, P, P]
     lib.oracle_head_scores.argtypes = [i64, i32, i32, P, i32, P, P, P, P, P, P]
+    lib.oracle_philox4x32_10.argtypes = [P, P, P]
+    lib.oracle_philox4x32_10.restype = None
+    lib.oracle_act_compress.argtypes = [i64, i32, P, i32, i32, i32, ctypes.c_uint64, P, P]
+    lib.oracle_act_decompress.argtypes = [i64, i32, i32, i32, P, P, P]
     _lib = lib
     return lib
 
@@ -402,3 +406,38 @@ def gat_forward(rowptr, col, X, params, slope=0.2, x_dtype=BF16, act_dtype=BF16,
     EZ2, _ = linear(EH1.astype(np.float32), np.abs(decode(params["W2"], wd)).astype(np.float32))
     return _gat_layer(rowptr, col, round_to(Z2, act_dtype), EZ2, params["a_src2"], params["a_dst2"],
                       1, C, slope, params["b2"], "none", act_dtype, rows=rows)
+
+
+def philox4x32_10(counter, key):
+    """The four 32-bit outputs of Philox4x32-10 for a 4-word counter and a 2-word key."""
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.empty(4, np.uint32)
+    _load().oracle_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def codec_layout(n, F, bits, group):
+    """(groups per row, uint64 code words, fp32 stats) of a compressed n x F array."""
+    ng = (F + group - 1) // group
+    return ng, n * ng * (group // 64) * bits, n * ng * 2
+
+
+def act_compress(A, bits, group, seed, a_dtype=None):
+    """Codes (uint64 bit planes) and stats (fp32 min, step per group) of A [n, F]."""
+    A = np.ascontiguousarray(A)
+    n, F = A.shape
+    _, n_words, n_stats = codec_layout(n, F, bits, group)
+    codes = np.empty(n_words, np.uint64)
+    stats = np.empty(n_stats, np.float32)
+    _check(_load().oracle_act_compress(n, F, _p(A), _x_code(A, a_dtype), bits, group,
+                                       ctypes.c_uint64(seed), _p(codes), _p(stats)), "act_compress")
+    return codes, stats
+
+
+def act_decompress(codes, stats, n, F, bits, group):
+    out = np.empty((n, F), np.float32)
+    _check(_load().oracle_act_decompress(n, F, bits, group, _p(np.ascontiguousarray(codes, np.uint64)),
+                                         _p(np.ascontiguousarray(stats, np.float32)), _p(out)),
+           "act_decompress")
+    return out

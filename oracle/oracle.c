@@ -729,3 +729,110 @@ int oracle_head_scores(int64_t n, int32_t H, int32_t D, const void *Z, int32_t z
         }
     return 0;
 }
+
+/* ------------------------------------- activation compression (next row 4) */
+
+/* Philox4x32-10, the counter-based generator of Salmon, Moraes, Dror and Shaw
+ * ("Parallel random numbers: as easy as 1, 2, 3", SC 2011): ten rounds of two
+ * 32x32 -> 64-bit multiplications (multipliers 0xD2511F53 and 0xCD9E8D57)
+ * whose high halves are xored with the other counter words and the key, the
+ * key advanced by the Weyl constants 0x9E3779B9 and 0xBB67AE85 between
+ * rounds. */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+        c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Uniform in [0, 1) for element e of an activation array: word e mod 4 of
+ * Philox4x32-10 at counter (e / 4 low, e / 4 high, 0, 0) with key (seed low,
+ * seed high), its top 24 bits scaled by 2^-24 (exact in fp32). */
+static float codec_uniform(uint64_t seed, int64_t e)
+{
+    uint32_t ctr[4] = {(uint32_t)((uint64_t)e >> 2), (uint32_t)((uint64_t)e >> 34), 0u, 0u};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t r[4];
+    oracle_philox4x32_10(ctr, key, r);
+    return (float)(r[e & 3] >> 8) * (1.0f / 16777216.0f);
+}
+
+/* Per-group b-bit quantization with stochastic rounding (activation
+ * compression, section 2 and the activation-memory table of the evaluation;
+ * the scheme follows the ActNN line of work the paper builds on):
+ * each row of the n x F array A is cut into groups of G consecutive features
+ * (G a multiple of 64, the last group of a row may be shorter).  For a group
+ * with minimum m and maximum M (fp32), range = M - m, s = (2^b - 1) / range and
+ * r = range / (2^b - 1) (both 0 when range is 0), every element x gets the
+ * code  q = clamp(floor(fma(x - m, s, u)), 0, 2^b - 1)  with u the uniform of
+ * its flat index e = i * F + f, all in fp32 (so the integer decision is taken
+ * in the kernel's precision).  Codes are stored as bit planes: each block of 64
+ * consecutive codes of a group is b uint64 words, word p holding bit p of
+ * code j at bit j (codes past the end of the row are 0).  stats[2g], stats[2g+1]
+ * = (m, r).  Decoding: x' = fma(q, r, m). */
+int oracle_act_compress(int64_t n, int32_t F, const void *A, int32_t a_dtype, int32_t bits,
+                        int32_t G, uint64_t seed, uint64_t *codes, float *stats)
+{
+    if (n < 0 || F < 1 || bits < 1 || bits > 8 || G < 64 || G % 64 != 0) return -1;
+    int32_t ng = (F + G - 1) / G, nb = G / 64;
+    float qmax = (float)((1 << bits) - 1);
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        for (int32_t gi = 0; gi < ng; ++gi) {
+            int64_t g = i * ng + gi;
+            int32_t f0 = gi * G, f1 = f0 + G < F ? f0 + G : F;
+            float m = (float)load_elem(A, a_dtype, i * F + f0), M = m;
+            for (int32_t f = f0; f < f1; ++f) {
+                float x = (float)load_elem(A, a_dtype, i * F + f);
+                if (x < m) m = x;
+                if (x > M) M = x;
+            }
+            float range = M - m;
+            float s = range > 0.0f ? qmax / range : 0.0f;
+            float r = range > 0.0f ? range / qmax : 0.0f;
+            stats[2 * g] = m;
+            stats[2 * g + 1] = r;
+            uint64_t *w = codes + g * (int64_t)nb * bits;
+            for (int64_t t = 0; t < (int64_t)nb * bits; ++t) w[t] = 0;
+            for (int32_t f = f0; f < f1; ++f) {
+                float x = (float)load_elem(A, a_dtype, i * F + f);
+                float u = codec_uniform(seed, i * F + f);
+                float v = floorf(fmaf(x - m, s, u));
+                if (v < 0.0f) v = 0.0f;
+                if (v > qmax) v = qmax;
+                uint32_t q = (uint32_t)v;
+                int32_t j = f - f0, blk = j / 64, bit = j % 64;
+                for (int32_t p = 0; p < bits; ++p)
+                    if ((q >> p) & 1u) w[(int64_t)blk * bits + p] |= (uint64_t)1 << bit;
+            }
+        }
+    return 0;
+}
+
+/* The decoded n x F array (fp32 values; callers round to the output format). */
+int oracle_act_decompress(int64_t n, int32_t F, int32_t bits, int32_t G, const uint64_t *codes,
+                          const float *stats, float *out)
+{
+    if (n < 0 || F < 1 || bits < 1 || bits > 8 || G < 64 || G % 64 != 0) return -1;
+    int32_t ng = (F + G - 1) / G, nb = G / 64;
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        for (int32_t f = 0; f < F; ++f) {
+            int64_t g = i * ng + f / G;
+            int32_t j = f % G, blk = j / 64, bit = j % 64;
+            const uint64_t *w = codes + g * (int64_t)nb * bits + (int64_t)blk * bits;
+            uint32_t q = 0;
+            for (int32_t p = 0; p < bits; ++p) q |= (uint32_t)((w[p] >> bit) & 1u) << p;
+            out[i * F + f] = fmaf((float)q, stats[2 * g + 1], stats[2 * g]);
+        }
+    return 0;
+}

@@ -895,3 +895,68 @@ def test_gat_forward_zero_attention_is_a_mean():
     Z2 = _dec(oracle.round_to(H1 @ _dec(p["W2"]).T, oracle.BF16))
     np.testing.assert_allclose(Y, M @ Z2 + p["b2"], rtol=1e-11, atol=1e-11)
     assert np.all(np.abs(Y) <= E * (1 + 2 ** -6))
+
+
+# ------------------------------------------------------------ activation compression codec
+
+def test_philox_known_answers():
+    kat = json.load(open(os.path.join(GOLDEN, "philox4x32_10_kat.json")))
+    for v in kat["vectors"]:
+        out = oracle.philox4x32_10([int(x, 16) for x in v["counter"]], [int(x, 16) for x in v["key"]])
+        assert [int(x) for x in out] == [int(x, 16) for x in v["out"]]
+
+
+def test_codec_bit_planes_hand_example():
+    # codes j % 4 on an exact grid (m = 0, M = 3, s = r = 1): the uniform never moves them
+    x = (np.arange(64) % 4).astype(np.float32)[None, :]
+    codes, stats = oracle.act_compress(x, 2, 64, seed=123)
+    assert stats.tolist() == [0.0, 1.0]
+    assert codes.tolist() == [0xAAAAAAAAAAAAAAAA, 0xCCCCCCCCCCCCCCCC]
+    assert np.array_equal(oracle.act_decompress(codes, stats, 1, 64, 2, 64), x)
+
+
+def test_codec_exact_grid_and_constant_groups():
+    # 8 bits, values m + j / 16: s = 16 and r = 1/16 exactly, every value recovered
+    x = (np.arange(256, dtype=np.float32) / 16.0 - 3.0)[None, :]
+    codes, stats = oracle.act_compress(x, 8, 256, seed=9)
+    assert np.array_equal(oracle.act_decompress(codes, stats, 1, 256, 8, 256), x)
+    # a constant group: every code 0, decoded exactly
+    c = np.full((3, 128), 1.25, np.float32)
+    codes, stats = oracle.act_compress(c, 3, 64, seed=1)
+    assert not codes.any() and np.array_equal(oracle.act_decompress(codes, stats, 3, 128, 3, 64), c)
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
+def test_codec_error_bound_ragged_rows(bits):
+    """|x' - x| < one step of the group, codes past the end of a ragged row are 0."""
+    rng = np.random.default_rng(60 + bits)
+    n, F, G = 17, 100, 64
+    x = rng.standard_normal((n, F)).astype(np.float32)
+    codes, stats = oracle.act_compress(x, bits, G, seed=77)
+    y = oracle.act_decompress(codes, stats, n, F, bits, G)
+    ng = 2
+    step = stats[1::2].reshape(n, ng)
+    per_elem = np.concatenate([np.repeat(step[:, :1], 64, 1), np.repeat(step[:, 1:], F - 64, 1)], 1)
+    assert np.all(np.abs(y - x) <= per_elem * (1 + 1e-5) + 1e-7)
+    w = codes.reshape(n, ng, 1, bits)
+    assert not np.any(w[:, 1, 0, :] >> np.uint64(36))       # 36 valid codes in the second group
+    mins = stats[0::2].reshape(n, ng)
+    assert np.array_equal(mins[:, 0], x[:, :64].min(1)) and np.array_equal(mins[:, 1], x[:, 64:].min(1))
+
+
+def test_codec_stochastic_rounding_is_unbiased():
+    """The mean of the decoded values over many seeds converges to x (2 bits)."""
+    rng = np.random.default_rng(61)
+    x = rng.standard_normal((1, 64)).astype(np.float32)
+    acc = np.zeros((1, 64))
+    trials = 400
+    for seed in range(trials):
+        codes, stats = oracle.act_compress(x, 2, 64, seed=seed)
+        acc += oracle.act_decompress(codes, stats, 1, 64, 2, 64)
+    step = float(stats[1])
+    # each decode is within one step, so its variance is at most step^2 / 4
+    assert np.max(np.abs(acc / trials - x)) <= 5 * (step / 2) / np.sqrt(trials)
+    # and the seed matters
+    c1, _ = oracle.act_compress(x, 2, 64, seed=1)
+    c2, _ = oracle.act_compress(x, 2, 64, seed=2)
+    assert not np.array_equal(c1, c2)
