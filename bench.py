@@ -440,6 +440,22 @@ def main():
                   + M * H * D * 2 + 4 * M * H)
     b_bwd = b_bwd_rows + b_bwd_cols
 
+    # activation compression of the layer output Y (N x F bf16) at 2, 3, 4 bits, groups of F
+    codec = {}
+    for bits in (2, 3, 4):
+        words, nst = cg.act_codec_size(N, F, bits, F)
+        cbuf = torch.empty(words, dtype=torch.int64, device=dev)
+        sbuf = torch.empty(nst, dtype=torch.float32, device=dev)
+        dbuf = torch.empty((N, F), dtype=torch.bfloat16, device=dev)
+        ms_c = time_op(lambda: cg.act_compress(Y, bits, F, 1234, codes=cbuf, stats=sbuf))
+        ms_d = time_op(lambda: cg.act_decompress(cbuf, sbuf, N, F, bits, F, out=dbuf))
+        b_raw, b_cmp = N * F * 2, words * 8 + nst * 4
+        codec[f"{bits}bit"] = dict(compress_ms=ms_c, decompress_ms=ms_d,
+                                   compress_GBps=(b_raw + b_cmp) / (ms_c * 1e-3) / 1e9,
+                                   decompress_GBps=(b_raw + b_cmp) / (ms_d * 1e-3) / 1e9,
+                                   ratio_vs_fp32=(N * F * 4) / b_cmp, ratio_vs_bf16=b_raw / b_cmp)
+        del cbuf, sbuf, dbuf
+
     ms_mean = time_op(lambda: cg.gspmm(rowptr, col, val, X, "mean", plan=plan, out=Y))
     arg_buf = torch.empty((N, F), dtype=torch.int32, device=dev)
     ms_max = time_op(lambda: cg.gspmm(rowptr, col, val, X, "max", plan=plan, out=Y,
@@ -465,6 +481,7 @@ def main():
                              cols_pass_GBps=b_bwd_cols / ((k_bwd.get("gat_bwd_cols", 0)
                                                            + k_bwd.get("gat_bwd_cols_tiny", 0)) * 1e-3) / 1e9
                              if k_bwd.get("gat_bwd_cols") else None),
+        "act_codec": codec,
         "sddmm_dot": dict(ms=ms_dot, algorithmic_GB=b_dot / 1e9,
                           eff_GBps=b_dot / (ms_dot * 1e-3) / 1e9, edges_per_s=E / (ms_dot * 1e-3)),
         "gspmm_mean": dict(ms=ms_mean, algorithmic_GB=b_mean / 1e9,
@@ -474,8 +491,10 @@ def main():
                                    eff_GBps=b_max / (ms_max * 1e-3) / 1e9,
                                    edges_per_s=E / (ms_max * 1e-3)),
     }
+    codec_txt = ", ".join("%s %.3f/%.3f" % (k, v["compress_ms"], v["decompress_ms"]) for k, v in codec.items())
     log(f"extra: sddmm_edge_softmax {ms_soft:.3f} ms, gat_aggregate+alpha {ms_gat_a:.3f} ms, "
         f"gspmm mean {ms_mean:.3f} ms, max+arg {ms_max:.3f} ms, sddmm_dot {ms_dot:.3f} ms, "
+        f"codec (compress/decompress) {codec_txt} ms, "
         f"gat backward {ms_bwd:.3f} ms "
         f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd.items())})")
 

@@ -296,6 +296,35 @@ cogdl_status cogdl_head_scores(int64_t n, int32_t H, int32_t D, const void *Z,
                                float *s_src, float *s_dst, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Activation compression (the paper's activation-compression training, 2-4
+ * bits in its evaluation): per-group b-bit quantization with stochastic
+ * rounding of an n x F activation array A (fp32 / bf16 / fp16).
+ * Each row is cut into groups of `group` consecutive features (a multiple of
+ * 64, at least 64; the last group of a row may be shorter); bits in [1, 8].
+ * For a group with minimum m and maximum M, s = (2^bits - 1) / (M - m) and the
+ * step r = (M - m) / (2^bits - 1) (both 0 when M == m); feature x with flat
+ * index e = i * F + f gets the code
+ *     q = clamp(floor(fma(x - m, s, u)), 0, 2^bits - 1)        (fp32)
+ * where u in [0, 1) is word e mod 4 of Philox4x32-10 at counter
+ * (e / 4 mod 2^32, e / 2^34, 0, 0) with key (seed mod 2^32, seed / 2^32),
+ * its top 24 bits times 2^-24.  Decoding gives fma(q, r, m), an unbiased
+ * estimate of x within one step r.
+ * Layout: stats[2g], stats[2g+1] = (m, r) for group g = i * groups_per_row + j;
+ * codes: group g owns (group / 64) * bits uint64 words, each block of 64
+ * consecutive features being `bits` bit planes (plane p has bit p of the code
+ * of feature 64 t + l at bit l; features past the end of the row code 0).
+ * cogdl_act_codec_size gives the number of code words and stat floats.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_act_codec_size(int64_t n, int32_t F, int32_t bits, int32_t group,
+                                  int64_t *code_words, int64_t *stat_floats);
+cogdl_status cogdl_act_compress(int64_t n, int32_t F, const void *A, cogdl_dtype a_dtype,
+                                int32_t bits, int32_t group, uint64_t seed, uint64_t *codes,
+                                float *stats, hipStream_t stream);
+cogdl_status cogdl_act_decompress(int64_t n, int32_t F, int32_t bits, int32_t group,
+                                  const uint64_t *codes, const float *stats, void *out,
+                                  cogdl_dtype out_dtype, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Dot-product SDDMM -- section 2.2, T = A (.) (P Q^T), per head: for every
  * edge k = (i, col[k]) and head h
  *     out[k * H + h] = sum_d P[i, h, d] * Q[col[k], h, d]

@@ -69,6 +69,9 @@ def lib():
                                           ctypes.c_int, P, ctypes.c_int, P, P, ctypes.c_int, P, P]
     L.cogdl_linear.argtypes = [i64, i32, i32, P, P, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P]
     L.cogdl_head_scores.argtypes = [i64, i32, i32, P, ctypes.c_int, P, P, P, P, P]
+    L.cogdl_act_codec_size.argtypes = [i64, i32, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.cogdl_act_compress.argtypes = [i64, i32, P, ctypes.c_int, i32, i32, ctypes.c_uint64, P, P, P]
+    L.cogdl_act_decompress.argtypes = [i64, i32, i32, i32, P, P, P, ctypes.c_int, P]
     L.cogdl_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_csr_to_csc_workspace.argtypes = [i32, i32, i64, ctypes.POINTER(sz)]
     L.cogdl_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P, sz, P]
@@ -87,7 +90,8 @@ def lib():
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate",
                  "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act", "cogdl_linear",
-                 "cogdl_head_scores"):
+                 "cogdl_head_scores", "cogdl_act_codec_size", "cogdl_act_compress",
+                 "cogdl_act_decompress"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -477,3 +481,40 @@ def gat_forward(rowptr, col, X, params, negative_slope: float = 0.2, plan: Plan 
     s_src2, s_dst2 = head_scores(Z2, params["a_src2"], params["a_dst2"])
     return gat_aggregate(rowptr, col, s_dst2, s_src2, Z2, negative_slope, plan=plan,
                          bias=params["b2"]).view(n, C)
+
+
+def act_codec_size(n: int, F: int, bits: int, group: int):
+    """(uint64 code words, fp32 stats) of a compressed n x F activation array."""
+    w, st = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().cogdl_act_codec_size(n, F, bits, group, ctypes.byref(w), ctypes.byref(st)),
+           "cogdl_act_codec_size")
+    return w.value, st.value
+
+
+def act_compress(A, bits: int, group: int, seed: int, codes=None, stats=None):
+    """Per-group `bits`-bit stochastic quantization of A [n, F]: returns (codes int64 view of
+    the uint64 bit planes, stats fp32 [groups, 2] = (min, step))."""
+    import torch
+    _dev(A, "A")
+    n, F = A.shape
+    words, nst = act_codec_size(n, F, bits, group)
+    if codes is None:
+        codes = torch.empty(max(words, 1), dtype=torch.int64, device=A.device)
+    if stats is None:
+        stats = torch.empty(max(nst, 1), dtype=torch.float32, device=A.device)
+    _dev(codes, "codes", torch.int64), _dev(stats, "stats", torch.float32)
+    _check(lib().cogdl_act_compress(n, F, _ptr(A), _dtype_code(A), bits, group,
+                                    ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), _ptr(codes),
+                                    _ptr(stats), _stream()), "cogdl_act_compress")
+    return codes[:words], stats[:nst]
+
+
+def act_decompress(codes, stats, n: int, F: int, bits: int, group: int, out_dtype=None, out=None):
+    import torch
+    _dev(codes, "codes", torch.int64), _dev(stats, "stats", torch.float32)
+    if out is None:
+        out = torch.empty((n, F), dtype=out_dtype or torch.float32, device=codes.device)
+    _dev(out, "out")
+    _check(lib().cogdl_act_decompress(n, F, bits, group, _ptr(codes), _ptr(stats), _ptr(out),
+                                      _dtype_code(out), _stream()), "cogdl_act_decompress")
+    return out

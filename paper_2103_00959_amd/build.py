@@ -19,7 +19,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcogdl_mi355.so")
-SOURCES = ["primitives.hip", "plan.hip", "spmm.hip", "gspmm.hip", "gat.hip", "gat_bwd.hip", "dense.hip", "csc.hip", "trace.hip"]
+SOURCES = ["primitives.hip", "plan.hip", "spmm.hip", "gspmm.hip", "gat.hip", "gat_bwd.hip", "dense.hip", "codec.hip", "csc.hip", "trace.hip"]
 
 ARCH = "gfx950"
 FLAGS = [

@@ -218,3 +218,21 @@ def test_linear_and_head_scores_validation(L):
     assert hs(4, 2, 8, FAKE, 1, None, FAKE, FAKE, FAKE, None) == INVALID
     assert hs(4, 2, 8, None, 1, FAKE, FAKE, FAKE, FAKE, None) == INVALID
     assert hs(4, 2, 8, FAKE, 1, None, None, None, None, None) == OK
+
+
+def test_codec_validation(L):
+    w, s = ctypes.c_int64(), ctypes.c_int64()
+    assert L.cogdl_act_codec_size(10, 100, 3, 64, ctypes.byref(w), ctypes.byref(s)) == OK
+    assert (w.value, s.value) == (10 * 2 * 1 * 3, 10 * 2 * 2)
+    assert L.cogdl_act_codec_size(10, 256, 2, 128, ctypes.byref(w), ctypes.byref(s)) == OK
+    assert (w.value, s.value) == (10 * 2 * 2 * 2, 10 * 2 * 2)
+    for bits, group in ((0, 64), (9, 64), (2, 32), (2, 96 + 1), (2, 0)):
+        assert L.cogdl_act_codec_size(10, 64, bits, group, ctypes.byref(w), ctypes.byref(s)) == INVALID
+    C = L.cogdl_act_compress
+    assert C(4, 64, FAKE, 5, 2, 64, ctypes.c_uint64(1), FAKE, FAKE, None) == DTYPE
+    assert C(4, 0, FAKE, 0, 2, 64, ctypes.c_uint64(1), FAKE, FAKE, None) == INVALID
+    assert C(4, 64, None, 0, 2, 64, ctypes.c_uint64(1), FAKE, FAKE, None) == INVALID
+    assert C(0, 64, None, 0, 2, 64, ctypes.c_uint64(1), None, None, None) == OK
+    D = L.cogdl_act_decompress
+    assert D(4, 64, 2, 64, FAKE, FAKE, FAKE, 3, None) == DTYPE
+    assert D(4, 64, 2, 64, None, FAKE, FAKE, 0, None) == INVALID
