@@ -1,10 +1,10 @@
 // CSR -> CSC transpose of the graph structure, the setup of the backward
 // pass of Eq. 1 (the gradient with respect to the node features is A^T G).
 //
-// A stable LSD radix sort of the edge ids keyed by column (8-bit digits, as
-// many passes as the column count needs) gives perm directly, with each
-// edge's row and value bits carried along as payloads (so nothing is gathered
-// at random afterwards); colptr is read off the sorted keys.  Every step is
+// A stable LSD radix sort of the edge ids keyed by column (digits of at most
+// 6 bits, as many passes as the column count needs) gives perm directly, with
+// each edge's row and value bits carried along as payloads (so nothing is
+// gathered at random afterwards); colptr is read off the sorted keys.  Every step is
 // integer work in a fixed order, so the result is bit-for-bit unique: inside
 // a column the edges keep increasing CSR edge id.
 #include "common.hpp"

@@ -41,7 +41,7 @@ __device__ __forceinline__ f32x16 mfma_32x32x16(uint4 a, uint4 b, f32x16 c)
                                                       __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-typedef uint4 uint4_a4 __attribute__((aligned(4)));
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 
 // Elements [i, i + 8) of a row, all inside the row, as one 16-byte load (zeros
 // when !ok).  ALIGN16: the address is 16-byte aligned; else only 4-byte
@@ -51,7 +51,10 @@ __device__ __forceinline__ uint4 load8_full(const T *__restrict__ p, int64_t i, 
 {
     if (!ok) return make_uint4(0u, 0u, 0u, 0u);
     if constexpr (ALIGN16) return *reinterpret_cast<const uint4 *>(p + i);
-    else return *reinterpret_cast<const uint4_a4 *>(p + i);
+    else {
+        const u32x4_a4 v = *reinterpret_cast<const u32x4_a4 *>(p + i);
+        return make_uint4(v.x, v.y, v.z, v.w);
+    }
 }
 
 // Elements [kk, kk + 8) of the row at row_base, zero past its width k or when

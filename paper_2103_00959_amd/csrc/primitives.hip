@@ -14,9 +14,10 @@ constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanBlock * kScanItems;   // 2048
 
 constexpr int kSortBlock = 256;                      // 4 wavefronts
-constexpr int kSortItems = 16;
-constexpr int kSortTile = kSortBlock * kSortItems;   // 4096
-constexpr int kDigits = 256;                         // 8-bit digits
+constexpr int kSortItems = 12;
+constexpr int kSortTile = kSortBlock * kSortItems;   // 3072
+constexpr int kDigits = 256;                         // digits of at most 8 bits
+constexpr int kMaxDigitBits = 6;                     // widest digit of a pass
 
 __device__ __forceinline__ int wave_inclusive_scan(int x)
 {
@@ -94,29 +95,45 @@ __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v)
         p[i] = v;
 }
 
-// Per-tile histogram of one 8-bit digit, stored digit-major so that an
-// exclusive scan of the whole table yields every (digit, tile) start slot.
+// Per-tile histogram of one digit (bits [shift, shift + dbits) of the key),
+// stored digit-major so that an exclusive scan of the whole table yields every
+// (digit, tile) start slot.  Each wavefront counts into its own LDS copy.
 __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__restrict__ keys, int64_t n,
-                                                           int shift, int n_tiles,
+                                                           int shift, int dbits, int n_tiles,
                                                            int32_t *__restrict__ hist)
 {
-    __shared__ int32_t h[kDigits];
-    h[threadIdx.x] = 0;
+    constexpr int kWaves = kSortBlock / kWave;
+    __shared__ int32_t h[kWaves][kDigits];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) h[w][threadIdx.x] = 0;
     __syncthreads();
+    const int wv = threadIdx.x / kWave;
+    const uint32_t mask = (1u << dbits) - 1u;
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
-#pragma unroll 4
+    uint32_t key[kSortItems];
+#pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
-        int64_t e = base + (int64_t)i * kSortBlock + threadIdx.x;
-        if (e < n) atomicAdd(&h[(keys[e] >> shift) & (kDigits - 1)], 1);
+        const int64_t e = base + (int64_t)i * kSortBlock + threadIdx.x;
+        key[i] = keys[e < n ? e : n - 1];
+    }
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const int64_t e = base + (int64_t)i * kSortBlock + threadIdx.x;
+        if (e < n) atomicAdd(&h[wv][(key[i] >> shift) & mask], 1);
     }
     __syncthreads();
-    hist[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = h[threadIdx.x];
+    if (threadIdx.x < (1 << dbits)) {
+        int c = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) c += h[w][threadIdx.x];
+        hist[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = c;
+    }
 }
 
 // Stable scatter of one tile.  Wavefront w owns the contiguous quarter
-// [w * 1024, (w + 1) * 1024) of the tile and walks it 64 keys at a time; the
+// [w * 768, (w + 1) * 768) of the tile and walks it 64 keys at a time; the
 // rank of a key among equal digits is the number of lower lanes with the same
-// digit (found with eight ballots) plus the running per-wave count.  All
+// digit (found with one ballot per digit bit) plus the running per-wave count.  All
 // arrays of the tile are loaded up front (one memory round trip), then staged
 // in LDS in tile-sorted order two at a time and written out by consecutive
 // threads, so equal digits leave as contiguous runs instead of scattered
@@ -125,7 +142,7 @@ template <int NP>
 __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint32_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, int64_t n, int shift,
-    int n_tiles, const int32_t *__restrict__ offsets, RadixPayload p0, RadixPayload p1)
+    int dbits, int n_tiles, const int32_t *__restrict__ offsets, RadixPayload p0, RadixPayload p1)
 {
     constexpr int kWaves = kSortBlock / kWave;
     __shared__ int32_t wcnt[kWaves][kDigits];   // per-wave counts, then tile-local run starts
@@ -134,6 +151,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     __shared__ uint32_t stage[2][kSortTile];
     __shared__ uint8_t qdig[kSortTile];
     const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
+    const uint32_t dmask = (1u << dbits) - 1u;
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) wcnt[i][tid] = 0;
 
@@ -157,10 +175,11 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const bool valid = base + i * kWave + lane < n;
-        const int d = (int)((key[i] >> shift) & (kDigits - 1));
+        const int d = (int)((key[i] >> shift) & dmask);
         uint64_t peers = __ballot(valid);
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
+        for (int b = 0; b < kMaxDigitBits; ++b) {
+            if (b >= dbits) break;
             const int bit = (d >> b) & 1;
             const uint64_t m = __ballot(bit);
             peers &= bit ? m : ~m;
@@ -180,7 +199,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         int all;
         const int start = block_exclusive_scan(tot, &all);
         dstart[tid] = start;
-        gstart[tid] = offsets[(int64_t)tid * n_tiles + blockIdx.x];
+        gstart[tid] = tid <= (int)dmask ? offsets[(int64_t)tid * n_tiles + blockIdx.x] : 0;
         int run = start;
 #pragma unroll
         for (int i = 0; i < kWaves; ++i) {
@@ -193,7 +212,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         if (local[i] >= 0) {
-            const int d = (int)((key[i] >> shift) & (kDigits - 1));
+            const int d = (int)((key[i] >> shift) & dmask);
             local[i] += wcnt[w][d];
             stage[0][local[i]] = key[i];
             stage[1][local[i]] = val[i];
@@ -296,34 +315,41 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
     size_t hist_bytes = ((size_t)(hist_n + 1 + 64) * 4 + 255) & ~size_t(255);
     void *scan_ws = static_cast<char *>(ws) + hist_bytes;
 
-    int passes = (bits + 7) / 8;
+    // as few passes as digits of at most kMaxDigitBits allow, the bits spread
+    // evenly over them (longer runs per digit than a short last pass gives)
+    int passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
     if (passes < 1) passes = 1;
     const uint32_t *src_k = keys_in;
     const uint32_t *src_v = vals_in;
     RadixPayload a = pay0, b = pay1;
+    int shift = 0;
     for (int p = 0; p < passes; ++p) {
         const bool last = (p == passes - 1);
+        int dbits = (bits - shift + (passes - p) - 1) / (passes - p);
+        if (dbits < 1) dbits = 1;
         uint32_t *dst_k = last ? keys_out : ping_keys + (p & 1) * n;
         uint32_t *dst_v = last ? vals_out : ping_vals + (p & 1) * n;
         RadixPayload pa{a.in, last ? pay0.out : (pay0.ping ? pay0.ping + (p & 1) * n : nullptr), nullptr};
         RadixPayload pb{b.in, last ? pay1.out : (pay1.ping ? pay1.ping + (p & 1) * n : nullptr), nullptr};
-        COGDL_LAUNCH_HIP("radix_hist", k_radix_hist, (unsigned)tiles, kSortBlock, s, src_k, n, 8 * p,
-                         (int)tiles, hist);
-        hipError_t e = exclusive_scan(hist, hist, hist_n, scan_ws, s);
+        const int64_t used = (int64_t)(1 << dbits) * tiles;
+        COGDL_LAUNCH_HIP("radix_hist", k_radix_hist, (unsigned)tiles, kSortBlock, s, src_k, n, shift,
+                         dbits, (int)tiles, hist);
+        hipError_t e = exclusive_scan(hist, hist, used, scan_ws, s);
         if (e != hipSuccess) return e;
         if (np == 0)
             COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<0>, (unsigned)tiles, kSortBlock, s,
-                             src_k, src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist, pa, pb);
+                             src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb);
         else if (np == 1)
             COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<1>, (unsigned)tiles, kSortBlock, s,
-                             src_k, src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist, pa, pb);
+                             src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb);
         else
             COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<2>, (unsigned)tiles, kSortBlock, s,
-                             src_k, src_v, dst_k, dst_v, n, 8 * p, (int)tiles, hist, pa, pb);
+                             src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb);
         src_k = dst_k;
         src_v = dst_v;
         a.in = pa.out;
         b.in = pb.out;
+        shift += dbits;
     }
     return hipSuccess;
 }
