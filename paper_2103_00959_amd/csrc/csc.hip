@@ -110,22 +110,29 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
     uint32_t *ping_k = reinterpret_cast<uint32_t *>(ws + L.ping_k);
     uint32_t *ping_v = reinterpret_cast<uint32_t *>(ws + L.ping_v);
     uint32_t *skeys = reinterpret_cast<uint32_t *>(ws + L.skeys);
-    uint32_t *order = perm ? reinterpret_cast<uint32_t *>(perm)
-                           : reinterpret_cast<uint32_t *>(ws + L.vtmp);
 
     COGDL_LAUNCH("csc_expand_rows", k_expand_rows, grid_for(n_rows, kBlock / kWave), kBlock, stream,
                  rowptr, n_rows, row_of);
     const int bits = bits_for((uint64_t)(n_cols - 1));
-    RadixPayload rows{row_of, reinterpret_cast<uint32_t *>(row_t),
-                      reinterpret_cast<uint32_t *>(ws + L.ping_r)};
     RadixPayload vals;
     if (val) {
         vals.in = reinterpret_cast<const uint32_t *>(val);
         vals.out = reinterpret_cast<uint32_t *>(val_t);
         vals.ping = reinterpret_cast<uint32_t *>(ws + L.ping_w);
     }
-    COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), nullptr, skeys, order,
-                                   nnz, bits, ping_k, ping_v, ws + L.radix, stream, rows, vals));
+    if (perm) {
+        // edge ids as the sorted values, rows and edge values as payloads
+        RadixPayload rows{row_of, reinterpret_cast<uint32_t *>(row_t),
+                          reinterpret_cast<uint32_t *>(ws + L.ping_r)};
+        COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), nullptr, skeys,
+                                       reinterpret_cast<uint32_t *>(perm), nnz, bits, ping_k, ping_v,
+                                       ws + L.radix, stream, rows, vals));
+    } else {
+        // no edge ids wanted: the rows are the sorted values, one array less per pass
+        COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), row_of, skeys,
+                                       reinterpret_cast<uint32_t *>(row_t), nnz, bits, ping_k, ping_v,
+                                       ws + L.radix, stream, vals, RadixPayload{}));
+    }
     COGDL_LAUNCH("csc_colptr", k_colptr, grid_for(nnz, kBlock), kBlock, stream, skeys, nnz, n_cols,
                  colptr);
     return COGDL_OK;

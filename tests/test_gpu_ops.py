@@ -349,6 +349,15 @@ def test_csr_to_csc_bit_exact(cg, kind):
     assert np.array_equal(row_t.cpu().numpy(), r_ref)
     assert np.array_equal(perm.cpu().numpy(), p_ref)
     assert np.array_equal(val_t.cpu().numpy().view(np.uint32), v_ref.view(np.uint32))
+    # without edge ids (one array less through the sort) and without values
+    c2, r2, v2, p2 = cg.csr_to_csc(rp, cl, vl, g.n_cols, with_perm=False)
+    assert p2 is None and np.array_equal(c2.cpu().numpy(), c_ref)
+    assert np.array_equal(r2.cpu().numpy(), r_ref)
+    assert np.array_equal(v2.cpu().numpy().view(np.uint32), v_ref.view(np.uint32))
+    c3, r3, v3, p3 = cg.csr_to_csc(rp, cl, None, g.n_cols, with_perm=False)
+    assert v3 is None and np.array_equal(c3.cpu().numpy(), c_ref) and np.array_equal(r3.cpu().numpy(), r_ref)
+    c4, r4, v4, p4 = cg.csr_to_csc(rp, cl, None, g.n_cols)
+    assert np.array_equal(p4.cpu().numpy(), p_ref) and np.array_equal(r4.cpu().numpy(), r_ref)
 
 
 def test_csr_to_csc_many_columns(cg):
