@@ -119,8 +119,8 @@ def recorded_traffic(workload: str, kernel: str, profiles_dir: str | None = None
         return None
     d = disp[i]
     return dict(bytes=d["fetch_bytes"] + d["write_bytes"], fetch_bytes=d["fetch_bytes"],
-                write_bytes=d["write_bytes"], kernel=spec["name"], dispatch=i, dur_ms=d["dur_ms"],
-                source=os.path.basename(path))
+                write_bytes=d["write_bytes"], l2_hit=d.get("l2_hit"), kernel=spec["name"], dispatch=i,
+                dur_ms=d["dur_ms"], source=os.path.basename(path))
 
 
 def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
