@@ -455,32 +455,62 @@ def head_scores(Z, a_src, a_dst):
     return s_src, s_dst
 
 
+def _padded_output_layer(params, names_rows, names_cols):
+    """The output layer's parameters with the output count padded to a multiple of 8 (zero
+    rows / entries), prepared once per parameter dict: the aggregation then gathers
+    16-byte vectors instead of single 16-bit elements of rows like 41 classes wide.  The
+    padded outputs are exactly zero and are sliced away."""
+    import torch
+    key = "_padded_output_layer"
+    if key not in params:
+        C = params[names_rows[0]].shape[0]
+        C8 = (C + 7) // 8 * 8
+        pad = {}
+        for n_ in names_rows:                     # [C, ...] -> [C8, ...]
+            t = params[n_]
+            z = torch.zeros((C8,) + tuple(t.shape[1:]), dtype=t.dtype, device=t.device)
+            z[:C] = t
+            pad[n_] = z
+        for n_ in names_cols:                     # [1, C] -> [1, C8]
+            t = params[n_]
+            z = torch.zeros((t.shape[0], C8), dtype=t.dtype, device=t.device)
+            z[:, :C] = t
+            pad[n_] = z
+        params[key] = (C, C8, pad)
+    return params[key]
+
+
 def gcn_forward(rowptr, col, val, X, params, plan: Plan | None = None):
     """2-layer GCN inference: H1 = relu(A (X W1^T) + b1), Y = A (H1 W2^T) + b2, every step a
     library kernel (dense layers on the matrix cores, aggregations with the bias and
     activation in their epilogue).  params: dict of W1 [hid, in], b1 [hid], W2 [out, hid],
-    b2 [out]; activations stay in X's dtype."""
+    b2 [out]; activations stay in X's dtype.  Returns Y [n, out] (a view of the padded
+    output when out is not a multiple of 8)."""
+    C, C8, pad = _padded_output_layer(params, ("W2", "b2"), ())
     Z1 = linear(X, params["W1"])
     H1 = gspmm(rowptr, col, val, Z1, "sum", plan=plan, bias=params["b1"], act="relu")
-    Z2 = linear(H1, params["W2"])
-    return gspmm(rowptr, col, val, Z2, "sum", plan=plan, bias=params["b2"], act="none")
+    Z2 = linear(H1, pad["W2"])
+    Y = gspmm(rowptr, col, val, Z2, "sum", plan=plan, bias=pad["b2"], act="none")
+    return Y if C8 == C else Y[:, :C]
 
 
 def gat_forward(rowptr, col, X, params, negative_slope: float = 0.2, plan: Plan | None = None):
     """2-layer GAT inference: layer 1 with H heads of D (concatenated, ELU), layer 2 with one
     head of C outputs.  params: W1 [H*D, in], a_src1 / a_dst1 [H, D], b1 [H*D], W2 [C, H*D],
-    a_src2 / a_dst2 [1, C], b2 [C]."""
+    a_src2 / a_dst2 [1, C], b2 [C].  Returns Y [n, C] (a view of the padded output when C is
+    not a multiple of 8)."""
     H, D = params["a_src1"].shape
-    C = params["W2"].shape[0]
+    C, C8, pad = _padded_output_layer(params, ("W2", "b2"), ("a_src2", "a_dst2"))
     n = X.shape[0]
     Z1 = linear(X, params["W1"]).view(n, H, D)
     s_src, s_dst = head_scores(Z1, params["a_src1"], params["a_dst1"])
     H1 = gat_aggregate(rowptr, col, s_dst, s_src, Z1, negative_slope, plan=plan, bias=params["b1"],
                        act="elu")
-    Z2 = linear(H1.view(n, H * D), params["W2"]).view(n, 1, C)
-    s_src2, s_dst2 = head_scores(Z2, params["a_src2"], params["a_dst2"])
-    return gat_aggregate(rowptr, col, s_dst2, s_src2, Z2, negative_slope, plan=plan,
-                         bias=params["b2"]).view(n, C)
+    Z2 = linear(H1.view(n, H * D), pad["W2"]).view(n, 1, C8)
+    s_src2, s_dst2 = head_scores(Z2, pad["a_src2"], pad["a_dst2"])
+    Y = gat_aggregate(rowptr, col, s_dst2, s_src2, Z2, negative_slope, plan=plan,
+                      bias=pad["b2"]).view(n, C8)
+    return Y if C8 == C else Y[:, :C]
 
 
 def act_codec_size(n: int, F: int, bits: int, group: int):
