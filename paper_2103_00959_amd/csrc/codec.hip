@@ -14,10 +14,14 @@
 // (e / 4, 0, 0) and key = seed, word e mod 4, top 24 bits times 2^-24.
 // Decoding: x' = fma(q, r, m), an unbiased estimate of x within one step.
 //
-// Mapping on gfx950: a wavefront per group.  The min/max is a butterfly over
-// the 64 lanes; each lane quantizes one feature of a block, and a block's b
-// bit planes are b wavefront ballots (one 64-bit mask each), written by lanes
-// 0..b-1, so a group of bf16 features reads 2G bytes and writes G b / 8.
+// Mapping on gfx950.  Rows of whole groups with 16-byte aligned rows (the
+// usual case, e.g. one group per 256-wide row): 8 consecutive features per
+// lane in 16-byte vectors, a group on G / 8 adjacent lanes (several groups per
+// wavefront), min/max by a butterfly within the group, each 64-feature block
+// of codes assembled from its 8 lanes' bytes by lane exchanges.  Otherwise
+// (ragged rows): a wavefront per group, one feature per lane, each block's b
+// bit planes as b wavefront ballots.  Either way a group of bf16 features
+// reads 2G bytes and writes G b / 8 + 8.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -26,9 +30,11 @@ namespace {
 
 constexpr int kBlock = 256;
 
-__device__ __forceinline__ uint32_t philox_word(uint64_t seed, int64_t e)
+// The four words of Philox4x32-10 at counter (c, 0, 0) (c = e / 4 as 64 bits)
+// with key = seed.
+__device__ __forceinline__ uint4 philox4(uint64_t seed, uint64_t c)
 {
-    uint32_t c0 = (uint32_t)((uint64_t)e >> 2), c1 = (uint32_t)((uint64_t)e >> 34), c2 = 0u, c3 = 0u;
+    uint32_t c0 = (uint32_t)c, c1 = (uint32_t)(c >> 32), c2 = 0u, c3 = 0u;
     uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
 #pragma unroll
     for (int round = 0; round < 10; ++round) {
@@ -42,9 +48,17 @@ __device__ __forceinline__ uint32_t philox_word(uint64_t seed, int64_t e)
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;
     }
-    const int w = (int)(e & 3);
-    return w == 0 ? c0 : w == 1 ? c1 : w == 2 ? c2 : c3;
+    return make_uint4(c0, c1, c2, c3);
 }
+
+__device__ __forceinline__ uint32_t philox_word(uint64_t seed, int64_t e)
+{
+    const uint4 r = philox4(seed, (uint64_t)e >> 2);
+    const int w = (int)(e & 3);
+    return w == 0 ? r.x : w == 1 ? r.y : w == 2 ? r.z : r.w;
+}
+
+__device__ __forceinline__ float uniform24(uint32_t r) { return (float)(r >> 8) * (1.0f / 16777216.0f); }
 
 __device__ __forceinline__ float wave_min(float v)
 {
@@ -107,7 +121,7 @@ __global__ __launch_bounds__(kBlock) void k_compress(CodecArgs a)
             if (j < len) {
                 float x[1];
                 load_vec<TA, 1>(A, base + j, x);
-                const float u = (float)(philox_word(a.seed, base + j) >> 8) * (1.0f / 16777216.0f);
+                const float u = uniform24(philox_word(a.seed, base + j));
                 float v = floorf(fmaf(x[0] - m, s, u));
                 v = v < 0.f ? 0.f : (v > qmax ? qmax : v);
                 q = (uint32_t)v;
@@ -165,6 +179,173 @@ unsigned codec_grid(int64_t groups)
     return (unsigned)b;
 }
 
+// ------------------------------------------------ vectorized path
+// Rows made of whole groups (F a multiple of G) with 16-byte aligned rows:
+// each lane holds 8 consecutive features, a group is LG = G / (8 NV) adjacent
+// lanes (8 to 64) holding NV vectors each, so a wavefront reads and writes
+// full 16-byte vectors and covers 64 / LG groups at a time.  A 64-feature
+// block of codes is 8 lanes: each contributes one byte per bit plane (its 8
+// codes), and the bytes are combined with three lane-exchange additions.
+
+__device__ __forceinline__ uint32_t lane_xor_u32(uint32_t v, int mask)
+{
+    return (uint32_t)__builtin_amdgcn_ds_bpermute((lane_id() ^ mask) << 2, (int)v);
+}
+
+template <typename T> struct Vec8;
+template <> struct Vec8<bf16_t> {
+    __device__ static void load(const bf16_t *p, int64_t i, float (&o)[8]) { load_vec<bf16_t, 8>(p, i, o); }
+    __device__ static void store(bf16_t *p, int64_t i, const float (&v)[8]) { store_vec<bf16_t, 8>(p, i, v); }
+};
+template <> struct Vec8<f16_t> {
+    __device__ static void load(const f16_t *p, int64_t i, float (&o)[8]) { load_vec<f16_t, 8>(p, i, o); }
+    __device__ static void store(f16_t *p, int64_t i, const float (&v)[8]) { store_vec<f16_t, 8>(p, i, v); }
+};
+template <> struct Vec8<float> {
+    __device__ static void load(const float *p, int64_t i, float (&o)[8])
+    {
+        float lo[4], hi[4];
+        load_vec<float, 4>(p, i, lo);
+        load_vec<float, 4>(p, i + 4, hi);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { o[e] = lo[e]; o[4 + e] = hi[e]; }
+    }
+    __device__ static void store(float *p, int64_t i, const float (&v)[8]) { store_vec<float, 8>(p, i, v); }
+};
+
+template <typename TA, int NV>
+__global__ __launch_bounds__(kBlock) void k_compress_v(CodecArgs a)
+{
+    const int lane = lane_id();
+    const int LG = a.G / (8 * NV);
+    const int sl = lane & (LG - 1);
+    const int per_wave = kWave / LG;
+    const int64_t groups = a.n * a.ng;
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave) * per_wave;
+    const float qmax = (float)((1 << a.bits) - 1);
+    const int nb = a.G / kWave;
+    const TA *__restrict__ A = static_cast<const TA *>(a.A);
+    for (int64_t g = wave * per_wave + lane / LG; g - lane / LG < groups; g += stride) {
+        const bool gok = g < groups;
+        const int64_t base = g * a.G;          // whole groups: the flat index of feature j is base + j
+        float x[NV][8];
+        float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            if (gok) {
+                Vec8<TA>::load(A, base + (int64_t)(v * LG + sl) * 8, x[v]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[v][e] = 0.f;
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                lo = fminf(lo, gok ? x[v][e] : INFINITY);
+                hi = fmaxf(hi, gok ? x[v][e] : -INFINITY);
+            }
+        }
+        for (int off = 1; off < LG; off <<= 1) {
+            lo = fminf(lo, lane_xor(lo, off));
+            hi = fmaxf(hi, lane_xor(hi, off));
+        }
+        const float range = hi - lo;
+        const float s = range > 0.f ? qmax / range : 0.f;
+        const float r = range > 0.f ? range / qmax : 0.f;
+        if (gok && sl == 0) {
+            a.stats[2 * g] = lo;
+            a.stats[2 * g + 1] = r;
+        }
+        uint64_t *__restrict__ w = a.codes + g * (int64_t)nb * a.bits;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const int64_t e0 = base + (int64_t)(v * LG + sl) * 8;   // a multiple of 8
+            // the 8 uniforms of these features: two Philox blocks of 4
+            const uint4 r0 = philox4(a.seed, (uint64_t)e0 >> 2);
+            const uint4 r1 = philox4(a.seed, ((uint64_t)e0 >> 2) + 1);
+            const uint32_t rw[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+            uint32_t q[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float u = uniform24(rw[e]);
+                float t = floorf(fmaf(x[v][e] - lo, s, u));
+                t = t < 0.f ? 0.f : (t > qmax ? qmax : t);
+                q[e] = (uint32_t)t;
+            }
+            const int blk = (v * LG + sl) / 8;     // 64-feature block of these 8 features
+            const int byte = sl & 7;               // their byte within the block's planes
+            for (int p = 0; p < a.bits; ++p) {
+                uint32_t frag = 0;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) frag |= ((q[e] >> p) & 1u) << e;
+                // bytes 0-3 of the plane in the low word, 4-7 in the high word
+                uint32_t wlo = byte < 4 ? frag << (8 * byte) : 0u;
+                uint32_t whi = byte >= 4 ? frag << (8 * (byte - 4)) : 0u;
+#pragma unroll
+                for (int off = 1; off < 8; off <<= 1) {
+                    wlo += lane_xor_u32(wlo, off);
+                    whi += lane_xor_u32(whi, off);
+                }
+                if (gok && byte == 0) w[(int64_t)blk * a.bits + p] = ((uint64_t)whi << 32) | wlo;
+            }
+        }
+    }
+}
+
+template <typename TO, int NV>
+__global__ __launch_bounds__(kBlock) void k_decompress_v(int64_t n, int bits, int G, int ng,
+                                                         const uint64_t *__restrict__ codes,
+                                                         const float *__restrict__ stats,
+                                                         TO *__restrict__ out)
+{
+    const int lane = lane_id();
+    const int LG = G / (8 * NV);
+    const int sl = lane & (LG - 1);
+    const int per_wave = kWave / LG;
+    const int64_t groups = n * ng;
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave) * per_wave;
+    const int nb = G / kWave;
+    for (int64_t g = wave * per_wave + lane / LG; g - lane / LG < groups; g += stride) {
+        if (g >= groups) continue;
+        const float m = stats[2 * g], r = stats[2 * g + 1];
+        const uint64_t *__restrict__ w = codes + g * (int64_t)nb * bits;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const int blk = (v * LG + sl) / 8;
+            const int byte = sl & 7;
+            uint32_t q[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+            for (int p = 0; p < bits; ++p) {
+                const uint32_t b8 = (uint32_t)(w[(int64_t)blk * bits + p] >> (8 * byte)) & 0xffu;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) q[e] |= ((b8 >> e) & 1u) << p;
+            }
+            float y[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) y[e] = fmaf((float)q[e], r, m);
+            Vec8<TO>::store(out, g * G + (int64_t)(v * LG + sl) * 8, y);
+        }
+    }
+}
+
+using CompressKernel = void (*)(CodecArgs);
+
+template <typename TA>
+CompressKernel pick_compress_v(int nv)
+{
+    if (nv == 1) return k_compress_v<TA, 1>;
+    if (nv == 2) return k_compress_v<TA, 2>;
+    if (nv == 4) return k_compress_v<TA, 4>;
+    return k_compress_v<TA, 8>;
+}
+
+// NV for the vectorized path (0: not applicable)
+int vector_nv(int32_t F, int32_t group, const void *p)
+{
+    if (F % group != 0 || group > 4096 || (uintptr_t)p % 16 != 0) return 0;
+    return group >= 512 ? group / 512 : 1;
+}
+
 }  // namespace
 }  // namespace cogdl
 
@@ -195,6 +376,16 @@ cogdl_status cogdl_act_compress(int64_t n, int32_t F, const void *A, cogdl_dtype
     if (n == 0) return COGDL_OK;
     CodecArgs a{n, F, bits, group, (F + group - 1) / group, seed, A, codes, stats};
     const unsigned b = codec_grid(n * a.ng);
+    const int nv = vector_nv(F, group, A);
+    if (nv > 0) {
+        const int per_wave = kWave / (group / (8 * nv));
+        const unsigned bv = codec_grid((n * a.ng + per_wave - 1) / per_wave);
+        CompressKernel k = a_dtype == COGDL_F32    ? pick_compress_v<float>(nv)
+                           : a_dtype == COGDL_BF16 ? pick_compress_v<bf16_t>(nv)
+                                                   : pick_compress_v<f16_t>(nv);
+        COGDL_LAUNCH("act_compress", k, bv, kBlock, stream, a);
+        return COGDL_OK;
+    }
     if (a_dtype == COGDL_F32)
         COGDL_LAUNCH("act_compress", k_compress<float>, b, kBlock, stream, a);
     else if (a_dtype == COGDL_BF16)
@@ -215,6 +406,31 @@ cogdl_status cogdl_act_decompress(int64_t n, int32_t F, int32_t bits, int32_t gr
     if (n == 0) return COGDL_OK;
     const int ng = (F + group - 1) / group;
     const unsigned b = codec_grid(n * ng);
+    const int nv = vector_nv(F, group, out);
+    if (nv > 0) {
+        const int per_wave = kWave / (group / (8 * nv));
+        const unsigned bv = codec_grid((n * ng + per_wave - 1) / per_wave);
+#define COGDL_DECOMP_V(TO)                                                                       \
+    do {                                                                                         \
+        if (nv == 1)                                                                             \
+            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 1>), bv, kBlock, stream, n, bits,  \
+                         group, ng, codes, stats, static_cast<TO *>(out));                       \
+        else if (nv == 2)                                                                        \
+            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 2>), bv, kBlock, stream, n, bits,  \
+                         group, ng, codes, stats, static_cast<TO *>(out));                       \
+        else if (nv == 4)                                                                        \
+            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 4>), bv, kBlock, stream, n, bits,  \
+                         group, ng, codes, stats, static_cast<TO *>(out));                       \
+        else                                                                                     \
+            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 8>), bv, kBlock, stream, n, bits,  \
+                         group, ng, codes, stats, static_cast<TO *>(out));                       \
+    } while (0)
+        if (out_dtype == COGDL_F32) COGDL_DECOMP_V(float);
+        else if (out_dtype == COGDL_BF16) COGDL_DECOMP_V(bf16_t);
+        else COGDL_DECOMP_V(f16_t);
+#undef COGDL_DECOMP_V
+        return COGDL_OK;
+    }
     if (out_dtype == COGDL_F32)
         COGDL_LAUNCH("act_decompress", k_decompress<float>, b, kBlock, stream, n, F, bits, group,
                      ng, codes, stats, static_cast<float *>(out));

@@ -197,7 +197,8 @@ def test_gat_model(cg, kind, spec):
 
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
 @pytest.mark.parametrize("n,F,G,at", [(50, 64, 64, "f32"), (300, 256, 256, "bf16"), (97, 300, 128, "bf16"),
-                                      (33, 41, 64, "f16"), (1000, 128, 64, "f32")])
+                                      (33, 41, 64, "f16"), (1000, 128, 64, "f32"), (21, 2048, 1024, "bf16"),
+                                      (7, 4096, 4096, "f32"), (13, 1024, 512, "f16"), (9, 2048, 2048, "bf16")])
 def test_act_codec_bit_exact(cg, bits, n, F, G, at):
     """Codes, stats and decoded values equal the oracle's bit for bit (the same
     Philox stream, the same fp32 operations)."""
