@@ -14,6 +14,9 @@ namespace cogdl {
 namespace {
 
 constexpr int kBlock = 256;
+// 6-bit digits: on 122M edges, runs of ~48 keys per digit and tile write whole
+// lines, where 8-bit digits (runs of 12) cost more than their saved pass
+constexpr int kCscDigitBits = 6;
 
 __global__ __launch_bounds__(kBlock) void k_expand_rows(const int32_t *__restrict__ rowptr,
                                                         int32_t n_rows,
@@ -126,12 +129,12 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
                           reinterpret_cast<uint32_t *>(ws + L.ping_r)};
         COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), nullptr, skeys,
                                        reinterpret_cast<uint32_t *>(perm), nnz, bits, ping_k, ping_v,
-                                       ws + L.radix, stream, rows, vals));
+                                       ws + L.radix, stream, rows, vals, kCscDigitBits));
     } else {
         // no edge ids wanted: the rows are the sorted values, one array less per pass
         COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), row_of, skeys,
                                        reinterpret_cast<uint32_t *>(row_t), nnz, bits, ping_k, ping_v,
-                                       ws + L.radix, stream, vals, RadixPayload{}));
+                                       ws + L.radix, stream, vals, RadixPayload{}, kCscDigitBits));
     }
     COGDL_LAUNCH("csc_colptr", k_colptr, grid_for(nnz, kBlock), kBlock, stream, skeys, nnz, n_cols,
                  colptr);

@@ -17,7 +17,7 @@ constexpr int kSortBlock = 256;                      // 4 wavefronts
 constexpr int kSortItems = 12;
 constexpr int kSortTile = kSortBlock * kSortItems;   // 3072
 constexpr int kDigits = 256;                         // digits of at most 8 bits
-constexpr int kMaxDigitBits = 6;                     // widest digit of a pass
+constexpr int kMaxDigitBits = 8;                     // widest digit of a pass
 
 __device__ __forceinline__ int wave_inclusive_scan(int x)
 {
@@ -305,8 +305,9 @@ size_t radix_workspace_bytes(int64_t n)
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
                             uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
                             uint32_t *ping_vals, void *ws, hipStream_t s, RadixPayload pay0,
-                            RadixPayload pay1)
+                            RadixPayload pay1, int max_digit_bits)
 {
+    if (max_digit_bits < 1 || max_digit_bits > kMaxDigitBits) max_digit_bits = kMaxDigitBits;
     if (n <= 0) return hipSuccess;
     const int np = pay0.in ? (pay1.in ? 2 : 1) : 0;
     const int64_t tiles = (n + kSortTile - 1) / kSortTile;
@@ -315,9 +316,9 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
     size_t hist_bytes = ((size_t)(hist_n + 1 + 64) * 4 + 255) & ~size_t(255);
     void *scan_ws = static_cast<char *>(ws) + hist_bytes;
 
-    // as few passes as digits of at most kMaxDigitBits allow, the bits spread
+    // as few passes as digits of at most max_digit_bits allow, the bits spread
     // evenly over them (longer runs per digit than a short last pass gives)
-    int passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
+    int passes = (bits + max_digit_bits - 1) / max_digit_bits;
     if (passes < 1) passes = 1;
     const uint32_t *src_k = keys_in;
     const uint32_t *src_v = vals_in;

@@ -274,3 +274,44 @@ def test_inference_reddit_shaped_sampled(cg):
             assert err <= 3 * 2.0 ** -7 + 1e-3, kind
     finally:
         plan.close()
+
+
+@pytest.mark.timeout(900)
+def test_features_beyond_4gib_use_64bit_gathers(cg):
+    """A feature matrix larger than the 32-bit offsets of the buffer gathers reach
+    (1,100,000 x 2048 bf16 = 4.2 GiB) takes the 64-bit gather path: the SpMM and
+    the GAT aggregation gather rows near its end, whole rows and split rows."""
+    import torch
+    n_cols, W = 1_100_000, 2048
+    rng = np.random.default_rng(77)
+    n_rows = 3000
+    deg = rng.integers(0, 40, n_rows)
+    deg[[0, 17, 2999]] = [5000, 3000, 1]                  # split rows under a small group size
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+    col = np.concatenate([np.sort(rng.choice(n_cols, d, replace=False)) for d in deg]).astype(np.int32)
+    col[::7] = n_cols - 1 - (np.arange(col[::7].size) % 5)  # rows at the very end of X
+    val = rng.standard_normal(col.size).astype(np.float32)
+    say(f"huge X: {n_cols} x {W} bf16 = {n_cols * W * 2 / 2**30:.2f} GiB, nnz={col.size}")
+    xb = synth.f32_to_bf16_bits(synth.normal_f32((n_cols, W), 9001))
+    xd = dev(xb.view(np.int16)).view(torch.bfloat16)
+    rp, cl, vl = dev(rowptr), dev(col), dev(val)
+    rows = np.unique(np.concatenate([[0, 17, 2999], rng.choice(n_rows, 200, replace=False)])).astype(np.int32)
+    idx = torch.from_numpy(rows).long().cuda()
+    for spec in (None, ("neighbor_group", 256)):
+        plan = None if spec is None else cg.Plan(rp, col.size, W, max_heads=8, mode=spec[0], group_size=spec[1])
+        try:
+            Y = cg.spmm(rp, cl, vl, xd, plan=plan, out_dtype=torch.float32)
+            Yr, Ar = oracle.spmm(rowptr, col, val, xb, x_dtype=oracle.BF16, rows=rows)
+            assert scaled_error(Y[idx], Yr, Ar) <= TOL_F32, spec
+            H, D = 8, W // 8
+            alpha = rng.random((col.size, H)).astype(np.float32)
+            Yg = cg.gat_aggregate(rp, cl, None, None, xd.view(n_cols, H, D), alpha_in=dev(alpha), plan=plan,
+                                  out_dtype=torch.float32)
+            Ygr, Agr = oracle.gat(rowptr, col, None, None, xb, H, D, alpha_in=alpha, x_dtype=oracle.BF16,
+                                  rows=rows)
+            assert scaled_error(Yg.reshape(n_rows, W)[idx], Ygr, Agr) <= TOL_F32, spec
+        finally:
+            if plan is not None:
+                plan.close()
+    del xd
+    torch.cuda.empty_cache()
