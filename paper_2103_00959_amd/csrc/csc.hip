@@ -2,7 +2,7 @@
 // pass of Eq. 1 (the gradient with respect to the node features is A^T G).
 //
 // A stable LSD radix sort of the edge ids keyed by column (digits of at most
-// 6 bits, as many passes as the column count needs) gives perm directly, with
+// 8 bits, as many passes as the column count needs) gives perm directly, with
 // each edge's row and value bits carried along as payloads (so nothing is
 // gathered at random afterwards); colptr is read off the sorted keys.  Every step is
 // integer work in a fixed order, so the result is bit-for-bit unique: inside
@@ -14,9 +14,6 @@ namespace cogdl {
 namespace {
 
 constexpr int kBlock = 256;
-// 6-bit digits: on 122M edges, runs of ~48 keys per digit and tile write whole
-// lines, where 8-bit digits (runs of 12) cost more than their saved pass
-constexpr int kCscDigitBits = 6;
 
 __global__ __launch_bounds__(kBlock) void k_expand_rows(const int32_t *__restrict__ rowptr,
                                                         int32_t n_rows,
@@ -129,12 +126,12 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
                           reinterpret_cast<uint32_t *>(ws + L.ping_r)};
         COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), nullptr, skeys,
                                        reinterpret_cast<uint32_t *>(perm), nnz, bits, ping_k, ping_v,
-                                       ws + L.radix, stream, rows, vals, kCscDigitBits));
+                                       ws + L.radix, stream, rows, vals));
     } else {
         // no edge ids wanted: the rows are the sorted values, one array less per pass
         COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), row_of, skeys,
                                        reinterpret_cast<uint32_t *>(row_t), nnz, bits, ping_k, ping_v,
-                                       ws + L.radix, stream, vals, RadixPayload{}, kCscDigitBits));
+                                       ws + L.radix, stream, vals, RadixPayload{}));
     }
     COGDL_LAUNCH("csc_colptr", k_colptr, grid_for(nnz, kBlock), kBlock, stream, skeys, nnz, n_cols,
                  colptr);

@@ -96,15 +96,13 @@ struct RadixPayload {
 // keys.  vals_in == nullptr means values 0..n-1.  Results land in keys_out /
 // vals_out (keys_out may be nullptr when the sorted keys are not needed); up
 // to two payload arrays move with the keys.  ping: 2 * n keys and 2 * n
-// values of scratch.  Digits are at most max_digit_bits (<= 8) wide, the key
-// bits spread evenly over the fewest passes that allows: narrow digits give
-// long runs per digit (large sorts), wide ones fewer passes (small sorts).
+// values of scratch.  Digits are at most 8 bits wide, the key bits spread
+// evenly over the fewest passes that allows.
 size_t radix_workspace_bytes(int64_t n);
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
                             uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
                             uint32_t *ping_vals, void *ws, hipStream_t s,
-                            RadixPayload pay0 = RadixPayload(), RadixPayload pay1 = RadixPayload(),
-                            int max_digit_bits = 8);
+                            RadixPayload pay0 = RadixPayload(), RadixPayload pay1 = RadixPayload());
 
 // Fill n int32 with a value (a kernel, so it is safe inside graph capture).
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);

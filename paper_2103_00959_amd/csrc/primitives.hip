@@ -14,8 +14,8 @@ constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanBlock * kScanItems;   // 2048
 
 constexpr int kSortBlock = 256;                      // 4 wavefronts
-constexpr int kSortItems = 12;
-constexpr int kSortTile = kSortBlock * kSortItems;   // 3072
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortBlock * kSortItems;   // 4096
 constexpr int kDigits = 256;                         // digits of at most 8 bits
 constexpr int kMaxDigitBits = 8;                     // widest digit of a pass
 
@@ -130,8 +130,21 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__res
     }
 }
 
+// Tile handled by workgroup b of nb.  Workgroups are dealt to the 8 XCDs
+// round-robin (b % 8), so XCD x gets the contiguous tile range
+// [x * nb / 8, (x + 1) * nb / 8) instead of every 8th tile: the tiles running
+// together on one XCD then write adjacent pieces of each digit's output run,
+// and the cache lines split between two tiles are completed in that XCD's L2
+// before they go to HBM.  Any bijection is correct; this one is a speed choice.
+__device__ __forceinline__ int xcd_tile(int b, int nb)
+{
+    constexpr int kXcds = 8;
+    const int x = b % kXcds, per = nb / kXcds, rem = nb % kXcds;
+    return x * per + (x < rem ? x : rem) + b / kXcds;
+}
+
 // Stable scatter of one tile.  Wavefront w owns the contiguous quarter
-// [w * 768, (w + 1) * 768) of the tile and walks it 64 keys at a time; the
+// [w * 1024, (w + 1) * 1024) of the tile and walks it 64 keys at a time; the
 // rank of a key among equal digits is the number of lower lanes with the same
 // digit (found with one ballot per digit bit) plus the running per-wave count.  All
 // arrays of the tile are loaded up front (one memory round trip), then staged
@@ -155,7 +168,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) wcnt[i][tid] = 0;
 
-    const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
+    const int tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int64_t tile0 = (int64_t)tile * kSortTile;
     const int count = (int)((n - tile0) < kSortTile ? (n - tile0) : kSortTile);
     const int64_t base = tile0 + (int64_t)w * kWave * kSortItems;
     uint32_t key[kSortItems], val[kSortItems], pa[NP > 0 ? kSortItems : 1], pb[NP > 1 ? kSortItems : 1];
@@ -199,7 +213,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         int all;
         const int start = block_exclusive_scan(tot, &all);
         dstart[tid] = start;
-        gstart[tid] = tid <= (int)dmask ? offsets[(int64_t)tid * n_tiles + blockIdx.x] : 0;
+        gstart[tid] = tid <= (int)dmask ? offsets[(int64_t)tid * n_tiles + tile] : 0;
         int run = start;
 #pragma unroll
         for (int i = 0; i < kWaves; ++i) {
@@ -305,9 +319,8 @@ size_t radix_workspace_bytes(int64_t n)
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
                             uint32_t *vals_out, int64_t n, int bits, uint32_t *ping_keys,
                             uint32_t *ping_vals, void *ws, hipStream_t s, RadixPayload pay0,
-                            RadixPayload pay1, int max_digit_bits)
+                            RadixPayload pay1)
 {
-    if (max_digit_bits < 1 || max_digit_bits > kMaxDigitBits) max_digit_bits = kMaxDigitBits;
     if (n <= 0) return hipSuccess;
     const int np = pay0.in ? (pay1.in ? 2 : 1) : 0;
     const int64_t tiles = (n + kSortTile - 1) / kSortTile;
@@ -316,9 +329,9 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
     size_t hist_bytes = ((size_t)(hist_n + 1 + 64) * 4 + 255) & ~size_t(255);
     void *scan_ws = static_cast<char *>(ws) + hist_bytes;
 
-    // as few passes as digits of at most max_digit_bits allow, the bits spread
-    // evenly over them (longer runs per digit than a short last pass gives)
-    int passes = (bits + max_digit_bits - 1) / max_digit_bits;
+    // as few passes as digits of at most 8 bits allow, the bits spread evenly
+    // over them (longer runs per digit than a short last pass gives)
+    int passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
     if (passes < 1) passes = 1;
     const uint32_t *src_k = keys_in;
     const uint32_t *src_v = vals_in;
