@@ -72,6 +72,27 @@ def b_plan(N, n_units):
     return 4 * (N + 1) + 16 * n_units
 
 
+# Compulsory bytes: every array once, the gathered feature rows (and GAT's
+# per-source scores) read once each instead of once per nonzero.
+def b_unique_spmm(n_out, n_in, E, F, sx, sy):
+    return 4 * (n_out + 1) + 8 * E + n_in * F * sx + n_out * F * sy
+
+
+def b_unique_gat(N, M, E, H, D, sx, sy):
+    return 4 * (N + 1) + 4 * E + 4 * N * H + 4 * M * H + M * H * D * sx + N * H * D * sy
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 # ----------------------------------------------------------- HBM counters
 
 # The step's candidate roofline kernels: the sources that define each one, its
@@ -149,6 +170,7 @@ def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
         edges_total += 2 * e
         chunk = min(chunk * 2, 200000)
     return dict(value=bytes_total / t_total / 1e9, unit="GB/s", cores=threads, kind="oracle",
+                cpu=cpu_model(),
                 sample=(f"SpMM (F=256 bf16) + fused GAT (4x64 bf16) on {done_rows} random rows "
                         f"({edges_total // 2} nonzeros each) of the same graph, fp64 oracle"),
                 seconds=t_total, edges_per_s=edges_total / t_total)
@@ -329,8 +351,8 @@ def main():
         step(step_evs[i])
     ev1.record()
     torch.cuda.synchronize()
-    op_ms = {op: sum(e[j].elapsed_time(e[j + 1]) for e in step_evs) / args.steps
-             for j, op in enumerate(OPS)}
+    op_all = {op: [e[j].elapsed_time(e[j + 1]) for e in step_evs] for j, op in enumerate(OPS)}
+    op_ms = {op: sum(v) / args.steps for op, v in op_all.items()}
     t_wall = time.perf_counter() - t_wall
     ms_step = ev0.elapsed_time(ev1) / args.steps
     trace = cg.trace_read()
@@ -356,13 +378,20 @@ def main():
     }
     B_step = sum(B.values())
     value = B_step / (ms_step * 1e-3) / 1e9
+    B_unique = dict(B, spmm=b_unique_spmm(N, M, E, F, 2, 2), spmm_t=b_unique_spmm(M, N, E, F, 2, 2),
+                    gat_aggregate=b_unique_gat(N, M, E, H, D, 2, 2))
+    FLOP = {"spmm": 2 * E * F, "spmm_t": 2 * E * F, "gat_aggregate": 2 * E * H * D + 8 * E * H}
     ops = {}
     for op in OPS:
         ms = op_ms[op]
-        ops[op] = dict(ms=ms, algorithmic_GB=B[op] / 1e9,
-                       eff_GBps=(B[op] / (ms * 1e-3) / 1e9) if ms > 0 else None,
-                       pct_peak=(B[op] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS) if ms > 0 else None,
-                       edges_per_s=(E / (ms * 1e-3)) if ms > 0 and not op.startswith("plan") else None)
+        ok = ms > 0
+        ops[op] = dict(ms=ms, ms_median=float(np.median(op_all[op])), ms_min=min(op_all[op]),
+                       algorithmic_GB=B[op] / 1e9,
+                       eff_GBps=(B[op] / (ms * 1e-3) / 1e9) if ok else None,
+                       pct_peak=(B[op] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS) if ok else None,
+                       unique_GBps=(B_unique[op] / (ms * 1e-3) / 1e9) if ok else None,
+                       GFLOPps=(FLOP[op] / (ms * 1e-3) / 1e9) if ok and op in FLOP else None,
+                       edges_per_s=(E / (ms * 1e-3)) if ok and not op.startswith("plan") else None)
     # dominant kernel: the largest device time per step; its algorithmic bytes
     # are its own edges and output rows (per nonzero: index, value, one feature
     # row; per row: row pointer and the output row)
@@ -491,6 +520,37 @@ def main():
                                    eff_GBps=b_max / (ms_max * 1e-3) / 1e9,
                                    edges_per_s=E / (ms_max * 1e-3)),
     }
+    # Warm mode: the same call back to back, so what the previous call left in
+    # L2 and the memory-side cache is reused (inside the step every operator
+    # follows gigabytes of unrelated traffic, which is the cold case).
+    def warm(fn, reps=10):
+        fn()
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        evs[0].record()
+        for i in range(reps):
+            fn()
+            evs[i + 1].record()
+        torch.cuda.synchronize()
+        t = [evs[i].elapsed_time(evs[i + 1]) for i in range(reps)]
+        return dict(ms_median=float(np.median(t)), ms_min=min(t))
+    warm_ops = {
+        "spmm": warm(lambda: cg.spmm(rowptr, col, val, X, plan=plan, out=Y)),
+        "spmm_t": warm(lambda: cg.spmm_t(colptr, row_t, val_t, Gt, plan_t=plan_t, out=dX)),
+        "gat_aggregate": warm(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
+                                                       out=Yg)),
+    }
+    for op, w in warm_ops.items():
+        w["eff_GBps"] = B[op] / (w["ms_median"] * 1e-3) / 1e9
+    # achievable-bandwidth ceiling: a plain 1 GiB device-to-device copy
+    cp_src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    cp_dst = torch.empty_like(cp_src)
+    cp = warm(lambda: cp_dst.copy_(cp_src), reps=5)
+    copy_GBps = 2 * (1 << 30) / (cp["ms_median"] * 1e-3) / 1e9
+    del cp_src, cp_dst
+    log(f"warm (back to back): " + ", ".join(f"{k} {v['ms_median']:.3f} ms" for k, v in warm_ops.items())
+        + f"; 1 GiB copy {copy_GBps:.0f} GB/s")
+
     codec_txt = ", ".join("%s %.3f/%.3f" % (k, v["compress_ms"], v["decompress_ms"]) for k, v in codec.items())
     log(f"extra: sddmm_edge_softmax {ms_soft:.3f} ms, gat_aggregate+alpha {ms_gat_a:.3f} ms, "
         f"gspmm mean {ms_mean:.3f} ms, max+arg {ms_max:.3f} ms, sddmm_dot {ms_dot:.3f} ms, "
@@ -515,6 +575,11 @@ def main():
         "edges_per_s": 3 * E / (ms_step * 1e-3),
         "edges_per_s_note": "nonzeros aggregated per second over the three gathers (SpMM, SpMM^T, GAT)",
         "ops": ops,
+        "ops_timing": ("ops: mean, median and min over the timed steps, each operator cold "
+                       "(it follows gigabytes of other traffic in the step); ops_warm: the same call "
+                       "repeated back to back"),
+        "ops_warm": warm_ops,
+        "copy_GBps": copy_GBps,
         "ops_outside_step": extra_ops,
         "kernels": kernels,
         "roofline": roofline,
