@@ -376,9 +376,17 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
  * (0 disables tracing and frees them); launches beyond the capacity are not
  * recorded.  cogdl_trace_get synchronizes on the i-th stop event and returns
  * the kernel's name (static storage) and its duration in milliseconds.  The
- * tracer is process-wide and not thread-safe.
+ * tracer is process-wide and not thread-safe.  Each recorded event pair
+ * costs the stream a few microseconds, so a timing run that only needs some
+ * kernels restricts the trace with cogdl_trace_filter(names): a
+ * comma-separated list of launch names (as cogdl_trace_get reports them);
+ * only launches named in it are recorded.  NULL or "" records every launch
+ * (the default); the list is copied; names longer than 63 characters or a
+ * list longer than 1023 characters give COGDL_ERR_INVALID and leave the
+ * filter unchanged.
  * ---------------------------------------------------------------------- */
 cogdl_status cogdl_trace_enable(int32_t capacity);
+cogdl_status cogdl_trace_filter(const char *names);
 cogdl_status cogdl_trace_reset(void);
 int32_t cogdl_trace_count(void);
 cogdl_status cogdl_trace_get(int32_t i, const char **name, float *ms);

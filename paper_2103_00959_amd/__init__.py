@@ -84,9 +84,10 @@ def lib():
                                      ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P,
                                      P, P]
     L.cogdl_trace_enable.argtypes = [i32]
+    L.cogdl_trace_filter.argtypes = [ctypes.c_char_p]
     L.cogdl_trace_count.restype = i32
     L.cogdl_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
-    for name in ("cogdl_trace_enable", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
+    for name in ("cogdl_trace_enable", "cogdl_trace_filter", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate",
                  "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act", "cogdl_linear",
@@ -191,6 +192,12 @@ class Plan:
 def trace_enable(capacity: int = 4096):
     """Record HIP events around every library kernel launch (0 disables)."""
     _check(lib().cogdl_trace_enable(int(capacity)), "cogdl_trace_enable")
+
+
+def trace_filter(names=None):
+    """Record only the launches with these names (an iterable of str); None: all."""
+    arg = None if names is None else ",".join(names).encode()
+    _check(lib().cogdl_trace_filter(arg), "cogdl_trace_filter")
 
 
 def trace_reset():

@@ -1,11 +1,13 @@
 // Kernel-level tracing: when enabled, every kernel the library launches is
-// bracketed by two HIP events recorded on its launch stream, so a caller can
-// read the device duration of each launch.  Events are created once by
+// bracketed by two HIP events recorded on its launch stream (or only the
+// launches a name filter lists), so a caller can read the device duration of
+// each launch.  Events are created once by
 // cogdl_trace_enable; the launch path only records them (nothing allocates).
 // The tracer is process-wide and not thread-safe.
 #include <string.h>
 
 #include <mutex>
+#include <string>
 #include <vector>
 
 #include "common.hpp"
@@ -20,9 +22,18 @@ struct Tracer {
     int32_t n = 0;
     std::vector<hipEvent_t> start, stop;
     std::vector<const char *> names;
+    std::vector<std::string> only;   // empty: record every launch
 };
 
 Tracer g_trace;
+
+bool traced(const char *name)
+{
+    if (g_trace.only.empty()) return true;
+    for (const std::string &o : g_trace.only)
+        if (o == name) return true;
+    return false;
+}
 
 void trace_free()
 {
@@ -39,7 +50,7 @@ void trace_free()
 
 int trace_begin(const char *name, hipStream_t s)
 {
-    if (!g_trace.on || g_trace.n >= g_trace.cap) return -1;
+    if (!g_trace.on || g_trace.n >= g_trace.cap || !traced(name)) return -1;
     const int i = g_trace.n++;
     g_trace.names[i] = name;
     (void)hipEventRecord(g_trace.start[i], s);
@@ -97,6 +108,25 @@ cogdl_status cogdl_trace_enable(int32_t capacity)
     g_trace.cap = capacity;
     g_trace.n = 0;
     g_trace.on = true;
+    return COGDL_OK;
+}
+
+cogdl_status cogdl_trace_filter(const char *names)
+{
+    std::vector<std::string> only;
+    if (names) {
+        if (strlen(names) > 1023) return COGDL_ERR_INVALID;
+        const char *p = names;
+        while (*p) {
+            const char *q = strchr(p, ',');
+            const size_t len = q ? (size_t)(q - p) : strlen(p);
+            if (len > 63) return COGDL_ERR_INVALID;
+            if (len > 0) only.emplace_back(p, len);
+            p += len;
+            if (*p == ',') ++p;
+        }
+    }
+    cogdl::g_trace.only.swap(only);
     return COGDL_OK;
 }
 

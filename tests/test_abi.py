@@ -43,6 +43,17 @@ def test_status_strings_and_version(L):
     assert L.cogdl_version() >= 100
 
 
+def test_trace_filter_validation(L):
+    # the filter is host state only: no device is touched
+    L.cogdl_trace_filter.argtypes = [ctypes.c_char_p]
+    assert L.cogdl_trace_filter(b"spmm,gat") == 0
+    assert L.cogdl_trace_filter(b"x" * 64) == 1          # a name longer than 63 characters
+    assert L.cogdl_trace_filter(b"a," * 600) == 1        # a list longer than 1023 characters
+    assert L.cogdl_trace_filter(b",,spmm,") == 0         # empty names are skipped
+    assert L.cogdl_trace_filter(None) == 0
+    assert L.cogdl_trace_filter(b"") == 0
+
+
 def _p(v):
     return ctypes.c_void_p(v)
 

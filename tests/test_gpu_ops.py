@@ -162,6 +162,28 @@ def test_spmm_deterministic(cg):
         plan.close()
 
 
+def test_trace_filter_records_only_listed_launches(cg):
+    import torch
+    g = _graph("hubs", seed=13)
+    rp, cl, vl = graph_to_dev(g)
+    _, _, xd = features((g.n_cols, 64), 3, "f32")
+    plan = cg.Plan(rp, g.nnz, 64, mode="neighbor_group", group_size=16)
+    try:
+        cg.trace_enable(64)
+        for only, expect in ((None, {"spmm", "spmm_tiny", "spmm_reduce"}), (["spmm"], {"spmm"}),
+                             (["spmm_reduce", "nothing"], {"spmm_reduce"})):
+            cg.trace_filter(only)
+            cg.trace_reset()
+            cg.spmm(rp, cl, vl, xd, plan=plan)
+            torch.cuda.synchronize()
+            names = [n for n, ms in cg.trace_read()]
+            assert set(names) == expect and len(names) == len(expect), (only, names)
+    finally:
+        cg.trace_filter(None)
+        cg.trace_enable(0)
+        plan.close()
+
+
 # ---------------------------------------------------------------- GSpMM mean / max
 
 @pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1", "empty"])
