@@ -15,28 +15,103 @@ namespace {
 
 constexpr int kBlock = 256;
 
+// Row of every edge.  Wavefront w covers the edges [w * kExpandSpan, ...): it
+// finds the row holding its first edge by a 64-way search of rowptr (each
+// round narrows the candidate rows 64-fold, four rounds for a few million
+// rows), then walks its edges 64 at a time against a window of 64
+// consecutive row ends held one per lane; the row of edge e is the window's
+// first row plus the number of window rows that end at or before e (a binary
+// search across the lanes).  Empty rows need no care: the search keeps the
+// last row starting at or before the edge, and the window just moves on.
+constexpr int kExpandSpan = 2048;
+constexpr int kExpandEdges = 4;
+
 __global__ __launch_bounds__(kBlock) void k_expand_rows(const int32_t *__restrict__ rowptr,
-                                                        int32_t n_rows,
+                                                        int32_t n_rows, int64_t nnz,
                                                         uint32_t *__restrict__ row_of)
 {
     const int lane = lane_id();
-    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
-    for (int64_t i = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; i < n_rows;
-         i += waves) {
-        const int beg = rowptr[i], end = rowptr[i + 1];
-        for (int k = beg + lane; k < end; k += kWave) row_of[k] = (uint32_t)i;
+    const int64_t e0 = ((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * kExpandSpan;
+    if (e0 >= nnz) return;
+    const int64_t e1 = e0 + kExpandSpan < nnz ? e0 + kExpandSpan : nnz;
+    // largest r < n_rows with rowptr[r] <= e0; invariant rowptr[lo] <= e0, answer in [lo, hi)
+    int64_t lo = 0, hi = n_rows;
+    while (hi - lo > 1) {
+        const int64_t step = (hi - lo + kWave - 1) / kWave;
+        const int64_t p = lo + (int64_t)lane * step;
+        const uint64_t b = __ballot(p < hi && rowptr[p] <= e0);   // a prefix of the lanes
+        const int top = 63 - __clzll(b);                           // lane 0 always holds
+        lo += (int64_t)top * step;
+        hi = lo + step < hi ? lo + step : hi;
+    }
+    int64_t r0 = lo;
+    int rend = r0 + lane < n_rows ? rowptr[r0 + lane + 1] : INT32_MAX;
+    // kExpandEdges edges per lane per round: their lane searches are independent
+    // and interleave, which hides the latency of the cross-lane reads
+    for (int64_t c = e0; c < e1; c += (int64_t)kWave * kExpandEdges) {
+        int64_t e[kExpandEdges], row[kExpandEdges];
+        bool done[kExpandEdges];
+#pragma unroll
+        for (int j = 0; j < kExpandEdges; ++j) {
+            e[j] = c + (int64_t)j * kWave + lane;
+            done[j] = e[j] >= e1;
+            row[j] = 0;
+        }
+        for (;;) {
+            // rows before the window's first row end at or before every edge left
+            int k[kExpandEdges];
+#pragma unroll
+            for (int j = 0; j < kExpandEdges; ++j) k[j] = 0;
+#pragma unroll
+            for (int b = kWave / 2; b > 0; b >>= 1)
+#pragma unroll
+                for (int j = 0; j < kExpandEdges; ++j) {
+                    const int probe = __shfl(rend, k[j] + b - 1);
+                    if ((int64_t)probe <= e[j]) k[j] += b;
+                }
+            const int last_end = __shfl(rend, kWave - 1);
+            bool left = false;
+#pragma unroll
+            for (int j = 0; j < kExpandEdges; ++j) {
+                if (!done[j] && e[j] < (int64_t)last_end) {
+                    row[j] = r0 + k[j];
+                    done[j] = true;
+                }
+                left = left || !done[j];
+            }
+            if (__ballot(left) == 0) break;
+            r0 += kWave;
+            rend = r0 + lane < n_rows ? rowptr[r0 + lane + 1] : INT32_MAX;
+        }
+#pragma unroll
+        for (int j = 0; j < kExpandEdges; ++j)
+            if (e[j] < e1) row_of[e[j]] = (uint32_t)row[j];
     }
 }
 
-// colptr[c] = first slot whose key is >= c, from the sorted keys.
+// colptr[c] = first slot whose key is >= c, from the sorted keys; each thread
+// reads four consecutive keys with one 16-byte load.
 __global__ __launch_bounds__(kBlock) void k_colptr(const uint32_t *__restrict__ skeys, int64_t nnz,
                                                    int32_t n_cols, int32_t *__restrict__ colptr)
 {
-    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kBlock) {
-        const int64_t key = skeys[p];
-        const int64_t prev = p > 0 ? (int64_t)skeys[p - 1] : -1;
+    const int64_t q = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * 4;
+    if (q >= nnz) return;
+    uint32_t k[4];
+    if (q + 4 <= nnz) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(skeys + q);
+        k[0] = v.x; k[1] = v.y; k[2] = v.z; k[3] = v.w;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) k[i] = q + i < nnz ? skeys[q + i] : 0u;
+    }
+    int64_t prev = q > 0 ? (int64_t)skeys[q - 1] : -1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t p = q + i;
+        if (p >= nnz) break;
+        const int64_t key = k[i];
         for (int64_t c = prev + 1; c <= key; ++c) colptr[c] = (int32_t)p;
+        prev = key;
         if (p == nnz - 1)
             for (int64_t c = key + 1; c <= n_cols; ++c) colptr[c] = (int32_t)nnz;
     }
@@ -64,13 +139,6 @@ CscLayout csc_layout(int64_t nnz)
     return L;
 }
 
-unsigned grid_for(int64_t n, int per_block)
-{
-    int64_t b = (n + per_block - 1) / per_block;
-    if (b > 16384) b = 16384;
-    if (b < 1) b = 1;
-    return (unsigned)b;
-}
 
 }  // namespace
 }  // namespace cogdl
@@ -111,8 +179,10 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
     uint32_t *ping_v = reinterpret_cast<uint32_t *>(ws + L.ping_v);
     uint32_t *skeys = reinterpret_cast<uint32_t *>(ws + L.skeys);
 
-    COGDL_LAUNCH("csc_expand_rows", k_expand_rows, grid_for(n_rows, kBlock / kWave), kBlock, stream,
-                 rowptr, n_rows, row_of);
+    const int64_t waves = (nnz + kExpandSpan - 1) / kExpandSpan;
+    COGDL_LAUNCH("csc_expand_rows", k_expand_rows,
+                 (unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)), kBlock, stream, rowptr,
+                 n_rows, nnz, row_of);
     const int bits = bits_for((uint64_t)(n_cols - 1));
     RadixPayload vals;
     if (val) {
@@ -133,8 +203,8 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
                                        reinterpret_cast<uint32_t *>(row_t), nnz, bits, ping_k, ping_v,
                                        ws + L.radix, stream, vals, RadixPayload{}));
     }
-    COGDL_LAUNCH("csc_colptr", k_colptr, grid_for(nnz, kBlock), kBlock, stream, skeys, nnz, n_cols,
-                 colptr);
+    COGDL_LAUNCH("csc_colptr", k_colptr, (unsigned)((nnz + 4 * kBlock - 1) / (4 * kBlock)), kBlock,
+                 stream, skeys, nnz, n_cols, colptr);
     return COGDL_OK;
 }
 

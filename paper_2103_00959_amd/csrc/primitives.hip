@@ -97,17 +97,22 @@ __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v)
 
 // Per-tile histogram of one digit (bits [shift, shift + dbits) of the key),
 // stored digit-major so that an exclusive scan of the whole table yields every
-// (digit, tile) start slot.  Each wavefront counts into its own LDS copy.
+// (digit, tile) start slot.  Each wavefront counts into kHistCopies LDS copies
+// (lane % kHistCopies picks one), so the lanes of a wavefront that share a
+// digit, common on the high digits of power-law keys, collide on one LDS
+// address a quarter as often.
+constexpr int kHistCopies = 4;
+
 __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__restrict__ keys, int64_t n,
                                                            int shift, int dbits, int n_tiles,
                                                            int32_t *__restrict__ hist)
 {
-    constexpr int kWaves = kSortBlock / kWave;
-    __shared__ int32_t h[kWaves][kDigits];
+    constexpr int kCopies = (kSortBlock / kWave) * kHistCopies;
+    __shared__ int32_t h[kCopies][kDigits];
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) h[w][threadIdx.x] = 0;
+    for (int w = 0; w < kCopies; ++w) h[w][threadIdx.x] = 0;
     __syncthreads();
-    const int wv = threadIdx.x / kWave;
+    const int copy = (threadIdx.x / kWave) * kHistCopies + lane_id() % kHistCopies;
     const uint32_t mask = (1u << dbits) - 1u;
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
     uint32_t key[kSortItems];
@@ -119,13 +124,13 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__res
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
         const int64_t e = base + (int64_t)i * kSortBlock + threadIdx.x;
-        if (e < n) atomicAdd(&h[wv][(key[i] >> shift) & mask], 1);
+        if (e < n) atomicAdd(&h[copy][(key[i] >> shift) & mask], 1);
     }
     __syncthreads();
     if (threadIdx.x < (1 << dbits)) {
         int c = 0;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) c += h[w][threadIdx.x];
+        for (int w = 0; w < kCopies; ++w) c += h[w][threadIdx.x];
         hist[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = c;
     }
 }
