@@ -32,6 +32,9 @@
  *     leaves every output untouched.
  *   - The library trusts the device contents (rowptr[n_rows] == nnz, columns
  *     in range): it does not read device memory to check them.
+ *   - Edge ids are int32: nnz may be at most COGDL_MAX_NNZ (2^31 - 4097, which
+ *     leaves room for one batch of indices past the last edge); a larger nnz
+ *     gives COGDL_ERR_TOO_LARGE.
  *   - A failed launch returns COGDL_ERR_LAUNCH; a device fault surfaces at the
  *     caller's next synchronization.  No C++ exception crosses this ABI.
  *
@@ -64,6 +67,8 @@ typedef enum {
     COGDL_ERR_LAUNCH = 5,    /* a kernel launch or HIP runtime call failed */
     COGDL_ERR_TOO_LARGE = 6  /* a size exceeds what the int32 index format can hold */
 } cogdl_status;
+
+#define COGDL_MAX_NNZ 2147479551LL   /* 2^31 - 4097 */
 
 typedef enum { COGDL_F32 = 0, COGDL_BF16 = 1, COGDL_F16 = 2 } cogdl_dtype;
 

@@ -28,6 +28,7 @@ COGDL_F32, COGDL_BF16, COGDL_F16 = 0, 1, 2
 BALANCE = {"auto": 0, "row_split": 1, "neighbor_group": 2}
 MODE_NAMES = {1: "row_split", 2: "neighbor_group"}
 MAX_HEADS = 64
+MAX_NNZ = 2**31 - 4097     # COGDL_MAX_NNZ: int32 edge ids with room for one batch past the end
 
 _lib = None
 

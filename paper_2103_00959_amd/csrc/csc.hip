@@ -150,7 +150,7 @@ extern "C" {
 cogdl_status cogdl_csr_to_csc_workspace(int32_t n_rows, int32_t n_cols, int64_t nnz, size_t *bytes)
 {
     if (!bytes || n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
-    if (nnz > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (nnz > COGDL_MAX_NNZ) return COGDL_ERR_TOO_LARGE;
     *bytes = csc_layout(nnz).total;
     return COGDL_OK;
 }
@@ -161,7 +161,7 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
                               size_t workspace_bytes, hipStream_t stream)
 {
     if (n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
-    if (nnz > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (nnz > COGDL_MAX_NNZ) return COGDL_ERR_TOO_LARGE;
     if (!colptr) return COGDL_ERR_INVALID;
     if (n_rows > 0 && !rowptr) return COGDL_ERR_INVALID;
     if (nnz > 0 && (!col || !row_t || n_rows == 0 || n_cols == 0)) return COGDL_ERR_INVALID;

@@ -452,7 +452,7 @@ cogdl_status check_heads(int32_t n_rows, int32_t n_cols, int64_t nnz, const int3
 {
     if (n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
     if (H < 1 || H > COGDL_MAX_HEADS || D < 1) return COGDL_ERR_INVALID;
-    if (nnz > INT32_MAX || (int64_t)H * D > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (nnz > COGDL_MAX_NNZ || (int64_t)H * D > INT32_MAX) return COGDL_ERR_TOO_LARGE;
     if (n_rows > 0 && !rowptr) return COGDL_ERR_INVALID;
     if (nnz > 0 && (!col || n_rows == 0 || n_cols == 0)) return COGDL_ERR_INVALID;
     return COGDL_OK;

@@ -211,7 +211,7 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
         (mode != COGDL_BALANCE_AUTO && mode != COGDL_BALANCE_ROW_SPLIT &&
          mode != COGDL_BALANCE_NEIGHBOR_GROUP))
         return COGDL_ERR_INVALID;
-    if (nnz > INT32_MAX || n_rows == INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (nnz > COGDL_MAX_NNZ || n_rows == INT32_MAX) return COGDL_ERR_TOO_LARGE;
     if (n_rows == 0 && nnz != 0) return COGDL_ERR_INVALID;
     int32_t G = group_size;
     if (G == 0) {

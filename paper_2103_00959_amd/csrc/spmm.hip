@@ -206,7 +206,7 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     if (!dtype_ok(xdt) || !dtype_ok(ydt)) return COGDL_ERR_DTYPE;
     const bool maxr = reduce == COGDL_REDUCE_MAX;
     if (maxr && ydt != COGDL_F32 && ydt != xdt) return COGDL_ERR_DTYPE;
-    if (nnz > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    if (nnz > COGDL_MAX_NNZ) return COGDL_ERR_TOO_LARGE;
     if (out_rows > 0 && !ptr) return COGDL_ERR_INVALID;
     if (nnz > 0 && (!idx || out_rows == 0 || in_rows == 0)) return COGDL_ERR_INVALID;
     if (out_rows > 0 && F > 0 && !Y) return COGDL_ERR_INVALID;

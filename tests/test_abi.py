@@ -43,6 +43,29 @@ def test_status_strings_and_version(L):
     assert L.cogdl_version() >= 100
 
 
+def _max_nnz():
+    m = re.search(r"#define COGDL_MAX_NNZ (\d+)LL", open(HEADER).read())
+    return int(m.group(1))
+
+
+def test_max_nnz_limit(L):
+    """Edge counts above COGDL_MAX_NNZ (2^31 - 4097) are refused by every entry point that
+    takes one: int32 edge ids need room for a batch of indices past the last edge."""
+    import paper_2103_00959_amd as cgm
+    big = _max_nnz() + 1
+    assert big == (1 << 31) - 4096 and cgm.MAX_NNZ == big - 1
+    b = ctypes.c_size_t(0)
+    h = ctypes.c_void_p()
+    assert L.cogdl_spmm(2, 2, big, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == TOO_LARGE
+    assert L.cogdl_spmm_t(2, 2, big, FAKE, FAKE, None, 4, FAKE, 0, FAKE, 0, None, None) == TOO_LARGE
+    assert L.cogdl_csr_to_csc_workspace(10, 10, big, ctypes.byref(b)) == TOO_LARGE
+    assert L.cogdl_csr_to_csc_workspace(10, 10, big - 1, ctypes.byref(b)) == OK
+    assert L.cogdl_plan_create(4, big, FAKE, 16, 0, 0, 0, None, ctypes.byref(h)) == TOO_LARGE
+    assert L.cogdl_sddmm_dot(2, 2, big, FAKE, FAKE, 2, 4, FAKE, 0, FAKE, 0, FAKE, None, None) == TOO_LARGE
+    assert L.cogdl_sddmm_edge_softmax(2, 2, big, FAKE, FAKE, 2, FAKE, FAKE, ctypes.c_float(0.2), FAKE,
+                                      None, None) == TOO_LARGE
+
+
 def test_trace_filter_validation(L):
     # the filter is host state only: no device is touched
     L.cogdl_trace_filter.argtypes = [ctypes.c_char_p]

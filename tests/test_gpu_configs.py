@@ -315,3 +315,84 @@ def test_features_beyond_4gib_use_64bit_gathers(cg):
                 plan.close()
     del xd
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_max_nnz_int32_edge_ids(cg):
+    """The largest edge count the int32 edge ids allow (2^31 - 4097 nonzeros, 8.6 GB per
+    edge array): the SpMM on sampled rows and SpMM^T on sampled columns against the oracle,
+    the transpose checked on every slot by its definition (column counts, each slot's column,
+    row and value bits, edge ids increasing inside a column, which together make perm a
+    permutation)."""
+    import torch
+    nnz = cg.MAX_NNZ
+    n_rows, n_cols, F = 1 << 20, 4093, 8
+    rng = np.random.default_rng(4242)
+    cuts = np.sort(rng.integers(0, nnz + 1, n_rows - 1))
+    cuts[:10] = 0                                          # rows 0..9 empty
+    rowptr = np.concatenate([[0], cuts, [nnz]]).astype(np.int64)
+    gen = torch.Generator(device="cuda").manual_seed(4243)
+    say(f"max nnz: {nnz} nonzeros, {n_rows} x {n_cols}")
+    rp = torch.from_numpy(rowptr.astype(np.int32)).cuda()
+    cl = torch.randint(0, n_cols, (nnz,), dtype=torch.int32, device="cuda", generator=gen)
+    vl = torch.rand(nnz, dtype=torch.float32, device="cuda", generator=gen)
+    xd = torch.randn(n_cols, F, dtype=torch.float32, device="cuda", generator=gen)
+    xh = xd.cpu().numpy()
+    # SpMM on the first, last, empty and random rows
+    rows = np.unique(np.concatenate([[0, 5, 10, 11, n_rows - 1], rng.choice(n_rows, 40, replace=False)]))
+    sub_ptr = np.concatenate([[0], np.cumsum(rowptr[rows + 1] - rowptr[rows])]).astype(np.int32)
+    sub_col = np.concatenate([cl[rowptr[r]:rowptr[r + 1]].cpu().numpy() for r in rows]).astype(np.int32)
+    sub_val = np.concatenate([vl[rowptr[r]:rowptr[r + 1]].cpu().numpy() for r in rows]).astype(np.float32)
+    plan = cg.Plan(rp, nnz, F)
+    try:
+        Y = cg.spmm(rp, cl, vl, xd, plan=plan)
+        Yr, Ar = oracle.spmm(sub_ptr, sub_col, sub_val, xh)
+        assert scaled_error(Y[torch.from_numpy(rows).cuda()], Yr, Ar) <= TOL_F32
+    finally:
+        plan.close()
+    del Y
+    # transpose
+    colptr, row_t, val_t, perm = cg.csr_to_csc(rp, cl, vl, n_cols)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    counts = torch.zeros(n_cols, dtype=torch.int64, device="cuda")
+    for ch in cl.split(1 << 27):
+        counts += torch.bincount(ch.long(), minlength=n_cols)
+    ref_ptr = torch.zeros(n_cols + 1, dtype=torch.int64, device="cuda")
+    ref_ptr[1:] = torch.cumsum(counts, 0)
+    assert torch.equal(colptr.long(), ref_ptr)
+    rp64 = rp.long()
+    last_col, last_edge = -1, -1
+    for s0 in range(0, nnz, 1 << 27):
+        s1 = min(s0 + (1 << 27), nnz)
+        slots = torch.arange(s0, s1, dtype=torch.int64, device="cuda")
+        cslot = torch.searchsorted(ref_ptr[1:], slots, right=True)
+        pc = perm[s0:s1].long()
+        assert int(pc.min()) >= 0 and int(pc.max()) < nnz
+        assert torch.equal(cl[pc].long(), cslot)
+        assert torch.equal(row_t[s0:s1].long(), torch.searchsorted(rp64[1:], pc, right=True))
+        assert torch.equal(val_t[s0:s1].view(torch.int32), vl[pc].view(torch.int32))
+        same = cslot[1:] == cslot[:-1]
+        assert bool((pc[1:][same] > pc[:-1][same]).all())
+        if int(cslot[0]) == last_col:
+            assert int(pc[0]) > last_edge
+        last_col, last_edge = int(cslot[-1]), int(pc[-1])
+        del slots, cslot, pc, same
+    say("max nnz: transpose verified on every slot")
+    # SpMM^T on sampled columns: the oracle sums each column's edges in CSR order
+    G = torch.randn(n_rows, F, dtype=torch.float32, device="cuda", generator=gen)
+    gh = G.cpu().numpy()
+    plan_t = cg.Plan(colptr, nnz, F)
+    try:
+        dX = cg.spmm_t(colptr, row_t, val_t, G, plan_t=plan_t)
+        for j in (0, 1, n_cols // 2, n_cols - 1):
+            edges = torch.nonzero(cl == j).flatten()
+            r = torch.searchsorted(rp64[1:], edges, right=True).cpu().numpy().astype(np.int32)
+            v = vl[edges].cpu().numpy()
+            ptr1 = np.array([0, r.size], np.int32)
+            yr, ar = oracle.spmm(ptr1, r, v, gh)
+            assert scaled_error(dX[j:j + 1], yr, ar) <= TOL_F32, j
+    finally:
+        plan_t.close()
+    del cl, vl, colptr, row_t, val_t, perm, G
+    torch.cuda.empty_cache()
