@@ -38,8 +38,11 @@ __device__ __forceinline__ uint4 philox4(uint64_t seed, uint64_t c)
     uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
 #pragma unroll
     for (int round = 0; round < 10; ++round) {
-        const uint32_t hi0 = __umulhi(0xD2511F53u, c0), lo0 = 0xD2511F53u * c0;
-        const uint32_t hi1 = __umulhi(0xCD9E8D57u, c2), lo1 = 0xCD9E8D57u * c2;
+        // each 32 x 32 -> 64-bit product in one instruction (v_mad_u64_u32)
+        // instead of separate high and low multiplies
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0, p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
         const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
         c0 = n0;
         c1 = lo1;
@@ -62,14 +65,12 @@ __device__ __forceinline__ float uniform24(uint32_t r) { return (float)(r >> 8) 
 
 __device__ __forceinline__ float wave_min(float v)
 {
-    for (int off = 1; off < kWave; off <<= 1) v = fminf(v, lane_xor(v, off));
-    return v;
+    return group_reduce(v, kWave, [](float a, float b) { return fminf(a, b); });
 }
 
 __device__ __forceinline__ float wave_max(float v)
 {
-    for (int off = 1; off < kWave; off <<= 1) v = fmaxf(v, lane_xor(v, off));
-    return v;
+    return group_reduce(v, kWave, [](float a, float b) { return fmaxf(a, b); });
 }
 
 struct CodecArgs {
@@ -171,6 +172,16 @@ cogdl_status check_codec(int64_t n, int32_t F, int32_t bits, int32_t group)
     return COGDL_OK;
 }
 
+// Workgroups for `waves` wavefronts of work, at most what fits on the chip at once.
+unsigned resident_grid(const void *kernel, int64_t waves)
+{
+    int64_t b = (waves + (kBlock / kWave) - 1) / (kBlock / kWave);
+    const int64_t res = resident_blocks(kernel, kBlock);
+    if (b > res) b = res;
+    if (b < 1) b = 1;
+    return (unsigned)b;
+}
+
 unsigned codec_grid(int64_t groups)
 {
     int64_t b = (groups + (kBlock / kWave) - 1) / (kBlock / kWave);
@@ -185,12 +196,7 @@ unsigned codec_grid(int64_t groups)
 // lanes (8 to 64) holding NV vectors each, so a wavefront reads and writes
 // full 16-byte vectors and covers 64 / LG groups at a time.  A 64-feature
 // block of codes is 8 lanes: each contributes one byte per bit plane (its 8
-// codes), and the bytes are combined with three lane-exchange additions.
-
-__device__ __forceinline__ uint32_t lane_xor_u32(uint32_t v, int mask)
-{
-    return (uint32_t)__builtin_amdgcn_ds_bpermute((lane_id() ^ mask) << 2, (int)v);
-}
+// codes), and the bytes are combined by a three-level butterfly sum.
 
 template <typename T> struct Vec8;
 template <> struct Vec8<bf16_t> {
@@ -245,10 +251,8 @@ __global__ __launch_bounds__(kBlock) void k_compress_v(CodecArgs a)
                 hi = fmaxf(hi, gok ? x[v][e] : -INFINITY);
             }
         }
-        for (int off = 1; off < LG; off <<= 1) {
-            lo = fminf(lo, lane_xor(lo, off));
-            hi = fmaxf(hi, lane_xor(hi, off));
-        }
+        lo = group_reduce(lo, LG, [](float u, float v) { return fminf(u, v); });
+        hi = group_reduce(hi, LG, [](float u, float v) { return fmaxf(u, v); });
         const float range = hi - lo;
         const float s = range > 0.f ? qmax / range : 0.f;
         const float r = range > 0.f ? range / qmax : 0.f;
@@ -281,11 +285,9 @@ __global__ __launch_bounds__(kBlock) void k_compress_v(CodecArgs a)
                 // bytes 0-3 of the plane in the low word, 4-7 in the high word
                 uint32_t wlo = byte < 4 ? frag << (8 * byte) : 0u;
                 uint32_t whi = byte >= 4 ? frag << (8 * (byte - 4)) : 0u;
-#pragma unroll
-                for (int off = 1; off < 8; off <<= 1) {
-                    wlo += lane_xor_u32(wlo, off);
-                    whi += lane_xor_u32(whi, off);
-                }
+                const auto add = [](uint32_t u, uint32_t v) { return u + v; };
+                wlo = group_reduce(wlo, 8, add);
+                whi = group_reduce(whi, 8, add);
                 if (gok && byte == 0) w[(int64_t)blk * a.bits + p] = ((uint64_t)whi << 32) | wlo;
             }
         }
@@ -306,17 +308,42 @@ __global__ __launch_bounds__(kBlock) void k_decompress_v(int64_t n, int bits, in
     const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
     const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave) * per_wave;
     const int nb = G / kWave;
-    for (int64_t g = wave * per_wave + lane / LG; g - lane / LG < groups; g += stride) {
-        if (g >= groups) continue;
-        const float m = stats[2 * g], r = stats[2 * g + 1];
-        const uint64_t *__restrict__ w = codes + g * (int64_t)nb * bits;
+    const int byte = sl & 7;   // this lane's byte of each plane word of its block
+    const uint32_t *__restrict__ c32 = reinterpret_cast<const uint32_t *>(codes);
+    // a group's stats and, per vector and plane, the 32-bit half of the plane
+    // word that holds this lane's byte; fetched one group ahead
+    const auto fetch = [&](int64_t g, float &m, float &r, uint32_t (&h)[NV][8]) {
+        m = stats[2 * g];
+        r = stats[2 * g + 1];
+        const int64_t w0 = g * (int64_t)nb * bits;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
             const int blk = (v * LG + sl) / 8;
-            const int byte = sl & 7;
+#pragma unroll
+            for (int p = 0; p < 8; ++p)
+                h[v][p] = p < bits ? c32[2 * (w0 + (int64_t)blk * bits + p) + (byte >> 2)] : 0u;
+        }
+    };
+    int64_t g = wave * per_wave + lane / LG;
+    float mn = 0.f, rn = 0.f;
+    uint32_t hn[NV][8] = {};
+    if (g < groups) fetch(g, mn, rn, hn);
+    for (; g - lane / LG < groups; g += stride) {
+        const bool gok = g < groups;
+        const float m = mn, r = rn;
+        uint32_t h[NV][8];
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int p = 0; p < 8; ++p) h[v][p] = hn[v][p];
+        if (g + stride < groups) fetch(g + stride, mn, rn, hn);
+        if (!gok) continue;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
             uint32_t q[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-            for (int p = 0; p < bits; ++p) {
-                const uint32_t b8 = (uint32_t)(w[(int64_t)blk * bits + p] >> (8 * byte)) & 0xffu;
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                const uint32_t b8 = (h[v][p] >> (8 * (byte & 3))) & 0xffu;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) q[e] |= ((b8 >> e) & 1u) << p;
             }
@@ -379,10 +406,12 @@ cogdl_status cogdl_act_compress(int64_t n, int32_t F, const void *A, cogdl_dtype
     const int nv = vector_nv(F, group, A);
     if (nv > 0) {
         const int per_wave = kWave / (group / (8 * nv));
-        const unsigned bv = codec_grid((n * a.ng + per_wave - 1) / per_wave);
         CompressKernel k = a_dtype == COGDL_F32    ? pick_compress_v<float>(nv)
                            : a_dtype == COGDL_BF16 ? pick_compress_v<bf16_t>(nv)
                                                    : pick_compress_v<f16_t>(nv);
+        // a grid past the resident size, no prefetch: a resident grid walking the
+        // groups with the next one fetched ahead measured 10-15% slower here
+        const unsigned bv = codec_grid((n * a.ng + per_wave - 1) / per_wave);
         COGDL_LAUNCH("act_compress", k, bv, kBlock, stream, a);
         return COGDL_OK;
     }
@@ -409,21 +438,14 @@ cogdl_status cogdl_act_decompress(int64_t n, int32_t F, int32_t bits, int32_t gr
     const int nv = vector_nv(F, group, out);
     if (nv > 0) {
         const int per_wave = kWave / (group / (8 * nv));
-        const unsigned bv = codec_grid((n * ng + per_wave - 1) / per_wave);
+        const int64_t wv = (n * ng + per_wave - 1) / per_wave;
 #define COGDL_DECOMP_V(TO)                                                                       \
     do {                                                                                         \
-        if (nv == 1)                                                                             \
-            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 1>), bv, kBlock, stream, n, bits,  \
-                         group, ng, codes, stats, static_cast<TO *>(out));                       \
-        else if (nv == 2)                                                                        \
-            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 2>), bv, kBlock, stream, n, bits,  \
-                         group, ng, codes, stats, static_cast<TO *>(out));                       \
-        else if (nv == 4)                                                                        \
-            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 4>), bv, kBlock, stream, n, bits,  \
-                         group, ng, codes, stats, static_cast<TO *>(out));                       \
-        else                                                                                     \
-            COGDL_LAUNCH("act_decompress", (k_decompress_v<TO, 8>), bv, kBlock, stream, n, bits,  \
-                         group, ng, codes, stats, static_cast<TO *>(out));                       \
+        auto k = nv == 1 ? k_decompress_v<TO, 1> : nv == 2 ? k_decompress_v<TO, 2>              \
+                 : nv == 4 ? k_decompress_v<TO, 4> : k_decompress_v<TO, 8>;                     \
+        const unsigned bv = resident_grid(reinterpret_cast<const void *>(k), wv);                \
+        COGDL_LAUNCH("act_decompress", k, bv, kBlock, stream, n, bits, group, ng, codes, stats,  \
+                     static_cast<TO *>(out));                                                    \
     } while (0)
         if (out_dtype == COGDL_F32) COGDL_DECOMP_V(float);
         else if (out_dtype == COGDL_BF16) COGDL_DECOMP_V(bf16_t);

@@ -302,6 +302,57 @@ __device__ __forceinline__ float lane_xor(float v, int mask)
     return __int_as_float(__builtin_amdgcn_ds_bpermute((lane_id() ^ mask) << 2, __float_as_int(v)));
 }
 
+// Butterfly reductions over the G adjacent lanes of a group (G a power of two
+// up to 64, groups aligned to G): every lane ends with its group's reduction,
+// and partners pair up exactly as in a lane ^ 1, ^ 2, ..., ^ G/2 butterfly.
+// Levels 1 and 2 are DPP quad permutes (lane ^ 1, lane ^ 2); levels 4 and 8 the
+// DPP mirrors within 8 and 16 lanes (lane 7 - i, 15 - i), which once the lower
+// levels have made each half of the span uniform hold the same value as lane
+// ^ 4 / lane ^ 8; level 16 a swizzle (lane ^ 16 inside 32 lanes); level 32
+// ds_bpermute.  DPP moves do not go through the LDS crossbar, so a reduction
+// costs a few cycles per level instead of an LDS round trip.  Every lane of a
+// group must be active.
+template <int OFF>
+__device__ __forceinline__ int bfly_partner(int v)
+{
+    if constexpr (OFF == 1) return __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false);
+    else if constexpr (OFF == 2) return __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false);
+    else if constexpr (OFF == 4) return __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false);
+    else if constexpr (OFF == 8) return __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false);
+    else if constexpr (OFF == 16) return __builtin_amdgcn_ds_swizzle(v, 0x401F);
+    else return __builtin_amdgcn_ds_bpermute((lane_id() ^ OFF) << 2, v);
+}
+
+template <int OFF>
+__device__ __forceinline__ float bfly_partner(float v)
+{
+    return __int_as_float(bfly_partner<OFF>(__float_as_int(v)));
+}
+
+template <int OFF>
+__device__ __forceinline__ uint32_t bfly_partner(uint32_t v)
+{
+    return (uint32_t)bfly_partner<OFF>((int)v);
+}
+
+// Reduce v over groups of G lanes (G uniform across the wavefront) with op.
+template <typename T, typename Op>
+__device__ __forceinline__ T group_reduce(T v, int G, Op op)
+{
+    if (G > 1) v = op(v, bfly_partner<1>(v));
+    if (G > 2) v = op(v, bfly_partner<2>(v));
+    if (G > 4) v = op(v, bfly_partner<4>(v));
+    if (G > 8) v = op(v, bfly_partner<8>(v));
+    if (G > 16) v = op(v, bfly_partner<16>(v));
+    if (G > 32) v = op(v, bfly_partner<32>(v));
+    return v;
+}
+
+__device__ __forceinline__ float group_sum(float v, int G)
+{
+    return group_reduce(v, G, [](float a, float b) { return a + b; });
+}
+
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // Merge two online-softmax states (m, z): the pair describing

@@ -167,10 +167,8 @@ __global__ __launch_bounds__(kBlock) void k_head_scores(int64_t n, int H, int D,
                 ps = fmaf(z[0], a_src[(int64_t)h * D + d], ps);
                 pd = fmaf(z[0], a_dst[(int64_t)h * D + d], pd);
             }
-            for (int off = 1; off < kWave; off <<= 1) {
-                ps += lane_xor(ps, off);
-                pd += lane_xor(pd, off);
-            }
+            ps = group_sum(ps, kWave);
+            pd = group_sum(pd, kWave);
             if (lane == 0) {
                 if (s_src) s_src[node * H + h] = ps;
                 if (s_dst) s_dst[node * H + h] = pd;

@@ -170,10 +170,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 }
                 // complete the dot products over the head's lanes (every lane of
                 // the head ends with the same bits: each level adds the same pair)
-                for (int off = 1; off < L; off <<= 1) {
 #pragma unroll
-                    for (int t = 0; t < U; ++t) pd[t] += lane_xor(pd[t], off);
-                }
+                for (int t = 0; t < U; ++t) pd[t] = group_sum(pd[t], L);
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
                     const int64_t k = k0 + j + t;
@@ -218,7 +216,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                         }
                     }
                 }
-                for (int off = 1; off < L; off <<= 1) sdt += lane_xor(sdt, off);
+                sdt = group_sum(sdt, L);
                 if (act && q == 0) a.ds_dst[(int64_t)row * H + h] = sdt;
             }
         }

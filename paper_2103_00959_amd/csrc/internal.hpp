@@ -11,7 +11,7 @@
 
 namespace cogdl {
 
-// Work unit: rows [beg, end) of one row, reduced either straight into the
+// Work unit: edges [beg, end) of one row, reduced either straight into the
 // output (part < 0) or into partial-sum slot `part`.
 // Layout int4 {row, beg, end, part}.
 
