@@ -42,7 +42,6 @@ struct SoftArgs {
     float *gstats;
     int32_t sstride;
     int32_t log2S;              // k_softmax: lanes per unit
-    int32_t parked;             // k_alpha_split: alpha holds the raw scores of split rows
     const int4 *part_units;     // k_alpha_split: {row, beg, end, split}
     const int32_t *n_parts;
     const float *rstats;        // per split row: m[max_heads], z[max_heads]
@@ -238,8 +237,8 @@ __global__ __launch_bounds__(kBlock) void k_softmax_merge(const int4 *__restrict
     }
 }
 
-// alpha for the edges of split rows, one wavefront per neighbour group: from
-// the raw scores k_softmax parked in alpha, or by gathering the scores again.
+// alpha for the edges of split rows, one wavefront per neighbour group, from
+// the raw scores that k_softmax or k_gat parked in alpha.
 __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
 {
     const int lane = lane_id();
@@ -254,25 +253,7 @@ __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
         const int4 d = a.part_units[p];
         const float m = a.rstats[(int64_t)d.w * a.sstride + h];
         const float rz = 1.f / a.rstats[(int64_t)d.w * a.sstride + (a.sstride >> 1) + h];
-        if (a.parked) {
-            constexpr int R = 8;
-            for (int k0 = d.y + slot; k0 < d.z; k0 += R * eps) {
-                float e[R];
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const int k = k0 + r * eps;
-                    e[r] = k < d.z ? a.alpha[(int64_t)k * H + h] : 0.f;
-                }
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const int k = k0 + r * eps;
-                    if (k < d.z) a.alpha[(int64_t)k * H + h] = __expf(e[r] - m) * rz;
-                }
-            }
-        } else {
-            const float sd = a.s_dst[(int64_t)d.x * H + h];
-            alpha_sweep<8>(a.col, a.s_src, a.alpha, H, h, sd, a.slope, m, rz, d.y, d.z, slot, eps);
-        }
+        alpha_from_parked<8>(a.alpha, H, h, m, rz, d.y, d.z, slot, eps);
     }
 }
 
@@ -430,7 +411,6 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
         return COGDL_OK;
     };
     a.log2S = 6;
-    a.parked = 1;
     if (!P) a.u_hi = nullptr;
     st = launch("softmax", k_softmax<8>, a);
     if (st != COGDL_OK) return st;

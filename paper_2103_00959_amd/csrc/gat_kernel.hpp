@@ -52,31 +52,25 @@ __device__ __forceinline__ int4 fetch_gat_unit(const GatArgs &a, int64_t u, int6
     return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
 }
 
-// alpha[k, h] = exp(e_kh - m) * rz for the edges k = beg + slot + j * slots
-// of one head h, R gathers in flight per lane: the column indices of R edges
-// are loaded together (clamped to the last edge), then their R source scores,
-// then the R results are stored.
+// alpha[k, h] = exp(e_kh - m) * rz for the edges k = beg + slot + j * slots of
+// one head h, R loads in flight per lane; the raw scores e_kh are read from
+// alpha itself, where the aggregation or the softmax parked them (a contiguous
+// re-read instead of a second random gather of s_src).
 template <int R>
-__device__ __forceinline__ void alpha_sweep(const int32_t *__restrict__ col,
-                                            const float *__restrict__ s_src,
-                                            float *__restrict__ alpha, int H, int h, float sd,
-                                            float slope, float m, float rz, int beg, int end,
-                                            int slot, int slots)
+__device__ __forceinline__ void alpha_from_parked(float *__restrict__ alpha, int H, int h, float m,
+                                                  float rz, int beg, int end, int slot, int slots)
 {
     for (int k0 = beg + slot; k0 < end; k0 += R * slots) {
-        int cc[R];
+        float e[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int k = k0 + r * slots;
-            cc[r] = col[k < end ? k : end - 1];
+            e[r] = k < end ? alpha[(int64_t)k * H + h] : 0.f;
         }
-        float sv[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) sv[r] = s_src[(int64_t)cc[r] * H + h];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int k = k0 + r * slots;
-            if (k < end) alpha[(int64_t)k * H + h] = __expf(leaky_relu(sd + sv[r], slope) - m) * rz;
+            if (k < end) alpha[(int64_t)k * H + h] = __expf(e[r] - m) * rz;
         }
     }
 }
@@ -84,8 +78,11 @@ __device__ __forceinline__ void alpha_sweep(const int32_t *__restrict__ col,
 // BWD = true: the backward pass of the aggregation, run on the CSC of the
 // graph (rows of this launch = source nodes): the weights are the forward
 // alpha through perm, and each row also sums dscore (through perm) per head.
+// The one-chunk forward variants are held to 128 VGPRs (4 wavefronts per SIMD,
+// the occupancy their loop reaches without the bound), so that parking alpha
+// does not cost a wavefront of latency hiding.
 template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD>
-__global__ __launch_bounds__(kGatBlock) void k_gat(GatArgs a)
+__global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k_gat(GatArgs a)
 {
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
     const int log2S = a.log2S;
@@ -188,6 +185,13 @@ __global__ __launch_bounds__(kGatBlock) void k_gat(GatArgs a)
                             w[t][c] = (ok[t] && act[c]) ? leaky_relu(sd[c] + w[t][c], a.slope) : -INFINITY;
                             mb = fmaxf(mb, w[t][c]);
                         }
+                        // alpha wanted: park the raw scores, one lane per head and edge
+                        // (the lane of the head's first feature in this slab)
+                        if (a.alpha_out != nullptr && act[c] && fe[c] % a.D == 0) {
+#pragma unroll
+                            for (int t = 0; t < U; ++t)
+                                if (ok[t]) a.alpha_out[(int64_t)(k0 + j + t) * H + hd[c]] = w[t][c];
+                        }
                         if (mb > m[c]) {
                             const float r = __expf(m[c] - mb);
                             z[c] *= r;
@@ -277,9 +281,12 @@ __global__ __launch_bounds__(kGatBlock) void k_gat(GatArgs a)
                     const float rr = lane_bcast(rz[c], gbase + src_l);
                     if (c == src_c) { m1 = mm; r1 = rr; }
                 }
+                // the scores were parked by other lanes of this wavefront: wait for
+                // those stores before reading them back
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
                 if (mine_head && slot < eps)
-                    alpha_sweep<4>(col, a.s_src, a.alpha_out, H, h1, a.s_dst[(int64_t)row * H + h1],
-                                   a.slope, m1, r1, beg, end, slot, eps);
+                    alpha_from_parked<4>(a.alpha_out, H, h1, m1, r1, beg, end, slot, eps);
             }
         }
         if (un >= hi) break;
