@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--alpha-out", action="store_true", help="also write alpha in the GAT step")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the steps, copy a buffer of this many MiB (counter calibration)")
+    ap.add_argument("--workloads", action="store_true",
+                    help="instead of the step: time each workload's own operators (workloads 1-4 "
+                         "in their own dtypes), cold and warm, one JSON line per workload and op")
     return ap.parse_args()
 
 
@@ -225,12 +228,121 @@ def run_inference(cg, synth, dev, time_op_kernels):
     }
 
 
+def run_workloads(reps=20, warm_reps=3):
+    """Each workload's operators in its own configuration (fp32 features; plans on AUTO with
+    the default group size), one JSON line per (workload, op).  Cold: a 1 GiB buffer is
+    written before every timed call, so L2 and the Infinity Cache hold none of its inputs;
+    warm: the same call back to back.  Median and minimum of `reps` calls after `warm_reps`
+    untimed ones; plan creation and the transpose are preprocessing, reported on their own."""
+    import torch
+
+    import paper_2103_00959_amd as cg
+    from paper_2103_00959_amd import synth
+
+    dev = torch.device("cuda:0")
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+
+    def times(fn):
+        for _ in range(warm_reps):
+            fn()
+        cold, warm = [], []
+        for _ in range(reps):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            cold.append(e0.elapsed_time(e1))
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        evs[0].record()
+        for i in range(reps):
+            fn()
+            evs[i + 1].record()
+        torch.cuda.synchronize()
+        warm = [evs[i].elapsed_time(evs[i + 1]) for i in range(reps)]
+        return cold, warm
+
+    def record(k, cfg, op, B, E, cold, warm, note=None):
+        mc, mw = float(np.median(cold)), float(np.median(warm))
+        out = {"workload": cfg["name"], "config": k, "op": op, "algorithmic_GB": B / 1e9,
+               "cold_ms_median": mc, "cold_ms_min": min(cold),
+               "warm_ms_median": mw, "warm_ms_min": min(warm),
+               "cold_eff_GBps": B / (mc * 1e-3) / 1e9, "cold_pct_peak": B / (mc * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+               "warm_eff_GBps": B / (mw * 1e-3) / 1e9,
+               "cold_edges_per_s": E / (mc * 1e-3) if E else None}
+        if note:
+            out["note"] = note
+        print(json.dumps(out), flush=True)
+        log(f"{cfg['name']} {op}: cold {mc:.3f} ms ({out['cold_pct_peak'] * 100:.1f}% of peak), "
+            f"warm {mw:.3f} ms")
+
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)   # noqa: E731
+    for k in (1, 2, 3, 4):
+        cfg = synth.CONFIGS[k]
+        g = synth.config_graph(k, verbose=True)
+        N, M, E = g.n_rows, g.n_cols, g.nnz
+        rowptr, col = up(g.rowptr), up(g.col)
+        val = up(g.val) if g.val is not None else None
+        t0 = time.perf_counter()
+        plan = cg.Plan(rowptr, E, max_feat=max(cfg.get("F", 1), cfg.get("H", 1) * cfg.get("D", 1)),
+                       max_heads=cfg.get("H", 0))
+        torch.cuda.synchronize()
+        log(f"{cfg['name']}: plan created in {(time.perf_counter() - t0) * 1e3:.1f} ms (host clock)")
+        cold, warm = times(lambda: plan.rebuild(rowptr))
+        record(k, cfg, "plan_rebuild", b_plan(N, plan.info()["n_units"]), 0, cold, warm)
+        if "F" in cfg:
+            F = cfg["F"]
+            X = up(synth.normal_f32((M, F), 2000 + k))
+            Y = torch.empty((N, F), dtype=torch.float32, device=dev)
+            cold, warm = times(lambda: cg.spmm(rowptr, col, val, X, plan=plan, out=Y))
+            record(k, cfg, "spmm", b_spmm(N, M, E, F, 4, 4), E, cold, warm,
+                   note="X fits the 256 MB Infinity Cache" if M * F * 4 <= (256 << 20) else None)
+            if k == 2:
+                colptr, row_t, val_t, perm = cg.csr_to_csc(rowptr, col, val, M)
+                ws = torch.empty(cg.csr_to_csc_workspace(N, M, E), dtype=torch.uint8, device=dev)
+                cold, warm = times(lambda: cg.csr_to_csc(rowptr, col, val, M, workspace=ws))
+                record(k, cfg, "csr_to_csc", b_csc(N, M, E), E, cold, warm)
+                plan_t = cg.Plan(colptr, E, max_feat=F)
+                G = up(synth.normal_f32((N, F), 4000 + k))
+                dX = torch.empty((M, F), dtype=torch.float32, device=dev)
+                cold, warm = times(lambda: cg.spmm_t(colptr, row_t, val_t, G, plan_t=plan_t, out=dX))
+                record(k, cfg, "spmm_t", b_spmm(M, N, E, F, 4, 4), E, cold, warm)
+                plan_t.close()
+                del colptr, row_t, val_t, perm, ws, G, dX
+            del X, Y
+        if "H" in cfg:
+            H, D = cfg["H"], cfg["D"]
+            rng = np.random.default_rng(3000 + k)
+            s_dst = up(rng.standard_normal((N, H), dtype=np.float32))
+            s_src = up(rng.standard_normal((M, H), dtype=np.float32))
+            Xg = up(synth.normal_f32((M, H * D), 2100 + k)).view(M, H, D)
+            Yg = torch.empty((N, H, D), dtype=torch.float32, device=dev)
+            alpha = torch.empty((E, H), dtype=torch.float32, device=dev)
+            cold, warm = times(lambda: cg.sddmm_edge_softmax(rowptr, col, s_dst, s_src, 0.2, plan=plan,
+                                                             out=alpha))
+            record(k, cfg, "sddmm_edge_softmax",
+                   4 * (N + 1) + 4 * E + 4 * N * H + 4 * E * H + 4 * E * H, E, cold, warm)
+            for a_out in (False, True):
+                cold, warm = times(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
+                                                            out=Yg, alpha_out=alpha if a_out else None))
+                record(k, cfg, "gat_aggregate" + ("_alpha_out" if a_out else ""),
+                       b_gat(N, E, H, D, 4, 4, a_out), E, cold, warm)
+            del s_dst, s_src, Xg, Yg, alpha
+        plan.close()
+        del rowptr, col, val
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path has no "
               f"multi-GPU mode in this build", file=sys.stderr)
         sys.exit(2)
+    if args.workloads:
+        run_workloads()
+        return
     import torch
 
     import paper_2103_00959_amd as cg
