@@ -21,7 +21,8 @@
  * Memory and ownership
  *   - Every array argument is a DEVICE pointer owned by the caller; the
  *     library neither frees nor retains it.  Outputs are fully overwritten,
- *     never accumulated into.
+ *     never accumulated into, and must not overlap any input or each other
+ *     (an output may hold intermediate values before the call completes).
  *   - Only cogdl_plan_create allocates device memory and only
  *     cogdl_plan_destroy frees it.  The operator calls never allocate.
  *
