@@ -69,15 +69,23 @@ __device__ __forceinline__ int4 fetch_bwd_unit(const BwdArgs &a, int64_t u, int6
     return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
 }
 
-__device__ __forceinline__ float score_grad(float t, float slope, float al, float da, float c)
+// The score gradient of edge k and head h is f * alpha * (dalpha - c), with f
+// the LeakyReLU slope at the pre-activation t and c the row's sum of alpha *
+// dalpha.  Pass 1 parks u = f * alpha in dscore (c is not known yet); once c
+// is, dscore = u * (dalpha - c).
+__device__ __forceinline__ float park_value(float t, float slope, float al)
 {
-    return (t > 0.f ? 1.f : slope) * al * (da - c);
+    return (t > 0.f ? 1.f : slope) * al;
 }
+
+__device__ __forceinline__ float parked_grad(float u, float da, float c) { return u * (da - c); }
 
 // Pass 1, feature-parallel: one S-lane sub-group per unit, lane = VEC
 // consecutive features, head h on lanes [h L, (h + 1) L).  Requires one
 // chunk per lane (H * D <= S * VEC) and L a power of two.  Every edge k of a
-// unit is parked by lane q = (k - beg) mod M of its head, M = min(L, U).
+// unit is owned by lane q = (k - beg) mod M of its head, M = min(L, U): that
+// lane alone loads the edge's alpha and source score, adds its term of c, and
+// parks its dalpha and u; the head's lanes then add up their shares of c.
 template <typename TX, int VEC, bool BUF, bool DOT>
 __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 {
@@ -143,14 +151,20 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 float xv[PACKED ? 1 : U][VEC];
                 uint4 xw[PACKED ? U : 1];
                 float al[U], ss[U];
+                bool mine[U];
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
                     const bool on = ok[t] && act;
+                    mine[t] = on && writer && (t & (M - 1)) == q;
                     if constexpr (PACKED) xw[t] = X.load_raw16((int64_t)cc[t] * a.W + fe, on);
                     else X.load((int64_t)cc[t] * a.W + fe, on, xv[t]);
+                    al[t] = 0.f;
+                    ss[t] = 0.f;
                     if constexpr (!DOT) {
-                        al[t] = a.alpha[on ? (int64_t)(k0 + j + t) * H + h : 0];
-                        ss[t] = a.s_src[on ? (int64_t)cc[t] * H + h : 0];
+                        if (mine[t]) {
+                            al[t] = a.alpha[(int64_t)(k0 + j + t) * H + h];
+                            ss[t] = a.s_src[(int64_t)cc[t] * H + h];
+                        }
                     }
                 }
                 float pd[U];
@@ -175,10 +189,12 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
                     const int64_t k = k0 + j + t;
-                    if constexpr (!DOT) c += (ok[t] && act) ? al[t] * pd[t] : 0.f;
-                    if (ok[t] && writer && (t & (M - 1)) == q) {
+                    if (mine[t]) {
                         a.dalpha[k * H + h] = pd[t];
-                        if constexpr (!DOT) a.dscore[k * H + h] = sd + ss[t];
+                        if constexpr (!DOT) {
+                            c += al[t] * pd[t];
+                            a.dscore[k * H + h] = park_value(sd + ss[t], a.slope, al[t]);
+                        }
                     }
                 }
             }
@@ -188,6 +204,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
             (dn.z > dn.y) ? col[dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1] : 0;
 
         if constexpr (!DOT) {
+            // the head's lanes hold shares of c (owners only, the others 0)
+            c = group_sum(c, L);
             if (part >= 0) {
                 if (act && q == 0) a.gstats[(int64_t)part * a.sstride + h] = c;
             } else {
@@ -196,20 +214,19 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 float sdt = 0.f;
                 if (writer) {
                     for (int o0 = q; o0 < end - beg; o0 += R * M) {
-                        float da[R], tv[R], av[R];
+                        float da[R], uv[R];
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
                             const int64_t k = (int64_t)beg + (o < end - beg ? o : o0);
                             da[r] = a.dalpha[k * H + h];
-                            tv[r] = a.dscore[k * H + h];
-                            av[r] = a.alpha[k * H + h];
+                            uv[r] = a.dscore[k * H + h];
                         }
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
                             if (o < end - beg) {
-                                const float g = score_grad(tv[r], a.slope, av[r], da[r], c);
+                                const float g = parked_grad(uv[r], da[r], c);
                                 a.dscore[((int64_t)beg + o) * H + h] = g;
                                 sdt += g;
                             }
@@ -277,8 +294,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
                 }
                 a.dalpha[(int64_t)k * H + h] = s;
                 if constexpr (!DOT) {
-                    c += a.alpha[(int64_t)k * H + h] * s;
-                    a.dscore[(int64_t)k * H + h] = sd + a.s_src[(int64_t)j * H + h];
+                    const float al = a.alpha[(int64_t)k * H + h];
+                    c += al * s;
+                    a.dscore[(int64_t)k * H + h] = park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al);
                 }
             }
         }
@@ -292,7 +310,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
         if (live) {
             for (int k = beg + slot; k < end; k += eps) {
                 const int64_t i = (int64_t)k * H + h;
-                const float g = score_grad(a.dscore[i], a.slope, a.alpha[i], a.dalpha[i], c);
+                const float g = parked_grad(a.dscore[i], a.dalpha[i], c);
                 a.dscore[i] = g;
                 sdt += g;
             }
@@ -326,20 +344,19 @@ __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
         float sdt = 0.f;
         if (live) {
             for (int k0 = d.y + slot; k0 < d.z; k0 += R * eps) {
-                float da[R], tv[R], av[R];
+                float da[R], uv[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
                     const int64_t i = (int64_t)(k < d.z ? k : k0) * H + h;
                     da[r] = a.dalpha[i];
-                    tv[r] = a.dscore[i];
-                    av[r] = a.alpha[i];
+                    uv[r] = a.dscore[i];
                 }
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
                     if (k < d.z) {
-                        const float g = score_grad(tv[r], a.slope, av[r], da[r], c);
+                        const float g = parked_grad(uv[r], da[r], c);
                         a.dscore[(int64_t)k * H + h] = g;
                         sdt += g;
                     }
