@@ -1,4 +1,5 @@
-"""Host-side logic of bench.py that needs no GPU: the traffic record lookup."""
+"""Host-side logic of bench.py that needs no GPU: the traffic record lookup, the
+algorithmic-byte models and the one-GPU guard."""
 import json
 
 import bench
@@ -23,3 +24,28 @@ def test_recorded_traffic_lookup(tmp_path):
     rec["source_sha16"]["spmm_t"] = "0" * 16
     (prof / "wl_hbm_traffic.json").write_text(json.dumps(rec))
     assert bench.recorded_traffic("wl", "spmm_t", str(prof)) is None
+
+
+def test_byte_models_match_the_workload_table():
+    """The algorithmic-byte models reproduce the figures of the measurement table for the
+    workloads' sizes (GB, three significant digits as tabulated)."""
+    N5, E5 = 2_400_000, 122_400_000
+    assert round(bench.b_spmm(N5, N5, E5, 256, 2, 2) / 1e9, 1) == 64.9
+    assert round(bench.b_unique_spmm(N5, N5, E5, 256, 2, 2) / 1e9, 2) == 3.45
+    assert round(bench.b_gat(N5, E5, 4, 64, 2, 2, False) / 1e9, 1) == 66.4
+    N4, E4 = 2_449_029, 64_308_169
+    assert round(bench.b_gat(N4, E4, 8, 16, 4, 4, False) / 1e9, 1) == 36.6
+    assert round(bench.b_gat(N4, E4, 8, 16, 4, 4, True) / 1e9, 1) == 38.6
+    soft = 4 * (N4 + 1) + 4 * E4 + 4 * N4 * 8 + 8 * E4 * 8
+    assert round(soft / 1e9, 2) == 4.46
+    assert round(bench.b_spmm(169_343, 169_343, 2_501_829, 128, 4, 4) / 1e9, 3) == 1.388
+    assert round(bench.b_spmm(232_965, 232_965, 114_615_892, 256, 4, 4) / 1e9, 1) == 118.5
+
+
+def test_more_than_one_gpu_is_refused():
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
