@@ -80,9 +80,11 @@ void trace_end(int slot, hipStream_t s);
 
 // Exclusive prefix sum of n int32 values; out has n + 1 entries and out[n]
 // receives the total.  in and out may alias.  Workspace size from
-// scan_workspace_bytes(n).
-size_t scan_workspace_bytes(int64_t n);
+// scan_workspace_bytes(n, 1).  exclusive_scan3 scans three arrays of n + 1
+// entries in place with the launches of one (workspace scan_workspace_bytes(n, 3)).
+size_t scan_workspace_bytes(int64_t n, int arrays = 1);
 hipError_t exclusive_scan(const int32_t *in, int32_t *out, int64_t n, void *ws, hipStream_t s);
+hipError_t exclusive_scan3(int32_t *a0, int32_t *a1, int32_t *a2, int64_t n, void *ws, hipStream_t s);
 
 // An extra 32-bit array carried through a radix sort: read from `in`,
 // written in sorted order to `out`; `ping` is 2 * n elements of scratch.

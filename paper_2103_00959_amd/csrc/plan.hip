@@ -157,9 +157,7 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, hipStream_t s)
                  P.counters);
     COGDL_LAUNCH("plan_counts", k_plan_counts, blocks, 256, s, rowptr, n, P.group_size,
                  (int)P.mode_req, P.counters, P.row_units, P.row_parts, P.row_split);
-    COGDL_HIP_TRY(exclusive_scan(P.row_units, P.row_units, n, P.scan_ws, s));
-    COGDL_HIP_TRY(exclusive_scan(P.row_parts, P.row_parts, n, P.scan_ws, s));
-    COGDL_HIP_TRY(exclusive_scan(P.row_split, P.row_split, n, P.scan_ws, s));
+    COGDL_HIP_TRY(exclusive_scan3(P.row_units, P.row_parts, P.row_split, n, P.scan_ws, s));
     COGDL_LAUNCH("plan_emit", k_plan_emit, blocks, 256, s, rowptr, n, P.group_size, P.counters,
                  P.row_units, P.row_parts, P.row_split, P.units_tmp, P.sort_keys, P.split_rows,
                  P.part_units);
@@ -248,7 +246,7 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
     const size_t o_vals = take(4 * 3 * (size_t)P.cap_units);
     P.sort_ws_bytes = cogdl::radix_workspace_bytes(P.cap_units);
     const size_t o_sort_ws = take(P.sort_ws_bytes);
-    P.scan_ws_bytes = cogdl::scan_workspace_bytes(n_rows);
+    P.scan_ws_bytes = cogdl::scan_workspace_bytes(n_rows, 3);
     const size_t o_scan_ws = take(P.scan_ws_bytes);
     const size_t o_partials = take(sizeof(float) * (size_t)P.cap_partials * pstride);
     const size_t o_parg = take(sizeof(int32_t) * (size_t)P.cap_partials * pstride);

@@ -50,42 +50,60 @@ __device__ __forceinline__ int block_exclusive_scan(int x, int *total)
     return before + inc - x;
 }
 
-__global__ __launch_bounds__(kScanBlock) void k_tile_reduce(const int32_t *__restrict__ in, int64_t n,
-                                                            int32_t *__restrict__ tile_sums)
+// K arrays scanned side by side (one launch for all of them); sums of the
+// tiles of array k at tile_sums[k * stride + tile].
+template <int K>
+struct ScanSet {
+    const int32_t *in[K];
+    int32_t *out[K];
+};
+
+template <int K>
+__global__ __launch_bounds__(kScanBlock) void k_tile_reduce(ScanSet<K> a, int64_t n,
+                                                            int32_t *__restrict__ tile_sums,
+                                                            int64_t stride)
 {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-    int s = 0;
 #pragma unroll
-    for (int i = 0; i < kScanItems; ++i)
-        if (base + i < n) s += in[base + i];
-    int total;
-    block_exclusive_scan(s, &total);
-    if (threadIdx.x == 0) tile_sums[blockIdx.x] = total;
+    for (int k = 0; k < K; ++k) {
+        int s = 0;
+#pragma unroll
+        for (int i = 0; i < kScanItems; ++i)
+            if (base + i < n) s += a.in[k][base + i];
+        int total;
+        block_exclusive_scan(s, &total);
+        if (threadIdx.x == 0) tile_sums[k * stride + blockIdx.x] = total;
+    }
 }
 
-// Scan one tile; add the tile's offset (tile_offs == nullptr: single tile).
-// The block holding the last element also writes out[n] = total.
-__global__ __launch_bounds__(kScanBlock) void k_tile_scan(const int32_t *in, int32_t *out, int64_t n,
-                                                          const int32_t *__restrict__ tile_offs)
+// Scan one tile of each array; add the tile's offset (tile_offs == nullptr:
+// single tile).  The block holding the last element also writes out[n] = total.
+template <int K>
+__global__ __launch_bounds__(kScanBlock) void k_tile_scan(ScanSet<K> a, int64_t n,
+                                                          const int32_t *__restrict__ tile_offs,
+                                                          int64_t stride)
 {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-    int v[kScanItems];
-    int s = 0;
 #pragma unroll
-    for (int i = 0; i < kScanItems; ++i) {
-        v[i] = (base + i < n) ? in[base + i] : 0;
-        s += v[i];
-    }
-    int total;
-    int run = block_exclusive_scan(s, &total);   // contains a barrier: all reads done
-    const int off = tile_offs ? tile_offs[blockIdx.x] : 0;
-    run += off;
+    for (int k = 0; k < K; ++k) {
+        int v[kScanItems];
+        int s = 0;
 #pragma unroll
-    for (int i = 0; i < kScanItems; ++i) {
-        if (base + i < n) out[base + i] = run;
-        run += v[i];
+        for (int i = 0; i < kScanItems; ++i) {
+            v[i] = (base + i < n) ? a.in[k][base + i] : 0;
+            s += v[i];
+        }
+        int total;
+        int run = block_exclusive_scan(s, &total);   // contains a barrier: all reads done
+        const int off = tile_offs ? tile_offs[k * stride + blockIdx.x] : 0;
+        run += off;
+#pragma unroll
+        for (int i = 0; i < kScanItems; ++i) {
+            if (base + i < n) a.out[k][base + i] = run;
+            run += v[i];
+        }
+        if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) a.out[k][n] = off + total;
     }
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = off + total;
 }
 
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v)
@@ -275,32 +293,56 @@ int64_t scan_levels_ints(int64_t n)
     return total;
 }
 
-hipError_t scan_rec(const int32_t *in, int32_t *out, int64_t n, int32_t *ws, hipStream_t s)
+template <int K>
+hipError_t scan_rec(ScanSet<K> a, int64_t n, int32_t *ws, hipStream_t s)
 {
     if (n <= 0) {
-        COGDL_LAUNCH_HIP("fill", k_fill_i32, 1, 64, s, out, 1, 0);
+        for (int k = 0; k < K; ++k) COGDL_LAUNCH_HIP("fill", k_fill_i32, 1, 64, s, a.out[k], 1, 0);
         return hipSuccess;
     }
     const int64_t tiles = (n + kScanTile - 1) / kScanTile;
     if (tiles == 1) {
-        COGDL_LAUNCH_HIP("scan_tile", k_tile_scan, 1, kScanBlock, s, in, out, n, nullptr);
+        COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, 1, kScanBlock, s, a, n, nullptr, 0);
         return hipSuccess;
     }
+    // the tile sums of array k at ws[k * (tiles + 1)], scanned in place
+    const int64_t stride = tiles + 1;
     int32_t *sums = ws;
-    COGDL_LAUNCH_HIP("scan_reduce", k_tile_reduce, (unsigned)tiles, kScanBlock, s, in, n, sums);
-    hipError_t e = scan_rec(sums, sums, tiles, ws + tiles + 1, s);
+    COGDL_LAUNCH_HIP("scan_reduce", k_tile_reduce<K>, (unsigned)tiles, kScanBlock, s, a, n, sums,
+                     stride);
+    ScanSet<K> b;
+    for (int k = 0; k < K; ++k) {
+        b.in[k] = sums + k * stride;
+        b.out[k] = sums + k * stride;
+    }
+    hipError_t e = scan_rec<K>(b, tiles, ws + K * stride, s);
     if (e != hipSuccess) return e;
-    COGDL_LAUNCH_HIP("scan_tile", k_tile_scan, (unsigned)tiles, kScanBlock, s, in, out, n, sums);
+    COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, (unsigned)tiles, kScanBlock, s, a, n, sums, stride);
     return hipSuccess;
 }
 
 }  // namespace
 
-size_t scan_workspace_bytes(int64_t n) { return (size_t)(scan_levels_ints(n) + 16) * 4; }
+size_t scan_workspace_bytes(int64_t n, int arrays)
+{
+    return (size_t)(arrays * scan_levels_ints(n) + 16) * 4;
+}
 
 hipError_t exclusive_scan(const int32_t *in, int32_t *out, int64_t n, void *ws, hipStream_t s)
 {
-    return scan_rec(in, out, n, static_cast<int32_t *>(ws), s);
+    ScanSet<1> a;
+    a.in[0] = in;
+    a.out[0] = out;
+    return scan_rec<1>(a, n, static_cast<int32_t *>(ws), s);
+}
+
+hipError_t exclusive_scan3(int32_t *a0, int32_t *a1, int32_t *a2, int64_t n, void *ws, hipStream_t s)
+{
+    ScanSet<3> a;
+    a.in[0] = a.out[0] = a0;
+    a.in[1] = a.out[1] = a1;
+    a.in[2] = a.out[2] = a2;
+    return scan_rec<3>(a, n, static_cast<int32_t *>(ws), s);
 }
 
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s)
