@@ -76,16 +76,30 @@ __global__ __launch_bounds__(kScanBlock) void k_tile_reduce(ScanSet<K> a, int64_
     }
 }
 
-// Scan one tile of each array; add the tile's offset (tile_offs == nullptr:
-// single tile).  The block holding the last element also writes out[n] = total.
+// Scan one tile of each array and add the tile's offset: tile_offs[k * stride +
+// tile] when given; else, with `sums` given, the sum of sums[k * stride + t]
+// over the tiles t before this one (added up by the block itself, so a scan
+// of up to kDirectTiles tiles needs no second level); else 0 (single tile).
+// The block holding the last element also writes out[n] = total.
+constexpr int64_t kDirectTiles = 8192;
+
 template <int K>
 __global__ __launch_bounds__(kScanBlock) void k_tile_scan(ScanSet<K> a, int64_t n,
                                                           const int32_t *__restrict__ tile_offs,
-                                                          int64_t stride)
+                                                          int64_t stride,
+                                                          const int32_t *__restrict__ sums)
 {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
+        int before = 0;
+        if (!tile_offs && sums) {
+            int part = 0;
+            for (int t = threadIdx.x; t < (int)blockIdx.x; t += kScanBlock) part += sums[k * stride + t];
+            int all;
+            block_exclusive_scan(part, &all);
+            before = all;
+        }
         int v[kScanItems];
         int s = 0;
 #pragma unroll
@@ -95,7 +109,7 @@ __global__ __launch_bounds__(kScanBlock) void k_tile_scan(ScanSet<K> a, int64_t 
         }
         int total;
         int run = block_exclusive_scan(s, &total);   // contains a barrier: all reads done
-        const int off = tile_offs ? tile_offs[k * stride + blockIdx.x] : 0;
+        const int off = tile_offs ? tile_offs[k * stride + blockIdx.x] : before;
         run += off;
 #pragma unroll
         for (int i = 0; i < kScanItems; ++i) {
@@ -302,7 +316,7 @@ hipError_t scan_rec(ScanSet<K> a, int64_t n, int32_t *ws, hipStream_t s)
     }
     const int64_t tiles = (n + kScanTile - 1) / kScanTile;
     if (tiles == 1) {
-        COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, 1, kScanBlock, s, a, n, nullptr, 0);
+        COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, 1, kScanBlock, s, a, n, nullptr, 0, nullptr);
         return hipSuccess;
     }
     // the tile sums of array k at ws[k * (tiles + 1)], scanned in place
@@ -310,6 +324,11 @@ hipError_t scan_rec(ScanSet<K> a, int64_t n, int32_t *ws, hipStream_t s)
     int32_t *sums = ws;
     COGDL_LAUNCH_HIP("scan_reduce", k_tile_reduce<K>, (unsigned)tiles, kScanBlock, s, a, n, sums,
                      stride);
+    if (tiles <= kDirectTiles) {
+        COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, (unsigned)tiles, kScanBlock, s, a, n, nullptr,
+                         stride, sums);
+        return hipSuccess;
+    }
     ScanSet<K> b;
     for (int k = 0; k < K; ++k) {
         b.in[k] = sums + k * stride;
@@ -317,7 +336,8 @@ hipError_t scan_rec(ScanSet<K> a, int64_t n, int32_t *ws, hipStream_t s)
     }
     hipError_t e = scan_rec<K>(b, tiles, ws + K * stride, s);
     if (e != hipSuccess) return e;
-    COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, (unsigned)tiles, kScanBlock, s, a, n, sums, stride);
+    COGDL_LAUNCH_HIP("scan_tile", k_tile_scan<K>, (unsigned)tiles, kScanBlock, s, a, n, sums, stride,
+                     nullptr);
     return hipSuccess;
 }
 
