@@ -1,7 +1,7 @@
 """Seeded random sweep: graphs, feature widths, dtypes, balancer plans and head
 layouts drawn at random (a fixed seed per case, so every run checks the same
-cases), each operator of the hot path and of the backward compared with the
-oracle.  It covers the combinations the parametrized tests do not spell out:
+cases), each operator of the hot path, the backward, the GSpMM variants, the
+dense layer and the codec compared with the oracle.  It covers the combinations the parametrized tests do not spell out:
 tiny and empty matrices, rectangular shapes, duplicates with unsorted columns,
 hub rows against small neighbour groups, odd widths with 16-bit formats."""
 import numpy as np
@@ -147,3 +147,70 @@ def test_random_gat_forward_backward(cg, seed):
         assert scaled_error(out["dX"].reshape(ref["dX"].shape), ref["dX"], ref["dX_abs"]) <= TOL_F32, "dX"
     finally:
         _close(plan, plan_t)
+
+
+@pytest.mark.parametrize("seed", range(N_CASES))
+def test_random_gspmm_max_and_messages(cg, seed):
+    """Max with edge ids bit for bit (values rounded once to the output format, the first
+    edge attaining each maximum); add / sub messages with the fp32 tolerance."""
+    import torch
+    rng, g, spec = _case(seed)
+    F = int(rng.choice([1, 3, 8, 24, 64, 130]))
+    xk = KINDS[int(rng.integers(0, 3))]
+    yk = "f32" if rng.random() < 0.5 else xk
+    say(f"random max {seed}: {g.n_rows}x{g.n_cols} nnz={g.nnz} F={F} {xk}->{yk} plan={spec}")
+    rp, cl, vl = graph_to_dev(g)
+    xh, xc, xd = features((g.n_cols, F), 800 + seed, xk)
+    out_dtype = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[yk]
+    plan = _plan(cg, rp, g.nnz, spec, F)
+    try:
+        Y, arg = cg.gspmm(rp, cl, vl, xd, "max", plan=plan, out_dtype=out_dtype, return_arg=True)
+        Yr, _, ar = oracle.gspmm(g.rowptr, g.col, g.val, xh, "max", n_cols=g.n_cols, x_dtype=xc)
+        code = {"f32": oracle.F32, "bf16": oracle.BF16, "f16": oracle.F16}[yk]
+        want = oracle.decode(oracle.round_to(Yr, code), code)
+        assert np.array_equal(to_f64(Y).reshape(Yr.shape), want.reshape(Yr.shape)), "max"
+        assert np.array_equal(arg.cpu().numpy().reshape(ar.shape), ar), "argmax"
+        compute = ["add", "sub"][int(rng.integers(0, 2))]
+        reduce = ["sum", "mean"][int(rng.integers(0, 2))]
+        Ya = cg.gspmm(rp, cl, vl, xd, reduce, plan=plan, out_dtype=torch.float32, compute=compute)
+        Yar, Aar, _ = oracle.gspmm(g.rowptr, g.col, g.val, xh, reduce, n_cols=g.n_cols, x_dtype=xc,
+                                   compute=compute)
+        assert scaled_error(Ya, Yar, Aar) <= TOL_F32, (reduce, compute)
+    finally:
+        _close(plan)
+
+
+@pytest.mark.parametrize("seed", range(N_CASES // 3))
+def test_random_linear_and_codec(cg, seed):
+    """Dense layer (any row count, k, m, bias and activation) with the fp32 tolerance; codec
+    codes, stats and decodes bit for bit for random shapes, groups and bit widths."""
+    import torch
+    rng = np.random.default_rng(9500 + seed)
+    n, k, m = int(rng.integers(1, 700)), int(rng.integers(1, 700)), int(rng.integers(1, 300))
+    dt = ["bf16", "f16"][int(rng.integers(0, 2))]
+    act = ["none", "relu", "elu"][int(rng.integers(0, 3))]
+    code = oracle.BF16 if dt == "bf16" else oracle.F16
+    to_bits = synth.f32_to_bf16_bits if dt == "bf16" else synth.f32_to_f16_bits
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float16
+    xb = to_bits(rng.standard_normal((n, k)).astype(np.float32))
+    wb = to_bits((rng.standard_normal((m, k)) / np.sqrt(k)).astype(np.float32))
+    b = rng.standard_normal(m).astype(np.float32)
+    say(f"random linear {seed}: {n}x{k}x{m} {dt} {act}")
+    Y = cg.linear(dev(xb.view(np.int16)).view(tdt), dev(wb.view(np.int16)).view(tdt), bias=dev(b), act=act,
+                  out_dtype=torch.float32)
+    Yr, Ar = oracle.linear(xb, wb, b, act, x_dtype=code, w_dtype=code)
+    assert scaled_error(Y, Yr, Ar) <= TOL_F32, "linear"
+    bits = int(rng.integers(1, 9))
+    G = int(rng.choice([64, 128, 256, 512]))
+    rows, F = int(rng.integers(1, 600)), int(rng.integers(1, 700))
+    at = KINDS[int(rng.integers(0, 3))]
+    xh, xc, xd = features((rows, F), 950 + seed, at)
+    cseed = int(rng.integers(0, 2**63))
+    say(f"random codec {seed}: {rows}x{F} G={G} bits={bits} {at}")
+    codes, stats = cg.act_compress(xd, bits, G, cseed)
+    c_ref, s_ref = oracle.act_compress(xh, bits, G, cseed, a_dtype=xc)
+    assert np.array_equal(codes.cpu().numpy().view(np.uint64), c_ref)
+    assert np.array_equal(stats.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+    y = cg.act_decompress(codes, stats, rows, F, bits, G)
+    y_ref = oracle.act_decompress(c_ref, s_ref, rows, F, bits, G)
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), y_ref.view(np.uint32))
