@@ -355,6 +355,93 @@ __device__ __forceinline__ float group_sum(float v, int G)
 
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// Rows of CSR edges, resolved by one wavefront (all 64 lanes, uniform control
+// flow) for edges handed over in increasing order.  start(e0) finds the row
+// holding edge e0 by a 64-way search of rowptr (each round narrows the
+// candidate rows 64-fold); the cursor then keeps a window of 64 consecutive
+// row ends, one per lane, and the row of edge e is the window's first row plus
+// the number of window rows ending at or before e (a binary search across the
+// lanes).  Empty rows need no care: the search keeps the last row starting at
+// or before the edge, and the window just moves on.
+struct RowCursor {
+    const int32_t *rowptr;
+    int64_t n_rows;
+    int64_t r0;   // first row of the window
+    int rend;     // end of row r0 + lane (INT32_MAX past the last row)
+
+    // The row holding edge e0: the largest r < n with rp[r] <= e0.
+    __device__ __forceinline__ static int64_t find(const int32_t *rp, int64_t n, int64_t e0)
+    {
+        const int lane = lane_id();
+        int64_t lo = 0, hi = n;   // rp[lo] <= e0, answer in [lo, hi)
+        while (hi - lo > 1) {
+            const int64_t step = (hi - lo + kWave - 1) / kWave;
+            const int64_t p = lo + (int64_t)lane * step;
+            const uint64_t b = __ballot(p < hi && rp[p] <= e0);   // a prefix of the lanes
+            const int top = 63 - __clzll(b);                       // lane 0 always holds
+            lo += (int64_t)top * step;
+            hi = lo + step < hi ? lo + step : hi;
+        }
+        return lo;
+    }
+
+    // Window at row r (which must hold the first edge handed over).
+    __device__ __forceinline__ void start_at(const int32_t *rp, int64_t n, int64_t r)
+    {
+        rowptr = rp;
+        n_rows = n;
+        r0 = r;
+        const int lane = lane_id();
+        rend = r0 + lane < n ? rp[r0 + lane + 1] : INT32_MAX;
+    }
+
+    __device__ __forceinline__ void start(const int32_t *rp, int64_t n, int64_t e0)
+    {
+        start_at(rp, n, find(rp, n, e0));
+    }
+
+    // row[j] of edge e[j] for the lanes with want[j]; every e[j] must be at or
+    // after the edges of earlier calls (the window only moves forward).  The NE
+    // lane searches are independent and interleave.
+    template <int NE>
+    __device__ __forceinline__ void resolve(const int64_t (&e)[NE], const bool (&want)[NE],
+                                            int64_t (&row)[NE])
+    {
+        const int lane = lane_id();
+        bool done[NE];
+#pragma unroll
+        for (int j = 0; j < NE; ++j) {
+            done[j] = !want[j];
+            row[j] = 0;
+        }
+        for (;;) {
+            int k[NE];
+#pragma unroll
+            for (int j = 0; j < NE; ++j) k[j] = 0;
+#pragma unroll
+            for (int b = kWave / 2; b > 0; b >>= 1)
+#pragma unroll
+                for (int j = 0; j < NE; ++j) {
+                    const int probe = __shfl(rend, k[j] + b - 1);
+                    if ((int64_t)probe <= e[j]) k[j] += b;
+                }
+            const int last_end = __shfl(rend, kWave - 1);
+            bool left = false;
+#pragma unroll
+            for (int j = 0; j < NE; ++j) {
+                if (!done[j] && e[j] < (int64_t)last_end) {
+                    row[j] = r0 + k[j];
+                    done[j] = true;
+                }
+                left = left || !done[j];
+            }
+            if (__ballot(left) == 0) break;
+            r0 += kWave;
+            rend = r0 + lane < n_rows ? rowptr[r0 + lane + 1] : INT32_MAX;
+        }
+    }
+};
+
 // Merge two online-softmax states (m, z): the pair describing
 // z * exp(m) = sum exp(e).  An empty state is (-inf, 0).
 __device__ __forceinline__ void softmax_merge(float &m, float &z, float m2, float z2)

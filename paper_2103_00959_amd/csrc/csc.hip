@@ -15,14 +15,8 @@ namespace {
 
 constexpr int kBlock = 256;
 
-// Row of every edge.  Wavefront w covers the edges [w * kExpandSpan, ...): it
-// finds the row holding its first edge by a 64-way search of rowptr (each
-// round narrows the candidate rows 64-fold, four rounds for a few million
-// rows), then walks its edges 64 at a time against a window of 64
-// consecutive row ends held one per lane; the row of edge e is the window's
-// first row plus the number of window rows that end at or before e (a binary
-// search across the lanes).  Empty rows need no care: the search keeps the
-// last row starting at or before the edge, and the window just moves on.
+// Row of every edge (the transpose without edge ids): wavefront w covers the
+// edges [w * kExpandSpan, ...) with a RowCursor, 4 x 64 edges per round.
 constexpr int kExpandSpan = 2048;
 constexpr int kExpandEdges = 4;
 
@@ -34,58 +28,20 @@ __global__ __launch_bounds__(kBlock) void k_expand_rows(const int32_t *__restric
     const int64_t e0 = ((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * kExpandSpan;
     if (e0 >= nnz) return;
     const int64_t e1 = e0 + kExpandSpan < nnz ? e0 + kExpandSpan : nnz;
-    // largest r < n_rows with rowptr[r] <= e0; invariant rowptr[lo] <= e0, answer in [lo, hi)
-    int64_t lo = 0, hi = n_rows;
-    while (hi - lo > 1) {
-        const int64_t step = (hi - lo + kWave - 1) / kWave;
-        const int64_t p = lo + (int64_t)lane * step;
-        const uint64_t b = __ballot(p < hi && rowptr[p] <= e0);   // a prefix of the lanes
-        const int top = 63 - __clzll(b);                           // lane 0 always holds
-        lo += (int64_t)top * step;
-        hi = lo + step < hi ? lo + step : hi;
-    }
-    int64_t r0 = lo;
-    int rend = r0 + lane < n_rows ? rowptr[r0 + lane + 1] : INT32_MAX;
-    // kExpandEdges edges per lane per round: their lane searches are independent
-    // and interleave, which hides the latency of the cross-lane reads
+    RowCursor rc;
+    rc.start(rowptr, n_rows, e0);
     for (int64_t c = e0; c < e1; c += (int64_t)kWave * kExpandEdges) {
         int64_t e[kExpandEdges], row[kExpandEdges];
-        bool done[kExpandEdges];
+        bool want[kExpandEdges];
 #pragma unroll
         for (int j = 0; j < kExpandEdges; ++j) {
             e[j] = c + (int64_t)j * kWave + lane;
-            done[j] = e[j] >= e1;
-            row[j] = 0;
+            want[j] = e[j] < e1;
         }
-        for (;;) {
-            // rows before the window's first row end at or before every edge left
-            int k[kExpandEdges];
-#pragma unroll
-            for (int j = 0; j < kExpandEdges; ++j) k[j] = 0;
-#pragma unroll
-            for (int b = kWave / 2; b > 0; b >>= 1)
-#pragma unroll
-                for (int j = 0; j < kExpandEdges; ++j) {
-                    const int probe = __shfl(rend, k[j] + b - 1);
-                    if ((int64_t)probe <= e[j]) k[j] += b;
-                }
-            const int last_end = __shfl(rend, kWave - 1);
-            bool left = false;
-#pragma unroll
-            for (int j = 0; j < kExpandEdges; ++j) {
-                if (!done[j] && e[j] < (int64_t)last_end) {
-                    row[j] = r0 + k[j];
-                    done[j] = true;
-                }
-                left = left || !done[j];
-            }
-            if (__ballot(left) == 0) break;
-            r0 += kWave;
-            rend = r0 + lane < n_rows ? rowptr[r0 + lane + 1] : INT32_MAX;
-        }
+        rc.resolve<kExpandEdges>(e, want, row);
 #pragma unroll
         for (int j = 0; j < kExpandEdges; ++j)
-            if (e[j] < e1) row_of[e[j]] = (uint32_t)row[j];
+            if (want[j]) row_of[e[j]] = (uint32_t)row[j];
     }
 }
 
@@ -180,9 +136,10 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
     uint32_t *skeys = reinterpret_cast<uint32_t *>(ws + L.skeys);
 
     const int64_t waves = (nnz + kExpandSpan - 1) / kExpandSpan;
-    COGDL_LAUNCH("csc_expand_rows", k_expand_rows,
-                 (unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)), kBlock, stream, rowptr,
-                 n_rows, nnz, row_of);
+    if (!perm)
+        COGDL_LAUNCH("csc_expand_rows", k_expand_rows,
+                     (unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)), kBlock, stream,
+                     rowptr, n_rows, nnz, row_of);
     const int bits = bits_for((uint64_t)(n_cols - 1));
     RadixPayload vals;
     if (val) {
@@ -191,9 +148,10 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
         vals.ping = reinterpret_cast<uint32_t *>(ws + L.ping_w);
     }
     if (perm) {
-        // edge ids as the sorted values, rows and edge values as payloads
-        RadixPayload rows{row_of, reinterpret_cast<uint32_t *>(row_t),
-                          reinterpret_cast<uint32_t *>(ws + L.ping_r)};
+        // edge ids as the sorted values, rows (found from rowptr by the first
+        // pass) and edge values as payloads
+        RadixPayload rows{nullptr, reinterpret_cast<uint32_t *>(row_t),
+                          reinterpret_cast<uint32_t *>(ws + L.ping_r), rowptr, n_rows};
         COGDL_HIP_TRY(radix_sort_pairs(reinterpret_cast<const uint32_t *>(col), nullptr, skeys,
                                        reinterpret_cast<uint32_t *>(perm), nnz, bits, ping_k, ping_v,
                                        ws + L.radix, stream, rows, vals));

@@ -88,10 +88,15 @@ hipError_t exclusive_scan3(int32_t *a0, int32_t *a1, int32_t *a2, int64_t n, voi
 
 // An extra 32-bit array carried through a radix sort: read from `in`,
 // written in sorted order to `out`; `ping` is 2 * n elements of scratch.
+// For the first payload only, `in` may be nullptr with `rowptr` set: the
+// values are then the CSR rows of the elements (element e = edge e of the
+// rowptr of n_rows rows), found by the sort itself instead of read.
 struct RadixPayload {
     const uint32_t *in = nullptr;
     uint32_t *out = nullptr;
     uint32_t *ping = nullptr;
+    const int32_t *rowptr = nullptr;
+    int64_t n_rows = 0;
 };
 
 // Stable LSD radix sort of (key, value) pairs on the low `bits` bits of the

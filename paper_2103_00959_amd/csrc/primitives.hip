@@ -137,7 +137,10 @@ constexpr int kHistCopies = 4;
 
 __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__restrict__ keys, int64_t n,
                                                            int shift, int dbits, int n_tiles,
-                                                           int32_t *__restrict__ hist)
+                                                           int32_t *__restrict__ hist,
+                                                           const int32_t *__restrict__ rowptr,
+                                                           int64_t n_rows,
+                                                           int32_t *__restrict__ start_rows)
 {
     constexpr int kCopies = (kSortBlock / kWave) * kHistCopies;
     __shared__ int32_t h[kCopies][kDigits];
@@ -165,6 +168,15 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t *__res
         for (int w = 0; w < kCopies; ++w) c += h[w][threadIdx.x];
         hist[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = c;
     }
+    // the scatter's CSR rows: the row holding the first element of each
+    // wavefront's quarter of the tile, found here where latency is cheap
+    if (start_rows) {
+        const int64_t wb = base + (int64_t)(threadIdx.x / kWave) * kWave * kSortItems;
+        if (wb < n) {
+            const int64_t r = RowCursor::find(rowptr, n_rows, wb);
+            if (lane_id() == 0) start_rows[(int64_t)blockIdx.x * (kSortBlock / kWave) + threadIdx.x / kWave] = (int32_t)r;
+        }
+    }
 }
 
 // Tile handled by workgroup b of nb.  Workgroups are dealt to the 8 XCDs
@@ -187,12 +199,16 @@ __device__ __forceinline__ int xcd_tile(int b, int nb)
 // arrays of the tile are loaded up front (one memory round trip), then staged
 // in LDS in tile-sorted order two at a time and written out by consecutive
 // threads, so equal digits leave as contiguous runs instead of scattered
-// 4-byte stores.  NP extra 32-bit payloads travel with each key.
-template <int NP>
+// 4-byte stores.  NP extra 32-bit payloads travel with each key; ROWS: the
+// first payload is the CSR row of each element, resolved by each wavefront
+// for its 16 chunks of 64 consecutive elements with a RowCursor started at
+// the row k_radix_hist found for that wavefront (start_rows).
+template <int NP, bool ROWS>
 __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint32_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, int64_t n, int shift,
-    int dbits, int n_tiles, const int32_t *__restrict__ offsets, RadixPayload p0, RadixPayload p1)
+    int dbits, int n_tiles, const int32_t *__restrict__ offsets, RadixPayload p0, RadixPayload p1,
+    const int32_t *__restrict__ start_rows)
 {
     constexpr int kWaves = kSortBlock / kWave;
     __shared__ int32_t wcnt[kWaves][kDigits];   // per-wave counts, then tile-local run starts
@@ -216,8 +232,28 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
         const int64_t ec = e < n ? e : n - 1;     // clamped: loads need no branch
         key[i] = keys_in[ec];
         val[i] = vals_in ? vals_in[ec] : (uint32_t)e;
-        if constexpr (NP > 0) pa[i] = p0.in[ec];
+        if constexpr (NP > 0 && !ROWS) pa[i] = p0.in[ec];
         if constexpr (NP > 1) pb[i] = p1.in[ec];
+    }
+    if constexpr (ROWS) {
+        static_assert(NP > 0 && kSortItems % 4 == 0, "rows need a payload slot");
+        if (base < n) {                               // uniform across the wavefront
+            RowCursor rc;
+            rc.start_at(p0.rowptr, p0.n_rows, start_rows[(int64_t)tile * kWaves + w]);
+#pragma unroll
+            for (int i0 = 0; i0 < kSortItems; i0 += 4) {
+                int64_t e[4], row[4];
+                bool want[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    e[j] = base + (int64_t)(i0 + j) * kWave + lane;
+                    want[j] = e[j] < n;
+                }
+                rc.resolve<4>(e, want, row);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) pa[i0 + j] = (uint32_t)row[j];
+            }
+        }
     }
     __syncthreads();
 
@@ -374,13 +410,16 @@ hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s)
     return hipSuccess;
 }
 
+// Workspace of a radix sort of n keys: the digit table (+ its scan's scratch)
+// and one start row per wavefront of a tile (rows generated from rowptr).
 size_t radix_workspace_bytes(int64_t n)
 {
     const int64_t tiles = (n + kSortTile - 1) / kSortTile;
     const int64_t hist = (int64_t)kDigits * (tiles > 0 ? tiles : 1) + 1;
     size_t b = (size_t)(hist + 64) * 4;
     b = (b + 255) & ~size_t(255);
-    return b + scan_workspace_bytes(hist);
+    b += (scan_workspace_bytes(hist) + 255) & ~size_t(255);
+    return b + (size_t)(tiles > 0 ? tiles : 1) * (kSortBlock / kWave) * 4;
 }
 
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, uint32_t *keys_out,
@@ -389,12 +428,14 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
                             RadixPayload pay1)
 {
     if (n <= 0) return hipSuccess;
-    const int np = pay0.in ? (pay1.in ? 2 : 1) : 0;
+    const int np = (pay0.in || pay0.rowptr) ? (pay1.in ? 2 : 1) : 0;
     const int64_t tiles = (n + kSortTile - 1) / kSortTile;
     const int64_t hist_n = (int64_t)kDigits * tiles;
     int32_t *hist = static_cast<int32_t *>(ws);
     size_t hist_bytes = ((size_t)(hist_n + 1 + 64) * 4 + 255) & ~size_t(255);
     void *scan_ws = static_cast<char *>(ws) + hist_bytes;
+    int32_t *start_rows = reinterpret_cast<int32_t *>(
+        static_cast<char *>(scan_ws) + ((scan_workspace_bytes(hist_n + 1) + 255) & ~size_t(255)));
 
     // as few passes as digits of at most 8 bits allow, the bits spread evenly
     // over them (longer runs per digit than a short last pass gives)
@@ -411,21 +452,25 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
         uint32_t *dst_k = last ? keys_out : ping_keys + (p & 1) * n;
         uint32_t *dst_v = last ? vals_out : ping_vals + (p & 1) * n;
         RadixPayload pa{a.in, last ? pay0.out : (pay0.ping ? pay0.ping + (p & 1) * n : nullptr), nullptr};
+        const bool rows = p == 0 && pay0.rowptr != nullptr && pay0.in == nullptr;
+        pa.rowptr = pay0.rowptr;
+        pa.n_rows = pay0.n_rows;
         RadixPayload pb{b.in, last ? pay1.out : (pay1.ping ? pay1.ping + (p & 1) * n : nullptr), nullptr};
         const int64_t used = (int64_t)(1 << dbits) * tiles;
         COGDL_LAUNCH_HIP("radix_hist", k_radix_hist, (unsigned)tiles, kSortBlock, s, src_k, n, shift,
-                         dbits, (int)tiles, hist);
+                         dbits, (int)tiles, hist, pay0.rowptr, pay0.n_rows, rows ? start_rows : nullptr);
         hipError_t e = exclusive_scan(hist, hist, used, scan_ws, s);
         if (e != hipSuccess) return e;
-        if (np == 0)
-            COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<0>, (unsigned)tiles, kSortBlock, s,
-                             src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb);
-        else if (np == 1)
-            COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<1>, (unsigned)tiles, kSortBlock, s,
-                             src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb);
-        else
-            COGDL_LAUNCH_HIP("radix_scatter", k_radix_scatter<2>, (unsigned)tiles, kSortBlock, s,
-                             src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb);
+#define COGDL_SCATTER(NPV, ROWSV)                                                                \
+    COGDL_LAUNCH_HIP("radix_scatter", (k_radix_scatter<NPV, ROWSV>), (unsigned)tiles, kSortBlock, s, \
+                     src_k, src_v, dst_k, dst_v, n, shift, dbits, (int)tiles, hist, pa, pb,          \
+                     start_rows)
+        if (np == 0) COGDL_SCATTER(0, false);
+        else if (np == 1 && rows) COGDL_SCATTER(1, true);
+        else if (np == 1) COGDL_SCATTER(1, false);
+        else if (rows) COGDL_SCATTER(2, true);
+        else COGDL_SCATTER(2, false);
+#undef COGDL_SCATTER
         src_k = dst_k;
         src_v = dst_v;
         a.in = pa.out;
