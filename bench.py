@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--workloads", action="store_true",
                     help="instead of the step: time each workload's own operators (workloads 1-4 "
                          "in their own dtypes), cold and warm, one JSON line per workload and op")
+    ap.add_argument("--reps", type=int, default=20, help="--workloads: timed calls per op (cold and warm)")
+    ap.add_argument("--warm-reps", type=int, default=3,
+                    help="--workloads: untimed calls per op before timing (at least 1)")
     return ap.parse_args()
 
 
@@ -228,12 +231,70 @@ def run_inference(cg, synth, dev, time_op_kernels):
     }
 
 
-def run_workloads(reps=20, warm_reps=3):
+# Library sources behind the operators of the workloads mode (balancer, scan and radix
+# sort, transpose, SpMM, edge softmax and GAT aggregation).
+WORKLOAD_SOURCES = ["common.hpp", "internal.hpp", "primitives.hip", "plan.hip", "csc.hip",
+                    "spmm_kernel.hpp", "spmm.hip", "gat_kernel.hpp", "gat.hip"]
+
+
+def workloads_source_sha() -> str:
+    """Hash of the sources of the workloads mode's operators and the header: the workload
+    counters recorded under profiles/ hold only while it is unchanged."""
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    csrc = os.path.join(here, "paper_2103_00959_amd", "csrc")
+    files = [os.path.join(csrc, f) for f in WORKLOAD_SOURCES] + [os.path.join(here, "include", "cogdl.h")]
+    return hashlib.sha256(b"".join(open(f, "rb").read() for f in files)).hexdigest()[:16]
+
+
+def recorded_workload_traffic(profiles_dir: str | None = None):
+    """{"<workload>/<op>": {fetch_bytes, write_bytes, l2_hit, ...}} from the committed
+    rocprofv3 summary of a --workloads run (HBM bytes of one cold call of each op), or
+    None when any library source changed since the counters were taken."""
+    if profiles_dir is None:
+        profiles_dir = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles")
+    path = os.path.join(profiles_dir, "workloads_1_to_4_hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_sha16") != workloads_source_sha():
+        return None
+    return rec.get("ops")
+
+
+def oracle_rate(run, units, budget_s, chunk=256, full=False):
+    """Time the oracle over a random sample of `units` output rows (or columns), growing
+    the chunk until `budget_s` is spent or every unit is done; run(sel) does one chunk
+    and returns (algorithmic bytes, nonzeros) of it.  full: one call over all units."""
+    if full:
+        t0 = time.perf_counter()
+        b, e = run(None)
+        return dict(seconds=time.perf_counter() - t0, bytes=b, edges=e, units=units)
+    order = np.random.default_rng(11).permutation(units).astype(np.int32)
+    done, t, b_tot, e_tot = 0, 0.0, 0, 0
+    while done < units and (done == 0 or t < budget_s):
+        sel = np.sort(order[done:done + chunk])
+        done += sel.size
+        t0 = time.perf_counter()
+        b, e = run(sel)
+        t += time.perf_counter() - t0
+        b_tot += b
+        e_tot += e
+        chunk = min(chunk * 2, 1 << 18)
+    return dict(seconds=t, bytes=b_tot, edges=e_tot, units=done)
+
+
+def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
     """Each workload's operators in its own configuration (fp32 features; plans on AUTO with
     the default group size), one JSON line per (workload, op).  Cold: a 1 GiB buffer is
     written before every timed call, so L2 and the Infinity Cache hold none of its inputs;
     warm: the same call back to back.  Median and minimum of `reps` calls after `warm_reps`
-    untimed ones; plan creation and the transpose are preprocessing, reported on their own."""
+    untimed ones; plan creation and the transpose are preprocessing, reported on their own.
+    Each line also carries the compulsory-byte rate, GFLOP/s, whether the gathered table fits
+    the 256 MB Infinity Cache, a 1 GiB copy's rate (the achievable ceiling), the HBM bytes
+    of one cold call from the committed rocprofv3 counters of this mode (when the library
+    sources are unchanged since), and the fp64 CPU oracle's rate on the same op (all host
+    threads; also one thread for workloads 1 and 2, whose ops the oracle does whole)."""
     import torch
 
     import paper_2103_00959_amd as cg
@@ -241,9 +302,39 @@ def run_workloads(reps=20, warm_reps=3):
 
     dev = torch.device("cuda:0")
     flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    # a dispatch of a kernel no op uses opens and closes each op's section of a kernel trace
+    marker = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    # achievable ceiling (and the counters' calibration): a plain 1 GiB device copy
+    cp_dst = torch.empty_like(flush)
+    flush.fill_(3)
+    cp_ms = []
+    for _ in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        cp_dst.copy_(flush)
+        e1.record()
+        torch.cuda.synchronize()
+        cp_ms.append(e0.elapsed_time(e1))
+    copy_GBps = 2 * (1 << 30) / (float(np.median(cp_ms[1:])) * 1e-3) / 1e9
+    del cp_dst
+    log(f"1 GiB copy: {copy_GBps:.0f} GB/s")
+    hbm = recorded_workload_traffic()
+    threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    cpu_name = cpu_model()
+    if cpu:
+        import oracle
 
     def times(fn):
-        for _ in range(warm_reps):
+        # the first untimed call is traced to count the library launches of one call
+        marker.bitwise_not_()
+        cg.trace_enable(256)
+        cg.trace_reset()
+        fn()
+        torch.cuda.synchronize()
+        launches = len(cg.trace_read())
+        cg.trace_enable(0)
+        for _ in range(max(warm_reps, 1) - 1):
             fn()
         cold, warm = [], []
         for _ in range(reps):
@@ -261,27 +352,59 @@ def run_workloads(reps=20, warm_reps=3):
             evs[i + 1].record()
         torch.cuda.synchronize()
         warm = [evs[i].elapsed_time(evs[i + 1]) for i in range(reps)]
-        return cold, warm
+        marker.bitwise_not_()           # and closes it
+        return cold, warm, launches
 
-    def record(k, cfg, op, B, E, cold, warm, note=None):
+    def oracle_line(k, run, units, whole=False, parallel=True):
+        """CPU oracle timing of one op: all threads on a bounded random sample of the output
+        rows (the whole op for workloads 1 and 2, and always when whole = True), plus one
+        thread over the whole op for workloads 1 and 2.  parallel = False: that oracle
+        routine is a serial loop, so one thread is what it uses."""
+        if not cpu:
+            return None
+        oracle.set_threads(threads)
+        r = oracle_rate(run, units, cpu_budget_s, full=whole or k <= 2)
+        out = dict(kind="oracle", cores=threads if parallel else 1, cpu=cpu_name, seconds=r["seconds"],
+                   GBps=r["bytes"] / r["seconds"] / 1e9,
+                   edges_per_s=r["edges"] / r["seconds"] if r["edges"] else None,
+                   sample=("whole op" if r["units"] == units else f"{r['units']} of {units} random output rows"))
+        if k <= 2 and parallel:
+            oracle.set_threads(1)
+            r1 = oracle_rate(run, units, cpu_budget_s, full=True)
+            out.update(GBps_1core=r1["bytes"] / r1["seconds"] / 1e9, seconds_1core=r1["seconds"])
+            oracle.set_threads(threads)
+        return out
+
+    def record(k, cfg, op, B, B_u, E, flop, table_bytes, res, cpu_rec):
+        cold, warm, launches = res
         mc, mw = float(np.median(cold)), float(np.median(warm))
         out = {"workload": cfg["name"], "config": k, "op": op, "algorithmic_GB": B / 1e9,
+               "unique_GB": B_u / 1e9,
                "cold_ms_median": mc, "cold_ms_min": min(cold),
                "warm_ms_median": mw, "warm_ms_min": min(warm),
                "cold_eff_GBps": B / (mc * 1e-3) / 1e9, "cold_pct_peak": B / (mc * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                "warm_eff_GBps": B / (mw * 1e-3) / 1e9,
-               "cold_edges_per_s": E / (mc * 1e-3) if E else None}
-        if note:
-            out["note"] = note
+               "cold_unique_GBps": B_u / (mc * 1e-3) / 1e9,
+               "cold_edges_per_s": E / (mc * 1e-3) if E else None,
+               "cold_GFLOPps": flop / (mc * 1e-3) / 1e9 if flop else None,
+               "cache_resident": (table_bytes <= (256 << 20)) if table_bytes else None,
+               "copy_GBps": copy_GBps, "launches_per_call": launches,
+               "hbm_GBps": None, "l2_hit": None, "cpu_oracle": cpu_rec}
+        h = hbm.get(f"{cfg['name']}/{op}") if hbm else None
+        if h:
+            out["hbm_GB"] = (h["fetch_bytes"] + h["write_bytes"]) / 1e9
+            out["hbm_GBps"] = (h["fetch_bytes"] + h["write_bytes"]) / (mc * 1e-3) / 1e9
+            out["l2_hit"] = h.get("l2_hit")
         print(json.dumps(out), flush=True)
         log(f"{cfg['name']} {op}: cold {mc:.3f} ms ({out['cold_pct_peak'] * 100:.1f}% of peak), "
-            f"warm {mw:.3f} ms")
+            f"warm {mw:.3f} ms" + (f", oracle {cpu_rec['GBps']:.2f} GB/s" if cpu_rec else ""))
 
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)   # noqa: E731
     for k in (1, 2, 3, 4):
         cfg = synth.CONFIGS[k]
         g = synth.config_graph(k, verbose=True)
         N, M, E = g.n_rows, g.n_cols, g.nnz
+        deg = np.diff(g.rowptr.astype(np.int64))
         rowptr, col = up(g.rowptr), up(g.col)
         val = up(g.val) if g.val is not None else None
         t0 = time.perf_counter()
@@ -289,45 +412,84 @@ def run_workloads(reps=20, warm_reps=3):
                        max_heads=cfg.get("H", 0))
         torch.cuda.synchronize()
         log(f"{cfg['name']}: plan created in {(time.perf_counter() - t0) * 1e3:.1f} ms (host clock)")
-        cold, warm = times(lambda: plan.rebuild(rowptr))
-        record(k, cfg, "plan_rebuild", b_plan(N, plan.info()["n_units"]), 0, cold, warm)
+        res = times(lambda: plan.rebuild(rowptr))
+        inf = plan.info()
+        Bp = b_plan(N, inf["n_units"])
+
+        def run_plan(sel):
+            oracle.neighbor_groups(g.rowptr, inf["group_size"], inf["mode"])
+            return Bp, 0
+        record(k, cfg, "plan_rebuild", Bp, Bp, 0, 0, 0, res, oracle_line(k, run_plan, N, True, False))
         if "F" in cfg:
             F = cfg["F"]
-            X = up(synth.normal_f32((M, F), 2000 + k))
+            Xn = synth.normal_f32((M, F), 2000 + k)
+            X = up(Xn)
             Y = torch.empty((N, F), dtype=torch.float32, device=dev)
-            cold, warm = times(lambda: cg.spmm(rowptr, col, val, X, plan=plan, out=Y))
-            record(k, cfg, "spmm", b_spmm(N, M, E, F, 4, 4), E, cold, warm,
-                   note="X fits the 256 MB Infinity Cache" if M * F * 4 <= (256 << 20) else None)
+            res = times(lambda: cg.spmm(rowptr, col, val, X, plan=plan, out=Y))
+
+            def run_spmm(sel):
+                oracle.spmm(g.rowptr, g.col, g.val, Xn, rows=sel)
+                n, e = (N, E) if sel is None else (sel.size, int(deg[sel].sum()))
+                return b_spmm(n, M, e, F, 4, 4), e
+            record(k, cfg, "spmm", b_spmm(N, M, E, F, 4, 4), b_unique_spmm(N, M, E, F, 4, 4), E,
+                   2 * E * F, M * F * 4, res, oracle_line(k, run_spmm, N))
             if k == 2:
                 colptr, row_t, val_t, perm = cg.csr_to_csc(rowptr, col, val, M)
                 ws = torch.empty(cg.csr_to_csc_workspace(N, M, E), dtype=torch.uint8, device=dev)
-                cold, warm = times(lambda: cg.csr_to_csc(rowptr, col, val, M, workspace=ws))
-                record(k, cfg, "csr_to_csc", b_csc(N, M, E), E, cold, warm)
+                res = times(lambda: cg.csr_to_csc(rowptr, col, val, M, workspace=ws))
+
+                def run_csc(sel):
+                    oracle.csr_to_csc(g.rowptr, g.col, g.val, M)
+                    return b_csc(N, M, E), E
+                record(k, cfg, "csr_to_csc", b_csc(N, M, E), b_csc(N, M, E), E, 0, 0, res,
+                       oracle_line(k, run_csc, M, True, False))
                 plan_t = cg.Plan(colptr, E, max_feat=F)
-                G = up(synth.normal_f32((N, F), 4000 + k))
+                Gn = synth.normal_f32((N, F), 4000 + k)
+                G = up(Gn)
                 dX = torch.empty((M, F), dtype=torch.float32, device=dev)
-                cold, warm = times(lambda: cg.spmm_t(colptr, row_t, val_t, G, plan_t=plan_t, out=dX))
-                record(k, cfg, "spmm_t", b_spmm(M, N, E, F, 4, 4), E, cold, warm)
+                res = times(lambda: cg.spmm_t(colptr, row_t, val_t, G, plan_t=plan_t, out=dX))
+                cdeg = np.bincount(g.col, minlength=M).astype(np.int64)
+
+                def run_spmm_t(sel):
+                    oracle.spmm_t(g.rowptr, g.col, g.val, Gn, M, cols=sel)
+                    n, e = (M, E) if sel is None else (sel.size, int(cdeg[sel].sum()))
+                    return b_spmm(n, N, e, F, 4, 4), e
+                record(k, cfg, "spmm_t", b_spmm(M, N, E, F, 4, 4), b_unique_spmm(M, N, E, F, 4, 4), E,
+                       2 * E * F, N * F * 4, res, oracle_line(k, run_spmm_t, M, True, False))
                 plan_t.close()
                 del colptr, row_t, val_t, perm, ws, G, dX
             del X, Y
         if "H" in cfg:
             H, D = cfg["H"], cfg["D"]
             rng = np.random.default_rng(3000 + k)
-            s_dst = up(rng.standard_normal((N, H), dtype=np.float32))
-            s_src = up(rng.standard_normal((M, H), dtype=np.float32))
-            Xg = up(synth.normal_f32((M, H * D), 2100 + k)).view(M, H, D)
+            sd_n = rng.standard_normal((N, H), dtype=np.float32)
+            ss_n = rng.standard_normal((M, H), dtype=np.float32)
+            Xg_n = synth.normal_f32((M, H * D), 2100 + k)
+            s_dst, s_src = up(sd_n), up(ss_n)
+            Xg = up(Xg_n).view(M, H, D)
             Yg = torch.empty((N, H, D), dtype=torch.float32, device=dev)
             alpha = torch.empty((E, H), dtype=torch.float32, device=dev)
-            cold, warm = times(lambda: cg.sddmm_edge_softmax(rowptr, col, s_dst, s_src, 0.2, plan=plan,
-                                                             out=alpha))
-            record(k, cfg, "sddmm_edge_softmax",
-                   4 * (N + 1) + 4 * E + 4 * N * H + 4 * E * H + 4 * E * H, E, cold, warm)
+            res = times(lambda: cg.sddmm_edge_softmax(rowptr, col, s_dst, s_src, 0.2, plan=plan, out=alpha))
+            b_sm = lambda n, e: 4 * (n + 1) + 4 * e + 4 * n * H + 4 * e * H + 4 * e * H   # noqa: E731
+
+            def run_softmax(sel):
+                oracle.edge_softmax(g.rowptr, g.col, sd_n, ss_n, slope=0.2, rows=sel)
+                n, e = (N, E) if sel is None else (sel.size, int(deg[sel].sum()))
+                return b_sm(n, e), e
+            record(k, cfg, "sddmm_edge_softmax", b_sm(N, E), b_sm(N, E) - 4 * E * H + 4 * M * H, E,
+                   0, M * H * 4, res, oracle_line(k, run_softmax, N))
             for a_out in (False, True):
-                cold, warm = times(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
-                                                            out=Yg, alpha_out=alpha if a_out else None))
+                res = times(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
+                                                     out=Yg, alpha_out=alpha if a_out else None))
+
+                def run_gat(sel, a_out=a_out):
+                    oracle.gat(g.rowptr, g.col, sd_n, ss_n, Xg_n, H, D, slope=0.2, rows=sel)
+                    n, e = (N, E) if sel is None else (sel.size, int(deg[sel].sum()))
+                    return b_gat(n, e, H, D, 4, 4, a_out), e
                 record(k, cfg, "gat_aggregate" + ("_alpha_out" if a_out else ""),
-                       b_gat(N, E, H, D, 4, 4, a_out), E, cold, warm)
+                       b_gat(N, E, H, D, 4, 4, a_out),
+                       b_unique_gat(N, M, E, H, D, 4, 4) + (4 * E * H if a_out else 0), E,
+                       2 * E * H * D + 8 * E * H, M * H * D * 4, res, oracle_line(k, run_gat, N))
             del s_dst, s_src, Xg, Yg, alpha
         plan.close()
         del rowptr, col, val
@@ -341,7 +503,7 @@ def main():
               f"multi-GPU mode in this build", file=sys.stderr)
         sys.exit(2)
     if args.workloads:
-        run_workloads()
+        run_workloads(reps=args.reps, warm_reps=args.warm_reps, cpu=not args.no_cpu_baseline)
         return
     import torch
 

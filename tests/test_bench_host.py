@@ -49,3 +49,39 @@ def test_more_than_one_gpu_is_refused():
                        timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_workload_traffic_lookup(tmp_path):
+    # the committed per-op record either matches the current library sources or is ignored
+    r = bench.recorded_workload_traffic()
+    assert r is None or all(v["fetch_bytes"] > 0 and v["write_bytes"] >= 0 for v in r.values())
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    ops = {"medium_rmat_169343/spmm": {"fetch_bytes": 5.0, "write_bytes": 2.0, "l2_hit": 0.5}}
+    rec = {"source_sha16": bench.workloads_source_sha(), "ops": ops}
+    (prof / "workloads_1_to_4_hbm_traffic.json").write_text(json.dumps(rec))
+    assert bench.recorded_workload_traffic(str(prof)) == ops
+    rec["source_sha16"] = "0" * 16
+    (prof / "workloads_1_to_4_hbm_traffic.json").write_text(json.dumps(rec))
+    assert bench.recorded_workload_traffic(str(prof)) is None
+
+
+def test_oracle_rate_sampling():
+    """The CPU-oracle timer visits each output row at most once, in growing chunks, and
+    stops at the budget or when every row is done; whole = one call over everything."""
+    seen = []
+
+    def run(sel):
+        if sel is None:
+            return 100, 10
+        seen.extend(sel.tolist())
+        return 2 * sel.size, sel.size
+
+    r = bench.oracle_rate(run, 1000, budget_s=60.0, chunk=7)
+    assert r["units"] == 1000 and sorted(seen) == list(range(1000))
+    assert r["bytes"] == 2000 and r["edges"] == 1000
+    seen.clear()
+    r = bench.oracle_rate(run, 10**6, budget_s=0.0, chunk=5)   # budget spent after one chunk
+    assert r["units"] == 5 and len(set(seen)) == 5
+    r = bench.oracle_rate(run, 1000, budget_s=0.0, full=True)
+    assert r["units"] == 1000 and r["bytes"] == 100
