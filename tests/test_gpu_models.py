@@ -38,8 +38,11 @@ def _f16_dev(x):
     return bits, dev(bits.view(np.int16)).view(torch.float16)
 
 
+# k covers one to 62 full 16-k steps (fewer, as many and one more than the loads
+# kept in flight), a partial last step, and widths with only 4-byte or 2-byte alignment
 @pytest.mark.parametrize("n,k,m", [(1, 16, 32), (300, 602, 128), (129, 64, 41), (1000, 128, 512),
-                                   (5, 7, 3), (257, 24, 200), (64, 1000, 16)])
+                                   (5, 7, 3), (257, 24, 200), (64, 1000, 16), (70, 32, 96),
+                                   (70, 48, 64), (131, 66, 33)])
 @pytest.mark.parametrize("dt,yt,act", [("bf16", "f32", "none"), ("bf16", "bf16", "relu"),
                                        ("f16", "f32", "elu"), ("f16", "f16", "none")])
 def test_linear(cg, n, k, m, dt, yt, act):
@@ -62,7 +65,11 @@ def test_linear(cg, n, k, m, dt, yt, act):
     assert scaled_error(Y0, Y0r, A0r) <= TOL_F32
 
 
-@pytest.mark.parametrize("H,D,zt", [(4, 32, "bf16"), (1, 41, "bf16"), (3, 5, "f32"), (8, 128, "f16")])
+# vector path (heads of whole 16-byte vectors, H * D / VEC lanes a power of two up to 64):
+# (4, 32), (8, 8), (1, 64), (2, 256), (4, 4), (16, 8); per-node fallback: the others
+@pytest.mark.parametrize("H,D,zt", [(4, 32, "bf16"), (1, 41, "bf16"), (3, 5, "f32"), (8, 128, "f16"),
+                                    (8, 8, "f32"), (1, 64, "bf16"), (2, 256, "bf16"), (4, 4, "f32"),
+                                    (16, 8, "f16")])
 def test_head_scores(cg, H, D, zt):
     rng = np.random.default_rng(H * D)
     n = 777
