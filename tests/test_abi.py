@@ -270,3 +270,16 @@ def test_codec_validation(L):
     D = L.cogdl_act_decompress
     assert D(4, 64, 2, 64, FAKE, FAKE, FAKE, 3, None) == DTYPE
     assert D(4, 64, 2, 64, None, FAKE, FAKE, 0, None) == INVALID
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    """No CPU fallback: without the HIP library every entry point of the binding raises."""
+    import torch
+    monkeypatch.setattr(cg, "_lib", None)
+    monkeypatch.setattr(cg, "LIB_PATH", os.path.join(ROOT, "no_such_dir", "libcogdl_mi355.so"))
+    with pytest.raises(cg.CogdlError, match="missing"):
+        cg.lib()
+    rowptr = torch.zeros(3, dtype=torch.int32)
+    col = torch.zeros(0, dtype=torch.int32)
+    with pytest.raises(Exception):
+        cg.spmm(rowptr, col, None, torch.zeros((2, 4)))
