@@ -42,7 +42,7 @@ def _f16_dev(x):
 # kept in flight), a partial last step, and widths with only 4-byte or 2-byte alignment
 @pytest.mark.parametrize("n,k,m", [(1, 16, 32), (300, 602, 128), (129, 64, 41), (1000, 128, 512),
                                    (5, 7, 3), (257, 24, 200), (64, 1000, 16), (70, 32, 96),
-                                   (70, 48, 64), (131, 66, 33)])
+                                   (70, 48, 64), (131, 66, 33), (5, 0, 3)])
 @pytest.mark.parametrize("dt,yt,act", [("bf16", "f32", "none"), ("bf16", "bf16", "relu"),
                                        ("f16", "f32", "elu"), ("f16", "f16", "none")])
 def test_linear(cg, n, k, m, dt, yt, act):
