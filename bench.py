@@ -29,6 +29,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
+SLICE_MIN = 128          # COGDL_DEFAULT_SLICE_MIN: rows longer than this are column-sliced
 METRIC = "SpMM & GAT-aggregate effective HBM GB/s (% of peak) and edges/sec, 1 MI355X"
 
 
@@ -47,6 +48,8 @@ def parse():
     ap.add_argument("--no-inference", action="store_true",
                     help="skip the 2-layer GCN / GAT inference timing on the Reddit-shaped graph")
     ap.add_argument("--group-size", type=int, default=0)
+    ap.add_argument("--plain-plans", action="store_true",
+                    help="balancer plans without column slicing (the paper's neighbour groups only)")
     ap.add_argument("--alpha-out", action="store_true", help="also write alpha in the GAT step")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the steps, copy a buffer of this many MiB (counter calibration)")
@@ -557,9 +560,12 @@ def main():
                                      cg._ptr(colptr), cg._ptr(row_t), cg._ptr(val_t), cg._ptr(perm),
                                      cg._ptr(ws), ws.numel(), stream()), "csr_to_csc")
 
-    plan = cg.Plan(rowptr, E, max_feat=max(F, H * D), max_heads=H, group_size=args.group_size)
+    # column-sliced plans (each XCD gathers from its own eighth of the table), or plain ones
+    sl = {} if args.plain_plans else dict(col=col, n_cols=M)
+    sl_t = {} if args.plain_plans else dict(col=row_t, n_cols=N)
+    plan = cg.Plan(rowptr, E, max_feat=max(F, H * D), max_heads=H, group_size=args.group_size, **sl)
     csc()
-    plan_t = cg.Plan(colptr, E, max_feat=F, max_heads=H, group_size=args.group_size)
+    plan_t = cg.Plan(colptr, E, max_feat=F, max_heads=H, group_size=args.group_size, **sl_t)
     torch.cuda.synchronize()
     info, info_t = plan.info(), plan_t.info()
     log(f"plan: {info['mode_name']} units={info['n_units']} long={info['n_long_units']} "
@@ -568,13 +574,18 @@ def main():
     # Edges and directly written rows of the long-unit and tiny-unit kernels
     # (split rows are written by the reduce kernel): the algorithmic bytes of
     # an op are split exactly between its kernels.
+    # A unit runs in the tiny-unit kernel when the plan uses neighbour groups larger than
+    # the tiny size and the unit has at most that many edges (sliced plans keep one
+    # long/tiny pair of ranges per XCD list, so the split is by size, not by position).
+    TINY = 8                                                        # kTinyUnit
     def unit_split(p, inf):
         un = p.units().cpu().numpy().astype(np.int64)
-        nb = inf["n_long_units"]
         size = un[:, 2] - un[:, 1]
         direct = un[:, 3] < 0
-        return dict(E_long=int(size[:nb].sum()), R_long=int(direct[:nb].sum()),
-                    E_tiny=int(size[nb:].sum()), R_tiny=int(direct[nb:].sum()),
+        tiny = (size <= TINY) if (inf["mode"] == 2 and inf["group_size"] > TINY) else np.zeros(len(un), bool)
+        assert int((~tiny).sum()) == inf["n_long_units"]
+        return dict(E_long=int(size[~tiny].sum()), R_long=int((direct & ~tiny).sum()),
+                    E_tiny=int(size[tiny].sum()), R_tiny=int((direct & tiny).sum()),
                     R_split=inf["n_split_rows"])
     us, us_t = unit_split(plan, info), unit_split(plan_t, info_t)
 
@@ -863,7 +874,10 @@ def main():
                                 f"GAT H={H} x D={D} bf16, fp32 accumulation"),
                    "n_nodes": N, "nnz": E, "F": F, "H": H, "D": D, "feature_dtype": "bf16",
                    "accumulate": "f32", "group_size": info["group_size"],
-                   "balancer": info["mode_name"], "alpha_out": bool(args.alpha_out)},
+                   "balancer": info["mode_name"],
+                   "column_slices": None if args.plain_plans else
+                   f"8 column ranges, rows over {SLICE_MIN} nonzeros sliced, one unit list per XCD",
+                   "alpha_out": bool(args.alpha_out)},
         "pct_peak": value / HBM_PEAK_GBPS,
         "edges_per_s": 3 * E / (ms_step * 1e-3),
         "edges_per_s_note": "nonzeros aggregated per second over the three gathers (SpMM, SpMM^T, GAT)",

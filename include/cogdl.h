@@ -152,6 +152,42 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
  * and nnz (same mode request and group size).  Allocates nothing. */
 cogdl_status cogdl_plan_rebuild(cogdl_plan *plan, const int32_t *rowptr, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Column-sliced plan (a scheduling refinement of the neighbour-group backend
+ * for the MI355X, not part of the paper): in NEIGHBOR_GROUP mode every row
+ * with more than slice_min edges is also cut at the boundaries of 8 equal
+ * column ranges [s * w, (s + 1) * w), w = ceil(n_cols / 8) (then into groups
+ * of at most group_size edges, each a partial sum as above), and the units
+ * are executed as 8 lists: the units of column range s form list s, every
+ * other unit goes to list row % 8, and each list runs on one XCD, so the
+ * feature rows a list gathers come from one eighth of the table and stay in
+ * that XCD's L2.  Any row order of columns is accepted (unsorted rows are
+ * still cut into 8 contiguous pieces, only without the locality).  Results
+ * are those of the plain plan up to fp32 summation order.
+ *
+ * col         device, nnz int32: the graph's column indices (for the CSC,
+ *             the row indices row_t), read during every build.
+ * n_cols      number of columns (>= 1 when nnz > 0).
+ * slice_min   rows with more edges than this are sliced; 0 picks
+ *             COGDL_DEFAULT_SLICE_MIN.
+ * group_size  as for cogdl_plan_create, at most 2^24.
+ * The creation counts the sliced units of this graph (one host read-back) to
+ * size the plan.  cogdl_plan_rebuild_sliced re-runs the balancer on a graph
+ * with the plan's n_rows and nnz; if its sliced units would exceed the sizes
+ * taken at creation, that build slices no row.  A sliced plan is rebuilt
+ * only with cogdl_plan_rebuild_sliced (cogdl_plan_rebuild returns
+ * COGDL_ERR_INVALID for it), and serves every call a plain plan serves.
+ * ---------------------------------------------------------------------- */
+#define COGDL_DEFAULT_SLICE_MIN 128
+
+cogdl_status cogdl_plan_create_sliced(int32_t n_rows, int64_t nnz, const int32_t *rowptr,
+                                      const int32_t *col, int32_t n_cols, int32_t max_feat,
+                                      int32_t max_heads, cogdl_balance mode, int32_t group_size,
+                                      int32_t slice_min, hipStream_t stream, cogdl_plan **out);
+
+cogdl_status cogdl_plan_rebuild_sliced(cogdl_plan *plan, const int32_t *rowptr, const int32_t *col,
+                                       hipStream_t stream);
+
 /* Free the plan (synchronizes the device first).  NULL is accepted. */
 cogdl_status cogdl_plan_destroy(cogdl_plan *plan);
 

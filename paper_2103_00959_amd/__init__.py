@@ -60,6 +60,9 @@ def lib():
     L.cogdl_version.restype = i32
     L.cogdl_plan_create.argtypes = [i32, i64, P, i32, i32, ctypes.c_int, i32, P, ctypes.POINTER(P)]
     L.cogdl_plan_rebuild.argtypes = [P, P, P]
+    L.cogdl_plan_create_sliced.argtypes = [i32, i64, P, P, i32, i32, i32, ctypes.c_int, i32, i32, P,
+                                           ctypes.POINTER(P)]
+    L.cogdl_plan_rebuild_sliced.argtypes = [P, P, P, P]
     L.cogdl_plan_destroy.argtypes = [P]
     L.cogdl_plan_query.argtypes = [P, P, ctypes.POINTER(_PlanInfo)]
     L.cogdl_plan_units.argtypes = [P, P, i64, P]
@@ -88,7 +91,7 @@ def lib():
     L.cogdl_trace_filter.argtypes = [ctypes.c_char_p]
     L.cogdl_trace_count.restype = i32
     L.cogdl_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
-    for name in ("cogdl_trace_enable", "cogdl_trace_filter", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_destroy", "cogdl_plan_query",
+    for name in ("cogdl_trace_enable", "cogdl_trace_filter", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_create_sliced", "cogdl_plan_rebuild_sliced", "cogdl_plan_destroy", "cogdl_plan_query",
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate",
                  "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act", "cogdl_linear",
@@ -139,16 +142,29 @@ class Plan:
     """The data-aware workload balancer (section 2.2): run once per graph."""
 
     def __init__(self, rowptr, nnz: int, max_feat: int, max_heads: int = 0, mode: str = "auto",
-                 group_size: int = 0):
+                 group_size: int = 0, col=None, n_cols: int | None = None, slice_min: int = 0):
+        """With `col` (and `n_cols`), a column-sliced plan (cogdl_plan_create_sliced): long rows
+        are also cut at 8 column-range boundaries and each range's units run on one XCD."""
         import torch
         _dev(rowptr, "rowptr", torch.int32)
         self.rowptr = rowptr
         self.n_rows = rowptr.numel() - 1
         self.nnz = int(nnz)
+        self.sliced = col is not None
         h = ctypes.c_void_p()
-        _check(lib().cogdl_plan_create(self.n_rows, self.nnz, _ptr(rowptr), int(max_feat),
-                                       int(max_heads), BALANCE[mode], int(group_size), _stream(),
-                                       ctypes.byref(h)), "cogdl_plan_create")
+        if self.sliced:
+            _dev(col, "col", torch.int32)
+            if n_cols is None:
+                raise CogdlError("a sliced plan needs n_cols")
+            self.col = col
+            _check(lib().cogdl_plan_create_sliced(self.n_rows, self.nnz, _ptr(rowptr), _ptr(col), int(n_cols),
+                                                  int(max_feat), int(max_heads), BALANCE[mode], int(group_size),
+                                                  int(slice_min), _stream(), ctypes.byref(h)),
+                   "cogdl_plan_create_sliced")
+        else:
+            _check(lib().cogdl_plan_create(self.n_rows, self.nnz, _ptr(rowptr), int(max_feat),
+                                           int(max_heads), BALANCE[mode], int(group_size), _stream(),
+                                           ctypes.byref(h)), "cogdl_plan_create")
         self._h = h
 
     @property
@@ -157,12 +173,19 @@ class Plan:
             raise CogdlError("plan destroyed")
         return self._h
 
-    def rebuild(self, rowptr=None):
+    def rebuild(self, rowptr=None, col=None):
         import torch
         if rowptr is not None:
             _dev(rowptr, "rowptr", torch.int32)
             self.rowptr = rowptr
-        _check(lib().cogdl_plan_rebuild(self.handle, _ptr(self.rowptr), _stream()), "cogdl_plan_rebuild")
+        if self.sliced:
+            if col is not None:
+                _dev(col, "col", torch.int32)
+                self.col = col
+            _check(lib().cogdl_plan_rebuild_sliced(self.handle, _ptr(self.rowptr), _ptr(self.col), _stream()),
+                   "cogdl_plan_rebuild_sliced")
+        else:
+            _check(lib().cogdl_plan_rebuild(self.handle, _ptr(self.rowptr), _stream()), "cogdl_plan_rebuild")
 
     def info(self) -> dict:
         inf = _PlanInfo()

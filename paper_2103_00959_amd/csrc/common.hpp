@@ -478,4 +478,29 @@ __device__ __forceinline__ void epilogue(float (&v)[VEC], const float *__restric
     }
 }
 
+// Work-unit walk of a resident grid.  Sub-group `sub` (of `per_block` in each
+// workgroup) starts at unit `first` and steps by `step` while below `end`.
+// Without a unit list the walk covers rows [0, n_rows).  With `lists` == 1 it
+// covers units [*lo, *hi).  With `lists` > 1 the units form that many
+// consecutive lists, list x being [lo[x], hi[x]), and workgroup b walks list
+// b % lists together with the other workgroups of that list (the grid is a
+// multiple of `lists`): workgroups are dealt to the XCDs round-robin, so every
+// list runs on one XCD and its gathers share that XCD's L2.
+struct UnitWalk {
+    int64_t first, end, step;
+};
+
+__device__ __forceinline__ UnitWalk unit_walk(bool has_units, const int32_t *lo, const int32_t *hi,
+                                              int lists, int64_t n_rows, int per_block, int sub)
+{
+    if (!has_units)
+        return {(int64_t)blockIdx.x * per_block + sub, n_rows, (int64_t)gridDim.x * per_block};
+    if (lists <= 1)
+        return {(int64_t)*lo + (int64_t)blockIdx.x * per_block + sub, (int64_t)*hi,
+                (int64_t)gridDim.x * per_block};
+    const int x = blockIdx.x % lists;
+    return {(int64_t)lo[x] + (int64_t)(blockIdx.x / lists) * per_block + sub, (int64_t)hi[x],
+            (int64_t)(gridDim.x / lists) * per_block};
+}
+
 }  // namespace cogdl

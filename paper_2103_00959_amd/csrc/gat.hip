@@ -30,7 +30,8 @@ constexpr int kBlock = kGatBlock;
 struct SoftArgs {
     const int4 *units;
     const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
-    const int32_t *u_hi;
+    const int32_t *u_hi;        // (lists > 1: list x is [u_lo[x], u_hi[x]), see unit_walk)
+    int32_t lists = 1;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -99,13 +100,13 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
     const int h = lig % H;
     const int slot = lig / H;
     const bool live = slot < slots;
-    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
-    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
-    const int64_t lo = a.units ? *a.u_lo : 0;
-    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows,
+                                    kBlock >> log2S, threadIdx.x >> log2S);
+    const int64_t stride = walk.step;
+    const int64_t hi = walk.end;
     const int32_t *__restrict__ col = a.col;
 
-    int64_t u = lo + sub;
+    int64_t u = walk.first;
     if (u >= hi) return;
     int4 d = fetch_soft_unit(a, u, hi);
     for (;;) {
@@ -383,8 +384,7 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
 
     SoftArgs a{};
     a.units = P ? P->units : nullptr;
-    a.u_lo = P ? P->zero_dev() : nullptr;
-    a.u_hi = P ? P->n_big_dev() : nullptr;
+    if (P) set_units(a, long_units(*P));
     a.n_rows = n_rows;
     a.rowptr = rowptr;
     a.col = col;
@@ -407,17 +407,16 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(name, k, (unsigned)(blocks > 0 ? blocks : 1), kBlock, stream, args);
+        blocks = list_grid(blocks, args.lists);
+        COGDL_LAUNCH(name, k, (unsigned)blocks, kBlock, stream, args);
         return COGDL_OK;
     };
     a.log2S = 6;
-    if (!P) a.u_hi = nullptr;
     st = launch("softmax", k_softmax<8>, a);
     if (st != COGDL_OK) return st;
     if (P) {
         SoftArgs b = a;
-        b.u_lo = P->n_big_dev();
-        b.u_hi = P->n_units_dev();
+        set_units(b, tiny_units(*P));
         b.log2S = log2i(next_pow2(4 * H) < kWave ? next_pow2(4 * H) : kWave);
         st = launch("softmax_tiny", k_softmax<2>, b);
         if (st != COGDL_OK) return st;
@@ -476,8 +475,6 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     }
     GatArgs a{};
     a.units = P ? P->units : nullptr;
-    a.u_lo = P ? P->zero_dev() : nullptr;
-    a.u_hi = P ? P->n_units_dev() : nullptr;
     a.n_rows = n_rows;
     a.rowptr = rowptr;
     a.col = col;
@@ -504,28 +501,27 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     const int64_t units = P ? P->cap_units : n_rows;
     // tiny units (the sorted tail): S/4 lanes and four chunks per lane
     const bool tiny = P && m.ch == 1 && m.S >= 8 && m.S / 4 >= H;
-    if (tiny) a.u_hi = P->n_big_dev();
+    if (P) set_units(a, tiny ? long_units(*P) : all_units(*P));
     {
         const int64_t upb = kBlock >> m.log2S;
         GatKernel k = gat_pick<false>(x_dtype, y_dtype, m.vec, m.ch, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH("gat", k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock,
-                     stream, a);
+        blocks = list_grid(blocks, a.lists);
+        COGDL_LAUNCH("gat", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, stream, a);
     }
     if (tiny) {
         GatArgs b = a;
-        b.u_lo = P->n_big_dev();
-        b.u_hi = P->n_units_dev();
+        set_units(b, tiny_units(*P));
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
         GatKernel k = gat_pick<false>(x_dtype, y_dtype, m.vec, 4, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH("gat_tiny", k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
-                     kBlock, stream, b);
+        blocks = list_grid(blocks, b.lists);
+        COGDL_LAUNCH("gat_tiny", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, stream, b);
     }
     if (!P) return COGDL_OK;
 

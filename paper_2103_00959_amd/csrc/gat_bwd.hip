@@ -33,8 +33,9 @@ constexpr int kBlock = kGatBlock;
 
 struct BwdArgs {
     const int4 *units;          // nullptr: one unit per row in row order
-    const int32_t *u_lo;
+    const int32_t *u_lo;        // units [*u_lo, *u_hi), or per list (see unit_walk)
     const int32_t *u_hi;
+    int32_t lists = 1;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -106,15 +107,15 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
     const bool act = fe < a.W;
     const bool writer = act && q < M;
     const int H = a.H;
-    const int64_t sub = (int64_t)blockIdx.x * (kBlock >> log2S) + (threadIdx.x >> log2S);
-    const int64_t stride = (int64_t)gridDim.x * (kBlock >> log2S);
-    const int64_t lo = a.units ? *a.u_lo : 0;
-    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows,
+                                    kBlock >> log2S, threadIdx.x >> log2S);
+    const int64_t stride = walk.step;
+    const int64_t hi = walk.end;
     const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const TX *__restrict__ P = static_cast<const TX *>(a.P);
     const int32_t *__restrict__ col = a.col;
 
-    int64_t u = lo + sub;
+    int64_t u = walk.first;
     if (u >= hi) return;
     int4 d = fetch_bwd_unit(a, u, hi);
     int c_cur = 0;
@@ -271,13 +272,12 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
     const int h = lane % H;
     const int slot = lane / H;
     const bool live = slot < eps;
-    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
-    const int64_t lo = a.units ? *a.u_lo : 0;
-    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows,
+                                    kBlock / kWave, threadIdx.x / kWave);
+    const int64_t hi = walk.end;
     const TX *__restrict__ X = static_cast<const TX *>(a.X);
     const TP *__restrict__ P = static_cast<const TP *>(a.P);
-    for (int64_t u = lo + (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; u < hi;
-         u += waves) {
+    for (int64_t u = walk.first; u < hi; u += walk.step) {
         const int4 d = fetch_bwd_unit(a, u, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
         const float sd = DOT ? 0.f : a.s_dst[(int64_t)row * H + h];
@@ -451,13 +451,15 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(name, k, (unsigned)(blocks > 0 ? blocks : 1), kBlock, stream, a);
+        blocks = list_grid(blocks, a.lists);
+        COGDL_LAUNCH(name, k, (unsigned)blocks, kBlock, stream, a);
     } else {
         BwdKernel k = pick_any<DOT>(xdt, pdt);
         int64_t blocks = (units + (kBlock / kWave) - 1) / (kBlock / kWave);
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(name, k, (unsigned)(blocks > 0 ? blocks : 1), kBlock, stream, a);
+        blocks = list_grid(blocks, a.lists);
+        COGDL_LAUNCH(name, k, (unsigned)blocks, kBlock, stream, a);
     }
     return COGDL_OK;
 }
@@ -494,8 +496,7 @@ cogdl_status cogdl_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const 
     if (nnz == 0) return COGDL_OK;
     BwdArgs a{};
     a.units = Pl ? Pl->units : nullptr;
-    a.u_lo = Pl ? Pl->zero_dev() : nullptr;
-    a.u_hi = Pl ? Pl->n_units_dev() : nullptr;
+    if (Pl) set_units(a, all_units(*Pl));
     a.n_rows = n_rows;
     a.rowptr = rowptr;
     a.col = col;
@@ -537,8 +538,7 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     if (n_rows > 0) {
         BwdArgs a{};
         a.units = Pr ? Pr->units : nullptr;
-        a.u_lo = Pr ? Pr->zero_dev() : nullptr;
-        a.u_hi = Pr ? Pr->n_units_dev() : nullptr;
+        if (Pr) set_units(a, all_units(*Pr));
         a.n_rows = n_rows;
         a.rowptr = rowptr;
         a.col = col;
@@ -584,8 +584,6 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     }
     GatArgs g{};
     g.units = Pc ? Pc->units : nullptr;
-    g.u_lo = Pc ? Pc->zero_dev() : nullptr;
-    g.u_hi = Pc ? Pc->n_units_dev() : nullptr;
     g.n_rows = n_cols;
     g.rowptr = colptr;
     g.col = row_t;
@@ -608,28 +606,27 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     const bool buf = g.x_bytes <= kBufferMaxBytes;
     const int64_t units = Pc ? Pc->cap_units : n_cols;
     const bool tiny = Pc && m.ch == 1 && m.S >= 8 && m.S / 4 >= H;
-    if (tiny) g.u_hi = Pc->n_big_dev();
+    if (Pc) set_units(g, tiny ? long_units(*Pc) : all_units(*Pc));
     {
         const int64_t upb = kBlock >> m.log2S;
         GatKernel k = gat_pick<true>((int)dy_dtype, (int)dx_dtype, m.vec, m.ch, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH("gat_bwd_cols", k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
-                     kBlock, stream, g);
+        blocks = list_grid(blocks, g.lists);
+        COGDL_LAUNCH("gat_bwd_cols", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, stream, g);
     }
     if (tiny) {
         GatArgs b = g;
-        b.u_lo = Pc->n_big_dev();
-        b.u_hi = Pc->n_units_dev();
+        set_units(b, tiny_units(*Pc));
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
         GatKernel k = gat_pick<true>((int)dy_dtype, (int)dx_dtype, m.vec, 4, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH("gat_bwd_cols_tiny", k,
-                     dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs), kBlock, stream, b);
+        blocks = list_grid(blocks, b.lists);
+        COGDL_LAUNCH("gat_bwd_cols_tiny", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, stream, b);
     }
     if (!Pc) return COGDL_OK;
     st = sum_reduce_launch("gat_bwd_dx_reduce", *Pc, W, dX, (int)dx_dtype, false, nullptr,

@@ -14,7 +14,8 @@ constexpr int kGatBlock = 256;
 struct GatArgs {
     const int4 *units;
     const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
-    const int32_t *u_hi;
+    const int32_t *u_hi;        // (lists > 1: list x is [u_lo[x], u_hi[x]), see unit_walk)
+    int32_t lists = 1;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -92,10 +93,10 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
     const int gbase = lane & ~(S - 1);
     const int H = a.H;
     const bool soft = a.alpha_in == nullptr;
-    const int64_t sub = (int64_t)blockIdx.x * (kGatBlock >> log2S) + (threadIdx.x >> log2S);
-    const int64_t stride = (int64_t)gridDim.x * (kGatBlock >> log2S);
-    const int64_t lo = a.units ? *a.u_lo : 0;
-    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows,
+                                    kGatBlock >> log2S, threadIdx.x >> log2S);
+    const int64_t stride = walk.step;
+    const int64_t hi = walk.end;
 
     const int64_t f0 = (int64_t)blockIdx.y * a.slab;
     const int64_t f_end = (f0 + a.slab < a.W) ? f0 + a.slab : a.W;
@@ -116,7 +117,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
     const int q_slot = lig / H, q_head = lig % H;
 
     // Resident grid, software-pipelined over units as in the SpMM kernel.
-    int64_t u = lo + sub;
+    int64_t u = walk.first;
     if (u >= hi) return;
     int4 d = fetch_gat_unit(a, u, hi);
     int c_cur = 0, p_cur = 0;

@@ -15,6 +15,9 @@ namespace cogdl {
 // output (part < 0) or into partial-sum slot `part`.
 // Layout int4 {row, beg, end, part}.
 
+// Column slices of a sliced plan: one per XCD of the MI355X.
+constexpr int kSlices = 8;
+
 struct Plan {
     int32_t n_rows = 0;
     int64_t nnz = 0;
@@ -38,8 +41,9 @@ struct Plan {
     int32_t *row_units = nullptr; // [n_rows + 1] exclusive scan; [n_rows] = #units
     int32_t *row_parts = nullptr; // [n_rows + 1]; [n_rows] = #partial slots
     int32_t *row_split = nullptr; // [n_rows + 1]; [n_rows] = #split rows
-    int32_t *counters = nullptr;  // [4]: 0 close-degree rows, 1 chosen mode,
-                                  //      2 units longer than kTinyUnit, 3 zero
+    int32_t *counters = nullptr;  // [8]: 0 close-degree rows, 1 chosen mode,
+                                  //      2 units longer than kTinyUnit, 3 zero,
+                                  //      4 sliced plan: 1 when its rows were sliced
     uint32_t *sort_keys = nullptr;   // [4 * cap_units]: keys, 2 ping buffers, sorted keys
     uint32_t *sort_vals = nullptr;   // [3 * cap_units]: order, then 2 ping buffers
     void *sort_ws = nullptr;
@@ -51,6 +55,22 @@ struct Plan {
     float *gstats = nullptr;      // [cap_partials * max_heads * 2] per-group (m, z)
     float *rstats = nullptr;      // [cap_split * max_heads * 2] per-split-row (m, z)
 
+    // Sliced plans (cogdl_plan_create_sliced): in neighbour-group mode a row
+    // with more than slice_min edges is cut at the boundaries of kSlices equal
+    // column ranges (then into groups of at most group_size edges), and the
+    // units form kSlices lists, slice s in list s and every other unit in list
+    // row % kSlices, so that each list's gathers stay inside one column range.
+    int32_t sliced = 0;
+    int32_t n_cols = 0;
+    int32_t slice_min = 0;
+    int32_t key_bits = 0;         // bits of the in-list sort key (group_size - size)
+    void *base2 = nullptr;        // second allocation (sliced plans)
+    int32_t *lists_tbl = nullptr; // [3 * kSlices]: list starts, ends of the long units, list ends
+    int32_t *alt_units = nullptr; // [n_rows + 1] x 3: the unsliced counts, used when the
+    int32_t *alt_parts = nullptr; //   sliced ones exceed the capacities
+    int32_t *alt_split = nullptr;
+    int32_t *row_cuts = nullptr;  // [n_rows][kSlices - 1]: the inner cuts of each sliced row
+
     const int32_t *n_units_dev() const { return row_units + n_rows; }
     const int32_t *n_big_dev() const { return counters + 2; }
     const int32_t *zero_dev() const { return counters + 3; }
@@ -60,6 +80,48 @@ struct Plan {
 
 // Units of at most this many edges run in the narrow-sub-group path.
 constexpr int kTinyUnit = 8;
+
+// The unit ranges a launch walks (see unit_walk): the long units, the tiny
+// units or all of them; one range, or one per list for a sliced plan.
+struct UnitRange {
+    const int32_t *lo;
+    const int32_t *hi;
+    int lists;
+};
+
+inline UnitRange long_units(const Plan &P)
+{
+    if (P.sliced) return {P.lists_tbl, P.lists_tbl + kSlices, kSlices};
+    return {P.zero_dev(), P.n_big_dev(), 1};
+}
+
+inline UnitRange tiny_units(const Plan &P)
+{
+    if (P.sliced) return {P.lists_tbl + kSlices, P.lists_tbl + 2 * kSlices, kSlices};
+    return {P.n_big_dev(), P.n_units_dev(), 1};
+}
+
+inline UnitRange all_units(const Plan &P)
+{
+    if (P.sliced) return {P.lists_tbl, P.lists_tbl + 2 * kSlices, kSlices};
+    return {P.zero_dev(), P.n_units_dev(), 1};
+}
+
+template <typename Args>
+inline void set_units(Args &a, const UnitRange &r)
+{
+    a.u_lo = r.lo;
+    a.u_hi = r.hi;
+    a.lists = r.lists;
+}
+
+// A grid of `blocks` workgroups adjusted for `lists` lists: a multiple of it.
+inline int64_t list_grid(int64_t blocks, int lists)
+{
+    if (lists <= 1) return blocks > 0 ? blocks : 1;
+    const int64_t b = blocks / lists * lists;
+    return b < lists ? lists : b;
+}
 
 const Plan *plan_of(const cogdl_plan *h);
 

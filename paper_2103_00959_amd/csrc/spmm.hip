@@ -220,8 +220,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     const RowMap m = row_map(F, dtype_bytes(xdt), F, aligned);
     SpmmArgs a;
     a.units = P ? P->units : nullptr;
-    a.u_lo = P ? P->zero_dev() : nullptr;
-    a.u_hi = P ? P->n_units_dev() : nullptr;
+    a.u_lo = nullptr;
+    a.u_hi = nullptr;
     a.n_rows = out_rows;
     a.rowptr = ptr;
     a.col = idx;
@@ -250,7 +250,7 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
     // Units of at most kTinyUnit edges (the sorted tail) run with S/4 lanes and
     // four chunks per lane: four times as many rows in flight per wavefront.
     const bool tiny = P && m.ch == 1 && m.S >= 8;
-    if (tiny) a.u_hi = P->n_big_dev();
+    if (P) set_units(a, tiny ? long_units(*P) : all_units(*P));
     {
         const int64_t upb = kBlock >> m.log2S;
         SpmmKernel k = pick(m.ch);
@@ -258,13 +258,12 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(names.main, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
-                     kBlock, s, a);
+        blocks = list_grid(blocks, a.lists);
+        COGDL_LAUNCH(names.main, k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, s, a);
     }
     if (tiny) {
         SpmmArgs b = a;
-        b.u_lo = P->n_big_dev();
-        b.u_hi = P->n_units_dev();
+        set_units(b, tiny_units(*P));
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
         SpmmKernel k = pick(4);
@@ -272,8 +271,8 @@ cogdl_status spmm_common(int32_t out_rows, int32_t in_rows, int64_t nnz, const i
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
-        COGDL_LAUNCH(names.tiny, k, dim3((unsigned)(blocks > 0 ? blocks : 1), (unsigned)m.n_slabs),
-                     kBlock, s, b);
+        blocks = list_grid(blocks, b.lists);
+        COGDL_LAUNCH(names.tiny, k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, s, b);
     }
     if (!P) return COGDL_OK;
     if (maxr) return max_reduce_launch(names.reduce, *P, F, Y, ydt, bias, act, a.arg, s);

@@ -14,7 +14,8 @@ constexpr int kSpmmBlock = 256;
 struct SpmmArgs {
     const int4 *units;          // nullptr: one unit per row in row order
     const int32_t *u_lo;        // with units: this launch runs units [*u_lo, *u_hi)
-    const int32_t *u_hi;
+    const int32_t *u_hi;        // (lists > 1: list x is [u_lo[x], u_hi[x]), see unit_walk)
+    int32_t lists = 1;
     int32_t n_rows;
     const int32_t *rowptr;
     const int32_t *col;
@@ -78,10 +79,10 @@ __global__ __launch_bounds__(kSpmmBlock) void k_spmm(SpmmArgs a)
     const int lane = lane_id();
     const int lig = lane & (S - 1);
     const int gbase = lane & ~(S - 1);
-    const int64_t sub = (int64_t)blockIdx.x * (kSpmmBlock >> log2S) + (threadIdx.x >> log2S);
-    const int64_t stride = (int64_t)gridDim.x * (kSpmmBlock >> log2S);
-    const int64_t lo = a.units ? *a.u_lo : 0;
-    const int64_t hi = a.units ? *a.u_hi : a.n_rows;
+    const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows,
+                                    kSpmmBlock >> log2S, threadIdx.x >> log2S);
+    const int64_t stride = walk.step;
+    const int64_t hi = walk.end;
 
     const int64_t f0 = (int64_t)blockIdx.y * a.slab;
     const int64_t f_end = (f0 + a.slab < a.F) ? f0 + a.slab : a.F;
@@ -96,12 +97,12 @@ __global__ __launch_bounds__(kSpmmBlock) void k_spmm(SpmmArgs a)
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ val = a.val;
 
-    // Resident grid: sub-group i runs units lo + i, lo + i + stride, ...; the
-    // units are sorted by length, so neighbouring sub-groups get equal work.
+    // Resident grid: sub-group i of a list runs its units i, i + stride, ...;
+    // the units are sorted by length, so neighbouring sub-groups get equal work.
     // The loop is software-pipelined: the next unit's descriptor is fetched
     // when a unit starts and its first index chunk before the current output
     // is stored, so short units do not pay three dependent memory trips each.
-    int64_t u = lo + sub;
+    int64_t u = walk.first;
     if (u >= hi) return;
     int4 d = fetch_unit(a, u, hi);
     int c_cur = 0;

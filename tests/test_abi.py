@@ -283,3 +283,29 @@ def test_missing_library_fails_loudly(monkeypatch):
     col = torch.zeros(0, dtype=torch.int32)
     with pytest.raises(Exception):
         cg.spmm(rowptr, col, None, torch.zeros((2, 4)))
+
+
+def test_sliced_plan_validation(L):
+    """Column-sliced plans: bad arguments are refused before anything is allocated."""
+    h = ctypes.c_void_p()
+    P = ctypes.c_void_p
+    args = dict(n_rows=4, nnz=8, rowptr=FAKE, col=FAKE, n_cols=4, max_feat=8, max_heads=0, mode=0,
+                group_size=0, slice_min=0)
+
+    def create(**kw):
+        a = dict(args, **kw)
+        return L.cogdl_plan_create_sliced(a["n_rows"], a["nnz"], a["rowptr"], a["col"], a["n_cols"],
+                                          a["max_feat"], a["max_heads"], a["mode"], a["group_size"],
+                                          a["slice_min"], None, ctypes.byref(h))
+    assert create(col=None) == INVALID
+    assert create(n_cols=0) == INVALID
+    assert create(n_cols=-1) == INVALID
+    assert create(slice_min=-1) == INVALID
+    assert create(group_size=(1 << 24) + 1) == INVALID
+    assert create(max_feat=0) == INVALID
+    assert create(mode=7) == INVALID
+    assert create(nnz=_max_nnz() + 1) == TOO_LARGE
+    assert L.cogdl_plan_create_sliced(4, 8, FAKE, FAKE, 4, 8, 0, 0, 0, 0, None, None) == INVALID
+    assert L.cogdl_plan_rebuild_sliced(None, FAKE, FAKE, None) == INVALID
+    assert L.cogdl_plan_rebuild(None, FAKE, None) == INVALID
+    del P
