@@ -208,7 +208,7 @@ def run_inference(cg, synth, dev, time_op_kernels):
         p = synth.model_params(kind, k, hid, C, Hh, seed=7100 if kind == "gcn" else 7200)
         params[kind] = {n: (bf16(v) if n.startswith("W") else torch.from_numpy(v).to(dev))
                         for n, v in p.items()}
-    plan = cg.Plan(rowptr, E, max_feat=hid, max_heads=Hh)
+    plan = cg.Plan(rowptr, E, max_feat=hid, max_heads=Hh, col=col, n_cols=N)
     torch.cuda.synchronize()
     ms_gcn, k_gcn = time_op_kernels(lambda: cg.gcn_forward(rowptr, col, val, X, params["gcn"], plan=plan))
     ms_gat, k_gat = time_op_kernels(lambda: cg.gat_forward(rowptr, col, X, params["gat"], spec["slope"],
@@ -288,8 +288,8 @@ def oracle_rate(run, units, budget_s, chunk=256, full=False):
 
 
 def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
-    """Each workload's operators in its own configuration (fp32 features; plans on AUTO with
-    the default group size), one JSON line per (workload, op).  Cold: a 1 GiB buffer is
+    """Each workload's operators in its own configuration (fp32 features; column-sliced plans
+    on AUTO with the default group size), one JSON line per (workload, op).  Cold: a 1 GiB buffer is
     written before every timed call, so L2 and the Infinity Cache hold none of its inputs;
     warm: the same call back to back.  Median and minimum of `reps` calls after `warm_reps`
     untimed ones; plan creation and the transpose are preprocessing, reported on their own.
@@ -391,7 +391,7 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
                "cold_edges_per_s": E / (mc * 1e-3) if E else None,
                "cold_GFLOPps": flop / (mc * 1e-3) / 1e9 if flop else None,
                "cache_resident": (table_bytes <= (256 << 20)) if table_bytes else None,
-               "copy_GBps": copy_GBps, "launches_per_call": launches,
+               "copy_GBps": copy_GBps, "launches_per_call": launches, "plans": "column-sliced",
                "hbm_GBps": None, "l2_hit": None, "cpu_oracle": cpu_rec}
         h = hbm.get(f"{cfg['name']}/{op}") if hbm else None
         if h:
@@ -412,7 +412,7 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
         val = up(g.val) if g.val is not None else None
         t0 = time.perf_counter()
         plan = cg.Plan(rowptr, E, max_feat=max(cfg.get("F", 1), cfg.get("H", 1) * cfg.get("D", 1)),
-                       max_heads=cfg.get("H", 0))
+                       max_heads=cfg.get("H", 0), col=col, n_cols=M)
         torch.cuda.synchronize()
         log(f"{cfg['name']}: plan created in {(time.perf_counter() - t0) * 1e3:.1f} ms (host clock)")
         res = times(lambda: plan.rebuild(rowptr))
@@ -446,7 +446,7 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
                     return b_csc(N, M, E), E
                 record(k, cfg, "csr_to_csc", b_csc(N, M, E), b_csc(N, M, E), E, 0, 0, res,
                        oracle_line(k, run_csc, M, True, False))
-                plan_t = cg.Plan(colptr, E, max_feat=F)
+                plan_t = cg.Plan(colptr, E, max_feat=F, col=row_t, n_cols=N)
                 Gn = synth.normal_f32((N, F), 4000 + k)
                 G = up(Gn)
                 dX = torch.empty((M, F), dtype=torch.float32, device=dev)

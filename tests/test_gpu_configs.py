@@ -131,9 +131,11 @@ def test_gat_layer_sampled(cg):
 
 
 @pytest.mark.timeout(900)
-def test_skewed_mixed_precision_sampled(cg):
+@pytest.mark.parametrize("sliced", [True, False])
+def test_skewed_mixed_precision_sampled(cg, sliced):
     """2.4M nodes, 122.4M nonzeros with 100k-300k-edge hubs, bf16 features:
-    the benchmark's launch configuration (SpMM, transpose, SpMM^T, fused GAT)."""
+    the benchmark's launch configuration (SpMM, transpose, SpMM^T, fused GAT;
+    column-sliced plans as the benchmark builds them, and plain ones)."""
     import torch
     g = synth.config_graph(5, verbose=True)
     N, E = g.n_rows, g.nnz
@@ -141,7 +143,7 @@ def test_skewed_mixed_precision_sampled(cg):
     say(f"skewed n={N} nnz={E}")
     rp, cl, vl = dev(g.rowptr), dev(g.col), dev(g.val)
     xh, xc, xd = features((N, F), 2005, "bf16")
-    plan = cg.Plan(rp, E, max_feat=F, max_heads=H)
+    plan = cg.Plan(rp, E, max_feat=F, max_heads=H, **(dict(col=cl, n_cols=N) if sliced else {}))
     rows = _sample_rows(g)
     idx = torch.from_numpy(rows).long().cuda()
     try:
@@ -178,7 +180,7 @@ def test_skewed_mixed_precision_sampled(cg):
     assert np.array_equal(val_t.cpu().numpy().view(np.uint32), v_ref.view(np.uint32))
     del c_ref, r_ref, v_ref, p_ref
     gh, gc, gd = features((N, F), 4005, "bf16")
-    plan_t = cg.Plan(colptr, E, max_feat=F)
+    plan_t = cg.Plan(colptr, E, max_feat=F, **(dict(col=row_t, n_cols=N) if sliced else {}))
     try:
         dX = cg.spmm_t(colptr, row_t, val_t, gd, plan_t=plan_t, out_dtype=torch.float32)
         cdeg = np.diff(c_ref_cols := colptr.cpu().numpy())
@@ -195,7 +197,8 @@ def test_skewed_mixed_precision_sampled(cg):
 
 
 @pytest.mark.timeout(900)
-def test_gat_backward_skewed_sampled(cg):
+@pytest.mark.parametrize("sliced", [True, False])
+def test_gat_backward_skewed_sampled(cg, sliced):
     """2.4M nodes, 122.4M nonzeros with hubs, H = 4 x D = 64 bf16: the GAT
     backward in the benchmark's launch configuration, compared on sampled rows
     (attention and score gradients, ds_dst) and sampled columns (ds_src, dX),
@@ -213,8 +216,8 @@ def test_gat_backward_skewed_sampled(cg):
     xh, xc, xd = features((N, H, D), 2205, "bf16")
     gh, gc, gd = features((N, H, D), 4105, "bf16")
     colptr, row_t, _, perm = cg.csr_to_csc(rp, cl, None, N)
-    plan = cg.Plan(rp, E, max_feat=H * D, max_heads=H)
-    plan_t = cg.Plan(colptr, E, max_feat=H * D, max_heads=H)
+    plan = cg.Plan(rp, E, max_feat=H * D, max_heads=H, **(dict(col=cl, n_cols=N) if sliced else {}))
+    plan_t = cg.Plan(colptr, E, max_feat=H * D, max_heads=H, **(dict(col=row_t, n_cols=N) if sliced else {}))
     try:
         out = cg.gat_backward(rp, cl, colptr, row_t, perm, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
                               plan=plan, plan_t=plan_t)
