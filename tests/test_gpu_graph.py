@@ -33,8 +33,8 @@ def _graph(seed):
     return synth.Graph(rowptr, col, rng.standard_normal(col.size).astype(np.float32), 2000, 2000)
 
 
-@pytest.mark.parametrize("seed", [1, 2])
-def test_step_under_graph_capture(cg, seed):
+@pytest.mark.parametrize("seed,sliced", [(1, False), (2, False), (3, True), (4, True)])
+def test_step_under_graph_capture(cg, seed, sliced):
     import torch
     g = _graph(seed)
     N, E = g.n_rows, g.nnz
@@ -56,7 +56,8 @@ def test_step_under_graph_capture(cg, seed):
     perm = torch.empty(E, dtype=torch.int32, device="cuda")
     ws = torch.empty(cg.csr_to_csc_workspace(N, N, E), dtype=torch.uint8, device="cuda")
     L = cg.lib()
-    plan = cg.Plan(rp, E, max_feat=F, max_heads=H, mode="neighbor_group", group_size=64)
+    plan = cg.Plan(rp, E, max_feat=F, max_heads=H, mode="neighbor_group", group_size=64,
+                   **(dict(col=cl, n_cols=N, slice_min=32) if sliced else {}))
 
     def csc():
         cg._check(L.cogdl_csr_to_csc(N, N, E, cg._ptr(rp), cg._ptr(cl), cg._ptr(vl), cg._ptr(colptr),
@@ -64,7 +65,8 @@ def test_step_under_graph_capture(cg, seed):
                                      ws.numel(), cg._stream()), "csr_to_csc")
 
     csc()
-    plan_t = cg.Plan(colptr, E, max_feat=F, max_heads=H, mode="neighbor_group", group_size=64)
+    plan_t = cg.Plan(colptr, E, max_feat=F, max_heads=H, mode="neighbor_group", group_size=64,
+                     **(dict(col=row_t, n_cols=N, slice_min=32) if sliced else {}))
 
     def step():
         plan.rebuild(rp)
