@@ -259,10 +259,10 @@ __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
 }
 
 // GAT split rows: combine the groups' unnormalized sums with the log-sum-exp
-// rule, write Y and the row's (m, z) for the alpha pass.  One workgroup per
-// split row; every wavefront merges the (m, z) states (cheap, identical), then
-// wavefront w adds the groups g = w, w + 4, ... scaled by exp(m_g - m), and the
-// four sums are combined in wavefront order through LDS.
+// rule, write Y and the row's (m, z) for the alpha pass.  A wavefront per
+// split row: it merges the groups' (m, z) states, then group g, scaled by
+// exp(m_g - m), goes to chain g mod 4; the chains add their groups in
+// increasing order and are combined as (c0 + c1) + (c2 + c3).
 template <typename TY, int VEC>
 __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ split_rows,
                                                        const int32_t *__restrict__ n_split,
@@ -274,19 +274,18 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
                                                        const float *__restrict__ bias, int act_code,
                                                        TY *__restrict__ Y)
 {
-    constexpr int kW = kBlock / kWave;
-    __shared__ float red[kW][kWave * VEC];
     const int lane = lane_id();
-    const int w = threadIdx.x / kWave;
     const int64_t W = (int64_t)H * D;
     const int32_t ns = *n_split;
-    for (int64_t s = blockIdx.x; s < ns; s += gridDim.x) {
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns;
+         s += waves) {
         const int4 d = split_rows[s];
         const int64_t row = d.x;
         const int p0 = d.y, np = d.z;
         float m, z;
         merge_groups(gstats, sstride, p0, np, H, m, z);   // lane h holds head h
-        if (w == 0 && lane < H) {
+        if (lane < H) {
             rstats[s * sstride + lane] = m;
             rstats[s * sstride + (sstride >> 1) + lane] = z;
         }
@@ -296,49 +295,42 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
             const int h = act ? (int)(f / D) : 0;
             const float M = lane_bcast(m, h);
             const float rZ = 1.f / lane_bcast(z, h);
-            float a0[VEC], a1[VEC];
+            if (!act) continue;
+            float c[4][VEC];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) a0[e] = a1[e] = 0.f;
-            if (act) {
-                int g = w;
-                for (; g + kW < np; g += 2 * kW) {
-                    const int64_t q0 = p0 + g, q1 = q0 + kW;
-                    const float s0 = __expf(gstats[q0 * sstride + h] - M);
-                    const float s1 = __expf(gstats[q1 * sstride + h] - M);
-                    float x0[VEC], x1[VEC];
-                    load_vec<float, VEC>(partials, q0 * pstride + f, x0);
-                    load_vec<float, VEC>(partials, q1 * pstride + f, x1);
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        a0[e] = fmaf(x0[e], s0, a0[e]);
-                        a1[e] = fmaf(x1[e], s1, a1[e]);
-                    }
+                for (int e = 0; e < VEC; ++e) c[j][e] = 0.f;
+            int g = 0;
+            for (; g + 4 <= np; g += 4) {
+                float x[4][VEC], sc[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t q = p0 + g + j;
+                    sc[j] = __expf(gstats[q * sstride + h] - M);
+                    load_vec<float, VEC>(partials, q * pstride + f, x[j]);
                 }
-                if (g < np) {
-                    const int64_t q0 = p0 + g;
-                    const float s0 = __expf(gstats[q0 * sstride + h] - M);
-                    float x0[VEC];
-                    load_vec<float, VEC>(partials, q0 * pstride + f, x0);
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) a0[e] = fmaf(x0[e], s0, a0[e]);
-                }
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) c[j][e] = fmaf(x[j][e], sc[j], c[j][e]);
             }
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) red[w][lane * VEC + e] = a0[e] + a1[e];
-            __syncthreads();
-            if (w == 0 && act) {
-                float v[VEC];
+            for (int j = 0; j < 3; ++j) {
+                if (g + j < np) {
+                    const int64_t q = p0 + g + j;
+                    const float sc = __expf(gstats[q * sstride + h] - M);
+                    float x[VEC];
+                    load_vec<float, VEC>(partials, q * pstride + f, x);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    float t = red[0][lane * VEC + e];
-#pragma unroll
-                    for (int i = 1; i < kW; ++i) t += red[i][lane * VEC + e];
-                    v[e] = t * rZ;
+                    for (int e = 0; e < VEC; ++e) c[j][e] = fmaf(x[e], sc, c[j][e]);
                 }
-                epilogue<VEC>(v, bias, act_code, f);
-                store_out<TY, VEC>(Y, row * W + f, v);
             }
-            __syncthreads();
+            float v[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) v[e] = ((c[0][e] + c[1][e]) + (c[2][e] + c[3][e])) * rZ;
+            epilogue<VEC>(v, bias, act_code, f);
+            store_out<TY, VEC>(Y, row * W + f, v);
         }
     }
 }
@@ -526,8 +518,7 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     if (!P) return COGDL_OK;
 
     if (!soft) return sum_reduce_launch("gat_sum_reduce", *P, W, Y, y_dtype, false, bias, act, stream);
-    const int64_t rblocks = P->cap_split < 4096 ? P->cap_split : 4096;
-    const unsigned rb = (unsigned)(rblocks < 1 ? 1 : rblocks);
+    const unsigned rb = grid_waves(P->cap_split);
     const bool v4 = D % 4 == 0 && (uintptr_t)Y % (4 * dtype_bytes(y_dtype)) == 0;
 #define COGDL_GAT_REDUCE(TY, V)                                                                  \
     COGDL_LAUNCH("gat_reduce", (k_gat_reduce<TY, V>), rb, kBlock, stream, P->split_rows,         \

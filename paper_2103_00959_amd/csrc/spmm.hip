@@ -25,12 +25,14 @@ namespace {
 
 constexpr int kBlock = kSpmmBlock;
 
-// Y[row, :] = sum of the row's partial rows (times 1 / degree for mean).  One
-// workgroup per split row (grid-stride over the device-side count, uniform
-// per workgroup): wavefront w adds the slots g = w, w + 4, ... in increasing
-// order on two interleaved chains, VEC features per lane, and the four
-// wavefront sums are added in wavefront order through LDS, so the result does
-// not depend on timing.
+// Y[row, :] = sum of the row's partial rows (times 1 / degree for mean).  A
+// wavefront per split row (grid-stride over the device-side count, uniform
+// per wavefront), VEC features per lane: slot g goes to chain g mod 4, the
+// four chains add their slots in increasing order and are combined as
+// (c0 + c1) + (c2 + c3), so the result does not depend on timing.  Four
+// slots' loads are in flight per step, and a workgroup's four wavefronts work
+// on four different rows (column-sliced plans make a hundred thousand short
+// split rows, where a workgroup per row waited on its own barrier).
 template <typename TY, int VEC>
 __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__ split_rows,
                                                         const int32_t *__restrict__ n_split,
@@ -39,55 +41,51 @@ __global__ __launch_bounds__(kBlock) void k_spmm_reduce(const int4 *__restrict__
                                                         const float *__restrict__ bias, int act_code,
                                                         TY *__restrict__ Y)
 {
-    constexpr int kW = kBlock / kWave;
-    __shared__ float red[kW][kWave * VEC];
     const int lane = lane_id();
-    const int w = threadIdx.x / kWave;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
     const int32_t ns = *n_split;
-    for (int64_t s = blockIdx.x; s < ns; s += gridDim.x) {
+    for (int64_t s = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; s < ns;
+         s += waves) {
         const int4 d = split_rows[s];
         const int64_t row = d.x, p0 = d.y;
         const int np = d.z;
         const float scale = (mean && d.w > 0) ? 1.f / (float)d.w : 1.f;
         for (int64_t fb = 0; fb < F; fb += kWave * VEC) {
             const int64_t f = fb + (int64_t)lane * VEC;
-            const bool act = f < F;
-            float a0[VEC], a1[VEC];
+            if (f >= F) continue;
+            float c[4][VEC];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) a0[e] = a1[e] = 0.f;
-            if (act) {
-                const float *p = partials + p0 * pstride + f;
-                int g = w;
-                for (; g + kW < np; g += 2 * kW) {
-                    float x0[VEC], x1[VEC];
-                    load_vec<float, VEC>(p, (int64_t)g * pstride, x0);
-                    load_vec<float, VEC>(p, (int64_t)(g + kW) * pstride, x1);
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) { a0[e] += x0[e]; a1[e] += x1[e]; }
-                }
-                if (g < np) {
-                    float x0[VEC];
-                    load_vec<float, VEC>(p, (int64_t)g * pstride, x0);
+                for (int e = 0; e < VEC; ++e) c[j][e] = 0.f;
+            const float *p = partials + p0 * pstride + f;
+            int g = 0;
+            for (; g + 4 <= np; g += 4) {
+                float x[4][VEC];
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) a0[e] += x0[e];
-                }
+                for (int j = 0; j < 4; ++j) load_vec<float, VEC>(p, (int64_t)(g + j) * pstride, x[j]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) c[j][e] += x[j][e];
             }
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) red[w][lane * VEC + e] = a0[e] + a1[e];
-            __syncthreads();
-            if (w == 0 && act) {
-                float v[VEC];
+            for (int j = 0; j < 3; ++j) {
+                if (g + j < np) {
+                    float x[VEC];
+                    load_vec<float, VEC>(p, (int64_t)(g + j) * pstride, x);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    v[e] = red[0][lane * VEC + e];
-#pragma unroll
-                    for (int i = 1; i < kW; ++i) v[e] += red[i][lane * VEC + e];
-                    if (mean) v[e] *= scale;
+                    for (int e = 0; e < VEC; ++e) c[j][e] += x[e];
                 }
-                epilogue<VEC>(v, bias, act_code, f);
-                store_out<TY, VEC>(Y, row * F + f, v);
             }
-            __syncthreads();
+            float v[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                v[e] = (c[0][e] + c[1][e]) + (c[2][e] + c[3][e]);
+                if (mean) v[e] *= scale;
+            }
+            epilogue<VEC>(v, bias, act_code, f);
+            store_out<TY, VEC>(Y, row * F + f, v);
         }
     }
 }
@@ -134,8 +132,9 @@ cogdl_status reduce_launch_v(const char *name, const Plan &P, int64_t F, void *Y
                              bool mean, const float *bias, int act, hipStream_t s)
 {
     const int64_t pstride = (P.max_feat + 7) / 8 * 8;
-    int64_t blocks = P.cap_split;
-    if (blocks > 4096) blocks = 4096;
+    constexpr int wpb = kBlock / kWave;
+    int64_t blocks = (P.cap_split + wpb - 1) / wpb;
+    if (blocks > 2048) blocks = 2048;
     if (blocks < 1) blocks = 1;
     const unsigned b = (unsigned)blocks;
     const int mn = mean ? 1 : 0;
