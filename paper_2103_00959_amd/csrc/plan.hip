@@ -9,7 +9,15 @@
 //   3. orders the units longest first (a stable sort, so equal lengths keep
 //      row order) so that wavefronts sharing a workgroup get equal work and
 //      the heaviest units start first.
-// Every count stays on the device: no host synchronization, nothing read back.
+// Every count stays on the device: no host synchronization, nothing read back
+// (a column-sliced plan reads its unit totals back once, at creation, to size
+// itself).
+//
+// Column-sliced plans (an MI355X addition, cogdl_plan_create_sliced): in
+// neighbour-group mode a row with more than slice_min edges is also cut at the
+// boundaries of kSlices equal column ranges, and the units form kSlices lists
+// (range s in list s, every other unit in list row % kSlices), sorted by
+// (list, length), each walked by the workgroups of one XCD.
 #include <new>
 
 #include "common.hpp"
