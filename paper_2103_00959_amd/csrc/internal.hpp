@@ -70,6 +70,8 @@ struct Plan {
     int32_t *alt_parts = nullptr; //   sliced ones exceed the capacities
     int32_t *alt_split = nullptr;
     int32_t *row_cuts = nullptr;  // [n_rows][kSlices - 1]: the inner cuts of each sliced row
+    unsigned long long *totals = nullptr;  // [3]: sliced units, partial slots, split rows
+    unsigned long long *block_totals = nullptr;  // [3 per workgroup of the count pass]
 
     const int32_t *n_units_dev() const { return row_units + n_rows; }
     const int32_t *n_big_dev() const { return counters + 2; }

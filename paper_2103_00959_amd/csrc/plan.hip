@@ -162,21 +162,16 @@ __device__ __forceinline__ void slice_cuts(const int32_t *__restrict__ col, int 
     cut[kSlices] = end;
 }
 
-// Per-row counts of a sliced plan: the sliced ones (a row with more than
-// slice_min edges gives ceil(len / G) units per nonempty slice) and, in the
-// alt arrays, the unsliced ones the build falls back to when the sliced
-// totals exceed the plan's capacities.
-__global__ void k_plan_counts_sliced(const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
-                                     int32_t n_rows, int32_t G, int req, int64_t width, int32_t slice_min,
-                                     int32_t *__restrict__ counters, int32_t *__restrict__ row_units,
-                                     int32_t *__restrict__ row_parts, int32_t *__restrict__ row_split,
-                                     int32_t *__restrict__ alt_units, int32_t *__restrict__ alt_parts,
-                                     int32_t *__restrict__ alt_split, int32_t *__restrict__ row_cuts)
+// The sliced unit count of row i (its cuts stored in row_cuts) after writing
+// its unsliced counts to the alt arrays.
+__device__ __forceinline__ int row_counts_sliced(const int32_t *__restrict__ rowptr,
+                                                      const int32_t *__restrict__ col, int i, int32_t G,
+                                                      int mode, int64_t width, int32_t slice_min,
+                                                      int32_t *__restrict__ alt_units,
+                                                      int32_t *__restrict__ alt_parts,
+                                                      int32_t *__restrict__ alt_split,
+                                                      int32_t *__restrict__ row_cuts)
 {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    const int mode = plan_mode(counters, n_rows, req);
-    if (i == 0) counters[1] = mode;
-    if (i >= n_rows) return;
     const int beg = rowptr[i], end = rowptr[i + 1];
     const int d = end - beg;
     const bool ng = mode == COGDL_BALANCE_NEIGHBOR_GROUP;
@@ -192,21 +187,87 @@ __global__ void k_plan_counts_sliced(const int32_t *__restrict__ rowptr, const i
 #pragma unroll
         for (int s = 1; s < kSlices; ++s) row_cuts[(int64_t)i * (kSlices - 1) + s - 1] = cut[s];
     }
-    row_units[i] = u;
-    row_parts[i] = u > 1 ? u : 0;
-    row_split[i] = u > 1 ? 1 : 0;
+    return u;
+}
+
+// Per-row counts of a sliced plan: the sliced ones (a row with more than
+// slice_min edges gives ceil(len / G) units per nonempty slice), summed per
+// workgroup into block_totals, and, in the alt arrays, the
+// unsliced ones the build falls back to when the sliced totals exceed the
+// plan's capacities.
+__global__ void k_plan_counts_sliced(const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+                                     int32_t n_rows, int32_t G, int req, int64_t width, int32_t slice_min,
+                                     int32_t *__restrict__ counters, int32_t *__restrict__ row_units,
+                                     int32_t *__restrict__ row_parts, int32_t *__restrict__ row_split,
+                                     int32_t *__restrict__ alt_units, int32_t *__restrict__ alt_parts,
+                                     int32_t *__restrict__ alt_split, int32_t *__restrict__ row_cuts,
+                                     unsigned long long *__restrict__ block_totals)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    const int mode = plan_mode(counters, n_rows, req);
+    if (i == 0) counters[1] = mode;
+    uint32_t su = 0, sp = 0, ss = 0;
+    if (i < n_rows) {
+        const int u = row_counts_sliced(rowptr, col, i, G, mode, width, slice_min, alt_units, alt_parts,
+                                        alt_split, row_cuts);
+        row_units[i] = u;
+        row_parts[i] = u > 1 ? u : 0;
+        row_split[i] = u > 1 ? 1 : 0;
+        su = (uint32_t)u;
+        sp = u > 1 ? (uint32_t)u : 0u;
+        ss = u > 1 ? 1u : 0u;
+    }
+    // workgroup sums, one slot per workgroup (k_plan_fit adds them up: atomics
+    // from every wavefront on three addresses serialize)
+    __shared__ uint32_t wsum[3][256 / kWave];
+    const auto add = [](uint32_t a, uint32_t b) { return a + b; };
+    su = group_reduce(su, kWave, add);
+    sp = group_reduce(sp, kWave, add);
+    ss = group_reduce(ss, kWave, add);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        wsum[0][w] = su;
+        wsum[1][w] = sp;
+        wsum[2][w] = ss;
+    }
+    __syncthreads();
+    if (threadIdx.x < 3) {
+        unsigned long long t = 0;
+        for (int j = 0; j < (int)(blockDim.x / kWave); ++j) t += wsum[threadIdx.x][j];
+        block_totals[(int64_t)blockIdx.x * 3 + threadIdx.x] = t;
+    }
 }
 
 // counters[4] = 1 when the sliced totals fit the capacities (else the
 // unsliced counts replace them and no row is sliced).
-__global__ void k_plan_fit(const int32_t *__restrict__ row_units, const int32_t *__restrict__ row_parts,
-                           const int32_t *__restrict__ row_split, int32_t n_rows, int64_t cap_units,
-                           int64_t cap_partials, int64_t cap_split, int32_t *__restrict__ counters)
+// The sliced totals (units, partial slots, split rows) from the workgroup sums
+// of k_plan_counts_sliced, in a fixed order (one workgroup of 256 threads).
+__global__ __launch_bounds__(256) void k_plan_fit(const unsigned long long *__restrict__ block_totals,
+                                                  int64_t n_blocks, int64_t cap_units, int64_t cap_partials,
+                                                  int64_t cap_split, unsigned long long *__restrict__ totals,
+                                                  int32_t *__restrict__ counters)
 {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    const bool fits = row_units[n_rows] <= cap_units && row_parts[n_rows] <= cap_partials &&
-                      row_split[n_rows] <= cap_split;
-    counters[4] = fits ? 1 : 0;
+    __shared__ unsigned long long part[3][256];
+    unsigned long long t[3] = {0, 0, 0};
+    for (int64_t b = threadIdx.x; b < n_blocks; b += blockDim.x)
+#pragma unroll
+        for (int c = 0; c < 3; ++c) t[c] += block_totals[b * 3 + c];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) part[c][threadIdx.x] = t[c];
+    __syncthreads();
+    if (threadIdx.x < 3) {
+        unsigned long long sum = 0;
+        for (int j = 0; j < (int)blockDim.x; ++j) sum += part[threadIdx.x][j];
+        totals[threadIdx.x] = sum;
+        part[threadIdx.x][0] = sum;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const bool fits = part[0][0] <= (unsigned long long)cap_units &&
+                          part[1][0] <= (unsigned long long)cap_partials &&
+                          part[2][0] <= (unsigned long long)cap_split;
+        counters[4] = fits ? 1 : 0;
+    }
 }
 
 __global__ void k_plan_fallback(int32_t n_rows, const int32_t *__restrict__ counters,
@@ -215,7 +276,7 @@ __global__ void k_plan_fallback(int32_t n_rows, const int32_t *__restrict__ coun
                                 const int32_t *__restrict__ alt_parts, const int32_t *__restrict__ alt_split)
 {
     if (counters[4] != 0) return;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= n_rows;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_rows;
          i += (int64_t)gridDim.x * blockDim.x) {
         row_units[i] = alt_units[i];
         row_parts[i] = alt_parts[i];
@@ -356,9 +417,10 @@ cogdl_status plan_counts_sliced(Plan &P, const int32_t *rowptr, const int32_t *c
     const int64_t width = ((int64_t)P.n_cols + kSlices - 1) / kSlices;
     COGDL_LAUNCH("plan_counts", k_plan_counts_sliced, blocks, 256, s, rowptr, col, n, P.group_size,
                  (int)P.mode_req, width > 0 ? width : 1, P.slice_min, P.counters, P.row_units,
-                 P.row_parts, P.row_split, P.alt_units, P.alt_parts, P.alt_split, P.row_cuts);
-    COGDL_HIP_TRY(exclusive_scan3(P.row_units, P.row_parts, P.row_split, n, P.scan_ws, s));
-    COGDL_HIP_TRY(exclusive_scan3(P.alt_units, P.alt_parts, P.alt_split, n, P.scan_ws, s));
+                 P.row_parts, P.row_split, P.alt_units, P.alt_parts, P.alt_split, P.row_cuts,
+                 P.block_totals);
+    COGDL_LAUNCH("plan_fit", k_plan_fit, 1, 256, s, P.block_totals, (int64_t)blocks, P.cap_units,
+                 P.cap_partials, P.cap_split, P.totals, P.counters);
     return COGDL_OK;
 }
 
@@ -385,11 +447,10 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, const int32_t *col, hipS
     if (P.sliced) {
         const cogdl_status st = plan_counts_sliced(P, rowptr, col, s);
         if (st != COGDL_OK) return st;
-        COGDL_LAUNCH("plan_fit", k_plan_fit, 1, 64, s, P.row_units, P.row_parts, P.row_split, n,
-                     P.cap_units, P.cap_partials, P.cap_split, P.counters);
         COGDL_LAUNCH("plan_fallback", k_plan_fallback, blocks < 1024 ? blocks : 1024, 256, s, n,
                      P.counters, P.row_units, P.row_parts, P.row_split, P.alt_units, P.alt_parts,
                      P.alt_split);
+        COGDL_HIP_TRY(exclusive_scan3(P.row_units, P.row_parts, P.row_split, n, P.scan_ws, s));
         COGDL_LAUNCH("plan_emit", k_plan_emit_sliced, blocks, 256, s, rowptr, n, G, kb, P.slice_min,
                      P.row_cuts, P.counters, P.row_units, P.row_parts, P.row_split, P.units_tmp,
                      P.sort_keys, P.split_rows, P.part_units);
@@ -484,11 +545,13 @@ size_t row_layout(Plan &P, char *b, bool assign)
     const size_t o_counters = take(4 * 8);
     P.scan_ws_bytes = scan_workspace_bytes(P.n_rows, 3);
     const size_t o_scan_ws = take(P.scan_ws_bytes);
-    size_t o_alt = 0, o_tbl = 0, o_cuts = 0;
+    size_t o_alt = 0, o_tbl = 0, o_cuts = 0, o_tot = 0, o_btot = 0;
     if (P.sliced) {
         o_alt = take(3 * rows);
         o_tbl = take(4 * 3 * kSlices);
         o_cuts = take(4 * (kSlices - 1) * (size_t)P.n_rows);
+        o_tot = take(8 * 3);
+        o_btot = take(8 * 3 * (((size_t)P.n_rows + 255) / 256 + 1));
     }
     if (assign) {
         P.row_units = reinterpret_cast<int32_t *>(b + o_row_units);
@@ -502,6 +565,8 @@ size_t row_layout(Plan &P, char *b, bool assign)
             P.alt_split = P.alt_parts + (P.n_rows + 1);
             P.lists_tbl = reinterpret_cast<int32_t *>(b + o_tbl);
             P.row_cuts = reinterpret_cast<int32_t *>(b + o_cuts);
+            P.totals = reinterpret_cast<unsigned long long *>(b + o_tot);
+            P.block_totals = reinterpret_cast<unsigned long long *>(b + o_btot);
         }
     }
     return off;
@@ -634,7 +699,7 @@ cogdl_status cogdl_plan_create_sliced(int32_t n_rows, int64_t nnz, const int32_t
     P.cap_split = nnz / G + 1;
     P.cap_partials = 2 * (nnz / G) + 2;
     if (n_rows > 0) {
-        int32_t tot[3] = {0, 0, 0};
+        unsigned long long tot[3] = {0, 0, 0};
         const unsigned blocks = (unsigned)((n_rows + 255) / 256);
         cogdl_status st = COGDL_OK;
         if (cogdl::fill_i32(P.counters, 8, 0, stream) != hipSuccess) st = COGDL_ERR_LAUNCH;
@@ -645,18 +710,16 @@ cogdl_status cogdl_plan_create_sliced(int32_t n_rows, int64_t nnz, const int32_t
         }
         if (st == COGDL_OK) st = cogdl::plan_counts_sliced(P, rowptr, col, stream);
         if (st == COGDL_OK &&
-            (hipMemcpyAsync(&tot[0], P.row_units + n_rows, 4, hipMemcpyDeviceToHost, stream) != hipSuccess ||
-             hipMemcpyAsync(&tot[1], P.row_parts + n_rows, 4, hipMemcpyDeviceToHost, stream) != hipSuccess ||
-             hipMemcpyAsync(&tot[2], P.row_split + n_rows, 4, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+            (hipMemcpyAsync(&tot[0], P.totals, sizeof(tot), hipMemcpyDeviceToHost, stream) != hipSuccess ||
              hipStreamSynchronize(stream) != hipSuccess))
             st = COGDL_ERR_LAUNCH;
         if (st != COGDL_OK) {
             cogdl::plan_free(h);
             return st;
         }
-        if (tot[0] + 1 > P.cap_units) P.cap_units = tot[0] + 1;
-        if (tot[1] + 2 > P.cap_partials) P.cap_partials = tot[1] + 2;
-        if (tot[2] + 1 > P.cap_split) P.cap_split = tot[2] + 1;
+        if ((int64_t)tot[0] + 1 > P.cap_units) P.cap_units = (int64_t)tot[0] + 1;
+        if ((int64_t)tot[1] + 2 > P.cap_partials) P.cap_partials = (int64_t)tot[1] + 2;
+        if ((int64_t)tot[2] + 1 > P.cap_split) P.cap_split = (int64_t)tot[2] + 1;
     }
     if (cogdl::plan_alloc(P) != COGDL_OK) {
         cogdl::plan_free(h);
