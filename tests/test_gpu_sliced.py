@@ -16,7 +16,7 @@ from test_gpu_random import KINDS, _case, _close
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 60
+N_CASES = 100
 SLICES = 8
 
 
