@@ -200,3 +200,53 @@ def test_sliced_gat_forward_backward(cg, seed):
         assert scaled_error(out["dX"].reshape(ref["dX"].shape), ref["dX"], ref["dX_abs"]) <= TOL_F32, "dX"
     finally:
         _close(plan, plan_t)
+
+
+def _degree_graph(deg, n_cols, seed):
+    rng = np.random.default_rng(seed)
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+    col = np.concatenate([np.sort(rng.choice(n_cols, d, replace=False)) for d in deg]).astype(np.int32)
+    from paper_2103_00959_amd import synth
+    return synth.Graph(rowptr, col, rng.standard_normal(col.size).astype(np.float32), len(deg), n_cols)
+
+
+def test_sliced_rebuild_beyond_capacity_falls_back(cg):
+    """A sliced plan sized on one graph, rebuilt on a graph with the same n_rows and nnz but
+    far more sliced units than it has room for: that build slices no row (the plain
+    neighbour groups, unit for unit) and every result stays right; rebuilt on the first graph
+    again, it slices as before."""
+    import torch
+    n, n_cols, smin = 1000, 1000, 32
+    deg_a = np.full(n, 6, np.int64)
+    deg_a[7] = 206                                  # one row over the slice threshold
+    deg_b = np.full(n, 1, np.int64)
+    deg_b[:20] = 250                                # twenty long rows, 8 pieces each
+    deg_b[20:] = (deg_a.sum() - 20 * 250) // (n - 20)
+    deg_b[-1] += deg_a.sum() - deg_b.sum()
+    assert deg_a.sum() == deg_b.sum()
+    ga, gb = _degree_graph(deg_a, n_cols, 1), _degree_graph(deg_b, n_cols, 2)
+    E = int(deg_a.sum())
+    rpa, cla, vla = graph_to_dev(ga)
+    rpb, clb, vlb = graph_to_dev(gb)
+    plan = cg.Plan(rpa, E, max_feat=64, mode="neighbor_group", col=cla, n_cols=n_cols, slice_min=smin)
+    try:
+        info = plan.info()
+        G = info["group_size"]
+        units_a = sorted(map(tuple, plan.units().cpu().numpy()[:, :3].tolist()))
+        assert units_a == expected_pieces(ga.rowptr, ga.col, n_cols, G, smin, True)
+        for g, rp, cl, vl, sliced in ((gb, rpb, clb, vlb, False), (ga, rpa, cla, vla, True)):
+            plan.rebuild(rp, cl)
+            units = sorted(map(tuple, plan.units().cpu().numpy()[:, :3].tolist()))
+            if sliced:
+                assert units == units_a
+            else:
+                plain = sorted(map(tuple, oracle.neighbor_groups(g.rowptr, G, 2).tolist()))
+                assert units == plain
+                assert len(expected_pieces(g.rowptr, g.col, n_cols, G, smin, True)) > plan.info()["n_units"]
+            xh, xc, xd = features((n_cols, 64), 5, "f32")
+            Y = cg.spmm(rp, cl, vl, xd, plan=plan)
+            Yr, Ar = oracle.spmm(g.rowptr, g.col, g.val, xh, x_dtype=xc)
+            assert scaled_error(Y, Yr, Ar) <= TOL_F32
+            torch.cuda.synchronize()
+    finally:
+        plan.close()
