@@ -187,7 +187,7 @@ def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
 
 # ----------------------------------------------------------- main
 
-def run_inference(cg, synth, dev, time_op_kernels):
+def run_inference(cg, synth, dev, time_op_kernels, sliced=True):
     """End-to-end 2-layer GCN and GAT inference (hidden 128, GAT with 4 heads) on the
     Reddit-shaped graph: every step a library kernel, activations bf16."""
     import torch
@@ -208,7 +208,7 @@ def run_inference(cg, synth, dev, time_op_kernels):
         p = synth.model_params(kind, k, hid, C, Hh, seed=7100 if kind == "gcn" else 7200)
         params[kind] = {n: (bf16(v) if n.startswith("W") else torch.from_numpy(v).to(dev))
                         for n, v in p.items()}
-    plan = cg.Plan(rowptr, E, max_feat=hid, max_heads=Hh, col=col, n_cols=N)
+    plan = cg.Plan(rowptr, E, max_feat=hid, max_heads=Hh, **(dict(col=col, n_cols=N) if sliced else {}))
     torch.cuda.synchronize()
     ms_gcn, k_gcn = time_op_kernels(lambda: cg.gcn_forward(rowptr, col, val, X, params["gcn"], plan=plan))
     ms_gat, k_gat = time_op_kernels(lambda: cg.gat_forward(rowptr, col, X, params["gat"], spec["slope"],
@@ -862,7 +862,8 @@ def main():
         f"gat backward {ms_bwd:.3f} ms "
         f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd.items())})")
 
-    inference = None if args.no_inference else run_inference(cg, synth, dev, time_op_kernels)
+    inference = None if args.no_inference else run_inference(cg, synth, dev, time_op_kernels,
+                                                             sliced=not args.plain_plans)
 
     out = {
         "metric": METRIC, "value": value, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
