@@ -725,6 +725,7 @@ cogdl_status cogdl_plan_create_sliced(int32_t n_rows, int64_t nnz, const int32_t
         cogdl::plan_free(h);
         return COGDL_ERR_NOMEM;
     }
+    P.bytes += rows_bytes;                 // both allocations, as cogdl_plan_query reports them
     cogdl_status st = cogdl::plan_build(P, rowptr, col, stream);
     if (st != COGDL_OK) {
         cogdl::plan_free(h);
