@@ -149,7 +149,11 @@ cogdl_status cogdl_plan_create(int32_t n_rows, int64_t nnz, const int32_t *rowpt
                                int32_t group_size, hipStream_t stream, cogdl_plan **out);
 
 /* Re-run the balancer of an existing plan on a rowptr with the plan's n_rows
- * and nnz (same mode request and group size).  Allocates nothing. */
+ * and nnz (same mode request and group size).  Allocates nothing.  The build
+ * never writes past the plan: if the device rowptr holds more edges than the
+ * plan was created for (rowptr[n_rows] > nnz, a broken contract the host
+ * cannot see), the plan is left empty (no work unit runs) and the next
+ * cogdl_plan_query returns COGDL_ERR_PLAN. */
 cogdl_status cogdl_plan_rebuild(cogdl_plan *plan, const int32_t *rowptr, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -191,7 +195,11 @@ cogdl_status cogdl_plan_rebuild_sliced(cogdl_plan *plan, const int32_t *rowptr, 
 /* Free the plan (synchronizes the device first).  NULL is accepted. */
 cogdl_status cogdl_plan_destroy(cogdl_plan *plan);
 
-/* Read the plan's counters back to the host (synchronizes `stream`). */
+/* Read the plan's counters back to the host (synchronizes `stream`).
+ * Returns COGDL_ERR_PLAN (with *info filled) when the last build found more
+ * work units, partial slots or split rows than the plan's capacities, i.e. a
+ * rowptr with more than nnz edges; the plan is then empty until a build on a
+ * conforming rowptr. */
 cogdl_status cogdl_plan_query(const cogdl_plan *plan, hipStream_t stream, cogdl_plan_info *info);
 
 /* Copy the work units, in execution order, to `units` (device, 4 int32 per

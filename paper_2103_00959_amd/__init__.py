@@ -138,6 +138,70 @@ def _dev(t, name, dtype=None):
     return t
 
 
+# Size checks.  The C ABI receives bare pointers and cannot see how large a
+# tensor is, so every size the library will read or write through is checked
+# here, before any device check and before anything is launched: a tensor of
+# the wrong size would otherwise be read or written out of bounds on the GPU.
+def _tensor(t, name):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise CogdlError(f"{name} must be a torch tensor, got {type(t).__name__}")
+    return t
+
+
+def _dims(t, name, ndim):
+    _tensor(t, name)
+    if t.dim() != ndim:
+        raise CogdlError(f"{name} must have {ndim} dimensions, got shape {tuple(t.shape)}")
+    return tuple(t.shape)
+
+
+def _numel(t, name, n):
+    """t is None, or a tensor of exactly n elements."""
+    if t is None:
+        return
+    _tensor(t, name)
+    if t.numel() != n:
+        raise CogdlError(f"{name} has {t.numel()} elements, expected {n}")
+
+
+def _at_least(t, name, n):
+    if t is None:
+        return
+    _tensor(t, name)
+    if t.numel() < n:
+        raise CogdlError(f"{name} has {t.numel()} elements, needs at least {n}")
+
+
+def _index_array(t, name):
+    """A 1-D int32 index array (rowptr, col, ...): its element count."""
+    _dims(t, name, 1)
+    return t.numel()
+
+
+def _rowptr_rows(rowptr, name="rowptr"):
+    n = _index_array(rowptr, name)
+    if n < 1:
+        raise CogdlError(f"{name} needs at least one entry (n_rows + 1)")
+    return n - 1
+
+
+def _feat2(X, name):
+    """(rows, width) of a feature matrix given as [rows, F] or [rows]."""
+    _tensor(X, name)
+    if X.dim() == 2:
+        return X.shape[0], X.shape[1]
+    if X.dim() == 1:
+        return X.shape[0], 1
+    raise CogdlError(f"{name} must be [rows, F] or [rows], got shape {tuple(X.shape)}")
+
+
+def _plan_matches(plan, n_rows, nnz, name="plan"):
+    if plan is not None and (plan.n_rows != n_rows or plan.nnz != nnz):
+        raise CogdlError(f"{name} was built for {plan.n_rows} rows and {plan.nnz} nonzeros, "
+                         f"the call has {n_rows} rows and {nnz} nonzeros")
+
+
 class Plan:
     """The data-aware workload balancer (section 2.2): run once per graph."""
 
@@ -146,16 +210,23 @@ class Plan:
         """With `col` (and `n_cols`), a column-sliced plan (cogdl_plan_create_sliced): long rows
         are also cut at 8 column-range boundaries and each range's units run on one XCD."""
         import torch
+        self._h = None
+        n_rows = _rowptr_rows(rowptr)
+        if mode not in BALANCE:
+            raise CogdlError(f"mode must be one of {sorted(BALANCE)}")
+        self.sliced = col is not None
+        if self.sliced:
+            _index_array(col, "col")
+            _numel(col, "col", int(nnz))
+            if n_cols is None:
+                raise CogdlError("a sliced plan needs n_cols")
         _dev(rowptr, "rowptr", torch.int32)
         self.rowptr = rowptr
-        self.n_rows = rowptr.numel() - 1
+        self.n_rows = n_rows
         self.nnz = int(nnz)
-        self.sliced = col is not None
         h = ctypes.c_void_p()
         if self.sliced:
             _dev(col, "col", torch.int32)
-            if n_cols is None:
-                raise CogdlError("a sliced plan needs n_cols")
             self.col = col
             _check(lib().cogdl_plan_create_sliced(self.n_rows, self.nnz, _ptr(rowptr), _ptr(col), int(n_cols),
                                                   int(max_feat), int(max_heads), BALANCE[mode], int(group_size),
@@ -175,6 +246,14 @@ class Plan:
 
     def rebuild(self, rowptr=None, col=None):
         import torch
+        if rowptr is not None:
+            _numel(rowptr, "rowptr", self.n_rows + 1)
+            _index_array(rowptr, "rowptr")
+        if col is not None:
+            if not self.sliced:
+                raise CogdlError("only a sliced plan is rebuilt with col")
+            _numel(col, "col", self.nnz)
+            _index_array(col, "col")
         if rowptr is not None:
             _dev(rowptr, "rowptr", torch.int32)
             self.rowptr = rowptr
@@ -243,17 +322,27 @@ def _plan_handle(plan):
     return None if plan is None else plan.handle
 
 
+def _graph(rowptr, col, val=None, val_name="val"):
+    """(n_rows, nnz) of a CSR (or CSC) graph, with the sizes of its arrays checked."""
+    n_rows = _rowptr_rows(rowptr)
+    nnz = _index_array(col, "col")
+    _numel(val, val_name, nnz)
+    return n_rows, nnz
+
+
 def spmm(rowptr, col, val, X, plan: Plan | None = None, out_dtype=None, out=None):
     """Y[i] = sum_k val[k] * X[col[k]] over row i (Eq. 1, sum of products)."""
     import torch
+    n_rows, nnz = _graph(rowptr, col, val)
+    n_cols, F = _feat2(X, "X")
+    _numel(out, "out", n_rows * F)
+    _plan_matches(plan, n_rows, nnz)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
     _dev(val, "val", torch.float32), _dev(X, "X")
-    n_rows = rowptr.numel() - 1
-    F = X.shape[1] if X.dim() > 1 else 1
     if out is None:
         out = torch.empty((n_rows, F), dtype=out_dtype or X.dtype, device=X.device)
     _dev(out, "out")
-    _check(lib().cogdl_spmm(n_rows, X.shape[0], col.numel(), _ptr(rowptr), _ptr(col), _ptr(val), F,
+    _check(lib().cogdl_spmm(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(val), F,
                             _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), _plan_handle(plan),
                             _stream()), "cogdl_spmm")
     return out
@@ -280,20 +369,24 @@ def gspmm(rowptr, col, val, X, reduce: str = "sum", plan: Plan | None = None, ou
         raise ValueError(f"compute must be one of {sorted(COMPUTE)}")
     if act not in ACT:
         raise ValueError(f"act must be one of {sorted(ACT)}")
+    if (return_arg or arg is not None) and reduce != "max":
+        raise ValueError("return_arg / arg need reduce='max'")
+    n_rows, nnz = _graph(rowptr, col, val)
+    n_cols, F = _feat2(X, "X")
+    _numel(out, "out", n_rows * F)
+    _numel(arg, "arg", n_rows * F)
+    _numel(bias, "bias", F)
+    _plan_matches(plan, n_rows, nnz)
     _dev(bias, "bias", torch.float32)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
     _dev(val, "val", torch.float32), _dev(X, "X")
-    n_rows = rowptr.numel() - 1
-    F = X.shape[1] if X.dim() > 1 else 1
     if out is None:
         out = torch.empty((n_rows, F), dtype=out_dtype or X.dtype, device=X.device)
     _dev(out, "out")
-    if return_arg and reduce != "max":
-        raise ValueError("return_arg needs reduce='max'")
     if return_arg and arg is None:
         arg = torch.empty((n_rows, F), dtype=torch.int32, device=X.device)
     _dev(arg, "arg", torch.int32)
-    _check(lib().cogdl_gspmm(n_rows, X.shape[0], col.numel(), _ptr(rowptr), _ptr(col), _ptr(val), F,
+    _check(lib().cogdl_gspmm(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(val), F,
                              _ptr(X), _dtype_code(X), _ptr(out), _dtype_code(out), REDUCE[reduce],
                              COMPUTE[compute], _ptr(bias), ACT[act], _ptr(arg), _plan_handle(plan),
                              _stream()), "cogdl_gspmm")
@@ -310,9 +403,13 @@ def csr_to_csc_workspace(n_rows: int, n_cols: int, nnz: int) -> int:
 def csr_to_csc(rowptr, col, val, n_cols: int, workspace=None, with_perm: bool = True):
     """Stable transpose: (colptr, row_t, val_t, perm); inside a column edges keep CSR order."""
     import torch
+    n_rows, nnz = _graph(rowptr, col, val)
+    n_cols = int(n_cols)
+    if n_cols < 0:
+        raise CogdlError("n_cols must be >= 0")
+    if workspace is not None:
+        _dims(workspace, "workspace", 1)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(val, "val", torch.float32)
-    n_rows = rowptr.numel() - 1
-    nnz = col.numel()
     dev = rowptr.device
     colptr = torch.empty(n_cols + 1, dtype=torch.int32, device=dev)
     row_t = torch.empty(nnz, dtype=torch.int32, device=dev)
@@ -321,40 +418,57 @@ def csr_to_csc(rowptr, col, val, n_cols: int, workspace=None, with_perm: bool = 
     need = csr_to_csc_workspace(n_rows, n_cols, nnz)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    _dev(workspace, "workspace")
     _check(lib().cogdl_csr_to_csc(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(val),
                                   _ptr(colptr), _ptr(row_t), _ptr(val_t), _ptr(perm), _ptr(workspace),
-                                  workspace.numel(), _stream()), "cogdl_csr_to_csc")
+                                  workspace.numel() * workspace.element_size(), _stream()),
+           "cogdl_csr_to_csc")
     return colptr, row_t, val_t, perm
 
 
 def spmm_t(colptr, row_t, val_t, G, plan_t: Plan | None = None, out_dtype=None, out=None):
     """dX = A^T G from the CSC arrays of A; G is n_rows x F."""
     import torch
+    n_cols = _rowptr_rows(colptr, "colptr")
+    nnz = _index_array(row_t, "row_t")
+    _numel(val_t, "val_t", nnz)
+    n_rows, F = _feat2(G, "G")
+    _numel(out, "out", n_cols * F)
+    _plan_matches(plan_t, n_cols, nnz, "plan_t")
     _dev(colptr, "colptr", torch.int32), _dev(row_t, "row_t", torch.int32)
     _dev(val_t, "val_t", torch.float32), _dev(G, "G")
-    n_cols = colptr.numel() - 1
-    F = G.shape[1] if G.dim() > 1 else 1
     if out is None:
         out = torch.empty((n_cols, F), dtype=out_dtype or G.dtype, device=G.device)
     _dev(out, "out")
-    _check(lib().cogdl_spmm_t(G.shape[0], n_cols, row_t.numel(), _ptr(colptr), _ptr(row_t),
+    _check(lib().cogdl_spmm_t(n_rows, n_cols, nnz, _ptr(colptr), _ptr(row_t),
                               _ptr(val_t), F, _ptr(G), _dtype_code(G), _ptr(out), _dtype_code(out),
                               _plan_handle(plan_t), _stream()), "cogdl_spmm_t")
     return out
+
+
+def _scores(t, name, rows, H):
+    """A per-node score array [rows, H] (fp32)."""
+    shape = _dims(t, name, 2)
+    if shape != (rows, H):
+        raise CogdlError(f"{name} must be [{rows}, {H}], got {shape}")
 
 
 def sddmm_edge_softmax(rowptr, col, s_dst, s_src, negative_slope: float = 0.2,
                        plan: Plan | None = None, out=None):
     """alpha[k, h] = softmax over row i of LeakyReLU(s_dst[i, h] + s_src[col[k], h])."""
     import torch
+    n_rows, nnz = _graph(rowptr, col)
+    _dims(s_src, "s_src", 2)
+    n_cols, H = s_src.shape
+    _scores(s_dst, "s_dst", n_rows, H)
+    _numel(out, "alpha", nnz * H)
+    _plan_matches(plan, n_rows, nnz)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32)
     _dev(s_dst, "s_dst", torch.float32), _dev(s_src, "s_src", torch.float32)
-    H = s_dst.shape[1]
-    nnz = col.numel()
     if out is None:
         out = torch.empty((nnz, H), dtype=torch.float32, device=col.device)
     _dev(out, "alpha", torch.float32)
-    _check(lib().cogdl_sddmm_edge_softmax(rowptr.numel() - 1, s_src.shape[0], nnz, _ptr(rowptr),
+    _check(lib().cogdl_sddmm_edge_softmax(n_rows, n_cols, nnz, _ptr(rowptr),
                                           _ptr(col), H, _ptr(s_dst), _ptr(s_src),
                                           float(negative_slope), _ptr(out), _plan_handle(plan),
                                           _stream()), "cogdl_sddmm_edge_softmax")
@@ -369,15 +483,25 @@ def gat_aggregate(rowptr, col, s_dst, s_src, X, negative_slope: float = 0.2, alp
     import torch
     if act not in ACT:
         raise ValueError(f"act must be one of {sorted(ACT)}")
+    n_rows, nnz = _graph(rowptr, col)
+    n_cols, H, D = _dims(X, "X", 3)
+    if alpha_in is None:
+        _scores(s_dst, "s_dst", n_rows, H)
+        _scores(s_src, "s_src", n_cols, H)
+    else:
+        if s_dst is not None:
+            _scores(s_dst, "s_dst", n_rows, H)
+        if s_src is not None:
+            _scores(s_src, "s_src", n_cols, H)
+        _numel(alpha_in, "alpha_in", nnz * H)
+    _numel(out, "out", n_rows * H * D)
+    _numel(alpha_out, "alpha_out", nnz * H)
+    _numel(bias, "bias", H * D)
+    _plan_matches(plan, n_rows, nnz)
     _dev(bias, "bias", torch.float32)
     _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(X, "X")
     _dev(s_dst, "s_dst", torch.float32), _dev(s_src, "s_src", torch.float32)
     _dev(alpha_in, "alpha_in", torch.float32)
-    if X.dim() != 3:
-        raise CogdlError("X must be [n_cols, H, D]")
-    n_cols, H, D = X.shape
-    n_rows = rowptr.numel() - 1
-    nnz = col.numel()
     if out is None:
         out = torch.empty((n_rows, H, D), dtype=out_dtype or X.dtype, device=X.device)
     _dev(out, "out")
@@ -403,16 +527,20 @@ def sddmm_dot(rowptr, col, P, Q, plan: Plan | None = None, out=None):
     """out[k, h] = <P[i, h, :], Q[col[k], h, :]> for every edge k = (i, col[k]):
     the SDDMM of section 2.2 per head.  P is [n_rows, H, D], Q [n_cols, H, D]."""
     import torch
-    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(P, "P"), _dev(Q, "Q")
-    if P.dim() != 3 or Q.dim() != 3 or P.shape[1:] != Q.shape[1:]:
+    n_rows, nnz = _graph(rowptr, col)
+    pr, H, D = _dims(P, "P", 3)
+    n_cols, qh, qd = _dims(Q, "Q", 3)
+    if (qh, qd) != (H, D):
         raise CogdlError("P and Q must be [n, H, D] with the same H and D")
-    _, H, D = P.shape
-    n_rows = rowptr.numel() - 1
-    nnz = col.numel()
+    if pr != n_rows:
+        raise CogdlError(f"P has {pr} rows, the graph {n_rows}")
+    _numel(out, "out", nnz * H)
+    _plan_matches(plan, n_rows, nnz)
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(P, "P"), _dev(Q, "Q")
     if out is None:
         out = torch.empty((nnz, H), dtype=torch.float32, device=P.device)
     _dev(out, "out", torch.float32)
-    _check(lib().cogdl_sddmm_dot(n_rows, Q.shape[0], nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(P),
+    _check(lib().cogdl_sddmm_dot(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(P),
                                  _dtype_code(P), _ptr(Q), _dtype_code(Q), _ptr(out), _plan_handle(plan),
                                  _stream()), "cogdl_sddmm_dot")
     return out
@@ -425,19 +553,34 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     alpha [nnz, H] the forward weights; (colptr, row_t, perm) the CSC from csr_to_csc.
     Returns dict(dX, dalpha, dscore, ds_dst, ds_src); ``out`` may supply these tensors."""
     import torch
+    n_rows, nnz = _graph(rowptr, col)
+    n_cols, H, D = _dims(X, "X", 3)
+    if _dims(dY, "dY", 3) != (n_rows, H, D):
+        raise CogdlError(f"dY must be [{n_rows}, {H}, {D}], got {tuple(dY.shape)}")
+    _numel(colptr, "colptr", n_cols + 1)
+    _index_array(colptr, "colptr")
+    for t, name in ((row_t, "row_t"), (perm, "perm")):
+        _numel(t, name, nnz)
+        _index_array(t, name)
+    _scores(s_dst, "s_dst", n_rows, H)
+    _scores(s_src, "s_src", n_cols, H)
+    _numel(alpha, "alpha", nnz * H)
+    o = dict(out or {})
+    sizes = {"dX": n_cols * H * D, "dalpha": nnz * H, "dscore": nnz * H, "ds_dst": n_rows * H,
+             "ds_src": n_cols * H}
+    for k in o:
+        if k not in sizes:
+            raise CogdlError(f"unknown output {k!r}")
+        _numel(o[k], k, sizes[k])
+    _plan_matches(plan, n_rows, nnz)
+    _plan_matches(plan_t, n_cols, nnz, "plan_t")
     for t, name, dt in ((rowptr, "rowptr", torch.int32), (col, "col", torch.int32),
                         (colptr, "colptr", torch.int32), (row_t, "row_t", torch.int32),
                         (perm, "perm", torch.int32), (s_dst, "s_dst", torch.float32),
                         (s_src, "s_src", torch.float32), (alpha, "alpha", torch.float32)):
         _dev(t, name, dt)
     _dev(X, "X"), _dev(dY, "dY")
-    if X.dim() != 3 or dY.dim() != 3 or X.shape[1:] != dY.shape[1:]:
-        raise CogdlError("X and dY must be [n, H, D] with the same H and D")
-    n_cols, H, D = X.shape
-    n_rows = rowptr.numel() - 1
-    nnz = col.numel()
     dev = X.device
-    o = dict(out or {})
     o.setdefault("dX", torch.empty((n_cols, H, D), dtype=dx_dtype or X.dtype, device=dev))
     o.setdefault("dalpha", torch.empty((nnz, H), dtype=torch.float32, device=dev))
     o.setdefault("dscore", torch.empty((nnz, H), dtype=torch.float32, device=dev))
@@ -459,13 +602,15 @@ def linear(X, W, bias=None, act: str = "none", out_dtype=None, out=None):
     """Y = act(X W^T + bias) on the matrix cores.  X [n, k] and W [m, k] (a layer's out x in
     weights) both bf16 or both fp16; bias fp32 [m] or None."""
     import torch
-    _dev(X, "X"), _dev(W, "W"), _dev(bias, "bias", torch.float32)
     if act not in ACT:
         raise ValueError(f"act must be one of {sorted(ACT)}")
-    if X.dim() != 2 or W.dim() != 2 or X.shape[1] != W.shape[1] or X.dtype != W.dtype:
+    n, k = _dims(X, "X", 2)
+    m, kw = _dims(W, "W", 2)
+    if kw != k or X.dtype != W.dtype:
         raise CogdlError("X must be [n, k] and W [m, k] of the same dtype")
-    n, k = X.shape
-    m = W.shape[0]
+    _numel(bias, "bias", m)
+    _numel(out, "out", n * m)
+    _dev(X, "X"), _dev(W, "W"), _dev(bias, "bias", torch.float32)
     if out is None:
         out = torch.empty((n, m), dtype=out_dtype or X.dtype, device=X.device)
     _dev(out, "out")
@@ -477,8 +622,10 @@ def linear(X, W, bias=None, act: str = "none", out_dtype=None, out=None):
 def head_scores(Z, a_src, a_dst):
     """s_src[i, h] = <Z[i, h, :], a_src[h]>, s_dst likewise; Z [n, H, D], a_* fp32 [H, D]."""
     import torch
+    n, H, D = _dims(Z, "Z", 3)
+    _numel(a_src, "a_src", H * D)
+    _numel(a_dst, "a_dst", H * D)
     _dev(Z, "Z"), _dev(a_src, "a_src", torch.float32), _dev(a_dst, "a_dst", torch.float32)
-    n, H, D = Z.shape
     s_src = torch.empty((n, H), dtype=torch.float32, device=Z.device)
     s_dst = torch.empty((n, H), dtype=torch.float32, device=Z.device)
     _check(lib().cogdl_head_scores(n, H, D, _ptr(Z), _dtype_code(Z), _ptr(a_src), _ptr(a_dst),
@@ -556,9 +703,11 @@ def act_compress(A, bits: int, group: int, seed: int, codes=None, stats=None):
     """Per-group `bits`-bit stochastic quantization of A [n, F]: returns (codes int64 view of
     the uint64 bit planes, stats fp32 [groups, 2] = (min, step))."""
     import torch
-    _dev(A, "A")
-    n, F = A.shape
+    n, F = _dims(A, "A", 2)
     words, nst = act_codec_size(n, F, bits, group)
+    _at_least(codes, "codes", words)
+    _at_least(stats, "stats", nst)
+    _dev(A, "A")
     if codes is None:
         codes = torch.empty(max(words, 1), dtype=torch.int64, device=A.device)
     if stats is None:
@@ -572,6 +721,10 @@ def act_compress(A, bits: int, group: int, seed: int, codes=None, stats=None):
 
 def act_decompress(codes, stats, n: int, F: int, bits: int, group: int, out_dtype=None, out=None):
     import torch
+    words, nst = act_codec_size(n, F, bits, group)
+    _at_least(codes, "codes", words)
+    _at_least(stats, "stats", nst)
+    _numel(out, "out", n * F)
     _dev(codes, "codes", torch.int64), _dev(stats, "stats", torch.float32)
     if out is None:
         out = torch.empty((n, F), dtype=out_dtype or torch.float32, device=codes.device)

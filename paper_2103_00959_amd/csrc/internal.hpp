@@ -43,7 +43,9 @@ struct Plan {
     int32_t *row_split = nullptr; // [n_rows + 1]; [n_rows] = #split rows
     int32_t *counters = nullptr;  // [8]: 0 close-degree rows, 1 chosen mode,
                                   //      2 units longer than kTinyUnit, 3 zero,
-                                  //      4 sliced plan: 1 when its rows were sliced
+                                  //      4 sliced plan: 1 when its rows were sliced,
+                                  //      5 1 when the last build's totals exceeded the
+                                  //        capacities (the plan was left empty)
     uint32_t *sort_keys = nullptr;   // [4 * cap_units]: keys, 2 ping buffers, sorted keys
     uint32_t *sort_vals = nullptr;   // [3 * cap_units]: order, then 2 ping buffers
     void *sort_ws = nullptr;

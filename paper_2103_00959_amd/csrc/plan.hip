@@ -74,6 +74,27 @@ __global__ void k_plan_counts(const int32_t *__restrict__ rowptr, int32_t n_rows
     row_split[i] = u > 1 ? 1 : 0;
 }
 
+// After the count scan: the totals (units, partial slots, split rows) of this
+// rowptr must fit the capacities the plan was allocated with.  They do
+// whenever rowptr[n_rows] is the nnz given at creation; a rowptr with more
+// edges would make the emit pass write past the plan's arrays, so instead the
+// totals are set to zero (an empty plan, no unit runs) and counters[5] = 1,
+// which cogdl_plan_query reports as COGDL_ERR_PLAN.
+__global__ void k_plan_check(int32_t *__restrict__ n_units, int32_t *__restrict__ n_parts,
+                             int32_t *__restrict__ n_split, int64_t cap_units, int64_t cap_partials,
+                             int64_t cap_split, int32_t *__restrict__ counters)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    const bool fits = *n_units <= cap_units && *n_parts <= cap_partials && *n_split <= cap_split &&
+                      *n_units >= 0 && *n_parts >= 0 && *n_split >= 0;
+    if (!fits) {
+        *n_units = 0;
+        *n_parts = 0;
+        *n_split = 0;
+    }
+    counters[5] = fits ? 0 : 1;
+}
+
 // Emit the units of each row in row order, with their sort keys.
 __global__ void k_plan_emit(const int32_t *__restrict__ rowptr, int32_t n_rows, int32_t G,
                             const int32_t *__restrict__ counters,
@@ -84,7 +105,7 @@ __global__ void k_plan_emit(const int32_t *__restrict__ rowptr, int32_t n_rows, 
                             int4 *__restrict__ part_units)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n_rows) return;
+    if (i >= n_rows || counters[5] != 0) return;
     const bool ng = counters[1] == COGDL_BALANCE_NEIGHBOR_GROUP;
     const int beg = rowptr[i], end = rowptr[i + 1];
     const int u0 = row_units[i];
@@ -297,7 +318,7 @@ __global__ void k_plan_emit_sliced(const int32_t *__restrict__ rowptr, int32_t n
                                    int4 *__restrict__ part_units)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n_rows) return;
+    if (i >= n_rows || counters[5] != 0) return;
     const bool ng = counters[1] == COGDL_BALANCE_NEIGHBOR_GROUP;
     const bool slice = ng && counters[4] != 0;
     const int beg = rowptr[i], end = rowptr[i + 1];
@@ -451,6 +472,8 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, const int32_t *col, hipS
                      P.counters, P.row_units, P.row_parts, P.row_split, P.alt_units, P.alt_parts,
                      P.alt_split);
         COGDL_HIP_TRY(exclusive_scan3(P.row_units, P.row_parts, P.row_split, n, P.scan_ws, s));
+        COGDL_LAUNCH("plan_check", k_plan_check, 1, 64, s, P.row_units + n, P.row_parts + n,
+                     P.row_split + n, P.cap_units, P.cap_partials, P.cap_split, P.counters);
         COGDL_LAUNCH("plan_emit", k_plan_emit_sliced, blocks, 256, s, rowptr, n, G, kb, P.slice_min,
                      P.row_cuts, P.counters, P.row_units, P.row_parts, P.row_split, P.units_tmp,
                      P.sort_keys, P.split_rows, P.part_units);
@@ -458,6 +481,8 @@ cogdl_status plan_build(Plan &P, const int32_t *rowptr, const int32_t *col, hipS
         COGDL_LAUNCH("plan_counts", k_plan_counts, blocks, 256, s, rowptr, n, G, (int)P.mode_req,
                      P.counters, P.row_units, P.row_parts, P.row_split);
         COGDL_HIP_TRY(exclusive_scan3(P.row_units, P.row_parts, P.row_split, n, P.scan_ws, s));
+        COGDL_LAUNCH("plan_check", k_plan_check, 1, 64, s, P.row_units + n, P.row_parts + n,
+                     P.row_split + n, P.cap_units, P.cap_partials, P.cap_split, P.counters);
         COGDL_LAUNCH("plan_emit", k_plan_emit, blocks, 256, s, rowptr, n, G, P.counters,
                      P.row_units, P.row_parts, P.row_split, P.units_tmp, P.sort_keys, P.split_rows,
                      P.part_units);
@@ -764,12 +789,13 @@ cogdl_status cogdl_plan_query(const cogdl_plan *plan, hipStream_t stream, cogdl_
 {
     if (!plan || !info) return COGDL_ERR_INVALID;
     const Plan &P = plan->p;
-    int32_t v[5] = {0, 0, 0, 0, 0};
+    int32_t v[6] = {0, 0, 0, 0, 0, 0};
     COGDL_HIP_TRY(hipMemcpyAsync(&v[0], P.n_units_dev(), 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[1], P.n_split_dev(), 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[2], P.n_parts_dev(), 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[3], P.counters + 1, 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipMemcpyAsync(&v[4], P.counters + 2, 4, hipMemcpyDeviceToHost, stream));
+    COGDL_HIP_TRY(hipMemcpyAsync(&v[5], P.counters + 5, 4, hipMemcpyDeviceToHost, stream));
     COGDL_HIP_TRY(hipStreamSynchronize(stream));
     info->n_rows = P.n_rows;
     info->nnz = P.nnz;
@@ -784,7 +810,9 @@ cogdl_status cogdl_plan_query(const cogdl_plan *plan, hipStream_t stream, cogdl_
                                                                      : (int32_t)P.mode_req)
                                : v[3];
     info->device_bytes = (int64_t)P.bytes;
-    return COGDL_OK;
+    // the last build's rowptr held more edges than the plan was created for:
+    // the plan was left empty (see k_plan_check)
+    return (P.n_rows > 0 && v[5] != 0) ? COGDL_ERR_PLAN : COGDL_OK;
 }
 
 cogdl_status cogdl_plan_units(const cogdl_plan *plan, int32_t *units, int64_t capacity,

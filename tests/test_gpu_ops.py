@@ -632,3 +632,31 @@ def test_gat_backward_unnormalized_weights_and_repeat(cg):
     finally:
         plan.close()
         plan_t.close()
+
+
+def test_plan_rebuild_past_capacity_is_refused(cg):
+    """A rebuild on a rowptr holding more edges than the plan was created for must not write past
+    the plan: the build leaves the plan empty and cogdl_plan_query reports COGDL_ERR_PLAN; a
+    later build on a conforming rowptr restores it (checked against the oracle)."""
+    import torch
+    g = _graph("small", 3)
+    rp, col, val = graph_to_dev(g)
+    X_host, _, X = features((g.n_cols, 16), 77, "f32")
+    plan = cg.Plan(rp, g.nnz, max_feat=16, mode="neighbor_group", group_size=4)
+    try:
+        plan.info()
+        deg2 = 2 * np.diff(g.rowptr.astype(np.int64))           # every row twice as long
+        rp2 = dev(np.concatenate([[0], np.cumsum(deg2)]).astype(np.int32))
+        say(f"plan guard: nnz {g.nnz}, rebuilt on a rowptr of {int(deg2.sum())} edges")
+        plan.rebuild(rp2)
+        with pytest.raises(cg.CogdlError, match="plan does not match"):
+            plan.info()
+        plan.rebuild(rp)
+        info = plan.info()
+        assert info["n_units"] > 0
+        Y = cg.spmm(rp, col, val, X, plan=plan)
+        torch.cuda.synchronize()
+    finally:
+        plan.close()
+    Yr, Ar = oracle.spmm(g.rowptr, g.col, g.val, X_host)
+    assert scaled_error(Y, Yr, Ar) <= TOL_F32

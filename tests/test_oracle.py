@@ -3,6 +3,7 @@
 brute force on tiny graphs), chosen so that a dropped term, a wrong sign, a
 wrong index or a transposed operand fails at least one of them."""
 import json
+from fractions import Fraction
 import math
 import os
 
@@ -924,6 +925,69 @@ def test_codec_exact_grid_and_constant_groups():
     c = np.full((3, 128), 1.25, np.float32)
     codes, stats = oracle.act_compress(c, 3, 64, seed=1)
     assert not codes.any() and np.array_equal(oracle.act_decompress(codes, stats, 3, 128, 3, 64), c)
+
+
+def test_codec_decoder_rounds_once():
+    """The decoded value is fma(q, r, m): q * r + m rounded once to fp32 (the codec's definition).
+    Hand example where one rounding and two roundings differ: m = -3, r = 1 + 2^-23 (the fp32
+    just above 1), 2-bit codes 0, 1, 2, 3 on features 0..3 (bit planes 0b1010 and 0b1100).
+    Exactly: q r + m = -3, -2 + 2^-23, -1 + 2^-22 and 3 * 2^-23, each an fp32 value, so the
+    single rounding returns them unchanged.  Rounding q r first would give 3 r = 3 + 3 * 2^-23
+    -> 3 + 2^-21 (a tie between 3 + 2^-22 and 3 + 2^-21, broken to the even significand), and
+    then 2^-21 instead of 3 * 2^-23 for code 3.  Features 4..63 have code 0 and decode to m."""
+    r = np.frombuffer(np.uint32(0x3F800001).tobytes(), np.float32)[0]
+    stats = np.array([-3.0, r], np.float32)
+    codes = np.array([0b1010, 0b1100], np.uint64)        # plane 0, plane 1 of features 0..63
+    y = oracle.act_decompress(codes, stats, 1, 64, 2, 64)[0]
+    want = [-3.0, -2.0 + 2.0 ** -23, -1.0 + 2.0 ** -22, 3.0 * 2.0 ** -23]
+    assert [float(v) for v in y[:4]] == want
+    assert float(y[3]) != 2.0 ** -21
+    assert np.all(y[4:] == np.float32(-3.0))
+
+
+def _codec_uniform(seed, e):
+    """u of flat index e: word e mod 4 of Philox4x32-10 (pinned by its known answers) at counter
+    (e / 4 mod 2^32, e / 2^34, 0, 0), key (seed mod 2^32, seed / 2^32), top 24 bits times 2^-24."""
+    out = oracle.philox4x32_10([(e // 4) & 0xFFFFFFFF, e >> 34, 0, 0], [seed & 0xFFFFFFFF, seed >> 32])
+    return Fraction(int(out[e % 4]) >> 8, 1 << 24)
+
+
+def test_codec_quantizer_rounds_once():
+    """The code is floor(fma(x - m, s, u)): (x - m) s + u rounded once to fp32.  Constructed case
+    (1 bit, one group: x at feature 0, the maximum M at feature 1, zeros elsewhere, so m = 0 and
+    s = fl(1 / M)): with u > 1/2 and T = 1 - 2^-25 - u (an fp32 value on the 2^-25 grid of
+    [1/4, 1/2)), pick x so that the exact product P = x s lies strictly within 2^-26 below T.
+    Then P + u lies in (1 - 3 2^-26, 1 - 2 2^-26), whose nearest fp32 value is 1 - 2^-24, so the
+    single rounding gives code 0; rounding P first gives exactly T, then T + u = 1 - 2^-25, a tie
+    broken to 1.0, and code 1."""
+    import struct
+    f32 = lambda v: struct.unpack("<f", struct.pack("<f", float(v)))[0]   # noqa: E731
+
+    def neighbours(v, k):
+        b = struct.unpack("<I", struct.pack("<f", v))[0]
+        return [struct.unpack("<f", struct.pack("<I", b + d))[0] for d in range(-k, k + 1)]
+
+    for seed in range(1, 200):
+        u = _codec_uniform(seed, 0)
+        if not Fraction(1, 2) < u <= Fraction(3, 4):
+            continue
+        T = 1 - Fraction(1, 1 << 25) - u
+        for M in (3.0, 5.0, 7.0, 9.0, 11.0, 13.0):
+            s = f32(1.0 / M)
+            for x in neighbours(f32(float(T) / s), 64):
+                P = Fraction(x) * Fraction(s)
+                if 0 < x <= M and T - Fraction(1, 1 << 26) < P < T:
+                    row = np.zeros((1, 64), np.float32)
+                    row[0, 0], row[0, 1] = x, M
+                    codes, stats = oracle.act_compress(row, 1, 64, seed=seed)
+                    assert float(stats[0]) == 0.0 and float(stats[1]) == M
+                    # rounding the product first would give code 1 (the test is sensitive)
+                    two = np.float32(np.float32(x) * np.float32(s)) + np.float32(float(u))
+                    assert np.floor(two) == 1.0
+                    assert int(codes[0]) & 1 == 0, "code 0 expected from a single rounding"
+                    assert int(codes[0]) >> 1 & 1 == 1   # feature 1 (= M): s M rounds to 1
+                    return
+    raise AssertionError("no constructed case found")
 
 
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
