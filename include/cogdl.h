@@ -66,7 +66,7 @@ typedef enum {
     COGDL_ERR_PLAN = 3,      /* plan does not match the graph or the feature width */
     COGDL_ERR_NOMEM = 4,     /* device allocation failed (plan creation only) */
     COGDL_ERR_LAUNCH = 5,    /* a kernel launch or HIP runtime call failed */
-    COGDL_ERR_TOO_LARGE = 6  /* a size exceeds what the int32 index format can hold */
+    COGDL_ERR_TOO_LARGE = 6  /* a size exceeds what the int32 index format (or a static scratch) holds */
 } cogdl_status;
 
 #define COGDL_MAX_NNZ 2147479551LL   /* 2^31 - 4097 */
@@ -263,6 +263,28 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
                               const int32_t *col, const float *val, int32_t *colptr,
                               int32_t *row_t, float *val_t, int32_t *perm, void *workspace,
                               size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Allocation-free transpose, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): cogdl_csr_to_csc with the same arguments, outputs and errors,
+ * minus the workspace.  Its scratch is a static device array of
+ * COGDL_NOALLOC_SCRATCH_BYTES (64 MiB) on each GPU, placed when the library's
+ * code object is loaded there and held until the process ends; the call
+ * itself allocates nothing.  A graph whose workspace
+ * (cogdl_csr_to_csc_workspace) exceeds that size -- about 1.6M edges -- is
+ * refused with COGDL_ERR_TOO_LARGE before anything is launched.  All calls on
+ * one GPU share its array: calls that overlap in time on one GPU (several
+ * streams or threads) race and give undefined results; serialize them.
+ * Nothing in the scratch needs to be zero, so a call never depends on what the
+ * previous one left there.
+ * ---------------------------------------------------------------------- */
+#define COGDL_NOALLOC_SCRATCH_BYTES (64ull << 20)
+
+cogdl_status cogdl_csr_to_csc_noalloc(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col, const float *val,
+                                      int32_t *colptr, int32_t *row_t, float *val_t, int32_t *perm,
+                                      hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Transposed SpMM for the backward pass of Eq. 1:

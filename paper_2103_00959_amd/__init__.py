@@ -79,6 +79,7 @@ def lib():
     L.cogdl_spmm_t.argtypes = [i32, i32, i64, P, P, P, i32, P, ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_csr_to_csc_workspace.argtypes = [i32, i32, i64, ctypes.POINTER(sz)]
     L.cogdl_csr_to_csc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P, sz, P]
+    L.cogdl_csr_to_csc_noalloc.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, P]
     L.cogdl_sddmm_edge_softmax.argtypes = [i32, i32, i64, P, P, i32, P, P, f32, P, P, P]
     L.cogdl_gat_aggregate.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, P, ctypes.c_int,
                                       P, ctypes.c_int, P, P, P]
@@ -93,7 +94,8 @@ def lib():
     L.cogdl_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
     for name in ("cogdl_trace_enable", "cogdl_trace_filter", "cogdl_trace_reset", "cogdl_trace_get", "cogdl_plan_create", "cogdl_plan_rebuild", "cogdl_plan_create_sliced", "cogdl_plan_rebuild_sliced", "cogdl_plan_destroy", "cogdl_plan_query",
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
-                 "cogdl_csr_to_csc", "cogdl_sddmm_edge_softmax", "cogdl_gat_aggregate",
+                 "cogdl_csr_to_csc", "cogdl_csr_to_csc_noalloc", "cogdl_sddmm_edge_softmax",
+                 "cogdl_gat_aggregate",
                  "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act", "cogdl_linear",
                  "cogdl_head_scores", "cogdl_act_codec_size", "cogdl_act_compress",
                  "cogdl_act_decompress"):
@@ -423,6 +425,41 @@ def csr_to_csc(rowptr, col, val, n_cols: int, workspace=None, with_perm: bool = 
                                   _ptr(colptr), _ptr(row_t), _ptr(val_t), _ptr(perm), _ptr(workspace),
                                   workspace.numel() * workspace.element_size(), _stream()),
            "cogdl_csr_to_csc")
+    return colptr, row_t, val_t, perm
+
+
+def csr_to_csc_noalloc(rowptr, col, val, n_cols: int, out=None, with_perm: bool = True):
+    """The transpose of csr_to_csc through cogdl_csr_to_csc_noalloc, which allocates nothing
+    (its scratch is the library's static per-GPU array, so graphs up to about 1.6M edges).
+    ``out`` may supply (colptr, row_t, val_t, perm); calls on one GPU must not overlap."""
+    import torch
+    n_rows, nnz = _graph(rowptr, col, val)
+    n_cols = int(n_cols)
+    if n_cols < 0:
+        raise CogdlError("n_cols must be >= 0")
+    if out is not None:
+        colptr, row_t, val_t, perm = out
+        _numel(colptr, "colptr", n_cols + 1)
+        _numel(row_t, "row_t", nnz)
+        _numel(val_t, "val_t", nnz)
+        _numel(perm, "perm", nnz)
+    need, limit = csr_to_csc_workspace(n_rows, n_cols, nnz), 64 << 20   # COGDL_NOALLOC_SCRATCH_BYTES
+    if need > limit:
+        raise CogdlError(f"cogdl_csr_to_csc_noalloc: a graph of {nnz} edges needs {need} bytes of "
+                         f"scratch, the static scratch holds {limit}: use csr_to_csc with a workspace")
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(val, "val", torch.float32)
+    if out is None:
+        dev = rowptr.device
+        colptr = torch.empty(n_cols + 1, dtype=torch.int32, device=dev)
+        row_t = torch.empty(nnz, dtype=torch.int32, device=dev)
+        val_t = None if val is None else torch.empty(nnz, dtype=torch.float32, device=dev)
+        perm = torch.empty(nnz, dtype=torch.int32, device=dev) if with_perm else None
+    for t, name, dt in ((colptr, "colptr", torch.int32), (row_t, "row_t", torch.int32),
+                        (val_t, "val_t", torch.float32), (perm, "perm", torch.int32)):
+        _dev(t, name, dt)
+    _check(lib().cogdl_csr_to_csc_noalloc(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(val),
+                                          _ptr(colptr), _ptr(row_t), _ptr(val_t), _ptr(perm),
+                                          _stream()), "cogdl_csr_to_csc_noalloc")
     return colptr, row_t, val_t, perm
 
 

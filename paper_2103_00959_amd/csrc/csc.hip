@@ -7,6 +7,8 @@
 // gathered at random afterwards); colptr is read off the sorted keys.  Every step is
 // integer work in a fixed order, so the result is bit-for-bit unique: inside
 // a column the edges keep increasing CSR edge id.
+#include <mutex>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -74,7 +76,7 @@ __global__ __launch_bounds__(kBlock) void k_colptr(const uint32_t *__restrict__ 
 }
 
 struct CscLayout {
-    size_t row_of, ping_k, ping_v, ping_r, ping_w, skeys, vtmp, radix, total;
+    size_t row_of, ping_k, ping_v, ping_r, ping_w, skeys, radix, total;
 };
 
 size_t al(size_t b) { return (b + 255) & ~size_t(255); }
@@ -89,32 +91,43 @@ CscLayout csc_layout(int64_t nnz)
     L.ping_r = off; off += al(8 * (size_t)nnz);
     L.ping_w = off; off += al(8 * (size_t)nnz);
     L.skeys = off;  off += al(4 * (size_t)nnz);
-    L.vtmp = off;   off += al(4 * (size_t)nnz);
     L.radix = off;  off += al(radix_workspace_bytes(nnz));
     L.total = off;
     return L;
 }
 
 
-}  // namespace
-}  // namespace cogdl
+// Scratch of cogdl_csr_to_csc_noalloc: one copy per GPU, placed by the code
+// object loader and held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in symbol): it
+// uses the device address hipGetSymbolAddress returns, looked up once per
+// device on the first call with that device current.
+__device__ __align__(256) unsigned char scratch[COGDL_NOALLOC_SCRATCH_BYTES];
 
-using namespace cogdl;
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices] = {};
 
-extern "C" {
-
-cogdl_status cogdl_csr_to_csc_workspace(int32_t n_rows, int32_t n_cols, int64_t nnz, size_t *bytes)
+cogdl_status device_scratch(void **out)
 {
-    if (!bytes || n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
-    if (nnz > COGDL_MAX_NNZ) return COGDL_ERR_TOO_LARGE;
-    *bytes = csc_layout(nnz).total;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return COGDL_ERR_LAUNCH;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return COGDL_ERR_LAUNCH;
+        }
+        scratch_ptr[dev] = p;
+    }
+    *out = scratch_ptr[dev];
     return COGDL_OK;
 }
 
-cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
-                              const int32_t *col, const float *val, int32_t *colptr,
-                              int32_t *row_t, float *val_t, int32_t *perm, void *workspace,
-                              size_t workspace_bytes, hipStream_t stream)
+cogdl_status csc_check(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                       const int32_t *col, const float *val, const int32_t *colptr,
+                       const int32_t *row_t, const float *val_t)
 {
     if (n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
     if (nnz > COGDL_MAX_NNZ) return COGDL_ERR_TOO_LARGE;
@@ -122,14 +135,20 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
     if (n_rows > 0 && !rowptr) return COGDL_ERR_INVALID;
     if (nnz > 0 && (!col || !row_t || n_rows == 0 || n_cols == 0)) return COGDL_ERR_INVALID;
     if ((val == nullptr) != (val_t == nullptr)) return COGDL_ERR_INVALID;
+    return COGDL_OK;
+}
+
+// The transpose on a validated call, with `ws` holding at least
+// csc_layout(nnz).total bytes (256-byte aligned).
+cogdl_status csc_run(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                     const int32_t *col, const float *val, int32_t *colptr, int32_t *row_t,
+                     float *val_t, int32_t *perm, char *ws, hipStream_t stream)
+{
     const CscLayout L = csc_layout(nnz);
-    if (nnz > 0 && (!workspace || workspace_bytes < L.total || (uintptr_t)workspace % 256 != 0))
-        return COGDL_ERR_INVALID;
     if (nnz == 0) {
         COGDL_HIP_TRY(fill_i32(colptr, (int64_t)n_cols + 1, 0, stream));
         return COGDL_OK;
     }
-    char *ws = static_cast<char *>(workspace);
     uint32_t *row_of = reinterpret_cast<uint32_t *>(ws + L.row_of);
     uint32_t *ping_k = reinterpret_cast<uint32_t *>(ws + L.ping_k);
     uint32_t *ping_v = reinterpret_cast<uint32_t *>(ws + L.ping_v);
@@ -164,6 +183,52 @@ cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const
     COGDL_LAUNCH("csc_colptr", k_colptr, (unsigned)((nnz + 4 * kBlock - 1) / (4 * kBlock)), kBlock,
                  stream, skeys, nnz, n_cols, colptr);
     return COGDL_OK;
+}
+
+}  // namespace
+}  // namespace cogdl
+
+using namespace cogdl;
+
+extern "C" {
+
+cogdl_status cogdl_csr_to_csc_workspace(int32_t n_rows, int32_t n_cols, int64_t nnz, size_t *bytes)
+{
+    if (!bytes || n_rows < 0 || n_cols < 0 || nnz < 0) return COGDL_ERR_INVALID;
+    if (nnz > COGDL_MAX_NNZ) return COGDL_ERR_TOO_LARGE;
+    *bytes = csc_layout(nnz).total;
+    return COGDL_OK;
+}
+
+cogdl_status cogdl_csr_to_csc(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                              const int32_t *col, const float *val, int32_t *colptr,
+                              int32_t *row_t, float *val_t, int32_t *perm, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream)
+{
+    const cogdl_status st = csc_check(n_rows, n_cols, nnz, rowptr, col, val, colptr, row_t, val_t);
+    if (st != COGDL_OK) return st;
+    if (nnz > 0 && (!workspace || workspace_bytes < csc_layout(nnz).total ||
+                    (uintptr_t)workspace % 256 != 0))
+        return COGDL_ERR_INVALID;
+    return csc_run(n_rows, n_cols, nnz, rowptr, col, val, colptr, row_t, val_t, perm,
+                   static_cast<char *>(workspace), stream);
+}
+
+cogdl_status cogdl_csr_to_csc_noalloc(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col, const float *val,
+                                      int32_t *colptr, int32_t *row_t, float *val_t, int32_t *perm,
+                                      hipStream_t stream)
+{
+    const cogdl_status st = csc_check(n_rows, n_cols, nnz, rowptr, col, val, colptr, row_t, val_t);
+    if (st != COGDL_OK) return st;
+    if (csc_layout(nnz).total > (size_t)COGDL_NOALLOC_SCRATCH_BYTES) return COGDL_ERR_TOO_LARGE;
+    void *ws = nullptr;
+    if (nnz > 0) {
+        const cogdl_status sp = device_scratch(&ws);
+        if (sp != COGDL_OK) return sp;
+    }
+    return csc_run(n_rows, n_cols, nnz, rowptr, col, val, colptr, row_t, val_t, perm,
+                   static_cast<char *>(ws), stream);
 }
 
 }  // extern "C"

@@ -522,7 +522,7 @@ const char *cogdl_status_string(cogdl_status s)
     case COGDL_ERR_PLAN: return "plan does not match the call";
     case COGDL_ERR_NOMEM: return "device allocation failed";
     case COGDL_ERR_LAUNCH: return "kernel launch or HIP call failed";
-    case COGDL_ERR_TOO_LARGE: return "size exceeds the int32 index format";
+    case COGDL_ERR_TOO_LARGE: return "size exceeds a limit of the call (int32 indices, or the static scratch of the allocation-free transpose)";
     }
     return "unknown status";
 }

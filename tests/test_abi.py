@@ -158,6 +158,33 @@ def test_csc_validation(L):
                               None) == INVALID
 
 
+def _noalloc_limit():
+    m = re.search(r"#define COGDL_NOALLOC_SCRATCH_BYTES \((\d+)ull << (\d+)\)", open(HEADER).read())
+    return int(m.group(1)) << int(m.group(2))
+
+
+def test_csc_noalloc_validation(L):
+    """The allocation-free transpose refuses graphs whose workspace exceeds its static scratch,
+    and bad arguments, on the host (nothing touches the device)."""
+    limit = _noalloc_limit()
+    assert limit == 64 << 20
+    b = ctypes.c_size_t()
+    lo, hi = 1, 1 << 24                      # largest nnz whose workspace fits the scratch
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        assert L.cogdl_csr_to_csc_workspace(10, 10, mid, ctypes.byref(b)) == OK
+        lo, hi = (mid, hi) if b.value <= limit else (lo, mid - 1)
+    assert 1_500_000 < lo < 1_800_000        # "about 1.6M edges", as the header says
+    nz = lo + 1
+    assert L.cogdl_csr_to_csc_noalloc(10, 10, nz, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, None) == TOO_LARGE
+    assert L.cogdl_csr_to_csc_noalloc(10, 10, _max_nnz() + 1, FAKE, FAKE, None, FAKE, FAKE, None, FAKE,
+                                      None) == TOO_LARGE
+    assert L.cogdl_csr_to_csc_noalloc(-1, 10, 8, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, None) == INVALID
+    assert L.cogdl_csr_to_csc_noalloc(4, 4, 8, FAKE, FAKE, None, None, FAKE, None, FAKE, None) == INVALID
+    assert L.cogdl_csr_to_csc_noalloc(4, 4, 8, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, None) == INVALID
+    assert L.cogdl_csr_to_csc_noalloc(4, 4, 8, FAKE, None, None, FAKE, FAKE, None, FAKE, None) == INVALID
+
+
 def test_attention_validation(L):
     s = ctypes.c_float(0.2)
     # head count bounds
