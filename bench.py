@@ -51,6 +51,16 @@ def parse():
     ap.add_argument("--plain-plans", action="store_true",
                     help="balancer plans without column slicing (the paper's neighbour groups only)")
     ap.add_argument("--alpha-out", action="store_true", help="also write alpha in the GAT step")
+    ap.add_argument("--counter-probe", metavar="JSON", default=None,
+                    help="run one warmup step, one step and the calibration kernels between marker "
+                         "kernels (for rocprofv3 --pmc), write the step's library launch names to JSON")
+    ap.add_argument("--no-live-counters", action="store_true",
+                    help="do not run the counter probe under rocprofv3; take the HBM bytes from the "
+                         "committed record under profiles/ when it matches the sources")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                    help="FETCH_DIR WRITE_DIR PROBE_JSON [REQ_DIR]: write profiles/<workload>_hbm_traffic.json "
+                         "and _hbm_counters.txt from a FETCH_SIZE and a WRITE_SIZE rocprofv3 run of "
+                         "--counter-probe (and a run of the raw read-request counters), then exit")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the steps, copy a buffer of this many MiB (counter calibration)")
     ap.add_argument("--workloads", action="store_true",
@@ -103,54 +113,185 @@ def cpu_model():
 
 
 # ----------------------------------------------------------- HBM counters
+#
+# The roofline fraction is taken from measured bytes: rocprofv3's FETCH_SIZE
+# (bytes the L2 fetched from the fabric) and WRITE_SIZE (bytes it wrote) of the
+# dominant kernel's dispatch in one step of the same workload, each scaled by
+# what the counter reads for a copy of known size.  `--counter-probe` runs one
+# warmup step, one step and the calibration kernels (libcogdl_calib.so: a
+# copy, a streaming read, a gather of whole 128-byte lines and a gather of
+# 16-byte rows, all of known traffic), each section between two marker
+# kernels; bench.py runs it under rocprofv3 as a child process (one pass per
+# counter) and reads the CSV back.  The calibrated record of such a run is
+# also committed under profiles/ and used when the live run is unavailable
+# and the library sources are unchanged.
 
-# The step's candidate roofline kernels: the sources that define each one, its
-# instantiation on the benchmark workload (bf16 in and out, 16-byte vectors,
-# one chunk, buffer gathers), and which of that kernel's dispatches in one step
-# is the op (the SpMM and the transposed SpMM share an instantiation).
-ROOFLINE_KERNELS = {
-    "spmm": dict(files=["common.hpp", "internal.hpp", "spmm_kernel.hpp", "spmm.hip"],
-                 name="void k_spmm<bf16_t, bf16_t, 8, 1, true, false, false>", per_step=2, index=0),
-    "spmm_t": dict(files=["common.hpp", "internal.hpp", "spmm_kernel.hpp", "spmm.hip"],
-                   name="void k_spmm<bf16_t, bf16_t, 8, 1, true, false, false>", per_step=2, index=1),
-    "gat": dict(files=["common.hpp", "internal.hpp", "gat_kernel.hpp", "gat.hip"],
-                name="void k_gat<bf16_t, bf16_t, 8, 1, true, false>", per_step=1, index=0),
-}
+MARKER = "bitwise_not"                     # the torch kernel launched between sections
+PROBE_SECTIONS = ["step", "calib_copy", "calib_read", "calib_gather128", "calib_gather64", "calib_gather32",
+                  "calib_gather16"]
+GATHER_ROW_BYTES = (128, 64, 32, 16)
+CALIB_BYTES = 1 << 30                      # copy and read size
+CALIB_ROWS = 1 << 22                       # rows of each gather, distinct lines of a 2 GiB table
+CALIB_TABLE_LINES = 1 << 24
+HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def kernel_source_sha(kernel: str) -> str:
+def calib_known_bytes():
+    """(read, written) bytes of each calibration section, fixed by its arguments."""
+    n = CALIB_ROWS
+    out = {"calib_copy": (CALIB_BYTES, CALIB_BYTES), "calib_read": (CALIB_BYTES, 4096 * 4)}
+    for rb in GATHER_ROW_BYTES:
+        out[f"calib_gather{rb}"] = (n * rb + 4 * n, 4 * n)
+    return out
+
+
+def library_source_sha() -> str:
+    """Hash of every library source and the header: a committed counter record holds
+    only while it is unchanged."""
+    import glob
     import hashlib
-    here = os.path.dirname(os.path.abspath(__file__))
-    csrc = os.path.join(here, "paper_2103_00959_amd", "csrc")
-    files = ROOFLINE_KERNELS[kernel]["files"]
-    return hashlib.sha256(b"".join(open(os.path.join(csrc, f), "rb").read() for f in files)).hexdigest()[:16]
+    csrc = os.path.join(HERE, "paper_2103_00959_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp")))
+    files.append(os.path.join(HERE, "include", "cogdl.h"))
+    return hashlib.sha256(b"".join(open(f, "rb").read() for f in files)).hexdigest()[:16]
 
 
-def recorded_traffic(workload: str, kernel: str, profiles_dir: str | None = None):
-    """HBM bytes of one launch of the step's kernel `kernel` from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled by the copy calibration;
-    the dispatch of the timed step of a --warmup 1 run), or None when that
-    kernel's sources changed since the counters were taken."""
+def calib_lib():
+    import ctypes
+    L = ctypes.CDLL(os.path.join(HERE, "paper_2103_00959_amd", "libcogdl_calib.so"))
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.cogdl_calib_read.argtypes = [P, i64, P, P]
+    L.cogdl_calib_copy.argtypes = [P, P, i64, P]
+    L.cogdl_calib_gather.argtypes = [P, i64, i32, P, i64, P, P]
+    return L
+
+
+def read_dispatches(d: str, counter: str):
+    """[(kernel name, counter value)] per dispatch, in dispatch order, from the CSV of a
+    rocprofv3 --pmc <counter> --kernel-trace -d d -o run --output-format csv run."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise RuntimeError(f"no counter CSV under {d}")
+    disp = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            k = (f, int(r["Dispatch_Id"]))
+            e = disp.setdefault(k, [r["Kernel_Name"], 0.0])
+            e[1] += float(r["Counter_Value"])
+    return [tuple(v) for _, v in sorted(disp.items(), key=lambda kv: kv[0][1])]
+
+
+def probe_sections(disp):
+    """{section: [(name, value), ...]} between the marker dispatches of one probe run."""
+    marks = [i for i, (n, _) in enumerate(disp) if MARKER in n]
+    if len(marks) != len(PROBE_SECTIONS) + 1:
+        raise RuntimeError(f"expected {len(PROBE_SECTIONS) + 1} marker dispatches, found {len(marks)}")
+    return {sec: disp[marks[j] + 1:marks[j + 1]] for j, sec in enumerate(PROBE_SECTIONS)}
+
+
+def summarize_probe(fetch_dir: str, write_dir: str, launches: list):
+    """Calibrated HBM bytes of every dispatch of the probe's step (launch names from the
+    library's trace, in order) and the calibration table."""
+    F = probe_sections(read_dispatches(fetch_dir, "FETCH_SIZE"))
+    W = probe_sections(read_dispatches(write_dir, "WRITE_SIZE"))
+    known = calib_known_bytes()
+    kib = 1024.0
+    raw = {sec: (sum(v for _, v in F[sec]) * kib, sum(v for _, v in W[sec]) * kib) for sec in known}
+    fetch_scale = known["calib_copy"][0] / raw["calib_copy"][0]
+    write_scale = known["calib_copy"][1] / raw["calib_copy"][1]
+    calib = {}
+    for sec, (kr, kw) in known.items():
+        fr, wr = raw[sec]
+        calib[sec] = dict(known_read=kr, known_write=kw, fetch_raw=fr, write_raw=wr,
+                          read_over_fetch_raw=kr / fr if fr else None,
+                          fetch_calibrated_over_known=fr * fetch_scale / kr if kr else None)
+    step_f, step_w = F["step"], W["step"]
+    if len(step_f) != len(launches) or len(step_w) != len(launches):
+        raise RuntimeError(f"step dispatches {len(step_f)}/{len(step_w)} != {len(launches)} library launches")
+    step = [dict(launch=launches[i], kernel=step_f[i][0], fetch_bytes=step_f[i][1] * kib * fetch_scale,
+                 write_bytes=step_w[i][1] * kib * write_scale) for i in range(len(launches))]
+    return dict(fetch_scale=fetch_scale, write_scale=write_scale, calibration=calib, step=step,
+                step_bytes=sum(d["fetch_bytes"] + d["write_bytes"] for d in step))
+
+
+def kernel_traffic(summary, launch: str):
+    """Calibrated bytes of the first dispatch of library launch `launch` in the step."""
+    for d in summary["step"]:
+        if d["launch"] == launch:
+            return dict(bytes=d["fetch_bytes"] + d["write_bytes"], fetch_bytes=d["fetch_bytes"],
+                        write_bytes=d["write_bytes"], kernel=d["kernel"])
+    return None
+
+
+def recorded_traffic(workload: str, profiles_dir: str | None = None):
+    """The committed counter summary of the step (profiles/<workload>_hbm_traffic.json), or
+    None when any library source changed since it was taken."""
     if profiles_dir is None:
-        profiles_dir = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles")
+        profiles_dir = os.path.join(HERE, "profiles")
     path = os.path.join(profiles_dir, f"{workload}_hbm_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    shas = rec.get("source_sha16")
-    if not isinstance(shas, dict) or shas.get(kernel) != kernel_source_sha(kernel):
+    if rec.get("source_sha16") != library_source_sha():
         return None
-    spec = ROOFLINE_KERNELS[kernel]
-    disp = rec["kernels"].get(spec["name"])
-    if not disp:
-        return None
-    i = spec["per_step"] * rec.get("warmup", 1) + spec["index"]
-    if i >= len(disp):
-        return None
-    d = disp[i]
-    return dict(bytes=d["fetch_bytes"] + d["write_bytes"], fetch_bytes=d["fetch_bytes"],
-                write_bytes=d["write_bytes"], l2_hit=d.get("l2_hit"), kernel=spec["name"], dispatch=i,
-                dur_ms=d["dur_ms"], source=os.path.basename(path))
+    rec["source"] = os.path.relpath(path, HERE)
+    return rec
+
+
+def probe_command(args, out_json: str):
+    cmd = [sys.executable, os.path.abspath(__file__), "--counter-probe", out_json, "--config", str(args.config),
+           "--group-size", str(args.group_size)]
+    if args.plain_plans:
+        cmd.append("--plain-plans")
+    if args.alpha_out:
+        cmd.append("--alpha-out")
+    return cmd
+
+
+def live_counters(args, timeout_s: float = 300.0):
+    """Run the counter probe under rocprofv3 (a FETCH_SIZE pass, then a WRITE_SIZE pass) as
+    child processes and summarize it; (summary, None) or (None, reason)."""
+    import shutil
+    import signal
+    import subprocess
+    import tempfile
+    exe = shutil.which("rocprofv3") or "/opt/rocm/bin/rocprofv3"
+    if not os.path.exists(exe):
+        return None, "rocprofv3 not found"
+    base = tempfile.mkdtemp(prefix="cogdl_counters_", dir="/tmp")
+    out_json = os.path.join(base, "probe.json")
+    env = dict(os.environ, TMPDIR="/tmp")
+    dirs = {}
+    for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        d = os.path.join(base, tag)
+        cmd = [exe, "--pmc", ctr, "--kernel-trace", "-d", d, "-o", "run", "--output-format", "csv", "--"]
+        cmd += probe_command(args, out_json)
+        log(f"counters: {ctr} pass")
+        with open(os.path.join(base, f"{tag}.log"), "w") as lf:
+            p = subprocess.Popen(cmd, cwd="/tmp", env=env, stdout=lf, stderr=subprocess.STDOUT,
+                                 start_new_session=True)
+            try:
+                rc = p.wait(timeout=timeout_s)
+            except subprocess.TimeoutExpired:
+                os.killpg(p.pid, signal.SIGKILL)
+                p.wait()
+                return None, f"{ctr} pass timed out after {timeout_s:.0f} s"
+        # rocprofv3 may end with a segmentation fault after the program finished and
+        # its results are complete: the probe's own output file says whether it did
+        if rc != 0 and not os.path.exists(out_json):
+            return None, f"{ctr} pass exited with {rc}"
+        dirs[tag] = d
+    try:
+        probe = json.load(open(out_json))
+        summary = summarize_probe(dirs["fetch"], dirs["write"], probe["launches"])
+    except Exception as e:       # noqa: BLE001  (a measurement aid: report, never fail the bench)
+        return None, f"counter summary failed: {e}"
+    summary["source"] = "live: rocprofv3 child runs of bench.py --counter-probe in this run"
+    return summary, None
 
 
 def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
@@ -499,6 +640,130 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
         torch.cuda.empty_cache()
 
 
+def counter_probe(args, cg, step, dev):
+    """The probe run under rocprofv3: one warmup step, then [marker] one step [marker] and the
+    calibration kernels, each followed by a marker; the step's library launch names go to
+    args.counter_probe (JSON), so that its dispatches can be named one by one."""
+    import ctypes
+
+    import torch
+    # calibration inputs first: every kernel that prepares them runs before the first marker
+    C = calib_lib()
+    s = cg._stream()
+    P = lambda t: ctypes.c_void_p(t.data_ptr())                      # noqa: E731
+    src = torch.full((CALIB_BYTES,), 1, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    sink = torch.empty(4096, dtype=torch.int32, device=dev)
+    table = torch.full((CALIB_TABLE_LINES * 128,), 2, dtype=torch.uint8, device=dev)
+    gen = torch.Generator(device=dev).manual_seed(17)
+    perm = torch.randperm(CALIB_TABLE_LINES, generator=gen, device=dev, dtype=torch.int64)
+    # each gather reads its own rows: CALIB_ROWS distinct lines, disjoint between sections
+    idx = [perm[i * CALIB_ROWS:(i + 1) * CALIB_ROWS].to(torch.int32).contiguous()
+           for i in range(len(GATHER_ROW_BYTES))]
+    lo, hi = int(perm.min()), int(perm.max())
+    assert 0 <= lo and hi < CALIB_TABLE_LINES        # every gathered row is inside the table
+    out = torch.empty(CALIB_ROWS, dtype=torch.int32, device=dev)
+    marker = torch.zeros(1, dtype=torch.int32, device=dev)
+    step()
+    torch.cuda.synchronize()
+    cg.trace_enable(4096)
+    cg.trace_filter(None)
+    cg.trace_reset()
+    marker.bitwise_not_()
+    step()
+    marker.bitwise_not_()
+    torch.cuda.synchronize()
+    launches = [n for n, _ in cg.trace_read()]
+    cg.trace_enable(0)
+    checks = [C.cogdl_calib_copy(P(src), P(dst), CALIB_BYTES, s)]
+    marker.bitwise_not_()
+    checks.append(C.cogdl_calib_read(P(src), CALIB_BYTES, P(sink), s))
+    marker.bitwise_not_()
+    for rb, ix in zip(GATHER_ROW_BYTES, idx):
+        checks.append(C.cogdl_calib_gather(P(table), 128, rb, P(ix), CALIB_ROWS, P(out), s))
+        marker.bitwise_not_()
+    torch.cuda.synchronize()
+    if any(checks):
+        raise SystemExit(f"calibration kernel refused its arguments: {checks}")
+    with open(args.counter_probe, "w") as f:
+        json.dump({"launches": launches, "sections": PROBE_SECTIONS}, f)
+    log(f"counter probe done: {len(launches)} library launches in the step")
+
+
+REQ_COUNTERS = ("TCC_BUBBLE_sum", "TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum")
+
+
+def request_mix(req_dir, launches):
+    """Read requests the L2 sent to the fabric per section (and per step launch), by size:
+    128-byte (TCC_BUBBLE), 32-byte (TCC_EA0_RDREQ_32B) and the 64-byte rest of TCC_EA0_RDREQ
+    (the counters FETCH_SIZE is computed from)."""
+    secs = {c: probe_sections(read_dispatches(req_dir, c)) for c in REQ_COUNTERS}
+    out = {}
+    for sec in PROBE_SECTIONS:
+        rows = list(zip(*(secs[c][sec] for c in REQ_COUNTERS)))
+        names = ["calib"] if sec != "step" else launches
+        if sec == "step" and len(rows) != len(launches):
+            raise RuntimeError("request-counter run does not match the probe's launches")
+        for i, r in enumerate(rows):
+            b128, tot, b32 = (v for _, v in r)
+            key = sec if sec != "step" else f"step/{i:02d} {names[i]}"
+            if sec != "step" and i > 0:
+                prev = out[key]
+                b128, tot, b32 = prev["req128"] + b128, prev["req_total"] + tot, prev["req32"] + b32
+            out[key] = dict(req128=b128, req32=b32, req64=tot - b128 - b32, req_total=tot)
+    return out
+
+
+def write_counter_profile(args, fetch_dir, write_dir, probe_json, req_dir=None):
+    """profiles/<workload>_hbm_traffic.json (the record bench.py falls back on) and a readable
+    _hbm_counters.txt from one FETCH_SIZE and one WRITE_SIZE run of --counter-probe."""
+    from paper_2103_00959_amd import synth
+    cfg = synth.CONFIGS[args.config]
+    probe = json.load(open(probe_json))
+    summ = summarize_probe(fetch_dir, write_dir, probe["launches"])
+    summ["source_sha16"] = library_source_sha()
+    summ["workload"] = cfg["name"]
+    flags = " ".join(probe_command(args, "PROBE_JSON")[3:])
+    cmd = ("cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {c} --kernel-trace -d DIR -o run --output-format csv -- "
+           f"python3 bench.py --counter-probe PROBE_JSON {flags}")
+    summ["commands"] = {"fetch": cmd.format(c="FETCH_SIZE"), "write": cmd.format(c="WRITE_SIZE")}
+    out = os.path.join(HERE, "profiles", f"{cfg['name']}_hbm_traffic.json")
+    json.dump(summ, open(out, "w"), indent=1)
+    lines = [f"# HBM bytes of one step of {cfg['name']} on one MI355X, per dispatch, from rocprofv3 counters",
+             f"# FETCH_SIZE: {summ['commands']['fetch']}",
+             f"# WRITE_SIZE: {summ['commands']['write']}",
+             f"# (bench.py runs the same two passes itself unless --no-live-counters; this record is its fallback)",
+             f"# library sources sha256[:16] {summ['source_sha16']}",
+             "# calibration (kernels of known traffic, libcogdl_calib.so): bytes the section must read / write,",
+             "# raw counter bytes, and known / raw; the copy's ratios are the scales applied to every dispatch",
+             f"# {'section':18s} {'known_read':>12s} {'fetch_raw':>12s} {'read/raw':>9s} {'known_wr':>12s} "
+             f"{'write_raw':>12s} {'wr/raw':>7s}"]
+    for sec, c in summ["calibration"].items():
+        lines.append(f"# {sec:18s} {c['known_read']:12.4e} {c['fetch_raw']:12.4e} "
+                     f"{c['known_read'] / c['fetch_raw']:9.4f} {c['known_write']:12.4e} {c['write_raw']:12.4e} "
+                     f"{(c['known_write'] / c['write_raw']) if c['write_raw'] else float('nan'):7.4f}")
+    lines.append(f"# scales: fetch x{summ['fetch_scale']:.4f}, write x{summ['write_scale']:.4f}")
+    lines.append(f"{'launch':22s} {'kernel':64s} {'fetch_GB':>9s} {'write_GB':>9s}")
+    for d in summ["step"]:
+        lines.append(f"{d['launch']:22s} {d['kernel'][:64]:64s} {d['fetch_bytes'] / 1e9:9.4f} "
+                     f"{d['write_bytes'] / 1e9:9.4f}")
+    lines.append(f"step total {summ['step_bytes'] / 1e9:.3f} GB")
+    if req_dir:
+        mix = request_mix(req_dir, probe["launches"])
+        summ["read_requests"] = mix
+        json.dump(summ, open(out, "w"), indent=1)
+        lines.append("# read requests the L2 sent to the fabric, by size (raw counts: "
+                     + " ".join(REQ_COUNTERS) + f"), command: {cmd.format(c=' '.join(REQ_COUNTERS))}")
+        lines.append(f"{'section / launch':40s} {'128B':>12s} {'64B':>12s} {'32B':>12s} {'bytes_by_size':>14s}")
+        for k, v in mix.items():
+            if k.startswith("step/") and not any(t in k for t in (" spmm", " gat", "radix_scatter")):
+                continue
+            by = 128 * v["req128"] + 64 * v["req64"] + 32 * v["req32"]
+            lines.append(f"{k:40s} {v['req128']:12.4e} {v['req64']:12.4e} {v['req32']:12.4e} {by:14.4e}")
+    open(os.path.join(HERE, "profiles", f"{cfg['name']}_hbm_counters.txt"), "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -507,6 +772,11 @@ def main():
         sys.exit(2)
     if args.workloads:
         run_workloads(reps=args.reps, warm_reps=args.warm_reps, cpu=not args.no_cpu_baseline)
+        return
+    if args.summarize_counters:
+        if len(args.summarize_counters) not in (3, 4):
+            raise SystemExit("--summarize-counters FETCH_DIR WRITE_DIR PROBE_JSON [REQ_DIR]")
+        write_counter_profile(args, *args.summarize_counters)
         return
     import torch
 
@@ -522,16 +792,6 @@ def main():
     N, M, E = g.n_rows, g.n_cols, g.nnz
     F, H, D = cfg["F"], cfg["H"], cfg["D"]
     log(f"graph ready N={N} E={E} in {time.time() - t0:.1f}s")
-    X32 = synth.normal_f32((M, F), 2000 + args.config)
-    X_bits = synth.f32_to_bf16_bits(X32)
-    del X32
-    G_bits = synth.f32_to_bf16_bits(synth.normal_f32((N, F), 4000 + args.config))
-    Xg_bits = synth.f32_to_bf16_bits(synth.normal_f32((M, H * D), 2100 + args.config))
-    rng = np.random.default_rng(3000 + args.config)
-    sd = rng.standard_normal((N, H), dtype=np.float32)
-    ss = rng.standard_normal((M, H), dtype=np.float32)
-    log(f"features ready in {time.time() - t0:.1f}s")
-
     dev = torch.device("cuda:0")
 
     def up(a, dt=None):
@@ -539,10 +799,30 @@ def main():
         return t.view(dt) if dt is not None else t
 
     rowptr, col, val = up(g.rowptr), up(g.col), up(g.val)
-    X = up(X_bits.view(np.int16), torch.bfloat16)
-    Gt = up(G_bits.view(np.int16), torch.bfloat16)
-    Xg = up(Xg_bits.view(np.int16), torch.bfloat16).view(M, H, D)
-    s_dst, s_src = up(sd), up(ss)
+    if args.counter_probe:
+        # The counter probe only measures memory traffic, which these kernels take from
+        # the graph and the shapes alone (no access depends on a feature or score value):
+        # normal features drawn on the device spare the host generation.
+        gen = torch.Generator(device=dev).manual_seed(2000 + args.config)
+        X = torch.randn((M, F), generator=gen, device=dev).to(torch.bfloat16)
+        Gt = torch.randn((N, F), generator=gen, device=dev).to(torch.bfloat16)
+        Xg = torch.randn((M, H, D), generator=gen, device=dev).to(torch.bfloat16)
+        s_dst = torch.randn((N, H), generator=gen, device=dev)
+        s_src = torch.randn((M, H), generator=gen, device=dev)
+    else:
+        X32 = synth.normal_f32((M, F), 2000 + args.config)
+        X_bits = synth.f32_to_bf16_bits(X32)
+        del X32
+        G_bits = synth.f32_to_bf16_bits(synth.normal_f32((N, F), 4000 + args.config))
+        Xg_bits = synth.f32_to_bf16_bits(synth.normal_f32((M, H * D), 2100 + args.config))
+        rng = np.random.default_rng(3000 + args.config)
+        sd = rng.standard_normal((N, H), dtype=np.float32)
+        ss = rng.standard_normal((M, H), dtype=np.float32)
+        X = up(X_bits.view(np.int16), torch.bfloat16)
+        Gt = up(G_bits.view(np.int16), torch.bfloat16)
+        Xg = up(Xg_bits.view(np.int16), torch.bfloat16).view(M, H, D)
+        s_dst, s_src = up(sd), up(ss)
+    log(f"features ready in {time.time() - t0:.1f}s")
     Y = torch.empty((N, F), dtype=torch.bfloat16, device=dev)
     dX = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
     Yg = torch.empty((N, H, D), dtype=torch.bfloat16, device=dev)
@@ -607,6 +887,10 @@ def main():
         cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg,  # a5-a7
                          alpha_out=alpha)
         mark(6)
+
+    if args.counter_probe:
+        counter_probe(args, cg, step, dev)
+        return
 
     if args.calib_copy_mib > 0:
         # a plain device-to-device copy of known size, for scaling the HBM counters
@@ -706,15 +990,42 @@ def main():
         "gat": us["E_long"] * e_gat + us["R_long"] * r_gat,
     }
     dom = max(kbytes, key=lambda k: kernels.get(k, {"total_ms": 0})["total_ms"])
+    dom_op = {"spmm": "spmm", "spmm_t": "spmm_t", "gat": "gat_aggregate"}[dom]
     dom_bytes = kbytes[dom]
     dom_launches = [ms for name, ms in roof_trace if name == dom]
     dom_ms = sum(dom_launches) / len(dom_launches)
-    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    tr = recorded_traffic(cfg["name"], dom)
-    roofline = dict(bound="hbm", kernel=dom, achieved=achieved, peak=HBM_PEAK_GBPS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBPS, traffic=(tr["bytes"] if tr else None),
-                    algorithmic_bytes_per_launch=dom_bytes, avg_ms=dom_ms,
-                    traffic_detail=tr)
+    eff = dom_bytes / (dom_ms * 1e-3) / 1e9
+    # measured HBM bytes: the probe under rocprofv3 in this run, else the committed record
+    counters, why = (None, "--no-live-counters") if args.no_live_counters else live_counters(args)
+    if counters is None:
+        log(f"live counters unavailable ({why}); falling back on the committed record")
+        counters = recorded_traffic(cfg["name"])
+    tr = kernel_traffic(counters, dom) if counters else None
+    hbm_rate = tr["bytes"] / (dom_ms * 1e-3) / 1e9 if tr else None
+    roofline = dict(
+        bound="hbm", kernel=dom, achieved=hbm_rate, peak=HBM_PEAK_GBPS, unit="GB/s",
+        frac=hbm_rate / HBM_PEAK_GBPS if tr else None, traffic=tr["bytes"] if tr else None,
+        basis=("achieved = measured HBM bytes of one launch (rocprofv3 FETCH_SIZE + WRITE_SIZE of the "
+               "kernel's dispatch in one step of this workload, each scaled by what the counter reads "
+               "for a copy of known size) / the kernel's mean launch time over the timed region (HIP "
+               "events on its stream)"),
+        avg_ms=dom_ms, launches_timed=len(dom_launches),
+        effective_GBps=eff, effective_frac=eff / HBM_PEAK_GBPS, algorithmic_bytes_per_launch=dom_bytes,
+        effective_note=("algorithmic bytes (one gather of the feature row per nonzero) / time: above "
+                        "the HBM peak when hot rows are served from L2, so not an HBM fraction"),
+        compulsory_GBps=B_unique[dom_op] / (op_ms[dom_op] * 1e-3) / 1e9,
+        traffic_detail=(dict(tr, source=counters.get("source"), fetch_scale=counters["fetch_scale"],
+                             write_scale=counters["write_scale"],
+                             hbm_over_algorithmic=tr["bytes"] / dom_bytes) if tr else None),
+        counters_unavailable=None if counters else why)
+    step_hbm = None
+    if counters:
+        sb = counters["step_bytes"]
+        step_hbm = dict(bytes=sb, GBps=sb / (ms_step * 1e-3) / 1e9, frac=sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                        note="calibrated FETCH_SIZE + WRITE_SIZE summed over every dispatch of one step / step time",
+                        calibration=counters["calibration"],
+                        per_launch_GB={f"{i:02d} {d['launch']}": round((d["fetch_bytes"] + d["write_bytes"]) / 1e9, 4)
+                                       for i, d in enumerate(counters["step"])})
 
     # Entry points outside the fused forward step, timed on the same inputs:
     # the standalone SDDMM + edge softmax (alpha written), the fused
@@ -896,6 +1207,7 @@ def main():
         "ops_outside_step": extra_ops,
         "kernels": kernels,
         "roofline": roofline,
+        "step_hbm": step_hbm,
         "inference": inference,
     }
     if not args.no_cpu_baseline:

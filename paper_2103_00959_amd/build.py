@@ -19,6 +19,9 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcogdl_mi355.so")
+# counter-calibration kernels (known traffic), a library of their own
+CALIB_LIB = os.path.join(HERE, "libcogdl_calib.so")
+CALIB_SOURCES = ["calib.hip"]
 SOURCES = ["primitives.hip", "plan.hip", "spmm.hip", "gspmm.hip", "gat.hip", "gat_bwd.hip", "dense.hip", "codec.hip", "csc.hip", "trace.hip"]
 
 ARCH = "gfx950"
@@ -43,7 +46,7 @@ def build(verbose: bool = True, jobs: int | None = None) -> str:
     t0 = time.time()
     procs = []
     objs = []
-    for src in SOURCES:
+    for src in SOURCES + CALIB_SOURCES:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
         objs.append(obj)
         cmd = [cc, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
@@ -61,9 +64,12 @@ def build(verbose: bool = True, jobs: int | None = None) -> str:
             print("\n".join(lines))
     if failed:
         raise RuntimeError(f"hipcc failed for {failed}")
-    tmp = LIB + f".tmp{os.getpid()}"
-    subprocess.run([cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs], check=True)
-    os.replace(tmp, LIB)
+    calib_objs = objs[len(SOURCES):]
+    objs = objs[:len(SOURCES)]
+    for lib_path, lib_objs in ((LIB, objs), (CALIB_LIB, calib_objs)):
+        tmp = lib_path + f".tmp{os.getpid()}"
+        subprocess.run([cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *lib_objs], check=True)
+        os.replace(tmp, lib_path)
     if verbose:
         print(f"[build] {LIB} in {time.time() - t0:.1f}s")
     return LIB

@@ -36,6 +36,31 @@ def test_header_symbols_exported(L):
         assert hasattr(L, s), s
 
 
+def test_calibration_library_exports_and_validation():
+    """libcogdl_calib.so (counter calibration kernels) exports what include/cogdl_calib.h
+    declares and refuses bad arguments on the host (nothing is launched here)."""
+    from paper_2103_00959_amd import build
+    if not os.path.exists(build.CALIB_LIB):
+        build.build(verbose=False)
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "cogdl_calib.h")).read(), flags=re.S)
+    syms = sorted(set(re.findall(r"\b(cogdl_calib_[a-z_0-9]+)\s*\(", text)))
+    assert syms == ["cogdl_calib_copy", "cogdl_calib_gather", "cogdl_calib_read"]
+    import bench
+    C = bench.calib_lib()
+    for s_ in syms:
+        assert hasattr(C, s_)
+    A = _p(0x100000)                       # 128-byte aligned, never dereferenced
+    assert C.cogdl_calib_read(A, 100, A, None) == 1             # not a multiple of 16
+    assert C.cogdl_calib_read(_p(0x100008), 160, A, None) == 1  # misaligned
+    assert C.cogdl_calib_read(None, 160, A, None) == 1
+    assert C.cogdl_calib_copy(A, A, 0, None) == 1
+    assert C.cogdl_calib_copy(A, _p(0x100004), 160, None) == 1
+    assert C.cogdl_calib_gather(A, 128, 48, A, 10, A, None) == 1    # row size
+    assert C.cogdl_calib_gather(A, 64, 16, A, 10, A, None) == 1     # stride not a line multiple
+    assert C.cogdl_calib_gather(_p(0x100040), 128, 16, A, 10, A, None) == 1
+    assert C.cogdl_calib_gather(A, 128, 16, A, 0, A, None) == 1
+
+
 def test_status_strings_and_version(L):
     for code in range(7):
         assert len(L.cogdl_status_string(code)) > 0

@@ -5,25 +5,63 @@ import json
 import bench
 
 
+def _write_probe_csv(d, counter, rows):
+    """A rocprofv3-style counter CSV: one row per (dispatch, counter)."""
+    import csv
+    d.mkdir(parents=True)
+    with open(d / "run_counter_collection.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for i, (name, v) in enumerate(rows):
+            # two rows for one dispatch (per-dimension values are summed)
+            w.writerow({"Dispatch_Id": i + 1, "Kernel_Name": name, "Counter_Name": counter,
+                        "Counter_Value": v / 2})
+            w.writerow({"Dispatch_Id": i + 1, "Kernel_Name": name, "Counter_Name": counter,
+                        "Counter_Value": v / 2})
+
+
+def test_probe_summary_from_counter_csv(tmp_path):
+    """Sections are cut at the marker dispatches, the copy sets the scales, and every dispatch
+    of the step gets its launch name and calibrated bytes."""
+    M = "void at::native::bitwise_not_kernel"
+    known = bench.calib_known_bytes()
+    kib = 1024.0
+    fetch = [("warm", 1.0), (M, 0), ("void k_spmm<...>", 100.0), ("void k_gat<...>", 300.0), (M, 0),
+             ("copy", known["calib_copy"][0] / 2 / kib), (M, 0), ("read", known["calib_read"][0] / 2 / kib),
+             (M, 0), ("g128", known["calib_gather128"][0] / 2 / kib), (M, 0), ("g64", 4096.0), (M, 0),
+             ("g32", 4096.0), (M, 0), ("g16", 4096.0), (M, 0)]
+    write = [(n, (v / 2 if n not in ("copy",) else known["calib_copy"][1] / kib)) for n, v in fetch]
+    _write_probe_csv(tmp_path / "f", "FETCH_SIZE", fetch)
+    _write_probe_csv(tmp_path / "w", "WRITE_SIZE", write)
+    s = bench.summarize_probe(str(tmp_path / "f"), str(tmp_path / "w"), ["spmm", "gat"])
+    assert s["fetch_scale"] == 2.0 and s["write_scale"] == 1.0
+    assert [d["launch"] for d in s["step"]] == ["spmm", "gat"]
+    g = bench.kernel_traffic(s, "gat")
+    assert g["fetch_bytes"] == 300.0 * kib * 2 and g["write_bytes"] == 150.0 * kib
+    assert s["step_bytes"] == (100 + 300) * kib * 2 + (50 + 150) * kib
+    assert abs(s["calibration"]["calib_read"]["fetch_calibrated_over_known"] - 1.0) < 1e-12
+    assert abs(s["calibration"]["calib_gather128"]["fetch_calibrated_over_known"] - 1.0) < 1e-12
+    assert bench.kernel_traffic(s, "spmm_t") is None
+    # a launch list that does not match the step's dispatches is refused
+    import pytest
+    with pytest.raises(RuntimeError):
+        bench.summarize_probe(str(tmp_path / "f"), str(tmp_path / "w"), ["spmm"])
+
+
 def test_recorded_traffic_lookup(tmp_path):
     # the committed record either matches the current sources or is ignored
-    for k in bench.ROOFLINE_KERNELS:
-        r = bench.recorded_traffic("skewed_rmat_2400000_hubs", k)
-        assert r is None or r["bytes"] > 0
-    # a record written for the current sources is found at the timed step's dispatch
+    r = bench.recorded_traffic("skewed_rmat_2400000_hubs")
+    assert r is None or r["step_bytes"] > 0
     prof = tmp_path / "profiles"
     prof.mkdir()
-    spec = bench.ROOFLINE_KERNELS["spmm_t"]
-    disp = [{"fetch_bytes": 10.0 * i, "write_bytes": 1.0, "dur_ms": 0.1} for i in range(6)]
-    rec = {"source_sha16": {k: bench.kernel_source_sha(k) for k in bench.ROOFLINE_KERNELS},
-           "warmup": 1, "kernels": {spec["name"]: disp}}
+    rec = {"source_sha16": bench.library_source_sha(), "fetch_scale": 2.0, "write_scale": 1.0,
+           "step": [{"launch": "gat", "kernel": "k", "fetch_bytes": 3.0, "write_bytes": 1.0}], "step_bytes": 4.0}
     (prof / "wl_hbm_traffic.json").write_text(json.dumps(rec))
-    r = bench.recorded_traffic("wl", "spmm_t", str(prof))
-    assert r["dispatch"] == 3 and r["bytes"] == 31.0
-    # stale sources: ignored
-    rec["source_sha16"]["spmm_t"] = "0" * 16
+    r = bench.recorded_traffic("wl", str(prof))
+    assert bench.kernel_traffic(r, "gat")["bytes"] == 4.0
+    rec["source_sha16"] = "0" * 16                  # stale sources: ignored
     (prof / "wl_hbm_traffic.json").write_text(json.dumps(rec))
-    assert bench.recorded_traffic("wl", "spmm_t", str(prof)) is None
+    assert bench.recorded_traffic("wl", str(prof)) is None
 
 
 def test_byte_models_match_the_workload_table():
