@@ -50,7 +50,12 @@ def parse():
     ap.add_argument("--group-size", type=int, default=0)
     ap.add_argument("--plain-plans", action="store_true",
                     help="balancer plans without column slicing (the paper's neighbour groups only)")
-    ap.add_argument("--alpha-out", action="store_true", help="also write alpha in the GAT step")
+    ap.add_argument("--alpha-out", action="store_true",
+                    help="also write alpha in the GAT step (takes the given-scores entry point)")
+    ap.add_argument("--gat-scores", choices=("proj", "given"), default="proj",
+                    help="GAT step: source scores projected from the gathered feature rows "
+                         "(cogdl_gat_aggregate_proj, s_src = X a_src) or read from s_src "
+                         "(cogdl_gat_aggregate)")
     ap.add_argument("--counter-probe", metavar="JSON", default=None,
                     help="run one warmup step, one step and the calibration kernels between marker "
                          "kernels (for rocprofv3 --pmc), write the step's library launch names to JSON")
@@ -85,6 +90,12 @@ def b_csc(N, M, E):
 def b_gat(N, E, H, D, sx, sy, alpha_out):
     return 4 * (N + 1) + 4 * E + 4 * N * H + 4 * E * H + E * H * D * sx + N * H * D * sy + (
         4 * E * H if alpha_out else 0)
+
+
+def b_gat_proj(N, E, H, D, sx, sy):
+    """The fused aggregation with source scores projected from the gathered rows: no score row
+    per nonzero, the attention vector a_src (4HD) once instead."""
+    return 4 * (N + 1) + 4 * E + 4 * N * H + E * H * D * sx + N * H * D * sy + 4 * H * D
 
 
 def b_plan(N, n_units):
@@ -249,6 +260,7 @@ def probe_command(args, out_json: str):
         cmd.append("--plain-plans")
     if args.alpha_out:
         cmd.append("--alpha-out")
+    cmd += ["--gat-scores", args.gat_scores]
     return cmd
 
 
@@ -294,12 +306,21 @@ def live_counters(args, timeout_s: float = 300.0):
     return summary, None
 
 
-def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
+def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s, a_src=None):
     """Time the oracle (fp64, all host threads) on a random row sample of the
-    SpMM and GAT steps, growing the sample until the budget is spent."""
+    SpMM and GAT steps, growing the sample until the budget is spent.  With
+    a_src (projected source scores) the oracle first computes every node's
+    source score (timed and counted: X read once), then aggregates."""
     import oracle
     threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     oracle.set_threads(threads)
+    t_proj, b_proj = 0.0, 0
+    if a_src is not None:
+        t0 = time.perf_counter()
+        ss64 = oracle.head_scores(Xg_bits, a_src, a_src, H, D, z_dtype=oracle.BF16)[0]
+        t_proj = time.perf_counter() - t0
+        ss = ss64.astype(np.float32)
+        b_proj = g.n_cols * H * D * 2 + 4 * g.n_cols * H
     rng = np.random.default_rng(9)
     deg = np.diff(g.rowptr.astype(np.int64))
     rows_all = rng.permutation(g.n_rows).astype(np.int32)
@@ -316,13 +337,17 @@ def cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, budget_s):
         oracle.spmm(g.rowptr, g.col, g.val, X_bits, x_dtype=oracle.BF16, rows=sel)
         oracle.gat(g.rowptr, g.col, sd, ss, Xg_bits, H, D, slope=0.2, x_dtype=oracle.BF16, rows=sel)
         t_total += time.perf_counter() - t0
-        bytes_total += b_spmm(sel.size, g.n_cols, e, F, 2, 2) + b_gat(sel.size, e, H, D, 2, 2, False)
+        bytes_total += b_spmm(sel.size, g.n_cols, e, F, 2, 2) + (
+            b_gat(sel.size, e, H, D, 2, 2, False) if a_src is None else b_gat_proj(sel.size, e, H, D, 2, 2))
         edges_total += 2 * e
         chunk = min(chunk * 2, 200000)
+    t_total += t_proj
+    bytes_total += b_proj
     return dict(value=bytes_total / t_total / 1e9, unit="GB/s", cores=threads, kind="oracle",
                 cpu=cpu_model(),
                 sample=(f"SpMM (F=256 bf16) + fused GAT (4x64 bf16) on {done_rows} random rows "
-                        f"({edges_total // 2} nonzeros each) of the same graph, fp64 oracle"),
+                        f"({edges_total // 2} nonzeros each) of the same graph, fp64 oracle"
+                        + ("; the source scores of all nodes first (X a_src)" if a_src is not None else "")),
                 seconds=t_total, edges_per_s=edges_total / t_total)
 
 
@@ -809,6 +834,7 @@ def main():
         Xg = torch.randn((M, H, D), generator=gen, device=dev).to(torch.bfloat16)
         s_dst = torch.randn((N, H), generator=gen, device=dev)
         s_src = torch.randn((M, H), generator=gen, device=dev)
+        a_src = torch.randn((H, D), generator=gen, device=dev) / float(np.sqrt(D))
     else:
         X32 = synth.normal_f32((M, F), 2000 + args.config)
         X_bits = synth.f32_to_bf16_bits(X32)
@@ -818,10 +844,13 @@ def main():
         rng = np.random.default_rng(3000 + args.config)
         sd = rng.standard_normal((N, H), dtype=np.float32)
         ss = rng.standard_normal((M, H), dtype=np.float32)
+        # the attention vector of the projected source scores: N(0, 1/D) per entry, so that
+        # s_src = X a_src is N(0, 1) like the given scores
+        a_src_h = (np.random.default_rng(3100 + args.config).standard_normal((H, D)) / np.sqrt(D)).astype(np.float32)
         X = up(X_bits.view(np.int16), torch.bfloat16)
         Gt = up(G_bits.view(np.int16), torch.bfloat16)
         Xg = up(Xg_bits.view(np.int16), torch.bfloat16).view(M, H, D)
-        s_dst, s_src = up(sd), up(ss)
+        s_dst, s_src, a_src = up(sd), up(ss), up(a_src_h)
     log(f"features ready in {time.time() - t0:.1f}s")
     Y = torch.empty((N, F), dtype=torch.bfloat16, device=dev)
     dX = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
@@ -870,6 +899,8 @@ def main():
     us, us_t = unit_split(plan, info), unit_split(plan_t, info_t)
 
     OPS = ["plan", "spmm", "csr_to_csc", "plan_t", "spmm_t", "gat_aggregate"]
+    proj = args.gat_scores == "proj" and not args.alpha_out
+    gat_k = "gat_proj" if proj else "gat"          # the GAT step's long-unit kernel
 
     def step(evs=None):
         mark = (lambda i: evs[i].record()) if evs is not None else (lambda i: None)
@@ -884,8 +915,10 @@ def main():
         mark(4)
         cg.spmm_t(colptr, row_t, val_t, Gt, plan_t=plan_t, out=dX)             # a4
         mark(5)
-        cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg,  # a5-a7
-                         alpha_out=alpha)
+        if proj:                                                               # a5-a7
+            cg.gat_aggregate_proj(rowptr, col, s_dst, a_src, Xg, 0.2, plan=plan, out=Yg)
+        else:
+            cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg, alpha_out=alpha)
         mark(6)
 
     if args.counter_probe:
@@ -911,7 +944,7 @@ def main():
     # Timed region: the K steps with HIP events only around the launches of
     # the roofline candidates (an event pair costs the stream a few
     # microseconds; around every launch they would add about 0.6 ms a step).
-    ROOF = ("spmm", "spmm_t", "gat")
+    ROOF = ("spmm", "spmm_t", gat_k)
     cg.trace_enable(128 * args.steps + 64)
     cg.trace_filter(ROOF)
     cg.trace_reset()
@@ -961,13 +994,14 @@ def main():
         "spmm": b_spmm(N, M, E, F, 2, 2),
         "csr_to_csc": b_csc(N, M, E),
         "spmm_t": b_spmm(M, N, E, F, 2, 2),
-        "gat_aggregate": b_gat(N, E, H, D, 2, 2, args.alpha_out),
+        "gat_aggregate": b_gat_proj(N, E, H, D, 2, 2) if proj else b_gat(N, E, H, D, 2, 2, args.alpha_out),
     }
     B_step = sum(B.values())
     value = B_step / (ms_step * 1e-3) / 1e9
     B_unique = dict(B, spmm=b_unique_spmm(N, M, E, F, 2, 2), spmm_t=b_unique_spmm(M, N, E, F, 2, 2),
-                    gat_aggregate=b_unique_gat(N, M, E, H, D, 2, 2))
-    FLOP = {"spmm": 2 * E * F, "spmm_t": 2 * E * F, "gat_aggregate": 2 * E * H * D + 8 * E * H}
+                    gat_aggregate=b_unique_gat(N, M, E, H, D, 2, 2) - (4 * M * H - 4 * H * D if proj else 0))
+    FLOP = {"spmm": 2 * E * F, "spmm_t": 2 * E * F,
+            "gat_aggregate": (4 if proj else 2) * E * H * D + 8 * E * H}
     ops = {}
     for op in OPS:
         ms = op_ms[op]
@@ -983,14 +1017,14 @@ def main():
     # are its own edges and output rows (per nonzero: index, value, one feature
     # row; per row: row pointer and the output row)
     e_sp, r_sp = 8 + F * 2, 4 + F * 2
-    e_gat, r_gat = 4 + 4 * H + H * D * 2, 4 + 4 * H + H * D * 2
+    e_gat, r_gat = 4 + (0 if proj else 4 * H) + H * D * 2, 4 + 4 * H + H * D * 2
     kbytes = {
         "spmm": us["E_long"] * e_sp + us["R_long"] * r_sp,
         "spmm_t": us_t["E_long"] * e_sp + us_t["R_long"] * r_sp,
-        "gat": us["E_long"] * e_gat + us["R_long"] * r_gat,
+        gat_k: us["E_long"] * e_gat + us["R_long"] * r_gat,
     }
     dom = max(kbytes, key=lambda k: kernels.get(k, {"total_ms": 0})["total_ms"])
-    dom_op = {"spmm": "spmm", "spmm_t": "spmm_t", "gat": "gat_aggregate"}[dom]
+    dom_op = {"spmm": "spmm", "spmm_t": "spmm_t", gat_k: "gat_aggregate"}[dom]
     dom_bytes = kbytes[dom]
     dom_launches = [ms for name, ms in roof_trace if name == dom]
     dom_ms = sum(dom_launches) / len(dom_launches)
@@ -1044,10 +1078,8 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
 
-    ms_soft = time_op(lambda: cg.sddmm_edge_softmax(rowptr, col, s_dst, s_src, 0.2, plan=plan,
-                                                    out=alpha_buf))
-    ms_gat_a = time_op(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
-                                                out=Yg, alpha_out=alpha_buf))
+
+
     def time_op_kernels(fn, reps=5):
         """Average time of fn and of each library kernel it launches."""
         ms = time_op(fn, reps)
@@ -1061,6 +1093,13 @@ def main():
             per_k[name] = per_k.get(name, 0.0) + kms / reps
         cg.trace_enable(0)
         return ms, per_k
+
+    ms_gat_given, k_gat_given = time_op_kernels(
+        lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan, out=Yg))
+    ms_soft, k_soft = time_op_kernels(lambda: cg.sddmm_edge_softmax(rowptr, col, s_dst, s_src, 0.2, plan=plan,
+                                                                    out=alpha_buf))
+    ms_gat_a, k_gat_a = time_op_kernels(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
+                                                                 out=Yg, alpha_out=alpha_buf))
 
     # GAT backward (dY random bf16, the forward's alpha), CSR pass + CSC pass
     dYg = up(synth.f32_to_bf16_bits(synth.normal_f32((N, H * D), 4100 + args.config)).view(np.int16),
@@ -1112,10 +1151,14 @@ def main():
     extra_ops = {
         "sddmm_edge_softmax": dict(ms=ms_soft, algorithmic_GB=b_soft / 1e9,
                                    eff_GBps=b_soft / (ms_soft * 1e-3) / 1e9,
-                                   edges_per_s=E / (ms_soft * 1e-3)),
+                                   edges_per_s=E / (ms_soft * 1e-3), kernels_ms=k_soft),
+        "gat_aggregate_given_scores": dict(ms=ms_gat_given, algorithmic_GB=b_gat(N, E, H, D, 2, 2, False) / 1e9,
+                                           eff_GBps=b_gat(N, E, H, D, 2, 2, False) / (ms_gat_given * 1e-3) / 1e9,
+                                           edges_per_s=E / (ms_gat_given * 1e-3), kernels_ms=k_gat_given),
         "gat_aggregate_with_alpha": dict(ms=ms_gat_a, algorithmic_GB=b_gat_a / 1e9,
                                          eff_GBps=b_gat_a / (ms_gat_a * 1e-3) / 1e9,
-                                         edges_per_s=E / (ms_gat_a * 1e-3)),
+                                         edges_per_s=E / (ms_gat_a * 1e-3), kernels_ms=k_gat_a,
+                                         over_given_scores_ms=ms_gat_a - ms_gat_given),
         "gat_backward": dict(ms=ms_bwd, algorithmic_GB=b_bwd / 1e9,
                              eff_GBps=b_bwd / (ms_bwd * 1e-3) / 1e9,
                              edges_per_s=E / (ms_bwd * 1e-3),
@@ -1152,7 +1195,9 @@ def main():
     warm_ops = {
         "spmm": warm(lambda: cg.spmm(rowptr, col, val, X, plan=plan, out=Y)),
         "spmm_t": warm(lambda: cg.spmm_t(colptr, row_t, val_t, Gt, plan_t=plan_t, out=dX)),
-        "gat_aggregate": warm(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
+        "gat_aggregate": warm(lambda: cg.gat_aggregate_proj(rowptr, col, s_dst, a_src, Xg, 0.2, plan=plan,
+                                                            out=Yg)) if proj else
+        warm(lambda: cg.gat_aggregate(rowptr, col, s_dst, s_src, Xg, 0.2, plan=plan,
                                                        out=Yg)),
     }
     for op, w in warm_ops.items():
@@ -1189,7 +1234,10 @@ def main():
                    "balancer": info["mode_name"],
                    "column_slices": None if args.plain_plans else
                    f"8 column ranges, rows over {SLICE_MIN} nonzeros sliced, one unit list per XCD",
-                   "alpha_out": bool(args.alpha_out)},
+                   "alpha_out": bool(args.alpha_out),
+                   "gat_source_scores": ("projected from the gathered feature rows in the kernel: "
+                                         "s_src[j] = X[j] a_src, a_src N(0, 1/D) (cogdl_gat_aggregate_proj)"
+                                         if proj else "given N x H fp32 ~N(0,1) (cogdl_gat_aggregate)")},
         "pct_peak": value / HBM_PEAK_GBPS,
         "edges_per_s": 3 * E / (ms_step * 1e-3),
         "edges_per_s_note": "nonzeros aggregated per second over the three gathers (SpMM, SpMM^T, GAT)",
@@ -1212,7 +1260,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("CPU baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(g, X_bits, Xg_bits, sd, ss, H, D, F, args.cpu_seconds,
+                                           a_src=a_src_h if proj else None)
         log(f"CPU baseline {out['cpu_baseline']['value']:.2f} GB/s on {out['cpu_baseline']['cores']} threads")
     plan.close()
     plan_t.close()

@@ -346,6 +346,30 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
                                      float *alpha_out, const float *bias, cogdl_act act,
                                      const cogdl_plan *plan, hipStream_t stream);
 
+/* The fused GAT aggregation of a GAT layer whose source scores are the
+ * projection of the aggregated features (section 2.2's multi-head attention;
+ * in a GAT layer s_src = Z a_src per head): instead of reading s_src, each
+ * edge's source score is formed from the feature row the aggregation gathers
+ * anyway,
+ *     s_src[j, h] = sum_d X[j, h, d] * a_src[h, d]      (fp32, in the kernel)
+ * and the scores, LeakyReLU, edge softmax and multi-head SpMM follow as in
+ * cogdl_gat_aggregate_act.  This spares the random score-row read of every
+ * edge (a whole cache line for a 4H-byte row).  a_src: fp32 H x D.  The head's
+ * D features must be whole 16-byte vectors (D * element size a multiple of
+ * 16) with D / (16 / element size) a power of two, and X and Y 16-byte
+ * aligned; other shapes give COGDL_ERR_INVALID (use cogdl_head_scores and
+ * cogdl_gat_aggregate_act).  Attention weights are not written (a backward
+ * pass takes s_src from cogdl_head_scores and alpha from cogdl_gat_aggregate).
+ * The scores are rounded in another order than cogdl_head_scores rounds
+ * them, so the two paths agree to rounding, not bit for bit.  Other arguments
+ * and errors as for cogdl_gat_aggregate_act. */
+cogdl_status cogdl_gat_aggregate_proj(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col, int32_t H,
+                                      int32_t D, const float *s_dst, const float *a_src,
+                                      float negative_slope, const void *X, cogdl_dtype x_dtype,
+                                      void *Y, cogdl_dtype y_dtype, const float *bias,
+                                      cogdl_act act, const cogdl_plan *plan, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Dense layer of the GCN and GAT models that the sparse operators of section
  * 2.2 serve (the feature transform of every layer; the paper's end-to-end

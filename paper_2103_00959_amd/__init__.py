@@ -71,6 +71,8 @@ def lib():
                               ctypes.c_int, ctypes.c_int, P, ctypes.c_int, P, P, P]
     L.cogdl_gat_aggregate_act.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, P,
                                           ctypes.c_int, P, ctypes.c_int, P, P, ctypes.c_int, P, P]
+    L.cogdl_gat_aggregate_proj.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, ctypes.c_int, P,
+                                           ctypes.c_int, P, ctypes.c_int, P, P]
     L.cogdl_linear.argtypes = [i64, i32, i32, P, P, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P]
     L.cogdl_head_scores.argtypes = [i64, i32, i32, P, ctypes.c_int, P, P, P, P, P]
     L.cogdl_act_codec_size.argtypes = [i64, i32, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -96,7 +98,8 @@ def lib():
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_csr_to_csc_noalloc", "cogdl_sddmm_edge_softmax",
                  "cogdl_gat_aggregate",
-                 "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act", "cogdl_linear",
+                 "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act",
+                 "cogdl_gat_aggregate_proj", "cogdl_linear",
                  "cogdl_head_scores", "cogdl_act_codec_size", "cogdl_act_compress",
                  "cogdl_act_decompress"):
         getattr(L, name).restype = ctypes.c_int
@@ -560,6 +563,34 @@ def gat_aggregate(rowptr, col, s_dst, s_src, X, negative_slope: float = 0.2, alp
     return (out, alpha_out) if return_alpha else out
 
 
+def gat_aggregate_proj(rowptr, col, s_dst, a_src, X, negative_slope: float = 0.2,
+                       plan: Plan | None = None, out_dtype=None, out=None, bias=None, act: str = "none"):
+    """Fused GAT aggregation with the source scores projected from the gathered rows:
+    s_src[j, h] = <X[j, h, :], a_src[h, :]> inside the kernel (cogdl_gat_aggregate_proj).
+    X [n_cols, H, D] with D * itemsize a multiple of 16 bytes; a_src fp32 [H, D]."""
+    import torch
+    if act not in ACT:
+        raise ValueError(f"act must be one of {sorted(ACT)}")
+    n_rows, nnz = _graph(rowptr, col)
+    n_cols, H, D = _dims(X, "X", 3)
+    _scores(s_dst, "s_dst", n_rows, H)
+    _numel(a_src, "a_src", H * D)
+    _numel(out, "out", n_rows * H * D)
+    _numel(bias, "bias", H * D)
+    _plan_matches(plan, n_rows, nnz)
+    _dev(bias, "bias", torch.float32), _dev(a_src, "a_src", torch.float32)
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(X, "X")
+    _dev(s_dst, "s_dst", torch.float32)
+    if out is None:
+        out = torch.empty((n_rows, H, D), dtype=out_dtype or X.dtype, device=X.device)
+    _dev(out, "out")
+    _check(lib().cogdl_gat_aggregate_proj(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(s_dst),
+                                          _ptr(a_src), float(negative_slope), _ptr(X), _dtype_code(X),
+                                          _ptr(out), _dtype_code(out), _ptr(bias), ACT[act],
+                                          _plan_handle(plan), _stream()), "cogdl_gat_aggregate_proj")
+    return out
+
+
 def sddmm_dot(rowptr, col, P, Q, plan: Plan | None = None, out=None):
     """out[k, h] = <P[i, h, :], Q[col[k], h, :]> for every edge k = (i, col[k]):
     the SDDMM of section 2.2 per head.  P is [n_rows, H, D], Q [n_cols, H, D]."""
@@ -657,14 +688,17 @@ def linear(X, W, bias=None, act: str = "none", out_dtype=None, out=None):
 
 
 def head_scores(Z, a_src, a_dst):
-    """s_src[i, h] = <Z[i, h, :], a_src[h]>, s_dst likewise; Z [n, H, D], a_* fp32 [H, D]."""
+    """s_src[i, h] = <Z[i, h, :], a_src[h]>, s_dst likewise; Z [n, H, D], a_* fp32 [H, D].
+    Either vector may be None; its scores are then not computed (returned as None)."""
     import torch
     n, H, D = _dims(Z, "Z", 3)
+    if a_src is None and a_dst is None:
+        raise CogdlError("head_scores needs a_src or a_dst")
     _numel(a_src, "a_src", H * D)
     _numel(a_dst, "a_dst", H * D)
     _dev(Z, "Z"), _dev(a_src, "a_src", torch.float32), _dev(a_dst, "a_dst", torch.float32)
-    s_src = torch.empty((n, H), dtype=torch.float32, device=Z.device)
-    s_dst = torch.empty((n, H), dtype=torch.float32, device=Z.device)
+    s_src = None if a_src is None else torch.empty((n, H), dtype=torch.float32, device=Z.device)
+    s_dst = None if a_dst is None else torch.empty((n, H), dtype=torch.float32, device=Z.device)
     _check(lib().cogdl_head_scores(n, H, D, _ptr(Z), _dtype_code(Z), _ptr(a_src), _ptr(a_dst),
                                    _ptr(s_src), _ptr(s_dst), _stream()), "cogdl_head_scores")
     return s_src, s_dst
@@ -709,6 +743,14 @@ def gcn_forward(rowptr, col, val, X, params, plan: Plan | None = None):
     return Y if C8 == C else Y[:, :C]
 
 
+def _proj_ok(Z):
+    """Whether cogdl_gat_aggregate_proj takes heads of this shape: [n, H, D] with each head a
+    power-of-two number of 16-byte vectors."""
+    per = 16 // Z.element_size()
+    D = Z.shape[2]
+    return D % per == 0 and ((D // per) & (D // per - 1)) == 0 and Z.data_ptr() % 16 == 0
+
+
 def gat_forward(rowptr, col, X, params, negative_slope: float = 0.2, plan: Plan | None = None):
     """2-layer GAT inference: layer 1 with H heads of D (concatenated, ELU), layer 2 with one
     head of C outputs.  params: W1 [H*D, in], a_src1 / a_dst1 [H, D], b1 [H*D], W2 [C, H*D],
@@ -718,9 +760,15 @@ def gat_forward(rowptr, col, X, params, negative_slope: float = 0.2, plan: Plan 
     C, C8, pad = _padded_output_layer(params, ("W2", "b2"), ("a_src2", "a_dst2"))
     n = X.shape[0]
     Z1 = linear(X, params["W1"]).view(n, H, D)
-    s_src, s_dst = head_scores(Z1, params["a_src1"], params["a_dst1"])
-    H1 = gat_aggregate(rowptr, col, s_dst, s_src, Z1, negative_slope, plan=plan, bias=params["b1"],
-                       act="elu")
+    if _proj_ok(Z1):
+        # source scores formed from the rows the aggregation gathers: only s_dst is precomputed
+        _, s_dst = head_scores(Z1, None, params["a_dst1"])
+        H1 = gat_aggregate_proj(rowptr, col, s_dst, params["a_src1"], Z1, negative_slope, plan=plan,
+                                bias=params["b1"], act="elu")
+    else:
+        s_src, s_dst = head_scores(Z1, params["a_src1"], params["a_dst1"])
+        H1 = gat_aggregate(rowptr, col, s_dst, s_src, Z1, negative_slope, plan=plan, bias=params["b1"],
+                           act="elu")
     Z2 = linear(H1.view(n, H * D), pad["W2"]).view(n, 1, C8)
     s_src2, s_dst2 = head_scores(Z2, pad["a_src2"], pad["a_dst2"])
     Y = gat_aggregate(rowptr, col, s_dst2, s_src2, Z2, negative_slope, plan=plan,

@@ -22,7 +22,7 @@ LIB = os.path.join(HERE, "libcogdl_mi355.so")
 # counter-calibration kernels (known traffic), a library of their own
 CALIB_LIB = os.path.join(HERE, "libcogdl_calib.so")
 CALIB_SOURCES = ["calib.hip"]
-SOURCES = ["primitives.hip", "plan.hip", "spmm.hip", "gspmm.hip", "gat.hip", "gat_bwd.hip", "dense.hip", "codec.hip", "csc.hip", "trace.hip"]
+SOURCES = ["primitives.hip", "plan.hip", "spmm.hip", "gspmm.hip", "gat.hip", "gat_proj.hip", "gat_bwd.hip", "dense.hip", "codec.hip", "csc.hip", "trace.hip"]
 
 ARCH = "gfx950"
 FLAGS = [

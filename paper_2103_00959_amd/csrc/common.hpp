@@ -454,6 +454,32 @@ __device__ __forceinline__ void softmax_merge(float &m, float &z, float m2, floa
 
 __device__ __forceinline__ float leaky_relu(float t, float slope) { return t > 0.f ? t : slope * t; }
 
+// An attention weight for storing, alpha = exp(e - m) * rz, with e the fp32
+// score of the edge (as the softmax loops compute it), m the row's maximum of
+// those scores and rz = 1 / z its normalizer.  The fast exponential of the
+// loops evaluates exp on the rounded product (e - m) * log2(e), whose rounding
+// error grows with |e - m|; here e - m and the product are carried as
+// unevaluated pairs (hi, lo) of fp32 values (the two-sum and fma error terms,
+// Knuth / Dekker), so only the hardware exp2 of the high part (v_exp_f32) and
+// the final roundings err:
+//     exp(x_hi + x_lo) = 2^y_hi * (1 + y_lo ln 2 + x_lo),  y = x_hi log2(e).
+// A row's maximal score gives exactly exp(0) = 1 (so a degree-1 row's weight
+// is exactly 1).
+__device__ __forceinline__ float alpha_value(float e, float m, float rz)
+{
+    constexpr float kLog2e = 1.44269502f;        // log2(e) rounded to fp32
+    constexpr float kLog2eLo = 1.92596299e-8f;   // log2(e) - kLog2e
+    constexpr float kLn2 = 0.693147182f;
+    const float x = e - m;
+    const float c = x - e;
+    const float x_lo = (e - (x - c)) + (-m - c);
+    const float y = x * kLog2e;
+    const float y_lo = fmaf(x, kLog2e, -y) + x * kLog2eLo;
+    const float r = __builtin_amdgcn_exp2f(y);
+    const float corr = fmaf(y_lo, kLn2, x_lo);
+    return fmaf(r, corr, r) * rz;
+}
+
 // The epilogue activations of the layer entry points (cogdl_act codes).
 __device__ __forceinline__ float apply_act(float v, int act)
 {

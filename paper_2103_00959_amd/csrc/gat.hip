@@ -85,8 +85,9 @@ __device__ __forceinline__ int4 fetch_soft_unit(const SoftArgs &a, int64_t u, in
 // step and R steps in flight per lane; resident grid, each sub-group striding
 // over the units with the next descriptor prefetched.  Whole rows: alpha
 // written (from the scores kept in registers when the row fits in one pass of
-// R steps, else by a second, batched sweep); neighbour groups: (m, z) per head
-// into gstats.
+// R steps, else by a second, batched sweep over the scores parked in alpha);
+// neighbour groups: (m, z) per head into gstats, scores parked.  Stored
+// weights go through alpha_value.
 template <int R>
 __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
 {
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = beg + slot + r * slots;
-                    if (k < end) a.alpha[(int64_t)k * H + h] = __expf(ev[r] - m) * rz;
+                    if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(ev[r], m, rz);
                 }
             } else {
                 // the parked scores, same lane-to-element map as when they were written
@@ -179,7 +180,7 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
 #pragma unroll
                     for (int r = 0; r < R; ++r) {
                         const int k = k0 + r * slots;
-                        if (k < end) a.alpha[(int64_t)k * H + h] = __expf(e[r] - m) * rz;
+                        if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(e[r], m, rz);
                     }
                 }
             }
@@ -254,7 +255,7 @@ __global__ __launch_bounds__(kBlock) void k_alpha_split(SoftArgs a)
         const int4 d = a.part_units[p];
         const float m = a.rstats[(int64_t)d.w * a.sstride + h];
         const float rz = 1.f / a.rstats[(int64_t)d.w * a.sstride + (a.sstride >> 1) + h];
-        alpha_from_parked<8>(a.alpha, H, h, m, rz, d.y, d.z, slot, eps);
+        alpha_from_parked<8>(a.alpha, 0, a.alpha, H, h, m, rz, d.y, d.z, slot, eps);
     }
 }
 
@@ -354,6 +355,13 @@ cogdl_status check_graph(int32_t n_rows, int32_t n_cols, int64_t nnz, const int3
     return COGDL_OK;
 }
 
+cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                                const int32_t *col, int32_t H, int32_t D, const float *s_dst,
+                                const float *s_src, const float *a_src, float negative_slope,
+                                const float *alpha_in, const void *X, cogdl_dtype x_dtype, void *Y,
+                                cogdl_dtype y_dtype, float *alpha_out, const float *bias,
+                                cogdl_act act, const cogdl_plan *plan, hipStream_t stream);
+
 }  // namespace
 }  // namespace cogdl
 
@@ -440,6 +448,36 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
                                      float *alpha_out, const float *bias, cogdl_act act,
                                      const cogdl_plan *plan, hipStream_t stream)
 {
+    return gat_aggregate_impl(n_rows, n_cols, nnz, rowptr, col, H, D, s_dst, s_src, nullptr,
+                              negative_slope, alpha_in, X, x_dtype, Y, y_dtype, alpha_out, bias, act,
+                              plan, stream);
+}
+
+cogdl_status cogdl_gat_aggregate_proj(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col, int32_t H,
+                                      int32_t D, const float *s_dst, const float *a_src,
+                                      float negative_slope, const void *X, cogdl_dtype x_dtype,
+                                      void *Y, cogdl_dtype y_dtype, const float *bias,
+                                      cogdl_act act, const cogdl_plan *plan, hipStream_t stream)
+{
+    if (!a_src) return COGDL_ERR_INVALID;
+    return gat_aggregate_impl(n_rows, n_cols, nnz, rowptr, col, H, D, s_dst, nullptr, a_src,
+                              negative_slope, nullptr, X, x_dtype, Y, y_dtype, nullptr, bias, act,
+                              plan, stream);
+}
+
+}  // extern "C"
+
+namespace cogdl {
+namespace {
+
+cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                                const int32_t *col, int32_t H, int32_t D, const float *s_dst,
+                                const float *s_src, const float *a_src, float negative_slope,
+                                const float *alpha_in, const void *X, cogdl_dtype x_dtype, void *Y,
+                                cogdl_dtype y_dtype, float *alpha_out, const float *bias,
+                                cogdl_act act, const cogdl_plan *plan, hipStream_t stream)
+{
     if (act < COGDL_ACT_NONE || act > COGDL_ACT_ELU) return COGDL_ERR_INVALID;
     cogdl_status st = check_graph(n_rows, n_cols, nnz, rowptr, col, H);
     if (st != COGDL_OK) return st;
@@ -447,9 +485,11 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype)) return COGDL_ERR_DTYPE;
     const int64_t W = (int64_t)H * D;
     if (W > INT32_MAX) return COGDL_ERR_TOO_LARGE;
+    const bool proj = a_src != nullptr;
     const bool soft = alpha_in == nullptr;
     if (soft && n_rows > 0 && !s_dst) return COGDL_ERR_INVALID;
-    if (soft && nnz > 0 && !s_src) return COGDL_ERR_INVALID;
+    if (soft && !proj && nnz > 0 && !s_src) return COGDL_ERR_INVALID;
+    if (proj && (!soft || alpha_out)) return COGDL_ERR_INVALID;
     if (n_rows > 0 && !Y) return COGDL_ERR_INVALID;
     if (nnz > 0 && !X) return COGDL_ERR_INVALID;
     const Plan *P = plan_of(plan);
@@ -465,6 +505,11 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
         m.slab = m.S * m.ch * m.vec;
         m.n_slabs = (int)((W + m.slab - 1) / m.slab);
     }
+    // projected source scores: each head on L = D / VEC adjacent lanes of one chunk
+    const int hl = D / m.vec;
+    if (proj && (m.vec * dtype_bytes(x_dtype) != 16 || D % m.vec != 0 || (hl & (hl - 1)) != 0 ||
+                 hl > m.S))
+        return COGDL_ERR_INVALID;
     GatArgs a{};
     a.units = P ? P->units : nullptr;
     a.n_rows = n_rows;
@@ -483,6 +528,8 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     a.alpha_out = soft ? alpha_out : nullptr;
     a.bias = bias;
     a.act = act;
+    a.a_src = a_src;
+    a.park_cap = 0;
     a.partials = P ? P->partials : nullptr;
     a.pstride = P ? (P->max_feat + 7) / 8 * 8 : 0;
     a.gstats = P ? P->gstats : nullptr;
@@ -492,28 +539,37 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     const bool buf = a.x_bytes <= kBufferMaxBytes;
     const int64_t units = P ? P->cap_units : n_rows;
     // tiny units (the sorted tail): S/4 lanes and four chunks per lane
-    const bool tiny = P && m.ch == 1 && m.S >= 8 && m.S / 4 >= H;
+    const bool tiny = P && m.ch == 1 && m.S >= 8 && m.S / 4 >= H && (!proj || hl <= m.S / 4);
     if (P) set_units(a, tiny ? long_units(*P) : all_units(*P));
     {
         const int64_t upb = kBlock >> m.log2S;
-        GatKernel k = gat_pick<false>(x_dtype, y_dtype, m.vec, m.ch, buf);
+        GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, m.ch, buf)
+                           : gat_pick<false>(x_dtype, y_dtype, m.vec, m.ch, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
         blocks = list_grid(blocks, a.lists);
-        COGDL_LAUNCH("gat", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, stream, a);
+        // alpha wanted: each sub-group parks whole rows' scores in its share of kParkFloats of LDS
+        const size_t shm = a.alpha_out ? sizeof(float) * kParkFloats : 0;
+        a.park_cap = a.alpha_out ? kParkFloats / (kBlock >> m.log2S) : 0;
+        COGDL_LAUNCH_SHM(proj ? "gat_proj" : "gat", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock,
+                         shm, stream, a);
     }
     if (tiny) {
         GatArgs b = a;
         set_units(b, tiny_units(*P));
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
-        GatKernel k = gat_pick<false>(x_dtype, y_dtype, m.vec, 4, buf);
+        GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, 4, buf)
+                           : gat_pick<false>(x_dtype, y_dtype, m.vec, 4, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
         blocks = list_grid(blocks, b.lists);
-        COGDL_LAUNCH("gat_tiny", k, dim3((unsigned)blocks, (unsigned)m.n_slabs), kBlock, stream, b);
+        const size_t shm = b.alpha_out ? sizeof(float) * kParkFloats : 0;
+        b.park_cap = b.alpha_out ? kParkFloats / (kBlock >> b.log2S) : 0;
+        COGDL_LAUNCH_SHM(proj ? "gat_proj_tiny" : "gat_tiny", k, dim3((unsigned)blocks, (unsigned)m.n_slabs),
+                         kBlock, shm, stream, b);
     }
     if (!P) return COGDL_OK;
 
@@ -550,4 +606,6 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
     return COGDL_OK;
 }
 
-}  // extern "C"
+}  // namespace
+}  // namespace cogdl
+

@@ -38,6 +38,8 @@ struct GatArgs {
     float *ds_out;              // BWD: those sums, n_rows x H (split rows: gstats)
     const float *bias;          // epilogue: Y = act(aggregate + bias), bias nullable
     int32_t act;
+    const float *a_src;         // PROJ: the source score is X[j, h, :] . a_src[h, :] (H x D fp32)
+    int32_t park_cap;           // alpha wanted: LDS floats per sub-group for parked scores (0: none)
     int32_t sstride;            // 2 * max_heads
     int32_t slab;
     int32_t log2S;
@@ -53,12 +55,14 @@ __device__ __forceinline__ int4 fetch_gat_unit(const GatArgs &a, int64_t u, int6
     return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
 }
 
-// alpha[k, h] = exp(e_kh - m) * rz for the edges k = beg + slot + j * slots of
-// one head h, R loads in flight per lane; the raw scores e_kh are read from
-// alpha itself, where the aggregation or the softmax parked them (a contiguous
-// re-read instead of a second random gather of s_src).
+// alpha[k, h] = alpha_value(e_kh, m, rz) for the edges k = beg + slot + j * slots
+// of one head h, R loads in flight per lane; the raw scores e_kh are read from
+// `parked` at index (k - base) * H + h, where the aggregation or the softmax
+// parked them: alpha itself (base 0; a contiguous re-read instead of a second
+// random gather of s_src) or a row buffer in LDS (base = beg).
 template <int R>
-__device__ __forceinline__ void alpha_from_parked(float *__restrict__ alpha, int H, int h, float m,
+__device__ __forceinline__ void alpha_from_parked(const float *parked, int64_t base,
+                                                  float *__restrict__ alpha, int H, int h, float m,
                                                   float rz, int beg, int end, int slot, int slots)
 {
     for (int k0 = beg + slot; k0 < end; k0 += R * slots) {
@@ -66,23 +70,30 @@ __device__ __forceinline__ void alpha_from_parked(float *__restrict__ alpha, int
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int k = k0 + r * slots;
-            e[r] = k < end ? alpha[(int64_t)k * H + h] : 0.f;
+            e[r] = k < end ? parked[(k - base) * H + h] : 0.f;
         }
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int k = k0 + r * slots;
-            if (k < end) alpha[(int64_t)k * H + h] = __expf(e[r] - m) * rz;
+            if (k < end) alpha[(int64_t)k * H + h] = alpha_value(e[r], m, rz);
         }
     }
 }
 
-// BWD = true: the backward pass of the aggregation, run on the CSC of the
-// graph (rows of this launch = source nodes): the weights are the forward
-// alpha through perm, and each row also sums dscore (through perm) per head.
-// The one-chunk forward variants are held to 128 VGPRs (4 wavefronts per SIMD,
-// the occupancy their loop reaches without the bound), so that parking alpha
-// does not cost a wavefront of latency hiding.
-template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD>
+// Scores of a whole-row unit parked in LDS when alpha is wanted: each sub-group
+// of a k_gat workgroup owns kParkFloats / (sub-groups per workgroup) floats of
+// the dynamic LDS, enough for rows of that many / H edges; longer rows and
+// neighbour groups of split rows park in alpha.
+constexpr int kParkFloats = 8192;   // 32 KB per workgroup
+
+// PROJ = true: the source score of each edge is formed from the gathered
+// feature row itself, s = X[j, h, :] . a_src[h, :] (each lane's VEC products,
+// then a butterfly over the L = D / VEC adjacent lanes of the head, which
+// leaves every lane of the head with the same bits), instead of being gathered
+// from s_src: a GAT layer's source score is that projection, and the random
+// 4H-byte score row of each edge costs a whole cache line.  Needs 16-byte
+// vectors, L a power of two and each head inside one chunk (the host checks).
+template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD, bool PROJ = false>
 __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k_gat(GatArgs a)
 {
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
@@ -112,8 +123,22 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
     const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ wsrc = soft ? a.s_src : a.alpha_in;
+    // PROJ: this lane's VEC entries of a_src, and the lanes per head
+    float asrc[PROJ ? CH : 1][PROJ ? VEC : 1];
+    const int hl = PROJ ? a.D / VEC : 1;
+    if constexpr (PROJ) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) asrc[c][e] = act[c] ? a.a_src[fe[c] + e] : 0.f;
+    }
     // (edge slot, head) lane layout of the alpha sweep: eps edges per step
     const int eps = S / H;
+    extern __shared__ float park_buf[];
+    // whole-row units whose scores fit this sub-group's LDS buffer park there
+    // (computed where used: both stay out of the registers of the main loop)
+#define COGDL_PARK_LDS (a.park_cap > 0 && part < 0 && (end - beg) * H <= a.park_cap)
+#define COGDL_LDS_PARK (park_buf + (threadIdx.x >> log2S) * a.park_cap)
     const int q_slot = lig / H, q_head = lig % H;
 
     // Resident grid, software-pipelined over units as in the SpMM kernel.
@@ -170,13 +195,24 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         const int64_t wi = BWD ? (int64_t)pk[t] * H + hd[c]
                                          : soft ? (int64_t)cc[t] * H + hd[c]
                                                 : (int64_t)(k0 + j + t) * H + hd[c];
-                        w[t][c] = wsrc[on ? wi : 0];
+                        if constexpr (!PROJ) w[t][c] = wsrc[on ? wi : 0];
                         if constexpr (BWD) {
                             const float g = a.dscore[on ? wi : 0];
                             dsum[c] += on ? g : 0.f;
                         }
                         X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
                     }
+                if constexpr (PROJ) {
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) {
+                            float p = 0.f;
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) p = fmaf(xv[t][c][e], asrc[c][e], p);
+                            w[t][c] = group_sum(p, hl);
+                        }
+                }
                 if (soft) {
 #pragma unroll
                     for (int c = 0; c < CH; ++c) {
@@ -188,10 +224,16 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         }
                         // alpha wanted: park the raw scores, one lane per head and edge
                         // (the lane of the head's first feature in this slab)
-                        if (a.alpha_out != nullptr && act[c] && fe[c] % a.D == 0) {
+                        if constexpr (!PROJ) {
+                            if (a.alpha_out != nullptr && act[c] && fe[c] % a.D == 0) {
 #pragma unroll
-                            for (int t = 0; t < U; ++t)
-                                if (ok[t]) a.alpha_out[(int64_t)(k0 + j + t) * H + hd[c]] = w[t][c];
+                                for (int t = 0; t < U; ++t) {
+                                    if (!ok[t]) continue;
+                                    const int k = k0 + j + t;
+                                    if (COGDL_PARK_LDS) COGDL_LDS_PARK[(k - beg) * H + hd[c]] = w[t][c];
+                                    else a.alpha_out[(int64_t)k * H + hd[c]] = w[t][c];
+                                }
+                            }
                         }
                         if (mb > m[c]) {
                             const float r = __expf(m[c] - mb);
@@ -265,7 +307,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                     store_out<TY, VEC>(static_cast<TY *>(a.Y), (int64_t)row * a.W + fe[c], v);
                 }
             }
-            if (soft && a.alpha_out != nullptr) {
+            if (!PROJ && soft && a.alpha_out != nullptr) {   // (the PROJ entry writes no alpha)
                 // alpha of this whole-row unit: lanes as (edge slot, head); the
                 // (m, z) of head h comes from the lane holding the first feature
                 // of h in this slab.
@@ -286,8 +328,11 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                 // those stores before reading them back
                 __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-                if (mine_head && slot < eps)
-                    alpha_from_parked<4>(a.alpha_out, H, h1, m1, r1, beg, end, slot, eps);
+                if (mine_head && slot < eps) {
+                    if (COGDL_PARK_LDS)
+                        alpha_from_parked<4>(COGDL_LDS_PARK, beg, a.alpha_out, H, h1, m1, r1, beg, end, slot, eps);
+                    else alpha_from_parked<4>(a.alpha_out, 0, a.alpha_out, H, h1, m1, r1, beg, end, slot, eps);
+                }
             }
         }
         if (un >= hi) break;
@@ -297,6 +342,9 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
         p_cur = p_first_next;
     }
 }
+
+#undef COGDL_PARK_LDS
+#undef COGDL_LDS_PARK
 
 using GatKernel = void (*)(GatArgs);
 
@@ -334,4 +382,8 @@ GatKernel gat_pick(int xdt, int ydt, int vec, int ch, bool buf)
     if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, false, BWD>(ydt, vec, ch);
     return gat_pick_y<f16_t, false, BWD>(ydt, vec, ch);
 }
+
+// The PROJ forward kernels (16-byte vectors only), instantiated in gat_proj.hip.
+GatKernel gat_pick_proj(int xdt, int ydt, int ch, bool buf);
+
 }  // namespace cogdl

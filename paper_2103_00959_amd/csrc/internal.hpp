@@ -234,6 +234,16 @@ RowMap row_map(int64_t width, int elem_bytes, int unit_elems /* vec must divide 
         if (_e != hipSuccess) return COGDL_ERR_LAUNCH;               \
     } while (0)
 
+// The same with `shm` bytes of dynamic LDS per workgroup.
+#define COGDL_LAUNCH_SHM(name, kern, grid, block, shm, stream, ...)   \
+    do {                                                             \
+        const int _slot = ::cogdl::trace_begin(name, stream);        \
+        kern<<<(grid), (block), (shm), (stream)>>>(__VA_ARGS__);     \
+        const hipError_t _e = hipGetLastError();                     \
+        ::cogdl::trace_end(_slot, stream);                           \
+        if (_e != hipSuccess) return COGDL_ERR_LAUNCH;               \
+    } while (0)
+
 // Same for functions returning hipError_t.
 #define COGDL_LAUNCH_HIP(name, kern, grid, block, stream, ...)        \
     do {                                                             \

@@ -424,11 +424,36 @@ def _scores(n_rows, n_cols, H, seed, scale=1.0):
     return sd, ss
 
 
-def _alpha_close(a_gpu, a_ref):
+FLT_MIN = float(np.finfo(np.float32).tiny)
+
+
+def _alpha_close(a_gpu, a_ref, scale=None):
+    """Relative error over every weight whose reference is a normal fp32 value, divided by
+    `scale` (per weight, default 1): the result must be <= TOL_ALPHA.  Below FLT_MIN (weights
+    that underflow in fp32) the absolute error must stay under FLT_MIN."""
     a = to_f64(a_gpu).reshape(a_ref.shape)
     if a_ref.size == 0:
         return 0.0
-    return float(np.max(np.abs(a - a_ref) / a_ref))
+    normal = a_ref >= FLT_MIN
+    assert np.all(np.abs(a[~normal] - a_ref[~normal]) <= FLT_MIN)
+    rel = np.abs(a - a_ref) / np.where(normal, a_ref, 1.0)
+    if scale is not None:
+        rel = rel / scale
+    return float(np.max(rel[normal])) if normal.any() else 0.0
+
+
+def _alpha_bound_scale(g, sd, ss, slope=0.2):
+    """The alpha tolerance of the score rounding, as a factor on TOL_ALPHA per weight:
+    (1e-5 + 2^-23 max_{k' in row} |e_k'|) / 1e-5.  The kernels score an edge in fp32
+    (e = LeakyReLU(s_dst + s_src) rounded once), which moves each weight by at most
+    2^-24 (|e_k| + max |e_k'|) relative; the exponential itself is evaluated to a few units
+    in the last place.  Scores from the fp64 inputs, per head."""
+    rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
+    t = sd[rows].astype(np.float64) + ss[g.col].astype(np.float64)
+    e = np.where(t > 0, t, slope * t)
+    emax = np.zeros((g.n_rows, sd.shape[1]))
+    np.maximum.at(emax, rows, np.abs(e))
+    return (TOL_ALPHA + 2.0 ** -23 * emax[rows]) / TOL_ALPHA
 
 
 @pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1"])
@@ -465,9 +490,46 @@ def test_softmax_degree_one_rows_exact_and_wide_scores(cg):
     np.add.at(sums, rows, a_h.astype(np.float64))
     assert np.max(np.abs(sums[d > 0] - 1.0)) <= 1e-5
     a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
-    # with wide score ranges the tiny weights carry the exp argument's rounding
-    rel = np.abs(a_h - a_ref) / a_ref
-    assert np.max(rel[a_ref > 1e-6]) <= TOL_ALPHA
+    assert _alpha_close(a, a_ref, _alpha_bound_scale(g, sd, ss)) <= TOL_ALPHA
+
+
+@pytest.mark.parametrize("scale", [8.0, 24.0])
+def test_alpha_wide_scores_every_plan(cg, scale):
+    """Scores N(0, scale^2): |e - m| reaches the range where the weights approach FLT_MIN
+    (scale 24), so the exponent's conditioning is exercised; every weight whose reference is a
+    normal fp32 value is compared at 1e-5 plus the rounding of its fp32 score (see
+    _alpha_bound_scale), for the standalone softmax and the fused aggregation's alpha, with
+    plain, neighbour-group and column-sliced plans (sliced and split rows take the separate
+    rescoring pass)."""
+    g = _graph("hubs", seed=9)
+    rp, cl, _ = graph_to_dev(g)
+    H, D = 4, 8
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 79, scale=scale)
+    a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+    bound = _alpha_bound_scale(g, sd, ss)
+    say(f"wide scores x{scale}: smallest normal reference weight {a_ref[a_ref >= FLT_MIN].min():.3e}, "
+        f"{int((a_ref < FLT_MIN).sum())} below FLT_MIN, bound up to {bound.max() * TOL_ALPHA:.2e}")
+    _, _, xd = features((g.n_cols, H, D), 61, "f32")
+    specs = [None, ("auto", 0, False), ("neighbor_group", 5, False), ("neighbor_group", 64, True),
+             ("neighbor_group", 7, True)]
+    for spec in specs:
+        if spec is None:
+            plan = None
+        else:
+            mode, G, sliced = spec
+            plan = cg.Plan(rp, g.nnz, max_feat=H * D, max_heads=H, mode=mode, group_size=G,
+                           **(dict(col=cl, n_cols=g.n_cols, slice_min=16) if sliced else {}))
+        try:
+            a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
+            err = _alpha_close(a, a_ref, bound)
+            assert err <= TOL_ALPHA, (scale, spec, err)
+            _, a2 = cg.gat_aggregate(rp, cl, dev(sd), dev(ss), xd, 0.2, plan=plan, return_alpha=True)
+            err2 = _alpha_close(a2, a_ref, bound)
+            assert err2 <= TOL_ALPHA, (scale, spec, err2)
+            say(f"  plan {spec}: softmax {err:.2e}, gat alpha {err2:.2e}")
+        finally:
+            if plan is not None:
+                plan.close()
 
 
 @pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
@@ -660,3 +722,65 @@ def test_plan_rebuild_past_capacity_is_refused(cg):
         plan.close()
     Yr, Ar = oracle.spmm(g.rowptr, g.col, g.val, X_host)
     assert scaled_error(Y, Yr, Ar) <= TOL_F32
+
+
+@pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
+@pytest.mark.parametrize("H,D,xk,yk", [(4, 64, "bf16", "bf16"), (8, 16, "f32", "f32"), (2, 32, "f16", "f32"),
+                                       (1, 8, "f32", "f32"), (4, 32, "bf16", "f32"), (16, 8, "bf16", "bf16")])
+def test_gat_aggregate_proj(cg, kind, H, D, xk, yk):
+    """Source scores projected from the gathered rows against the oracle model: the oracle's
+    head scores (fp64) feed its fused aggregation.  Bar: the aggregation's tolerance plus the
+    score's own rounding, 2 (D 2^-24 max_j sum_d |X_jd a_hd| + 2^-24 max |s|) (a score moved by
+    ds moves each output by at most 2 ds times its error scale)."""
+    import torch
+    g = _graph(kind)
+    say(f"gat proj {kind} H={H} D={D} {xk}->{yk}")
+    rp, cl, _ = graph_to_dev(g)
+    sd, _ = _scores(g.n_rows, g.n_cols, H, 52 + H)
+    rng = np.random.default_rng(53 + D)
+    a_src = (rng.standard_normal((H, D)) / np.sqrt(D)).astype(np.float32)
+    xh, xc, xd = features((g.n_cols, H, D), 62 + D, xk)
+    ss_ref, _, ss_abs, _ = oracle.head_scores(xh.reshape(g.n_cols, H * D), a_src, a_src, H, D, z_dtype=xc)
+    Yr, Ar = oracle.gat(g.rowptr, g.col, sd, ss_ref.astype(np.float32), xh.reshape(g.n_cols, H * D), H, D,
+                        slope=0.2, x_dtype=xc)
+    u = 2.0 ** -24
+    score_term = 2 * (D * u * float(ss_abs.max(initial=0.0)) + u * float(np.abs(ss_ref).max(initial=0.0)))
+    out_dtype = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[yk]
+    for spec in (None, ("auto", 0), ("neighbor_group", 6), "sliced"):
+        if spec == "sliced":
+            plan = cg.Plan(rp, g.nnz, max_feat=H * D, max_heads=H, mode="neighbor_group", group_size=9,
+                           col=cl, n_cols=g.n_cols, slice_min=16)
+        else:
+            plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+        try:
+            Y = cg.gat_aggregate_proj(rp, cl, dev(sd), dev(a_src), xd, 0.2, plan=plan, out_dtype=out_dtype)
+            err = scaled_error(Y.reshape(g.n_rows, H * D), Yr, Ar)
+            assert err <= tol_for(xk, yk) + score_term, (kind, H, D, spec, err, score_term)
+            # deterministic
+            assert torch.equal(cg.gat_aggregate_proj(rp, cl, dev(sd), dev(a_src), xd, 0.2, plan=plan,
+                                                     out_dtype=out_dtype), Y)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+def test_gat_aggregate_proj_shapes_refused(cg):
+    """Heads that are not whole 16-byte vectors in a power-of-two lane count are refused before any
+    launch, as is a missing a_src."""
+    g = _graph("small")
+    rp, cl, _ = graph_to_dev(g)
+    for H, D, xk in ((2, 5, "f32"), (3, 12, "f32"), (1, 48, "bf16"), (2, 4, "bf16")):
+        sd, _ = _scores(g.n_rows, g.n_cols, H, 3)
+        _, _, xd = features((g.n_cols, H, D), 4, xk)
+        a_src = dev(np.ones((H, D), np.float32))
+        with pytest.raises(cg.CogdlError, match="invalid argument"):
+            cg.gat_aggregate_proj(rp, cl, dev(sd), a_src, xd)
+    L = cg.lib()
+    H, D = 4, 16
+    sd, _ = _scores(g.n_rows, g.n_cols, H, 3)
+    _, _, xd = features((g.n_cols, H, D), 4, "f32")
+    import torch
+    Y = torch.empty((g.n_rows, H, D), dtype=torch.float32, device="cuda")
+    st = L.cogdl_gat_aggregate_proj(g.n_rows, g.n_cols, g.nnz, cg._ptr(rp), cg._ptr(cl), H, D, cg._ptr(dev(sd)),
+                                    None, 0.2, cg._ptr(xd), 0, cg._ptr(Y), 0, None, 0, None, cg._stream())
+    assert st == 1
