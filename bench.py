@@ -59,6 +59,12 @@ def parse():
     ap.add_argument("--counter-probe", metavar="JSON", default=None,
                     help="run one warmup step, one step and the calibration kernels between marker "
                          "kernels (for rocprofv3 --pmc), write the step's library launch names to JSON")
+    ap.add_argument("--workloads-probe", metavar="JSON", default=None,
+                    help="run each workloads-mode op once, cold, between marker kernels (for rocprofv3 "
+                         "--pmc) and write the ops' keys to JSON")
+    ap.add_argument("--wl-reps", type=int, default=5, help="timed calls per workload op in the default run")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the per-workload operator lines (workloads 1-4) of the default run")
     ap.add_argument("--no-live-counters", action="store_true",
                     help="do not run the counter probe under rocprofv3; take the HBM bytes from the "
                          "committed record under profiles/ when it matches the sources")
@@ -267,36 +273,11 @@ def probe_command(args, out_json: str):
 def live_counters(args, timeout_s: float = 300.0):
     """Run the counter probe under rocprofv3 (a FETCH_SIZE pass, then a WRITE_SIZE pass) as
     child processes and summarize it; (summary, None) or (None, reason)."""
-    import shutil
-    import signal
-    import subprocess
     import tempfile
-    exe = shutil.which("rocprofv3") or "/opt/rocm/bin/rocprofv3"
-    if not os.path.exists(exe):
-        return None, "rocprofv3 not found"
-    base = tempfile.mkdtemp(prefix="cogdl_counters_", dir="/tmp")
-    out_json = os.path.join(base, "probe.json")
-    env = dict(os.environ, TMPDIR="/tmp")
-    dirs = {}
-    for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
-        d = os.path.join(base, tag)
-        cmd = [exe, "--pmc", ctr, "--kernel-trace", "-d", d, "-o", "run", "--output-format", "csv", "--"]
-        cmd += probe_command(args, out_json)
-        log(f"counters: {ctr} pass")
-        with open(os.path.join(base, f"{tag}.log"), "w") as lf:
-            p = subprocess.Popen(cmd, cwd="/tmp", env=env, stdout=lf, stderr=subprocess.STDOUT,
-                                 start_new_session=True)
-            try:
-                rc = p.wait(timeout=timeout_s)
-            except subprocess.TimeoutExpired:
-                os.killpg(p.pid, signal.SIGKILL)
-                p.wait()
-                return None, f"{ctr} pass timed out after {timeout_s:.0f} s"
-        # rocprofv3 may end with a segmentation fault after the program finished and
-        # its results are complete: the probe's own output file says whether it did
-        if rc != 0 and not os.path.exists(out_json):
-            return None, f"{ctr} pass exited with {rc}"
-        dirs[tag] = d
+    out_json = os.path.join(tempfile.mkdtemp(prefix="cogdl_probe_", dir="/tmp"), "probe.json")
+    dirs, why = run_probe_passes(probe_command(args, out_json)[2:], out_json, timeout_s)
+    if dirs is None:
+        return None, why
     try:
         probe = json.load(open(out_json))
         summary = summarize_probe(dirs["fetch"], dirs["write"], probe["launches"])
@@ -453,7 +434,7 @@ def oracle_rate(run, units, budget_s, chunk=256, full=False):
     return dict(seconds=t, bytes=b_tot, edges=e_tot, units=done)
 
 
-def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
+def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0, hbm=None, probe=None, emit=None):
     """Each workload's operators in its own configuration (fp32 features; column-sliced plans
     on AUTO with the default group size), one JSON line per (workload, op).  Cold: a 1 GiB buffer is
     written before every timed call, so L2 and the Infinity Cache hold none of its inputs;
@@ -463,7 +444,13 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
     the 256 MB Infinity Cache, a 1 GiB copy's rate (the achievable ceiling), the HBM bytes
     of one cold call from the committed rocprofv3 counters of this mode (when the library
     sources are unchanged since), and the fp64 CPU oracle's rate on the same op (all host
-    threads; also one thread for workloads 1 and 2, whose ops the oracle does whole)."""
+    threads; also one thread for workloads 1 and 2, whose ops the oracle does whole).
+
+    hbm: {"<workload>/<op>": {fetch_bytes, write_bytes}} measured in this run (else the
+    committed record is used).  probe: a path; instead of timing, every op runs once, cold
+    (after the 1 GiB flush), between two marker kernels, and the ops' keys go to that JSON
+    file (run under rocprofv3 for the counters).  emit: called with each record (default:
+    print it as a JSON line).  Returns the records."""
     import torch
 
     import paper_2103_00959_amd as cg
@@ -488,13 +475,27 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
     copy_GBps = 2 * (1 << 30) / (float(np.median(cp_ms[1:])) * 1e-3) / 1e9
     del cp_dst
     log(f"1 GiB copy: {copy_GBps:.0f} GB/s")
-    hbm = recorded_workload_traffic()
+    hbm_source = "live" if hbm is not None else "profiles/workloads_1_to_4_hbm_traffic.json"
+    if hbm is None:
+        hbm = recorded_workload_traffic()
+    records, probe_keys = [], []
+    if emit is None:
+        emit = lambda r: print(json.dumps(r), flush=True)          # noqa: E731
     threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     cpu_name = cpu_model()
     if cpu:
         import oracle
 
     def times(fn):
+        if probe:
+            fn()                             # warm (plans, caches of first use)
+            flush.fill_(1)
+            torch.cuda.synchronize()
+            marker.bitwise_not_()
+            fn()
+            marker.bitwise_not_()
+            torch.cuda.synchronize()
+            return None
         # the first untimed call is traced to count the library launches of one call
         marker.bitwise_not_()
         cg.trace_enable(256)
@@ -545,6 +546,9 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
         return out
 
     def record(k, cfg, op, B, B_u, E, flop, table_bytes, res, cpu_rec):
+        if probe:
+            probe_keys.append(f"{cfg['name']}/{op}")
+            return
         cold, warm, launches = res
         mc, mw = float(np.median(cold)), float(np.median(warm))
         out = {"workload": cfg["name"], "config": k, "op": op, "algorithmic_GB": B / 1e9,
@@ -558,13 +562,16 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
                "cold_GFLOPps": flop / (mc * 1e-3) / 1e9 if flop else None,
                "cache_resident": (table_bytes <= (256 << 20)) if table_bytes else None,
                "copy_GBps": copy_GBps, "launches_per_call": launches, "plans": "column-sliced",
-               "hbm_GBps": None, "l2_hit": None, "cpu_oracle": cpu_rec}
+               "hbm_GBps": None, "l2_hit": None, "hbm_source": None, "cpu_oracle": cpu_rec}
         h = hbm.get(f"{cfg['name']}/{op}") if hbm else None
         if h:
             out["hbm_GB"] = (h["fetch_bytes"] + h["write_bytes"]) / 1e9
             out["hbm_GBps"] = (h["fetch_bytes"] + h["write_bytes"]) / (mc * 1e-3) / 1e9
+            out["hbm_frac"] = out["hbm_GBps"] / HBM_PEAK_GBPS
             out["l2_hit"] = h.get("l2_hit")
-        print(json.dumps(out), flush=True)
+            out["hbm_source"] = hbm_source
+        records.append(out)
+        emit(out)
         log(f"{cfg['name']} {op}: cold {mc:.3f} ms ({out['cold_pct_peak'] * 100:.1f}% of peak), "
             f"warm {mw:.3f} ms" + (f", oracle {cpu_rec['GBps']:.2f} GB/s" if cpu_rec else ""))
 
@@ -663,6 +670,91 @@ def run_workloads(reps=20, warm_reps=3, cpu=True, cpu_budget_s=2.0):
         plan.close()
         del rowptr, col, val
         torch.cuda.empty_cache()
+    if probe:
+        # the copy of known size that scales the counters, as its own section
+        import ctypes
+        C = calib_lib()
+        dst = torch.empty_like(flush)
+        torch.cuda.synchronize()
+        marker.bitwise_not_()
+        rc = C.cogdl_calib_copy(ctypes.c_void_p(flush.data_ptr()), ctypes.c_void_p(dst.data_ptr()), CALIB_BYTES,
+                                cg._stream())
+        marker.bitwise_not_()
+        torch.cuda.synchronize()
+        if rc:
+            raise SystemExit("calibration copy refused its arguments")
+        probe_keys.append("calib_copy")
+        with open(probe, "w") as f:
+            json.dump({"keys": probe_keys}, f)
+        log(f"workloads probe done: {len(probe_keys)} sections")
+    return records
+
+
+def summarize_workloads_probe(fetch_dir: str, write_dir: str, keys: list):
+    """{"<workload>/<op>": {fetch_bytes, write_bytes}} of one cold call of each op of a
+    --workloads-probe run: the dispatches between each pair of markers, scaled by what the
+    counters read for the closing 1 GiB copy."""
+    out = {}
+    for counter, d, field in (("FETCH_SIZE", fetch_dir, "fetch_bytes"), ("WRITE_SIZE", write_dir, "write_bytes")):
+        disp = read_dispatches(d, counter)
+        marks = [i for i, (n, _) in enumerate(disp) if MARKER in n]
+        if len(marks) != 2 * len(keys):
+            raise RuntimeError(f"expected {2 * len(keys)} marker dispatches, found {len(marks)}")
+        sums = [sum(v for _, v in disp[marks[2 * i] + 1:marks[2 * i + 1]]) * 1024.0 for i in range(len(keys))]
+        scale = CALIB_BYTES / sums[keys.index("calib_copy")]
+        for key, b in zip(keys, sums):
+            out.setdefault(key, {})[field] = b * scale
+            out[key][field.replace("bytes", "scale")] = scale
+    out.pop("calib_copy")
+    return out
+
+
+def run_probe_passes(probe_args: list, out_json: str, timeout_s: float = 300.0):
+    """Run `bench.py <probe_args>` under rocprofv3, one FETCH_SIZE and one WRITE_SIZE pass,
+    as child processes; ({"fetch": dir, "write": dir}, None) or (None, reason)."""
+    import shutil
+    import signal
+    import subprocess
+    import tempfile
+    exe = shutil.which("rocprofv3") or "/opt/rocm/bin/rocprofv3"
+    if not os.path.exists(exe):
+        return None, "rocprofv3 not found"
+    base = tempfile.mkdtemp(prefix="cogdl_counters_", dir="/tmp")
+    env = dict(os.environ, TMPDIR="/tmp")
+    dirs = {}
+    for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        d = os.path.join(base, tag)
+        cmd = [exe, "--pmc", ctr, "--kernel-trace", "-d", d, "-o", "run", "--output-format", "csv", "--",
+               sys.executable, os.path.abspath(__file__)] + probe_args
+        log(f"counters: {ctr} pass of {' '.join(probe_args[:1])}")
+        with open(os.path.join(base, f"{tag}.log"), "w") as lf:
+            p = subprocess.Popen(cmd, cwd="/tmp", env=env, stdout=lf, stderr=subprocess.STDOUT,
+                                 start_new_session=True)
+            try:
+                rc = p.wait(timeout=timeout_s)
+            except subprocess.TimeoutExpired:
+                os.killpg(p.pid, signal.SIGKILL)
+                p.wait()
+                return None, f"{ctr} pass timed out after {timeout_s:.0f} s"
+        # rocprofv3 may end with a segmentation fault after the program finished and
+        # its results are complete: the probe's own output file says whether it did
+        if rc != 0 and not os.path.exists(out_json):
+            return None, f"{ctr} pass exited with {rc}"
+        dirs[tag] = d
+    return dirs, None
+
+
+def live_workload_counters(args, timeout_s: float = 300.0):
+    """Counter bytes of one cold call of every workloads-mode op, measured in this run."""
+    import tempfile
+    out_json = os.path.join(tempfile.mkdtemp(prefix="cogdl_wlprobe_", dir="/tmp"), "probe.json")
+    dirs, why = run_probe_passes(["--workloads-probe", out_json], out_json, timeout_s)
+    if dirs is None:
+        return None, why
+    try:
+        return summarize_workloads_probe(dirs["fetch"], dirs["write"], json.load(open(out_json))["keys"]), None
+    except Exception as e:       # noqa: BLE001  (a measurement aid: report, never fail the bench)
+        return None, f"workload counter summary failed: {e}"
 
 
 def counter_probe(args, cg, step, dev):
@@ -795,8 +887,16 @@ def main():
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path has no "
               f"multi-GPU mode in this build", file=sys.stderr)
         sys.exit(2)
+    if args.workloads_probe:
+        run_workloads(reps=1, warm_reps=1, cpu=False, probe=args.workloads_probe, emit=lambda r: None)
+        return
     if args.workloads:
-        run_workloads(reps=args.reps, warm_reps=args.warm_reps, cpu=not args.no_cpu_baseline)
+        wl_hbm = None
+        if not args.no_live_counters:
+            wl_hbm, why = live_workload_counters(args)
+            if wl_hbm is None:
+                log(f"live workload counters unavailable ({why})")
+        run_workloads(reps=args.reps, warm_reps=args.warm_reps, cpu=not args.no_cpu_baseline, hbm=wl_hbm)
         return
     if args.summarize_counters:
         if len(args.summarize_counters) not in (3, 4):
@@ -1265,6 +1365,19 @@ def main():
         log(f"CPU baseline {out['cpu_baseline']['value']:.2f} GB/s on {out['cpu_baseline']['cores']} threads")
     plan.close()
     plan_t.close()
+    if not args.no_workloads:
+        # The other workloads' own operators (workloads 1-4 in their own dtypes and plans),
+        # each with its time, rates, HBM bytes from counters and the CPU oracle's rate.
+        wl_hbm, why = (None, "--no-live-counters") if args.no_live_counters else live_workload_counters(args)
+        if wl_hbm is None:
+            log(f"live workload counters unavailable ({why}); falling back on the committed record")
+        out["workloads"] = run_workloads(reps=args.wl_reps, warm_reps=2, cpu=not args.no_cpu_baseline,
+                                         cpu_budget_s=1.0, hbm=wl_hbm, emit=lambda r: None)
+        out["workloads_note"] = ("workloads 1-4 (cold: a 1 GiB buffer written before each call; warm: back to "
+                                 "back), median and minimum of wl_reps calls; hbm_* from the counters of one cold "
+                                 "call (hbm_source); cpu_oracle: the fp64 oracle on all host threads (and one thread "
+                                 "for workloads 1-2); cache_resident: the gathered table fits the 256 MB Infinity "
+                                 "Cache, so algorithmic rates can exceed the HBM peak there")
     print(json.dumps(out), flush=True)
 
 

@@ -543,7 +543,9 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
     if (P) set_units(a, tiny ? long_units(*P) : all_units(*P));
     {
         const int64_t upb = kBlock >> m.log2S;
-        GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, m.ch, buf)
+        // one chunk with 8 lanes per head: the distributed-softmax kernel (batches of 8 edges)
+        const bool dist = m.ch == 1 && hl == 8;
+        GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, m.ch, buf, dist)
                            : gat_pick<false>(x_dtype, y_dtype, m.vec, m.ch, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
@@ -560,7 +562,7 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
         set_units(b, tiny_units(*P));
         b.log2S = m.log2S - 2;
         const int64_t upb = kBlock >> b.log2S;
-        GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, 4, buf)
+        GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, 4, buf, false)
                            : gat_pick<false>(x_dtype, y_dtype, m.vec, 4, buf);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);

@@ -86,16 +86,61 @@ __device__ __forceinline__ void alpha_from_parked(const float *parked, int64_t b
 // neighbour groups of split rows park in alpha.
 constexpr int kParkFloats = 8192;   // 32 KB per workgroup
 
-// PROJ = true: the source score of each edge is formed from the gathered
+// Sum over the 8 lanes of an aligned group of each lane's v[t], scattered:
+// lane hp (its position in the group) ends with the full sum of v[hp].  Three
+// exchange levels (lane ^ 1, ^ 2 by DPP, ^ 4 by a swizzle), each lane keeping
+// the half of its values whose index bit matches its own position bit.
+__device__ __forceinline__ float reduce_scatter8(const float (&v)[8], int hp)
+{
+    const bool b0 = hp & 1, b1 = hp & 2, b2 = hp & 4;
+    float k4[4], k2[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float keep = b0 ? v[2 * i + 1] : v[2 * i];
+        const float send = b0 ? v[2 * i] : v[2 * i + 1];
+        k4[i] = keep + bfly_partner<1>(send);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float keep = b1 ? k4[2 * i + 1] : k4[2 * i];
+        const float send = b1 ? k4[2 * i] : k4[2 * i + 1];
+        k2[i] = keep + bfly_partner<2>(send);
+    }
+    const float keep = b2 ? k2[1] : k2[0];
+    const float send = b2 ? k2[0] : k2[1];
+    // lane ^ 4 inside each 32-lane half: swizzle bit mode, and 0x1f, or 0, xor 4
+    return keep + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(send), 0x101F));
+}
+
+// The value of lane T of this lane's aligned group of 8 (swizzle bit mode:
+// and 0x18 keeps the group, or T picks the lane).
+template <int T>
+__device__ __forceinline__ float from_group8(float v)
+{
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x18 | (T << 5)));
+}
+
+// PM (source-score mode): 0 reads s_src (or the given weights); 1 and 2 form
+// it from the gathered row.
+// PM = 1: the source score of each edge is formed from the gathered
 // feature row itself, s = X[j, h, :] . a_src[h, :] (each lane's VEC products,
 // then a butterfly over the L = D / VEC adjacent lanes of the head, which
 // leaves every lane of the head with the same bits), instead of being gathered
 // from s_src: a GAT layer's source score is that projection, and the random
 // 4H-byte score row of each edge costs a whole cache line.  Needs 16-byte
 // vectors, L a power of two and each head inside one chunk (the host checks).
-template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD, bool PROJ = false>
+// PM = 2 (one chunk, L equal to the U edges of a batch): the partial products
+// are reduce-scattered over the head's lanes instead, so each lane ends with
+// the score of one edge of the batch and does that edge's softmax arithmetic
+// alone (LeakyReLU, exp, its share of z; the batch maximum by a butterfly),
+// and the weights are handed back to the head's lanes by swizzles: the
+// per-edge scalar work of the softmax is done once per head instead of once
+// per lane of the head.
+template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD, int PM = 0>
 __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k_gat(GatArgs a)
 {
+    constexpr bool PROJ = PM != 0;
+    constexpr bool DIST = PM == 2;
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
     const int log2S = a.log2S;
     const int S = 1 << log2S;
@@ -123,6 +168,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
     const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ wsrc = soft ? a.s_src : a.alpha_in;
+    constexpr float kLog2eF = 1.44269504f;
     // PROJ: this lane's VEC entries of a_src, and the lanes per head
     float asrc[PROJ ? CH : 1][PROJ ? VEC : 1];
     const int hl = PROJ ? a.D / VEC : 1;
@@ -202,6 +248,40 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         }
                         X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
                     }
+                if constexpr (DIST) {
+                    static_assert(CH == 1 && U == 8, "one chunk, batches of 8 edges");
+                    const int hp = lig & (U - 1);
+                    float pp[U];
+#pragma unroll
+                    for (int t = 0; t < U; ++t) {
+                        float p = 0.f;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) p = fmaf(xv[t][0][e], asrc[0][e], p);
+                        pp[t] = p;
+                    }
+                    const float sc = reduce_scatter8(pp, hp);
+                    const float e1 = (j + hp < n && act[0]) ? leaky_relu(sd[0] + sc, a.slope) : -INFINITY;
+                    const float mb = fmaxf(m[0], group_reduce(e1, U, [](float x, float y) { return fmaxf(x, y); }));
+                    if (mb > m[0]) {
+                        const float r = __expf(m[0] - mb);
+                        z[0] *= r;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[0][e] *= r;
+                        m[0] = mb;
+                    }
+                    const float pl = __builtin_amdgcn_exp2f(fmaf(e1, kLog2eF, -m[0] * kLog2eF));
+                    z[0] += pl;            // this lane's share of z, summed over the head at the unit's end
+                    float wt[U];
+                    wt[0] = from_group8<0>(pl); wt[1] = from_group8<1>(pl);
+                    wt[2] = from_group8<2>(pl); wt[3] = from_group8<3>(pl);
+                    wt[4] = from_group8<4>(pl); wt[5] = from_group8<5>(pl);
+                    wt[6] = from_group8<6>(pl); wt[7] = from_group8<7>(pl);
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[0][e] = fmaf(wt[t], xv[t][0][e], acc[0][e]);
+                    continue;
+                }
                 if constexpr (PROJ) {
 #pragma unroll
                     for (int t = 0; t < U; ++t)
@@ -242,10 +322,15 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                             for (int e = 0; e < VEC; ++e) acc[c][e] *= r;
                             m[c] = mb;
                         }
+                        // exp(w - m) = 2^(w log2 e - m log2 e): one fma per edge; a masked
+                        // edge (-inf) gives 2^-inf = 0.  m is finite here on every lane that
+                        // stores (its first batch holds a valid edge); a lane past the row's
+                        // width (no store) may compute NaN, which no other lane reads.
+                        const float ml = m[c] * kLog2eF;
                         float zb = 0.f;
 #pragma unroll
                         for (int t = 0; t < U; ++t) {
-                            w[t][c] = (w[t][c] == -INFINITY) ? 0.f : __expf(w[t][c] - m[c]);
+                            w[t][c] = __builtin_amdgcn_exp2f(fmaf(w[t][c], kLog2eF, -ml));
                             zb += w[t][c];
                         }
                         z[c] += zb;
@@ -267,6 +352,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
             c_cur = c_nxt;
             if constexpr (BWD) p_cur = p_nxt;
         }
+        if constexpr (DIST) z[0] = group_sum(z[0], U);   // the head's shares of z
         int c_first_next = 0, p_first_next = 0;
         if (dn.z > dn.y) {
             const int k = dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1;
@@ -383,7 +469,9 @@ GatKernel gat_pick(int xdt, int ydt, int vec, int ch, bool buf)
     return gat_pick_y<f16_t, false, BWD>(ydt, vec, ch);
 }
 
-// The PROJ forward kernels (16-byte vectors only), instantiated in gat_proj.hip.
-GatKernel gat_pick_proj(int xdt, int ydt, int ch, bool buf);
+// The forward kernels with projected source scores (16-byte vectors only),
+// instantiated in gat_proj.hip; dist: the distributed-softmax mode (one chunk,
+// 8 lanes per head).
+GatKernel gat_pick_proj(int xdt, int ydt, int ch, bool buf, bool dist);
 
 }  // namespace cogdl

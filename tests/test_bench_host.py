@@ -123,3 +123,23 @@ def test_oracle_rate_sampling():
     assert r["units"] == 5 and len(set(seen)) == 5
     r = bench.oracle_rate(run, 1000, budget_s=0.0, full=True)
     assert r["units"] == 1000 and r["bytes"] == 100
+
+
+def test_workloads_probe_summary(tmp_path):
+    """Each op's section lies between its own pair of markers; the closing copy scales them."""
+    M = "void at::native::bitwise_not_kernel"
+    kib = 1024.0
+    copy_raw = bench.CALIB_BYTES / 2 / kib
+    fetch = [("setup", 9.0), (M, 0), ("k1", 10.0), ("k2", 5.0), (M, 0), ("between", 7.0),
+             (M, 0), ("k3", 4.0), (M, 0), (M, 0), ("copy", copy_raw), (M, 0)]
+    write = [(n, v / 2) for n, v in fetch]
+    _write_probe_csv(tmp_path / "f", "FETCH_SIZE", fetch)
+    _write_probe_csv(tmp_path / "w", "WRITE_SIZE", write)
+    keys = ["wl/a", "wl/b", "calib_copy"]
+    r = bench.summarize_workloads_probe(str(tmp_path / "f"), str(tmp_path / "w"), keys)
+    assert set(r) == {"wl/a", "wl/b"}
+    assert r["wl/a"]["fetch_bytes"] == 15.0 * kib * 2 and r["wl/b"]["fetch_bytes"] == 4.0 * kib * 2
+    assert r["wl/a"]["write_bytes"] == 7.5 * kib * 4      # the copy reads a quarter of its size here
+    import pytest
+    with pytest.raises(RuntimeError):
+        bench.summarize_workloads_probe(str(tmp_path / "f"), str(tmp_path / "w"), keys[:2])

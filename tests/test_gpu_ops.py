@@ -726,10 +726,12 @@ def test_plan_rebuild_past_capacity_is_refused(cg):
 
 @pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
 @pytest.mark.parametrize("H,D,xk,yk", [(4, 64, "bf16", "bf16"), (8, 16, "f32", "f32"), (2, 32, "f16", "f32"),
-                                       (1, 8, "f32", "f32"), (4, 32, "bf16", "f32"), (16, 8, "bf16", "bf16")])
+                                       (1, 8, "f32", "f32"), (4, 32, "bf16", "f32"), (16, 8, "bf16", "bf16"),
+                                       (4, 32, "f32", "f32"), (2, 64, "bf16", "f32"), (1, 64, "f16", "f16")])
 def test_gat_aggregate_proj(cg, kind, H, D, xk, yk):
     """Source scores projected from the gathered rows against the oracle model: the oracle's
-    head scores (fp64) feed its fused aggregation.  Bar: the aggregation's tolerance plus the
+    head scores (fp64) feed its fused aggregation.  Heads of 8 lanes (bf16/fp16 D = 64, fp32
+    D = 32) take the distributed-softmax kernel, the others the per-lane one.  Bar: the aggregation's tolerance plus the
     score's own rounding, 2 (D 2^-24 max_j sum_d |X_jd a_hd| + 2^-24 max |s|) (a score moved by
     ds moves each output by at most 2 ds times its error scale)."""
     import torch
