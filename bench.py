@@ -840,7 +840,7 @@ def write_counter_profile(args, fetch_dir, write_dir, probe_json, req_dir=None):
     summ = summarize_probe(fetch_dir, write_dir, probe["launches"])
     summ["source_sha16"] = library_source_sha()
     summ["workload"] = cfg["name"]
-    flags = " ".join(probe_command(args, "PROBE_JSON")[3:])
+    flags = " ".join(probe_command(args, "PROBE_JSON")[4:])
     cmd = ("cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {c} --kernel-trace -d DIR -o run --output-format csv -- "
            f"python3 bench.py --counter-probe PROBE_JSON {flags}")
     summ["commands"] = {"fetch": cmd.format(c="FETCH_SIZE"), "write": cmd.format(c="WRITE_SIZE")}

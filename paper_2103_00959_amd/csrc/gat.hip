@@ -543,10 +543,11 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
     if (P) set_units(a, tiny ? long_units(*P) : all_units(*P));
     {
         const int64_t upb = kBlock >> m.log2S;
-        // one chunk with 8 lanes per head: the distributed-softmax kernel (batches of 8 edges)
-        const bool dist = m.ch == 1 && hl == 8;
+        // one chunk of 16-byte vectors with 8 lanes per head: the distributed-softmax
+        // kernel (batches of 8 edges, one edge's score per lane)
+        const bool dist = soft && m.ch == 1 && m.vec * dtype_bytes(x_dtype) == 16 && D % m.vec == 0 && hl == 8;
         GatKernel k = proj ? gat_pick_proj(x_dtype, y_dtype, m.ch, buf, dist)
-                           : gat_pick<false>(x_dtype, y_dtype, m.vec, m.ch, buf);
+                           : gat_pick<false>(x_dtype, y_dtype, m.vec, m.ch, buf, dist);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;

@@ -120,8 +120,8 @@ __device__ __forceinline__ float from_group8(float v)
     return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x18 | (T << 5)));
 }
 
-// PM (source-score mode): 0 reads s_src (or the given weights); 1 and 2 form
-// it from the gathered row.
+// PM (source-score mode): 0 and 3 read s_src (or, BWD / alpha_in, the given
+// weights); 1 and 2 form it from the gathered row.
 // PM = 1: the source score of each edge is formed from the gathered
 // feature row itself, s = X[j, h, :] . a_src[h, :] (each lane's VEC products,
 // then a butterfly over the L = D / VEC adjacent lanes of the head, which
@@ -135,12 +135,15 @@ __device__ __forceinline__ float from_group8(float v)
 // alone (LeakyReLU, exp, its share of z; the batch maximum by a butterfly),
 // and the weights are handed back to the head's lanes by swizzles: the
 // per-edge scalar work of the softmax is done once per head instead of once
-// per lane of the head.
+// per lane of the head.  PM = 3 is the same distribution with the scores read
+// from s_src: each lane reads the score of its own edge only (softmax forward
+// only, not BWD or given weights).
 template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD, int PM = 0>
 __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k_gat(GatArgs a)
 {
-    constexpr bool PROJ = PM != 0;
-    constexpr bool DIST = PM == 2;
+    constexpr bool PROJ = PM == 1 || PM == 2;
+    constexpr bool DIST = PM == 2 || PM == 3;
+    static_assert(!(DIST && BWD), "the distributed softmax is a forward path");
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
     const int log2S = a.log2S;
     const int S = 1 << log2S;
@@ -241,7 +244,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         const int64_t wi = BWD ? (int64_t)pk[t] * H + hd[c]
                                          : soft ? (int64_t)cc[t] * H + hd[c]
                                                 : (int64_t)(k0 + j + t) * H + hd[c];
-                        if constexpr (!PROJ) w[t][c] = wsrc[on ? wi : 0];
+                        if constexpr (!PROJ && !DIST) w[t][c] = wsrc[on ? wi : 0];
                         if constexpr (BWD) {
                             const float g = a.dscore[on ? wi : 0];
                             dsum[c] += on ? g : 0.f;
@@ -251,16 +254,31 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                 if constexpr (DIST) {
                     static_assert(CH == 1 && U == 8, "one chunk, batches of 8 edges");
                     const int hp = lig & (U - 1);
-                    float pp[U];
+                    const bool mine = j + hp < n && act[0];       // this lane's edge of the batch
+                    float sc;
+                    if constexpr (PROJ) {
+                        float pp[U];
 #pragma unroll
-                    for (int t = 0; t < U; ++t) {
-                        float p = 0.f;
+                        for (int t = 0; t < U; ++t) {
+                            float p = 0.f;
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) p = fmaf(xv[t][0][e], asrc[0][e], p);
-                        pp[t] = p;
+                            for (int e = 0; e < VEC; ++e) p = fmaf(xv[t][0][e], asrc[0][e], p);
+                            pp[t] = p;
+                        }
+                        sc = reduce_scatter8(pp, hp);
+                    } else {
+                        const int cme = lane_bcast(c_cur, gbase + j + hp);
+                        sc = wsrc[mine ? (int64_t)cme * H + hd[0] : 0];
                     }
-                    const float sc = reduce_scatter8(pp, hp);
-                    const float e1 = (j + hp < n && act[0]) ? leaky_relu(sd[0] + sc, a.slope) : -INFINITY;
+                    const float e1 = mine ? leaky_relu(sd[0] + sc, a.slope) : -INFINITY;
+                    if constexpr (!PROJ) {
+                        // alpha wanted: each lane parks the score of its own edge
+                        if (a.alpha_out != nullptr && mine) {
+                            const int k = k0 + j + hp;
+                            if (COGDL_PARK_LDS) COGDL_LDS_PARK[(k - beg) * H + hd[0]] = e1;
+                            else a.alpha_out[(int64_t)k * H + hd[0]] = e1;
+                        }
+                    }
                     const float mb = fmaxf(m[0], group_reduce(e1, U, [](float x, float y) { return fmaxf(x, y); }));
                     if (mb > m[0]) {
                         const float r = __expf(m[0] - mb);
@@ -435,7 +453,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
 using GatKernel = void (*)(GatArgs);
 
 template <typename TX, typename TY, bool BUF, bool BWD>
-GatKernel gat_pick_vec(int vec, int ch)
+GatKernel gat_pick_vec(int vec, int ch, bool dist)
 {
     constexpr int V = (int)(16 / sizeof(TX));
     if (vec == 1) {
@@ -443,30 +461,37 @@ GatKernel gat_pick_vec(int vec, int ch)
         if (ch == 2) return k_gat<TX, TY, 1, 2, BUF, BWD>;
         return k_gat<TX, TY, 1, 4, BUF, BWD>;
     }
-    if (ch == 1) return k_gat<TX, TY, V, 1, BUF, BWD>;
+    if (ch == 1) {
+        if constexpr (!BWD) {
+            if (dist) return k_gat<TX, TY, V, 1, BUF, false, 3>;
+        }
+        return k_gat<TX, TY, V, 1, BUF, BWD>;
+    }
     if (ch == 2) return k_gat<TX, TY, V, 2, BUF, BWD>;
     return k_gat<TX, TY, V, 4, BUF, BWD>;
 }
 
 template <typename TX, bool BUF, bool BWD>
-GatKernel gat_pick_y(int ydt, int vec, int ch)
+GatKernel gat_pick_y(int ydt, int vec, int ch, bool dist)
 {
-    if (ydt == COGDL_F32) return gat_pick_vec<TX, float, BUF, BWD>(vec, ch);
-    if (ydt == COGDL_BF16) return gat_pick_vec<TX, bf16_t, BUF, BWD>(vec, ch);
-    return gat_pick_vec<TX, f16_t, BUF, BWD>(vec, ch);
+    if (ydt == COGDL_F32) return gat_pick_vec<TX, float, BUF, BWD>(vec, ch, dist);
+    if (ydt == COGDL_BF16) return gat_pick_vec<TX, bf16_t, BUF, BWD>(vec, ch, dist);
+    return gat_pick_vec<TX, f16_t, BUF, BWD>(vec, ch, dist);
 }
 
+// dist: the distributed-softmax forward kernel (scores read from s_src, one
+// chunk of 16-byte vectors, 8 lanes per head); BWD ignores it.
 template <bool BWD>
-GatKernel gat_pick(int xdt, int ydt, int vec, int ch, bool buf)
+GatKernel gat_pick(int xdt, int ydt, int vec, int ch, bool buf, bool dist = false)
 {
     if (buf) {
-        if (xdt == COGDL_F32) return gat_pick_y<float, true, BWD>(ydt, vec, ch);
-        if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, true, BWD>(ydt, vec, ch);
-        return gat_pick_y<f16_t, true, BWD>(ydt, vec, ch);
+        if (xdt == COGDL_F32) return gat_pick_y<float, true, BWD>(ydt, vec, ch, dist);
+        if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, true, BWD>(ydt, vec, ch, dist);
+        return gat_pick_y<f16_t, true, BWD>(ydt, vec, ch, dist);
     }
-    if (xdt == COGDL_F32) return gat_pick_y<float, false, BWD>(ydt, vec, ch);
-    if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, false, BWD>(ydt, vec, ch);
-    return gat_pick_y<f16_t, false, BWD>(ydt, vec, ch);
+    if (xdt == COGDL_F32) return gat_pick_y<float, false, BWD>(ydt, vec, ch, dist);
+    if (xdt == COGDL_BF16) return gat_pick_y<bf16_t, false, BWD>(ydt, vec, ch, dist);
+    return gat_pick_y<f16_t, false, BWD>(ydt, vec, ch, dist);
 }
 
 // The forward kernels with projected source scores (16-byte vectors only),

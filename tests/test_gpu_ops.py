@@ -494,7 +494,8 @@ def test_softmax_degree_one_rows_exact_and_wide_scores(cg):
 
 
 @pytest.mark.parametrize("scale", [8.0, 24.0])
-def test_alpha_wide_scores_every_plan(cg, scale):
+@pytest.mark.parametrize("D,xk", [(8, "f32"), (64, "bf16")])
+def test_alpha_wide_scores_every_plan(cg, scale, D, xk):
     """Scores N(0, scale^2): |e - m| reaches the range where the weights approach FLT_MIN
     (scale 24), so the exponent's conditioning is exercised; every weight whose reference is a
     normal fp32 value is compared at 1e-5 plus the rounding of its fp32 score (see
@@ -503,13 +504,13 @@ def test_alpha_wide_scores_every_plan(cg, scale):
     rescoring pass)."""
     g = _graph("hubs", seed=9)
     rp, cl, _ = graph_to_dev(g)
-    H, D = 4, 8
+    H = 4
     sd, ss = _scores(g.n_rows, g.n_cols, H, 79, scale=scale)
     a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
     bound = _alpha_bound_scale(g, sd, ss)
     say(f"wide scores x{scale}: smallest normal reference weight {a_ref[a_ref >= FLT_MIN].min():.3e}, "
         f"{int((a_ref < FLT_MIN).sum())} below FLT_MIN, bound up to {bound.max() * TOL_ALPHA:.2e}")
-    _, _, xd = features((g.n_cols, H, D), 61, "f32")
+    _, _, xd = features((g.n_cols, H, D), 61, xk)      # D = 64 bf16: the distributed-softmax kernel
     specs = [None, ("auto", 0, False), ("neighbor_group", 5, False), ("neighbor_group", 64, True),
              ("neighbor_group", 7, True)]
     for spec in specs:
