@@ -1209,7 +1209,8 @@ def main():
                "dalpha": torch.empty((E, H), dtype=torch.float32, device=dev),
                "dscore": torch.empty((E, H), dtype=torch.float32, device=dev),
                "ds_dst": torch.empty((N, H), dtype=torch.float32, device=dev),
-               "ds_src": torch.empty((M, H), dtype=torch.float32, device=dev)}
+               "ds_src": torch.empty((M, H), dtype=torch.float32, device=dev),
+               "edge_work": torch.empty((E, H, 2), dtype=torch.float32, device=dev)}
     ms_bwd, k_bwd = time_op_kernels(lambda: cg.gat_backward(
         rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha_buf, Xg, dYg, 0.2, plan=plan,
         plan_t=plan_t, out=bwd_out))
@@ -1217,8 +1218,11 @@ def main():
     ms_dot, k_dot = time_op_kernels(lambda: cg.sddmm_dot(rowptr, col, dYg, Xg, plan=plan, out=dot_out))
     b_dot = 4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * E * H
     del bwd_out, dYg, dot_out
+    # rows pass: rowptr, col, dY rows, gathered X rows, s_dst, alpha, s_src, dalpha, dscore,
+    # the (alpha, dscore) records, ds_dst; cols pass: colptr, row_t, perm, gathered dY rows,
+    # one 8H-byte record per edge, dX, ds_src
     b_bwd_rows = (4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * N * H + 4 * E * H
-                  + 4 * E * H + 4 * E * H + 4 * E * H + 4 * N * H)
+                  + 4 * E * H + 4 * E * H + 4 * E * H + 8 * E * H + 4 * N * H)
     b_bwd_cols = (4 * (M + 1) + 4 * E + 4 * E + E * H * D * 2 + 4 * E * H + 4 * E * H
                   + M * H * D * 2 + 4 * M * H)
     b_bwd = b_bwd_rows + b_bwd_cols

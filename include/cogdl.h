@@ -450,9 +450,15 @@ cogdl_status cogdl_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const 
  * colptr, row_t, perm: the CSC of the same graph from cogdl_csr_to_csc.
  * plan: NULL or a plan on rowptr with max_heads >= H; plan_t: NULL or a plan
  * on colptr with max_feat >= H*D and max_heads >= H.  dalpha and dscore are
- * nnz x H fp32 outputs (dscore also serves as scratch during the call).
- * fp32 accumulation; every output is overwritten.  Both plans' workspaces are
- * used: one call per plan pair in flight.
+ * nnz x H fp32 outputs.  edge_work: caller-owned device scratch of nnz x H x 2
+ * floats, 8-byte aligned (NULL allowed only when nnz == 0): the first pass
+ * leaves there, per edge k (CSR order) and head h, the pair
+ * (alpha[k,h], dscore[k,h]) at floats 2(kH + h) and 2(kH + h) + 1, which the
+ * second pass reads through perm (one record per edge instead of two rows);
+ * it holds those pairs on return.  fp32 accumulation; every output is
+ * overwritten.  Both plans' workspaces and edge_work are used: one call per
+ * plan pair and workspace in flight.  COGDL_ERR_INVALID for a missing or
+ * misaligned edge_work.
  * ---------------------------------------------------------------------- */
 cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                 const int32_t *rowptr, const int32_t *col, const int32_t *colptr,
@@ -461,8 +467,8 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                 const float *alpha, const void *X, cogdl_dtype x_dtype,
                                 const void *dY, cogdl_dtype dy_dtype, void *dX,
                                 cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
-                                float *ds_src, const cogdl_plan *plan, const cogdl_plan *plan_t,
-                                hipStream_t stream);
+                                float *ds_src, float *edge_work, const cogdl_plan *plan,
+                                const cogdl_plan *plan_t, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel tracing (instrumentation, not part of the paper's method).  When

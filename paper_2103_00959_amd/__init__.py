@@ -89,7 +89,7 @@ def lib():
                                   P, P, P]
     L.cogdl_gat_backward.argtypes = [i32, i32, i64, P, P, P, P, P, i32, i32, P, P, f32, P, P,
                                      ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P,
-                                     P, P]
+                                     P, P, P]
     L.cogdl_trace_enable.argtypes = [i32]
     L.cogdl_trace_filter.argtypes = [ctypes.c_char_p]
     L.cogdl_trace_count.restype = i32
@@ -619,7 +619,9 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
                  dx_dtype=None, out=None):
     """Gradients of gat_aggregate for dY = dL/dY.  X is [n_cols, H, D], dY [n_rows, H, D],
     alpha [nnz, H] the forward weights; (colptr, row_t, perm) the CSC from csr_to_csc.
-    Returns dict(dX, dalpha, dscore, ds_dst, ds_src); ``out`` may supply these tensors."""
+    Returns dict(dX, dalpha, dscore, ds_dst, ds_src, edge_work); ``out`` may supply these
+    tensors.  edge_work (fp32, 2 nnz H) is the library's scratch between its two passes: it
+    ends holding the pair (alpha, dscore) of every edge and head."""
     import torch
     n_rows, nnz = _graph(rowptr, col)
     n_cols, H, D = _dims(X, "X", 3)
@@ -635,7 +637,7 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     _numel(alpha, "alpha", nnz * H)
     o = dict(out or {})
     sizes = {"dX": n_cols * H * D, "dalpha": nnz * H, "dscore": nnz * H, "ds_dst": n_rows * H,
-             "ds_src": n_cols * H}
+             "ds_src": n_cols * H, "edge_work": 2 * nnz * H}
     for k in o:
         if k not in sizes:
             raise CogdlError(f"unknown output {k!r}")
@@ -654,14 +656,15 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     o.setdefault("dscore", torch.empty((nnz, H), dtype=torch.float32, device=dev))
     o.setdefault("ds_dst", torch.empty((n_rows, H), dtype=torch.float32, device=dev))
     o.setdefault("ds_src", torch.empty((n_cols, H), dtype=torch.float32, device=dev))
+    o.setdefault("edge_work", torch.empty((nnz, H, 2), dtype=torch.float32, device=dev))
     _dev(o["dX"], "dX")
-    for k in ("dalpha", "dscore", "ds_dst", "ds_src"):
+    for k in ("dalpha", "dscore", "ds_dst", "ds_src", "edge_work"):
         _dev(o[k], k, torch.float32)
     _check(lib().cogdl_gat_backward(
         n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(colptr), _ptr(row_t), _ptr(perm), H, D,
         _ptr(s_dst), _ptr(s_src), float(negative_slope), _ptr(alpha), _ptr(X), _dtype_code(X),
         _ptr(dY), _dtype_code(dY), _ptr(o["dX"]), _dtype_code(o["dX"]), _ptr(o["dalpha"]),
-        _ptr(o["dscore"]), _ptr(o["ds_dst"]), _ptr(o["ds_src"]), _plan_handle(plan),
+        _ptr(o["dscore"]), _ptr(o["ds_dst"]), _ptr(o["ds_src"]), _ptr(o["edge_work"]), _plan_handle(plan),
         _plan_handle(plan_t), _stream()), "cogdl_gat_backward")
     return o
 

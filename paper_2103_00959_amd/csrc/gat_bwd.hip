@@ -13,17 +13,20 @@
 // Pass 1 runs on the CSR units.  With the SpMM lane map (S lanes x VEC
 // features of a row, the L = D / VEC lanes of a head side by side) each lane
 // multiplies its dY elements into every gathered neighbour row and a
-// butterfly over the head's lanes completes the dot product, so the gathered
+// reduction over the head's lanes completes the dot product, so the gathered
 // rows are read once, as in the forward aggregation.  The lanes fold the row
-// sum c as they go and park dalpha and the pre-activation of every edge in
-// the two outputs (each value by a fixed lane); once c is complete, the same
-// lanes read their own parked values back and write dscore and ds_dst.  A
-// neighbour group of a split row leaves its share of c in the plan, and two
-// small kernels finish those rows once every group is done.
+// sum c as they go and park dalpha and the pair (alpha, f alpha) of every
+// edge (each value by a fixed lane); once c is complete, the same lanes read
+// their own parked values back and write dscore and ds_dst.  A neighbour
+// group of a split row leaves its share of c in the plan, and two small
+// kernels finish those rows once every group is done.
 //
-// Pass 2 is the aggregation kernel run on the CSC (rows = source nodes) with
-// the forward weights reached through perm, summing dscore per head along the
-// way: dX and ds_src in one sweep over dY.
+// The pairs (alpha, dscore) of an edge's heads end side by side in the
+// caller's edge workspace, 8 H bytes per edge in CSR order.  Pass 2 is the
+// aggregation kernel run on the CSC (rows = source nodes), reaching each
+// edge's pair through perm: one random 8H-byte record per edge instead of
+// two 4H-byte rows in two arrays, each of which costs a cache line.  It sums
+// dscore per head along the way: dX and ds_src in one sweep over dY.
 #include "gat_kernel.hpp"
 
 namespace cogdl {
@@ -50,7 +53,8 @@ struct BwdArgs {
     uint64_t x_bytes;
     const void *P;              // row operand (dY), n_rows x W
     float *dalpha;              // [nnz][H]
-    float *dscore;              // [nnz][H]; holds the pre-activations until the end
+    float *dscore;              // [nnz][H]
+    float2 *rec;                // [nnz][H] pairs (alpha, f alpha), then (alpha, dscore)
     float *ds_dst;              // [n_rows][H]
     float *gstats;              // split rows: per partial slot c[max_heads], sum[max_heads]
     int32_t sstride;            // 2 * max_heads
@@ -72,8 +76,11 @@ __device__ __forceinline__ int4 fetch_bwd_unit(const BwdArgs &a, int64_t u, int6
 
 // The score gradient of edge k and head h is f * alpha * (dalpha - c), with f
 // the LeakyReLU slope at the pre-activation t and c the row's sum of alpha *
-// dalpha.  Pass 1 parks u = f * alpha in dscore (c is not known yet); once c
-// is, dscore = u * (dalpha - c).
+// dalpha.  Pass 1 parks u = f * alpha (c is not known yet): beside alpha in
+// the edge record for a whole row, whose fix-up follows at once and finds the
+// record in the cache; in dscore for a neighbour group of a split row, whose
+// fix-up runs after the pass and reads alpha back from its input, so that the
+// record is written once, complete.  Once c is known, dscore = u (dalpha - c).
 __device__ __forceinline__ float park_value(float t, float slope, float al)
 {
     return (t > 0.f ? 1.f : slope) * al;
@@ -81,16 +88,38 @@ __device__ __forceinline__ float park_value(float t, float slope, float al)
 
 __device__ __forceinline__ float parked_grad(float u, float da, float c) { return u * (da - c); }
 
+// Fix-up of one parked edge-head: dscore from alpha, the parked u and
+// dalpha, into both the output and the record.
+__device__ __forceinline__ float finish_edge(const BwdArgs &a, int64_t i, float al, float u, float da, float c)
+{
+    const float g = parked_grad(u, da, c);
+    a.dscore[i] = g;
+    a.rec[i] = make_float2(al, g);
+    return g;
+}
+
+// Park the pair of edge-head i: the record (whole row) or u alone (split row).
+__device__ __forceinline__ void park_edge(const BwdArgs &a, int64_t i, bool split, float al, float u)
+{
+    if (split) a.dscore[i] = u;
+    else a.rec[i] = make_float2(al, u);
+}
+
 // Pass 1, feature-parallel: one S-lane sub-group per unit, lane = VEC
 // consecutive features, head h on lanes [h L, (h + 1) L).  Requires one
 // chunk per lane (H * D <= S * VEC) and L a power of two.  Every edge k of a
 // unit is owned by lane q = (k - beg) mod M of its head, M = min(L, U): that
 // lane alone loads the edge's alpha and source score, adds its term of c, and
 // parks its dalpha and u; the head's lanes then add up their shares of c.
-template <typename TX, int VEC, bool BUF, bool DOT>
+// RS (batches of U = 8 edges, L >= 8): the head's partial dot products are
+// reduce-scattered over aligned groups of 8 lanes, so lane q ends with the
+// group's sum for its own edge q mod 8 (7 exchanges for the batch instead of
+// 8 butterflies of log2 L), and L > 8 adds the groups by a butterfly.
+template <typename TX, int VEC, bool BUF, bool DOT, bool RS = false>
 __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 {
     constexpr int U = VEC == 1 ? 16 : 8;
+    static_assert(!RS || U == 8, "reduce-scatter over batches of 8 edges");
     // 16-bit features stay packed: four dot2 instructions per 16-byte vector
     // instead of widening both operands to fp32 (half the registers).
     constexpr bool PACKED = sizeof(TX) == 2 && VEC == 8;
@@ -161,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                     else X.load((int64_t)cc[t] * a.W + fe, on, xv[t]);
                     al[t] = 0.f;
                     ss[t] = 0.f;
-                    if constexpr (!DOT) {
+                    if constexpr (!DOT && !RS) {
                         if (mine[t]) {
                             al[t] = a.alpha[(int64_t)(k0 + j + t) * H + h];
                             ss[t] = a.s_src[(int64_t)cc[t] * H + h];
@@ -183,6 +212,26 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                     }
                     pd[t] = s;
                 }
+                if constexpr (RS) {
+                    // lane q completes the dot product of edge j + (q mod 8)
+                    const int t = q & 7;
+                    float s = reduce_scatter8(pd, t);
+                    for (int off = 8; off < L; off <<= 1) s += lane_xor(s, off);
+                    const bool own = j + t < n && writer;
+                    const int64_t k = k0 + j + t;
+                    // (a cross-lane read: every lane takes part)
+                    const int cme = DOT ? 0 : lane_bcast(c_cur, gbase + j + t);
+                    if (own) {
+                        a.dalpha[k * H + h] = s;
+                        if constexpr (!DOT) {
+                            const float al1 = a.alpha[k * H + h];
+                            const float ss1 = a.s_src[(int64_t)cme * H + h];
+                            c += al1 * s;
+                            park_edge(a, k * H + h, part >= 0, al1, park_value(sd + ss1, a.slope, al1));
+                        }
+                    }
+                    continue;
+                }
                 // complete the dot products over the head's lanes (every lane of
                 // the head ends with the same bits: each level adds the same pair)
 #pragma unroll
@@ -194,7 +243,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                         a.dalpha[k * H + h] = pd[t];
                         if constexpr (!DOT) {
                             c += al[t] * pd[t];
-                            a.dscore[k * H + h] = park_value(sd + ss[t], a.slope, al[t]);
+                            park_edge(a, k * H + h, part >= 0, al[t], park_value(sd + ss[t], a.slope, al[t]));
                         }
                     }
                 }
@@ -215,22 +264,20 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 float sdt = 0.f;
                 if (writer) {
                     for (int o0 = q; o0 < end - beg; o0 += R * M) {
-                        float da[R], uv[R];
+                        float da[R];
+                        float2 uv[R];
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
                             const int64_t k = (int64_t)beg + (o < end - beg ? o : o0);
                             da[r] = a.dalpha[k * H + h];
-                            uv[r] = a.dscore[k * H + h];
+                            uv[r] = a.rec[k * H + h];
                         }
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
-                            if (o < end - beg) {
-                                const float g = parked_grad(uv[r], da[r], c);
-                                a.dscore[((int64_t)beg + o) * H + h] = g;
-                                sdt += g;
-                            }
+                            if (o < end - beg)
+                                sdt += finish_edge(a, ((int64_t)beg + o) * H + h, uv[r].x, uv[r].y, da[r], c);
                         }
                     }
                 }
@@ -296,7 +343,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
                 if constexpr (!DOT) {
                     const float al = a.alpha[(int64_t)k * H + h];
                     c += al * s;
-                    a.dscore[(int64_t)k * H + h] = park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al);
+                    park_edge(a, (int64_t)k * H + h, part >= 0, al,
+                              park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al));
                 }
             }
         }
@@ -310,9 +358,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
         if (live) {
             for (int k = beg + slot; k < end; k += eps) {
                 const int64_t i = (int64_t)k * H + h;
-                const float g = parked_grad(a.dscore[i], a.dalpha[i], c);
-                a.dscore[i] = g;
-                sdt += g;
+                const float2 r = a.rec[i];
+                sdt += finish_edge(a, i, r.x, r.y, a.dalpha[i], c);
             }
         }
         sdt = slot_sum(live ? sdt : 0.f, H);
@@ -321,8 +368,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
 }
 
 // Split rows, after pass 1: every neighbour group adds up the shares of c of
-// all groups of its row (slot order), turns its parked edges into dscore and
-// leaves its share of ds_dst.  One wavefront per group, lanes (slot, head).
+// all groups of its row, turns its parked edges into dscore and leaves its
+// share of ds_dst.  One wavefront per group, lanes (slot, head); the shares
+// are loaded by the slots side by side and summed over the slots in a fixed
+// order (every group of a row forms the same c), and the next group's
+// descriptors are fetched while this one is processed.
 __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
 {
     const int lane = lane_id();
@@ -334,37 +384,44 @@ __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
     const int half = a.sstride >> 1;
     const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
     const int32_t np = *a.n_parts;
-    for (int64_t p = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; p < np;
-         p += waves) {
-        const int4 d = a.part_units[p];
-        const int4 sr = a.split_rows[d.w];
-        float c = 0.f;
-        for (int g = 0; g < sr.z; ++g) c += a.gstats[(int64_t)(sr.y + g) * a.sstride + h];
+    int64_t p = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    if (p >= np) return;
+    int4 d = a.part_units[p];
+    int4 sr = a.split_rows[d.w];
+    for (;;) {
+        const int64_t pn = p + waves;
+        const int4 dn = pn < np ? a.part_units[pn] : make_int4(0, 0, 0, 0);
+        float cs = 0.f;
+        if (live)
+            for (int g = slot; g < sr.z; g += eps) cs += a.gstats[(int64_t)(sr.y + g) * a.sstride + h];
+        const float c = slot_sum(live ? cs : 0.f, H);
+        const int4 srn = pn < np ? a.split_rows[dn.w] : make_int4(0, 0, 0, 0);
         constexpr int R = 8;
         float sdt = 0.f;
         if (live) {
             for (int k0 = d.y + slot; k0 < d.z; k0 += R * eps) {
-                float da[R], uv[R];
+                float da[R], uv[R], al[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
                     const int64_t i = (int64_t)(k < d.z ? k : k0) * H + h;
                     da[r] = a.dalpha[i];
                     uv[r] = a.dscore[i];
+                    al[r] = a.alpha[i];
                 }
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
-                    if (k < d.z) {
-                        const float g = parked_grad(uv[r], da[r], c);
-                        a.dscore[(int64_t)k * H + h] = g;
-                        sdt += g;
-                    }
+                    if (k < d.z) sdt += finish_edge(a, (int64_t)k * H + h, al[r], uv[r], da[r], c);
                 }
             }
         }
         sdt = slot_sum(live ? sdt : 0.f, H);
         if (slot == 0) a.gstats[p * a.sstride + half + h] = sdt;
+        if (pn >= np) break;
+        p = pn;
+        d = dn;
+        sr = srn;
     }
 }
 
@@ -392,19 +449,31 @@ __global__ __launch_bounds__(kBlock) void k_split_head_sums(const int4 *__restri
 
 using BwdKernel = void (*)(BwdArgs);
 
+template <typename TX, int VEC, bool DOT>
+BwdKernel pick_rows_rs(bool buf, bool rs)
+{
+    if constexpr (VEC == 1) {
+        return buf ? k_bwd_rows<TX, 1, true, DOT> : k_bwd_rows<TX, 1, false, DOT>;
+    } else {
+        if (rs) return buf ? k_bwd_rows<TX, VEC, true, DOT, true> : k_bwd_rows<TX, VEC, false, DOT, true>;
+        return buf ? k_bwd_rows<TX, VEC, true, DOT> : k_bwd_rows<TX, VEC, false, DOT>;
+    }
+}
+
+// rs: the head spans 8 or more lanes (reduce-scatter; vector kernels only)
 template <bool DOT>
-BwdKernel pick_rows(int dt, bool buf, int vec)
+BwdKernel pick_rows(int dt, bool buf, int vec, bool rs)
 {
     if (dt == COGDL_F32) {
-        if (vec == 4) return buf ? k_bwd_rows<float, 4, true, DOT> : k_bwd_rows<float, 4, false, DOT>;
-        return buf ? k_bwd_rows<float, 1, true, DOT> : k_bwd_rows<float, 1, false, DOT>;
+        if (vec == 4) return pick_rows_rs<float, 4, DOT>(buf, rs);
+        return pick_rows_rs<float, 1, DOT>(buf, rs);
     }
     if (dt == COGDL_BF16) {
-        if (vec == 8) return buf ? k_bwd_rows<bf16_t, 8, true, DOT> : k_bwd_rows<bf16_t, 8, false, DOT>;
-        return buf ? k_bwd_rows<bf16_t, 1, true, DOT> : k_bwd_rows<bf16_t, 1, false, DOT>;
+        if (vec == 8) return pick_rows_rs<bf16_t, 8, DOT>(buf, rs);
+        return pick_rows_rs<bf16_t, 1, DOT>(buf, rs);
     }
-    if (vec == 8) return buf ? k_bwd_rows<f16_t, 8, true, DOT> : k_bwd_rows<f16_t, 8, false, DOT>;
-    return buf ? k_bwd_rows<f16_t, 1, true, DOT> : k_bwd_rows<f16_t, 1, false, DOT>;
+    if (vec == 8) return pick_rows_rs<f16_t, 8, DOT>(buf, rs);
+    return pick_rows_rs<f16_t, 1, DOT>(buf, rs);
 }
 
 template <typename TX, bool DOT>
@@ -446,7 +515,7 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
     if (fast) {
         a.log2S = m.log2S;
         a.log2L = log2i(L);
-        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec);
+        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec, L >= 8);
         const int64_t upb = kBlock >> m.log2S;
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
@@ -517,16 +586,18 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                 const float *alpha, const void *X, cogdl_dtype x_dtype,
                                 const void *dY, cogdl_dtype dy_dtype, void *dX,
                                 cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
-                                float *ds_src, const cogdl_plan *plan, const cogdl_plan *plan_t,
-                                hipStream_t stream)
+                                float *ds_src, float *edge_work, const cogdl_plan *plan,
+                                const cogdl_plan *plan_t, hipStream_t stream)
 {
     cogdl_status st = check_heads(n_rows, n_cols, nnz, rowptr, col, H, D);
     if (st != COGDL_OK) return st;
     if (!dtype_ok(x_dtype) || !dtype_ok(dy_dtype) || !dtype_ok(dx_dtype)) return COGDL_ERR_DTYPE;
     if (n_cols > 0 && (!colptr || !dX || !ds_src)) return COGDL_ERR_INVALID;
     if (n_rows > 0 && (!ds_dst || !s_dst || !dY)) return COGDL_ERR_INVALID;
-    if (nnz > 0 && (!row_t || !perm || !s_src || !alpha || !X || !dalpha || !dscore))
+    if (nnz > 0 && (!row_t || !perm || !s_src || !alpha || !X || !dalpha || !dscore || !edge_work ||
+                    (uintptr_t)edge_work % alignof(float2) != 0))
         return COGDL_ERR_INVALID;
+    float2 *rec = reinterpret_cast<float2 *>(edge_work);
     const int64_t W = (int64_t)H * D;
     const Plan *Pr = plan_of(plan);
     const Plan *Pc = plan_of(plan_t);
@@ -554,6 +625,7 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
         a.P = dY;
         a.dalpha = dalpha;
         a.dscore = dscore;
+        a.rec = rec;
         a.ds_dst = ds_dst;
         a.gstats = Pr ? Pr->gstats : nullptr;
         a.sstride = Pr ? 2 * Pr->max_heads : 0;
@@ -599,7 +671,7 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     g.gstats = Pc ? Pc->gstats : nullptr;
     g.sstride = Pc ? 2 * Pc->max_heads : 0;
     g.perm = perm;
-    g.dscore = dscore;
+    g.rec = rec;
     g.ds_out = ds_src;
     g.slab = m.slab;
     g.log2S = m.log2S;
@@ -609,7 +681,9 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     if (Pc) set_units(g, tiny ? long_units(*Pc) : all_units(*Pc));
     {
         const int64_t upb = kBlock >> m.log2S;
-        GatKernel k = gat_pick<true>((int)dy_dtype, (int)dx_dtype, m.vec, m.ch, buf);
+        // one edge's record per lane when a head is exactly eight 16-byte vectors
+        const bool dist = m.ch == 1 && m.vec * dtype_bytes(dy_dtype) == 16 && D == 8 * m.vec;
+        GatKernel k = gat_pick<true>((int)dy_dtype, (int)dx_dtype, m.vec, m.ch, buf, dist);
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;

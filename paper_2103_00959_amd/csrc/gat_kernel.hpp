@@ -33,8 +33,8 @@ struct GatArgs {
     float *partials;
     int64_t pstride;
     float *gstats;              // per partial slot: m[max_heads], z[max_heads]
-    const int32_t *perm;        // BWD: weight of edge k is alpha_in[perm[k]] (CSC of the graph)
-    const float *dscore;        // BWD: per-edge, per-head values summed per row (through perm)
+    const int32_t *perm;        // BWD: edge k of this CSC is edge perm[k] of the CSR
+    const float2 *rec;          // BWD: per CSR edge and head (weight, value summed per row)
     float *ds_out;              // BWD: those sums, n_rows x H (split rows: gstats)
     const float *bias;          // epilogue: Y = act(aggregate + bias), bias nullable
     int32_t act;
@@ -136,14 +136,16 @@ __device__ __forceinline__ float from_group8(float v)
 // and the weights are handed back to the head's lanes by swizzles: the
 // per-edge scalar work of the softmax is done once per head instead of once
 // per lane of the head.  PM = 3 is the same distribution with the scores read
-// from s_src: each lane reads the score of its own edge only (softmax forward
-// only, not BWD or given weights).
+// from s_src: each lane reads the score of its own edge only.  BWD with PM = 3:
+// each lane reads the (weight, value) record of its own edge of the batch, the
+// weights reach the head's lanes by swizzles and each lane sums the values of
+// its own edges, added over the head at the unit's end.
 template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD, int PM = 0>
 __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k_gat(GatArgs a)
 {
     constexpr bool PROJ = PM == 1 || PM == 2;
     constexpr bool DIST = PM == 2 || PM == 3;
-    static_assert(!(DIST && BWD), "the distributed softmax is a forward path");
+    static_assert(!BWD || PM == 0 || PM == 3, "the backward reads its weights");
     constexpr int U = (VEC == 1 ? 16 : 8) / CH;
     const int log2S = a.log2S;
     const int S = 1 << log2S;
@@ -232,7 +234,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                 for (int t = 0; t < U; ++t) {
                     ok[t] = j + t < n;
                     cc[t] = lane_bcast(c_cur, gbase + (ok[t] ? j + t : j));
-                    if constexpr (BWD) pk[t] = lane_bcast(p_cur, gbase + (ok[t] ? j + t : j));
+                    if constexpr (BWD && !DIST) pk[t] = lane_bcast(p_cur, gbase + (ok[t] ? j + t : j));
                 }
                 float w[U][CH];
                 float xv[U][CH][VEC];
@@ -244,14 +246,34 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         const int64_t wi = BWD ? (int64_t)pk[t] * H + hd[c]
                                          : soft ? (int64_t)cc[t] * H + hd[c]
                                                 : (int64_t)(k0 + j + t) * H + hd[c];
-                        if constexpr (!PROJ && !DIST) w[t][c] = wsrc[on ? wi : 0];
-                        if constexpr (BWD) {
-                            const float g = a.dscore[on ? wi : 0];
-                            dsum[c] += on ? g : 0.f;
+                        if constexpr (BWD && !DIST) {
+                            const float2 r = a.rec[on ? wi : 0];
+                            w[t][c] = r.x;
+                            dsum[c] += on ? r.y : 0.f;
+                        } else if constexpr (!PROJ && !DIST) {
+                            w[t][c] = wsrc[on ? wi : 0];
                         }
                         X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
                     }
-                if constexpr (DIST) {
+                if constexpr (DIST && BWD) {
+                    static_assert(CH == 1 && U == 8, "one chunk, batches of 8 edges");
+                    const int hp = lig & (U - 1);
+                    const bool mine = j + hp < n && act[0];
+                    const int pme = lane_bcast(p_cur, gbase + j + hp);
+                    const float2 r = a.rec[mine ? (int64_t)pme * H + hd[0] : 0];
+                    dsum[0] += mine ? r.y : 0.f;
+                    const float wv = mine ? r.x : 0.f;
+                    float wt[U];
+                    wt[0] = from_group8<0>(wv); wt[1] = from_group8<1>(wv);
+                    wt[2] = from_group8<2>(wv); wt[3] = from_group8<3>(wv);
+                    wt[4] = from_group8<4>(wv); wt[5] = from_group8<5>(wv);
+                    wt[6] = from_group8<6>(wv); wt[7] = from_group8<7>(wv);
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) acc[0][e] = fmaf(wt[t], xv[t][0][e], acc[0][e]);
+                    continue;
+                } else if constexpr (DIST) {
                     static_assert(CH == 1 && U == 8, "one chunk, batches of 8 edges");
                     const int hp = lig & (U - 1);
                     const bool mine = j + hp < n && act[0];       // this lane's edge of the batch
@@ -370,7 +392,8 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
             c_cur = c_nxt;
             if constexpr (BWD) p_cur = p_nxt;
         }
-        if constexpr (DIST) z[0] = group_sum(z[0], U);   // the head's shares of z
+        if constexpr (DIST && BWD) dsum[0] = group_sum(dsum[0], U);   // the head's shares
+        else if constexpr (DIST) z[0] = group_sum(z[0], U);          // the head's shares of z
         int c_first_next = 0, p_first_next = 0;
         if (dn.z > dn.y) {
             const int k = dn.y + lig < dn.z - 1 ? dn.y + lig : dn.z - 1;
@@ -462,9 +485,7 @@ GatKernel gat_pick_vec(int vec, int ch, bool dist)
         return k_gat<TX, TY, 1, 4, BUF, BWD>;
     }
     if (ch == 1) {
-        if constexpr (!BWD) {
-            if (dist) return k_gat<TX, TY, V, 1, BUF, false, 3>;
-        }
+        if (dist) return k_gat<TX, TY, V, 1, BUF, BWD, 3>;
         return k_gat<TX, TY, V, 1, BUF, BWD>;
     }
     if (ch == 2) return k_gat<TX, TY, V, 2, BUF, BWD>;
@@ -479,8 +500,8 @@ GatKernel gat_pick_y(int ydt, int vec, int ch, bool dist)
     return gat_pick_vec<TX, f16_t, BUF, BWD>(vec, ch, dist);
 }
 
-// dist: the distributed-softmax forward kernel (scores read from s_src, one
-// chunk of 16-byte vectors, 8 lanes per head); BWD ignores it.
+// dist: the distributed kernel (PM = 3: scores read from s_src, or BWD's
+// records, one edge per lane; one chunk of 16-byte vectors, 8 lanes per head).
 template <bool BWD>
 GatKernel gat_pick(int xdt, int ydt, int vec, int ch, bool buf, bool dist = false)
 {

@@ -268,10 +268,10 @@ def test_sddmm_dot_validation(L):
 
 def test_gat_backward_validation(L):
     def B(n_rows, n_cols, nnz, H=2, D=4, xdt=0, ydt=0, dxdt=0, colptr=FAKE, perm=FAKE, alpha=FAKE,
-          dscore=FAKE, ds_src=FAKE):
+          dscore=FAKE, ds_src=FAKE, work=FAKE):
         return L.cogdl_gat_backward(n_rows, n_cols, nnz, FAKE, FAKE, colptr, FAKE, perm, H, D, FAKE,
                                     FAKE, ctypes.c_float(0.2), alpha, FAKE, xdt, FAKE, ydt, FAKE, dxdt,
-                                    FAKE, dscore, FAKE, ds_src, None, None, None)
+                                    FAKE, dscore, FAKE, ds_src, work, None, None, None)
     assert B(2, 2, 3, H=0) == INVALID
     assert B(2, 2, 3, D=0) == INVALID
     assert B(2, 2, 3, xdt=4) == DTYPE
@@ -281,6 +281,8 @@ def test_gat_backward_validation(L):
     assert B(2, 2, 3, alpha=None) == INVALID
     assert B(2, 2, 3, dscore=None) == INVALID
     assert B(2, 2, 3, ds_src=None) == INVALID
+    assert B(2, 2, 3, work=None) == INVALID
+    assert B(2, 2, 3, work=_p(0x1004)) == INVALID        # the edge records are 8-byte pairs
     assert B(2, 2, 1 << 31) == TOO_LARGE
     assert B(-1, 2, 0) == INVALID
 

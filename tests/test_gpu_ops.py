@@ -7,8 +7,8 @@ import pytest
 import oracle
 from paper_2103_00959_amd import synth
 
-from gpu_util import (TOL_ALPHA, TOL_F32, dev, features, graph_to_dev, say, scaled_error, to_f64,
-                      tol_for)
+from gpu_util import (FLT_MIN, TOL_ALPHA, TOL_F32, alpha_bound_scale, alpha_close, dev, features,
+                      graph_to_dev, say, scaled_error, to_f64, tol_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -424,38 +424,6 @@ def _scores(n_rows, n_cols, H, seed, scale=1.0):
     return sd, ss
 
 
-FLT_MIN = float(np.finfo(np.float32).tiny)
-
-
-def _alpha_close(a_gpu, a_ref, scale=None):
-    """Relative error over every weight whose reference is a normal fp32 value, divided by
-    `scale` (per weight, default 1): the result must be <= TOL_ALPHA.  Below FLT_MIN (weights
-    that underflow in fp32) the absolute error must stay under FLT_MIN."""
-    a = to_f64(a_gpu).reshape(a_ref.shape)
-    if a_ref.size == 0:
-        return 0.0
-    normal = a_ref >= FLT_MIN
-    assert np.all(np.abs(a[~normal] - a_ref[~normal]) <= FLT_MIN)
-    rel = np.abs(a - a_ref) / np.where(normal, a_ref, 1.0)
-    if scale is not None:
-        rel = rel / scale
-    return float(np.max(rel[normal])) if normal.any() else 0.0
-
-
-def _alpha_bound_scale(g, sd, ss, slope=0.2):
-    """The alpha tolerance of the score rounding, as a factor on TOL_ALPHA per weight:
-    (1e-5 + 2^-23 max_{k' in row} |e_k'|) / 1e-5.  The kernels score an edge in fp32
-    (e = LeakyReLU(s_dst + s_src) rounded once), which moves each weight by at most
-    2^-24 (|e_k| + max |e_k'|) relative; the exponential itself is evaluated to a few units
-    in the last place.  Scores from the fp64 inputs, per head."""
-    rows = np.repeat(np.arange(g.n_rows), np.diff(g.rowptr))
-    t = sd[rows].astype(np.float64) + ss[g.col].astype(np.float64)
-    e = np.where(t > 0, t, slope * t)
-    emax = np.zeros((g.n_rows, sd.shape[1]))
-    np.maximum.at(emax, rows, np.abs(e))
-    return (TOL_ALPHA + 2.0 ** -23 * emax[rows]) / TOL_ALPHA
-
-
 @pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1"])
 @pytest.mark.parametrize("H", [1, 3, 4, 8, 64])
 def test_sddmm_edge_softmax(cg, kind, H):
@@ -468,7 +436,7 @@ def test_sddmm_edge_softmax(cg, kind, H):
         plan = _make_plan(cg, rp, g.nnz, spec, 1, max_heads=H)
         try:
             a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
-            err = _alpha_close(a, a_ref)
+            err = alpha_close(a, a_ref)
             assert err <= TOL_ALPHA, (kind, H, spec, err)
         finally:
             if plan is not None:
@@ -490,7 +458,7 @@ def test_softmax_degree_one_rows_exact_and_wide_scores(cg):
     np.add.at(sums, rows, a_h.astype(np.float64))
     assert np.max(np.abs(sums[d > 0] - 1.0)) <= 1e-5
     a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
-    assert _alpha_close(a, a_ref, _alpha_bound_scale(g, sd, ss)) <= TOL_ALPHA
+    assert alpha_close(a, a_ref, alpha_bound_scale(g.rowptr, g.col, sd, ss)) <= TOL_ALPHA
 
 
 @pytest.mark.parametrize("scale", [8.0, 24.0])
@@ -499,7 +467,7 @@ def test_alpha_wide_scores_every_plan(cg, scale, D, xk):
     """Scores N(0, scale^2): |e - m| reaches the range where the weights approach FLT_MIN
     (scale 24), so the exponent's conditioning is exercised; every weight whose reference is a
     normal fp32 value is compared at 1e-5 plus the rounding of its fp32 score (see
-    _alpha_bound_scale), for the standalone softmax and the fused aggregation's alpha, with
+    alpha_bound_scale), for the standalone softmax and the fused aggregation's alpha, with
     plain, neighbour-group and column-sliced plans (sliced and split rows take the separate
     rescoring pass)."""
     g = _graph("hubs", seed=9)
@@ -507,7 +475,7 @@ def test_alpha_wide_scores_every_plan(cg, scale, D, xk):
     H = 4
     sd, ss = _scores(g.n_rows, g.n_cols, H, 79, scale=scale)
     a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
-    bound = _alpha_bound_scale(g, sd, ss)
+    bound = alpha_bound_scale(g.rowptr, g.col, sd, ss)
     say(f"wide scores x{scale}: smallest normal reference weight {a_ref[a_ref >= FLT_MIN].min():.3e}, "
         f"{int((a_ref < FLT_MIN).sum())} below FLT_MIN, bound up to {bound.max() * TOL_ALPHA:.2e}")
     _, _, xd = features((g.n_cols, H, D), 61, xk)      # D = 64 bf16: the distributed-softmax kernel
@@ -522,10 +490,10 @@ def test_alpha_wide_scores_every_plan(cg, scale, D, xk):
                            **(dict(col=cl, n_cols=g.n_cols, slice_min=16) if sliced else {}))
         try:
             a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
-            err = _alpha_close(a, a_ref, bound)
+            err = alpha_close(a, a_ref, bound)
             assert err <= TOL_ALPHA, (scale, spec, err)
             _, a2 = cg.gat_aggregate(rp, cl, dev(sd), dev(ss), xd, 0.2, plan=plan, return_alpha=True)
-            err2 = _alpha_close(a2, a_ref, bound)
+            err2 = alpha_close(a2, a_ref, bound)
             assert err2 <= TOL_ALPHA, (scale, spec, err2)
             say(f"  plan {spec}: softmax {err:.2e}, gat alpha {err2:.2e}")
         finally:
@@ -554,7 +522,7 @@ def test_gat_aggregate(cg, kind, H, D, xk, yk):
                                     return_alpha=True)
             err = scaled_error(Y.reshape(g.n_rows, H * D), Yr, Ar)
             assert err <= tol_for(xk, yk), (kind, H, D, spec, err)
-            assert _alpha_close(a, a_ref) <= TOL_ALPHA, (kind, H, D, spec)
+            assert alpha_close(a, a_ref) <= TOL_ALPHA, (kind, H, D, spec)
             Y2 = cg.gat_aggregate(rp, cl, dev(sd), dev(ss), xd, 0.2, plan=plan, out_dtype=out_dtype)
             assert torch.equal(Y2, Y)                        # alpha_out does not change Y
         finally:
@@ -624,13 +592,19 @@ def _bwd_inputs(g, H, D, xk, seed, softmax_alpha=True):
     if softmax_alpha:
         alpha = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2).astype(np.float32)
     else:
-        alpha = np.random.default_rng(seed).random((g.nnz, H)).astype(np.float32)
+        alpha = np.random.default_rng(seed).uniform(-1.0, 1.0, (g.nnz, H)).astype(np.float32)
     xh, xc, xd = features((g.n_cols, H, D), seed + 1, xk)
     gh, gc, gd = features((g.n_rows, H, D), seed + 2, xk)
     return sd, ss, alpha, (xh, xc, xd), (gh, gc, gd)
 
 
-def _check_bwd(out, ref, what):
+def _check_bwd(out, ref, what, alpha=None):
+    import torch
+    if alpha is not None:
+        # the edge records end as the pairs (alpha, dscore), bit for bit
+        rec = out["edge_work"]
+        assert torch.equal(rec[..., 0].reshape(-1), dev(alpha).reshape(-1)), (what, "edge_work alpha")
+        assert torch.equal(rec[..., 1].reshape(-1), out["dscore"].reshape(-1)), (what, "edge_work dscore")
     for k in ("dalpha", "dscore", "ds_dst", "ds_src"):
         err = scaled_error(out[k], ref[k], ref[k + "_abs"])
         assert err <= TOL_F32, (what, k, err)
@@ -645,7 +619,8 @@ PLAN_PAIRS = [(None, None), (("auto", 0), ("auto", 0)), (("row_split", 0), ("row
 @pytest.mark.parametrize("kind", ["small", "dups", "hubs", "cfg1"])
 @pytest.mark.parametrize("H,D,xk,dxk", [(4, 64, "bf16", "bf16"), (8, 16, "f32", "f32"), (3, 5, "f32", "f32"),
                                         (1, 1, "f32", "f32"), (2, 40, "f16", "f32"), (4, 64, "bf16", "f32"),
-                                        (16, 80, "f32", "f32")])
+                                        (16, 80, "f32", "f32"), (2, 32, "f32", "bf16"), (2, 64, "f16", "f16"),
+                                        (2, 64, "f32", "f32")])
 def test_gat_backward(cg, kind, H, D, xk, dxk):
     import torch
     g = _graph(kind)
@@ -655,7 +630,7 @@ def test_gat_backward(cg, kind, H, D, xk, dxk):
     colptr, row_t, _, perm = oracle.csr_to_csc(g.rowptr, g.col, None, g.n_cols)
     ref = oracle.gat_backward(g.rowptr, g.col, sd, ss, alpha, xh.reshape(g.n_cols, H * D),
                               gh.reshape(g.n_rows, H * D), H, D, slope=0.2, x_dtype=xc, dy_dtype=gc)
-    dx_dtype = {"f32": torch.float32, "bf16": torch.bfloat16}[dxk]
+    dx_dtype = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dxk]
     cp_d, rt_d, pm_d = dev(colptr), dev(row_t), dev(perm)
     for spec, spec_t in PLAN_PAIRS:
         plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
@@ -663,7 +638,7 @@ def test_gat_backward(cg, kind, H, D, xk, dxk):
         try:
             out = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
                                   plan=plan, plan_t=plan_t, dx_dtype=dx_dtype)
-            _check_bwd(out, ref, (kind, H, D, spec, spec_t))
+            _check_bwd(out, ref, (kind, H, D, spec, spec_t), alpha)
         finally:
             for p in (plan, plan_t):
                 if p is not None:
@@ -671,8 +646,8 @@ def test_gat_backward(cg, kind, H, D, xk, dxk):
 
 
 def test_gat_backward_unnormalized_weights_and_repeat(cg):
-    """Any fp32 weights (not only softmax outputs), two calls in a row on the
-    same plans give the same bits (the plan workspaces are reused)."""
+    """Any fp32 weights (not only softmax outputs: here of either sign), two calls in a row
+    on the same plans give the same bits (the plan workspaces are reused)."""
     import torch
     g = _graph("hubs", seed=14)
     H, D = 4, 64
@@ -687,7 +662,7 @@ def test_gat_backward_unnormalized_weights_and_repeat(cg):
     try:
         a = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
                             plan=plan, plan_t=plan_t, dx_dtype=torch.float32)
-        _check_bwd(a, ref, "unnormalized")
+        _check_bwd(a, ref, "unnormalized", alpha)
         b = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2,
                             plan=plan, plan_t=plan_t, dx_dtype=torch.float32)
         for k in a:
