@@ -72,6 +72,13 @@ def parse():
                     help="FETCH_DIR WRITE_DIR PROBE_JSON [REQ_DIR]: write profiles/<workload>_hbm_traffic.json "
                          "and _hbm_counters.txt from a FETCH_SIZE and a WRITE_SIZE rocprofv3 run of "
                          "--counter-probe (and a run of the raw read-request counters), then exit")
+    ap.add_argument("--summarize-workloads", nargs=3, metavar="PATH",
+                    help="FETCH_DIR WRITE_DIR PROBE_JSON: write profiles/workloads_1_to_4_hbm_traffic.json "
+                         "and _hbm_counters.txt from a FETCH_SIZE and a WRITE_SIZE rocprofv3 run of "
+                         "--workloads-probe, then exit")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_DIR", "COMMAND"),
+                    help="write profiles/<workload>_kernel_stats.txt from the kernel statistics of a "
+                         "rocprofv3 --kernel-trace --stats run (COMMAND: the command that made it), then exit")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the steps, copy a buffer of this many MiB (counter calibration)")
     ap.add_argument("--workloads", action="store_true",
@@ -881,6 +888,59 @@ def write_counter_profile(args, fetch_dir, write_dir, probe_json, req_dir=None):
     print("\n".join(lines))
 
 
+def write_workload_profile(fetch_dir, write_dir, probe_json, out_dir=None):
+    """profiles/workloads_1_to_4_hbm_traffic.json (the record the workload lines fall back on)
+    and a readable .txt from one FETCH_SIZE and one WRITE_SIZE run of --workloads-probe."""
+    keys = json.load(open(probe_json))["keys"]
+    ops = summarize_workloads_probe(fetch_dir, write_dir, keys)
+    cmd = ("cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {c} --kernel-trace -d DIR -o run --output-format csv -- "
+           "python3 bench.py --workloads-probe PROBE_JSON")
+    rec = {"source_sha16": workloads_source_sha(), "ops": ops,
+           "commands": {"fetch": cmd.format(c="FETCH_SIZE"), "write": cmd.format(c="WRITE_SIZE"),
+                        "summary": "python3 bench.py --summarize-workloads FETCH_DIR WRITE_DIR PROBE_JSON"}}
+    base = os.path.join(out_dir or os.path.join(HERE, "profiles"), "workloads_1_to_4_hbm")
+    json.dump(rec, open(base + "_traffic.json", "w"), indent=1)
+    lines = ["# HBM bytes of one cold call of each workloads-mode operator (workloads 1-4, their own dtypes),",
+             "# one MI355X: the dispatches between the op's two marker kernels, each counter scaled by what it",
+             "# reads for the run's closing plain 1 GiB device copy",
+             f"# FETCH_SIZE: {rec['commands']['fetch']}",
+             f"# WRITE_SIZE: {rec['commands']['write']}",
+             f"# summary: {rec['commands']['summary']}",
+             f"# workload-op sources sha256[:16] {rec['source_sha16']} (the record is ignored once they change)",
+             f"{'workload/op':48s} {'fetch_GB':>9s} {'write_GB':>9s} {'fetch_x':>8s} {'write_x':>8s}"]
+    for k, v in ops.items():
+        lines.append(f"{k:48s} {v['fetch_bytes'] / 1e9:9.4f} {v['write_bytes'] / 1e9:9.4f} "
+                     f"{v['fetch_scale']:8.3f} {v['write_scale']:8.3f}")
+    open(base + "_counters.txt", "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def write_stats_profile(args, stats_dir, command, out_dir=None):
+    """profiles/<workload>_kernel_stats.txt from run_kernel_stats.csv of a rocprofv3
+    --kernel-trace --stats run: calls, average and total time per kernel."""
+    import csv
+    import glob
+    from paper_2103_00959_amd import synth
+    cfg = synth.CONFIGS[args.config]
+    files = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {stats_dir}")
+    rows = list(csv.DictReader(open(files[0])))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = [f"# Kernel time of {cfg['name']}, one MI355X (rocprofv3 kernel statistics; durations in ms)",
+             f"# command: {command}",
+             f"# library sources sha256[:16] {library_source_sha()}",
+             f"{'kernel':90s} {'calls':>6s} {'avg_ms':>9s} {'min_ms':>9s} {'max_ms':>9s} {'total_ms':>10s} {'pct':>6s}"]
+    for r in rows:
+        name = r["Name"].replace("cogdl::(anonymous namespace)::", "").replace("cogdl::", "")
+        lines.append(f"{name[:90]:90s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e6:9.4f} "
+                     f"{float(r['MinNs']) / 1e6:9.4f} {float(r['MaxNs']) / 1e6:9.4f} "
+                     f"{float(r['TotalDurationNs']) / 1e6:10.3f} {float(r['Percentage']):6.2f}")
+    out = os.path.join(out_dir or os.path.join(HERE, "profiles"), f"{cfg['name']}_kernel_stats.txt")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines[:30]))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -897,6 +957,12 @@ def main():
             if wl_hbm is None:
                 log(f"live workload counters unavailable ({why})")
         run_workloads(reps=args.reps, warm_reps=args.warm_reps, cpu=not args.no_cpu_baseline, hbm=wl_hbm)
+        return
+    if args.summarize_workloads:
+        write_workload_profile(*args.summarize_workloads)
+        return
+    if args.summarize_stats:
+        write_stats_profile(args, *args.summarize_stats)
         return
     if args.summarize_counters:
         if len(args.summarize_counters) not in (3, 4):

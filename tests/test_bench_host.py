@@ -143,3 +143,41 @@ def test_workloads_probe_summary(tmp_path):
     import pytest
     with pytest.raises(RuntimeError):
         bench.summarize_workloads_probe(str(tmp_path / "f"), str(tmp_path / "w"), keys[:2])
+
+
+def test_workload_profile_writer(tmp_path):
+    """--summarize-workloads: the per-op record the workload lines fall back on, stamped with the
+    sources' hash, read back by recorded_workload_traffic."""
+    M = "void at::native::bitwise_not_kernel"
+    kib = 1024.0
+    copy_raw = bench.CALIB_BYTES / 2 / kib
+    fetch = [(M, 0), ("k1", 10.0), (M, 0), (M, 0), ("copy", copy_raw), (M, 0)]
+    _write_probe_csv(tmp_path / "f", "FETCH_SIZE", fetch)
+    _write_probe_csv(tmp_path / "w", "WRITE_SIZE", [(n, v) for n, v in fetch])
+    probe = tmp_path / "probe.json"
+    probe.write_text(json.dumps({"keys": ["wl/spmm", "calib_copy"]}))
+    out = tmp_path / "profiles"
+    out.mkdir()
+    bench.write_workload_profile(str(tmp_path / "f"), str(tmp_path / "w"), str(probe), str(out))
+    ops = bench.recorded_workload_traffic(str(out))
+    assert ops["wl/spmm"]["fetch_bytes"] == 10.0 * kib * 2
+    assert (out / "workloads_1_to_4_hbm_counters.txt").read_text().count("wl/spmm") == 1
+
+
+def test_stats_profile_writer(tmp_path):
+    """--summarize-stats: kernels ordered by total time, durations in ms, the command recorded."""
+    import argparse
+    d = tmp_path / "stats"
+    d.mkdir()
+    (d / "run_kernel_stats.csv").write_text(
+        '"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+        '"void cogdl::k_a<int>(cogdl::X)",2,3000000,1500000.0,25.0,1000000,2000000,1.0\n'
+        '"void cogdl::k_b<int>(cogdl::X)",3,9000000,3000000.0,75.0,2000000,4000000,1.0\n')
+    out = tmp_path / "profiles"
+    out.mkdir()
+    bench.write_stats_profile(argparse.Namespace(config=5), str(d), "the command", str(out))
+    txt = (out / "skewed_rmat_2400000_hubs_kernel_stats.txt").read_text().splitlines()
+    assert txt[1] == "# command: the command"
+    body = [l for l in txt if not l.startswith("#")][1:]
+    assert body[0].startswith("void k_b<int>") and "3.0000" in body[0]
+    assert body[1].startswith("void k_a<int>")
