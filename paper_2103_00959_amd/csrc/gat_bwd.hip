@@ -55,6 +55,7 @@ struct BwdArgs {
     float *dalpha;              // [nnz][H]
     float *dscore;              // [nnz][H]
     float2 *rec;                // [nnz][H] pairs (alpha, f alpha), then (alpha, dscore)
+    int32_t park_cap;           // LDS floats per sub-group for whole rows' parked u (0: none)
     float *ds_dst;              // [n_rows][H]
     float *gstats;              // split rows: per partial slot c[max_heads], sum[max_heads]
     int32_t sstride;            // 2 * max_heads
@@ -98,12 +99,19 @@ __device__ __forceinline__ float finish_edge(const BwdArgs &a, int64_t i, float 
     return g;
 }
 
-// Park the pair of edge-head i: the record (whole row) or u alone (split row).
-__device__ __forceinline__ void park_edge(const BwdArgs &a, int64_t i, bool split, float al, float u)
+// Park the pair of edge-head i: the record (whole row) or u alone (split row);
+// a whole row that fits its sub-group's LDS share parks u there at `li` (the
+// fix-up reads alpha back from its input, still in the cache).
+__device__ __forceinline__ void park_edge(const BwdArgs &a, int64_t i, bool split, float al, float u,
+                                          float *lds, int li)
 {
     if (split) a.dscore[i] = u;
+    else if (lds) lds[li] = u;
     else a.rec[i] = make_float2(al, u);
 }
+
+// LDS floats of a rows workgroup for whole rows' parked u, shared by its sub-groups.
+constexpr int kRowParkFloats = 4096;
 
 // Pass 1, feature-parallel: one S-lane sub-group per unit, lane = VEC
 // consecutive features, head h on lanes [h L, (h + 1) L).  Requires one
@@ -143,6 +151,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
     const RowGather<TX, VEC, BUF> X(a.X, a.x_bytes);
     const TX *__restrict__ P = static_cast<const TX *>(a.P);
     const int32_t *__restrict__ col = a.col;
+    extern __shared__ float row_park[];
+    float *const park_mine = row_park + (threadIdx.x >> log2S) * a.park_cap;
 
     int64_t u = walk.first;
     if (u >= hi) return;
@@ -153,6 +163,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
         const int64_t un = u + stride;
         const int4 dn = fetch_bwd_unit(a, un, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        // a whole row whose u fit this sub-group's LDS share parks them there
+        float *const lds = (!DOT && part < 0 && (end - beg) * H <= a.park_cap) ? park_mine : nullptr;
         float p[PACKED ? 1 : VEC];
         uint4 pw = make_uint4(0u, 0u, 0u, 0u);
         if constexpr (PACKED) {
@@ -227,7 +239,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                             const float al1 = a.alpha[k * H + h];
                             const float ss1 = a.s_src[(int64_t)cme * H + h];
                             c += al1 * s;
-                            park_edge(a, k * H + h, part >= 0, al1, park_value(sd + ss1, a.slope, al1));
+                            park_edge(a, k * H + h, part >= 0, al1, park_value(sd + ss1, a.slope, al1), lds,
+                                      (int)(k - beg) * H + h);
                         }
                     }
                     continue;
@@ -243,7 +256,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                         a.dalpha[k * H + h] = pd[t];
                         if constexpr (!DOT) {
                             c += al[t] * pd[t];
-                            park_edge(a, k * H + h, part >= 0, al[t], park_value(sd + ss[t], a.slope, al[t]));
+                            park_edge(a, k * H + h, part >= 0, al[t], park_value(sd + ss[t], a.slope, al[t]), lds,
+                                      (int)(k - beg) * H + h);
                         }
                     }
                 }
@@ -269,9 +283,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
-                            const int64_t k = (int64_t)beg + (o < end - beg ? o : o0);
+                            const int oc = o < end - beg ? o : o0;
+                            const int64_t k = (int64_t)beg + oc;
                             da[r] = a.dalpha[k * H + h];
-                            uv[r] = a.rec[k * H + h];
+                            if (lds) uv[r] = make_float2(a.alpha[k * H + h], lds[oc * H + h]);
+                            else uv[r] = a.rec[k * H + h];
                         }
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
@@ -344,7 +360,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
                     const float al = a.alpha[(int64_t)k * H + h];
                     c += al * s;
                     park_edge(a, (int64_t)k * H + h, part >= 0, al,
-                              park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al));
+                              park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al), nullptr, 0);
                 }
             }
         }
@@ -517,13 +533,16 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
         a.log2L = log2i(L);
         BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec, L >= 8);
         const int64_t upb = kBlock >> m.log2S;
+        a.park_cap = DOT ? 0 : kRowParkFloats / (int)upb;
+        const size_t shm = DOT ? 0 : sizeof(float) * kRowParkFloats;
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
         blocks = list_grid(blocks, a.lists);
-        COGDL_LAUNCH(name, k, (unsigned)blocks, kBlock, stream, a);
+        COGDL_LAUNCH_SHM(name, k, (unsigned)blocks, kBlock, shm, stream, a);
     } else {
         BwdKernel k = pick_any<DOT>(xdt, pdt);
+        a.park_cap = 0;
         int64_t blocks = (units + (kBlock / kWave) - 1) / (kBlock / kWave);
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
