@@ -438,7 +438,10 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
         static_cast<char *>(scan_ws) + ((scan_workspace_bytes(hist_n + 1) + 255) & ~size_t(255)));
 
     // as few passes as digits of at most 8 bits allow, the bits spread evenly
-    // over them (longer runs per digit than a short last pass gives)
+    // over them (longer runs per digit than a short last pass gives), a
+    // remainder going to the last passes: a narrower digit gives longer runs,
+    // which matters most in the first pass (it also generates the CSR rows)
+    // and least in the last (the high bits of power-law keys take few values)
     int passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
     if (passes < 1) passes = 1;
     const uint32_t *src_k = keys_in;
@@ -447,7 +450,7 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, ui
     int shift = 0;
     for (int p = 0; p < passes; ++p) {
         const bool last = (p == passes - 1);
-        int dbits = (bits - shift + (passes - p) - 1) / (passes - p);
+        int dbits = (bits - shift) / (passes - p);
         if (dbits < 1) dbits = 1;
         uint32_t *dst_k = last ? keys_out : ping_keys + (p & 1) * n;
         uint32_t *dst_v = last ? vals_out : ping_vals + (p & 1) * n;
