@@ -224,6 +224,27 @@ def test_act_codec_bit_exact(cg, bits, n, F, G, at):
                           oracle.round_to(y_ref.astype(np.float64), oracle.BF16))
 
 
+@pytest.mark.parametrize("case", ["flat_index_whole", "flat_index_ragged", "clamp_whole", "clamp_ragged"])
+def test_act_codec_constructed_cases(cg, case):
+    """The hand-constructed codec inputs (each code on a threshold of its own uniform; the clamp
+    where 255 + u rounds to 256) give the expected codes on both kernel paths (rows of whole
+    16-byte aligned groups, ragged rows), bit for bit equal to the oracle's."""
+    from codec_cases import clamp_case, flat_index_case
+    if case.startswith("flat"):
+        seed, bits = 0x5EED0001F00D, 1
+        x, want = flat_index_case(seed, 3, 256 if case.endswith("whole") else 200)
+    else:
+        seed, bits = 11, 8
+        x, _, want = clamp_case(seed, 0 if case.endswith("whole") else 8)
+    n, F = x.shape
+    codes, stats = cg.act_compress(dev(x), bits, 64, seed)
+    c_ref, s_ref = oracle.act_compress(x, bits, 64, seed)
+    assert np.array_equal(codes.cpu().numpy().view(np.uint64), c_ref)
+    assert np.array_equal(stats.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+    y = cg.act_decompress(codes, stats, n, F, bits, 64)
+    assert np.array_equal(y.cpu().numpy(), want)
+
+
 def test_act_codec_round_trip_on_aggregated_activations(cg):
     """Compress the GCN layer-1 activations of a graph at 2, 3, 4 bits: decoded
     values within one step of the originals, memory ratio as designed."""

@@ -945,11 +945,7 @@ def test_codec_decoder_rounds_once():
     assert np.all(y[4:] == np.float32(-3.0))
 
 
-def _codec_uniform(seed, e):
-    """u of flat index e: word e mod 4 of Philox4x32-10 (pinned by its known answers) at counter
-    (e / 4 mod 2^32, e / 2^34, 0, 0), key (seed mod 2^32, seed / 2^32), top 24 bits times 2^-24."""
-    out = oracle.philox4x32_10([(e // 4) & 0xFFFFFFFF, e >> 34, 0, 0], [seed & 0xFFFFFFFF, seed >> 32])
-    return Fraction(int(out[e % 4]) >> 8, 1 << 24)
+from codec_cases import codec_uniform as _codec_uniform  # noqa: E402
 
 
 def test_codec_quantizer_rounds_once():
@@ -990,54 +986,33 @@ def test_codec_quantizer_rounds_once():
     raise AssertionError("no constructed case found")
 
 
-def test_codec_codes_follow_the_uniform_of_their_flat_index():
-    """Each code takes the uniform of its own flat index e = i F + f.  Constructed case (1 bit,
-    every group holding a 0 and a 1, so m = 0, s = 1 and the code is floor(fl(x + u))): a probe
-    at x = 1 - u_e (exact in fp32: u_e is a multiple of 2^-24) sums to exactly 1, code 1; a probe
-    one step of 2^-24 lower sums to 1 - 2^-24, code 0.  Any other word, counter, index or
-    resolution of u moves some probe across 1.  Rows of 200 features: three full groups and a
-    ragged one, all four words of a Philox block."""
-    seed, n, F, G = 0x5EED0001F00D, 3, 200, 64
-    x = np.zeros((n, F), np.float32)
-    want = np.zeros((n, F))
-    for i in range(n):
-        for f in range(F):
-            j = f % G
-            if j == 0:
-                continue                                   # the group's minimum 0: code 0
-            if j == 1:
-                x[i, f], want[i, f] = 1.0, 1.0             # its maximum 1: code 1
-                continue
-            e = i * F + f
-            u = _codec_uniform(seed, e)
-            v = 1 - u if (e * 7 + i) % 3 else 1 - u - Fraction(1, 1 << 24)
-            assert Fraction(float(np.float32(float(v)))) == v      # exact in fp32
-            x[i, f] = float(v)
-            want[i, f] = 1.0 if v + u == 1 else 0.0
+@pytest.mark.parametrize("F", [200, 256])
+def test_codec_codes_follow_the_uniform_of_their_flat_index(F):
+    """Each code takes the uniform of its own flat index e = i F + f (constructed in
+    codec_cases.flat_index_case): any other word, counter, index or resolution of u moves some
+    probe across 1.  Three rows of whole groups or of three groups and a ragged one, all four
+    words of a Philox block."""
+    from codec_cases import flat_index_case
+    n, G, seed = 3, 64, 0x5EED0001F00D
+    x, want = flat_index_case(seed, n, F, G)
     codes, stats = oracle.act_compress(x, 1, G, seed=seed)
     assert np.all(stats[0::2] == 0.0) and np.all(stats[1::2] == 1.0)
-    y = oracle.act_decompress(codes, stats, n, F, 1, G)
-    assert np.array_equal(y, want.astype(np.float32))
+    assert np.array_equal(oracle.act_decompress(codes, stats, n, F, 1, G), want)
     assert 0 < want.sum() < want.size
 
 
-def test_codec_code_never_exceeds_the_top_level():
-    """The code is clamped to 2^b - 1.  Constructed case (8 bits, a group holding 0 and 255, so
-    s = 1): at an element whose uniform is at least 1 - 2^-17, 255 + u rounds to 256 in fp32 (the
-    fp32 step between 128 and 256 is 2^-16), and the code must still be 255 (as bit planes, 256
-    would read back as 0)."""
+@pytest.mark.parametrize("tail", [0, 8])
+def test_codec_code_never_exceeds_the_top_level(tail):
+    """The code is clamped to 2^b - 1 (constructed in codec_cases.clamp_case, where 255 + u
+    rounds to 256; as bit planes, 256 would read back as 0)."""
+    from codec_cases import clamp_case
     seed = 11
-    top = Fraction((1 << 24) - (1 << 7), 1 << 24)
-    e = next(e for e in range(1 << 22) if _codec_uniform(seed, e) >= top)
-    F = (e // 64 + 1) * 64
-    x = np.zeros((1, F), np.float32)
-    x[0, e] = 255.0
+    x, e, want = clamp_case(seed, tail)
+    F = x.shape[1]
     codes, stats = oracle.act_compress(x, 8, 64, seed=seed)
     g = e // 64
     assert float(stats[2 * g]) == 0.0 and float(stats[2 * g + 1]) == 1.0
-    assert float(np.float32(255.0) + np.float32(float(_codec_uniform(seed, e)))) == 256.0
-    y = oracle.act_decompress(codes, stats, 1, F, 8, 64)
-    assert float(y[0, e]) == 255.0
+    assert np.array_equal(oracle.act_decompress(codes, stats, 1, F, 8, 64), want)
 
 
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
