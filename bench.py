@@ -1291,6 +1291,13 @@ def main():
     ms_bwd, k_bwd = time_op_kernels(lambda: cg.gat_backward(
         rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha_buf, Xg, dYg, 0.2, plan=plan,
         plan_t=plan_t, out=bwd_out))
+    # the same with only a layer's gradients (ds_dst, ds_src, dX; dscore stays in the records)
+    lay_out = {k: bwd_out[k] for k in ("dX", "ds_dst", "ds_src", "edge_work")}
+    lay_out.update(dalpha=None, dscore=None)
+    ms_bwd_l, k_bwd_l = time_op_kernels(lambda: cg.gat_backward(
+        rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha_buf, Xg, dYg, 0.2, plan=plan,
+        plan_t=plan_t, out=lay_out))
+    del lay_out
     dot_out = torch.empty((E, H), dtype=torch.float32, device=dev)
     ms_dot, k_dot = time_op_kernels(lambda: cg.sddmm_dot(rowptr, col, dYg, Xg, plan=plan, out=dot_out))
     b_dot = 4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * E * H
@@ -1303,6 +1310,7 @@ def main():
     b_bwd_cols = (4 * (M + 1) + 4 * E + 4 * E + E * H * D * 2 + 4 * E * H + 4 * E * H
                   + M * H * D * 2 + 4 * M * H)
     b_bwd = b_bwd_rows + b_bwd_cols
+    b_bwd_l = b_bwd - 8 * E * H                    # no dalpha, no dscore written
 
     # activation compression of the layer output Y (N x F bf16) at 2, 3, 4 bits, groups of F
     codec = {}
@@ -1350,6 +1358,10 @@ def main():
                              cols_pass_GBps=b_bwd_cols / ((k_bwd.get("gat_bwd_cols", 0)
                                                            + k_bwd.get("gat_bwd_cols_tiny", 0)) * 1e-3) / 1e9
                              if k_bwd.get("gat_bwd_cols") else None),
+        "gat_backward_layer_gradients": dict(
+            ms=ms_bwd_l, algorithmic_GB=b_bwd_l / 1e9, eff_GBps=b_bwd_l / (ms_bwd_l * 1e-3) / 1e9,
+            edges_per_s=E / (ms_bwd_l * 1e-3), kernels_ms=k_bwd_l,
+            note="dalpha and dscore not written: ds_dst, ds_src, dX and the (alpha, dscore) records"),
         "act_codec": codec,
         "sddmm_dot": dict(ms=ms_dot, algorithmic_GB=b_dot / 1e9,
                           eff_GBps=b_dot / (ms_dot * 1e-3) / 1e9, edges_per_s=E / (ms_dot * 1e-3)),
@@ -1398,7 +1410,9 @@ def main():
         f"gspmm mean {ms_mean:.3f} ms, max+arg {ms_max:.3f} ms, sddmm_dot {ms_dot:.3f} ms, "
         f"codec (compress/decompress) {codec_txt} ms, "
         f"gat backward {ms_bwd:.3f} ms "
-        f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd.items())})")
+        f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd.items())}), "
+        f"layer gradients only {ms_bwd_l:.3f} ms "
+        f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd_l.items())})")
 
     inference = None if args.no_inference else run_inference(cg, synth, dev, time_op_kernels,
                                                              sliced=not args.plain_plans)

@@ -450,7 +450,9 @@ cogdl_status cogdl_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const 
  * colptr, row_t, perm: the CSC of the same graph from cogdl_csr_to_csc.
  * plan: NULL or a plan on rowptr with max_heads >= H; plan_t: NULL or a plan
  * on colptr with max_feat >= H*D and max_heads >= H.  dalpha and dscore are
- * nnz x H fp32 outputs.  edge_work: caller-owned device scratch of nnz x H x 2
+ * nnz x H fp32 outputs, each of which may be NULL (not written: a layer's
+ * backward needs only ds_dst, ds_src and dX, and dscore is also left in
+ * edge_work).  edge_work: caller-owned device scratch of nnz x H x 2
  * floats, 8-byte aligned (NULL allowed only when nnz == 0): the first pass
  * leaves there, per edge k (CSR order) and head h, the pair
  * (alpha[k,h], dscore[k,h]) at floats 2(kH + h) and 2(kH + h) + 1, which the

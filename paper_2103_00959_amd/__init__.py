@@ -620,8 +620,9 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     """Gradients of gat_aggregate for dY = dL/dY.  X is [n_cols, H, D], dY [n_rows, H, D],
     alpha [nnz, H] the forward weights; (colptr, row_t, perm) the CSC from csr_to_csc.
     Returns dict(dX, dalpha, dscore, ds_dst, ds_src, edge_work); ``out`` may supply these
-    tensors.  edge_work (fp32, 2 nnz H) is the library's scratch between its two passes: it
-    ends holding the pair (alpha, dscore) of every edge and head."""
+    tensors, and ``out={"dalpha": None, "dscore": None}`` (either or both) leaves those
+    outputs out.  edge_work (fp32, 2 nnz H) is the library's scratch between its two passes:
+    it ends holding the pair (alpha, dscore) of every edge and head."""
     import torch
     n_rows, nnz = _graph(rowptr, col)
     n_cols, H, D = _dims(X, "X", 3)
@@ -641,7 +642,10 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     for k in o:
         if k not in sizes:
             raise CogdlError(f"unknown output {k!r}")
-        _numel(o[k], k, sizes[k])
+        if o[k] is None and k not in ("dalpha", "dscore"):
+            raise CogdlError(f"output {k!r} is required")
+        if o[k] is not None:
+            _numel(o[k], k, sizes[k])
     _plan_matches(plan, n_rows, nnz)
     _plan_matches(plan_t, n_cols, nnz, "plan_t")
     for t, name, dt in ((rowptr, "rowptr", torch.int32), (col, "col", torch.int32),
@@ -659,7 +663,8 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     o.setdefault("edge_work", torch.empty((nnz, H, 2), dtype=torch.float32, device=dev))
     _dev(o["dX"], "dX")
     for k in ("dalpha", "dscore", "ds_dst", "ds_src", "edge_work"):
-        _dev(o[k], k, torch.float32)
+        if o[k] is not None:
+            _dev(o[k], k, torch.float32)
     _check(lib().cogdl_gat_backward(
         n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(colptr), _ptr(row_t), _ptr(perm), H, D,
         _ptr(s_dst), _ptr(s_src), float(negative_slope), _ptr(alpha), _ptr(X), _dtype_code(X),

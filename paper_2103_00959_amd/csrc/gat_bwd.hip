@@ -77,11 +77,12 @@ __device__ __forceinline__ int4 fetch_bwd_unit(const BwdArgs &a, int64_t u, int6
 
 // The score gradient of edge k and head h is f * alpha * (dalpha - c), with f
 // the LeakyReLU slope at the pre-activation t and c the row's sum of alpha *
-// dalpha.  Pass 1 parks u = f * alpha (c is not known yet): beside alpha in
-// the edge record for a whole row, whose fix-up follows at once and finds the
-// record in the cache; in dscore for a neighbour group of a split row, whose
-// fix-up runs after the pass and reads alpha back from its input, so that the
-// record is written once, complete.  Once c is known, dscore = u (dalpha - c).
+// dalpha.  Pass 1 parks u = f * alpha and dalpha (c is not known yet); once
+// c is known, dscore = u (dalpha - c), alpha read back from its input.  The
+// dalpha and dscore outputs are optional: dalpha parks in its output when
+// there is one, and a split row's u in dscore when both are there; every
+// other pair goes to the edge's record (dalpha, u), which the fix-up then
+// overwrites with (alpha, dscore).
 __device__ __forceinline__ float park_value(float t, float slope, float al)
 {
     return (t > 0.f ? 1.f : slope) * al;
@@ -89,28 +90,50 @@ __device__ __forceinline__ float park_value(float t, float slope, float al)
 
 __device__ __forceinline__ float parked_grad(float u, float da, float c) { return u * (da - c); }
 
+// a + b rounded on its own: a sum of stored values is not fused with the
+// multiply that produced b (so every kernel variant forms ds_dst from exactly
+// the dscore values it writes).
+__device__ __forceinline__ float add_stored(float a, float b)
+{
+#pragma clang fp contract(off)
+    return a + b;
+}
+
 // Fix-up of one parked edge-head: dscore from alpha, the parked u and
-// dalpha, into both the output and the record.
+// dalpha, into the record and the output (SEP: there is one).
+template <bool SEP>
 __device__ __forceinline__ float finish_edge(const BwdArgs &a, int64_t i, float al, float u, float da, float c)
 {
     const float g = parked_grad(u, da, c);
-    a.dscore[i] = g;
+    if (SEP || a.dscore) a.dscore[i] = g;
     a.rec[i] = make_float2(al, g);
     return g;
 }
 
-// Park the pair of edge-head i: the record (whole row) or u alone (split row);
-// a whole row that fits its sub-group's LDS share parks u there at `li` (the
-// fix-up reads alpha back from its input, still in the cache).
-__device__ __forceinline__ void park_edge(const BwdArgs &a, int64_t i, bool split, float al, float u,
+// Park edge-head i until c is known.  SEP (dalpha and dscore both written):
+// dalpha is in its output, so u alone parks, in dscore for a split row, in
+// the LDS slot `li` for a whole row that fits its sub-group's share, else
+// beside alpha in the record.  Otherwise the pair (dalpha, u) parks, in LDS
+// (slots 2 li, 2 li + 1) or in the record.
+template <bool SEP>
+__device__ __forceinline__ void park_edge(const BwdArgs &a, int64_t i, bool split, float al, float da, float u,
                                           float *lds, int li)
 {
-    if (split) a.dscore[i] = u;
-    else if (lds) lds[li] = u;
-    else a.rec[i] = make_float2(al, u);
+    if constexpr (SEP) {
+        if (split) a.dscore[i] = u;
+        else if (lds) lds[li] = u;
+        else a.rec[i] = make_float2(al, u);
+    } else {
+        if (lds) {
+            lds[2 * li] = da;
+            lds[2 * li + 1] = u;
+        } else {
+            a.rec[i] = make_float2(da, u);
+        }
+    }
 }
 
-// LDS floats of a rows workgroup for whole rows' parked u, shared by its sub-groups.
+// LDS floats of a rows workgroup for whole rows' parked values, shared by its sub-groups.
 constexpr int kRowParkFloats = 4096;
 
 // Pass 1, feature-parallel: one S-lane sub-group per unit, lane = VEC
@@ -123,7 +146,7 @@ constexpr int kRowParkFloats = 4096;
 // reduce-scattered over aligned groups of 8 lanes, so lane q ends with the
 // group's sum for its own edge q mod 8 (7 exchanges for the batch instead of
 // 8 butterflies of log2 L), and L > 8 adds the groups by a butterfly.
-template <typename TX, int VEC, bool BUF, bool DOT, bool RS = false>
+template <typename TX, int VEC, bool BUF, bool DOT, bool RS = false, bool SEP = true>
 __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 {
     constexpr int U = VEC == 1 ? 16 : 8;
@@ -163,8 +186,10 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
         const int64_t un = u + stride;
         const int4 dn = fetch_bwd_unit(a, un, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
-        // a whole row whose u fit this sub-group's LDS share parks them there
-        float *const lds = (!DOT && part < 0 && (end - beg) * H <= a.park_cap) ? park_mine : nullptr;
+        // a whole row whose parked values fit this sub-group's LDS share parks them
+        // there (reduce-scatter kernels; the others keep their registers for the batch)
+        float *const lds =
+            (RS && !DOT && part < 0 && (end - beg) * H * (SEP ? 1 : 2) <= a.park_cap) ? park_mine : nullptr;
         float p[PACKED ? 1 : VEC];
         uint4 pw = make_uint4(0u, 0u, 0u, 0u);
         if constexpr (PACKED) {
@@ -234,13 +259,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                     // (a cross-lane read: every lane takes part)
                     const int cme = DOT ? 0 : lane_bcast(c_cur, gbase + j + t);
                     if (own) {
-                        a.dalpha[k * H + h] = s;
+                        if (DOT || SEP || a.dalpha) a.dalpha[k * H + h] = s;
                         if constexpr (!DOT) {
                             const float al1 = a.alpha[k * H + h];
                             const float ss1 = a.s_src[(int64_t)cme * H + h];
-                            c += al1 * s;
-                            park_edge(a, k * H + h, part >= 0, al1, park_value(sd + ss1, a.slope, al1), lds,
-                                      (int)(k - beg) * H + h);
+                            c = fmaf(al1, s, c);
+                            park_edge<SEP>(a, k * H + h, part >= 0, al1, s, park_value(sd + ss1, a.slope, al1),
+                                           lds, (int)(k - beg) * H + h);
                         }
                     }
                     continue;
@@ -253,11 +278,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 for (int t = 0; t < U; ++t) {
                     const int64_t k = k0 + j + t;
                     if (mine[t]) {
-                        a.dalpha[k * H + h] = pd[t];
+                        if (DOT || SEP || a.dalpha) a.dalpha[k * H + h] = pd[t];
                         if constexpr (!DOT) {
-                            c += al[t] * pd[t];
-                            park_edge(a, k * H + h, part >= 0, al[t], park_value(sd + ss[t], a.slope, al[t]), lds,
-                                      (int)(k - beg) * H + h);
+                            c = fmaf(al[t], pd[t], c);
+                            park_edge<SEP>(a, k * H + h, part >= 0, al[t], pd[t],
+                                           park_value(sd + ss[t], a.slope, al[t]), lds, (int)(k - beg) * H + h);
                         }
                     }
                 }
@@ -278,22 +303,34 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 float sdt = 0.f;
                 if (writer) {
                     for (int o0 = q; o0 < end - beg; o0 += R * M) {
-                        float da[R];
-                        float2 uv[R];
+                        float al[R], da[R], uv[R];
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
                             const int oc = o < end - beg ? o : o0;
-                            const int64_t k = (int64_t)beg + oc;
-                            da[r] = a.dalpha[k * H + h];
-                            if (lds) uv[r] = make_float2(a.alpha[k * H + h], lds[oc * H + h]);
-                            else uv[r] = a.rec[k * H + h];
+                            const int64_t i = ((int64_t)beg + oc) * H + h;
+                            const int li = oc * H + h;
+                            if constexpr (SEP) {
+                                // dalpha from its output; u from LDS (alpha from the input)
+                                // or the record (alpha, u)
+                                da[r] = a.dalpha[i];
+                                const float2 p = lds ? make_float2(a.alpha[i], lds[li]) : a.rec[i];
+                                al[r] = p.x;
+                                uv[r] = p.y;
+                            } else {
+                                // the pair (dalpha, u) from LDS or the record; alpha from the input
+                                const float2 p = lds ? make_float2(lds[2 * li], lds[2 * li + 1]) : a.rec[i];
+                                al[r] = a.alpha[i];
+                                da[r] = p.x;
+                                uv[r] = p.y;
+                            }
                         }
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
                             if (o < end - beg)
-                                sdt += finish_edge(a, ((int64_t)beg + o) * H + h, uv[r].x, uv[r].y, da[r], c);
+                                sdt = add_stored(sdt, finish_edge<SEP>(a, ((int64_t)beg + o) * H + h, al[r], uv[r],
+                                                                        da[r], c));
                         }
                     }
                 }
@@ -340,6 +377,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
     const int64_t hi = walk.end;
     const TX *__restrict__ X = static_cast<const TX *>(a.X);
     const TP *__restrict__ P = static_cast<const TP *>(a.P);
+    const bool sep = a.dalpha && a.dscore;
     for (int64_t u = walk.first; u < hi; u += walk.step) {
         const int4 d = fetch_bwd_unit(a, u, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
@@ -355,12 +393,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
                     load_vec<TX, 1>(X, (int64_t)j * a.W + (int64_t)h * a.D + e, xv);
                     s = fmaf(pv[0], xv[0], s);
                 }
-                a.dalpha[(int64_t)k * H + h] = s;
+                if (DOT || a.dalpha) a.dalpha[(int64_t)k * H + h] = s;
                 if constexpr (!DOT) {
                     const float al = a.alpha[(int64_t)k * H + h];
-                    c += al * s;
-                    park_edge(a, (int64_t)k * H + h, part >= 0, al,
-                              park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al), nullptr, 0);
+                    c = fmaf(al, s, c);
+                    const float u1 = park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al);
+                    if (sep) park_edge<true>(a, (int64_t)k * H + h, part >= 0, al, s, u1, nullptr, 0);
+                    else park_edge<false>(a, (int64_t)k * H + h, part >= 0, al, s, u1, nullptr, 0);
                 }
             }
         }
@@ -375,7 +414,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
             for (int k = beg + slot; k < end; k += eps) {
                 const int64_t i = (int64_t)k * H + h;
                 const float2 r = a.rec[i];
-                sdt += finish_edge(a, i, r.x, r.y, a.dalpha[i], c);
+                const float g = sep ? finish_edge<true>(a, i, r.x, r.y, a.dalpha[i], c)   // (alpha, u)
+                                    : finish_edge<false>(a, i, a.alpha[i], r.y, r.x, c); // (dalpha, u)
+                sdt = add_stored(sdt, g);
             }
         }
         sdt = slot_sum(live ? sdt : 0.f, H);
@@ -389,6 +430,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
 // are loaded by the slots side by side and summed over the slots in a fixed
 // order (every group of a row forms the same c), and the next group's
 // descriptors are fetched while this one is processed.
+template <bool SEP>
 __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
 {
     const int lane = lane_id();
@@ -421,14 +463,20 @@ __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
                     const int64_t i = (int64_t)(k < d.z ? k : k0) * H + h;
-                    da[r] = a.dalpha[i];
-                    uv[r] = a.dscore[i];
+                    if constexpr (SEP) {            // dalpha and the u parked in dscore
+                        da[r] = a.dalpha[i];
+                        uv[r] = a.dscore[i];
+                    } else {                        // the parked pair (dalpha, u)
+                        const float2 q = a.rec[i];
+                        da[r] = q.x;
+                        uv[r] = q.y;
+                    }
                     al[r] = a.alpha[i];
                 }
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
-                    if (k < d.z) sdt += finish_edge(a, (int64_t)k * H + h, al[r], uv[r], da[r], c);
+                    if (k < d.z) sdt = add_stored(sdt, finish_edge<SEP>(a, (int64_t)k * H + h, al[r], uv[r], da[r], c));
                 }
             }
         }
@@ -465,31 +513,40 @@ __global__ __launch_bounds__(kBlock) void k_split_head_sums(const int4 *__restri
 
 using BwdKernel = void (*)(BwdArgs);
 
-template <typename TX, int VEC, bool DOT>
+template <typename TX, int VEC, bool DOT, bool SEP>
 BwdKernel pick_rows_rs(bool buf, bool rs)
 {
     if constexpr (VEC == 1) {
-        return buf ? k_bwd_rows<TX, 1, true, DOT> : k_bwd_rows<TX, 1, false, DOT>;
+        return buf ? k_bwd_rows<TX, 1, true, DOT, false, SEP> : k_bwd_rows<TX, 1, false, DOT, false, SEP>;
     } else {
-        if (rs) return buf ? k_bwd_rows<TX, VEC, true, DOT, true> : k_bwd_rows<TX, VEC, false, DOT, true>;
-        return buf ? k_bwd_rows<TX, VEC, true, DOT> : k_bwd_rows<TX, VEC, false, DOT>;
+        if (rs)
+            return buf ? k_bwd_rows<TX, VEC, true, DOT, true, SEP> : k_bwd_rows<TX, VEC, false, DOT, true, SEP>;
+        return buf ? k_bwd_rows<TX, VEC, true, DOT, false, SEP> : k_bwd_rows<TX, VEC, false, DOT, false, SEP>;
     }
 }
 
-// rs: the head spans 8 or more lanes (reduce-scatter; vector kernels only)
-template <bool DOT>
-BwdKernel pick_rows(int dt, bool buf, int vec, bool rs)
+template <bool DOT, bool SEP>
+BwdKernel pick_rows_t(int dt, bool buf, int vec, bool rs)
 {
     if (dt == COGDL_F32) {
-        if (vec == 4) return pick_rows_rs<float, 4, DOT>(buf, rs);
-        return pick_rows_rs<float, 1, DOT>(buf, rs);
+        if (vec == 4) return pick_rows_rs<float, 4, DOT, SEP>(buf, rs);
+        return pick_rows_rs<float, 1, DOT, SEP>(buf, rs);
     }
     if (dt == COGDL_BF16) {
-        if (vec == 8) return pick_rows_rs<bf16_t, 8, DOT>(buf, rs);
-        return pick_rows_rs<bf16_t, 1, DOT>(buf, rs);
+        if (vec == 8) return pick_rows_rs<bf16_t, 8, DOT, SEP>(buf, rs);
+        return pick_rows_rs<bf16_t, 1, DOT, SEP>(buf, rs);
     }
-    if (vec == 8) return pick_rows_rs<f16_t, 8, DOT>(buf, rs);
-    return pick_rows_rs<f16_t, 1, DOT>(buf, rs);
+    if (vec == 8) return pick_rows_rs<f16_t, 8, DOT, SEP>(buf, rs);
+    return pick_rows_rs<f16_t, 1, DOT, SEP>(buf, rs);
+}
+
+// rs: the head spans 8 or more lanes (reduce-scatter; vector kernels only);
+// sep: dalpha and dscore are both written (the dot-product kernels ignore it)
+template <bool DOT>
+BwdKernel pick_rows(int dt, bool buf, int vec, bool rs, bool sep)
+{
+    if (DOT || sep) return pick_rows_t<DOT, true>(dt, buf, vec, rs);
+    return pick_rows_t<DOT, false>(dt, buf, vec, rs);
 }
 
 template <typename TX, bool DOT>
@@ -531,10 +588,12 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
     if (fast) {
         a.log2S = m.log2S;
         a.log2L = log2i(L);
-        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec, L >= 8);
+        const bool rs = m.vec > 1 && L >= 8;
+        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec, rs, a.dalpha && a.dscore);
         const int64_t upb = kBlock >> m.log2S;
-        a.park_cap = DOT ? 0 : kRowParkFloats / (int)upb;
-        const size_t shm = DOT ? 0 : sizeof(float) * kRowParkFloats;
+        const bool park_lds = !DOT && rs;
+        a.park_cap = park_lds ? kRowParkFloats / (int)upb : 0;
+        const size_t shm = park_lds ? sizeof(float) * kRowParkFloats : 0;
         int64_t blocks = (units + upb - 1) / upb;
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
         if (blocks > res) blocks = res;
@@ -613,7 +672,7 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     if (!dtype_ok(x_dtype) || !dtype_ok(dy_dtype) || !dtype_ok(dx_dtype)) return COGDL_ERR_DTYPE;
     if (n_cols > 0 && (!colptr || !dX || !ds_src)) return COGDL_ERR_INVALID;
     if (n_rows > 0 && (!ds_dst || !s_dst || !dY)) return COGDL_ERR_INVALID;
-    if (nnz > 0 && (!row_t || !perm || !s_src || !alpha || !X || !dalpha || !dscore || !edge_work ||
+    if (nnz > 0 && (!row_t || !perm || !s_src || !alpha || !X || !edge_work ||
                     (uintptr_t)edge_work % alignof(float2) != 0))
         return COGDL_ERR_INVALID;
     float2 *rec = reinterpret_cast<float2 *>(edge_work);
@@ -655,8 +714,12 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
         st = rows_pass<false>(a, Pr, (int)x_dtype, (int)dy_dtype, "gat_bwd_rows", stream);
         if (st != COGDL_OK) return st;
         if (Pr) {
-            COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges, wave_grid(Pr->cap_partials),
-                         kBlock, stream, a);
+            if (dalpha && dscore)
+                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<true>, wave_grid(Pr->cap_partials),
+                             kBlock, stream, a);
+            else
+                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<false>, wave_grid(Pr->cap_partials),
+                             kBlock, stream, a);
             COGDL_LAUNCH("gat_bwd_split_dst", k_split_head_sums, wave_grid(Pr->cap_split), kBlock,
                          stream, Pr->split_rows, Pr->n_split_dev(), Pr->gstats, a.sstride,
                          Pr->max_heads, H, ds_dst);

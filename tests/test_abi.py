@@ -279,7 +279,8 @@ def test_gat_backward_validation(L):
     assert B(2, 2, 3, colptr=None) == INVALID
     assert B(2, 2, 3, perm=None) == INVALID
     assert B(2, 2, 3, alpha=None) == INVALID
-    assert B(2, 2, 3, dscore=None) == INVALID
+    # dscore (like dalpha) may be NULL; the missing workspace is what is refused here
+    assert B(2, 2, 3, dscore=None, work=None) == INVALID
     assert B(2, 2, 3, ds_src=None) == INVALID
     assert B(2, 2, 3, work=None) == INVALID
     assert B(2, 2, 3, work=_p(0x1004)) == INVALID        # the edge records are 8-byte pairs

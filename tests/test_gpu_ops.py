@@ -672,6 +672,44 @@ def test_gat_backward_unnormalized_weights_and_repeat(cg):
         plan_t.close()
 
 
+@pytest.mark.parametrize("kind", ["hubs", "dups"])
+@pytest.mark.parametrize("H,D,xk", [(4, 64, "bf16"), (8, 16, "f32"), (3, 5, "f32"), (2, 64, "f16")])
+def test_gat_backward_without_edge_outputs(cg, kind, H, D, xk):
+    """dalpha and dscore left out (either or both): ds_dst, ds_src, dX and the (alpha, dscore)
+    records are the full call's bit for bit, on every plan pair (whole rows parked in LDS as
+    pairs or in the records, split rows' pairs in the records)."""
+    import torch
+    g = _graph(kind, seed=21)
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss, alpha, (xh, xc, xd), (gh, gc, gd) = _bwd_inputs(g, H, D, xk, 300 + H * D)
+    colptr, row_t, _, perm = oracle.csr_to_csc(g.rowptr, g.col, None, g.n_cols)
+    cp_d, rt_d, pm_d = dev(colptr), dev(row_t), dev(perm)
+    args = (rp, cl, cp_d, rt_d, pm_d, dev(sd), dev(ss), dev(alpha), xd, gd, 0.2)
+    for spec, spec_t in PLAN_PAIRS + [("sliced", "sliced")]:
+        say(f"gat_backward without edge outputs {kind} H={H} D={D} {xk} {spec}")
+        if spec == "sliced":
+            plan = cg.Plan(rp, g.nnz, H * D, max_heads=H, mode="neighbor_group", group_size=16, col=cl,
+                           n_cols=g.n_cols, slice_min=8)
+            plan_t = cg.Plan(cp_d, g.nnz, H * D, max_heads=H, mode="neighbor_group", group_size=16,
+                             col=rt_d, n_cols=g.n_rows, slice_min=8)
+        else:
+            plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+            plan_t = _make_plan(cg, cp_d, g.nnz, spec_t, H * D, max_heads=H)
+        try:
+            full = cg.gat_backward(*args, plan=plan, plan_t=plan_t, dx_dtype=torch.float32)
+            for drop in (("dalpha", "dscore"), ("dscore",), ("dalpha",)):
+                part = cg.gat_backward(*args, plan=plan, plan_t=plan_t, dx_dtype=torch.float32,
+                                       out={k: None for k in drop})
+                for k in ("dX", "ds_dst", "ds_src", "edge_work") + tuple(
+                        k for k in ("dalpha", "dscore") if k not in drop):
+                    assert torch.equal(part[k], full[k]), (kind, H, D, spec, drop, k)
+                assert all(part[k] is None for k in drop)
+        finally:
+            for p in (plan, plan_t):
+                if p is not None:
+                    p.close()
+
+
 def test_plan_rebuild_past_capacity_is_refused(cg):
     """A rebuild on a rowptr holding more edges than the plan was created for must not write past
     the plan: the build leaves the plan empty and cogdl_plan_query reports COGDL_ERR_PLAN; a
