@@ -15,11 +15,14 @@
 // multiplies its dY elements into every gathered neighbour row and a
 // reduction over the head's lanes completes the dot product, so the gathered
 // rows are read once, as in the forward aggregation.  The lanes fold the row
-// sum c as they go and park dalpha and the pair (alpha, f alpha) of every
-// edge (each value by a fixed lane); once c is complete, the same lanes read
-// their own parked values back and write dscore and ds_dst.  A neighbour
-// group of a split row leaves its share of c in the plan, and two small
-// kernels finish those rows once every group is done.
+// sum c as they go and park dalpha and u = f alpha of every edge (each value
+// by a fixed lane: in LDS for a whole row that fits, else in memory); once c
+// is complete, the same lanes read their own parked values back and write
+// dscore and ds_dst.  A neighbour group of a split row leaves its share of c
+// in the plan, and two small kernels finish those rows once every group is
+// done.  dalpha and dscore are optional outputs: a layer's backward needs
+// only ds_dst, ds_src and dX, and its kernels then park in LDS and the
+// records alone.
 //
 // The pairs (alpha, dscore) of an edge's heads end side by side in the
 // caller's edge workspace, 8 H bytes per edge in CSR order.  Pass 2 is the
@@ -52,10 +55,10 @@ struct BwdArgs {
     const void *X;              // gathered operand, n_cols x W
     uint64_t x_bytes;
     const void *P;              // row operand (dY), n_rows x W
-    float *dalpha;              // [nnz][H]
-    float *dscore;              // [nnz][H]
-    float2 *rec;                // [nnz][H] pairs (alpha, f alpha), then (alpha, dscore)
-    int32_t park_cap;           // LDS floats per sub-group for whole rows' parked u (0: none)
+    float *dalpha;              // [nnz][H], or nullptr (not written)
+    float *dscore;              // [nnz][H], or nullptr (not written)
+    float2 *rec;                // [nnz][H] parked pairs (see park_edge), then (alpha, dscore)
+    int32_t park_cap;           // LDS floats per sub-group for whole rows' parked values (0: none)
     float *ds_dst;              // [n_rows][H]
     float *gstats;              // split rows: per partial slot c[max_heads], sum[max_heads]
     int32_t sstride;            // 2 * max_heads
