@@ -1297,7 +1297,15 @@ def main():
     ms_bwd_l, k_bwd_l = time_op_kernels(lambda: cg.gat_backward(
         rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha_buf, Xg, dYg, 0.2, plan=plan,
         plan_t=plan_t, out=lay_out))
-    del lay_out
+    # a training step's pair without alpha in memory: the forward keeps each row's softmax
+    # state (max, 1 / normalizer), the backward rebuilds the weights from it
+    st_buf = torch.empty((N, 2, H), dtype=torch.float32, device=dev)
+    ms_gat_st, k_gat_st = time_op_kernels(lambda: cg.gat_aggregate_stats(
+        rowptr, col, s_dst, Xg, s_src=s_src, negative_slope=0.2, plan=plan, out=Yg, stats_out=st_buf))
+    ms_bwd_st, k_bwd_st = time_op_kernels(lambda: cg.gat_backward(
+        rowptr, col, colptr, row_t, perm, s_dst, s_src, None, Xg, dYg, 0.2, plan=plan,
+        plan_t=plan_t, out=lay_out, row_stats=st_buf))
+    del lay_out, st_buf
     dot_out = torch.empty((E, H), dtype=torch.float32, device=dev)
     ms_dot, k_dot = time_op_kernels(lambda: cg.sddmm_dot(rowptr, col, dYg, Xg, plan=plan, out=dot_out))
     b_dot = 4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * E * H
@@ -1311,6 +1319,8 @@ def main():
                   + M * H * D * 2 + 4 * M * H)
     b_bwd = b_bwd_rows + b_bwd_cols
     b_bwd_l = b_bwd - 8 * E * H                    # no dalpha, no dscore written
+    b_bwd_st = b_bwd_l - 4 * E * H + 8 * N * H       # row states read instead of alpha
+    b_gat_st = b_gat(N, E, H, D, 2, 2, False) + 8 * N * H
 
     # activation compression of the layer output Y (N x F bf16) at 2, 3, 4 bits, groups of F
     codec = {}
@@ -1362,6 +1372,13 @@ def main():
             ms=ms_bwd_l, algorithmic_GB=b_bwd_l / 1e9, eff_GBps=b_bwd_l / (ms_bwd_l * 1e-3) / 1e9,
             edges_per_s=E / (ms_bwd_l * 1e-3), kernels_ms=k_bwd_l,
             note="dalpha and dscore not written: ds_dst, ds_src, dX and the (alpha, dscore) records"),
+        "gat_training_pair_row_states": dict(
+            forward_ms=ms_gat_st, backward_ms=ms_bwd_st, ms=ms_gat_st + ms_bwd_st,
+            forward_algorithmic_GB=b_gat_st / 1e9, backward_algorithmic_GB=b_bwd_st / 1e9,
+            forward_kernels_ms=k_gat_st, backward_kernels_ms=k_bwd_st,
+            with_alpha_ms=ms_gat_a + ms_bwd_l,
+            note="forward with each row's softmax state instead of alpha, backward rebuilding the "
+                 "weights (layer gradients only); with_alpha_ms: the same pair through alpha"),
         "act_codec": codec,
         "sddmm_dot": dict(ms=ms_dot, algorithmic_GB=b_dot / 1e9,
                           eff_GBps=b_dot / (ms_dot * 1e-3) / 1e9, edges_per_s=E / (ms_dot * 1e-3)),
@@ -1412,7 +1429,9 @@ def main():
         f"gat backward {ms_bwd:.3f} ms "
         f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd.items())}), "
         f"layer gradients only {ms_bwd_l:.3f} ms "
-        f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd_l.items())})")
+        f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd_l.items())}); "
+        f"training pair through row states {ms_gat_st:.3f} + {ms_bwd_st:.3f} ms "
+        f"(through alpha {ms_gat_a:.3f} + {ms_bwd_l:.3f} ms)")
 
     inference = None if args.no_inference else run_inference(cg, synth, dev, time_op_kernels,
                                                              sliced=not args.plain_plans)

@@ -371,6 +371,26 @@ cogdl_status cogdl_gat_aggregate_proj(int32_t n_rows, int32_t n_cols, int64_t nn
                                       cogdl_act act, const cogdl_plan *plan, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * The attention layer of cogdl_gat_aggregate_act / _proj for training: Y as
+ * there, and instead of alpha (nnz x H) the final softmax state of every
+ * row, row_stats[i * 2H + h] = m[i,h] (the row's maximum score) and
+ * row_stats[i * 2H + H + h] = 1 / z[i,h] (its normalizer), n_rows x 2H fp32,
+ * from which cogdl_gat_backward_stats rebuilds every weight with the same
+ * bits as alpha_out would hold (section 2.2: the edge softmax's
+ * exp(e - m) / z; an empty row gets m = -inf, 1/z = 1).  Exactly one of
+ * s_src (scores given, as cogdl_gat_aggregate_act) and a_src (projected, as
+ * cogdl_gat_aggregate_proj, same requirements) is non-NULL; row_stats is
+ * required.  COGDL_ERR_INVALID otherwise.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_gat_aggregate_stats(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                       const int32_t *rowptr, const int32_t *col, int32_t H,
+                                       int32_t D, const float *s_dst, const float *s_src,
+                                       const float *a_src, float negative_slope, const void *X,
+                                       cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype,
+                                       float *row_stats, const float *bias, cogdl_act act,
+                                       const cogdl_plan *plan, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Dense layer of the GCN and GAT models that the sparse operators of section
  * 2.2 serve (the feature transform of every layer; the paper's end-to-end
  * inference workload is a 2-layer GCN or GAT):
@@ -471,6 +491,31 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
                                 cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
                                 float *ds_src, float *edge_work, const cogdl_plan *plan,
                                 const cogdl_plan *plan_t, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * cogdl_gat_backward with the forward weights rebuilt instead of read:
+ * row_stats (n_rows x 2H fp32, as written by cogdl_gat_aggregate_stats on
+ * the same graph and scores) replaces alpha, and the first pass forms
+ * alpha[k,h] = exp(e - m[i,h]) / z[i,h] from the score e it already gathers
+ * s_src for, with the forward's own arithmetic: with the scores the forward
+ * was given, every output equals cogdl_gat_backward's on that forward's
+ * alpha, bit for bit (the records of edge_work included).  With projected
+ * scores, s_src here is the caller's projection (cogdl_head_scores), equal
+ * to the forward's up to rounding.  The weights rebuilt are softmax outputs
+ * (>= 0).  Everything else as cogdl_gat_backward; COGDL_ERR_INVALID for a
+ * missing row_stats.
+ * ---------------------------------------------------------------------- */
+cogdl_status cogdl_gat_backward_stats(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col,
+                                      const int32_t *colptr, const int32_t *row_t,
+                                      const int32_t *perm, int32_t H, int32_t D,
+                                      const float *s_dst, const float *s_src,
+                                      float negative_slope, const float *row_stats, const void *X,
+                                      cogdl_dtype x_dtype, const void *dY, cogdl_dtype dy_dtype,
+                                      void *dX, cogdl_dtype dx_dtype, float *dalpha,
+                                      float *dscore, float *ds_dst, float *ds_src,
+                                      float *edge_work, const cogdl_plan *plan,
+                                      const cogdl_plan *plan_t, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel tracing (instrumentation, not part of the paper's method).  When

@@ -73,6 +73,8 @@ def lib():
                                           ctypes.c_int, P, ctypes.c_int, P, P, ctypes.c_int, P, P]
     L.cogdl_gat_aggregate_proj.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, f32, P, ctypes.c_int, P,
                                            ctypes.c_int, P, ctypes.c_int, P, P]
+    L.cogdl_gat_aggregate_stats.argtypes = [i32, i32, i64, P, P, i32, i32, P, P, P, f32, P, ctypes.c_int, P,
+                                            ctypes.c_int, P, P, ctypes.c_int, P, P]
     L.cogdl_linear.argtypes = [i64, i32, i32, P, P, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P]
     L.cogdl_head_scores.argtypes = [i64, i32, i32, P, ctypes.c_int, P, P, P, P, P]
     L.cogdl_act_codec_size.argtypes = [i64, i32, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -90,6 +92,7 @@ def lib():
     L.cogdl_gat_backward.argtypes = [i32, i32, i64, P, P, P, P, P, i32, i32, P, P, f32, P, P,
                                      ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P,
                                      P, P, P]
+    L.cogdl_gat_backward_stats.argtypes = L.cogdl_gat_backward.argtypes
     L.cogdl_trace_enable.argtypes = [i32]
     L.cogdl_trace_filter.argtypes = [ctypes.c_char_p]
     L.cogdl_trace_count.restype = i32
@@ -98,8 +101,9 @@ def lib():
                  "cogdl_plan_units", "cogdl_spmm", "cogdl_gspmm", "cogdl_spmm_t", "cogdl_csr_to_csc_workspace",
                  "cogdl_csr_to_csc", "cogdl_csr_to_csc_noalloc", "cogdl_sddmm_edge_softmax",
                  "cogdl_gat_aggregate",
-                 "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_aggregate_act",
-                 "cogdl_gat_aggregate_proj", "cogdl_linear",
+                 "cogdl_sddmm_dot", "cogdl_gat_backward", "cogdl_gat_backward_stats",
+                 "cogdl_gat_aggregate_act", "cogdl_gat_aggregate_proj", "cogdl_gat_aggregate_stats",
+                 "cogdl_linear",
                  "cogdl_head_scores", "cogdl_act_codec_size", "cogdl_act_compress",
                  "cogdl_act_decompress"):
         getattr(L, name).restype = ctypes.c_int
@@ -591,6 +595,46 @@ def gat_aggregate_proj(rowptr, col, s_dst, a_src, X, negative_slope: float = 0.2
     return out
 
 
+def gat_aggregate_stats(rowptr, col, s_dst, X, s_src=None, a_src=None, negative_slope: float = 0.2,
+                        plan: Plan | None = None, out_dtype=None, out=None, stats_out=None, bias=None,
+                        act: str = "none"):
+    """The GAT aggregation of a training step: returns (Y, row_stats), row_stats fp32
+    [n_rows, 2, H] = the final (max score, 1 / normalizer) of each row's softmax per head, from
+    which gat_backward(row_stats=...) rebuilds every weight instead of reading alpha.  Exactly
+    one of s_src (scores given) and a_src (projected from X, as gat_aggregate_proj)."""
+    import torch
+    if act not in ACT:
+        raise ValueError(f"act must be one of {sorted(ACT)}")
+    if (s_src is None) == (a_src is None):
+        raise CogdlError("give exactly one of s_src and a_src")
+    n_rows, nnz = _graph(rowptr, col)
+    n_cols, H, D = _dims(X, "X", 3)
+    _scores(s_dst, "s_dst", n_rows, H)
+    if s_src is not None:
+        _scores(s_src, "s_src", n_cols, H)
+    else:
+        _numel(a_src, "a_src", H * D)
+    _numel(out, "out", n_rows * H * D)
+    _numel(stats_out, "stats_out", n_rows * 2 * H)
+    _numel(bias, "bias", H * D)
+    _plan_matches(plan, n_rows, nnz)
+    _dev(bias, "bias", torch.float32), _dev(a_src, "a_src", torch.float32)
+    _dev(rowptr, "rowptr", torch.int32), _dev(col, "col", torch.int32), _dev(X, "X")
+    _dev(s_dst, "s_dst", torch.float32), _dev(s_src, "s_src", torch.float32)
+    if out is None:
+        out = torch.empty((n_rows, H, D), dtype=out_dtype or X.dtype, device=X.device)
+    _dev(out, "out")
+    if stats_out is None:
+        stats_out = torch.empty((n_rows, 2, H), dtype=torch.float32, device=X.device)
+    _dev(stats_out, "stats_out", torch.float32)
+    _check(lib().cogdl_gat_aggregate_stats(n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), H, D, _ptr(s_dst),
+                                           _ptr(s_src), _ptr(a_src), float(negative_slope), _ptr(X),
+                                           _dtype_code(X), _ptr(out), _dtype_code(out), _ptr(stats_out),
+                                           _ptr(bias), ACT[act], _plan_handle(plan), _stream()),
+           "cogdl_gat_aggregate_stats")
+    return out, stats_out
+
+
 def sddmm_dot(rowptr, col, P, Q, plan: Plan | None = None, out=None):
     """out[k, h] = <P[i, h, :], Q[col[k], h, :]> for every edge k = (i, col[k]):
     the SDDMM of section 2.2 per head.  P is [n_rows, H, D], Q [n_cols, H, D]."""
@@ -616,13 +660,15 @@ def sddmm_dot(rowptr, col, P, Q, plan: Plan | None = None, out=None):
 
 def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
                  negative_slope: float = 0.2, plan: Plan | None = None, plan_t: Plan | None = None,
-                 dx_dtype=None, out=None):
+                 dx_dtype=None, out=None, row_stats=None):
     """Gradients of gat_aggregate for dY = dL/dY.  X is [n_cols, H, D], dY [n_rows, H, D],
     alpha [nnz, H] the forward weights; (colptr, row_t, perm) the CSC from csr_to_csc.
     Returns dict(dX, dalpha, dscore, ds_dst, ds_src, edge_work); ``out`` may supply these
     tensors, and ``out={"dalpha": None, "dscore": None}`` (either or both) leaves those
     outputs out.  edge_work (fp32, 2 nnz H) is the library's scratch between its two passes:
-    it ends holding the pair (alpha, dscore) of every edge and head."""
+    it ends holding the pair (alpha, dscore) of every edge and head.  With alpha None and
+    row_stats (from gat_aggregate_stats) the weights are rebuilt instead of read
+    (cogdl_gat_backward_stats)."""
     import torch
     n_rows, nnz = _graph(rowptr, col)
     n_cols, H, D = _dims(X, "X", 3)
@@ -635,7 +681,10 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
         _index_array(t, name)
     _scores(s_dst, "s_dst", n_rows, H)
     _scores(s_src, "s_src", n_cols, H)
+    if (alpha is None) == (row_stats is None):
+        raise CogdlError("give exactly one of alpha and row_stats")
     _numel(alpha, "alpha", nnz * H)
+    _numel(row_stats, "row_stats", n_rows * 2 * H)
     o = dict(out or {})
     sizes = {"dX": n_cols * H * D, "dalpha": nnz * H, "dscore": nnz * H, "ds_dst": n_rows * H,
              "ds_src": n_cols * H, "edge_work": 2 * nnz * H}
@@ -651,7 +700,8 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     for t, name, dt in ((rowptr, "rowptr", torch.int32), (col, "col", torch.int32),
                         (colptr, "colptr", torch.int32), (row_t, "row_t", torch.int32),
                         (perm, "perm", torch.int32), (s_dst, "s_dst", torch.float32),
-                        (s_src, "s_src", torch.float32), (alpha, "alpha", torch.float32)):
+                        (s_src, "s_src", torch.float32), (alpha, "alpha", torch.float32),
+                        (row_stats, "row_stats", torch.float32)):
         _dev(t, name, dt)
     _dev(X, "X"), _dev(dY, "dY")
     dev = X.device
@@ -665,12 +715,13 @@ def gat_backward(rowptr, col, colptr, row_t, perm, s_dst, s_src, alpha, X, dY,
     for k in ("dalpha", "dscore", "ds_dst", "ds_src", "edge_work"):
         if o[k] is not None:
             _dev(o[k], k, torch.float32)
-    _check(lib().cogdl_gat_backward(
+    fn = "cogdl_gat_backward" if row_stats is None else "cogdl_gat_backward_stats"
+    _check(getattr(lib(), fn)(
         n_rows, n_cols, nnz, _ptr(rowptr), _ptr(col), _ptr(colptr), _ptr(row_t), _ptr(perm), H, D,
-        _ptr(s_dst), _ptr(s_src), float(negative_slope), _ptr(alpha), _ptr(X), _dtype_code(X),
-        _ptr(dY), _dtype_code(dY), _ptr(o["dX"]), _dtype_code(o["dX"]), _ptr(o["dalpha"]),
-        _ptr(o["dscore"]), _ptr(o["ds_dst"]), _ptr(o["ds_src"]), _ptr(o["edge_work"]), _plan_handle(plan),
-        _plan_handle(plan_t), _stream()), "cogdl_gat_backward")
+        _ptr(s_dst), _ptr(s_src), float(negative_slope), _ptr(alpha if row_stats is None else row_stats),
+        _ptr(X), _dtype_code(X), _ptr(dY), _dtype_code(dY), _ptr(o["dX"]), _dtype_code(o["dX"]),
+        _ptr(o["dalpha"]), _ptr(o["dscore"]), _ptr(o["ds_dst"]), _ptr(o["ds_src"]), _ptr(o["edge_work"]),
+        _plan_handle(plan), _plan_handle(plan_t), _stream()), fn)
     return o
 
 

@@ -272,6 +272,7 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
                                                        const float *__restrict__ gstats,
                                                        int sstride, int H, int D,
                                                        float *__restrict__ rstats,
+                                                       float *__restrict__ row_stats,
                                                        const float *__restrict__ bias, int act_code,
                                                        TY *__restrict__ Y)
 {
@@ -289,6 +290,10 @@ __global__ __launch_bounds__(kBlock) void k_gat_reduce(const int4 *__restrict__ 
         if (lane < H) {
             rstats[s * sstride + lane] = m;
             rstats[s * sstride + (sstride >> 1) + lane] = z;
+            if (row_stats) {                  // (m, 1/z), as the split-row alpha pass forms them
+                row_stats[row * 2 * H + lane] = m;
+                row_stats[row * 2 * H + H + lane] = 1.f / z;
+            }
         }
         for (int64_t fb = 0; fb < W; fb += kWave * VEC) {
             const int64_t f = fb + (int64_t)lane * VEC;
@@ -359,8 +364,9 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
                                 const int32_t *col, int32_t H, int32_t D, const float *s_dst,
                                 const float *s_src, const float *a_src, float negative_slope,
                                 const float *alpha_in, const void *X, cogdl_dtype x_dtype, void *Y,
-                                cogdl_dtype y_dtype, float *alpha_out, const float *bias,
-                                cogdl_act act, const cogdl_plan *plan, hipStream_t stream);
+                                cogdl_dtype y_dtype, float *alpha_out, float *row_stats,
+                                const float *bias, cogdl_act act, const cogdl_plan *plan,
+                                hipStream_t stream);
 
 }  // namespace
 }  // namespace cogdl
@@ -449,8 +455,8 @@ cogdl_status cogdl_gat_aggregate_act(int32_t n_rows, int32_t n_cols, int64_t nnz
                                      const cogdl_plan *plan, hipStream_t stream)
 {
     return gat_aggregate_impl(n_rows, n_cols, nnz, rowptr, col, H, D, s_dst, s_src, nullptr,
-                              negative_slope, alpha_in, X, x_dtype, Y, y_dtype, alpha_out, bias, act,
-                              plan, stream);
+                              negative_slope, alpha_in, X, x_dtype, Y, y_dtype, alpha_out, nullptr, bias,
+                              act, plan, stream);
 }
 
 cogdl_status cogdl_gat_aggregate_proj(int32_t n_rows, int32_t n_cols, int64_t nnz,
@@ -462,8 +468,24 @@ cogdl_status cogdl_gat_aggregate_proj(int32_t n_rows, int32_t n_cols, int64_t nn
 {
     if (!a_src) return COGDL_ERR_INVALID;
     return gat_aggregate_impl(n_rows, n_cols, nnz, rowptr, col, H, D, s_dst, nullptr, a_src,
-                              negative_slope, nullptr, X, x_dtype, Y, y_dtype, nullptr, bias, act,
-                              plan, stream);
+                              negative_slope, nullptr, X, x_dtype, Y, y_dtype, nullptr, nullptr, bias,
+                              act, plan, stream);
+}
+
+cogdl_status cogdl_gat_aggregate_stats(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                       const int32_t *rowptr, const int32_t *col, int32_t H,
+                                       int32_t D, const float *s_dst, const float *s_src,
+                                       const float *a_src, float negative_slope, const void *X,
+                                       cogdl_dtype x_dtype, void *Y, cogdl_dtype y_dtype,
+                                       float *row_stats, const float *bias, cogdl_act act,
+                                       const cogdl_plan *plan, hipStream_t stream)
+{
+    // exactly one of s_src (scores given) and a_src (scores projected)
+    if ((s_src == nullptr) == (a_src == nullptr)) return COGDL_ERR_INVALID;
+    if (n_rows > 0 && !row_stats) return COGDL_ERR_INVALID;
+    return gat_aggregate_impl(n_rows, n_cols, nnz, rowptr, col, H, D, s_dst, s_src, a_src,
+                              negative_slope, nullptr, X, x_dtype, Y, y_dtype, nullptr, row_stats, bias,
+                              act, plan, stream);
 }
 
 }  // extern "C"
@@ -475,8 +497,9 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
                                 const int32_t *col, int32_t H, int32_t D, const float *s_dst,
                                 const float *s_src, const float *a_src, float negative_slope,
                                 const float *alpha_in, const void *X, cogdl_dtype x_dtype, void *Y,
-                                cogdl_dtype y_dtype, float *alpha_out, const float *bias,
-                                cogdl_act act, const cogdl_plan *plan, hipStream_t stream)
+                                cogdl_dtype y_dtype, float *alpha_out, float *row_stats,
+                                const float *bias, cogdl_act act, const cogdl_plan *plan,
+                                hipStream_t stream)
 {
     if (act < COGDL_ACT_NONE || act > COGDL_ACT_ELU) return COGDL_ERR_INVALID;
     cogdl_status st = check_graph(n_rows, n_cols, nnz, rowptr, col, H);
@@ -490,6 +513,7 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
     if (soft && n_rows > 0 && !s_dst) return COGDL_ERR_INVALID;
     if (soft && !proj && nnz > 0 && !s_src) return COGDL_ERR_INVALID;
     if (proj && (!soft || alpha_out)) return COGDL_ERR_INVALID;
+    if (row_stats && !soft) return COGDL_ERR_INVALID;
     if (n_rows > 0 && !Y) return COGDL_ERR_INVALID;
     if (nnz > 0 && !X) return COGDL_ERR_INVALID;
     const Plan *P = plan_of(plan);
@@ -526,6 +550,7 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
     a.x_bytes = (uint64_t)n_cols * (uint64_t)W * (uint64_t)dtype_bytes(x_dtype);
     a.Y = Y;
     a.alpha_out = soft ? alpha_out : nullptr;
+    a.row_stats = row_stats;
     a.bias = bias;
     a.act = act;
     a.a_src = a_src;
@@ -582,7 +607,7 @@ cogdl_status gat_aggregate_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, con
 #define COGDL_GAT_REDUCE(TY, V)                                                                  \
     COGDL_LAUNCH("gat_reduce", (k_gat_reduce<TY, V>), rb, kBlock, stream, P->split_rows,         \
                  P->n_split_dev(), P->partials, a.pstride, P->gstats, a.sstride, H, D, P->rstats, \
-                 bias, act, static_cast<TY *>(Y))
+                 row_stats, bias, act, static_cast<TY *>(Y))
     if (y_dtype == COGDL_F32) {
         if (v4) COGDL_GAT_REDUCE(float, 4); else COGDL_GAT_REDUCE(float, 1);
     } else if (y_dtype == COGDL_BF16) {

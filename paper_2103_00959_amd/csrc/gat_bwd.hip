@@ -51,7 +51,8 @@ struct BwdArgs {
     const float *s_dst;
     const float *s_src;
     float slope;
-    const float *alpha;         // forward weights [nnz][H]; nullptr: the SDDMM alone
+    const float *alpha;         // forward weights [nnz][H]; nullptr: rebuilt from row_stats, or the SDDMM alone
+    const float *row_stats;     // per row the forward's (m, 1/z) of each head, 2H floats (or nullptr)
     const void *X;              // gathered operand, n_cols x W
     uint64_t x_bytes;
     const void *P;              // row operand (dY), n_rows x W
@@ -102,38 +103,54 @@ __device__ __forceinline__ float add_stored(float a, float b)
     return a + b;
 }
 
+// How pass 1 parks what the fix-up needs (c is not known yet):
+//   kParkSep:   alpha given, dalpha and dscore both written.  dalpha is in its
+//               output, so u alone parks: in dscore for a split row, in the LDS
+//               slot li for a whole row that fits its sub-group's share, else
+//               beside alpha in the record (alpha, u).
+//   kParkPair:  alpha given, an output left out: the pair (dalpha, u) parks in
+//               LDS (slots 2 li, 2 li + 1) or in the record.
+//   kParkStats: alpha rebuilt from the row's softmax state: the pair
+//               (dalpha, v) parks, v = alpha on the LeakyReLU's positive branch
+//               and -alpha on the other (alpha >= 0 here), so alpha = |v| and u
+//               = f alpha come back with the same bits.
+enum ParkMode { kParkSep, kParkPair, kParkStats };
+
 // Fix-up of one parked edge-head: dscore from alpha, the parked u and
-// dalpha, into the record and the output (SEP: there is one).
-template <bool SEP>
+// dalpha, into the record and the dscore output (when there is one).
+template <int PK>
 __device__ __forceinline__ float finish_edge(const BwdArgs &a, int64_t i, float al, float u, float da, float c)
 {
     const float g = parked_grad(u, da, c);
-    if (SEP || a.dscore) a.dscore[i] = g;
+    if (PK == kParkSep || a.dscore) a.dscore[i] = g;
     a.rec[i] = make_float2(al, g);
     return g;
 }
 
-// Park edge-head i until c is known.  SEP (dalpha and dscore both written):
-// dalpha is in its output, so u alone parks, in dscore for a split row, in
-// the LDS slot `li` for a whole row that fits its sub-group's share, else
-// beside alpha in the record.  Otherwise the pair (dalpha, u) parks, in LDS
-// (slots 2 li, 2 li + 1) or in the record.
-template <bool SEP>
+template <int PK>
 __device__ __forceinline__ void park_edge(const BwdArgs &a, int64_t i, bool split, float al, float da, float u,
                                           float *lds, int li)
 {
-    if constexpr (SEP) {
+    if constexpr (PK == kParkSep) {
         if (split) a.dscore[i] = u;
         else if (lds) lds[li] = u;
         else a.rec[i] = make_float2(al, u);
     } else {
+        const float v = PK == kParkStats ? (u == al ? al : -al) : u;
         if (lds) {
             lds[2 * li] = da;
-            lds[2 * li + 1] = u;
+            lds[2 * li + 1] = v;
         } else {
-            a.rec[i] = make_float2(da, u);
+            a.rec[i] = make_float2(da, v);
         }
     }
+}
+
+// (alpha, u) from a kParkStats value v.
+__device__ __forceinline__ float2 unpark_stats(float v, float slope)
+{
+    const float al = fabsf(v);
+    return make_float2(al, signbit(v) ? slope * al : al);
 }
 
 // LDS floats of a rows workgroup for whole rows' parked values, shared by its sub-groups.
@@ -149,7 +166,7 @@ constexpr int kRowParkFloats = 4096;
 // reduce-scattered over aligned groups of 8 lanes, so lane q ends with the
 // group's sum for its own edge q mod 8 (7 exchanges for the batch instead of
 // 8 butterflies of log2 L), and L > 8 adds the groups by a butterfly.
-template <typename TX, int VEC, bool BUF, bool DOT, bool RS = false, bool SEP = true>
+template <typename TX, int VEC, bool BUF, bool DOT, bool RS = false, int PK = kParkSep>
 __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
 {
     constexpr int U = VEC == 1 ? 16 : 8;
@@ -192,7 +209,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
         // a whole row whose parked values fit this sub-group's LDS share parks them
         // there (reduce-scatter kernels; the others keep their registers for the batch)
         float *const lds =
-            (RS && !DOT && part < 0 && (end - beg) * H * (SEP ? 1 : 2) <= a.park_cap) ? park_mine : nullptr;
+            (RS && !DOT && part < 0 && (end - beg) * H * (PK == kParkSep ? 1 : 2) <= a.park_cap) ? park_mine
+                                                                                                 : nullptr;
         float p[PACKED ? 1 : VEC];
         uint4 pw = make_uint4(0u, 0u, 0u, 0u);
         if constexpr (PACKED) {
@@ -204,6 +222,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
             for (int e = 0; e < VEC; ++e) p[e] = 0.f;
         }
         const float sd = (!DOT && act) ? a.s_dst[(int64_t)row * H + h] : 0.f;
+        // kParkStats: the row's softmax state for this lane's head
+        const float rm = (PK == kParkStats && act) ? a.row_stats[(int64_t)row * 2 * H + h] : 0.f;
+        const float rrz = (PK == kParkStats && act) ? a.row_stats[(int64_t)row * 2 * H + H + h] : 0.f;
         float c = 0.f;
 
         const int last = end - 1;
@@ -232,8 +253,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                     ss[t] = 0.f;
                     if constexpr (!DOT && !RS) {
                         if (mine[t]) {
-                            al[t] = a.alpha[(int64_t)(k0 + j + t) * H + h];
                             ss[t] = a.s_src[(int64_t)cc[t] * H + h];
+                            if constexpr (PK == kParkStats)
+                                al[t] = alpha_value(leaky_relu(sd + ss[t], a.slope), rm, rrz);
+                            else
+                                al[t] = a.alpha[(int64_t)(k0 + j + t) * H + h];
                         }
                     }
                 }
@@ -262,13 +286,14 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                     // (a cross-lane read: every lane takes part)
                     const int cme = DOT ? 0 : lane_bcast(c_cur, gbase + j + t);
                     if (own) {
-                        if (DOT || SEP || a.dalpha) a.dalpha[k * H + h] = s;
+                        if (DOT || PK == kParkSep || a.dalpha) a.dalpha[k * H + h] = s;
                         if constexpr (!DOT) {
-                            const float al1 = a.alpha[k * H + h];
                             const float ss1 = a.s_src[(int64_t)cme * H + h];
+                            const float al1 = PK == kParkStats ? alpha_value(leaky_relu(sd + ss1, a.slope), rm, rrz)
+                                                               : a.alpha[k * H + h];
                             c = fmaf(al1, s, c);
-                            park_edge<SEP>(a, k * H + h, part >= 0, al1, s, park_value(sd + ss1, a.slope, al1),
-                                           lds, (int)(k - beg) * H + h);
+                            park_edge<PK>(a, k * H + h, part >= 0, al1, s, park_value(sd + ss1, a.slope, al1),
+                                          lds, (int)(k - beg) * H + h);
                         }
                     }
                     continue;
@@ -281,11 +306,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                 for (int t = 0; t < U; ++t) {
                     const int64_t k = k0 + j + t;
                     if (mine[t]) {
-                        if (DOT || SEP || a.dalpha) a.dalpha[k * H + h] = pd[t];
+                        if (DOT || PK == kParkSep || a.dalpha) a.dalpha[k * H + h] = pd[t];
                         if constexpr (!DOT) {
                             c = fmaf(al[t], pd[t], c);
-                            park_edge<SEP>(a, k * H + h, part >= 0, al[t], pd[t],
-                                           park_value(sd + ss[t], a.slope, al[t]), lds, (int)(k - beg) * H + h);
+                            park_edge<PK>(a, k * H + h, part >= 0, al[t], pd[t],
+                                          park_value(sd + ss[t], a.slope, al[t]), lds, (int)(k - beg) * H + h);
                         }
                     }
                 }
@@ -313,7 +338,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                             const int oc = o < end - beg ? o : o0;
                             const int64_t i = ((int64_t)beg + oc) * H + h;
                             const int li = oc * H + h;
-                            if constexpr (SEP) {
+                            if constexpr (PK == kParkSep) {
                                 // dalpha from its output; u from LDS (alpha from the input)
                                 // or the record (alpha, u)
                                 da[r] = a.dalpha[i];
@@ -321,19 +346,26 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows(BwdArgs a)
                                 al[r] = p.x;
                                 uv[r] = p.y;
                             } else {
-                                // the pair (dalpha, u) from LDS or the record; alpha from the input
+                                // the pair from LDS or the record: (dalpha, u) with alpha from
+                                // the input, or (dalpha, v) holding alpha and u
                                 const float2 p = lds ? make_float2(lds[2 * li], lds[2 * li + 1]) : a.rec[i];
-                                al[r] = a.alpha[i];
                                 da[r] = p.x;
-                                uv[r] = p.y;
+                                if constexpr (PK == kParkStats) {
+                                    const float2 q = unpark_stats(p.y, a.slope);
+                                    al[r] = q.x;
+                                    uv[r] = q.y;
+                                } else {
+                                    al[r] = a.alpha[i];
+                                    uv[r] = p.y;
+                                }
                             }
                         }
 #pragma unroll
                         for (int r = 0; r < R; ++r) {
                             const int o = o0 + r * M;
                             if (o < end - beg)
-                                sdt = add_stored(sdt, finish_edge<SEP>(a, ((int64_t)beg + o) * H + h, al[r], uv[r],
-                                                                        da[r], c));
+                                sdt = add_stored(sdt, finish_edge<PK>(a, ((int64_t)beg + o) * H + h, al[r], uv[r],
+                                                                       da[r], c));
                         }
                     }
                 }
@@ -366,7 +398,7 @@ __device__ __forceinline__ float slot_sum(float v, int H)
 // Pass 1 for any shape: a wavefront per unit, lanes as (edge slot, head),
 // each lane forming whole dot products element by element.  Every edge is
 // parked by the lane of its slot.
-template <typename TX, typename TP, bool DOT>
+template <typename TX, typename TP, bool DOT, int PK = kParkSep>
 __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
 {
     const int lane = lane_id();
@@ -380,11 +412,12 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
     const int64_t hi = walk.end;
     const TX *__restrict__ X = static_cast<const TX *>(a.X);
     const TP *__restrict__ P = static_cast<const TP *>(a.P);
-    const bool sep = a.dalpha && a.dscore;
     for (int64_t u = walk.first; u < hi; u += walk.step) {
         const int4 d = fetch_bwd_unit(a, u, hi);
         const int row = d.x, beg = d.y, end = d.z, part = d.w;
         const float sd = DOT ? 0.f : a.s_dst[(int64_t)row * H + h];
+        const float rm = PK == kParkStats ? a.row_stats[(int64_t)row * 2 * H + h] : 0.f;
+        const float rrz = PK == kParkStats ? a.row_stats[(int64_t)row * 2 * H + H + h] : 0.f;
         float c = 0.f;
         if (live) {
             for (int k = beg + slot; k < end; k += eps) {
@@ -396,13 +429,14 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
                     load_vec<TX, 1>(X, (int64_t)j * a.W + (int64_t)h * a.D + e, xv);
                     s = fmaf(pv[0], xv[0], s);
                 }
-                if (DOT || a.dalpha) a.dalpha[(int64_t)k * H + h] = s;
+                if (DOT || PK == kParkSep || a.dalpha) a.dalpha[(int64_t)k * H + h] = s;
                 if constexpr (!DOT) {
-                    const float al = a.alpha[(int64_t)k * H + h];
+                    const float ss1 = a.s_src[(int64_t)j * H + h];
+                    const float al = PK == kParkStats ? alpha_value(leaky_relu(sd + ss1, a.slope), rm, rrz)
+                                                      : a.alpha[(int64_t)k * H + h];
                     c = fmaf(al, s, c);
-                    const float u1 = park_value(sd + a.s_src[(int64_t)j * H + h], a.slope, al);
-                    if (sep) park_edge<true>(a, (int64_t)k * H + h, part >= 0, al, s, u1, nullptr, 0);
-                    else park_edge<false>(a, (int64_t)k * H + h, part >= 0, al, s, u1, nullptr, 0);
+                    park_edge<PK>(a, (int64_t)k * H + h, part >= 0, al, s, park_value(sd + ss1, a.slope, al),
+                                  nullptr, 0);
                 }
             }
         }
@@ -417,8 +451,15 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
             for (int k = beg + slot; k < end; k += eps) {
                 const int64_t i = (int64_t)k * H + h;
                 const float2 r = a.rec[i];
-                const float g = sep ? finish_edge<true>(a, i, r.x, r.y, a.dalpha[i], c)   // (alpha, u)
-                                    : finish_edge<false>(a, i, a.alpha[i], r.y, r.x, c); // (dalpha, u)
+                float g;
+                if constexpr (PK == kParkSep) {
+                    g = finish_edge<PK>(a, i, r.x, r.y, a.dalpha[i], c);           // (alpha, u)
+                } else if constexpr (PK == kParkPair) {
+                    g = finish_edge<PK>(a, i, a.alpha[i], r.y, r.x, c);            // (dalpha, u)
+                } else {
+                    const float2 q = unpark_stats(r.y, a.slope);                   // (dalpha, v)
+                    g = finish_edge<PK>(a, i, q.x, q.y, r.x, c);
+                }
                 sdt = add_stored(sdt, g);
             }
         }
@@ -433,7 +474,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_rows_any(BwdArgs a)
 // are loaded by the slots side by side and summed over the slots in a fixed
 // order (every group of a row forms the same c), and the next group's
 // descriptors are fetched while this one is processed.
-template <bool SEP>
+template <int PK>
 __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
 {
     const int lane = lane_id();
@@ -466,20 +507,27 @@ __global__ __launch_bounds__(kBlock) void k_bwd_split_edges(BwdArgs a)
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
                     const int64_t i = (int64_t)(k < d.z ? k : k0) * H + h;
-                    if constexpr (SEP) {            // dalpha and the u parked in dscore
+                    if constexpr (PK == kParkSep) {         // dalpha and the u parked in dscore
                         da[r] = a.dalpha[i];
                         uv[r] = a.dscore[i];
-                    } else {                        // the parked pair (dalpha, u)
+                        al[r] = a.alpha[i];
+                    } else if constexpr (PK == kParkPair) { // the parked pair (dalpha, u)
                         const float2 q = a.rec[i];
                         da[r] = q.x;
                         uv[r] = q.y;
+                        al[r] = a.alpha[i];
+                    } else {                                // (dalpha, v): alpha and u from v
+                        const float2 q = a.rec[i];
+                        const float2 w = unpark_stats(q.y, a.slope);
+                        da[r] = q.x;
+                        al[r] = w.x;
+                        uv[r] = w.y;
                     }
-                    al[r] = a.alpha[i];
                 }
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int k = k0 + r * eps;
-                    if (k < d.z) sdt = add_stored(sdt, finish_edge<SEP>(a, (int64_t)k * H + h, al[r], uv[r], da[r], c));
+                    if (k < d.z) sdt = add_stored(sdt, finish_edge<PK>(a, (int64_t)k * H + h, al[r], uv[r], da[r], c));
                 }
             }
         }
@@ -516,56 +564,65 @@ __global__ __launch_bounds__(kBlock) void k_split_head_sums(const int4 *__restri
 
 using BwdKernel = void (*)(BwdArgs);
 
-template <typename TX, int VEC, bool DOT, bool SEP>
+template <typename TX, int VEC, bool DOT, int PK>
 BwdKernel pick_rows_rs(bool buf, bool rs)
 {
     if constexpr (VEC == 1) {
-        return buf ? k_bwd_rows<TX, 1, true, DOT, false, SEP> : k_bwd_rows<TX, 1, false, DOT, false, SEP>;
+        return buf ? k_bwd_rows<TX, 1, true, DOT, false, PK> : k_bwd_rows<TX, 1, false, DOT, false, PK>;
     } else {
         if (rs)
-            return buf ? k_bwd_rows<TX, VEC, true, DOT, true, SEP> : k_bwd_rows<TX, VEC, false, DOT, true, SEP>;
-        return buf ? k_bwd_rows<TX, VEC, true, DOT, false, SEP> : k_bwd_rows<TX, VEC, false, DOT, false, SEP>;
+            return buf ? k_bwd_rows<TX, VEC, true, DOT, true, PK> : k_bwd_rows<TX, VEC, false, DOT, true, PK>;
+        return buf ? k_bwd_rows<TX, VEC, true, DOT, false, PK> : k_bwd_rows<TX, VEC, false, DOT, false, PK>;
     }
 }
 
-template <bool DOT, bool SEP>
+template <bool DOT, int PK>
 BwdKernel pick_rows_t(int dt, bool buf, int vec, bool rs)
 {
     if (dt == COGDL_F32) {
-        if (vec == 4) return pick_rows_rs<float, 4, DOT, SEP>(buf, rs);
-        return pick_rows_rs<float, 1, DOT, SEP>(buf, rs);
+        if (vec == 4) return pick_rows_rs<float, 4, DOT, PK>(buf, rs);
+        return pick_rows_rs<float, 1, DOT, PK>(buf, rs);
     }
     if (dt == COGDL_BF16) {
-        if (vec == 8) return pick_rows_rs<bf16_t, 8, DOT, SEP>(buf, rs);
-        return pick_rows_rs<bf16_t, 1, DOT, SEP>(buf, rs);
+        if (vec == 8) return pick_rows_rs<bf16_t, 8, DOT, PK>(buf, rs);
+        return pick_rows_rs<bf16_t, 1, DOT, PK>(buf, rs);
     }
-    if (vec == 8) return pick_rows_rs<f16_t, 8, DOT, SEP>(buf, rs);
-    return pick_rows_rs<f16_t, 1, DOT, SEP>(buf, rs);
+    if (vec == 8) return pick_rows_rs<f16_t, 8, DOT, PK>(buf, rs);
+    return pick_rows_rs<f16_t, 1, DOT, PK>(buf, rs);
 }
 
 // rs: the head spans 8 or more lanes (reduce-scatter; vector kernels only);
-// sep: dalpha and dscore are both written (the dot-product kernels ignore it)
+// pk: the parking mode (the dot-product kernels have one)
 template <bool DOT>
-BwdKernel pick_rows(int dt, bool buf, int vec, bool rs, bool sep)
+BwdKernel pick_rows(int dt, bool buf, int vec, bool rs, int pk)
 {
-    if (DOT || sep) return pick_rows_t<DOT, true>(dt, buf, vec, rs);
-    return pick_rows_t<DOT, false>(dt, buf, vec, rs);
+    if (DOT || pk == kParkSep) return pick_rows_t<DOT, kParkSep>(dt, buf, vec, rs);
+    if (pk == kParkPair) return pick_rows_t<DOT, kParkPair>(dt, buf, vec, rs);
+    return pick_rows_t<DOT, kParkStats>(dt, buf, vec, rs);
 }
 
-template <typename TX, bool DOT>
+template <typename TX, bool DOT, int PK>
 BwdKernel pick_any_p(int pdt)
 {
-    if (pdt == COGDL_F32) return k_bwd_rows_any<TX, float, DOT>;
-    if (pdt == COGDL_BF16) return k_bwd_rows_any<TX, bf16_t, DOT>;
-    return k_bwd_rows_any<TX, f16_t, DOT>;
+    if (pdt == COGDL_F32) return k_bwd_rows_any<TX, float, DOT, PK>;
+    if (pdt == COGDL_BF16) return k_bwd_rows_any<TX, bf16_t, DOT, PK>;
+    return k_bwd_rows_any<TX, f16_t, DOT, PK>;
+}
+
+template <bool DOT, int PK>
+BwdKernel pick_any_t(int xdt, int pdt)
+{
+    if (xdt == COGDL_F32) return pick_any_p<float, DOT, PK>(pdt);
+    if (xdt == COGDL_BF16) return pick_any_p<bf16_t, DOT, PK>(pdt);
+    return pick_any_p<f16_t, DOT, PK>(pdt);
 }
 
 template <bool DOT>
-BwdKernel pick_any(int xdt, int pdt)
+BwdKernel pick_any(int xdt, int pdt, int pk)
 {
-    if (xdt == COGDL_F32) return pick_any_p<float, DOT>(pdt);
-    if (xdt == COGDL_BF16) return pick_any_p<bf16_t, DOT>(pdt);
-    return pick_any_p<f16_t, DOT>(pdt);
+    if (DOT || pk == kParkSep) return pick_any_t<DOT, kParkSep>(xdt, pdt);
+    if (pk == kParkPair) return pick_any_t<DOT, kParkPair>(xdt, pdt);
+    return pick_any_t<DOT, kParkStats>(xdt, pdt);
 }
 
 unsigned wave_grid(int64_t work)
@@ -584,6 +641,7 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
 {
     const int64_t units = P ? P->cap_units : a.n_rows;
     const int xb = dtype_bytes(xdt);
+    const int pk = a.row_stats ? kParkStats : (a.dalpha && a.dscore) ? kParkSep : kParkPair;
     const bool aligned = ((uintptr_t)a.X % 16 == 0) && ((uintptr_t)a.P % 16 == 0);
     const RowMap m = row_map(a.W, xb, a.D, aligned);
     const int L = a.D / m.vec;
@@ -592,7 +650,7 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
         a.log2S = m.log2S;
         a.log2L = log2i(L);
         const bool rs = m.vec > 1 && L >= 8;
-        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec, rs, a.dalpha && a.dscore);
+        BwdKernel k = pick_rows<DOT>(xdt, a.x_bytes <= kBufferMaxBytes, m.vec, rs, pk);
         const int64_t upb = kBlock >> m.log2S;
         const bool park_lds = !DOT && rs;
         a.park_cap = park_lds ? kRowParkFloats / (int)upb : 0;
@@ -603,7 +661,7 @@ cogdl_status rows_pass(BwdArgs a, const Plan *P, int xdt, int pdt, const char *n
         blocks = list_grid(blocks, a.lists);
         COGDL_LAUNCH_SHM(name, k, (unsigned)blocks, kBlock, shm, stream, a);
     } else {
-        BwdKernel k = pick_any<DOT>(xdt, pdt);
+        BwdKernel k = pick_any<DOT>(xdt, pdt, pk);
         a.park_cap = 0;
         int64_t blocks = (units + (kBlock / kWave) - 1) / (kBlock / kWave);
         const int64_t res = resident_blocks(reinterpret_cast<const void *>(k), kBlock);
@@ -660,23 +718,30 @@ cogdl_status cogdl_sddmm_dot(int32_t n_rows, int32_t n_cols, int64_t nnz, const 
     return rows_pass<true>(a, Pl, (int)q_dtype, (int)p_dtype, "sddmm_dot", stream);
 }
 
-cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
-                                const int32_t *rowptr, const int32_t *col, const int32_t *colptr,
-                                const int32_t *row_t, const int32_t *perm, int32_t H, int32_t D,
-                                const float *s_dst, const float *s_src, float negative_slope,
-                                const float *alpha, const void *X, cogdl_dtype x_dtype,
-                                const void *dY, cogdl_dtype dy_dtype, void *dX,
-                                cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
-                                float *ds_src, float *edge_work, const cogdl_plan *plan,
-                                const cogdl_plan *plan_t, hipStream_t stream)
+}  // extern "C"
+
+namespace cogdl {
+namespace {
+
+// The backward with the forward weights given (alpha) or rebuilt from the
+// forward's row softmax states (row_stats): exactly one of them.
+cogdl_status gat_backward_impl(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                               const int32_t *col, const int32_t *colptr, const int32_t *row_t,
+                               const int32_t *perm, int32_t H, int32_t D, const float *s_dst,
+                               const float *s_src, float negative_slope, const float *alpha,
+                               const float *row_stats, const void *X, cogdl_dtype x_dtype,
+                               const void *dY, cogdl_dtype dy_dtype, void *dX, cogdl_dtype dx_dtype,
+                               float *dalpha, float *dscore, float *ds_dst, float *ds_src,
+                               float *edge_work, const cogdl_plan *plan, const cogdl_plan *plan_t,
+                               hipStream_t stream)
 {
     cogdl_status st = check_heads(n_rows, n_cols, nnz, rowptr, col, H, D);
     if (st != COGDL_OK) return st;
     if (!dtype_ok(x_dtype) || !dtype_ok(dy_dtype) || !dtype_ok(dx_dtype)) return COGDL_ERR_DTYPE;
     if (n_cols > 0 && (!colptr || !dX || !ds_src)) return COGDL_ERR_INVALID;
     if (n_rows > 0 && (!ds_dst || !s_dst || !dY)) return COGDL_ERR_INVALID;
-    if (nnz > 0 && (!row_t || !perm || !s_src || !alpha || !X || !edge_work ||
-                    (uintptr_t)edge_work % alignof(float2) != 0))
+    if (nnz > 0 && (!row_t || !perm || !s_src || (alpha == nullptr) == (row_stats == nullptr) || !X ||
+                    !edge_work || (uintptr_t)edge_work % alignof(float2) != 0))
         return COGDL_ERR_INVALID;
     float2 *rec = reinterpret_cast<float2 *>(edge_work);
     const int64_t W = (int64_t)H * D;
@@ -701,6 +766,7 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
         a.s_src = s_src;
         a.slope = negative_slope;
         a.alpha = alpha;
+        a.row_stats = row_stats;
         a.X = X;
         a.x_bytes = (uint64_t)n_cols * (uint64_t)W * (uint64_t)dtype_bytes(x_dtype);
         a.P = dY;
@@ -717,11 +783,14 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
         st = rows_pass<false>(a, Pr, (int)x_dtype, (int)dy_dtype, "gat_bwd_rows", stream);
         if (st != COGDL_OK) return st;
         if (Pr) {
-            if (dalpha && dscore)
-                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<true>, wave_grid(Pr->cap_partials),
+            if (row_stats)
+                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<kParkStats>, wave_grid(Pr->cap_partials),
+                             kBlock, stream, a);
+            else if (dalpha && dscore)
+                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<kParkSep>, wave_grid(Pr->cap_partials),
                              kBlock, stream, a);
             else
-                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<false>, wave_grid(Pr->cap_partials),
+                COGDL_LAUNCH("gat_bwd_split_edges", k_bwd_split_edges<kParkPair>, wave_grid(Pr->cap_partials),
                              kBlock, stream, a);
             COGDL_LAUNCH("gat_bwd_split_dst", k_split_head_sums, wave_grid(Pr->cap_split), kBlock,
                          stream, Pr->split_rows, Pr->n_split_dev(), Pr->gstats, a.sstride,
@@ -794,6 +863,45 @@ cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
     COGDL_LAUNCH("gat_bwd_split_src", k_split_head_sums, wave_grid(Pc->cap_split), kBlock, stream,
                  Pc->split_rows, Pc->n_split_dev(), Pc->gstats, g.sstride, 0, H, ds_src);
     return COGDL_OK;
+}
+
+}  // namespace
+}  // namespace cogdl
+
+extern "C" {
+
+cogdl_status cogdl_gat_backward(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                const int32_t *rowptr, const int32_t *col, const int32_t *colptr,
+                                const int32_t *row_t, const int32_t *perm, int32_t H, int32_t D,
+                                const float *s_dst, const float *s_src, float negative_slope,
+                                const float *alpha, const void *X, cogdl_dtype x_dtype,
+                                const void *dY, cogdl_dtype dy_dtype, void *dX,
+                                cogdl_dtype dx_dtype, float *dalpha, float *dscore, float *ds_dst,
+                                float *ds_src, float *edge_work, const cogdl_plan *plan,
+                                const cogdl_plan *plan_t, hipStream_t stream)
+{
+    if (nnz > 0 && !alpha) return COGDL_ERR_INVALID;
+    return gat_backward_impl(n_rows, n_cols, nnz, rowptr, col, colptr, row_t, perm, H, D, s_dst, s_src,
+                             negative_slope, alpha, nullptr, X, x_dtype, dY, dy_dtype, dX, dx_dtype,
+                             dalpha, dscore, ds_dst, ds_src, edge_work, plan, plan_t, stream);
+}
+
+cogdl_status cogdl_gat_backward_stats(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                                      const int32_t *rowptr, const int32_t *col,
+                                      const int32_t *colptr, const int32_t *row_t,
+                                      const int32_t *perm, int32_t H, int32_t D,
+                                      const float *s_dst, const float *s_src,
+                                      float negative_slope, const float *row_stats, const void *X,
+                                      cogdl_dtype x_dtype, const void *dY, cogdl_dtype dy_dtype,
+                                      void *dX, cogdl_dtype dx_dtype, float *dalpha,
+                                      float *dscore, float *ds_dst, float *ds_src,
+                                      float *edge_work, const cogdl_plan *plan,
+                                      const cogdl_plan *plan_t, hipStream_t stream)
+{
+    if (nnz > 0 && !row_stats) return COGDL_ERR_INVALID;
+    return gat_backward_impl(n_rows, n_cols, nnz, rowptr, col, colptr, row_t, perm, H, D, s_dst, s_src,
+                             negative_slope, nullptr, row_stats, X, x_dtype, dY, dy_dtype, dX, dx_dtype,
+                             dalpha, dscore, ds_dst, ds_src, edge_work, plan, plan_t, stream);
 }
 
 }  // extern "C"

@@ -30,6 +30,7 @@ struct GatArgs {
     uint64_t x_bytes;           // size of X, bounds the buffer gathers
     void *Y;
     float *alpha_out;
+    float *row_stats;           // softmax: per row the final (m, 1/z) of each head, 2H floats (nullable)
     float *partials;
     int64_t pstride;
     float *gstats;              // per partial slot: m[max_heads], z[max_heads]
@@ -153,7 +154,7 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
     const int lig = lane & (S - 1);
     const int gbase = lane & ~(S - 1);
     const int H = a.H;
-    const bool soft = a.alpha_in == nullptr;
+    const bool soft = !BWD && a.alpha_in == nullptr;   // the backward reads its weights
     const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows,
                                     kGatBlock >> log2S, threadIdx.x >> log2S);
     const int64_t stride = walk.step;
@@ -426,6 +427,15 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 rz[c] = (soft && z[c] > 0.f) ? 1.f / z[c] : 1.f;
+                // the row's softmax state, from which alpha = alpha_value(e, m, 1/z) can be
+                // rebuilt (every lane of the head holds it; the lane of its first feature writes)
+                if (soft && a.row_stats != nullptr && act[c] && fe[c] % a.D == 0) {
+                    a.row_stats[(int64_t)row * 2 * H + hd[c]] = m[c];
+                    a.row_stats[(int64_t)row * 2 * H + H + hd[c]] = rz[c];
+                }
+            }
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
                 float v[VEC];
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) v[e] = acc[c][e] * rz[c];

@@ -288,6 +288,28 @@ def test_gat_backward_validation(L):
     assert B(-1, 2, 0) == INVALID
 
 
+def test_gat_stats_entry_points_validation(L):
+    """The training pair: the forward that writes row softmax states instead of alpha, and the
+    backward that rebuilds the weights from them (only failing calls are made)."""
+    def F(n_rows=2, n_cols=2, nnz=3, s_src=FAKE, a_src=None, stats=FAKE, act=0):
+        return L.cogdl_gat_aggregate_stats(n_rows, n_cols, nnz, FAKE, FAKE, 2, 8, FAKE, s_src, a_src,
+                                           ctypes.c_float(0.2), FAKE, 0, FAKE, 0, stats, None, act, None,
+                                           None)
+    assert F(s_src=None, a_src=None) == INVALID          # exactly one source of scores
+    assert F(s_src=FAKE, a_src=FAKE) == INVALID
+    assert F(stats=None) == INVALID
+    assert F(act=7) == INVALID
+    assert F(nnz=1 << 31) == TOO_LARGE
+
+    def B(row_stats=FAKE, work=FAKE, H=2):
+        return L.cogdl_gat_backward_stats(2, 2, 3, FAKE, FAKE, FAKE, FAKE, FAKE, H, 4, FAKE, FAKE,
+                                          ctypes.c_float(0.2), row_stats, FAKE, 0, FAKE, 0, FAKE, 0,
+                                          None, None, FAKE, FAKE, work, None, None, None)
+    assert B(row_stats=None) == INVALID
+    assert B(work=None) == INVALID
+    assert B(H=0) == INVALID
+
+
 def test_linear_and_head_scores_validation(L):
     lin = L.cogdl_linear
     # n, k, m, X, W, dtype, bias, act, Y, y_dtype, stream

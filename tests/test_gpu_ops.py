@@ -710,6 +710,86 @@ def test_gat_backward_without_edge_outputs(cg, kind, H, D, xk):
                     p.close()
 
 
+def _row_softmax_state(rowptr, col, sd, ss, slope=0.2):
+    """The oracle's per-row maximum score and normalizer (fp64, from the fp32 scores)."""
+    n, H = sd.shape
+    m = np.full((n, H), -np.inf)
+    z = np.zeros((n, H))
+    for i in range(n):
+        b, e = rowptr[i], rowptr[i + 1]
+        if e == b:
+            continue
+        t = sd[i].astype(np.float64)[None, :] + ss[col[b:e]].astype(np.float64)
+        sc = np.where(t > 0, t, slope * t)
+        m[i] = sc.max(0)
+        z[i] = np.exp(sc - m[i]).sum(0)
+    return m, z
+
+
+@pytest.mark.parametrize("kind", ["hubs", "dups", "small"])
+@pytest.mark.parametrize("H,D,xk", [(4, 64, "bf16"), (8, 16, "f32"), (3, 5, "f32"), (2, 64, "f16"), (1, 1, "f32")])
+def test_gat_training_pair_from_row_stats(cg, kind, H, D, xk):
+    """The forward that writes each row's softmax state (max score, 1 / normalizer) instead of
+    alpha, and the backward that rebuilds the weights from it: Y equals the alpha-writing
+    forward's bit for bit, the states match the oracle's, and every backward output (the
+    (alpha, dscore) records included) equals the backward on that forward's alpha bit for bit,
+    with and without the per-edge outputs, on every plan pair."""
+    import torch
+    g = _graph(kind, seed=31)
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 500 + H * D)
+    xh, xc, xd = features((g.n_cols, H, D), 600 + H * D, xk)
+    gh, gc, gd = features((g.n_rows, H, D), 601 + H * D, xk)
+    colptr, row_t, _, perm = oracle.csr_to_csc(g.rowptr, g.col, None, g.n_cols)
+    cp_d, rt_d, pm_d = dev(colptr), dev(row_t), dev(perm)
+    sd_d, ss_d = dev(sd), dev(ss)
+    m_ref, z_ref = _row_softmax_state(g.rowptr, g.col, sd, ss)
+    deg = np.diff(g.rowptr)
+    # per row and head: the weights' score-rounding factor (the largest over the row's edges)
+    scale = np.asarray(alpha_bound_scale(g.rowptr, g.col, sd, ss)).reshape(g.nnz, H)
+    row_scale = np.ones((g.n_rows, H))
+    np.maximum.at(row_scale, np.repeat(np.arange(g.n_rows), deg), scale)
+    for spec, spec_t in PLAN_PAIRS + [("sliced", "sliced")]:
+        say(f"gat training pair {kind} H={H} D={D} {xk} {spec}")
+        if spec == "sliced":
+            plan = cg.Plan(rp, g.nnz, H * D, max_heads=H, mode="neighbor_group", group_size=16, col=cl,
+                           n_cols=g.n_cols, slice_min=8)
+            plan_t = cg.Plan(cp_d, g.nnz, H * D, max_heads=H, mode="neighbor_group", group_size=16,
+                             col=rt_d, n_cols=g.n_rows, slice_min=8)
+        else:
+            plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+            plan_t = _make_plan(cg, cp_d, g.nnz, spec_t, H * D, max_heads=H)
+        try:
+            Ya, alpha = cg.gat_aggregate(rp, cl, sd_d, ss_d, xd, 0.2, plan=plan, out_dtype=torch.float32,
+                                         return_alpha=True)
+            Ys, st = cg.gat_aggregate_stats(rp, cl, sd_d, xd, s_src=ss_d, negative_slope=0.2, plan=plan,
+                                            out_dtype=torch.float32)
+            assert torch.equal(Ya, Ys), (kind, H, D, spec)
+            st_h = st.cpu().numpy().astype(np.float64)
+            m, rz = st_h[:, 0, :], st_h[:, 1, :]
+            has = deg > 0
+            assert np.all(np.isneginf(m[~has])) and np.all(rz[~has] == 1.0)
+            assert np.all(np.abs(m[has] - m_ref[has]) <= 1e-6 * np.maximum(1.0, np.abs(m_ref[has])))
+            # 1/z: each term within the weights' bound, the fp32 sum within 2^-23 per term
+            bound = TOL_ALPHA * row_scale[has] + 2.0 ** -23 * deg[has, None]
+            assert np.all(np.abs(rz[has] * z_ref[has] - 1.0) <= bound), (kind, H, D, spec)
+            for drop in ((), ("dalpha", "dscore")):
+                o = {k: None for k in drop}
+                ba = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, sd_d, ss_d, alpha, xd, gd, 0.2, plan=plan,
+                                     plan_t=plan_t, dx_dtype=torch.float32, out=dict(o))
+                bs = cg.gat_backward(rp, cl, cp_d, rt_d, pm_d, sd_d, ss_d, None, xd, gd, 0.2, plan=plan,
+                                     plan_t=plan_t, dx_dtype=torch.float32, out=dict(o), row_stats=st)
+                for k, v in ba.items():
+                    if v is None:
+                        assert bs[k] is None
+                    else:
+                        assert torch.equal(v, bs[k]), (kind, H, D, spec, drop, k)
+        finally:
+            for p in (plan, plan_t):
+                if p is not None:
+                    p.close()
+
+
 def test_plan_rebuild_past_capacity_is_refused(cg):
     """A rebuild on a rowptr holding more edges than the plan was created for must not write past
     the plan: the build leaves the plan empty and cogdl_plan_query reports COGDL_ERR_PLAN; a
@@ -775,6 +855,49 @@ def test_gat_aggregate_proj(cg, kind, H, D, xk, yk):
             # deterministic
             assert torch.equal(cg.gat_aggregate_proj(rp, cl, dev(sd), dev(a_src), xd, 0.2, plan=plan,
                                                      out_dtype=out_dtype), Y)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+@pytest.mark.parametrize("kind", ["hubs", "small"])
+@pytest.mark.parametrize("H,D,xk", [(4, 64, "bf16"), (2, 32, "f32"), (2, 16, "f32")])
+def test_gat_stats_projected_scores(cg, kind, H, D, xk):
+    """The row softmax states with projected source scores: Y equals cogdl_gat_aggregate_proj's
+    bit for bit, and each row's (max, 1 / normalizer) matches the oracle's on its fp64 head
+    scores within the score's rounding (as in test_gat_aggregate_proj) and the fp32 sum."""
+    import torch
+    g = _graph(kind)
+    rp, cl, _ = graph_to_dev(g)
+    sd, _ = _scores(g.n_rows, g.n_cols, H, 72 + H)
+    rng = np.random.default_rng(73 + D)
+    a_src = (rng.standard_normal((H, D)) / np.sqrt(D)).astype(np.float32)
+    xh, xc, xd = features((g.n_cols, H, D), 82 + D, xk)
+    ss_ref, _, ss_abs, _ = oracle.head_scores(xh.reshape(g.n_cols, H * D), a_src, a_src, H, D, z_dtype=xc)
+    m_ref, z_ref = _row_softmax_state(g.rowptr, g.col, sd, ss_ref)
+    u = 2.0 ** -24
+    ds = D * u * float(ss_abs.max(initial=0.0)) + u * float(np.abs(ss_ref).max(initial=0.0))
+    deg = np.diff(g.rowptr)
+    has = deg > 0
+    for spec in (None, ("neighbor_group", 6), "sliced"):
+        say(f"gat stats projected {kind} H={H} D={D} {xk} {spec}")
+        if spec == "sliced":
+            plan = cg.Plan(rp, g.nnz, max_feat=H * D, max_heads=H, mode="neighbor_group", group_size=9,
+                           col=cl, n_cols=g.n_cols, slice_min=16)
+        else:
+            plan = _make_plan(cg, rp, g.nnz, spec, H * D, max_heads=H)
+        try:
+            Yp = cg.gat_aggregate_proj(rp, cl, dev(sd), dev(a_src), xd, 0.2, plan=plan, out_dtype=torch.float32)
+            Ys, st = cg.gat_aggregate_stats(rp, cl, dev(sd), xd, a_src=dev(a_src), negative_slope=0.2,
+                                            plan=plan, out_dtype=torch.float32)
+            assert torch.equal(Yp, Ys), (kind, H, D, spec)
+            st_h = st.cpu().numpy().astype(np.float64)
+            m, rz = st_h[:, 0, :], st_h[:, 1, :]
+            assert np.all(np.isneginf(m[~has])) and np.all(rz[~has] == 1.0)
+            # a score moved by ds moves the maximum by at most ds and each exp term by about 2 ds
+            assert np.all(np.abs(m[has] - m_ref[has]) <= ds + 1e-6 * np.maximum(1.0, np.abs(m_ref[has])))
+            bound = TOL_ALPHA + 4 * ds + 2.0 ** -23 * deg[has, None]
+            assert np.all(np.abs(rz[has] * z_ref[has] - 1.0) <= bound), (kind, H, D, spec)
         finally:
             if plan is not None:
                 plan.close()
