@@ -1305,7 +1305,16 @@ def main():
     ms_bwd_st, k_bwd_st = time_op_kernels(lambda: cg.gat_backward(
         rowptr, col, colptr, row_t, perm, s_dst, s_src, None, Xg, dYg, 0.2, plan=plan,
         plan_t=plan_t, out=lay_out, row_stats=st_buf))
-    del lay_out, st_buf
+    # the same pair with the step's projected source scores: the backward takes s_src from one
+    # head-score pass over the features (which a layer needs for s_dst anyway)
+    ms_gat_stp, _ = time_op_kernels(lambda: cg.gat_aggregate_stats(
+        rowptr, col, s_dst, Xg, a_src=a_src, negative_slope=0.2, plan=plan, out=Yg, stats_out=st_buf))
+    ms_hs = time_op(lambda: cg.head_scores(Xg, a_src, None))
+    s_src_p, _ = cg.head_scores(Xg, a_src, None)
+    ms_bwd_stp, _ = time_op_kernels(lambda: cg.gat_backward(
+        rowptr, col, colptr, row_t, perm, s_dst, s_src_p, None, Xg, dYg, 0.2, plan=plan,
+        plan_t=plan_t, out=lay_out, row_stats=st_buf))
+    del lay_out, st_buf, s_src_p
     dot_out = torch.empty((E, H), dtype=torch.float32, device=dev)
     ms_dot, k_dot = time_op_kernels(lambda: cg.sddmm_dot(rowptr, col, dYg, Xg, plan=plan, out=dot_out))
     b_dot = 4 * (N + 1) + 4 * E + N * H * D * 2 + E * H * D * 2 + 4 * E * H
@@ -1377,8 +1386,12 @@ def main():
             forward_algorithmic_GB=b_gat_st / 1e9, backward_algorithmic_GB=b_bwd_st / 1e9,
             forward_kernels_ms=k_gat_st, backward_kernels_ms=k_bwd_st,
             with_alpha_ms=ms_gat_a + ms_bwd_l,
+            projected_scores=dict(forward_ms=ms_gat_stp, head_scores_ms=ms_hs, backward_ms=ms_bwd_stp,
+                                  ms=ms_gat_stp + ms_hs + ms_bwd_stp),
             note="forward with each row's softmax state instead of alpha, backward rebuilding the "
-                 "weights (layer gradients only); with_alpha_ms: the same pair through alpha"),
+                 "weights (layer gradients only); with_alpha_ms: the same pair through alpha; "
+                 "projected_scores: the forward forms s_src from the gathered rows, the backward "
+                 "takes it from a head-score pass"),
         "act_codec": codec,
         "sddmm_dot": dict(ms=ms_dot, algorithmic_GB=b_dot / 1e9,
                           eff_GBps=b_dot / (ms_dot * 1e-3) / 1e9, edges_per_s=E / (ms_dot * 1e-3)),
@@ -1431,7 +1444,8 @@ def main():
         f"layer gradients only {ms_bwd_l:.3f} ms "
         f"({', '.join(f'{k} {v:.3f}' for k, v in k_bwd_l.items())}); "
         f"training pair through row states {ms_gat_st:.3f} + {ms_bwd_st:.3f} ms "
-        f"(through alpha {ms_gat_a:.3f} + {ms_bwd_l:.3f} ms)")
+        f"(through alpha {ms_gat_a:.3f} + {ms_bwd_l:.3f} ms; projected scores {ms_gat_stp:.3f} + "
+        f"{ms_hs:.3f} + {ms_bwd_stp:.3f} ms)")
 
     inference = None if args.no_inference else run_inference(cg, synth, dev, time_op_kernels,
                                                              sliced=not args.plain_plans)
