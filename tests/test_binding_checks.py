@@ -112,6 +112,35 @@ def test_sddmm_dot_and_backward_sizes():
     raises_size(lambda: cg.gat_backward(**args, out={"dX": torch.zeros(5, 2, 2)}), "dX has 20 elements")
     raises_size(lambda: cg.gat_backward(**args, out={"ds_src": torch.zeros(4, 2)}), "ds_src has 8 elements")
     raises_size(lambda: cg.gat_backward(**args, out={"grad": torch.zeros(1)}), "unknown output")
+    # the per-edge outputs may be left out, no other
+    reaches_device_check(lambda: cg.gat_backward(**args, out={"dalpha": None, "dscore": None}))
+    raises_size(lambda: cg.gat_backward(**args, out={"ds_dst": None}), "output 'ds_dst' is required")
+    # the weights rebuilt from row softmax states instead of alpha
+    st = torch.zeros(4, 2, 2)
+    reaches_device_check(lambda: cg.gat_backward(**dict(args, alpha=None), row_stats=st))
+    raises_size(lambda: cg.gat_backward(**dict(args, alpha=None), row_stats=torch.zeros(4, 2, 1)),
+                "row_stats has 8 elements, expected 16")
+    raises_size(lambda: cg.gat_backward(**args, row_stats=st), "exactly one of alpha and row_stats")
+    raises_size(lambda: cg.gat_backward(**dict(args, alpha=None)), "exactly one of alpha and row_stats")
+
+
+def test_gat_stats_forward_sizes():
+    rp, col = graph()
+    sd, ss = torch.zeros(4, 2), torch.zeros(5, 2)
+    X = torch.zeros(5, 2, 8, dtype=f32)
+    reaches_device_check(lambda: cg.gat_aggregate_stats(rp, col, sd, X, s_src=ss))
+    reaches_device_check(lambda: cg.gat_aggregate_stats(rp, col, sd, X, a_src=torch.zeros(2, 8)))
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, sd, X), "exactly one of s_src and a_src")
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, sd, X, s_src=ss, a_src=torch.zeros(2, 8)),
+                "exactly one of s_src and a_src")
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, sd, X, a_src=torch.zeros(2, 7)),
+                "a_src has 14 elements, expected 16")
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, sd, X, s_src=torch.zeros(4, 2)), r"s_src must be \[5, 2\]")
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, torch.zeros(4, 3), X, s_src=ss), r"s_dst must be \[4, 2\]")
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, sd, X, s_src=ss, stats_out=torch.zeros(4, 2)),
+                "stats_out has 8 elements, expected 16")
+    raises_size(lambda: cg.gat_aggregate_stats(rp, col, sd, X, s_src=ss, out=torch.zeros(4, 2, 7)),
+                "out has 56 elements, expected 64")
 
 
 def test_dense_and_codec_sizes():
