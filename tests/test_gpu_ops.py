@@ -860,6 +860,36 @@ def test_gat_aggregate_proj(cg, kind, H, D, xk, yk):
                 plan.close()
 
 
+def test_gat_training_pair_empty_graph(cg):
+    """No edges at all: Y and every gradient are zero, each row's state is (-inf, 1)."""
+    import torch
+    e = _graph("empty")
+    rp, cl, _ = graph_to_dev(e)
+    H, D = 2, 8
+    sd, ss = _scores(e.n_rows, e.n_cols, H, 5)
+    _, _, xd = features((e.n_cols, H, D), 6, "f32")
+    _, _, gd = features((e.n_rows, H, D), 7, "f32")
+    colptr, row_t, _, perm = oracle.csr_to_csc(e.rowptr, e.col, None, e.n_cols)
+    cp_d = dev(colptr)
+    for spec in (None, ("auto", 0)):
+        say(f"gat training pair, empty graph, plan {spec}")
+        plan = _make_plan(cg, rp, 0, spec, H * D, max_heads=H)
+        plan_t = _make_plan(cg, cp_d, 0, spec, H * D, max_heads=H)
+        try:
+            Y, st = cg.gat_aggregate_stats(rp, cl, dev(sd), xd, s_src=dev(ss), plan=plan, out_dtype=torch.float32)
+            assert Y.shape == (e.n_rows, H, D) and float(Y.abs().max()) == 0.0
+            s_h = st.cpu().numpy()
+            assert np.all(np.isneginf(s_h[:, 0])) and np.all(s_h[:, 1] == 1.0)
+            b = cg.gat_backward(rp, cl, cp_d, dev(row_t), dev(perm), dev(sd), dev(ss), None, xd, gd, 0.2,
+                                plan=plan, plan_t=plan_t, dx_dtype=torch.float32, row_stats=st)
+            for k in ("dX", "ds_dst", "ds_src"):
+                assert float(b[k].abs().max()) == 0.0, k
+        finally:
+            for p in (plan, plan_t):
+                if p is not None:
+                    p.close()
+
+
 @pytest.mark.parametrize("kind", ["hubs", "small"])
 @pytest.mark.parametrize("H,D,xk", [(4, 64, "bf16"), (2, 32, "f32"), (2, 16, "f32")])
 def test_gat_stats_projected_scores(cg, kind, H, D, xk):
