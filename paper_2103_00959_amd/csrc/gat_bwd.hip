@@ -81,12 +81,9 @@ __device__ __forceinline__ int4 fetch_bwd_unit(const BwdArgs &a, int64_t u, int6
 
 // The score gradient of edge k and head h is f * alpha * (dalpha - c), with f
 // the LeakyReLU slope at the pre-activation t and c the row's sum of alpha *
-// dalpha.  Pass 1 parks u = f * alpha and dalpha (c is not known yet); once
-// c is known, dscore = u (dalpha - c), alpha read back from its input.  The
-// dalpha and dscore outputs are optional: dalpha parks in its output when
-// there is one, and a split row's u in dscore when both are there; every
-// other pair goes to the edge's record (dalpha, u), which the fix-up then
-// overwrites with (alpha, dscore).
+// dalpha.  Pass 1 parks u = f * alpha and dalpha, as ParkMode below lays
+// out (c is not known yet); once c is known, dscore = u (dalpha - c), and the
+// edge's record ends as (alpha, dscore).
 __device__ __forceinline__ float park_value(float t, float slope, float al)
 {
     return (t > 0.f ? 1.f : slope) * al;
