@@ -275,6 +275,47 @@ def test_gat_backward_skewed_sampled(cg, sliced):
 
 
 @pytest.mark.timeout(900)
+def test_gat_training_pair_skewed(cg):
+    """The training pair at full size (2.4M nodes, 122.4M nonzeros, 4 x 64 bf16, the benchmark's
+    sliced plans): the forward that keeps each row's softmax state gives the alpha-writing
+    forward's Y bit for bit, and the backward that rebuilds the weights from those states gives
+    the backward on that alpha bit for bit (the layer gradients and the (alpha, dscore) records,
+    whose weights are the forward's alpha)."""
+    import torch
+    g = synth.config_graph(5, verbose=True)
+    N, E = g.n_rows, g.nnz
+    H, D = 4, 64
+    say(f"GAT training pair skewed n={N} nnz={E}")
+    rp, cl = dev(g.rowptr), dev(g.col)
+    rng = np.random.default_rng(3107)
+    sd = dev(rng.standard_normal((N, H), dtype=np.float32))
+    ss = dev(rng.standard_normal((N, H), dtype=np.float32))
+    _, _, xd = features((N, H, D), 2207, "bf16")
+    _, _, gd = features((N, H, D), 4107, "bf16")
+    colptr, row_t, _, perm = cg.csr_to_csc(rp, cl, None, N)
+    plan = cg.Plan(rp, E, max_feat=H * D, max_heads=H, col=cl, n_cols=N)
+    plan_t = cg.Plan(colptr, E, max_feat=H * D, max_heads=H, col=row_t, n_cols=N)
+    try:
+        Ya, alpha = cg.gat_aggregate(rp, cl, sd, ss, xd, 0.2, plan=plan, return_alpha=True)
+        Ys, st = cg.gat_aggregate_stats(rp, cl, sd, xd, s_src=ss, plan=plan)
+        assert torch.equal(Ya, Ys)
+        del Ya, Ys
+        o = {"dalpha": None, "dscore": None}
+        ba = cg.gat_backward(rp, cl, colptr, row_t, perm, sd, ss, alpha, xd, gd, 0.2, plan=plan,
+                             plan_t=plan_t, out=dict(o))
+        bs = cg.gat_backward(rp, cl, colptr, row_t, perm, sd, ss, None, xd, gd, 0.2, plan=plan,
+                             plan_t=plan_t, out=dict(o), row_stats=st)
+        torch.cuda.synchronize()
+        for k in ("dX", "ds_dst", "ds_src", "edge_work"):
+            assert torch.equal(ba[k], bs[k]), k
+        assert torch.equal(bs["edge_work"][..., 0].reshape(-1), alpha.reshape(-1))
+        say("GAT training pair skewed: bit for bit")
+    finally:
+        plan.close()
+        plan_t.close()
+
+
+@pytest.mark.timeout(900)
 def test_inference_reddit_shaped_sampled(cg):
     """2-layer GCN and GAT inference (hidden 128, 4 heads, 602 inputs, 41 classes) on
     the Reddit-shaped graph (232,965 nodes, 114.6M nonzeros), bf16 activations:
