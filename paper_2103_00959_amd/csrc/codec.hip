@@ -246,9 +246,9 @@ __global__ __launch_bounds__(kBlock) void k_compress_v(CodecArgs a)
                 for (int e = 0; e < 8; ++e) x[v][e] = 0.f;
             }
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                lo = fminf(lo, gok ? x[v][e] : INFINITY);
-                hi = fmaxf(hi, gok ? x[v][e] : -INFINITY);
+            for (int e = 0; e < 8; ++e) {         // (a group past the end writes nothing)
+                lo = fminf(lo, x[v][e]);
+                hi = fmaxf(hi, x[v][e]);
             }
         }
         lo = group_reduce(lo, LG, [](float u, float v) { return fminf(u, v); });
@@ -272,8 +272,8 @@ __global__ __launch_bounds__(kBlock) void k_compress_v(CodecArgs a)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float u = uniform24(rw[e]);
-                float t = floorf(fmaf(x[v][e] - lo, s, u));
-                t = t < 0.f ? 0.f : (t > qmax ? qmax : t);
+                // the clamp to [0, qmax] as one median of three (t is finite)
+                const float t = __builtin_amdgcn_fmed3f(floorf(fmaf(x[v][e] - lo, s, u)), 0.f, qmax);
                 q[e] = (uint32_t)t;
             }
             const int blk = (v * LG + sl) / 8;     // 64-feature block of these 8 features
