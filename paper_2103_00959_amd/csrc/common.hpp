@@ -241,7 +241,7 @@ struct RowGather {
         }
     }
 
-  private:
+    // widening of raw words, for callers that keep rows packed
     __device__ __forceinline__ static float widen1(uint32_t h)
     {
         if constexpr (Fmt<TX>::code == COGDL_BF16) return __uint_as_float(h << 16);

@@ -175,10 +175,18 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ wsrc = soft ? a.s_src : a.alpha_in;
     constexpr float kLog2eF = 1.44269504f;
-    // PROJ: this lane's VEC entries of a_src, and the lanes per head
-    float asrc[PROJ ? CH : 1][PROJ ? VEC : 1];
+    // PROJ: this lane's VEC entries of a_src, and the lanes per head.  With
+    // several chunks per lane (the tiny-unit kernels) the slab's a_src sits in
+    // LDS instead and is read per batch, which keeps CH * VEC registers free.
+    constexpr bool ASRC_LDS = PM == 1 && CH > 1;
+    constexpr int kAsrcMax = kWave * CH * VEC;          // a slab's width at most
+    __shared__ float asrc_lds[ASRC_LDS ? kAsrcMax : 1];
+    float asrc[PROJ && !ASRC_LDS ? CH : 1][PROJ && !ASRC_LDS ? VEC : 1];
     const int hl = PROJ ? a.D / VEC : 1;
-    if constexpr (PROJ) {
+    if constexpr (ASRC_LDS) {
+        for (int64_t f = threadIdx.x; f < f_end - f0; f += kGatBlock) asrc_lds[f] = a.a_src[f0 + f];
+        __syncthreads();
+    } else if constexpr (PROJ) {
 #pragma unroll
         for (int c = 0; c < CH; ++c)
 #pragma unroll
@@ -238,7 +246,12 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                     if constexpr (BWD && !DIST) pk[t] = lane_bcast(p_cur, gbase + (ok[t] ? j + t : j));
                 }
                 float w[U][CH];
-                float xv[U][CH][VEC];
+                // the projected multi-chunk (tiny-unit) kernels keep 16-bit rows packed,
+                // one 16-byte word per chunk, and widen them where used: with a_src in
+                // LDS, a wavefront per SIMD more (the other kernels gain no wavefront)
+                constexpr bool XPACK = ASRC_LDS && sizeof(TX) == 2 && VEC == 8;
+                float xv[XPACK ? 1 : U][XPACK ? 1 : CH][XPACK ? 1 : VEC];
+                uint4 xw[XPACK ? U : 1][XPACK ? CH : 1];
 #pragma unroll
                 for (int t = 0; t < U; ++t)
 #pragma unroll
@@ -254,7 +267,8 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         } else if constexpr (!PROJ && !DIST) {
                             w[t][c] = wsrc[on ? wi : 0];
                         }
-                        X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
+                        if constexpr (XPACK) xw[t][c] = X.load_raw16((int64_t)cc[t] * a.W + fe[c], on);
+                        else X.load((int64_t)cc[t] * a.W + fe[c], on, xv[t][c]);
                     }
                 if constexpr (DIST && BWD) {
                     static_assert(CH == 1 && U == 8, "one chunk, batches of 8 edges");
@@ -323,7 +337,31 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                         for (int e = 0; e < VEC; ++e) acc[0][e] = fmaf(wt[t], xv[t][0][e], acc[0][e]);
                     continue;
                 }
-                if constexpr (PROJ) {
+                if constexpr (ASRC_LDS) {
+                    // (no instruction: keeps the a_src reads in the loop, out of registers)
+                    asm volatile("" ::: "memory");
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) {
+                        float as[VEC];
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) as[e] = asrc_lds[fe[c] - f0 + e];
+#pragma unroll
+                        for (int t = 0; t < U; ++t) {
+                            float xe[VEC];
+                            if constexpr (XPACK) {
+                                RowGather<TX, VEC, BUF>::unpack16(xw[t][c].x, xw[t][c].y, xw[t][c].z,
+                                                                  xw[t][c].w, xe);
+                            } else {
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) xe[e] = xv[t][c][e];
+                            }
+                            float p = 0.f;
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) p = fmaf(xe[e], as[e], p);
+                            w[t][c] = group_sum(p, hl);
+                        }
+                    }
+                } else if constexpr (PROJ) {
 #pragma unroll
                     for (int t = 0; t < U; ++t)
 #pragma unroll
@@ -387,8 +425,19 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                 for (int t = 0; t < U; ++t)
 #pragma unroll
                     for (int c = 0; c < CH; ++c)
+                        if constexpr (XPACK) {
+                            // widened again here (the asm keeps the first widening from
+                            // being carried in registers across the softmax step)
+                            uint4 q = xw[t][c];
+                            asm volatile("" : "+v"(q.x), "+v"(q.y), "+v"(q.z), "+v"(q.w));
+                            float xe[VEC];
+                            RowGather<TX, VEC, BUF>::unpack16(q.x, q.y, q.z, q.w, xe);
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xv[t][c][e], acc[c][e]);
+                            for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xe[e], acc[c][e]);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) acc[c][e] = fmaf(w[t][c], xv[t][c][e], acc[c][e]);
+                        }
             }
             c_cur = c_nxt;
             if constexpr (BWD) p_cur = p_nxt;
