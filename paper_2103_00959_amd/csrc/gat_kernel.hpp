@@ -141,8 +141,16 @@ __device__ __forceinline__ float from_group8(float v)
 // each lane reads the (weight, value) record of its own edge of the batch, the
 // weights reach the head's lanes by swizzles and each lane sums the values of
 // its own edges, added over the head at the unit's end.
+// The forward's four-chunk kernel with given scores and packed 16-bit rows runs
+// three wavefronts per SIMD (a few registers spilled, still faster than two).
+template <int VEC, int CH, bool BUF, bool BWD, int PM, int XB>
+constexpr bool gat_given_packed = BUF && !BWD && PM == 0 && CH == 4 && VEC == 8 && XB == 2;
+
 template <typename TX, typename TY, int VEC, int CH, bool BUF, bool BWD, int PM = 0>
-__global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k_gat(GatArgs a)
+__global__ __launch_bounds__(kGatBlock, ((CH == 1 && BUF && !BWD)                                   ? 4
+                                         : (gat_given_packed<VEC, CH, BUF, BWD, PM, (int)sizeof(TX)>) ? 3
+                                                                                                      : 1))
+void k_gat(GatArgs a)
 {
     constexpr bool PROJ = PM == 1 || PM == 2;
     constexpr bool DIST = PM == 2 || PM == 3;
@@ -246,10 +254,12 @@ __global__ __launch_bounds__(kGatBlock, (CH == 1 && BUF && !BWD) ? 4 : 1) void k
                     if constexpr (BWD && !DIST) pk[t] = lane_bcast(p_cur, gbase + (ok[t] ? j + t : j));
                 }
                 float w[U][CH];
-                // the projected multi-chunk (tiny-unit) kernels keep 16-bit rows packed,
-                // one 16-byte word per chunk, and widen them where used: with a_src in
-                // LDS, a wavefront per SIMD more (the other kernels gain no wavefront)
-                constexpr bool XPACK = ASRC_LDS && sizeof(TX) == 2 && VEC == 8;
+                // the multi-chunk (tiny-unit) kernels keep 16-bit rows packed, one
+                // 16-byte word per chunk, and widen them where used: the projected ones
+                // with a_src in LDS and the given-score four-chunk one gain a wavefront
+                // per SIMD (the other kernels gain none)
+                constexpr bool XPACK = (ASRC_LDS && sizeof(TX) == 2 && VEC == 8) ||
+                                       gat_given_packed<VEC, CH, BUF, BWD, PM, (int)sizeof(TX)>;
                 float xv[XPACK ? 1 : U][XPACK ? 1 : CH][XPACK ? 1 : VEC];
                 uint4 xw[XPACK ? U : 1][XPACK ? CH : 1];
 #pragma unroll
