@@ -81,14 +81,111 @@ __device__ __forceinline__ int4 fetch_soft_unit(const SoftArgs &a, int64_t u, in
     return make_int4(r, a.rowptr[r], a.rowptr[r + 1], -1);
 }
 
-// S lanes per work unit laid out as (edge slot, head), slots = S / H edges per
-// step and R steps in flight per lane; resident grid, each sub-group striding
-// over the units with the next descriptor prefetched.  Whole rows: alpha
-// written (from the scores kept in registers when the row fits in one pass of
-// R steps, else by a second, batched sweep over the scores parked in alpha);
+// One work unit of k_softmax with RR steps per pass: S lanes laid out as
+// (edge slot, head), slots = S / H edges per step.  Whole rows: alpha written
+// (from the scores kept in registers when the row fits in one pass of RR
+// steps, else by a second, batched sweep over the scores parked in alpha);
 // neighbour groups: (m, z) per head into gstats, scores parked.  Stored
 // weights go through alpha_value.
-template <int R>
+template <int RR>
+__device__ __forceinline__ void soft_unit(const SoftArgs &a, int4 d, int H, int S, int slots, int h, int slot,
+                                          bool live, int gbase)
+{
+    const int32_t *__restrict__ col = a.col;
+    const int row = d.x, beg = d.y, end = d.z, part = d.w;
+    const float sd = a.s_dst[(int64_t)row * H + h];
+    // A unit longer than one pass parks its raw scores in alpha and the
+    // second sweep reads them back (each lane only its own elements):
+    // a contiguous re-read instead of a second random gather of s_src.
+    const bool park = end - beg > RR * slots || part >= 0;
+    float m = -INFINITY, z = 0.f;
+    float ev[RR];
+    for (int k0 = beg + slot; k0 < end + slot; k0 += RR * slots) {
+        int cc[RR];
+#pragma unroll
+        for (int r = 0; r < RR; ++r) {
+            const int k = k0 + r * slots;
+            cc[r] = col[k < end ? k : end - 1];
+        }
+        float mb = m;
+#pragma unroll
+        for (int r = 0; r < RR; ++r) {
+            const float sv = a.s_src[(int64_t)cc[r] * H + h];
+            ev[r] = (live && k0 + r * slots < end) ? leaky_relu(sd + sv, a.slope) : -INFINITY;
+            mb = fmaxf(mb, ev[r]);
+        }
+        if (park && live) {
+#pragma unroll
+            for (int r = 0; r < RR; ++r) {
+                const int k = k0 + r * slots;
+                if (k < end) a.alpha[(int64_t)k * H + h] = ev[r];
+            }
+        }
+        if (mb > m) {
+            z *= __expf(m - mb);
+            m = mb;
+        }
+        // masked steps (score -inf) add nothing, also while m is still -inf
+        float zb = 0.f;
+#pragma unroll
+        for (int r = 0; r < RR; ++r) zb += ev[r] == -INFINITY ? 0.f : __expf(ev[r] - m);
+        z += zb;
+    }
+    if (!live) { m = -INFINITY; z = 0.f; }
+    merge_slots(m, z, H, S, gbase);
+    if (part >= 0) {
+        if (slot == 0) {
+            a.gstats[(int64_t)part * a.sstride + h] = m;
+            a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + h] = z;
+        }
+    } else if (live && end > beg) {
+        const float rz = 1.f / z;
+        if (!park) {
+            // one pass: this lane's scores are still in ev
+#pragma unroll
+            for (int r = 0; r < RR; ++r) {
+                const int k = beg + slot + r * slots;
+                if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(ev[r], m, rz);
+            }
+        } else {
+            // the parked scores, same lane-to-element map as when they were written
+            for (int k0 = beg + slot; k0 < end; k0 += RR * slots) {
+                float e[RR];
+#pragma unroll
+                for (int r = 0; r < RR; ++r) {
+                    const int k = k0 + r * slots;
+                    e[r] = k < end ? a.alpha[(int64_t)k * H + h] : 0.f;
+                }
+#pragma unroll
+                for (int r = 0; r < RR; ++r) {
+                    const int k = k0 + r * slots;
+                    if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(e[r], m, rz);
+                }
+            }
+        }
+    }
+}
+
+// A unit with the fewest steps per pass out of RR, 2 RR, ..., R that holds it
+// in one pass (R for longer ones).
+template <int RR, int R>
+__device__ __forceinline__ void soft_class(const SoftArgs &a, int4 d, int H, int S, int slots, int h, int slot,
+                                           bool live, int gbase)
+{
+    if constexpr (RR >= R) {
+        soft_unit<R>(a, d, H, S, slots, h, slot, live, gbase);
+    } else {
+        if (d.z - d.y <= RR * slots) soft_unit<RR>(a, d, H, S, slots, h, slot, live, gbase);
+        else soft_class<2 * RR, R>(a, d, H, S, slots, h, slot, live, gbase);
+    }
+}
+
+// S lanes per work unit, resident grid, each sub-group striding over the
+// units with the next descriptor prefetched.  Each unit runs with the fewest
+// steps per pass out of R0, 2 R0, ..., R that hold it in one pass: a short
+// unit issues fewer gathers for steps past its end, a longer one is kept out
+// of parking.
+template <int R, int R0>
 __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
 {
     const int log2S = a.log2S;
@@ -105,7 +202,6 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
                                     kBlock >> log2S, threadIdx.x >> log2S);
     const int64_t stride = walk.step;
     const int64_t hi = walk.end;
-    const int32_t *__restrict__ col = a.col;
 
     int64_t u = walk.first;
     if (u >= hi) return;
@@ -113,78 +209,7 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
     for (;;) {
         const int64_t un = u + stride;
         const int4 dn = fetch_soft_unit(a, un, hi);
-        const int row = d.x, beg = d.y, end = d.z, part = d.w;
-        const float sd = a.s_dst[(int64_t)row * H + h];
-        // A unit longer than one pass parks its raw scores in alpha and the
-        // second sweep reads them back (each lane only its own elements):
-        // a contiguous re-read instead of a second random gather of s_src.
-        const bool park = end - beg > R * slots || part >= 0;
-        float m = -INFINITY, z = 0.f;
-        float ev[R];
-        for (int k0 = beg + slot; k0 < end + slot; k0 += R * slots) {
-            int cc[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int k = k0 + r * slots;
-                cc[r] = col[k < end ? k : end - 1];
-            }
-            float mb = m;
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const float sv = a.s_src[(int64_t)cc[r] * H + h];
-                ev[r] = (live && k0 + r * slots < end) ? leaky_relu(sd + sv, a.slope) : -INFINITY;
-                mb = fmaxf(mb, ev[r]);
-            }
-            if (park && live) {
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const int k = k0 + r * slots;
-                    if (k < end) a.alpha[(int64_t)k * H + h] = ev[r];
-                }
-            }
-            if (mb > m) {
-                z *= __expf(m - mb);
-                m = mb;
-            }
-            // masked steps (score -inf) add nothing, also while m is still -inf
-            float zb = 0.f;
-#pragma unroll
-            for (int r = 0; r < R; ++r) zb += ev[r] == -INFINITY ? 0.f : __expf(ev[r] - m);
-            z += zb;
-        }
-        if (!live) { m = -INFINITY; z = 0.f; }
-        merge_slots(m, z, H, S, gbase);
-        if (part >= 0) {
-            if (slot == 0) {
-                a.gstats[(int64_t)part * a.sstride + h] = m;
-                a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + h] = z;
-            }
-        } else if (live && end > beg) {
-            const float rz = 1.f / z;
-            if (!park) {
-                // one pass: this lane's scores are still in ev
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const int k = beg + slot + r * slots;
-                    if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(ev[r], m, rz);
-                }
-            } else {
-                // the parked scores, same lane-to-element map as when they were written
-                for (int k0 = beg + slot; k0 < end; k0 += R * slots) {
-                    float e[R];
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        const int k = k0 + r * slots;
-                        e[r] = k < end ? a.alpha[(int64_t)k * H + h] : 0.f;
-                    }
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        const int k = k0 + r * slots;
-                        if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(e[r], m, rz);
-                    }
-                }
-            }
-        }
+        soft_class<R0, R>(a, d, H, S, slots, h, slot, live, gbase);
         if (un >= hi) break;
         u = un;
         d = dn;
@@ -418,13 +443,13 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
         return COGDL_OK;
     };
     a.log2S = 6;
-    st = launch("softmax", k_softmax<8>, a);
+    st = launch("softmax", k_softmax<16, 2>, a);
     if (st != COGDL_OK) return st;
     if (P) {
         SoftArgs b = a;
         set_units(b, tiny_units(*P));
         b.log2S = log2i(next_pow2(4 * H) < kWave ? next_pow2(4 * H) : kWave);
-        st = launch("softmax_tiny", k_softmax<2>, b);
+        st = launch("softmax_tiny", k_softmax<2, 2>, b);
         if (st != COGDL_OK) return st;
         COGDL_LAUNCH("softmax_merge", k_softmax_merge, grid_waves(P->cap_split), kBlock, stream,
                      P->split_rows, P->n_split_dev(), P->gstats, a.sstride, H, P->rstats);
