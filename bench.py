@@ -79,6 +79,9 @@ def parse():
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_DIR", "COMMAND"),
                     help="write profiles/<workload>_kernel_stats.txt from the kernel statistics of a "
                          "rocprofv3 --kernel-trace --stats run (COMMAND: the command that made it), then exit")
+    ap.add_argument("--summarize-plans", nargs=2, metavar=("SLICED_JSON", "PLAIN_JSON"),
+                    help="write profiles/<workload>_sliced_vs_plain.txt from the JSON lines of a default "
+                         "run and of a --plain-plans run (both with --no-cpu-baseline), then exit")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the steps, copy a buffer of this many MiB (counter calibration)")
     ap.add_argument("--workloads", action="store_true",
@@ -941,6 +944,43 @@ def write_stats_profile(args, stats_dir, command, out_dir=None):
     print("\n".join(lines[:30]))
 
 
+def write_plans_profile(sliced_json, plain_json, out_dir=None):
+    """profiles/<workload>_sliced_vs_plain.txt: the step, its operators and kernels, the operators
+    outside the step and the inference workload side by side for the two kinds of balancer plan."""
+    a, b = (json.loads(open(f).read().strip().splitlines()[-1]) for f in (sliced_json, plain_json))
+    if a["config"]["workload"] != b["config"]["workload"]:
+        raise SystemExit("the two runs measured different workloads")
+    name = a["config"]["workload"].split(":")[0]
+    rows = [("step ms (timed region)", a["ms_per_step"], b["ms_per_step"], 3),
+            ("value GB/s (algorithmic)", a["value"], b["value"], 0)]
+    rows += [(f"{k} ms", a["ops"][k]["ms"], b["ops"][k]["ms"], 3) for k in a["ops"] if k in b["ops"]]
+    rows += [(f"kernel {k} ms", a["kernels"][k]["avg_ms"], b["kernels"][k]["avg_ms"], 3)
+             for k in a["kernels"] if k in b["kernels"] and k.startswith(("spmm", "gat"))]
+    oa, ob = a.get("ops_outside_step", {}), b.get("ops_outside_step", {})
+    rows += [(f"outside the step: {k} ms", oa[k].get("ms"), ob[k].get("ms"), 3)
+             for k in oa if k in ob and isinstance(oa[k], dict) and isinstance(ob[k], dict)]
+    for m in ("gcn", "gat"):
+        if m in a.get("inference", {}) and m in b.get("inference", {}):
+            rows.append((f"inference {m.upper()} ms", a["inference"][m]["ms"], b["inference"][m]["ms"], 3))
+    rows.append((f"roofline kernel avg ms ({a['roofline']['kernel']})", a["roofline"]["avg_ms"],
+                 b["roofline"]["avg_ms"], 3))
+    lines = [f"# Column-sliced vs plain balancer plans on {name}, one MI355X, same box, back to back",
+             "# sliced: cd /tmp && python3 $GRAFT_REPO_ROOT/bench.py --no-cpu-baseline",
+             "# plain:  cd /tmp && python3 $GRAFT_REPO_ROOT/bench.py --no-cpu-baseline --plain-plans",
+             "# table:  python3 bench.py --summarize-plans SLICED_JSON PLAIN_JSON",
+             f"# library sources sha256[:16] {library_source_sha()}",
+             "# per-operator times: mean over the instrumented steps (events around every launch); step: "
+             "the timed region; inference: the Reddit-shaped workload 3 graph with the same kind of plan",
+             f"{'quantity':48s} {'sliced':>10s} {'plain':>10s}"]
+    for label, x, y, nd in rows:
+        if x is None or y is None:
+            continue
+        lines.append(f"{label:48s} {x:10.{nd}f} {y:10.{nd}f}")
+    out = os.path.join(out_dir or os.path.join(HERE, "profiles"), f"{name}_sliced_vs_plain.txt")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -963,6 +1003,9 @@ def main():
         return
     if args.summarize_stats:
         write_stats_profile(args, *args.summarize_stats)
+        return
+    if args.summarize_plans:
+        write_plans_profile(*args.summarize_plans)
         return
     if args.summarize_counters:
         if len(args.summarize_counters) not in (3, 4):

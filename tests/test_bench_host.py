@@ -181,3 +181,26 @@ def test_stats_profile_writer(tmp_path):
     body = [l for l in txt if not l.startswith("#")][1:]
     assert body[0].startswith("void k_b<int>") and "3.0000" in body[0]
     assert body[1].startswith("void k_a<int>")
+
+
+def test_plans_profile_writer(tmp_path):
+    """--summarize-plans: the two runs' lines side by side, refused for different workloads."""
+    import pytest
+
+    def line(step, wl="wl_a: graph"):
+        return {"ms_per_step": step, "value": 1000.0 / step, "config": {"workload": wl},
+                "ops": {"spmm": {"ms": step / 4}}, "kernels": {"spmm": {"avg_ms": step / 5}, "fill": {"avg_ms": 1.0}},
+                "ops_outside_step": {"sddmm_edge_softmax": {"ms": 2.0}},
+                "inference": {"gcn": {"ms": 3.0}}, "roofline": {"kernel": "spmm", "avg_ms": step / 5}}
+    a, b = tmp_path / "a.json", tmp_path / "b.json"
+    a.write_text("[bench] log line\n" + json.dumps(line(20.0)))
+    b.write_text(json.dumps(line(25.0)))
+    out = tmp_path / "profiles"
+    out.mkdir()
+    bench.write_plans_profile(str(a), str(b), str(out))
+    txt = (out / "wl_a_sliced_vs_plain.txt").read_text()
+    assert "step ms (timed region)" in txt and "20.000" in txt and "25.000" in txt
+    assert "kernel spmm ms" in txt and "kernel fill" not in txt and "inference GCN ms" in txt
+    b.write_text(json.dumps(line(25.0, "wl_b: other")))
+    with pytest.raises(SystemExit):
+        bench.write_plans_profile(str(a), str(b), str(out))
