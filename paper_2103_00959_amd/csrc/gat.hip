@@ -216,6 +216,136 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SoftArgs a)
     }
 }
 
+// The H scores of one node or edge as whole 8- and 16-byte words (H = 1, 2, 4
+// or 8, p aligned to min(4 H, 16) bytes).
+template <int H>
+__device__ __forceinline__ void load_heads(const float *__restrict__ p, float (&v)[H])
+{
+    if constexpr (H == 1) {
+        v[0] = p[0];
+    } else if constexpr (H == 2) {
+        const float2 t = *reinterpret_cast<const float2 *>(p);
+        v[0] = t.x;
+        v[1] = t.y;
+    } else {
+#pragma unroll
+        for (int q = 0; q < H / 4; ++q) {
+            const float4 t = reinterpret_cast<const float4 *>(p)[q];
+            v[4 * q] = t.x;
+            v[4 * q + 1] = t.y;
+            v[4 * q + 2] = t.z;
+            v[4 * q + 3] = t.w;
+        }
+    }
+}
+
+template <int H>
+__device__ __forceinline__ void store_heads(float *__restrict__ p, const float (&v)[H])
+{
+    if constexpr (H == 1) {
+        p[0] = v[0];
+    } else if constexpr (H == 2) {
+        *reinterpret_cast<float2 *>(p) = make_float2(v[0], v[1]);
+    } else {
+#pragma unroll
+        for (int q = 0; q < H / 4; ++q)
+            reinterpret_cast<float4 *>(p)[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    }
+}
+
+// Tiny units (at most kTinyUnit = 8 edges) for H = 1, 2, 4 or 8 heads: a quad
+// of lanes per unit (16 units per wavefront), each lane two edges (beg + lane
+// + 4 r) with all H source scores gathered as whole words.  The unit is one
+// pass: its maximum per head over the quad first (two DPP butterfly levels),
+// then the sum of exp(e - m), then the weights; a neighbour group of a split
+// row parks its raw scores and writes its (m, z) instead, as in k_softmax.
+template <int H>
+__global__ __launch_bounds__(kBlock) void k_softmax_quads(SoftArgs a)
+{
+    constexpr int L = 4, R = 2;
+    static_assert(L * R >= kTinyUnit, "one pass covers a tiny unit");
+    const int sub = lane_id() & (L - 1);
+    const UnitWalk walk = unit_walk(a.units != nullptr, a.u_lo, a.u_hi, a.lists, a.n_rows, kBlock / L,
+                                    threadIdx.x / L);
+    const int64_t stride = walk.step;
+    const int64_t hi = walk.end;
+    const int32_t *__restrict__ col = a.col;
+    const float *__restrict__ s_src = a.s_src;
+    float *__restrict__ alpha = a.alpha;
+
+    int64_t u = walk.first;
+    if (u >= hi) return;
+    int4 d = fetch_soft_unit(a, u, hi);
+    for (;;) {
+        const int64_t un = u + stride;
+        const int4 dn = fetch_soft_unit(a, un, hi);
+        const int row = d.x, beg = d.y, end = d.z, part = d.w;
+        if (end > beg) {
+            float sd[H];
+            load_heads<H>(a.s_dst + (int64_t)row * H, sd);
+            int cc[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int k = beg + sub + L * r;
+                cc[r] = col[k < end ? k : end - 1];
+            }
+            float e[R][H];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float sv[H];
+                load_heads<H>(s_src + (int64_t)cc[r] * H, sv);
+                const bool in = beg + sub + L * r < end;
+#pragma unroll
+                for (int h = 0; h < H; ++h) e[r][h] = in ? leaky_relu(sd[h] + sv[h], a.slope) : -INFINITY;
+            }
+            float m[H], z[H];
+#pragma unroll
+            for (int h = 0; h < H; ++h) {
+                float mh = e[0][h];
+#pragma unroll
+                for (int r = 1; r < R; ++r) mh = fmaxf(mh, e[r][h]);
+                mh = group_reduce(mh, L, [](float x, float y) { return fmaxf(x, y); });
+                float zh = 0.f;
+#pragma unroll
+                for (int r = 0; r < R; ++r) zh += e[r][h] == -INFINITY ? 0.f : __expf(e[r][h] - mh);
+                m[h] = mh;
+                z[h] = group_reduce(zh, L, [](float x, float y) { return x + y; });
+            }
+            if (part >= 0) {
+                if (sub == 0) {
+#pragma unroll
+                    for (int h = 0; h < H; ++h) {
+                        a.gstats[(int64_t)part * a.sstride + h] = m[h];
+                        a.gstats[(int64_t)part * a.sstride + (a.sstride >> 1) + h] = z[h];
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = beg + sub + L * r;
+                    if (k < end) store_heads<H>(alpha + (int64_t)k * H, e[r]);
+                }
+            } else {
+                float rz[H];
+#pragma unroll
+                for (int h = 0; h < H; ++h) rz[h] = 1.f / z[h];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int k = beg + sub + L * r;
+                    if (k < end) {
+                        float o[H];
+#pragma unroll
+                        for (int h = 0; h < H; ++h) o[h] = alpha_value(e[r][h], m[h], rz[h]);
+                        store_heads<H>(alpha + (int64_t)k * H, o);
+                    }
+                }
+            }
+        }
+        if (un >= hi) break;
+        u = un;
+        d = dn;
+    }
+}
+
 // Per split row: merge the (m, z) of its groups in slot order (64/H chains,
 // then the chains in order) into rstats.
 __device__ __forceinline__ void merge_groups(const float *gstats, int sstride, int p0, int np,
@@ -429,9 +559,10 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
     a.part_units = P ? P->part_units : nullptr;
     a.n_parts = P ? P->n_parts_dev() : nullptr;
     a.rstats = P ? P->rstats : nullptr;
-    // Units with more than kTinyUnit edges: a wavefront each, 8 steps of 64 / H
-    // edges in flight.  The sorted tail of tiny units: 4H lanes each (at most
-    // 64), two steps, so that one pass covers a unit of kTinyUnit edges.
+    // Units with more than kTinyUnit edges: a wavefront each, up to 16 steps of
+    // 64 / H edges in flight.  The sorted tail of tiny units: a quad of lanes
+    // each (or 4H lanes, at most 64, two steps), so that one pass covers a unit
+    // of kTinyUnit edges.
     const int64_t units = P ? P->cap_units : n_rows;
     auto launch = [&](const char *name, void (*k)(SoftArgs), const SoftArgs &args) {
         const int64_t upb = kBlock >> args.log2S;
@@ -448,8 +579,19 @@ cogdl_status cogdl_sddmm_edge_softmax(int32_t n_rows, int32_t n_cols, int64_t nn
     if (P) {
         SoftArgs b = a;
         set_units(b, tiny_units(*P));
-        b.log2S = log2i(next_pow2(4 * H) < kWave ? next_pow2(4 * H) : kWave);
-        st = launch("softmax_tiny", k_softmax<2, 2>, b);
+        // a quad per unit where the heads fill whole words, else 4H lanes as
+        // (edge slot, head), two steps
+        void (*k_tiny)(SoftArgs) = nullptr;
+        const uintptr_t words = (uintptr_t)s_dst | (uintptr_t)s_src | (uintptr_t)alpha;
+        if (words % (4 * (H < 4 ? H : 4)) == 0) {
+            if (H == 1) k_tiny = k_softmax_quads<1>;
+            else if (H == 2) k_tiny = k_softmax_quads<2>;
+            else if (H == 4) k_tiny = k_softmax_quads<4>;
+            else if (H == 8) k_tiny = k_softmax_quads<8>;
+        }
+        b.log2S = k_tiny ? 2 : log2i(next_pow2(4 * H) < kWave ? next_pow2(4 * H) : kWave);
+        if (!k_tiny) k_tiny = k_softmax<2, 2>;
+        st = launch("softmax_tiny", k_tiny, b);
         if (st != COGDL_OK) return st;
         COGDL_LAUNCH("softmax_merge", k_softmax_merge, grid_waves(P->cap_split), kBlock, stream,
                      P->split_rows, P->n_split_dev(), P->gstats, a.sstride, H, P->rstats);

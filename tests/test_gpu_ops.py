@@ -425,19 +425,47 @@ def _scores(n_rows, n_cols, H, seed, scale=1.0):
 
 
 @pytest.mark.parametrize("kind", ["small", "dups", "rect", "hubs", "cfg1"])
-@pytest.mark.parametrize("H", [1, 3, 4, 8, 64])
+@pytest.mark.parametrize("H", [1, 2, 3, 4, 8, 64])
 def test_sddmm_edge_softmax(cg, kind, H):
     g = _graph(kind)
     say(f"softmax {kind} H={H}")
     rp, cl, _ = graph_to_dev(g)
     sd, ss = _scores(g.n_rows, g.n_cols, H, 40 + H)
     a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
-    for spec in (None, ("auto", 0), ("row_split", 0), ("neighbor_group", 7), ("neighbor_group", 3)):
+    # ("neighbor_group", 16): long units and a tail of tiny ones (at most 8 edges)
+    for spec in (None, ("auto", 0), ("row_split", 0), ("neighbor_group", 7), ("neighbor_group", 3),
+                 ("neighbor_group", 16)):
         plan = _make_plan(cg, rp, g.nnz, spec, 1, max_heads=H)
         try:
             a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
             err = alpha_close(a, a_ref)
             assert err <= TOL_ALPHA, (kind, H, spec, err)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
+@pytest.mark.parametrize("H", [2, 4, 8])
+def test_softmax_unaligned_scores(cg, H):
+    """Score buffers that are not aligned to whole 16-byte words (a view one float into a larger
+    buffer) take the tiny units through the (edge slot, head) kernel instead of the quad one:
+    both layouts give the oracle's weights, on plans with tiny units, split rows or neither."""
+    import torch
+    g = _graph("hubs")
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 83 + H)
+    a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+    big = torch.zeros(g.n_cols * H + 1, dtype=torch.float32, device="cuda")
+    big[1:] = dev(ss).reshape(-1)
+    ss_off = big[1:].view(g.n_cols, H)
+    assert ss_off.data_ptr() % 8 == 4
+    for spec in (None, ("neighbor_group", 16), ("auto", 0)):
+        plan = _make_plan(cg, rp, g.nnz, spec, 1, max_heads=H)
+        try:
+            for s_src in (dev(ss), ss_off):
+                a = cg.sddmm_edge_softmax(rp, cl, dev(sd), s_src, 0.2, plan=plan)
+                err = alpha_close(a, a_ref)
+                assert err <= TOL_ALPHA, (H, spec, s_src.data_ptr() % 16, err)
         finally:
             if plan is not None:
                 plan.close()
