@@ -86,7 +86,8 @@ __device__ __forceinline__ int4 fetch_soft_unit(const SoftArgs &a, int64_t u, in
 // (from the scores kept in registers when the row fits in one pass of RR
 // steps, else by a second, batched sweep over the scores parked in alpha);
 // neighbour groups: (m, z) per head into gstats, scores parked.  Stored
-// weights go through alpha_value.
+// weights go through alpha_value.  A lane's weight indices advance by a fixed
+// step per edge slot step, formed once per pass.
 template <int RR>
 __device__ __forceinline__ void soft_unit(const SoftArgs &a, int4 d, int H, int S, int slots, int h, int slot,
                                           bool live, int gbase)
@@ -94,6 +95,7 @@ __device__ __forceinline__ void soft_unit(const SoftArgs &a, int4 d, int H, int 
     const int32_t *__restrict__ col = a.col;
     const int row = d.x, beg = d.y, end = d.z, part = d.w;
     const float sd = a.s_dst[(int64_t)row * H + h];
+    const int64_t hstep = slots * H;    // index step from one edge slot step to the next
     // A unit longer than one pass parks its raw scores in alpha and the
     // second sweep reads them back (each lane only its own elements):
     // a contiguous re-read instead of a second random gather of s_src.
@@ -101,6 +103,7 @@ __device__ __forceinline__ void soft_unit(const SoftArgs &a, int4 d, int H, int 
     float m = -INFINITY, z = 0.f;
     float ev[RR];
     for (int k0 = beg + slot; k0 < end + slot; k0 += RR * slots) {
+        const int64_t i0 = (int64_t)k0 * H + h;    // alpha index of this lane's first edge of the pass
         int cc[RR];
 #pragma unroll
         for (int r = 0; r < RR; ++r) {
@@ -118,7 +121,7 @@ __device__ __forceinline__ void soft_unit(const SoftArgs &a, int4 d, int H, int 
 #pragma unroll
             for (int r = 0; r < RR; ++r) {
                 const int k = k0 + r * slots;
-                if (k < end) a.alpha[(int64_t)k * H + h] = ev[r];
+                if (k < end) a.alpha[i0 + r * hstep] = ev[r];
             }
         }
         if (mb > m) {
@@ -142,24 +145,26 @@ __device__ __forceinline__ void soft_unit(const SoftArgs &a, int4 d, int H, int 
         const float rz = 1.f / z;
         if (!park) {
             // one pass: this lane's scores are still in ev
+            const int64_t i0 = (int64_t)(beg + slot) * H + h;
 #pragma unroll
             for (int r = 0; r < RR; ++r) {
                 const int k = beg + slot + r * slots;
-                if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(ev[r], m, rz);
+                if (k < end) a.alpha[i0 + r * hstep] = alpha_value(ev[r], m, rz);
             }
         } else {
             // the parked scores, same lane-to-element map as when they were written
             for (int k0 = beg + slot; k0 < end; k0 += RR * slots) {
+                const int64_t i0 = (int64_t)k0 * H + h;
                 float e[RR];
 #pragma unroll
                 for (int r = 0; r < RR; ++r) {
                     const int k = k0 + r * slots;
-                    e[r] = k < end ? a.alpha[(int64_t)k * H + h] : 0.f;
+                    e[r] = k < end ? a.alpha[i0 + r * hstep] : 0.f;
                 }
 #pragma unroll
                 for (int r = 0; r < RR; ++r) {
                     const int k = k0 + r * slots;
-                    if (k < end) a.alpha[(int64_t)k * H + h] = alpha_value(e[r], m, rz);
+                    if (k < end) a.alpha[i0 + r * hstep] = alpha_value(e[r], m, rz);
                 }
             }
         }
