@@ -445,6 +445,41 @@ def test_sddmm_edge_softmax(cg, kind, H):
                 plan.close()
 
 
+@pytest.mark.parametrize("H", [1, 3, 4, 8])
+def test_softmax_step_class_boundaries(cg, H):
+    """Rows whose lengths straddle every change of the long-unit kernel's steps per pass (2, 4, 8
+    and 16 steps of 64 / H edge slots, and a second pass) and the tiny-unit bound of 8 edges,
+    plan-free (whole rows, long ones parked), with neighbour groups (rows over the group size
+    split) and with column-sliced plans: every weight against the oracle's."""
+    import torch
+    rng = np.random.default_rng(90 + H)
+    slots = 64 // H
+    bounds = (8, 2 * slots, 4 * slots, 8 * slots, 16 * slots, 32 * slots)
+    lens = sorted({max(0, b + d) for b in bounds for d in (-1, 0, 1)} | {0, 1, 2, 700})
+    n_cols = 3000
+    deg = np.array([L for L in lens for _ in range(2)], dtype=np.int64)
+    rng.shuffle(deg)
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+    col = np.concatenate([np.sort(rng.choice(n_cols, d, replace=False)) for d in deg]).astype(np.int32)
+    g = synth.Graph(rowptr, col, np.ones(col.size, np.float32), deg.size, n_cols)
+    rp, cl, _ = graph_to_dev(g)
+    sd, ss = _scores(g.n_rows, g.n_cols, H, 91 + H)
+    a_ref = oracle.edge_softmax(g.rowptr, g.col, sd, ss, slope=0.2)
+    say(f"softmax class bounds H={H}: row lengths {lens}")
+    for spec in (None, ("neighbor_group", 256), ("neighbor_group", 64), "sliced"):
+        if spec == "sliced":
+            plan = cg.Plan(rp, g.nnz, max_feat=1, max_heads=H, col=cl, n_cols=g.n_cols, slice_min=16)
+        else:
+            plan = _make_plan(cg, rp, g.nnz, spec, 1, max_heads=H)
+        try:
+            a = cg.sddmm_edge_softmax(rp, cl, dev(sd), dev(ss), 0.2, plan=plan)
+            err = alpha_close(a, a_ref)
+            assert err <= TOL_ALPHA, (H, spec, err)
+        finally:
+            if plan is not None:
+                plan.close()
+
+
 @pytest.mark.parametrize("H", [2, 4, 8])
 def test_softmax_unaligned_scores(cg, H):
     """Score buffers that are not aligned to whole 16-byte words (a view one float into a larger
