@@ -3,13 +3,15 @@
 // row, and the multi-head SpMM that aggregates neighbour features with one
 // weight per edge and head.
 //
-// cogdl_sddmm_edge_softmax (alpha only): a sub-group of lanes per work unit
-// (a wavefront for long units, 4H lanes for the tiny tail), laid out as (edge
-// slot, head) so that S/H edges are scored per step with several steps in
-// flight; each lane keeps an online softmax state (m, z), the states of one
-// head are merged across slots with lane exchanges (a butterfly when H is a
-// power of two), and alpha = exp(e - m) / z is written with coalesced stores,
-// from registers when the unit fitted in one pass.
+// cogdl_sddmm_edge_softmax (alpha only): a wavefront per long unit, laid out
+// as (edge slot, head) so that 64/H edges are scored per step with as many
+// steps in flight as the unit needs (2 to 16); each lane keeps an online
+// softmax state (m, z), the states of one head are merged across slots with
+// lane exchanges (a butterfly when H is a power of two), and alpha =
+// exp(e - m) / z is written with coalesced stores, from registers when the
+// unit fitted in one pass.  The tiny tail runs a quad of lanes per unit (each
+// edge's H scores gathered as whole words) or, for other head counts, 4H
+// lanes in the (edge slot, head) layout.
 //
 // cogdl_gat_aggregate (fused): the gather mapping of the SpMM (S lanes x VEC
 // features per edge row).  Every lane computes the weight of its own head for
